@@ -1,0 +1,470 @@
+"""Pins for the oracle (CPU only).
+
+Each oracle function is checked against something other than itself: dense
+brute force written from the mathematical definition, closed forms of small
+graphs, library routines (numpy's stable argsort, scipy's softmax), invariants
+that hold at any size, and the worked BatchGraph example printed in the paper
+(Sec. 2.1.1). The cases are chosen so that a dropped term, a wrong sign or
+index, or a transposed operand fails at least one test.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import graphgen
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def dense_adj(edge_index, n, w=None, n_src=None):
+    """A[s, t] = sum of the weights of the edges s -> t (a multigraph adds up)."""
+    n_src = n if n_src is None else n_src
+    A = np.zeros((n_src, n), np.float64)
+    w = np.ones(edge_index.shape[1]) if w is None else np.asarray(w, np.float64)
+    np.add.at(A, (edge_index[0], edge_index[1]), w)
+    return A
+
+
+def dense_gcn(edge_index, n, w=None):
+    """D^-1/2 (A + I) D^-1/2 in float64, D the weighted in-degree including the loop."""
+    A = dense_adj(edge_index, n, w) + np.eye(n)
+    deg = A.sum(axis=0)
+    dinv = np.where(deg > 0, 1.0 / np.sqrt(np.where(deg > 0, deg, 1.0)), 0.0)
+    return dinv[:, None] * A * dinv[None, :], deg
+
+
+def propagate_dense(Ahat, x):
+    """y[t] = sum_s Ahat[s, t] x[s]: messages flow from source rows to target columns."""
+    return Ahat.T @ x.astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# CSR by target
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,n,e", [(1, 1, 5), (2, 7, 40), (3, 300, 5000), (4, 5000, 3)])
+def test_csr_is_numpy_stable_argsort(orc, seed, n, e):
+    ei = graphgen.random_graph(seed, n, e)
+    rowptr, col, perm = orc.csr_by_target(ei, n)
+    ref_perm = np.argsort(ei[1], kind="stable")
+    np.testing.assert_array_equal(perm, ref_perm)
+    np.testing.assert_array_equal(col, ei[0][ref_perm])
+    np.testing.assert_array_equal(np.diff(rowptr), np.bincount(ei[1], minlength=n))
+    assert rowptr[0] == 0 and rowptr[-1] == e
+
+
+def test_csr_brute_force_tiny(orc):
+    ei = graphgen.random_graph(11, 6, 25)
+    rowptr, col, perm = orc.csr_by_target(ei, 6)
+    k = 0
+    for t in range(6):  # O(N * E): scan all edges once per target, in input order
+        for e in range(ei.shape[1]):
+            if ei[1, e] == t:
+                assert perm[k] == e and col[k] == ei[0, e]
+                k += 1
+        assert rowptr[t + 1] == k
+
+
+def test_csr_invariants_and_empty(orc):
+    rowptr, col, perm = orc.csr_by_target(np.zeros((2, 0), np.int64), 4)
+    assert list(rowptr) == [0, 0, 0, 0, 0] and col.size == 0 and perm.size == 0
+    ei = graphgen.random_graph(5, 50, 2000, hub=3, hub_edges=500)
+    rowptr, col, perm = orc.csr_by_target(ei, 50)
+    assert sorted(perm.tolist()) == list(range(ei.shape[1]))
+    assert np.all(np.diff(ei[1][perm]) >= 0)
+    for t in range(50):
+        seg = perm[rowptr[t]:rowptr[t + 1]]
+        assert np.all(np.diff(seg) > 0)  # input order kept inside a row
+
+
+def test_csr_rejects_out_of_range(orc):
+    with pytest.raises(orc.OracleError) as ex:
+        orc.csr_by_target(np.array([[0, 1], [0, 5]]), 3)
+    assert ex.value.code == orc.ERR_INDEX_RANGE
+
+
+# ---------------------------------------------------------------------------
+# GCN normalisation
+# ---------------------------------------------------------------------------
+
+def test_gcn_norm_hand_example(orc):
+    g = json.load(open(os.path.join(GOLDEN, "gcn_path3_hand.json")))
+    ei = np.array(g["edge_index"])
+    out_ei, w, deg = orc.gcn_norm(ei, 3)
+    np.testing.assert_array_equal(deg, np.array(g["deg"], np.float32))
+    np.testing.assert_allclose(w, g["edge_weight_in_order_edges_then_loops"], rtol=4 * 2.0**-24)
+    np.testing.assert_array_equal(out_ei, np.array([[0, 1, 1, 2, 0, 1, 2], [1, 0, 2, 1, 0, 1, 2]]))
+    x = np.array(g["x"], np.float32)[:, None]
+    y, _ = orc.aggregate(out_ei, x, 3, "sum", edge_weight=w)
+    np.testing.assert_allclose(y[:, 0], g["y"], rtol=3e-7)
+
+
+@pytest.mark.parametrize("seed,n,e,weighted", [(1, 5, 12, False), (2, 17, 60, True),
+                                               (3, 64, 400, False), (4, 40, 300, True)])
+def test_gcn_matches_dense(orc, seed, n, e, weighted):
+    ei = graphgen.random_graph(seed, n, e)  # duplicates and self-loops included
+    w = (np.random.default_rng(seed).uniform(0.1, 2.0, e).astype(np.float32)
+         if weighted else None)
+    out_ei, what, deg = orc.gcn_norm(ei, n, edge_weight=w)
+    Ahat, ddeg = dense_gcn(ei, n, w)
+    np.testing.assert_allclose(deg, ddeg, rtol=1e-7)
+    x = graphgen.features(seed, n, 9)
+    y, S = orc.aggregate(out_ei, x, n, "sum", edge_weight=what)
+    ref = propagate_dense(Ahat, x)
+    # weights carry three float32 roundings each: |y - ref| <= 4u * sum |w x|
+    assert np.all(np.abs(y - ref) <= 4 * 2.0**-24 * S + 1e-300)
+
+
+def test_gcn_complete_graph(orc):
+    n = 7  # K_n plus loops: every A_hat entry is 1/n, so each output is the column mean
+    i, j = np.where(~np.eye(n, dtype=bool))
+    ei = np.stack([i, j]).astype(np.int64)
+    out_ei, w, deg = orc.gcn_norm(ei, n)
+    assert np.all(deg == n)
+    np.testing.assert_allclose(w, 1.0 / n, rtol=4 * 2.0**-24)
+    x = graphgen.features(1, n, 5)
+    y, _ = orc.aggregate(out_ei, x, n, "sum", edge_weight=w)
+    np.testing.assert_allclose(y, np.tile(x.astype(np.float64).mean(0), (n, 1)), atol=1e-6)
+
+
+def test_gcn_star(orc):
+    c = 9  # hub 0 with c leaves, both directions
+    leaves = np.arange(1, c + 1)
+    ei = np.stack([np.concatenate([leaves, np.zeros(c, int)]),
+                   np.concatenate([np.zeros(c, int), leaves])]).astype(np.int64)
+    out_ei, w, deg = orc.gcn_norm(ei, c + 1)
+    assert deg[0] == c + 1 and np.all(deg[1:] == 2)
+    np.testing.assert_allclose(w[:2 * c], 1 / math.sqrt(2 * (c + 1)), rtol=4 * 2.0**-24)
+    np.testing.assert_allclose(w[2 * c], 1 / (c + 1), rtol=4 * 2.0**-24)  # hub loop
+    np.testing.assert_allclose(w[2 * c + 1:], 0.5, rtol=4 * 2.0**-24)  # leaf loops
+
+
+def test_gcn_isolated_node_is_identity(orc):
+    ei = np.array([[0, 1], [1, 0]])  # node 2 isolated
+    out_ei, w, deg = orc.gcn_norm(ei, 3)
+    assert deg[2] == 1 and w[-1] == 1.0
+    x = graphgen.features(3, 3, 4)
+    y, _ = orc.aggregate(out_ei, x, 3, "sum", edge_weight=w)
+    assert np.array_equal(y[2].astype(np.float32), x[2])  # exactly
+
+
+def test_gcn_regular_ring(orc):
+    n, k = 12, 4  # 4-regular ring: A_hat = (A + I) / (k + 1)
+    src, tgt = [], []
+    for v in range(n):
+        for d in (1, 2):
+            src += [v, (v + d) % n]
+            tgt += [(v + d) % n, v]
+    ei = np.array([src, tgt], np.int64)
+    out_ei, w, deg = orc.gcn_norm(ei, n)
+    assert np.all(deg == k + 1)
+    np.testing.assert_allclose(w, 1 / (k + 1), rtol=4 * 2.0**-24)
+
+
+def test_gcn_sqrt_degree_is_fixed_point(orc):
+    # (A_hat s)_t = dinv_t * sum_{e->t} w_e = sqrt(deg_t) for s = sqrt(deg), at any size
+    n = 3000
+    ei = graphgen.random_graph(8, n, 60000, hub=5, hub_edges=4000)
+    out_ei, w, deg = orc.gcn_norm(ei, n)
+    s = np.sqrt(deg.astype(np.float64)).astype(np.float32)[:, None]
+    y, S = orc.aggregate(out_ei, s, n, "sum", edge_weight=w)
+    assert np.all(np.abs(y[:, 0] - s[:, 0]) <= 1e-6 * S[:, 0])
+
+
+def test_gcn_without_loops_and_zero_degree(orc):
+    ei = np.array([[0, 0], [1, 1]])  # target 0 and 2 have no in-edges, no loops
+    out_ei, w, deg = orc.gcn_norm(ei, 3, add_self_loops=False)
+    assert list(deg) == [0, 2, 0]
+    # src 0 has in-degree 0, so dinv[0] = 0 and its messages vanish
+    assert np.all(w == 0.0) and out_ei.shape == (2, 2)
+
+
+# ---------------------------------------------------------------------------
+# Aggregation
+# ---------------------------------------------------------------------------
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 12), n_src=st.integers(1, 12), e=st.integers(0, 60),
+       f=st.integers(1, 6), seed=st.integers(0, 10**6), weighted=st.booleans())
+def test_aggregate_sum_mean_dense(orc, n, n_src, e, f, seed, weighted):
+    ei = graphgen.random_graph(seed, n, e, n_src=n_src)
+    w = np.random.default_rng(seed).standard_normal(e).astype(np.float32) if weighted else None
+    x = graphgen.features(seed, n_src, f)
+    A = dense_adj(ei, n, w, n_src=n_src)
+    ref = A.T @ x.astype(np.float64)
+    y, S = orc.aggregate(ei, x, n, "sum", edge_weight=w)
+    assert np.all(np.abs(y - ref) <= 1e-12 * (S + 1e-300))
+    cnt = np.bincount(ei[1], minlength=n).astype(np.float64)
+    ym, _ = orc.aggregate(ei, x, n, "mean", edge_weight=w)
+    refm = np.where(cnt[:, None] > 0, ref / np.maximum(cnt, 1)[:, None], 0.0)
+    np.testing.assert_allclose(ym, refm, rtol=1e-12, atol=1e-12)
+
+
+def test_aggregate_per_head_weights(orc):
+    n, e, H, D = 9, 50, 3, 4
+    ei = graphgen.random_graph(4, n, e)
+    w = np.random.default_rng(4).standard_normal((e, H)).astype(np.float32)
+    x = graphgen.features(4, n, H * D)
+    y, _ = orc.aggregate(ei, x, n, "sum", edge_weight=w, heads=H)
+    for h in range(H):
+        A = dense_adj(ei, n, w[:, h])
+        ref = A.T @ x[:, h * D:(h + 1) * D].astype(np.float64)
+        np.testing.assert_allclose(y[:, h * D:(h + 1) * D], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_aggregate_ones_is_in_degree_and_mean_is_one(orc):
+    n = 200
+    ei = graphgen.random_graph(9, n, 3000)
+    x = np.ones((n, 3), np.float32)
+    y, _ = orc.aggregate(ei, x, n, "sum")
+    cnt = np.bincount(ei[1], minlength=n)
+    assert np.array_equal(y[:, 0], cnt.astype(np.float64))
+    ym, _ = orc.aggregate(ei, x, n, "mean")
+    assert np.array_equal(ym[:, 1], (cnt > 0).astype(np.float64))
+
+
+def test_aggregate_ldx_stride(orc):
+    n = 20
+    ei = graphgen.random_graph(2, n, 100)
+    big = graphgen.features(2, n, 11)
+    y1, _ = orc.aggregate(ei, big[:, :7], n, "sum")  # ldx = 11 > F = 7
+    y2, _ = orc.aggregate(ei, np.ascontiguousarray(big[:, :7]), n, "sum")
+    assert np.array_equal(y1, y2)
+
+
+def brute_max(ei, x, n, w):
+    F = x.shape[1]
+    out = np.zeros((n, F), np.float32)
+    arg = np.full((n, F), -1, np.int64)
+    for t in range(n):
+        es = [e for e in range(ei.shape[1]) if ei[1, e] == t]
+        for c in range(F):
+            best = None
+            for e in es:  # first maximal edge in input order wins
+                m = np.float32(w[e]) * x[ei[0, e], c]
+                if best is None or m > best:
+                    best, arg[t, c] = m, e
+            if best is not None:
+                out[t, c] = best
+    return out, arg
+
+
+def test_aggregate_max_brute_force_with_ties(orc):
+    n = 10
+    ei = graphgen.random_graph(6, n, 80)
+    w = np.random.default_rng(6).choice(np.float32([0.5, 1.0, -1.0, 2.0]), 80).astype(np.float32)
+    x = np.random.default_rng(7).integers(-2, 3, (n, 5)).astype(np.float32)  # many ties
+    x[0, 0] = -0.0
+    out, arg = orc.aggregate(ei, x, n, "max", edge_weight=w)
+    ref, refarg = brute_max(ei, x, n, w)
+    assert np.array_equal(out.view(np.int32), ref.view(np.int32))
+    assert np.array_equal(arg, refarg)
+
+
+def test_aggregate_max_signed_zero_is_a_tie(orc):
+    ei = np.array([[0, 1], [2, 2]])
+    x = np.array([[0.0], [-0.0], [5.0]], np.float32)
+    x[0, 0] = -0.0
+    x[1, 0] = 0.0
+    out, arg = orc.aggregate(ei, x, 3, "max")
+    assert arg[2, 0] == 0 and np.signbit(out[2, 0])  # -0 first, +0 does not replace it
+    assert arg[0, 0] == -1 and out[0, 0] == 0.0  # empty target
+
+
+def test_aggregate_max_properties(orc):
+    n = 300
+    ei = graphgen.random_graph(12, n, 5000)
+    w = np.random.default_rng(12).standard_normal(5000).astype(np.float32)
+    x = graphgen.features(12, n, 8)
+    out, arg = orc.aggregate(ei, x, n, "max", edge_weight=w)
+    cnt = np.bincount(ei[1], minlength=n)
+    for t in range(n):
+        for c in range(8):
+            if cnt[t] == 0:
+                assert arg[t, c] == -1 and out[t, c] == 0
+                continue
+            e = arg[t, c]
+            assert ei[1, e] == t
+            assert out[t, c] == np.float32(w[e]) * x[ei[0, e], c]
+            members = np.float32(w[ei[1] == t]) * x[ei[0][ei[1] == t], c]
+            assert np.all(members <= out[t, c])
+
+
+def test_aggregate_sampled_rows_equal_full(orc):
+    n = 500
+    ei = graphgen.random_graph(13, n, 8000)
+    x = graphgen.features(13, n, 6)
+    y, S = orc.aggregate(ei, x, n, "sum")
+    rows = np.array([3, 499, 0, 250])
+    ys, Ss = orc.aggregate(ei, x, n, "sum", rows=rows)
+    assert np.array_equal(ys, y[rows]) and np.array_equal(Ss, S[rows])
+    m, a = orc.aggregate(ei, x, n, "max")
+    ms, as_ = orc.aggregate(ei, x, n, "max", rows=rows)
+    assert np.array_equal(ms, m[rows]) and np.array_equal(as_, a[rows])
+
+
+# ---------------------------------------------------------------------------
+# Segment softmax
+# ---------------------------------------------------------------------------
+
+def test_softmax_matches_scipy(orc):
+    from scipy.special import softmax
+    n, e, H = 30, 400, 3
+    seg = graphgen.random_graph(3, n, e)[1]
+    s = (graphgen.features(3, e, H) * 4).astype(np.float32)
+    a64, a32 = orc.segment_softmax(s, seg, n)
+    for t in range(n):
+        idx = np.nonzero(seg == t)[0]
+        if idx.size:
+            ref = softmax(s[idx].astype(np.float64), axis=0)
+            np.testing.assert_allclose(a64[idx], ref, rtol=1e-13)
+    assert np.array_equal(a32, a64.astype(np.float32))
+
+
+def test_softmax_closed_forms(orc):
+    seg = np.array([0, 1, 1, 1, 2, 2, 3])
+    s = np.array([5.0, 2.0, 2.0, 2.0, -100.0, 100.0, -3e38], np.float32)
+    a64, a32 = orc.segment_softmax(s, seg, 5)
+    assert a32[0] == 1.0 and a32[6] == 1.0  # size-1 segments
+    assert np.all(a32[1:4] == np.float32(1.0 / 3.0))  # constant scores
+    assert a32[5] == 1.0 and a64[4] == pytest.approx(math.exp(-200.0), rel=1e-12)
+
+
+def test_softmax_wide_spread_stays_finite(orc):
+    # exp(1000) overflows double: only a shift by the segment maximum keeps every term finite
+    seg = np.array([0, 0, 0])
+    s = np.array([-500.0, 500.0, 499.0], np.float32)
+    a64, a32 = orc.segment_softmax(s, seg, 1)
+    assert np.all(np.isfinite(a64))
+    np.testing.assert_allclose(a64, [0.0, 1 / (1 + math.exp(-1)), math.exp(-1) / (1 + math.exp(-1))],
+                               rtol=1e-14, atol=1e-300)
+
+
+def test_softmax_sums_to_one_and_shift_invariant(orc):
+    n, e, H = 1000, 30000, 4
+    seg = graphgen.random_graph(21, n, e, hub=7, hub_edges=3000)[1]
+    s = graphgen.features(21, seg.shape[0], H) * 5
+    a64, _ = orc.segment_softmax(s, seg, n)
+    tot = np.zeros((n, H))
+    np.add.at(tot, seg, a64)
+    has = np.bincount(seg, minlength=n) > 0
+    np.testing.assert_allclose(tot[has], 1.0, rtol=1e-12)
+    shift = np.random.default_rng(1).integers(-8, 8, n).astype(np.float32)  # exact in fp32
+    b64, _ = orc.segment_softmax(s + shift[seg][:, None], seg, n)
+    np.testing.assert_allclose(b64, a64, rtol=1e-5)
+
+
+# ---------------------------------------------------------------------------
+# Pooling
+# ---------------------------------------------------------------------------
+
+def test_pool_single_graph_is_column_reduction(orc):
+    x = graphgen.features(5, 37, 6)
+    gi = np.zeros(37, np.int64)
+    s, _ = orc.segment_pool(x, gi, 1, "sum")
+    np.testing.assert_allclose(s[0], x.astype(np.float64).sum(0), rtol=1e-12)
+    m, _ = orc.segment_pool(x, gi, 1, "mean")
+    np.testing.assert_allclose(m[0], x.astype(np.float64).mean(0), rtol=1e-12, atol=1e-15)
+    mx, arg = orc.segment_pool(x, gi, 1, "max")
+    assert np.array_equal(mx[0], x.max(0)) and np.array_equal(arg[0], x.argmax(0))
+
+
+def test_pool_equals_aggregation_over_membership_edges(orc):
+    sizes = np.array([3, 0, 5, 1, 4])  # an empty graph included
+    gi = np.repeat(np.arange(5), sizes)
+    nb = gi.shape[0]
+    x = graphgen.features(6, nb, 7)
+    ei = np.stack([np.arange(nb), gi])  # node n -> graph gi[n]
+    for red in ("sum", "mean"):
+        p, ps = orc.segment_pool(x, gi, 5, red)
+        a, as_ = orc.aggregate(ei, x, 5, red)
+        assert np.array_equal(p, a) and np.array_equal(ps, as_)
+    p, pa = orc.segment_pool(x, gi, 5, "max")
+    a, aa = orc.aggregate(ei, x, 5, "max")
+    assert np.array_equal(p, a) and np.array_equal(pa, aa)  # edge id == node id here
+    assert np.all(pa[1] == -1) and np.all(p[1] == 0)
+
+
+def test_pool_total_and_mean(orc):
+    sizes = np.random.default_rng(2).integers(1, 30, 50)
+    gi = np.repeat(np.arange(50), sizes)
+    x = graphgen.features(7, gi.shape[0], 5)
+    s, S = orc.segment_pool(x, gi, 50, "sum")
+    np.testing.assert_allclose(s.sum(0), x.astype(np.float64).sum(0), rtol=1e-10, atol=1e-10)
+    m, _ = orc.segment_pool(x, gi, 50, "mean")
+    np.testing.assert_allclose(m, s / sizes[:, None], rtol=1e-14)
+
+
+def test_pool_errors(orc):
+    x = np.zeros((3, 2), np.float32)
+    with pytest.raises(orc.OracleError) as ex:
+        orc.segment_pool(x, np.array([0, 2, 1]), 3)
+    assert ex.value.code == orc.ERR_UNSORTED
+    with pytest.raises(orc.OracleError) as ex:
+        orc.segment_pool(x, np.array([0, 1, 3]), 3)
+    assert ex.value.code == orc.ERR_INDEX_RANGE
+
+
+# ---------------------------------------------------------------------------
+# GAT scores
+# ---------------------------------------------------------------------------
+
+def test_gat_scores_dense(orc):
+    n, e, H, D = 15, 90, 4, 3
+    ei = graphgen.random_graph(8, n, e)
+    h = graphgen.features(8, n, H * D)
+    r = np.random.default_rng(9)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    s, S = orc.gat_scores(ei, h, a_s, a_d, H, slope=0.2)
+    h3 = h.astype(np.float64).reshape(n, H, D)
+    z = np.einsum("nhd,hd->nh", h3, a_s)[ei[0]] + np.einsum("nhd,hd->nh", h3, a_d)[ei[1]]
+    ref = np.where(z >= 0, z, np.float64(np.float32(0.2)) * z)
+    np.testing.assert_allclose(s, ref, rtol=1e-12, atol=1e-12)
+    assert np.all(S >= np.abs(s) - 1e-12)
+
+
+# ---------------------------------------------------------------------------
+# BatchGraph (Sec. 2.1.1)
+# ---------------------------------------------------------------------------
+
+def test_batch_reindex_paper_example(orc):
+    g = json.load(open(os.path.join(GOLDEN, "batch_reindex_paper_example.json")))
+    off = orc.batch_offsets(np.array(g["sizes"]))
+    assert list(off[1:3]) == g["offsets_of_graphs_2_and_3"]
+    for ex in g["one_based_examples"]:
+        zero_based = ex["node"] - 1 + off[ex["graph"] - 1]
+        assert zero_based + 1 == ex["batched_index"]
+
+
+def test_batch_equals_per_graph(orc):
+    """Applying the GNN to each graph separately equals applying it to the
+    BatchGraph (Sec. 2.1.1): 3 GCN propagations then sum / mean / max pooling."""
+    sizes, graphs = graphgen.batch_of_small_graphs(77, 40, 10, 60, 0.1)
+    ei, gi = orc.batch_graphs(sizes, graphs)
+    ei2, gi2 = graphgen.stack_batch(sizes, graphs)  # the input generator's own batching
+    assert np.array_equal(ei, ei2) and np.array_equal(gi, gi2)
+    nb = int(sizes.sum())
+    x = graphgen.features(77, nb, 6)
+    out_ei, w, _ = orc.gcn_norm(ei, nb)
+    h = x
+    for _ in range(3):
+        h, _ = orc.aggregate(out_ei, h, nb, "sum", edge_weight=w)
+        h = h.astype(np.float32)
+    pooled = {r: orc.segment_pool(h, gi, len(sizes), r)[0] for r in ("sum", "mean", "max")}
+    off = orc.batch_offsets(sizes)
+    for i, (n, g) in enumerate(zip(sizes.tolist(), graphs)):
+        oe, ow, _ = orc.gcn_norm(g, n)
+        hl = x[off[i]:off[i + 1]]
+        for _ in range(3):
+            hl, _ = orc.aggregate(oe, hl, n, "sum", edge_weight=ow)
+            hl = hl.astype(np.float32)
+        assert np.array_equal(hl, h[off[i]:off[i + 1]])
+        loc = np.zeros(n, np.int64)
+        for r in ("sum", "mean", "max"):
+            assert np.array_equal(orc.segment_pool(hl, loc, 1, r)[0][0], pooled[r][i])
