@@ -1,0 +1,244 @@
+/*
+ * tfg.h — C ABI of the MI355X (gfx950) graph map-reduce hot path.
+ *
+ * The operations are the two aggregation types of tf_geometric (arXiv
+ * 2101.11552, Sec. 1): message aggregation — gather source-node features
+ * along the edges, scale them by edge weights, reduce them into the target
+ * node — and graph pooling — reduce the node vectors of each graph of a
+ * BatchGraph into one vector per graph. Around them sit the GCN normalisation
+ * the paper caches per graph (Sec. 3) and the map -> reduce -> map softmax
+ * workflow for attention scores (Sec. 2.1.2, Fig. 5).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Graphs are the paper's Graph object (Sec. 2.1.1): node features x, and the
+ * adjacency matrix in COO form: edge_index of shape [2, E], row-major, row 0
+ * the source ids and row 1 the target ids (edge e goes from edge_index[e] to
+ * edge_index[E + e]); edge_weight [E] (or [E, H], one weight per head).
+ * Messages flow source -> target and are reduced by the target id, the reduce
+ * key of the paper's reducer (Sec. 2.1.2).
+ *
+ * Index arrays are int32 (TFG_I32) or int64 (TFG_I64); node and edge counts
+ * must stay below 2^31 (else TFG_ERR_TOO_LARGE). Floating-point data is
+ * float32, row-major; a feature matrix has a leading dimension ldx >= F (in
+ * elements). Outputs are dense row-major with leading dimension F.
+ *
+ * Memory: every pointer except `tfg_graph*` handles is DEVICE memory owned by
+ * the caller. The library never allocates device memory: callers query the
+ * workspace size (tfg_*_ws_bytes) and pass a buffer of at least that many
+ * bytes (256-byte aligned). Inputs are only read; outputs must not overlap
+ * inputs. The only host allocation is the small tfg_graph struct.
+ *
+ * Streams: every call enqueues its kernels on `stream` (a hipStream_t; NULL is
+ * the null stream) and returns without waiting, except where a call is
+ * documented to synchronise. Buffers must stay valid until the stream work is
+ * done.
+ *
+ * Errors: calls return a tfg_status. Argument errors (null pointers, negative
+ * sizes, bad enums, a workspace that is too small) are detected on the host
+ * before anything is enqueued. Index errors (an id outside its range) and an
+ * unsorted graph index are detected on the device: kernels clamp such ids so
+ * they never access memory out of bounds, record the error in a device flag,
+ * and calls that synchronise report it. tfg_last_error() gives a message for
+ * the last failing call of the calling thread.
+ *
+ * Determinism: for fixed inputs, every output is bitwise reproducible from run
+ * to run (no floating-point atomics anywhere).
+ */
+#ifndef TFG_H
+#define TFG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TFG_ABI_VERSION 1
+
+typedef enum {
+    TFG_OK = 0,
+    TFG_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad enum, F % H != 0, mismatch with a graph */
+    TFG_ERR_INDEX_RANGE = 2, /* an edge id outside [0, N_src) / [0, N), a graph id outside [0, G) */
+    TFG_ERR_UNSORTED = 3,    /* graph_index is not non-decreasing */
+    TFG_ERR_TOO_LARGE = 4,   /* a count does not fit the 31-bit internal indexing */
+    TFG_ERR_WORKSPACE = 5,   /* buffer smaller than the size the matching query returned */
+    TFG_ERR_HIP = 6          /* the HIP runtime reported an error; see tfg_last_error() */
+} tfg_status;
+
+typedef enum { TFG_SUM = 0, TFG_MEAN = 1, TFG_MAX = 2 } tfg_reduce;
+typedef enum { TFG_I32 = 0, TFG_I64 = 1 } tfg_index_type;
+/* Order of a per-edge array: the caller's COO edge order, or the graph's CSR
+ * order (edges grouped by target, input order kept inside a target). */
+typedef enum { TFG_COO = 0, TFG_CSR = 1 } tfg_edge_order;
+
+typedef void *tfg_stream_t; /* hipStream_t */
+
+/* Opaque graph handle: the CSR-by-target form of one edge list plus the
+ * launch plan for it (host struct; its device arrays live in a caller-owned
+ * buffer). */
+typedef struct tfg_graph tfg_graph;
+
+const char *tfg_status_string(int status);
+/* Message for the last failing call on this thread ("" if none). */
+const char *tfg_last_error(void);
+int tfg_abi_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Graph handle: COO -> CSR by target.                                       */
+/* ------------------------------------------------------------------------ */
+/*
+ * The paper keeps graphs in COO form and reduces over unsorted keys (Sec.
+ * 2.1.1, 2.1.2); on the GPU the reduction is done over a CSR-by-target copy,
+ * built once per graph structure and reused, in the spirit of the paper's
+ * graph-level cache (Sec. 3).
+ *
+ * tfg_graph_bytes: sizes of the persistent buffer (`buf`, kept until
+ *   destroy) and of the scratch buffer (`scratch`, needed only during create)
+ *   for a graph of E input edges over N target nodes, with N self-loops
+ *   appended when add_self_loops != 0 (E' = E + N edges in total).
+ *
+ * tfg_graph_create: validates every id (source in [0, N_src), target in
+ *   [0, N)), builds rowptr [N+1], col [E'] (source id per CSR position) and
+ *   perm [E'] (input edge id per CSR position; ids E..E'-1 are the appended
+ *   loops, loop i having id E + i), and plans the aggregation launches.
+ *   The permutation is the unique stable one: edges sorted by target, input
+ *   order kept among equal targets. Synchronises `stream` once; returns
+ *   TFG_ERR_INDEX_RANGE (and no handle) if an id is out of range. `buf` must
+ *   stay valid and unmodified until tfg_graph_destroy; `scratch` may be reused
+ *   as soon as the call returns.
+ *
+ * tfg_graph_csr: copies rowptr / col / perm (any may be NULL) into caller
+ *   buffers of N+1 / E' / E' int32, enqueued on `stream`.
+ * tfg_graph_info: host-side sizes of the handle (any pointer may be NULL).
+ * tfg_check: synchronises `stream` and returns TFG_ERR_INDEX_RANGE if any
+ *   device-side check on this graph failed, else TFG_OK.
+ * tfg_graph_destroy: frees the host struct (not `buf`).
+ */
+int tfg_graph_bytes(int64_t E, int64_t N, int add_self_loops, size_t *buf_bytes,
+                    size_t *scratch_bytes);
+int tfg_graph_create(const void *edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
+                     int add_self_loops, void *buf, size_t buf_bytes, void *scratch,
+                     size_t scratch_bytes, tfg_stream_t stream, tfg_graph **out);
+int tfg_graph_csr(const tfg_graph *g, int32_t *rowptr, int32_t *col, int32_t *perm,
+                  tfg_stream_t stream);
+int tfg_graph_info(const tfg_graph *g, int64_t *E_total, int64_t *N, int64_t *N_src,
+                   int64_t *n_chunks, int64_t *n_rows_split);
+int tfg_check(const tfg_graph *g, tfg_stream_t stream);
+int tfg_graph_destroy(tfg_graph *g);
+
+/* ------------------------------------------------------------------------ */
+/* GCN normalisation                                                         */
+/* ------------------------------------------------------------------------ */
+/*
+ * The GCN propagation matrix A_hat = D^-1/2 (A + I) D^-1/2 (GCN, Sec. 2.2),
+ * edge by edge, cached per graph structure (Sec. 3):
+ *   - with add_self_loops, a loop (i, i) of weight 1 is appended after the E
+ *     input edges for every node i (E' = E + N); existing loops are kept;
+ *   - deg[t]  = sum of the weights of the edges entering t (float32; with
+ *     unit weights an exact integer);
+ *   - dinv[t] = 1 / sqrt(deg[t]) if deg[t] > 0, else 0 (IEEE sqrt, IEEE divide);
+ *   - w_hat[e] = (dinv[src_e] * w_e) * dinv[tgt_e] (float32, left to right).
+ * edge_weight: [E] float32 or NULL (all ones). N_src = N (square A).
+ * Outputs (each may be NULL):
+ *   out_edge_index      [2, E'] int32, COO: the input edges, then the loops;
+ *   out_edge_weight     [E'] w_hat in that COO order;
+ *   out_edge_weight_csr [E'] w_hat in the CSR order of `g` (needs g);
+ *   out_deg             [N].
+ * g: NULL, or a graph created from the same edge_index with the same N and
+ *   add_self_loops. With g == NULL a transient graph is built inside `ws`
+ *   (the call then synchronises and reports index errors).
+ */
+size_t tfg_gcn_norm_ws_bytes(int64_t E, int64_t N, int add_self_loops, const tfg_graph *g);
+int tfg_gcn_norm(const void *edge_index, int index_type, int64_t E, const float *edge_weight,
+                 int64_t N, int add_self_loops, const tfg_graph *g, int32_t *out_edge_index,
+                 float *out_edge_weight, float *out_edge_weight_csr, float *out_deg, void *ws,
+                 size_t ws_bytes, tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Message aggregation                                                       */
+/* ------------------------------------------------------------------------ */
+/*
+ * Message aggregation (Sec. 1, Fig. 1) with a reduce-by-target reducer (Sec.
+ * 2.1.2). For every edge e and feature column c the message is
+ *   m_e[c] = w_e[head(c)] * x[src_e, c],   head(c) = c / (F / H),
+ * (w_e = 1 when edge_weight is NULL) and for every target t:
+ *   TFG_SUM : out[t, c] = sum of m_e[c] over the edges entering t
+ *   TFG_MEAN: that sum divided by the number of edges entering t
+ *   TFG_MAX : out[t, c] = max of fl32(w * x) over those edges; argmax[t, c] is
+ *             the id of the winning edge in edge_index (the first one in input
+ *             order on ties; +0 and -0 tie)
+ * A target without edges gets 0 (and argmax -1).
+ *
+ * edge_index: [2, E] (E = all edges, including loops a previous
+ *   tfg_gcn_norm appended). edge_weight: NULL, [E] (H = 1) or [E, H], in
+ *   `weight_order` (TFG_CSR requires g). x: [N_src, F] with leading dimension
+ *   ldx. out: [N, F]. argmax: [N, F] int32, TFG_MAX only (may be NULL).
+ * Sums are float32 in a fixed order: each lane keeps short partial chains
+ *   that are combined pairwise, so the error stays within a few hundred units
+ *   of float32 rounding of the sum of |m_e[c]|, however long the row.
+ * g: NULL, or a graph of this edge_index (E' equal to E, same N and N_src);
+ *   NULL builds a transient graph in `ws` (then the call synchronises).
+ */
+size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N, int64_t F, int reduce, const tfg_graph *g);
+int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float *edge_weight,
+                  int64_t H, int weight_order, const float *x, int64_t N_src, int64_t F,
+                  int64_t ldx, int64_t N, int reduce, const tfg_graph *g, float *out,
+                  int32_t *argmax, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Attention: edge scores and segment softmax                               */
+/* ------------------------------------------------------------------------ */
+/*
+ * The first map of the paper's GAT workflow (Sec. 2.1.2, Fig. 5a): per node
+ * and head k, a_s[n, k] = sum_d a_src[k, d] h[n, k*D + d] and a_d likewise
+ * with a_dst; per edge, s[e, k] = LeakyReLU(a_s[src_e, k] + a_d[tgt_e, k])
+ * with negative slope `slope`. h: [N, H*D]; a_src, a_dst: [H, D];
+ * out_scores: [E, H] in the caller's edge order.
+ */
+size_t tfg_gat_edge_scores_ws_bytes(int64_t N, int64_t H);
+int tfg_gat_edge_scores(const void *edge_index, int index_type, int64_t E, const float *h,
+                        int64_t N, int64_t H, int64_t D, const float *a_src, const float *a_dst,
+                        float slope, float *out_scores, void *ws, size_t ws_bytes,
+                        tfg_stream_t stream);
+
+/*
+ * Segment softmax: the reduce and the last map of the same workflow (Sec.
+ * 2.1.2, Fig. 5): for every segment t (the edges with seg[e] = t) and head h,
+ *   out[e, h] = exp(s[e, h] - m) / sum over the segment of exp(s - m)
+ * with m the segment's maximum (a shift that leaves the result unchanged).
+ * scores: [E, H]; seg: [E] target ids in [0, N) (normally edge_index + E);
+ * out: [E, H] in the caller's edge order; out_csr: NULL or [E, H] in the CSR
+ * order of g (feeds tfg_aggregate with TFG_CSR weights). g: NULL or a graph
+ * whose targets are seg (built from the edge list seg belongs to).
+ */
+size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_graph *g);
+int tfg_segment_softmax(const float *scores, int64_t E, int64_t H, const void *seg,
+                        int index_type, int64_t N, const tfg_graph *g, float *out,
+                        float *out_csr, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Graph pooling                                                             */
+/* ------------------------------------------------------------------------ */
+/*
+ * Graph pooling (Sec. 1, Fig. 2a) over a BatchGraph's node_graph_index (Sec.
+ * 2.1.1): node n belongs to graph graph_index[n]; ids must be in [0, G) and
+ * non-decreasing (BatchGraph numbers the nodes graph by graph).
+ *   TFG_SUM / TFG_MEAN (divided by the node count) / TFG_MAX with argmax =
+ *   node id (the lowest on ties). A graph without nodes gets 0 (argmax -1).
+ * x: [Nb, F] with leading dimension ldx; out: [G, F]; argmax: [G, F] int32 or
+ * NULL (TFG_MAX only). validate != 0: synchronise and return
+ * TFG_ERR_INDEX_RANGE / TFG_ERR_UNSORTED for bad ids; validate == 0: do not
+ * wait (bad ids are clamped: no fault, unspecified values).
+ */
+size_t tfg_segment_pool_ws_bytes(int64_t Nb, int64_t G);
+int tfg_segment_pool(const float *x, int64_t Nb, int64_t F, int64_t ldx, const void *graph_index,
+                     int index_type, int64_t G, int reduce, float *out, int32_t *argmax,
+                     int validate, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TFG_H */

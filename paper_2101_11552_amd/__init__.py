@@ -1,0 +1,366 @@
+"""Python binding of libtfg.so, the MI355X (gfx950) graph map-reduce hot path.
+
+Argument marshalling only: every function here takes torch tensors on a ROCm
+device, allocates outputs and workspaces with torch, and calls the C entry
+point of the same name in ``include/tfg.h`` on torch's current stream. All
+computation happens in the HIP kernels of the library; there is no fallback.
+
+Index tensors may be int32 or int64. Features, weights and scores are
+float32. ``edge_index`` has shape [2, E] (row 0 sources, row 1 targets).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "TfgError", "Graph", "tfg_graph_create", "tfg_graph_csr", "tfg_check", "tfg_gcn_norm",
+    "tfg_aggregate", "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_pool",
+    "library_path", "load",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtfg.so")
+
+TFG_OK, TFG_ERR_INVALID_ARG, TFG_ERR_INDEX_RANGE, TFG_ERR_UNSORTED = 0, 1, 2, 3
+TFG_ERR_TOO_LARGE, TFG_ERR_WORKSPACE, TFG_ERR_HIP = 4, 5, 6
+_REDUCE = {"sum": 0, "mean": 1, "max": 2}
+_ORDER = {"coo": 0, "csr": 1}
+
+_lib = None
+
+
+class TfgError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class TfgIndexError(TfgError, IndexError):
+    pass
+
+
+class TfgValueError(TfgError, ValueError):
+    pass
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def load():
+    """Loads libtfg.so (built by ``paper_2101_11552_amd.build``); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run paper_2101_11552_amd/build.py "
+                           "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, sz, p, i32 = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int
+    ci = ctypes.c_int
+    sig = {
+        "tfg_status_string": (ctypes.c_char_p, [ci]),
+        "tfg_last_error": (ctypes.c_char_p, []),
+        "tfg_abi_version": (ci, []),
+        "tfg_graph_bytes": (ci, [i64, i64, ci, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
+        "tfg_graph_create": (ci, [p, ci, i64, i64, i64, ci, p, sz, p, sz, p,
+                                  ctypes.POINTER(p)]),
+        "tfg_graph_csr": (ci, [p, p, p, p, p]),
+        "tfg_graph_info": (ci, [p, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                ctypes.POINTER(i64), ctypes.POINTER(i64)]),
+        "tfg_check": (ci, [p, p]),
+        "tfg_graph_destroy": (ci, [p]),
+        "tfg_gcn_norm_ws_bytes": (sz, [i64, i64, ci, p]),
+        "tfg_gcn_norm": (ci, [p, ci, i64, p, i64, ci, p, p, p, p, p, p, sz, p]),
+        "tfg_aggregate_ws_bytes": (sz, [i64, i64, i64, ci, p]),
+        "tfg_aggregate": (ci, [p, ci, i64, p, i64, ci, p, i64, i64, i64, i64, ci, p, p, p, p,
+                               sz, p]),
+        "tfg_gat_edge_scores_ws_bytes": (sz, [i64, i64]),
+        "tfg_gat_edge_scores": (ci, [p, ci, i64, p, i64, i64, i64, p, p, ctypes.c_float, p, p,
+                                     sz, p]),
+        "tfg_segment_softmax_ws_bytes": (sz, [i64, i64, i64, p]),
+        "tfg_segment_softmax": (ci, [p, i64, i64, p, ci, i64, p, p, p, p, sz, p]),
+        "tfg_segment_pool_ws_bytes": (sz, [i64, i64]),
+        "tfg_segment_pool": (ci, [p, i64, i64, i64, p, ci, i64, ci, p, p, ci, p, sz, p]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    del i32
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status == TFG_OK:
+        return
+    lib = load()
+    msg = f"{lib.tfg_status_string(status).decode()}: {lib.tfg_last_error().decode()}"
+    if status == TFG_ERR_INDEX_RANGE:
+        raise TfgIndexError(status, msg)
+    if status in (TFG_ERR_INVALID_ARG, TFG_ERR_UNSORTED, TFG_ERR_TOO_LARGE, TFG_ERR_WORKSPACE):
+        raise TfgValueError(status, msg)
+    raise TfgError(status, msg)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _index_type(t: torch.Tensor) -> int:
+    if t.dtype == torch.int32:
+        return 0
+    if t.dtype == torch.int64:
+        return 1
+    raise TypeError(f"index tensor must be int32 or int64, got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, what: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    return t
+
+
+def _edges(edge_index: torch.Tensor) -> torch.Tensor:
+    _dev(edge_index, "edge_index")
+    if edge_index.dim() != 2 or edge_index.shape[0] != 2:
+        raise ValueError("edge_index must have shape [2, E]")
+    return edge_index.contiguous()
+
+
+def _f32(t: torch.Tensor | None, what: str) -> torch.Tensor | None:
+    if t is None:
+        return None
+    _dev(t, what)
+    if t.dtype != torch.float32:
+        raise TypeError(f"{what} must be float32")
+    return t.contiguous()
+
+
+def _rows(x: torch.Tensor, what: str):
+    """float32 2-D device tensor with unit column stride; returns (x, ldx)."""
+    _dev(x, what)
+    if x.dtype != torch.float32 or x.dim() != 2:
+        raise TypeError(f"{what} must be a float32 matrix")
+    if x.stride(1) != 1 or x.stride(0) < x.shape[1]:
+        x = x.contiguous()
+    return x, max(x.stride(0), x.shape[1])
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+class Graph:
+    """CSR-by-target form of one edge list (the handle of tfg_graph_create).
+
+    Holds the device buffer the handle's arrays live in; ``E`` counts all
+    edges, including the N self-loops appended when ``add_self_loops``."""
+
+    def __init__(self, handle, buf, E_in, E, N, N_src, loops, device):
+        self._h = handle
+        self.buf = buf
+        self.E_in, self.E, self.N, self.N_src, self.loops = E_in, E, N, N_src, loops
+        self.device = device
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self):
+        vals = [ctypes.c_int64() for _ in range(5)]
+        _check(load().tfg_graph_info(self._h, *[ctypes.byref(v) for v in vals]))
+        keys = ("E", "N", "N_src", "n_chunks", "n_rows_split")
+        return dict(zip(keys, (v.value for v in vals)))
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h is not None and _lib is not None:
+            _lib.tfg_graph_destroy(h)
+
+
+def tfg_graph_bytes(E: int, N: int, add_self_loops: bool = False):
+    b, s = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().tfg_graph_bytes(E, N, int(add_self_loops), ctypes.byref(b), ctypes.byref(s)))
+    return b.value, s.value
+
+
+def tfg_graph_create(edge_index: torch.Tensor, N: int, N_src: int | None = None,
+                     add_self_loops: bool = False, buf: torch.Tensor | None = None,
+                     scratch: torch.Tensor | None = None) -> Graph:
+    """COO -> CSR by target (synchronises once; raises IndexError on a bad id)."""
+    lib = load()
+    ei = _edges(edge_index)
+    E = ei.shape[1]
+    N_src = N if N_src is None else N_src
+    nb, ns = tfg_graph_bytes(E, N, add_self_loops)
+    dev = ei.device
+    if buf is None or buf.numel() < nb:
+        buf = _workspace(nb, dev)
+    if scratch is None or scratch.numel() < ns:
+        scratch = _workspace(ns, dev)
+    h = ctypes.c_void_p()
+    _check(lib.tfg_graph_create(_ptr(ei), _index_type(ei), E, N_src, N, int(add_self_loops),
+                                _ptr(buf), buf.numel(), _ptr(scratch), scratch.numel(),
+                                _stream(dev), ctypes.byref(h)))
+    return Graph(h, buf, E, E + (N if add_self_loops else 0), N, N_src, bool(add_self_loops), dev)
+
+
+def tfg_graph_csr(g: Graph):
+    """(rowptr [N+1], col [E], perm [E]) as int32 device tensors."""
+    rowptr = torch.empty(g.N + 1, dtype=torch.int32, device=g.device)
+    col = torch.empty(g.E, dtype=torch.int32, device=g.device)
+    perm = torch.empty(g.E, dtype=torch.int32, device=g.device)
+    _check(load().tfg_graph_csr(g.handle, _ptr(rowptr), _ptr(col), _ptr(perm), _stream(g.device)))
+    return rowptr, col, perm
+
+
+def tfg_check(g: Graph):
+    _check(load().tfg_check(g.handle, _stream(g.device)))
+
+
+def tfg_gcn_norm(edge_index: torch.Tensor, N: int, edge_weight: torch.Tensor | None = None,
+                 add_self_loops: bool = True, graph: Graph | None = None,
+                 out_edge_index: bool = True, out_edge_weight: bool = True,
+                 out_edge_weight_csr: bool | None = None, out_deg: bool = True,
+                 ws: torch.Tensor | None = None):
+    """GCN normalisation D^-1/2 (A + I) D^-1/2 per edge.
+
+    Returns a dict with the requested outputs: ``edge_index`` [2, E'] int32,
+    ``edge_weight`` [E'] (COO order), ``edge_weight_csr`` [E'] (CSR order of
+    ``graph``; default: requested when a graph is given) and ``deg`` [N]."""
+    lib = load()
+    ei = _edges(edge_index)
+    E = ei.shape[1]
+    dev = ei.device
+    w = _f32(edge_weight, "edge_weight")
+    Ep = E + (N if add_self_loops else 0)
+    if out_edge_weight_csr is None:
+        out_edge_weight_csr = graph is not None
+    res = {}
+    if out_edge_index:
+        res["edge_index"] = torch.empty((2, Ep), dtype=torch.int32, device=dev)
+    if out_edge_weight:
+        res["edge_weight"] = torch.empty(Ep, dtype=torch.float32, device=dev)
+    if out_edge_weight_csr:
+        res["edge_weight_csr"] = torch.empty(Ep, dtype=torch.float32, device=dev)
+    if out_deg:
+        res["deg"] = torch.empty(N, dtype=torch.float32, device=dev)
+    h = graph.handle if graph is not None else None
+    need = lib.tfg_gcn_norm_ws_bytes(E, N, int(add_self_loops), h)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    _check(lib.tfg_gcn_norm(_ptr(ei), _index_type(ei), E, _ptr(w), N, int(add_self_loops), h,
+                            _ptr(res.get("edge_index")), _ptr(res.get("edge_weight")),
+                            _ptr(res.get("edge_weight_csr")), _ptr(res.get("deg")), _ptr(ws),
+                            ws.numel(), _stream(dev)))
+    return res
+
+
+def tfg_aggregate_ws_bytes(E: int, N: int, F: int, reduce: str = "sum",
+                           graph: Graph | None = None) -> int:
+    return load().tfg_aggregate_ws_bytes(E, N, F, _REDUCE[reduce],
+                                         graph.handle if graph is not None else None)
+
+
+def tfg_aggregate(edge_index: torch.Tensor, x: torch.Tensor, N: int, reduce: str = "sum",
+                  edge_weight: torch.Tensor | None = None, heads: int = 1,
+                  weight_order: str = "coo", graph: Graph | None = None,
+                  out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
+                  ws: torch.Tensor | None = None):
+    """Message aggregation into N targets. Returns ``out`` [N, F] (and
+    ``argmax`` [N, F] int32 edge ids for ``reduce="max"``)."""
+    lib = load()
+    ei = _edges(edge_index)
+    E = ei.shape[1]
+    x, ldx = _rows(x, "x")
+    dev = x.device
+    N_src, F = x.shape
+    w = _f32(edge_weight, "edge_weight")
+    red = _REDUCE[reduce]
+    if out is None:
+        out = torch.empty((N, F), dtype=torch.float32, device=dev)
+    if red == 2 and argmax is None:
+        argmax = torch.empty((N, F), dtype=torch.int32, device=dev)
+    h = graph.handle if graph is not None else None
+    need = lib.tfg_aggregate_ws_bytes(E, N, F, red, h)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    _check(lib.tfg_aggregate(_ptr(ei), _index_type(ei), E, _ptr(w), heads, _ORDER[weight_order],
+                             _ptr(x), N_src, F, ldx, N, red, h, _ptr(out),
+                             _ptr(argmax) if red == 2 else None, _ptr(ws), ws.numel(),
+                             _stream(dev)))
+    return (out, argmax) if red == 2 else out
+
+
+def tfg_gat_edge_scores(edge_index: torch.Tensor, h: torch.Tensor, a_src: torch.Tensor,
+                        a_dst: torch.Tensor, slope: float = 0.2, out: torch.Tensor | None = None):
+    """LeakyReLU(a_src . h[src] + a_dst . h[tgt]) per edge and head -> [E, H]."""
+    lib = load()
+    ei = _edges(edge_index)
+    E = ei.shape[1]
+    h = _f32(h, "h")
+    N = h.shape[0]
+    a_src, a_dst = _f32(a_src, "a_src"), _f32(a_dst, "a_dst")
+    H = a_src.shape[0]
+    D = a_src.numel() // H
+    if h.shape[1] != H * D or a_dst.shape != a_src.shape:
+        raise ValueError("h must be [N, H*D] and a_src, a_dst [H, D]")
+    if out is None:
+        out = torch.empty((E, H), dtype=torch.float32, device=h.device)
+    ws = _workspace(lib.tfg_gat_edge_scores_ws_bytes(N, H), h.device)
+    _check(lib.tfg_gat_edge_scores(_ptr(ei), _index_type(ei), E, _ptr(h), N, H, D, _ptr(a_src),
+                                   _ptr(a_dst), float(slope), _ptr(out), _ptr(ws), ws.numel(),
+                                   _stream(h.device)))
+    return out
+
+
+def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
+                        graph: Graph | None = None, out_csr: bool = False):
+    """Softmax of scores [E, H] (or [E]) over the segments given by seg [E].
+    With ``out_csr`` (needs ``graph``) also returns the result in CSR order."""
+    lib = load()
+    s = _f32(scores, "scores")
+    squeeze = s.dim() == 1
+    s2 = s.reshape(s.shape[0], -1)
+    E, H = s2.shape
+    seg = _dev(seg, "seg").contiguous()
+    dev = s.device
+    out = torch.empty_like(s2)
+    oc = torch.empty_like(s2) if out_csr else None
+    h = graph.handle if graph is not None else None
+    ws = _workspace(lib.tfg_segment_softmax_ws_bytes(E, H, N, h), dev)
+    _check(lib.tfg_segment_softmax(_ptr(s2), E, H, _ptr(seg), _index_type(seg), N, h, _ptr(out),
+                                   _ptr(oc), _ptr(ws), ws.numel(), _stream(dev)))
+    if squeeze:
+        out = out.reshape(E)
+        oc = oc.reshape(E) if oc is not None else None
+    return (out, oc) if out_csr else out
+
+
+def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce: str = "sum",
+                     validate: bool = True, out: torch.Tensor | None = None):
+    """Pools node rows x [Nb, F] into G graphs by the sorted graph_index [Nb].
+    Returns out [G, F] (and argmax node ids [G, F] for ``reduce="max"``)."""
+    lib = load()
+    x, ldx = _rows(x, "x")
+    Nb, F = x.shape
+    gi = _dev(graph_index, "graph_index").contiguous()
+    red = _REDUCE[reduce]
+    dev = x.device
+    if out is None:
+        out = torch.empty((G, F), dtype=torch.float32, device=dev)
+    arg = torch.empty((G, F), dtype=torch.int32, device=dev) if red == 2 else None
+    ws = _workspace(lib.tfg_segment_pool_ws_bytes(Nb, G), dev)
+    _check(lib.tfg_segment_pool(_ptr(x), Nb, F, ldx, _ptr(gi), _index_type(gi), G, red, _ptr(out),
+                                _ptr(arg), int(validate), _ptr(ws), ws.numel(), _stream(dev)))
+    return (out, arg) if red == 2 else out

@@ -1,0 +1,361 @@
+// Message aggregation over the CSR-by-target graph (gfx950, wave64):
+// out[t, :] = reduce over the edges k of row t of w_k * x[col_k, :].
+//
+// One wavefront processes one work item (a whole row, or a chunk of at most
+// `chunk` edges of a long row). The 64 lanes are split into SLOTS edge slots of
+// 64/SLOTS lanes; each slot gathers one source row per step with V-wide vector
+// loads, so a wave has SLOTS * U row gathers in flight (U independent
+// accumulators per lane). Edge indices and weights are read once per 64 edges
+// with coalesced loads and broadcast from registers. Partial chains are short
+// (row length / (SLOTS * U)) and are combined pairwise, so the float32 error
+// stays small for long rows too; long rows are cut into chunks whose partial
+// results a fix-up pass combines in chunk order. No floating-point atomics:
+// every output is reproducible bit for bit.
+#include "tfg_internal.h"
+
+namespace tfg {
+namespace {
+
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+template <int V>
+__device__ __forceinline__ void load_row(const float* __restrict__ p, float (&v)[V]) {
+  if constexpr (V == 4) {
+    f4 t = *reinterpret_cast<const f4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else if constexpr (V == 2) {
+    f2 t = *reinterpret_cast<const f2*>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+    v[0] = *p;
+  }
+}
+
+template <int V>
+__device__ __forceinline__ void store_row(float* __restrict__ p, const float (&v)[V]) {
+  if constexpr (V == 4) {
+    f4 t = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<f4*>(p));
+  } else if constexpr (V == 2) {
+    f2 t = {v[0], v[1]};
+    __builtin_nontemporal_store(t, reinterpret_cast<f2*>(p));
+  } else {
+    __builtin_nontemporal_store(v[0], p);
+  }
+}
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Value held by lane (jbase + slot); jbase is wave-uniform.
+template <int SLOTS>
+__device__ __forceinline__ int bcast(int v, int jbase, int slot) {
+  if constexpr (SLOTS == 1) {
+    return __builtin_amdgcn_readlane(v, jbase);
+  } else if constexpr (SLOTS == 2) {
+    int a = __builtin_amdgcn_readlane(v, jbase);
+    int b = __builtin_amdgcn_readlane(v, jbase + 1);
+    return slot ? b : a;
+  } else if constexpr (SLOTS == 4) {
+    int a = __builtin_amdgcn_readlane(v, jbase);
+    int b = __builtin_amdgcn_readlane(v, jbase + 1);
+    int c = __builtin_amdgcn_readlane(v, jbase + 2);
+    int d = __builtin_amdgcn_readlane(v, jbase + 3);
+    return slot == 0 ? a : slot == 1 ? b : slot == 2 ? c : d;
+  } else {
+    return __shfl(v, jbase + slot);
+  }
+}
+template <int SLOTS>
+__device__ __forceinline__ float bcastf(float v, int jbase, int slot) {
+  return __int_as_float(bcast<SLOTS>(__float_as_int(v), jbase, slot));
+}
+
+// Max with the smallest edge id winning ties; arg < 0 marks "no edge yet".
+__device__ __forceinline__ void max_combine(float& v, int& a, float vb, int ab) {
+  bool take = ab >= 0 && (a < 0 || vb > v || (vb == v && ab < a));
+  v = take ? vb : v;
+  a = take ? ab : a;
+}
+
+template <int SLOTS>
+constexpr int unroll_for() {
+  return SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
+}
+
+template <int V, int SLOTS, bool MAX, bool HEADS>
+__global__ __launch_bounds__(kBlock) void spmm_rows(
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
+    int n_light, const int* __restrict__ col, const int* __restrict__ perm,
+    const float* __restrict__ w, int w_by_perm, int H, int per_head, const float* __restrict__ x,
+    int64_t ldx, int F, int mean, float* __restrict__ out, int* __restrict__ argout,
+    float* __restrict__ part, int* __restrict__ part_arg) {
+  constexpr int LPS = kWave / SLOTS;  // lanes per edge slot
+  constexpr int FC = LPS * V;         // feature columns per pass
+  constexpr int U = unroll_for<SLOTS>();
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy + n_light) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int slot = lane / LPS, sl = lane % LPS;
+  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int row = uniform(itp->row), kbeg = uniform(itp->kbeg), kend = uniform(itp->kend);
+  const int pslot = uniform(itp->slot);
+  const bool need_perm = MAX || w_by_perm;
+
+  for (int f0 = 0; f0 < F; f0 += FC) {
+    const int f = f0 + sl * V;
+    const bool fok = f < F;
+    const float* __restrict__ xf = x + (fok ? f : 0);
+    const int head = HEADS ? (fok ? f / per_head : 0) : 0;
+    float acc[U][V];
+    int arg[U][V];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        acc[u][v] = 0.0f;
+        arg[u][v] = -1;
+      }
+
+    for (int kb = kbeg; kb < kend; kb += kWave) {
+      const int n = min(kWave, kend - kb);
+      const bool lok = lane < n;
+      const int cj = lok ? __builtin_nontemporal_load(col + kb + lane) : 0;
+      const int pj = (lok && need_perm) ? __builtin_nontemporal_load(perm + kb + lane) : 0;
+      float wj = 1.0f;
+      if (!HEADS && w != nullptr && lok)
+        wj = __builtin_nontemporal_load(w + (w_by_perm ? pj : kb + lane));
+      for (int s0 = 0; s0 < n; s0 += SLOTS * U) {
+        float xv[U][V];
+        float wv[U];
+        int ev[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int jb = s0 + u * SLOTS;
+          ok[u] = jb + slot < n;
+          // cross-lane reads run with the whole wave active (a bpermute from an
+          // inactive lane does not return that lane's value)
+          const int c = bcast<SLOTS>(cj, jb, slot);
+          const int pe = need_perm ? bcast<SLOTS>(pj, jb, slot) : 0;
+          if constexpr (HEADS) {
+            wv[u] = 1.0f;
+            const int e = w_by_perm ? pe : kb + jb + slot;
+            if (w != nullptr && ok[u]) wv[u] = w[(int64_t)e * H + head];
+          } else {
+            wv[u] = bcastf<SLOTS>(wj, jb, slot);
+          }
+          if constexpr (MAX) ev[u] = pe;
+          if (ok[u] && fok) {
+            load_row<V>(xf + (int64_t)c * ldx, xv[u]);
+          } else {
+#pragma unroll
+            for (int v = 0; v < V; ++v) xv[u][v] = 0.0f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (ok[u]) {
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+              if constexpr (MAX) {
+                const float m = wv[u] * xv[u][v];
+                if (arg[u][v] < 0 || m > acc[u][v]) {
+                  acc[u][v] = m;
+                  arg[u][v] = ev[u];
+                }
+              } else {
+                acc[u][v] = __builtin_fmaf(wv[u], xv[u][v], acc[u][v]);
+              }
+            }
+          }
+        }
+      }
+    }
+
+    // Pairwise combination of the U accumulators, then across the slots.
+#pragma unroll
+    for (int step = 1; step < U; step <<= 1)
+#pragma unroll
+      for (int u = 0; u + step < U; u += 2 * step)
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          if constexpr (MAX)
+            max_combine(acc[u][v], arg[u][v], acc[u + step][v], arg[u + step][v]);
+          else
+            acc[u][v] += acc[u + step][v];
+        }
+#pragma unroll
+    for (int off = LPS; off < kWave; off <<= 1)
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const float ov = __shfl_xor(acc[0][v], off);
+        if constexpr (MAX) {
+          const int oa = __shfl_xor(arg[0][v], off);
+          max_combine(acc[0][v], arg[0][v], ov, oa);
+        } else {
+          acc[0][v] += ov;
+        }
+      }
+
+    if (slot == 0 && fok) {
+      if (pslot < 0) {
+        if (!MAX && mean && kend > kbeg) {
+          const float cnt = (float)(kend - kbeg);
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[0][v] = acc[0][v] / cnt;
+        }
+        if (MAX) {
+#pragma unroll
+          for (int v = 0; v < V; ++v)
+            if (arg[0][v] < 0) acc[0][v] = 0.0f;
+        }
+        store_row<V>(out + (int64_t)row * F + f, acc[0]);
+        if (MAX && argout != nullptr)
+#pragma unroll
+          for (int v = 0; v < V; ++v) argout[(int64_t)row * F + f + v] = arg[0][v];
+      } else {
+        float* p = part + (int64_t)pslot * F + f;
+#pragma unroll
+        for (int v = 0; v < V; ++v) p[v] = acc[0][v];
+        if (MAX)
+#pragma unroll
+          for (int v = 0; v < V; ++v) part_arg[(int64_t)pslot * F + f + v] = arg[0][v];
+      }
+    }
+  }
+}
+
+// Combines the partial results of each split row in chunk order: sums with
+// four interleaved accumulators combined pairwise, maxima with the tie rule.
+template <bool MAX>
+__global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict__ split,
+                                                     int n_split, const float* __restrict__ part,
+                                                     const int* __restrict__ part_arg, int F,
+                                                     int mean, float* __restrict__ out,
+                                                     int* __restrict__ argout) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_split) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const SplitRow sr = split[wid];
+  const int row = uniform(sr.row), slot0 = uniform(sr.slot0), nch = uniform(sr.nchunks);
+  const int deg = uniform(sr.deg);
+  for (int f = lane; f < F; f += kWave) {
+    if constexpr (MAX) {
+      float v = 0.0f;
+      int a = -1;
+      for (int j = 0; j < nch; ++j)
+        max_combine(v, a, part[(int64_t)(slot0 + j) * F + f], part_arg[(int64_t)(slot0 + j) * F + f]);
+      out[(int64_t)row * F + f] = a < 0 ? 0.0f : v;
+      if (argout != nullptr) argout[(int64_t)row * F + f] = a;
+    } else {
+      float a4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int j = 0; j < nch; ++j) a4[j & 3] += part[(int64_t)(slot0 + j) * F + f];
+      float s = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+      if (mean && deg > 0) s = s / (float)deg;
+      out[(int64_t)row * F + f] = s;
+    }
+  }
+}
+
+template <int V, int SLOTS, bool MAX, bool HEADS>
+void launch_rows(dim3 grid, hipStream_t s, const Graph& g, const float* w, int w_by_perm, int H,
+                 int per_head, const float* x, int64_t ldx, int F, int mean, float* out,
+                 int* argout, float* part, int* part_arg) {
+  spmm_rows<V, SLOTS, MAX, HEADS><<<grid, dim3(kBlock), 0, s>>>(
+      g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, w, w_by_perm, H, per_head, x, ldx, F,
+      mean, out, argout, part, part_arg);
+}
+
+template <int V, bool MAX, bool HEADS>
+void dispatch_slots(int slots, dim3 grid, hipStream_t s, const Graph& g, const float* w,
+                    int w_by_perm, int H, int per_head, const float* x, int64_t ldx, int F,
+                    int mean, float* out, int* argout, float* part, int* part_arg) {
+#define TFG_ROWS(SL)                                                                          \
+  launch_rows<V, SL, MAX, HEADS>(grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean, out, \
+                                 argout, part, part_arg)
+  switch (slots) {
+    case 1: TFG_ROWS(1); break;
+    case 2: TFG_ROWS(2); break;
+    case 4: TFG_ROWS(4); break;
+    case 8: TFG_ROWS(8); break;
+    default: TFG_ROWS(16); break;
+  }
+#undef TFG_ROWS
+}
+
+template <bool MAX, bool HEADS>
+void dispatch_vec(int vec, int slots, dim3 grid, hipStream_t s, const Graph& g, const float* w,
+                  int w_by_perm, int H, int per_head, const float* x, int64_t ldx, int F, int mean,
+                  float* out, int* argout, float* part, int* part_arg) {
+  if (vec == 4)
+    dispatch_slots<4, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
+                                  out, argout, part, part_arg);
+  else if (vec == 2)
+    dispatch_slots<2, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
+                                  out, argout, part, part_arg);
+  else
+    dispatch_slots<1, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
+                                  out, argout, part, part_arg);
+}
+
+}  // namespace
+
+size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce) {
+  size_t per = sizeof(float) + (reduce == TFG_MAX ? sizeof(int) : 0);
+  return align_up((size_t)std::max<int64_t>(n_partials, 1) * (size_t)F * per + 256, 256);
+}
+
+int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
+                     int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax, void* ws,
+                     hipStream_t s) {
+  if (g.N == 0 || F == 0) return TFG_OK;
+  const bool heads = H > 1 && w != nullptr;
+  const int per_head = (int)(F / H);
+  auto fits = [&](int v) {
+    return F % v == 0 && ldx % v == 0 && reinterpret_cast<uintptr_t>(x) % (4 * v) == 0 &&
+           (!heads || per_head % v == 0);
+  };
+  const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;
+  int lanes = (int)std::min<int64_t>((F + vec - 1) / vec, kWave);
+  int p2 = 1;
+  while (p2 < lanes) p2 <<= 1;
+  const int slots = std::min(kWave / p2, 16);
+  const int w_by_perm = (w != nullptr && w_order == TFG_COO) ? 1 : 0;
+  const int mean = reduce == TFG_MEAN;
+  const bool mx = reduce == TFG_MAX;
+
+  float* part = static_cast<float*>(ws);
+  int* part_arg = reinterpret_cast<int*>(part + (size_t)std::max(g.n_heavy, 1) * F);
+  const int waves = g.n_heavy + g.n_light;
+  dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
+  const int Fi = (int)F;
+  if (waves > 0) {
+    if (mx && heads)
+      dispatch_vec<true, true>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
+                               mean, out, argmax, part, part_arg);
+    else if (mx)
+      dispatch_vec<true, false>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
+                                mean, out, argmax, part, part_arg);
+    else if (heads)
+      dispatch_vec<false, true>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
+                                mean, out, argmax, part, part_arg);
+    else
+      dispatch_vec<false, false>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx,
+                                 Fi, mean, out, argmax, part, part_arg);
+    TFG_LAUNCHED("spmm_rows");
+  }
+  if (g.n_split > 0) {
+    dim3 fgrid((unsigned)((g.n_split + kBlock / kWave - 1) / (kBlock / kWave)));
+    if (mx)
+      fixup_rows<true><<<fgrid, dim3(kBlock), 0, s>>>(g.split, g.n_split, part, part_arg, Fi, mean,
+                                                      out, argmax);
+    else
+      fixup_rows<false><<<fgrid, dim3(kBlock), 0, s>>>(g.split, g.n_split, part, part_arg, Fi,
+                                                       mean, out, argmax);
+    TFG_LAUNCHED("fixup_rows");
+  }
+  return TFG_OK;
+}
+
+}  // namespace tfg

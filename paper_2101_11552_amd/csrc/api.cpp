@@ -1,0 +1,401 @@
+// extern "C" entry points of include/tfg.h: argument checks, workspace
+// carving and graph handles around the kernels in the .hip sources.
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "tfg_internal.h"
+
+struct tfg_graph {
+  tfg::Graph g;
+};
+
+namespace tfg {
+
+namespace {
+thread_local std::string g_last_error;
+constexpr int64_t kMaxCount = (int64_t(1) << 31) - 1;
+}  // namespace
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+int fail(int status, const std::string& msg) {
+  set_error(msg);
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  set_error(std::string(what) + ": " + hipGetErrorString(e));
+  return TFG_ERR_HIP;
+}
+
+namespace {
+
+hipStream_t as_stream(tfg_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool bad_index_type(int t) { return t != TFG_I32 && t != TFG_I64; }
+
+// Carves a caller buffer into 256-byte aligned pieces.
+struct Carver {
+  char* base;
+  size_t size, off = 0;
+  Carver(void* b, size_t n) : base(static_cast<char*>(b)), size(n) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off = align_up(off + bytes, 256);
+    return p;
+  }
+};
+
+size_t graph_total_bytes(int64_t E, int64_t N) {
+  return graph_layout(E, N, default_chunk()).total + graph_scratch_bytes(E, N);
+}
+
+int check_counts(int64_t E, int64_t N, int64_t N_src) {
+  if (E < 0 || N < 0 || N_src < 0) return fail(TFG_ERR_INVALID_ARG, "negative size");
+  if (E > kMaxCount || N >= kMaxCount || N_src >= kMaxCount)
+    return fail(TFG_ERR_TOO_LARGE, "edge or node count does not fit 31-bit indexing");
+  return TFG_OK;
+}
+
+// Fills g's device pointers from `buf` and builds the CSR form.
+int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int64_t E_in,
+                 int64_t N_src, int64_t N, int loops, void* buf, size_t buf_bytes, void* scratch,
+                 size_t scratch_bytes, hipStream_t s) {
+  g.E_in = E_in;
+  g.E = E_in + (loops ? N : 0);
+  g.N = N;
+  g.N_src = N_src;
+  g.loops = loops ? 1 : 0;
+  g.chunk = default_chunk();
+  int rc = check_counts(g.E, N, N_src);
+  if (rc) return rc;
+  GraphLayout L = graph_layout(g.E, N, g.chunk);
+  if (buf == nullptr || buf_bytes < L.total)
+    return fail(TFG_ERR_WORKSPACE, "graph buffer too small");
+  char* b = static_cast<char*>(buf);
+  g.rowptr = reinterpret_cast<int*>(b + L.rowptr);
+  g.col = reinterpret_cast<int*>(b + L.col);
+  g.perm = reinterpret_cast<int*>(b + L.perm);
+  g.heavy = reinterpret_cast<WorkItem*>(b + L.heavy);
+  g.light = reinterpret_cast<WorkItem*>(b + L.light);
+  g.split = reinterpret_cast<SplitRow*>(b + L.split);
+  g.counters = reinterpret_cast<int*>(b + L.counters);
+  TFG_HIP(hipGetDevice(&g.device));
+  return build_graph(g, src, tgt, index_type, scratch, scratch_bytes, s);
+}
+
+const void* tgt_row(const void* edge_index, int index_type, int64_t E) {
+  if (edge_index == nullptr) return nullptr;
+  return index_type == TFG_I64 ? static_cast<const void*>(static_cast<const int64_t*>(edge_index) + E)
+                               : static_cast<const void*>(static_cast<const int32_t*>(edge_index) + E);
+}
+
+// Either checks that `g` describes an edge list of E edges over N_src x N
+// (with or without loops), or builds a transient graph in the carver.
+int graph_or_transient(const tfg_graph* handle, Graph& tmp, const Graph*& g, const void* src,
+                       const void* tgt, int index_type, int64_t E, int64_t N_src, int64_t N,
+                       int loops, Carver& ws, hipStream_t s) {
+  if (handle) {
+    g = &handle->g;
+    if (g->E_in != E || g->N != N || g->N_src != N_src || g->loops != (loops ? 1 : 0))
+      return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
+    return TFG_OK;
+  }
+  const int64_t Ep = E + (loops ? N : 0);
+  GraphLayout L = graph_layout(Ep, N, default_chunk());
+  size_t sc = graph_scratch_bytes(Ep, N);
+  void* buf = ws.take(L.total);
+  void* scratch = ws.take(sc);
+  if (ws.off > ws.size) return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  int rc = create_graph(tmp, src, tgt, index_type, E, N_src, N, loops, buf, L.total, scratch, sc, s);
+  g = &tmp;
+  return rc;
+}
+
+}  // namespace
+}  // namespace tfg
+
+using namespace tfg;
+
+extern "C" {
+
+const char* tfg_status_string(int status) {
+  switch (status) {
+    case TFG_OK: return "ok";
+    case TFG_ERR_INVALID_ARG: return "invalid argument";
+    case TFG_ERR_INDEX_RANGE: return "index out of range";
+    case TFG_ERR_UNSORTED: return "graph index not sorted";
+    case TFG_ERR_TOO_LARGE: return "size too large";
+    case TFG_ERR_WORKSPACE: return "workspace too small";
+    case TFG_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* tfg_last_error(void) { return g_last_error.c_str(); }
+
+int tfg_abi_version(void) { return TFG_ABI_VERSION; }
+
+int tfg_graph_bytes(int64_t E, int64_t N, int add_self_loops, size_t* buf_bytes,
+                    size_t* scratch_bytes) {
+  int rc = check_counts(E, N, 0);
+  if (rc) return rc;
+  const int64_t Ep = E + (add_self_loops ? N : 0);
+  rc = check_counts(Ep, N, 0);
+  if (rc) return rc;
+  if (buf_bytes) *buf_bytes = graph_layout(Ep, N, default_chunk()).total;
+  if (scratch_bytes) *scratch_bytes = graph_scratch_bytes(Ep, N);
+  return TFG_OK;
+}
+
+int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
+                     int add_self_loops, void* buf, size_t buf_bytes, void* scratch,
+                     size_t scratch_bytes, tfg_stream_t stream, tfg_graph** out) {
+  if (out == nullptr) return fail(TFG_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  if (E > 0 && edge_index == nullptr) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
+  if (add_self_loops && N_src != N)
+    return fail(TFG_ERR_INVALID_ARG, "self-loops need N_src == N");
+  if (scratch == nullptr) return fail(TFG_ERR_INVALID_ARG, "scratch is NULL");
+  tfg_graph* h = new (std::nothrow) tfg_graph;
+  if (!h) return fail(TFG_ERR_HIP, "host allocation failed");
+  int rc = create_graph(h->g, edge_index, tgt_row(edge_index, index_type, E), index_type, E, N_src,
+                        N, add_self_loops, buf, buf_bytes, scratch, scratch_bytes,
+                        as_stream(stream));
+  if (rc) {
+    delete h;
+    return rc;
+  }
+  *out = h;
+  return TFG_OK;
+}
+
+int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* perm,
+                  tfg_stream_t stream) {
+  if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& g = h->g;
+  hipStream_t s = as_stream(stream);
+  if (rowptr)
+    TFG_HIP(hipMemcpyAsync(rowptr, g.rowptr, sizeof(int) * (g.N + 1), hipMemcpyDeviceToDevice, s));
+  if (col && g.E)
+    TFG_HIP(hipMemcpyAsync(col, g.col, sizeof(int) * g.E, hipMemcpyDeviceToDevice, s));
+  if (perm && g.E)
+    TFG_HIP(hipMemcpyAsync(perm, g.perm, sizeof(int) * g.E, hipMemcpyDeviceToDevice, s));
+  return TFG_OK;
+}
+
+int tfg_graph_info(const tfg_graph* h, int64_t* E_total, int64_t* N, int64_t* N_src,
+                   int64_t* n_chunks, int64_t* n_rows_split) {
+  if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  if (E_total) *E_total = h->g.E;
+  if (N) *N = h->g.N;
+  if (N_src) *N_src = h->g.N_src;
+  if (n_chunks) *n_chunks = h->g.n_heavy;
+  if (n_rows_split) *n_rows_split = h->g.n_split;
+  return TFG_OK;
+}
+
+int tfg_check(const tfg_graph* h, tfg_stream_t stream) {
+  if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  int flags = 0;
+  hipStream_t s = as_stream(stream);
+  TFG_HIP(hipMemcpyAsync(&flags, h->g.counters + 3, sizeof(int), hipMemcpyDeviceToHost, s));
+  TFG_HIP(hipStreamSynchronize(s));
+  if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "an id was out of range");
+  return TFG_OK;
+}
+
+int tfg_graph_destroy(tfg_graph* h) {
+  delete h;
+  return TFG_OK;
+}
+
+size_t tfg_gcn_norm_ws_bytes(int64_t E, int64_t N, int add_self_loops, const tfg_graph* g) {
+  if (E < 0 || N < 0) return 0;
+  size_t b = align_up(sizeof(float) * (size_t)std::max<int64_t>(N, 1), 256);
+  if (!g) b += graph_total_bytes(E + (add_self_loops ? N : 0), N);
+  return b;
+}
+
+int tfg_gcn_norm(const void* edge_index, int index_type, int64_t E, const float* edge_weight,
+                 int64_t N, int add_self_loops, const tfg_graph* g, int32_t* out_edge_index,
+                 float* out_edge_weight, float* out_edge_weight_csr, float* out_deg, void* ws,
+                 size_t ws_bytes, tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E + (add_self_loops ? N : 0), N, N);
+  if (rc) return rc;
+  if (E > 0 && edge_index == nullptr) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
+  if (ws == nullptr || ws_bytes < tfg_gcn_norm_ws_bytes(E, N, add_self_loops, g))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (out_edge_weight_csr && !g)
+    return fail(TFG_ERR_INVALID_ARG, "CSR-order output needs a graph handle");
+  hipStream_t s = as_stream(stream);
+  Carver c(ws, ws_bytes);
+  float* dinv = static_cast<float*>(c.take(sizeof(float) * (size_t)std::max<int64_t>(N, 1)));
+  Graph tmp;
+  const Graph* gp = nullptr;
+  rc = graph_or_transient(g, tmp, gp, edge_index, tgt_row(edge_index, index_type, E), index_type,
+                          E, N, N, add_self_loops, c, s);
+  if (rc) return rc;
+  rc = launch_gcn_norm(*gp, edge_index, index_type, edge_weight, out_edge_index, out_edge_weight,
+                       out_edge_weight_csr, out_deg, dinv, s);
+  if (rc) return rc;
+  if (!g) TFG_HIP(hipStreamSynchronize(s));  // the transient graph lives in ws
+  return TFG_OK;
+}
+
+size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N, int64_t F, int reduce, const tfg_graph* g) {
+  if (E < 0 || N < 0 || F < 0) return 0;
+  int64_t partials = g ? g->g.n_heavy : graph_layout(E, N, default_chunk()).cap_heavy;
+  size_t b = aggregate_partial_bytes(partials, F, reduce);
+  if (!g) b += graph_total_bytes(E, N);
+  return b;
+}
+
+int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float* edge_weight,
+                  int64_t H, int weight_order, const float* x, int64_t N_src, int64_t F,
+                  int64_t ldx, int64_t N, int reduce, const tfg_graph* g, float* out,
+                  int32_t* argmax, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E, N, N_src);
+  if (rc) return rc;
+  if (reduce != TFG_SUM && reduce != TFG_MEAN && reduce != TFG_MAX)
+    return fail(TFG_ERR_INVALID_ARG, "bad reduce");
+  if (weight_order != TFG_COO && weight_order != TFG_CSR)
+    return fail(TFG_ERR_INVALID_ARG, "bad weight order");
+  if (F < 0 || H < 1 || (F > 0 && F % H != 0))
+    return fail(TFG_ERR_INVALID_ARG, "F must be >= 0 and a multiple of H >= 1");
+  if (F >= kMaxCount || ldx < F) return fail(TFG_ERR_INVALID_ARG, "bad F / ldx");
+  if (N_src * std::max<int64_t>(ldx, 1) >= (int64_t(1) << 62)) return fail(TFG_ERR_TOO_LARGE, "x too large");
+  if (E > 0 && edge_index == nullptr) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
+  if (N > 0 && F > 0 && out == nullptr) return fail(TFG_ERR_INVALID_ARG, "out is NULL");
+  if (E > 0 && F > 0 && x == nullptr) return fail(TFG_ERR_INVALID_ARG, "x is NULL");
+  if (weight_order == TFG_CSR && edge_weight && !g)
+    return fail(TFG_ERR_INVALID_ARG, "CSR-order weights need a graph handle");
+  if (H > 1 && !edge_weight) H = 1;
+  if (ws == nullptr || ws_bytes < tfg_aggregate_ws_bytes(E, N, F, reduce, g))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  Carver c(ws, ws_bytes);
+  Graph tmp;
+  const Graph* gp = nullptr;
+  int64_t partials = g ? g->g.n_heavy : graph_layout(E, N, default_chunk()).cap_heavy;
+  void* part = c.take(aggregate_partial_bytes(partials, F, reduce));
+  if (g) {
+    // a handle built with loops describes the E' = E_in + N edges of this list
+    gp = &g->g;
+    if (gp->E != E || gp->N != N || gp->N_src != N_src)
+      return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
+  } else {
+    rc = graph_or_transient(nullptr, tmp, gp, edge_index, tgt_row(edge_index, index_type, E),
+                            index_type, E, N_src, N, 0, c, s);
+    if (rc) return rc;
+  }
+  rc = launch_aggregate(*gp, edge_weight, (int)H, weight_order, x, F, ldx, reduce, out, argmax,
+                        part, s);
+  if (rc) return rc;
+  if (!g) TFG_HIP(hipStreamSynchronize(s));
+  return TFG_OK;
+}
+
+size_t tfg_gat_edge_scores_ws_bytes(int64_t N, int64_t H) {
+  if (N < 0 || H < 0) return 0;
+  return align_up(sizeof(float) * (size_t)std::max<int64_t>(2 * N * H, 1), 256) + 256;
+}
+
+int tfg_gat_edge_scores(const void* edge_index, int index_type, int64_t E, const float* h,
+                        int64_t N, int64_t H, int64_t D, const float* a_src, const float* a_dst,
+                        float slope, float* out_scores, void* ws, size_t ws_bytes,
+                        tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E, N, N);
+  if (rc) return rc;
+  if (H < 1 || D < 1 || H * D >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad H / D");
+  if ((E > 0 && (edge_index == nullptr || out_scores == nullptr)) ||
+      (N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr)))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (E > 0 && N == 0) return fail(TFG_ERR_INDEX_RANGE, "edges on a graph without nodes");
+  if (ws == nullptr || ws_bytes < tfg_gat_edge_scores_ws_bytes(N, H))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  float* proj = static_cast<float*>(ws);
+  int* err = reinterpret_cast<int*>(static_cast<char*>(ws) +
+                                    align_up(sizeof(float) * (size_t)std::max<int64_t>(2 * N * H, 1), 256));
+  return launch_gat_scores(edge_index, index_type, E, h, N, (int)H, (int)D, a_src, a_dst, slope,
+                           out_scores, proj, err, as_stream(stream));
+}
+
+size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_graph* g) {
+  (void)H;
+  if (E < 0 || N < 0) return 0;
+  return g ? 256 : graph_total_bytes(E, N);
+}
+
+int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* seg, int index_type,
+                        int64_t N, const tfg_graph* g, float* out, float* out_csr, void* ws,
+                        size_t ws_bytes, tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E, N, 1);
+  if (rc) return rc;
+  if (H < 1 || E * H >= (int64_t(1) << 62)) return fail(TFG_ERR_INVALID_ARG, "bad H");
+  if (E > 0 && (scores == nullptr || out == nullptr)) return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (E > 0 && seg == nullptr && g == nullptr) return fail(TFG_ERR_INVALID_ARG, "seg is NULL");
+  if (out_csr && !g) return fail(TFG_ERR_INVALID_ARG, "CSR-order output needs a graph handle");
+  if (ws == nullptr || ws_bytes < tfg_segment_softmax_ws_bytes(E, H, N, g))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  Carver c(ws, ws_bytes);
+  const Graph* gp = nullptr;
+  Graph tmp;
+  if (g) {
+    gp = &g->g;
+    if (gp->E != E || gp->N != N) return fail(TFG_ERR_INVALID_ARG, "graph handle does not match");
+  } else {
+    rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
+    if (rc) return rc;
+  }
+  rc = launch_segment_softmax(*gp, scores, (int)H, out, out_csr, s);
+  if (rc) return rc;
+  if (!g) TFG_HIP(hipStreamSynchronize(s));
+  return TFG_OK;
+}
+
+size_t tfg_segment_pool_ws_bytes(int64_t Nb, int64_t G) {
+  (void)Nb;
+  if (G < 0) return 0;
+  return align_up(sizeof(int) * (size_t)(G + 1), 256) + 256;
+}
+
+int tfg_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const void* graph_index,
+                     int index_type, int64_t G, int reduce, float* out, int32_t* argmax,
+                     int validate, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(0, Nb, 0);
+  if (rc) return rc;
+  if (G < 0 || G >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad G");
+  if (F < 0 || F >= kMaxCount || ldx < F) return fail(TFG_ERR_INVALID_ARG, "bad F / ldx");
+  if (reduce != TFG_SUM && reduce != TFG_MEAN && reduce != TFG_MAX)
+    return fail(TFG_ERR_INVALID_ARG, "bad reduce");
+  if ((Nb > 0 && (graph_index == nullptr || (F > 0 && x == nullptr))) ||
+      (G > 0 && F > 0 && out == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (ws == nullptr || ws_bytes < tfg_segment_pool_ws_bytes(Nb, G))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  int* goff = static_cast<int*>(ws);
+  int* err = reinterpret_cast<int*>(static_cast<char*>(ws) + align_up(sizeof(int) * (size_t)(G + 1), 256));
+  rc = launch_segment_pool(x, Nb, F, ldx, graph_index, index_type, G, reduce, out, argmax, goff, err, s);
+  if (rc) return rc;
+  if (validate) {
+    int flags = 0;
+    TFG_HIP(hipMemcpyAsync(&flags, err, sizeof(int), hipMemcpyDeviceToHost, s));
+    TFG_HIP(hipStreamSynchronize(s));
+    if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "graph_index holds an id outside [0, G)");
+    if (flags & kErrUnsorted) return fail(TFG_ERR_UNSORTED, "graph_index is not non-decreasing");
+  }
+  return TFG_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+// GCN normalisation on the CSR-by-target graph (gfx950):
+//   deg[t]  = sum of the weights entering t (loops included when appended)
+//   dinv[t] = deg > 0 ? 1 / sqrt(deg) : 0         (IEEE sqrt, IEEE divide)
+//   w'[e]   = (dinv[src] * w[e]) * dinv[tgt]       (float32, left to right)
+// written in the caller's COO order and/or in the graph's CSR order; both
+// orders use the same operands in the same order, so they are bit-identical.
+#include "tfg_internal.h"
+
+namespace tfg {
+namespace {
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Weight of edge id e in the list with appended loops.
+__device__ __forceinline__ float edge_w(const float* __restrict__ w, int64_t E_in, int64_t e) {
+  return (w == nullptr || e >= E_in) ? 1.0f : w[e];
+}
+
+// Unit weights: the degree is the row length (exact in float32 below 2^24,
+// and rounded once above it).
+__global__ __launch_bounds__(kBlock) void degree_unit(const int* __restrict__ rowptr, int64_t N,
+                                                      float* __restrict__ deg,
+                                                      float* __restrict__ dinv) {
+  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N) return;
+  float d = (float)(rowptr[t + 1] - rowptr[t]);
+  if (deg) deg[t] = d;
+  dinv[t] = d > 0.0f ? 1.0f / sqrtf(d) : 0.0f;
+}
+
+// General weights: one wavefront per row, each lane summing a strided part of
+// the row in double, then a fixed-order tree across the lanes.
+__global__ __launch_bounds__(kBlock) void degree_weighted(const int* __restrict__ rowptr,
+                                                          const int* __restrict__ perm,
+                                                          const float* __restrict__ w,
+                                                          int64_t E_in, int64_t N,
+                                                          float* __restrict__ deg,
+                                                          float* __restrict__ dinv) {
+  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+  if (t >= N) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
+  double acc = 0.0;
+  for (int k = kb + lane; k < ke; k += kWave) acc += (double)edge_w(w, E_in, perm[k]);
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) {
+    float d = (float)acc;
+    if (deg) deg[t] = d;
+    dinv[t] = d > 0.0f ? 1.0f / sqrtf(d) : 0.0f;
+  }
+}
+
+// CSR order: one wavefront per aggregation work item (row or row chunk).
+__global__ __launch_bounds__(kBlock) void weights_csr(const WorkItem* __restrict__ heavy,
+                                                      int n_heavy,
+                                                      const WorkItem* __restrict__ light,
+                                                      int n_light, const int* __restrict__ col,
+                                                      const int* __restrict__ perm,
+                                                      const float* __restrict__ w, int64_t E_in,
+                                                      const float* __restrict__ dinv,
+                                                      float* __restrict__ out) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy + n_light) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const WorkItem* it = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int row = uniform(it->row), kb = uniform(it->kbeg), ke = uniform(it->kend);
+  const float dt = dinv[row];
+  for (int k = kb + lane; k < ke; k += kWave) {
+    const float we = w ? edge_w(w, E_in, perm[k]) : 1.0f;
+    const float a = dinv[col[k]] * we;
+    out[k] = a * dt;
+  }
+}
+
+// COO order (input edges, then loops), optionally writing the edge list.
+template <typename IdxT>
+__global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ src,
+                                                      const IdxT* __restrict__ tgt, int64_t E_in,
+                                                      int64_t E, int64_t N,
+                                                      const float* __restrict__ w,
+                                                      const float* __restrict__ dinv,
+                                                      int32_t* __restrict__ out_ei,
+                                                      float* __restrict__ out_w) {
+  int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  int s, t;
+  if (e < E_in) {
+    int64_t sv = (int64_t)src[e], tv = (int64_t)tgt[e];
+    s = (sv < 0 || sv >= N) ? 0 : (int)sv;  // ids were validated when the graph was built
+    t = (tv < 0 || tv >= N) ? 0 : (int)tv;
+  } else {
+    s = t = (int)(e - E_in);
+  }
+  if (out_ei) {
+    out_ei[e] = s;
+    out_ei[E + e] = t;
+  }
+  if (out_w) {
+    const float a = dinv[s] * edge_w(w, E_in, e);
+    out_w[e] = a * dinv[t];
+  }
+}
+
+}  // namespace
+
+int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
+                    const float* edge_weight, int32_t* out_edge_index, float* out_w,
+                    float* out_w_csr, float* out_deg, float* dinv, hipStream_t s) {
+  if (g.N == 0) return TFG_OK;
+  const unsigned nb_rows = (unsigned)((g.N + kBlock - 1) / kBlock);
+  if (edge_weight == nullptr) {
+    degree_unit<<<nb_rows, kBlock, 0, s>>>(g.rowptr, g.N, out_deg, dinv);
+  } else {
+    degree_weighted<<<(unsigned)((g.N + 3) / 4), kBlock, 0, s>>>(g.rowptr, g.perm, edge_weight,
+                                                                 g.E_in, g.N, out_deg, dinv);
+  }
+  TFG_LAUNCHED("gcn degree");
+  const int waves = g.n_heavy + g.n_light;
+  if (out_w_csr && waves > 0) {
+    weights_csr<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
+        g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, edge_weight, g.E_in, dinv,
+        out_w_csr);
+    TFG_LAUNCHED("gcn weights (CSR order)");
+  }
+  if ((out_w || out_edge_index) && g.E > 0) {
+    const unsigned nb = (unsigned)((g.E + kBlock - 1) / kBlock);
+    if (index_type == TFG_I64) {
+      const int64_t* ei = static_cast<const int64_t*>(edge_index);
+      weights_coo<int64_t><<<nb, kBlock, 0, s>>>(ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight,
+                                                  dinv, out_edge_index, out_w);
+    } else {
+      const int32_t* ei = static_cast<const int32_t*>(edge_index);
+      weights_coo<int32_t><<<nb, kBlock, 0, s>>>(ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight,
+                                                  dinv, out_edge_index, out_w);
+    }
+    TFG_LAUNCHED("gcn weights (COO order)");
+  }
+  return TFG_OK;
+}
+
+}  // namespace tfg

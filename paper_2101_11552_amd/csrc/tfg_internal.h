@@ -1,0 +1,106 @@
+// Internal declarations of the HIP library behind include/tfg.h (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/tfg.h"
+
+namespace tfg {
+
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kBlock = 256;        // threads per block for most kernels (4 waves)
+constexpr int kDefaultChunk = 512; // max edges per aggregation work item
+
+// Device error flag bits (graph->err and the pooling workspace flag).
+constexpr int kErrIndex = 1;
+constexpr int kErrUnsorted = 2;
+
+// One aggregation work item, processed by one wavefront: the CSR positions
+// [kbeg, kend) of target `row`. slot < 0: the item covers the whole row and
+// writes the output row; slot >= 0: the row is split, the item writes partial
+// result `slot` and a fix-up pass combines the row's partials in order.
+struct WorkItem {
+  int row, kbeg, kend, slot;
+};
+// A split row: its partials are slot0 .. slot0 + nchunks - 1, in row order.
+struct SplitRow {
+  int row, slot0, nchunks, deg;
+};
+
+// Host view of a graph; the arrays live in the caller's persistent buffer.
+struct Graph {
+  int64_t E_in = 0;    // input edges
+  int64_t E = 0;       // total edges (input + appended loops)
+  int64_t N = 0;       // targets
+  int64_t N_src = 0;   // sources
+  int loops = 0;
+  int chunk = kDefaultChunk;
+  int* rowptr = nullptr;  // [N+1]
+  int* col = nullptr;     // [E]
+  int* perm = nullptr;    // [E]
+  WorkItem* heavy = nullptr;  // chunks of split rows; heavy[i] writes partial i
+  WorkItem* light = nullptr;  // whole rows
+  SplitRow* split = nullptr;
+  int* counters = nullptr;    // device: [0] heavy, [1] light, [2] split, [3] error flags
+  int n_heavy = 0, n_light = 0, n_split = 0;
+  int device = 0;
+};
+
+// Sizes of the persistent / scratch parts of a graph.
+struct GraphLayout {
+  size_t rowptr, col, perm, heavy, light, split, counters, total;
+  int64_t cap_heavy, cap_light, cap_split;
+};
+GraphLayout graph_layout(int64_t E, int64_t N, int chunk);
+size_t graph_scratch_bytes(int64_t E, int64_t N);
+int default_chunk();
+
+// Thread-local error message.
+void set_error(const std::string& msg);
+int fail(int status, const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+
+#define TFG_HIP(call)                                   \
+  do {                                                  \
+    hipError_t e_ = (call);                             \
+    if (e_ != hipSuccess) return hip_fail(e_, #call);   \
+  } while (0)
+#define TFG_LAUNCHED(what)                              \
+  do {                                                  \
+    hipError_t e_ = hipGetLastError();                  \
+    if (e_ != hipSuccess) return hip_fail(e_, what);    \
+  } while (0)
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ---- launchers (each returns a tfg_status) --------------------------------
+// csr.hip
+// src may be NULL (a target-only list: col is then all zero).
+int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void* scratch,
+                size_t scratch_bytes, hipStream_t s);
+// norm.hip
+int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
+                    const float* edge_weight, int32_t* out_edge_index, float* out_w,
+                    float* out_w_csr, float* out_deg, float* dinv_ws, hipStream_t s);
+// aggregate.hip
+int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
+                     int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax,
+                     void* ws, hipStream_t s);
+size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce);
+// softmax.hip
+int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const float* h,
+                      int64_t N, int H, int D, const float* a_src, const float* a_dst,
+                      float slope, float* out, float* proj_ws, int* err, hipStream_t s);
+int launch_segment_softmax(const Graph& g, const float* scores, int H, float* out,
+                           float* out_csr, hipStream_t s);
+// pool.hip
+int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
+                        const void* graph_index, int index_type, int64_t G, int reduce,
+                        float* out, int32_t* argmax, int* goff_ws, int* err, hipStream_t s);
+
+}  // namespace tfg

@@ -1,0 +1,110 @@
+"""CPU-side checks of the C ABI: the library loads, exports every function the
+header declares, and rejects bad arguments on the host before touching a GPU."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tfg.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2101_11552_amd as tfg
+    return tfg.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tfg_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_calls():
+    names = declared_functions()
+    for n in ("tfg_gcn_norm", "tfg_aggregate", "tfg_segment_softmax", "tfg_segment_pool",
+              "tfg_graph_create", "tfg_gat_edge_scores"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", lib._name], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (tfg_[a-z0-9_]+)$", out, flags=re.M))
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        assert hasattr(lib, n)
+
+
+def test_status_strings_and_version(lib):
+    assert lib.tfg_abi_version() == 1
+    assert lib.tfg_status_string(0) == b"ok"
+    assert lib.tfg_status_string(2) == b"index out of range"
+    assert lib.tfg_status_string(99) == b"unknown status"
+
+
+def test_size_queries(lib):
+    b, s = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.tfg_graph_bytes(1000, 100, 1, ctypes.byref(b), ctypes.byref(s)) == 0
+    assert b.value >= 4 * (101 + 2 * 1100) and s.value >= 3 * 4 * 1100
+    assert lib.tfg_graph_bytes(-1, 100, 0, ctypes.byref(b), ctypes.byref(s)) == 1
+    assert lib.tfg_graph_bytes(2**31, 10, 0, ctypes.byref(b), ctypes.byref(s)) == 4
+    assert lib.tfg_graph_bytes(2**31 - 5, 10, 1, ctypes.byref(b), ctypes.byref(s)) == 4
+    assert lib.tfg_segment_pool_ws_bytes(100, 7) >= 8 * 4
+    assert lib.tfg_aggregate_ws_bytes(1000, 100, 64, 2, None) > lib.tfg_aggregate_ws_bytes(
+        1000, 100, 64, 0, None)
+
+
+def test_host_side_argument_errors(lib):
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails its checks first
+    h = ctypes.c_void_p()
+    # null output handle, bad index type
+    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, fake, 1 << 20, fake, 1 << 20, None, None) == 1
+    assert lib.tfg_graph_create(fake, 7, 10, 5, 5, 0, fake, 1 << 20, fake, 1 << 20, None,
+                                ctypes.byref(h)) == 1
+    # self-loops with a rectangular adjacency
+    assert lib.tfg_graph_create(fake, 0, 10, 4, 5, 1, fake, 1 << 20, fake, 1 << 20, None,
+                                ctypes.byref(h)) == 1
+    # buffer too small
+    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, fake, 16, fake, 1 << 20, None,
+                                ctypes.byref(h)) == 5
+    assert b"too small" in lib.tfg_last_error()
+    # aggregate: bad reduce, F not a multiple of H, ldx < F, workspace too small
+    args = dict(E=10, w=None, H=1, order=0, x=fake, N_src=5, F=8, ldx=8, N=5, red=0)
+
+    def agg(**kw):
+        a = {**args, **kw}
+        return lib.tfg_aggregate(fake, 0, a["E"], a["w"], a["H"], a["order"], a["x"], a["N_src"],
+                                 a["F"], a["ldx"], a["N"], a["red"], None, fake, None, fake,
+                                 kw.get("ws", 1 << 30), None)
+    assert agg(red=3) == 1
+    assert agg(w=fake, H=3) == 1
+    assert agg(ldx=4) == 1
+    assert agg(order=1, w=fake) == 1  # CSR-order weights need a graph
+    assert agg(ws=8) == 5
+    assert agg(E=-1) == 1
+    assert agg(N=2**31) == 4
+    # pooling: bad reduce, ldx < F
+    assert lib.tfg_segment_pool(fake, 10, 4, 4, fake, 0, 3, 5, fake, None, 1, fake, 1 << 20,
+                                None) == 1
+    assert lib.tfg_segment_pool(fake, 10, 4, 2, fake, 0, 3, 0, fake, None, 1, fake, 1 << 20,
+                                None) == 1
+    # softmax: CSR output without a graph
+    assert lib.tfg_segment_softmax(fake, 10, 2, fake, 0, 5, None, fake, fake, fake, 1 << 30,
+                                   None) == 1
+    # gat scores: bad heads
+    assert lib.tfg_gat_edge_scores(fake, 0, 10, fake, 5, 0, 4, fake, fake, 0.2, fake, fake,
+                                   1 << 20, None) == 1
+
+
+def test_python_binding_rejects_host_tensors():
+    import torch
+    import paper_2101_11552_amd as tfg
+    ei = torch.zeros((2, 3), dtype=torch.int64)
+    with pytest.raises(ValueError):
+        tfg.tfg_graph_create(ei, 4)

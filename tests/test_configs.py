@@ -1,0 +1,162 @@
+"""GPU parity on the five workloads at full size, in the launch configuration
+the benchmark uses (graph handle with self-loops, CSR-order weights).
+
+Each stage is checked on its own: the oracle of a stage consumes the GPU's
+output of the previous stage (bit-identical inputs), so every stage is gated
+on its own error and argmax stays checkable bit for bit. The largest graph is
+checked on all normalised weights and degrees (bit-exact), on the full CSR
+permutation through properties that determine it uniquely, and on a sample of
+output rows that the oracle computes one by one.
+"""
+
+import numpy as np
+import pytest
+
+import graphgen
+from test_parity import assert_rel, assert_scaled, dev, host, same_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tfg():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm device")
+    import paper_2101_11552_amd as lib
+    lib.load()
+    return lib
+
+
+def gcn_layer_setup(tfg, orc, ei, n):
+    g = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n, add_self_loops=True)
+    norm = tfg.tfg_gcn_norm(dev(ei.astype(np.int32)), n, graph=g)
+    oei, ow, odeg = orc.gcn_norm(ei, n)
+    assert np.array_equal(host(norm["edge_index"]), oei)
+    assert same_bits(host(norm["deg"]), odeg)
+    assert same_bits(host(norm["edge_weight"]), ow)
+    return g, norm, oei, ow
+
+
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_uniform_graphs(tfg, orc, name):
+    c = graphgen.CONFIGS[name]()
+    ei, x, n = c["edge_index"], c["x"], c["N"]
+    g, norm, oei, ow = gcn_layer_setup(tfg, orc, ei, n)
+    xd = dev(x)
+    kw = dict(edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    y = tfg.tfg_aggregate(norm["edge_index"], xd, n, "sum", **kw)
+    ref, S = orc.aggregate(oei, x, n, "sum", edge_weight=ow)
+    assert_scaled(host(y), ref, S, what=f"{name} sum")
+    if name == "c2":
+        ym = tfg.tfg_aggregate(norm["edge_index"], xd, n, "mean", **kw)
+        ref, S = orc.aggregate(oei, x, n, "mean", edge_weight=ow)
+        assert_scaled(host(ym), ref, S, what="c2 mean")
+        mx, arg = tfg.tfg_aggregate(norm["edge_index"], xd, n, "max", **kw)
+        rmx, rarg = orc.aggregate(oei, x, n, "max", edge_weight=ow)
+        assert same_bits(host(mx), rmx) and np.array_equal(host(arg), rarg)
+
+
+def test_gat_attention(tfg, orc):
+    c = graphgen.config3()
+    ei, h, n, H = c["edge_index"], c["h"], c["N"], c["H"]
+    eid = dev(ei.astype(np.int32))
+    g = tfg.tfg_graph_create(eid, n)  # no self-loops on this workload
+    s = tfg.tfg_gat_edge_scores(eid, dev(h), dev(c["a_src"]), dev(c["a_dst"]), c["slope"])
+    ref, S = orc.gat_scores(ei, h, c["a_src"], c["a_dst"], H, slope=np.float32(c["slope"]))
+    assert_scaled(host(s), ref, S, what="c3 scores")
+    alpha, alpha_csr = tfg.tfg_segment_softmax(s, eid[1], n, graph=g, out_csr=True)
+    s_h = host(s)
+    a64, _ = orc.segment_softmax(s_h, ei[1], n)
+    assert_rel(host(alpha), a64, what="c3 softmax")
+    y = tfg.tfg_aggregate(eid, dev(h), n, "sum", edge_weight=alpha_csr, heads=H,
+                          weight_order="csr", graph=g)
+    ref, S = orc.aggregate(ei, h, n, "sum", edge_weight=host(alpha), heads=H)
+    assert_scaled(host(y), ref, S, what="c3 per-head aggregation")
+    empty = np.bincount(ei[1], minlength=n) == 0
+    assert empty.mean() > 0.2 and np.all(host(y)[empty] == 0)
+
+
+def test_batched_pooling(tfg, orc):
+    c = graphgen.config5()
+    ei, x, n, G = c["edge_index"], c["x"], c["N"], c["G"]
+    g, norm, oei, ow = gcn_layer_setup(tfg, orc, ei, n)
+    kw = dict(edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    hd = dev(x)
+    scale = np.abs(x).astype(np.float32)
+    for layer in range(c["layers"]):
+        h_in = host(hd)
+        hd = tfg.tfg_aggregate(norm["edge_index"], hd, n, "sum", **kw)
+        ref, S = orc.aggregate(oei, h_in, n, "sum", edge_weight=ow)
+        assert_scaled(host(hd), ref, S, what=f"c5 layer {layer}")
+        scale = orc.aggregate(oei, scale, n, "sum", edge_weight=np.abs(ow))[0].astype(np.float32)
+    # the independent chain, against |A_hat|^3 |x|
+    ind = x
+    for _ in range(c["layers"]):
+        ind = orc.aggregate(oei, ind, n, "sum", edge_weight=ow)[0].astype(np.float32)
+    assert_scaled(host(hd), ind.astype(np.float64), scale.astype(np.float64) + 1e-30,
+                  tol=4e-5, what="c5 chained")
+    gi = dev(c["graph_index"].astype(np.int32))
+    h3 = host(hd)
+    for red in ("sum", "mean"):
+        p = tfg.tfg_segment_pool(hd, gi, G, red)
+        ref, S = orc.segment_pool(h3, c["graph_index"], G, red)
+        assert_scaled(host(p), ref, S, what=f"c5 pool {red}")
+    p, arg = tfg.tfg_segment_pool(hd, gi, G, "max")
+    ref, rarg = orc.segment_pool(h3, c["graph_index"], G, "max")
+    assert same_bits(host(p), ref) and np.array_equal(host(arg), rarg)
+
+
+@pytest.mark.timeout(900)
+def test_power_law_full_size(tfg, orc):
+    import torch
+    c = graphgen.config4(dtype=np.int32)
+    ei, x, n = c["edge_index"], c["x"], c["N"]
+    E = ei.shape[1]
+    eid = dev(ei)
+    g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+    info = g.info()
+    assert info["E"] == E + n and info["n_rows_split"] > 0
+    norm = tfg.tfg_gcn_norm(eid, n, graph=g)
+
+    # CSR: sorted by target, a permutation, input order inside each row -> unique
+    rowptr, col, perm = tfg.tfg_graph_csr(g)
+    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)])
+    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)])
+    cnt = torch.bincount(tgt_full.long(), minlength=n)
+    assert torch.equal(rowptr[1:].long() - rowptr[:-1].long(), cnt) and rowptr[0].item() == 0
+    pl = perm.long()
+    assert torch.equal(torch.bincount(pl, minlength=E + n), torch.ones(E + n, dtype=torch.long,
+                                                                     device=pl.device))
+    t_sorted = tgt_full[pl]
+    assert bool((t_sorted[1:] >= t_sorted[:-1]).all())
+    same_row = t_sorted[1:] == t_sorted[:-1]
+    assert bool((pl[1:][same_row] > pl[:-1][same_row]).all())
+    assert torch.equal(col, src_full[pl])
+    del tgt_full, src_full, pl, t_sorted, same_row
+
+    # degrees and weights: bit-exact against the oracle on the whole graph
+    oei, ow, odeg = orc.gcn_norm(ei, n)
+    assert same_bits(host(norm["deg"]), odeg)
+    assert same_bits(host(norm["edge_weight"]), ow)
+    assert same_bits(host(norm["edge_weight_csr"]), ow[host(perm)])
+
+    # aggregation: sampled rows (heaviest rows, split rows, random rows) one by one
+    y = tfg.tfg_aggregate(norm["edge_index"], dev(x), n, "sum",
+                          edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    deg = host(cnt)
+    rows = np.unique(np.concatenate([np.argsort(deg)[-40:], np.argsort(deg)[:20],
+                                     np.random.default_rng(0).choice(n, 1500, replace=False)]))
+    ref, S = orc.aggregate(oei, x, n, "sum", edge_weight=ow, rows=rows)
+    assert_scaled(host(y)[rows], ref, S, what="c4 sampled rows")
+
+    # invariant at full size: A_hat sqrt(deg) = sqrt(deg)
+    s = torch.sqrt(norm["deg"]).reshape(n, 1).repeat(1, 4).contiguous()
+    ys = tfg.tfg_aggregate(norm["edge_index"], s, n, "sum", edge_weight=norm["edge_weight_csr"],
+                           weight_order="csr", graph=g)
+    rel = (ys - s).abs() / s
+    assert float(rel.max()) <= 1e-5
+    # determinism
+    y2 = tfg.tfg_aggregate(norm["edge_index"], dev(x), n, "sum",
+                           edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    assert torch.equal(y, y2)

@@ -1,0 +1,289 @@
+"""GPU parity: every C-ABI call against the oracle on the same seeded inputs.
+
+Bars: bit-exact for the CSR permutation, degrees, normalised weights and max /
+argmax; for sums and means an error scaled by the size of the terms,
+|y - ref| / sum|terms| <= 1e-5 (the float32 summation bound; plain relative
+error is meaningless where a sum of N(0,1) terms cancels); for softmax a plain
+relative error <= 1e-5 (all terms positive).
+"""
+
+import numpy as np
+import pytest
+
+import graphgen
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+FLT_MIN = np.finfo(np.float32).tiny
+
+
+@pytest.fixture(scope="module")
+def tfg():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm device")
+    import paper_2101_11552_amd as lib
+    lib.load()
+    return lib
+
+
+def dev(a, dtype=None):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to("cuda:0")
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def assert_scaled(y, ref, S, tol=TOL, what=""):
+    y = np.asarray(y, np.float64)
+    zero = S == 0
+    assert np.all(y[zero] == 0), f"{what}: nonzero output where every term is zero"
+    err = np.abs(y[~zero] - ref[~zero]) / S[~zero]
+    worst = float(err.max()) if err.size else 0.0
+    assert worst <= tol, f"{what}: scaled error {worst:.3e} > {tol}"
+    return worst
+
+
+def assert_rel(y, ref, tol=TOL, what=""):
+    y = np.asarray(y, np.float64)
+    err = np.abs(y - ref) / np.maximum(np.abs(ref), FLT_MIN)
+    worst = float(err.max()) if err.size else 0.0
+    assert worst <= tol, f"{what}: relative error {worst:.3e} > {tol}"
+
+
+def same_bits(a, b):
+    a, b = np.asarray(a), np.asarray(b)
+    return a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# COO -> CSR
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,e,loops,idx", [
+    (1, 7, False, np.int64),            # N = 1: a single row
+    (300, 50_000, False, np.int32),     # one radix pass (9 bits), 13 tiles + ragged tail
+    (5_000, 70_001, True, np.int64),    # two passes, loops appended
+    (300_000, 40_000, False, np.int32),  # three passes (19 bits), mostly empty rows
+    (1000, 0, True, np.int32),          # no input edges: loops only
+])
+def test_csr_bit_exact(tfg, n, e, loops, idx):
+    ei = graphgen.random_graph(e + n, n, e, hub=n // 2, hub_edges=e // 4)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=loops)
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    full = ei
+    if loops:
+        full = np.concatenate([ei, np.stack([np.arange(n), np.arange(n)])], axis=1)
+    r, c, p = __import__("oracle").csr_by_target(full, n)
+    assert np.array_equal(rowptr, r) and np.array_equal(perm, p) and np.array_equal(col, c)
+
+
+def test_csr_rejects_out_of_range(tfg):
+    ei = np.array([[0, 1, 2], [1, 2, 9]])
+    with pytest.raises(IndexError):
+        tfg.tfg_graph_create(dev(ei), 5)
+    ei = np.array([[0, -1], [1, 2]])
+    with pytest.raises(IndexError):
+        tfg.tfg_graph_create(dev(ei.astype(np.int32)), 5)
+
+
+# ---------------------------------------------------------------------------
+# GCN normalisation
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("weighted,idx", [(False, np.int32), (True, np.int64)])
+def test_gcn_norm_bit_exact(tfg, orc, weighted, idx):
+    n, e = 4000, 60_000
+    ei = graphgen.random_graph(21, n, e, hub=3, hub_edges=5000)  # duplicates, loops, a hub
+    w = (np.random.default_rng(3).uniform(0.1, 3.0, ei.shape[1]).astype(np.float32)
+         if weighted else None)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=True)
+    r = tfg.tfg_gcn_norm(dev(ei.astype(idx)), n, edge_weight=None if w is None else dev(w), graph=g)
+    oei, ow, odeg = orc.gcn_norm(ei, n, edge_weight=w)
+    assert np.array_equal(host(r["edge_index"]), oei)
+    assert same_bits(host(r["deg"]), odeg)
+    assert same_bits(host(r["edge_weight"]), ow)
+    _, _, perm = orc.csr_by_target(oei, n)
+    assert same_bits(host(r["edge_weight_csr"]), ow[perm])
+    # functional path without a handle gives the same bits
+    r2 = tfg.tfg_gcn_norm(dev(ei.astype(idx)), n, edge_weight=None if w is None else dev(w))
+    assert same_bits(host(r2["edge_weight"]), ow)
+
+
+# ---------------------------------------------------------------------------
+# Aggregation
+# ---------------------------------------------------------------------------
+
+AGG_CASES = [
+    # n_src, n, e, F, ldx, heads
+    (600, 600, 20_000, 64, 64, 1),
+    (600, 700, 20_000, 128, 128, 1),
+    (500, 500, 9_000, 1, 1, 1),
+    (500, 500, 9_000, 3, 3, 1),
+    (400, 400, 9_000, 130, 133, 1),   # F not a multiple of 4, ldx > F
+    (800, 800, 30_000, 128, 136, 8),  # one weight per head
+    (300, 900, 6_000, 16, 16, 2),     # rectangular, many empty targets
+]
+
+
+@pytest.mark.parametrize("n_src,n,e,F,ldx,H", AGG_CASES)
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_aggregate(tfg, orc, n_src, n, e, F, ldx, H, reduce):
+    ei = graphgen.random_graph(e + F, n, e, n_src=n_src, hub=1, hub_edges=3 * 1200)  # split row
+    E = ei.shape[1]
+    big = graphgen.features(F, n_src, ldx)
+    x = big[:, :F]
+    w = np.random.default_rng(e).standard_normal((E, H) if H > 1 else E).astype(np.float32)
+    xd = dev(big)[:, :F]
+    g = tfg.tfg_graph_create(dev(ei), n, N_src=n_src)
+    assert g.info()["n_rows_split"] >= 1
+    res = tfg.tfg_aggregate(dev(ei), xd, n, reduce=reduce, edge_weight=dev(w), heads=H, graph=g)
+    if reduce == "max":
+        out, arg = (host(t) for t in res)
+        ref, refarg = orc.aggregate(ei, x, n, "max", edge_weight=w, heads=H)
+        assert same_bits(out, ref) and np.array_equal(arg, refarg)
+    else:
+        ref, S = orc.aggregate(ei, x, n, reduce, edge_weight=w, heads=H)
+        assert_scaled(host(res), ref, S, what=f"{reduce} F={F}")
+
+
+@pytest.mark.parametrize("reduce", ["sum", "max"])
+def test_aggregate_functional_and_csr_weights(tfg, orc, reduce):
+    n, e, F = 2000, 40_000, 64
+    ei = graphgen.random_graph(9, n, e, hub=11, hub_edges=4000)
+    x = graphgen.features(9, n, F)
+    w = np.random.default_rng(9).standard_normal(e + 4000).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n)
+    _, _, perm = orc.csr_by_target(ei, n)
+    a = tfg.tfg_aggregate(dev(ei), dev(x), n, reduce, edge_weight=dev(w))           # no handle
+    b = tfg.tfg_aggregate(dev(ei), dev(x), n, reduce, edge_weight=dev(w[perm]),
+                          weight_order="csr", graph=g)
+    c = tfg.tfg_aggregate(dev(ei), dev(x), n, reduce, edge_weight=dev(w), graph=g)  # COO + handle
+    if reduce == "max":
+        assert all(same_bits(host(a[0]), host(t[0])) for t in (b, c))
+        assert all(np.array_equal(host(a[1]), host(t[1])) for t in (b, c))
+    else:
+        assert same_bits(host(a), host(b)) and same_bits(host(a), host(c))
+
+
+def test_aggregate_unweighted_ones_is_degree(tfg):
+    n, e = 3000, 100_000
+    ei = graphgen.random_graph(4, n, e, hub=0, hub_edges=20_000)
+    y = host(tfg.tfg_aggregate(dev(ei), dev(np.ones((n, 4), np.float32)), n, "sum"))
+    cnt = np.bincount(ei[1], minlength=n).astype(np.float32)
+    assert np.array_equal(y, np.repeat(cnt[:, None], 4, axis=1))  # exact: integers < 2^24
+    m = host(tfg.tfg_aggregate(dev(ei), dev(np.ones((n, 4), np.float32)), n, "mean"))
+    assert np.array_equal(m[:, 0], (cnt > 0).astype(np.float32))
+
+
+def test_aggregate_edge_cases(tfg, orc):
+    x = graphgen.features(2, 5, 8)
+    empty = np.zeros((2, 0), np.int64)
+    y = host(tfg.tfg_aggregate(dev(empty), dev(x), 5, "sum"))
+    assert np.all(y == 0)
+    m, a = tfg.tfg_aggregate(dev(empty), dev(x), 5, "max")
+    assert np.all(host(m) == 0) and np.all(host(a) == -1)
+    one = np.array([[3], [0]])  # a single edge
+    y = host(tfg.tfg_aggregate(dev(one), dev(x), 5, "sum"))
+    assert np.array_equal(y[0], x[3]) and np.all(y[1:] == 0)
+    # ties and signed zeros: the first edge in input order wins
+    ei = np.array([[0, 1, 2, 0], [4, 4, 4, 4]])
+    xt = np.array([[-0.0], [0.0], [0.0], [-0.0], [0.0]], np.float32)
+    m, a = tfg.tfg_aggregate(dev(ei), dev(xt), 5, "max")
+    assert host(a)[4, 0] == 0 and np.signbit(host(m)[4, 0])
+
+
+def test_aggregate_deterministic(tfg):
+    n, e = 5000, 200_000
+    ei = graphgen.random_graph(31, n, e, hub=5, hub_edges=30_000)
+    x = dev(graphgen.features(31, n, 128))
+    w = dev(np.random.default_rng(31).standard_normal(e + 30_000).astype(np.float32))
+    g = tfg.tfg_graph_create(dev(ei), n)
+    y1 = host(tfg.tfg_aggregate(dev(ei), x, n, "sum", edge_weight=w, graph=g))
+    y2 = host(tfg.tfg_aggregate(dev(ei), x, n, "sum", edge_weight=w, graph=g))
+    g2 = tfg.tfg_graph_create(dev(ei), n)
+    y3 = host(tfg.tfg_aggregate(dev(ei), x, n, "sum", edge_weight=w, graph=g2))
+    assert same_bits(y1, y2) and same_bits(y1, y3)
+
+
+# ---------------------------------------------------------------------------
+# Attention: scores and softmax
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("H,D", [(8, 16), (1, 5), (3, 4)])
+def test_gat_scores(tfg, orc, H, D):
+    n, e = 3000, 50_000
+    ei = graphgen.random_graph(H * D, n, e)
+    h = graphgen.features(H, n, H * D)
+    r = np.random.default_rng(D)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    s = host(tfg.tfg_gat_edge_scores(dev(ei.astype(np.int32)), dev(h), dev(a_s), dev(a_d), 0.2))
+    ref, S = orc.gat_scores(ei, h, a_s, a_d, H, slope=np.float32(0.2))
+    assert_scaled(s, ref, S, what="gat scores")
+
+
+@pytest.mark.parametrize("H", [1, 8, 3])
+def test_segment_softmax(tfg, orc, H):
+    n, e = 5000, 80_000
+    ei = graphgen.random_graph(H, n, e, hub=2, hub_edges=6000)
+    E = ei.shape[1]
+    s = (graphgen.features(77, E, H) * 6).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n)
+    out, out_csr = tfg.tfg_segment_softmax(dev(s), dev(ei[1]), n, graph=g, out_csr=True)
+    ref64, _ = orc.segment_softmax(s, ei[1], n)
+    assert_rel(host(out), ref64, what="softmax")
+    _, _, perm = orc.csr_by_target(ei, n)
+    assert same_bits(host(out_csr), host(out)[perm])
+    plain = tfg.tfg_segment_softmax(dev(s), dev(ei[1]), n)  # no handle
+    assert same_bits(host(plain), host(out))
+    tot = np.zeros((n, H))
+    np.add.at(tot, ei[1], host(out).astype(np.float64))
+    has = np.bincount(ei[1], minlength=n) > 0
+    assert np.all(np.abs(tot[has] - 1) <= 1e-5)
+
+
+def test_segment_softmax_closed_forms(tfg):
+    seg = np.array([0, 1, 1, 1, 3])
+    s = np.array([5.0, 2.0, 2.0, 2.0, -7.0], np.float32)
+    out = host(tfg.tfg_segment_softmax(dev(s), dev(seg), 4))
+    assert out[0] == 1.0 and out[4] == 1.0 and np.all(out[1:4] == np.float32(1 / 3))
+
+
+# ---------------------------------------------------------------------------
+# Pooling
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("F,ldx", [(64, 64), (7, 9), (130, 130)])
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_segment_pool(tfg, orc, F, ldx, reduce):
+    sizes = np.random.default_rng(F).integers(0, 40, 700)
+    sizes[5] = 3000  # one large graph
+    gi = np.repeat(np.arange(700), sizes)
+    big = graphgen.features(ldx, gi.shape[0], ldx)
+    res = tfg.tfg_segment_pool(dev(big)[:, :F], dev(gi.astype(np.int32)), 703, reduce)
+    if reduce == "max":
+        ref, refarg = orc.segment_pool(big[:, :F], gi, 703, "max")
+        assert same_bits(host(res[0]), ref) and np.array_equal(host(res[1]), refarg)
+    else:
+        ref, S = orc.segment_pool(big[:, :F], gi, 703, reduce)
+        assert_scaled(host(res), ref, S, what=f"pool {reduce}")
+
+
+def test_segment_pool_errors(tfg):
+    x = dev(np.ones((3, 4), np.float32))
+    with pytest.raises(ValueError):
+        tfg.tfg_segment_pool(x, dev(np.array([0, 2, 1])), 3, "sum")
+    with pytest.raises(IndexError):
+        tfg.tfg_segment_pool(x, dev(np.array([0, 1, 3])), 3, "sum")
+    out = host(tfg.tfg_segment_pool(x, dev(np.array([1, 1, 1])), 4, "mean"))
+    assert np.all(out[0] == 0) and np.all(out[1] == 1) and np.all(out[2:] == 0)
+    empty = host(tfg.tfg_segment_pool(dev(np.zeros((0, 4), np.float32)),
+                                      dev(np.zeros(0, np.int64)), 2, "sum"))
+    assert np.all(empty == 0)
