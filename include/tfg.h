@@ -69,8 +69,8 @@ typedef enum {
 
 typedef enum { TFG_SUM = 0, TFG_MEAN = 1, TFG_MAX = 2 } tfg_reduce;
 typedef enum { TFG_I32 = 0, TFG_I64 = 1 } tfg_index_type;
-/* Order of a per-edge array: the caller's COO edge order, or the graph's CSR
- * order (edges grouped by target, input order kept inside a target). */
+/* Order of a per-edge array: the caller's COO edge order, or the graph order
+ * of a graph handle (edges grouped by target; see tfg_graph_create). */
 typedef enum { TFG_COO = 0, TFG_CSR = 1 } tfg_edge_order;
 
 typedef void *tfg_stream_t; /* hipStream_t */
@@ -94,37 +94,52 @@ int tfg_abi_version(void);
  * built once per graph structure and reused, in the spirit of the paper's
  * graph-level cache (Sec. 3).
  *
+ * Graph order. The handle orders the E' edges (the E input edges, then the N
+ * appended self-loops when add_self_loops != 0; loop i has edge id E + i) by
+ * the key (target, source part), keeping the input order among equal keys,
+ * where source part = source / ceil(N_src / P) for P source parts. This is
+ * the unique stable order for that key. With P = 1 it is the CSR by target
+ * with the input order inside each target; with P > 1 the edges of each
+ * target are further grouped by source range, which lets the aggregation
+ * visit the whole graph one source range at a time so that the gathered
+ * feature rows stay in the L2 caches. Every per-edge array passed in
+ * TFG_CSR order follows this order.
+ *
+ * src_parts: P, or 0 to let the library choose (P > 1 only when the source
+ *   table is large and rows are long: N_src * 512 bytes >= 32 MiB and
+ *   E' / N >= 16 * P; at most 16 parts).
+ *
  * tfg_graph_bytes: sizes of the persistent buffer (`buf`, kept until
- *   destroy) and of the scratch buffer (`scratch`, needed only during create)
- *   for a graph of E input edges over N target nodes, with N self-loops
- *   appended when add_self_loops != 0 (E' = E + N edges in total).
+ *   destroy) and of the scratch buffer (`scratch`, needed only during create).
  *
  * tfg_graph_create: validates every id (source in [0, N_src), target in
- *   [0, N)), builds rowptr [N+1], col [E'] (source id per CSR position) and
- *   perm [E'] (input edge id per CSR position; ids E..E'-1 are the appended
- *   loops, loop i having id E + i), and plans the aggregation launches.
- *   The permutation is the unique stable one: edges sorted by target, input
- *   order kept among equal targets. Synchronises `stream` once; returns
+ *   [0, N)), builds rowptr [N+1], col [E'] (source id per position) and perm
+ *   [E'] (input edge id per position) in graph order, and plans the
+ *   aggregation launches. Synchronises `stream` once; returns
  *   TFG_ERR_INDEX_RANGE (and no handle) if an id is out of range. `buf` must
  *   stay valid and unmodified until tfg_graph_destroy; `scratch` may be reused
  *   as soon as the call returns.
  *
  * tfg_graph_csr: copies rowptr / col / perm (any may be NULL) into caller
  *   buffers of N+1 / E' / E' int32, enqueued on `stream`.
+ * tfg_graph_segments: copies the N*P + 1 segment starts (segment t*P + p =
+ *   the edges of target t in source part p) into `segptr`.
  * tfg_graph_info: host-side sizes of the handle (any pointer may be NULL).
  * tfg_check: synchronises `stream` and returns TFG_ERR_INDEX_RANGE if any
  *   device-side check on this graph failed, else TFG_OK.
  * tfg_graph_destroy: frees the host struct (not `buf`).
  */
-int tfg_graph_bytes(int64_t E, int64_t N, int add_self_loops, size_t *buf_bytes,
-                    size_t *scratch_bytes);
+int tfg_graph_bytes(int64_t E, int64_t N_src, int64_t N, int add_self_loops, int src_parts,
+                    size_t *buf_bytes, size_t *scratch_bytes);
 int tfg_graph_create(const void *edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
-                     int add_self_loops, void *buf, size_t buf_bytes, void *scratch,
-                     size_t scratch_bytes, tfg_stream_t stream, tfg_graph **out);
+                     int add_self_loops, int src_parts, void *buf, size_t buf_bytes,
+                     void *scratch, size_t scratch_bytes, tfg_stream_t stream, tfg_graph **out);
 int tfg_graph_csr(const tfg_graph *g, int32_t *rowptr, int32_t *col, int32_t *perm,
                   tfg_stream_t stream);
+int tfg_graph_segments(const tfg_graph *g, int32_t *segptr, tfg_stream_t stream);
 int tfg_graph_info(const tfg_graph *g, int64_t *E_total, int64_t *N, int64_t *N_src,
-                   int64_t *n_chunks, int64_t *n_rows_split);
+                   int64_t *src_parts, int64_t *n_chunks, int64_t *n_rows_split,
+                   int64_t *n_part_items);
 int tfg_check(const tfg_graph *g, tfg_stream_t stream);
 int tfg_graph_destroy(tfg_graph *g);
 
@@ -144,7 +159,7 @@ int tfg_graph_destroy(tfg_graph *g);
  * Outputs (each may be NULL):
  *   out_edge_index      [2, E'] int32, COO: the input edges, then the loops;
  *   out_edge_weight     [E'] w_hat in that COO order;
- *   out_edge_weight_csr [E'] w_hat in the CSR order of `g` (needs g);
+ *   out_edge_weight_csr [E'] w_hat in the graph order of `g` (needs g);
  *   out_deg             [N].
  * g: NULL, or a graph created from the same edge_index with the same N and
  *   add_self_loops. With g == NULL a transient graph is built inside `ws`
@@ -172,16 +187,21 @@ int tfg_gcn_norm(const void *edge_index, int index_type, int64_t E, const float 
  * A target without edges gets 0 (and argmax -1).
  *
  * edge_index: [2, E] (E = all edges, including loops a previous
- *   tfg_gcn_norm appended). edge_weight: NULL, [E] (H = 1) or [E, H], in
- *   `weight_order` (TFG_CSR requires g). x: [N_src, F] with leading dimension
- *   ldx. out: [N, F]. argmax: [N, F] int32, TFG_MAX only (may be NULL).
+ *   tfg_gcn_norm appended); may be NULL when g is given. edge_weight: NULL,
+ *   [E] (H = 1) or [E, H], in `weight_order` (TFG_CSR: the graph order of g,
+ *   requires g). x: [N_src, F] with leading dimension ldx. out: [N, F].
+ *   argmax: [N, F] int32, TFG_MAX only (may be NULL).
  * Sums are float32 in a fixed order: each lane keeps short partial chains
  *   that are combined pairwise, so the error stays within a few hundred units
  *   of float32 rounding of the sum of |m_e[c]|, however long the row.
- * g: NULL, or a graph of this edge_index (E' equal to E, same N and N_src);
- *   NULL builds a transient graph in `ws` (then the call synchronises).
+ * g: NULL, or a graph of this edge_index (its E' equal to E, same N and
+ *   N_src); NULL builds a transient graph in `ws` (the call then synchronises).
+ *   With P > 1 source parts and a large x the call visits the graph one
+ *   source part at a time, writing partial rows to `ws` and combining them
+ *   in part order.
  */
-size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N, int64_t F, int reduce, const tfg_graph *g);
+size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N_src, int64_t N, int64_t F, int reduce,
+                              const tfg_graph *g);
 int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float *edge_weight,
                   int64_t H, int weight_order, const float *x, int64_t N_src, int64_t F,
                   int64_t ldx, int64_t N, int reduce, const tfg_graph *g, float *out,
@@ -209,7 +229,7 @@ int tfg_gat_edge_scores(const void *edge_index, int index_type, int64_t E, const
  *   out[e, h] = exp(s[e, h] - m) / sum over the segment of exp(s - m)
  * with m the segment's maximum (a shift that leaves the result unchanged).
  * scores: [E, H]; seg: [E] target ids in [0, N) (normally edge_index + E);
- * out: [E, H] in the caller's edge order; out_csr: NULL or [E, H] in the CSR
+ * out: [E, H] in the caller's edge order; out_csr: NULL or [E, H] in the graph
  * order of g (feeds tfg_aggregate with TFG_CSR weights). g: NULL or a graph
  * whose targets are seg (built from the edge list seg belongs to).
  */

@@ -42,6 +42,8 @@ def lib():
         _lib.orc_check_edges.argtypes = [i64, p, p, i64, i64]
         _lib.orc_csr_by_target.argtypes = [i64, i64, p, p, p, p, p]
         _lib.orc_csr_by_target.restype = None
+        _lib.orc_csr_by_key.argtypes = [i64, i64, i64, i64, p, p, p, p, p]
+        _lib.orc_csr_by_key.restype = None
         _lib.orc_gcn_norm.argtypes = [i64, i64, p, p, p, ctypes.c_int, p, p, p, p]
         _lib.orc_gcn_norm.restype = i64
         _lib.orc_aggregate.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, ctypes.c_int,
@@ -89,17 +91,25 @@ def check_edges(edge_index, n_src, n):
     return lib().orc_check_edges(ei.shape[1], _ptr(ei[0]), _ptr(ei[1]), n_src, n)
 
 
-def csr_by_target(edge_index, n):
-    """Stable counting sort by target: (rowptr [N+1], col [E], perm [E])."""
+def csr_by_target(edge_index, n, parts=1, n_src=None):
+    """Stable counting sort by (target, source part): (rowptr [N+1], col [E],
+    perm [E]); with ``parts`` > 1 also returns seg [N*parts+1] (the start of
+    every (target, part) key). Source part = source // ceil(n_src / parts)."""
     ei = _i64(edge_index)
     E = ei.shape[1]
-    _check(check_edges(ei, np.iinfo(np.int64).max, n))
-    rowptr = np.empty(n + 1, np.int64)
+    n_src = n if n_src is None else n_src
+    _check(check_edges(ei, n_src, n))
+    part_rows = max(-(-n_src // parts), 1)
+    seg = np.empty(n * parts + 1, np.int64)
     col = np.empty(E, np.int64)
     perm = np.empty(E, np.int64)
     src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
-    lib().orc_csr_by_target(E, n, _ptr(src), _ptr(tgt), _ptr(rowptr), _ptr(col), _ptr(perm))
-    return rowptr, col, perm
+    lib().orc_csr_by_key(E, n, parts, part_rows, _ptr(src), _ptr(tgt), _ptr(seg), _ptr(col),
+                         _ptr(perm))
+    rowptr = np.ascontiguousarray(seg[::parts])
+    if parts == 1:
+        return rowptr, col, perm
+    return rowptr, col, perm, seg
 
 
 def gcn_norm(edge_index, n, edge_weight=None, add_self_loops=True):

@@ -17,7 +17,8 @@ import os
 import torch
 
 __all__ = [
-    "TfgError", "Graph", "tfg_graph_create", "tfg_graph_csr", "tfg_check", "tfg_gcn_norm",
+    "TfgError", "Graph", "tfg_graph_create", "tfg_graph_csr", "tfg_graph_segments", "tfg_check",
+    "tfg_gcn_norm",
     "tfg_aggregate", "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_pool",
     "library_path", "load",
 ]
@@ -66,17 +67,17 @@ def load():
         "tfg_status_string": (ctypes.c_char_p, [ci]),
         "tfg_last_error": (ctypes.c_char_p, []),
         "tfg_abi_version": (ci, []),
-        "tfg_graph_bytes": (ci, [i64, i64, ci, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
-        "tfg_graph_create": (ci, [p, ci, i64, i64, i64, ci, p, sz, p, sz, p,
+        "tfg_graph_bytes": (ci, [i64, i64, i64, ci, ci, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
+        "tfg_graph_create": (ci, [p, ci, i64, i64, i64, ci, ci, p, sz, p, sz, p,
                                   ctypes.POINTER(p)]),
         "tfg_graph_csr": (ci, [p, p, p, p, p]),
-        "tfg_graph_info": (ci, [p, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64),
-                                ctypes.POINTER(i64), ctypes.POINTER(i64)]),
+        "tfg_graph_segments": (ci, [p, p, p]),
+        "tfg_graph_info": (ci, [p] + [ctypes.POINTER(i64)] * 7),
         "tfg_check": (ci, [p, p]),
         "tfg_graph_destroy": (ci, [p]),
         "tfg_gcn_norm_ws_bytes": (sz, [i64, i64, ci, p]),
         "tfg_gcn_norm": (ci, [p, ci, i64, p, i64, ci, p, p, p, p, p, p, sz, p]),
-        "tfg_aggregate_ws_bytes": (sz, [i64, i64, i64, ci, p]),
+        "tfg_aggregate_ws_bytes": (sz, [i64, i64, i64, i64, ci, p]),
         "tfg_aggregate": (ci, [p, ci, i64, p, i64, ci, p, i64, i64, i64, i64, ci, p, p, p, p,
                                sz, p]),
         "tfg_gat_edge_scores_ws_bytes": (sz, [i64, i64]),
@@ -177,9 +178,9 @@ class Graph:
         return self._h
 
     def info(self):
-        vals = [ctypes.c_int64() for _ in range(5)]
+        vals = [ctypes.c_int64() for _ in range(7)]
         _check(load().tfg_graph_info(self._h, *[ctypes.byref(v) for v in vals]))
-        keys = ("E", "N", "N_src", "n_chunks", "n_rows_split")
+        keys = ("E", "N", "N_src", "src_parts", "n_chunks", "n_rows_split", "n_part_items")
         return dict(zip(keys, (v.value for v in vals)))
 
     def __del__(self):
@@ -188,21 +189,27 @@ class Graph:
             _lib.tfg_graph_destroy(h)
 
 
-def tfg_graph_bytes(E: int, N: int, add_self_loops: bool = False):
+def tfg_graph_bytes(E: int, N: int, add_self_loops: bool = False, N_src: int | None = None,
+                    src_parts: int = 0):
     b, s = ctypes.c_size_t(), ctypes.c_size_t()
-    _check(load().tfg_graph_bytes(E, N, int(add_self_loops), ctypes.byref(b), ctypes.byref(s)))
+    N_src = N if N_src is None else N_src
+    _check(load().tfg_graph_bytes(E, N_src, N, int(add_self_loops), int(src_parts),
+                                  ctypes.byref(b), ctypes.byref(s)))
     return b.value, s.value
 
 
 def tfg_graph_create(edge_index: torch.Tensor, N: int, N_src: int | None = None,
-                     add_self_loops: bool = False, buf: torch.Tensor | None = None,
+                     add_self_loops: bool = False, src_parts: int = 0,
+                     buf: torch.Tensor | None = None,
                      scratch: torch.Tensor | None = None) -> Graph:
-    """COO -> CSR by target (synchronises once; raises IndexError on a bad id)."""
+    """COO -> CSR by (target, source part) (synchronises once; raises
+    IndexError on a bad id). src_parts: 0 = chosen by the library, 1 = the
+    plain stable CSR by target."""
     lib = load()
     ei = _edges(edge_index)
     E = ei.shape[1]
     N_src = N if N_src is None else N_src
-    nb, ns = tfg_graph_bytes(E, N, add_self_loops)
+    nb, ns = tfg_graph_bytes(E, N, add_self_loops, N_src, src_parts)
     dev = ei.device
     if buf is None or buf.numel() < nb:
         buf = _workspace(nb, dev)
@@ -210,8 +217,8 @@ def tfg_graph_create(edge_index: torch.Tensor, N: int, N_src: int | None = None,
         scratch = _workspace(ns, dev)
     h = ctypes.c_void_p()
     _check(lib.tfg_graph_create(_ptr(ei), _index_type(ei), E, N_src, N, int(add_self_loops),
-                                _ptr(buf), buf.numel(), _ptr(scratch), scratch.numel(),
-                                _stream(dev), ctypes.byref(h)))
+                                int(src_parts), _ptr(buf), buf.numel(), _ptr(scratch),
+                                scratch.numel(), _stream(dev), ctypes.byref(h)))
     return Graph(h, buf, E, E + (N if add_self_loops else 0), N, N_src, bool(add_self_loops), dev)
 
 
@@ -222,6 +229,14 @@ def tfg_graph_csr(g: Graph):
     perm = torch.empty(g.E, dtype=torch.int32, device=g.device)
     _check(load().tfg_graph_csr(g.handle, _ptr(rowptr), _ptr(col), _ptr(perm), _stream(g.device)))
     return rowptr, col, perm
+
+
+def tfg_graph_segments(g: Graph):
+    """Start of every (target, source part) segment: int32 [N * src_parts + 1]."""
+    parts = g.info()["src_parts"]
+    seg = torch.empty(g.N * parts + 1, dtype=torch.int32, device=g.device)
+    _check(load().tfg_graph_segments(g.handle, _ptr(seg), _stream(g.device)))
+    return seg
 
 
 def tfg_check(g: Graph):
@@ -267,21 +282,28 @@ def tfg_gcn_norm(edge_index: torch.Tensor, N: int, edge_weight: torch.Tensor | N
 
 
 def tfg_aggregate_ws_bytes(E: int, N: int, F: int, reduce: str = "sum",
-                           graph: Graph | None = None) -> int:
-    return load().tfg_aggregate_ws_bytes(E, N, F, _REDUCE[reduce],
+                           graph: Graph | None = None, N_src: int | None = None) -> int:
+    N_src = N if N_src is None else N_src
+    return load().tfg_aggregate_ws_bytes(E, N_src, N, F, _REDUCE[reduce],
                                          graph.handle if graph is not None else None)
 
 
-def tfg_aggregate(edge_index: torch.Tensor, x: torch.Tensor, N: int, reduce: str = "sum",
+def tfg_aggregate(edge_index: torch.Tensor | None, x: torch.Tensor, N: int, reduce: str = "sum",
                   edge_weight: torch.Tensor | None = None, heads: int = 1,
                   weight_order: str = "coo", graph: Graph | None = None,
                   out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
                   ws: torch.Tensor | None = None):
     """Message aggregation into N targets. Returns ``out`` [N, F] (and
-    ``argmax`` [N, F] int32 edge ids for ``reduce="max"``)."""
+    ``argmax`` [N, F] int32 edge ids for ``reduce="max"``). ``edge_index`` may
+    be None when ``graph`` is given."""
     lib = load()
-    ei = _edges(edge_index)
-    E = ei.shape[1]
+    if edge_index is None:
+        if graph is None:
+            raise ValueError("edge_index is needed without a graph")
+        ei, E = None, graph.E
+    else:
+        ei = _edges(edge_index)
+        E = ei.shape[1]
     x, ldx = _rows(x, "x")
     dev = x.device
     N_src, F = x.shape
@@ -292,10 +314,11 @@ def tfg_aggregate(edge_index: torch.Tensor, x: torch.Tensor, N: int, reduce: str
     if red == 2 and argmax is None:
         argmax = torch.empty((N, F), dtype=torch.int32, device=dev)
     h = graph.handle if graph is not None else None
-    need = lib.tfg_aggregate_ws_bytes(E, N, F, red, h)
+    need = lib.tfg_aggregate_ws_bytes(E, N_src, N, F, red, h)
     if ws is None or ws.numel() < need:
         ws = _workspace(need, dev)
-    _check(lib.tfg_aggregate(_ptr(ei), _index_type(ei), E, _ptr(w), heads, _ORDER[weight_order],
+    _check(lib.tfg_aggregate(_ptr(ei), _index_type(ei) if ei is not None else 0, E, _ptr(w), heads,
+                             _ORDER[weight_order],
                              _ptr(x), N_src, F, ldx, N, red, h, _ptr(out),
                              _ptr(argmax) if red == 2 else None, _ptr(ws), ws.numel(),
                              _stream(dev)))

@@ -11,6 +11,8 @@
 // stays small for long rows too; long rows are cut into chunks whose partial
 // results a fix-up pass combines in chunk order. No floating-point atomics:
 // every output is reproducible bit for bit.
+#include <cstdlib>
+
 #include "tfg_internal.h"
 
 namespace tfg {
@@ -78,12 +80,15 @@ __device__ __forceinline__ void max_combine(float& v, int& a, float vb, int ab) 
   a = take ? ab : a;
 }
 
-template <int SLOTS>
+// Independent row gathers in flight per edge slot: 8 for whole rows, 4 for
+// the short (row, source part) segments of the part plan.
+template <int SLOTS, bool SHORT>
 constexpr int unroll_for() {
-  return SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
+  constexpr int u = SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
+  return SHORT && u > 4 ? 4 : u;
 }
 
-template <int V, int SLOTS, bool MAX, bool HEADS>
+template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT>
 __global__ __launch_bounds__(kBlock) void spmm_rows(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
     int n_light, const int* __restrict__ col, const int* __restrict__ perm,
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
     float* __restrict__ part, int* __restrict__ part_arg) {
   constexpr int LPS = kWave / SLOTS;  // lanes per edge slot
   constexpr int FC = LPS * V;         // feature columns per pass
-  constexpr int U = unroll_for<SLOTS>();
+  constexpr int U = unroll_for<SLOTS, SHORT>();
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy + n_light) return;
   const int lane = threadIdx.x & (kWave - 1);
@@ -159,8 +164,10 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
 #pragma unroll
             for (int v = 0; v < V; ++v) {
               if constexpr (MAX) {
+                // edge ids need not increase along a row (rows may be grouped
+                // by source range), so ties compare the ids
                 const float m = wv[u] * xv[u][v];
-                if (arg[u][v] < 0 || m > acc[u][v]) {
+                if (arg[u][v] < 0 || m > acc[u][v] || (m == acc[u][v] && ev[u] < arg[u][v])) {
                   acc[u][v] = m;
                   arg[u][v] = ev[u];
                 }
@@ -228,7 +235,8 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
 
 // Combines the partial results of each split row in chunk order: sums with
 // four interleaved accumulators combined pairwise, maxima with the tie rule.
-template <bool MAX>
+// Lanes cover V consecutive features each.
+template <bool MAX, int V>
 __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict__ split,
                                                      int n_split, const float* __restrict__ part,
                                                      const int* __restrict__ part_arg, int F,
@@ -237,66 +245,112 @@ __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict_
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_split) return;
   const int lane = threadIdx.x & (kWave - 1);
-  const SplitRow sr = split[wid];
-  const int row = uniform(sr.row), slot0 = uniform(sr.slot0), nch = uniform(sr.nchunks);
-  const int deg = uniform(sr.deg);
-  for (int f = lane; f < F; f += kWave) {
+  const SplitRow* sr = split + wid;
+  const int row = uniform(sr->row), slot0 = uniform(sr->slot0), nch = uniform(sr->nchunks);
+  const int deg = uniform(sr->deg);
+  for (int f = lane * V; f < F; f += kWave * V) {
     if constexpr (MAX) {
-      float v = 0.0f;
-      int a = -1;
-      for (int j = 0; j < nch; ++j)
-        max_combine(v, a, part[(int64_t)(slot0 + j) * F + f], part_arg[(int64_t)(slot0 + j) * F + f]);
-      out[(int64_t)row * F + f] = a < 0 ? 0.0f : v;
-      if (argout != nullptr) argout[(int64_t)row * F + f] = a;
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        float best = 0.0f;
+        int a = -1;
+        for (int j = 0; j < nch; ++j)
+          max_combine(best, a, part[(int64_t)(slot0 + j) * F + f + v],
+                      part_arg[(int64_t)(slot0 + j) * F + f + v]);
+        out[(int64_t)row * F + f + v] = a < 0 ? 0.0f : best;
+        if (argout != nullptr) argout[(int64_t)row * F + f + v] = a;
+      }
     } else {
-      float a4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      for (int j = 0; j < nch; ++j) a4[j & 3] += part[(int64_t)(slot0 + j) * F + f];
-      float s = (a4[0] + a4[1]) + (a4[2] + a4[3]);
-      if (mean && deg > 0) s = s / (float)deg;
-      out[(int64_t)row * F + f] = s;
+      float a4[4][V];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < V; ++v) a4[i][v] = 0.0f;
+      int j = 0;
+      for (; j + 4 <= nch; j += 4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float t[V];
+          load_row<V>(part + (int64_t)(slot0 + j + i) * F + f, t);
+#pragma unroll
+          for (int v = 0; v < V; ++v) a4[i][v] += t[v];
+        }
+      }
+      for (int i = 0; j < nch; ++j, ++i) {
+        float t[V];
+        load_row<V>(part + (int64_t)(slot0 + j) * F + f, t);
+#pragma unroll
+        for (int v = 0; v < V; ++v) a4[i][v] += t[v];
+      }
+      float s[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        s[v] = (a4[0][v] + a4[1][v]) + (a4[2][v] + a4[3][v]);
+        if (mean && deg > 0) s[v] = s[v] / (float)deg;
+      }
+      store_row<V>(out + (int64_t)row * F + f, s);
     }
   }
 }
 
-template <int V, int SLOTS, bool MAX, bool HEADS>
-void launch_rows(dim3 grid, hipStream_t s, const Graph& g, const float* w, int w_by_perm, int H,
-                 int per_head, const float* x, int64_t ldx, int F, int mean, float* out,
-                 int* argout, float* part, int* part_arg) {
-  spmm_rows<V, SLOTS, MAX, HEADS><<<grid, dim3(kBlock), 0, s>>>(
-      g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, w, w_by_perm, H, per_head, x, ldx, F,
-      mean, out, argout, part, part_arg);
+// The kernel arguments shared by every instantiation.
+struct RowArgs {
+  const WorkItem* heavy;
+  int n_heavy;
+  const WorkItem* light;
+  int n_light;
+  const int* col;
+  const int* perm;
+  const float* w;
+  int w_by_perm, H, per_head;
+  const float* x;
+  int64_t ldx;
+  int F, mean;
+  float* out;
+  int* argout;
+  float* part;
+  int* part_arg;
+};
+
+template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT>
+void launch_rows(dim3 grid, hipStream_t s, const RowArgs& a) {
+  spmm_rows<V, SLOTS, MAX, HEADS, SHORT><<<grid, dim3(kBlock), 0, s>>>(
+      a.heavy, a.n_heavy, a.light, a.n_light, a.col, a.perm, a.w, a.w_by_perm, a.H, a.per_head,
+      a.x, a.ldx, a.F, a.mean, a.out, a.argout, a.part, a.part_arg);
 }
 
-template <int V, bool MAX, bool HEADS>
-void dispatch_slots(int slots, dim3 grid, hipStream_t s, const Graph& g, const float* w,
-                    int w_by_perm, int H, int per_head, const float* x, int64_t ldx, int F,
-                    int mean, float* out, int* argout, float* part, int* part_arg) {
-#define TFG_ROWS(SL)                                                                          \
-  launch_rows<V, SL, MAX, HEADS>(grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean, out, \
-                                 argout, part, part_arg)
+template <int V, bool MAX, bool HEADS, bool SHORT>
+void dispatch_slots(int slots, dim3 grid, hipStream_t s, const RowArgs& a) {
   switch (slots) {
-    case 1: TFG_ROWS(1); break;
-    case 2: TFG_ROWS(2); break;
-    case 4: TFG_ROWS(4); break;
-    case 8: TFG_ROWS(8); break;
-    default: TFG_ROWS(16); break;
+    case 1: launch_rows<V, 1, MAX, HEADS, SHORT>(grid, s, a); break;
+    case 2: launch_rows<V, 2, MAX, HEADS, SHORT>(grid, s, a); break;
+    case 4: launch_rows<V, 4, MAX, HEADS, SHORT>(grid, s, a); break;
+    case 8: launch_rows<V, 8, MAX, HEADS, SHORT>(grid, s, a); break;
+    default: launch_rows<V, 16, MAX, HEADS, SHORT>(grid, s, a); break;
   }
-#undef TFG_ROWS
 }
 
-template <bool MAX, bool HEADS>
-void dispatch_vec(int vec, int slots, dim3 grid, hipStream_t s, const Graph& g, const float* w,
-                  int w_by_perm, int H, int per_head, const float* x, int64_t ldx, int F, int mean,
-                  float* out, int* argout, float* part, int* part_arg) {
+template <bool MAX, bool HEADS, bool SHORT>
+void dispatch_vec(int vec, int slots, dim3 grid, hipStream_t s, const RowArgs& a) {
   if (vec == 4)
-    dispatch_slots<4, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
-                                  out, argout, part, part_arg);
+    dispatch_slots<4, MAX, HEADS, SHORT>(slots, grid, s, a);
   else if (vec == 2)
-    dispatch_slots<2, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
-                                  out, argout, part, part_arg);
+    dispatch_slots<2, MAX, HEADS, SHORT>(slots, grid, s, a);
   else
-    dispatch_slots<1, MAX, HEADS>(slots, grid, s, g, w, w_by_perm, H, per_head, x, ldx, F, mean,
-                                  out, argout, part, part_arg);
+    dispatch_slots<1, MAX, HEADS, SHORT>(slots, grid, s, a);
+}
+
+template <bool SHORT>
+void dispatch_kind(bool mx, bool heads, int vec, int slots, dim3 grid, hipStream_t s,
+                   const RowArgs& a) {
+  if (mx && heads)
+    dispatch_vec<true, true, SHORT>(vec, slots, grid, s, a);
+  else if (mx)
+    dispatch_vec<true, false, SHORT>(vec, slots, grid, s, a);
+  else if (heads)
+    dispatch_vec<false, true, SHORT>(vec, slots, grid, s, a);
+  else
+    dispatch_vec<false, false, SHORT>(vec, slots, grid, s, a);
 }
 
 }  // namespace
@@ -304,6 +358,15 @@ void dispatch_vec(int vec, int slots, dim3 grid, hipStream_t s, const Graph& g, 
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce) {
   size_t per = sizeof(float) + (reduce == TFG_MAX ? sizeof(int) : 0);
   return align_up((size_t)std::max<int64_t>(n_partials, 1) * (size_t)F * per + 256, 256);
+}
+
+bool use_part_plan(const Graph& g, int64_t F) {
+  if (g.parts <= 1 || g.n_pexec == 0) return false;
+  const char* v = std::getenv("TFG_PART_PLAN");  // "0": never, "1": always, unset: by size
+  if (v && v[0] == '0') return false;
+  if (v && v[0] == '1') return true;
+  // the gathered table must be much larger than the L2 caches (8 x 4 MB)
+  return (double)g.N_src * (double)F * 4.0 >= 32.0 * (1 << 20);
 }
 
 int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
@@ -317,42 +380,69 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
            (!heads || per_head % v == 0);
   };
   const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;
-  int lanes = (int)std::min<int64_t>((F + vec - 1) / vec, kWave);
+  const int lanes = (int)std::min<int64_t>((F + vec - 1) / vec, kWave);
   int p2 = 1;
   while (p2 < lanes) p2 <<= 1;
   const int slots = std::min(kWave / p2, 16);
-  const int w_by_perm = (w != nullptr && w_order == TFG_COO) ? 1 : 0;
-  const int mean = reduce == TFG_MEAN;
   const bool mx = reduce == TFG_MAX;
+  const bool part_plan = use_part_plan(g, F);
 
-  float* part = static_cast<float*>(ws);
-  int* part_arg = reinterpret_cast<int*>(part + (size_t)std::max(g.n_heavy, 1) * F);
-  const int waves = g.n_heavy + g.n_light;
-  dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
-  const int Fi = (int)F;
+  RowArgs a;
+  a.col = g.col;
+  a.perm = g.perm;
+  a.w = w;
+  a.w_by_perm = (w != nullptr && w_order == TFG_COO) ? 1 : 0;
+  a.H = H;
+  a.per_head = per_head;
+  a.x = x;
+  a.ldx = ldx;
+  a.F = (int)F;
+  a.mean = reduce == TFG_MEAN;
+  a.out = out;
+  a.argout = argmax;
+  const int n_partials = part_plan ? g.n_pexec : g.n_heavy;
+  a.part = static_cast<float*>(ws);
+  a.part_arg = reinterpret_cast<int*>(a.part + (size_t)std::max(n_partials, 1) * F);
+  const SplitRow* rows;
+  int n_rows;
+  if (part_plan) {
+    // every (part, row) item writes a partial; each row is reduced in part order
+    a.heavy = g.pexec;
+    a.n_heavy = g.n_pexec;
+    a.light = nullptr;
+    a.n_light = 0;
+    rows = g.prows;
+    n_rows = (int)g.N;
+  } else {
+    a.heavy = g.heavy;
+    a.n_heavy = g.n_heavy;
+    a.light = g.light;
+    a.n_light = g.n_light;
+    rows = g.split;
+    n_rows = g.n_split;
+  }
+  const int waves = a.n_heavy + a.n_light;
   if (waves > 0) {
-    if (mx && heads)
-      dispatch_vec<true, true>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
-                               mean, out, argmax, part, part_arg);
-    else if (mx)
-      dispatch_vec<true, false>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
-                                mean, out, argmax, part, part_arg);
-    else if (heads)
-      dispatch_vec<false, true>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx, Fi,
-                                mean, out, argmax, part, part_arg);
+    dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
+    if (part_plan)
+      dispatch_kind<true>(mx, heads, vec, slots, grid, s, a);
     else
-      dispatch_vec<false, false>(vec, slots, grid, s, g, w, w_by_perm, (int)H, per_head, x, ldx,
-                                 Fi, mean, out, argmax, part, part_arg);
+      dispatch_kind<false>(mx, heads, vec, slots, grid, s, a);
     TFG_LAUNCHED("spmm_rows");
   }
-  if (g.n_split > 0) {
-    dim3 fgrid((unsigned)((g.n_split + kBlock / kWave - 1) / (kBlock / kWave)));
+  if (n_rows > 0) {
+    dim3 fgrid((unsigned)((n_rows + kBlock / kWave - 1) / (kBlock / kWave)));
+    // partials are dense [slot, F] rows: 16-byte accesses when F is a multiple of 4
+    const bool f4 = F % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
     if (mx)
-      fixup_rows<true><<<fgrid, dim3(kBlock), 0, s>>>(g.split, g.n_split, part, part_arg, Fi, mean,
-                                                      out, argmax);
+      fixup_rows<true, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+                                                         a.mean, out, argmax);
+    else if (f4)
+      fixup_rows<false, 4><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+                                                          a.mean, out, argmax);
     else
-      fixup_rows<false><<<fgrid, dim3(kBlock), 0, s>>>(g.split, g.n_split, part, part_arg, Fi,
-                                                       mean, out, argmax);
+      fixup_rows<false, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+                                                          a.mean, out, argmax);
     TFG_LAUNCHED("fixup_rows");
   }
   return TFG_OK;

@@ -48,8 +48,8 @@ struct Carver {
   }
 };
 
-size_t graph_total_bytes(int64_t E, int64_t N) {
-  return graph_layout(E, N, default_chunk()).total + graph_scratch_bytes(E, N);
+size_t graph_total_bytes(int64_t E, int64_t N, int parts) {
+  return graph_layout(E, N, parts, default_chunk()).total + graph_scratch_bytes(E, N, parts);
 }
 
 int check_counts(int64_t E, int64_t N, int64_t N_src) {
@@ -61,8 +61,8 @@ int check_counts(int64_t E, int64_t N, int64_t N_src) {
 
 // Fills g's device pointers from `buf` and builds the CSR form.
 int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int64_t E_in,
-                 int64_t N_src, int64_t N, int loops, void* buf, size_t buf_bytes, void* scratch,
-                 size_t scratch_bytes, hipStream_t s) {
+                 int64_t N_src, int64_t N, int loops, int src_parts, void* buf, size_t buf_bytes,
+                 void* scratch, size_t scratch_bytes, hipStream_t s) {
   g.E_in = E_in;
   g.E = E_in + (loops ? N : 0);
   g.N = N;
@@ -71,16 +71,21 @@ int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int
   g.chunk = default_chunk();
   int rc = check_counts(g.E, N, N_src);
   if (rc) return rc;
-  GraphLayout L = graph_layout(g.E, N, g.chunk);
+  g.parts = choose_parts(g.E, N, N_src, src_parts);
+  g.part_rows = std::max<int64_t>((N_src + g.parts - 1) / g.parts, 1);
+  GraphLayout L = graph_layout(g.E, N, g.parts, g.chunk);
   if (buf == nullptr || buf_bytes < L.total)
     return fail(TFG_ERR_WORKSPACE, "graph buffer too small");
   char* b = static_cast<char*>(buf);
   g.rowptr = reinterpret_cast<int*>(b + L.rowptr);
+  g.segptr = g.parts > 1 ? reinterpret_cast<int*>(b + L.segptr) : g.rowptr;
   g.col = reinterpret_cast<int*>(b + L.col);
   g.perm = reinterpret_cast<int*>(b + L.perm);
   g.heavy = reinterpret_cast<WorkItem*>(b + L.heavy);
   g.light = reinterpret_cast<WorkItem*>(b + L.light);
   g.split = reinterpret_cast<SplitRow*>(b + L.split);
+  g.pexec = reinterpret_cast<WorkItem*>(b + L.pexec);
+  g.prows = reinterpret_cast<SplitRow*>(b + L.prows);
   g.counters = reinterpret_cast<int*>(b + L.counters);
   TFG_HIP(hipGetDevice(&g.device));
   return build_graph(g, src, tgt, index_type, scratch, scratch_bytes, s);
@@ -104,14 +109,33 @@ int graph_or_transient(const tfg_graph* handle, Graph& tmp, const Graph*& g, con
     return TFG_OK;
   }
   const int64_t Ep = E + (loops ? N : 0);
-  GraphLayout L = graph_layout(Ep, N, default_chunk());
-  size_t sc = graph_scratch_bytes(Ep, N);
+  const int parts = choose_parts(Ep, N, N_src, 0);
+  GraphLayout L = graph_layout(Ep, N, parts, default_chunk());
+  size_t sc = graph_scratch_bytes(Ep, N, parts);
   void* buf = ws.take(L.total);
   void* scratch = ws.take(sc);
   if (ws.off > ws.size) return fail(TFG_ERR_WORKSPACE, "workspace too small");
-  int rc = create_graph(tmp, src, tgt, index_type, E, N_src, N, loops, buf, L.total, scratch, sc, s);
+  int rc = create_graph(tmp, src, tgt, index_type, E, N_src, N, loops, 0, buf, L.total, scratch,
+                        sc, s);
   g = &tmp;
   return rc;
+}
+
+// Partial rows an aggregation needs: those of the plan it will use (for a
+// transient graph, the larger capacity of the two plans).
+int64_t partials_needed(int64_t E, int64_t N, int64_t N_src, int64_t F, const tfg_graph* g) {
+  if (g) return use_part_plan(g->g, F) ? g->g.n_pexec : g->g.n_heavy;
+  const int parts = choose_parts(E, N, N_src, 0);
+  const GraphLayout L = graph_layout(E, N, parts, default_chunk());
+  return std::max(L.cap_heavy, L.cap_pexec);
+}
+
+size_t aggregate_ws_needed(int64_t E, int64_t N, int64_t N_src, int64_t F, int reduce,
+                           const tfg_graph* g) {
+  if (E < 0 || N < 0 || N_src < 0 || F < 0) return 0;
+  size_t b = aggregate_partial_bytes(partials_needed(E, N, N_src, F, g), F, reduce);
+  if (!g) b += graph_total_bytes(E, N, choose_parts(E, N, N_src, 0));
+  return b;
 }
 
 }  // namespace
@@ -138,20 +162,21 @@ const char* tfg_last_error(void) { return g_last_error.c_str(); }
 
 int tfg_abi_version(void) { return TFG_ABI_VERSION; }
 
-int tfg_graph_bytes(int64_t E, int64_t N, int add_self_loops, size_t* buf_bytes,
-                    size_t* scratch_bytes) {
-  int rc = check_counts(E, N, 0);
+int tfg_graph_bytes(int64_t E, int64_t N_src, int64_t N, int add_self_loops, int src_parts,
+                    size_t* buf_bytes, size_t* scratch_bytes) {
+  int rc = check_counts(E, N, N_src);
   if (rc) return rc;
   const int64_t Ep = E + (add_self_loops ? N : 0);
-  rc = check_counts(Ep, N, 0);
+  rc = check_counts(Ep, N, N_src);
   if (rc) return rc;
-  if (buf_bytes) *buf_bytes = graph_layout(Ep, N, default_chunk()).total;
-  if (scratch_bytes) *scratch_bytes = graph_scratch_bytes(Ep, N);
+  const int parts = choose_parts(Ep, N, N_src, src_parts);
+  if (buf_bytes) *buf_bytes = graph_layout(Ep, N, parts, default_chunk()).total;
+  if (scratch_bytes) *scratch_bytes = graph_scratch_bytes(Ep, N, parts);
   return TFG_OK;
 }
 
 int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
-                     int add_self_loops, void* buf, size_t buf_bytes, void* scratch,
+                     int add_self_loops, int src_parts, void* buf, size_t buf_bytes, void* scratch,
                      size_t scratch_bytes, tfg_stream_t stream, tfg_graph** out) {
   if (out == nullptr) return fail(TFG_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
@@ -163,7 +188,7 @@ int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t 
   tfg_graph* h = new (std::nothrow) tfg_graph;
   if (!h) return fail(TFG_ERR_HIP, "host allocation failed");
   int rc = create_graph(h->g, edge_index, tgt_row(edge_index, index_type, E), index_type, E, N_src,
-                        N, add_self_loops, buf, buf_bytes, scratch, scratch_bytes,
+                        N, add_self_loops, src_parts, buf, buf_bytes, scratch, scratch_bytes,
                         as_stream(stream));
   if (rc) {
     delete h;
@@ -188,13 +213,24 @@ int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* pe
 }
 
 int tfg_graph_info(const tfg_graph* h, int64_t* E_total, int64_t* N, int64_t* N_src,
-                   int64_t* n_chunks, int64_t* n_rows_split) {
+                   int64_t* src_parts, int64_t* n_chunks, int64_t* n_rows_split,
+                   int64_t* n_part_items) {
   if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
   if (E_total) *E_total = h->g.E;
   if (N) *N = h->g.N;
   if (N_src) *N_src = h->g.N_src;
+  if (src_parts) *src_parts = h->g.parts;
   if (n_chunks) *n_chunks = h->g.n_heavy;
   if (n_rows_split) *n_rows_split = h->g.n_split;
+  if (n_part_items) *n_part_items = h->g.n_pexec;
+  return TFG_OK;
+}
+
+int tfg_graph_segments(const tfg_graph* h, int32_t* segptr, tfg_stream_t stream) {
+  if (!h || !segptr) return fail(TFG_ERR_INVALID_ARG, "NULL argument");
+  const Graph& g = h->g;
+  TFG_HIP(hipMemcpyAsync(segptr, g.segptr, sizeof(int) * (g.N * g.parts + 1),
+                         hipMemcpyDeviceToDevice, as_stream(stream)));
   return TFG_OK;
 }
 
@@ -216,7 +252,10 @@ int tfg_graph_destroy(tfg_graph* h) {
 size_t tfg_gcn_norm_ws_bytes(int64_t E, int64_t N, int add_self_loops, const tfg_graph* g) {
   if (E < 0 || N < 0) return 0;
   size_t b = align_up(sizeof(float) * (size_t)std::max<int64_t>(N, 1), 256);
-  if (!g) b += graph_total_bytes(E + (add_self_loops ? N : 0), N);
+  if (!g) {
+    const int64_t Ep = E + (add_self_loops ? N : 0);
+    b += graph_total_bytes(Ep, N, choose_parts(Ep, N, N, 0));
+  }
   return b;
 }
 
@@ -247,12 +286,9 @@ int tfg_gcn_norm(const void* edge_index, int index_type, int64_t E, const float*
   return TFG_OK;
 }
 
-size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N, int64_t F, int reduce, const tfg_graph* g) {
-  if (E < 0 || N < 0 || F < 0) return 0;
-  int64_t partials = g ? g->g.n_heavy : graph_layout(E, N, default_chunk()).cap_heavy;
-  size_t b = aggregate_partial_bytes(partials, F, reduce);
-  if (!g) b += graph_total_bytes(E, N);
-  return b;
+size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N_src, int64_t N, int64_t F, int reduce,
+                              const tfg_graph* g) {
+  return aggregate_ws_needed(E, N, N_src, F, reduce, g);
 }
 
 int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float* edge_weight,
@@ -270,20 +306,19 @@ int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float
     return fail(TFG_ERR_INVALID_ARG, "F must be >= 0 and a multiple of H >= 1");
   if (F >= kMaxCount || ldx < F) return fail(TFG_ERR_INVALID_ARG, "bad F / ldx");
   if (N_src * std::max<int64_t>(ldx, 1) >= (int64_t(1) << 62)) return fail(TFG_ERR_TOO_LARGE, "x too large");
-  if (E > 0 && edge_index == nullptr) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
+  if (E > 0 && edge_index == nullptr && !g) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
   if (N > 0 && F > 0 && out == nullptr) return fail(TFG_ERR_INVALID_ARG, "out is NULL");
   if (E > 0 && F > 0 && x == nullptr) return fail(TFG_ERR_INVALID_ARG, "x is NULL");
   if (weight_order == TFG_CSR && edge_weight && !g)
     return fail(TFG_ERR_INVALID_ARG, "CSR-order weights need a graph handle");
   if (H > 1 && !edge_weight) H = 1;
-  if (ws == nullptr || ws_bytes < tfg_aggregate_ws_bytes(E, N, F, reduce, g))
+  if (ws == nullptr || ws_bytes < aggregate_ws_needed(E, N, N_src, F, reduce, g))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
   hipStream_t s = as_stream(stream);
   Carver c(ws, ws_bytes);
   Graph tmp;
   const Graph* gp = nullptr;
-  int64_t partials = g ? g->g.n_heavy : graph_layout(E, N, default_chunk()).cap_heavy;
-  void* part = c.take(aggregate_partial_bytes(partials, F, reduce));
+  void* part = c.take(aggregate_partial_bytes(partials_needed(E, N, N_src, F, g), F, reduce));
   if (g) {
     // a handle built with loops describes the E' = E_in + N edges of this list
     gp = &g->g;
@@ -330,7 +365,7 @@ int tfg_gat_edge_scores(const void* edge_index, int index_type, int64_t E, const
 size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_graph* g) {
   (void)H;
   if (E < 0 || N < 0) return 0;
-  return g ? 256 : graph_total_bytes(E, N);
+  return g ? 256 : graph_total_bytes(E, N, choose_parts(E, N, 1, 0));
 }
 
 int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* seg, int index_type,

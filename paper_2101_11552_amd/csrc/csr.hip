@@ -1,9 +1,19 @@
-// COO -> CSR by target on the GPU (gfx950): validation + target histogram,
-// exclusive scans, a stable LSD radix sort of the edge ids by target, and the
-// aggregation work list. The result is the unique stable permutation (edges
-// sorted by target, input order kept among equal targets), so it is
-// bit-identical to a sequential counting sort.
+// COO -> CSR by target on the GPU (gfx950).
+//
+// The edges are sorted by the key (target, source part) with a stable LSD
+// radix sort, so the permutation is the unique one that orders the keys and
+// keeps the input order among equal keys (bit-identical to a sequential
+// counting sort). With one source part this is the CSR by target.
+//
+// Per radix pass: an upsweep counts the digits of every 8192-edge tile
+// (block-major histogram, coalesced), three small kernels turn the counts
+// into output offsets, and a scatter ranks each tile stably (one ballot per
+// digit bit per 64 edges), stages it in LDS in digit order and writes every
+// digit's run with consecutive addresses. Row pointers come from the run
+// boundaries of the sorted keys; the aggregation work lists from the row
+// pointers.
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 
 #include "tfg_internal.h"
@@ -15,12 +25,14 @@ constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;  // 2048
 
-constexpr int kSortThreads = 512;                // 8 waves
-constexpr int kSortItems = 8;                    // items per thread
-constexpr int kSortTile = kSortThreads * kSortItems;  // 4096 edges per block
+constexpr int kSortThreads = 1024;                    // 16 waves
+constexpr int kSortItems = 8;                         // items per thread
+constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 edges per tile
 constexpr int kSortWaves = kSortThreads / kWave;
 constexpr int kMaxDigitBits = 9;
-constexpr int kMaxRadix = 1 << kMaxDigitBits;    // 512 = kSortThreads
+constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 512
+constexpr int kHistChunk = 256;                       // tiles per offset chunk
+constexpr int kXcds = 8;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
@@ -53,25 +65,62 @@ __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int* total) {
   return off + incl - v;
 }
 
-// Edge e of the list with appended loops: ids < E_in come from edge_index
-// (clamped into range, with *bad set when out of range), ids >= E_in are the
-// loops (i, i), i = e - E_in.
+// Blocks are dispatched round-robin over the XCDs; tile_of() gives each XCD a
+// contiguous range of tiles, so neighbouring tiles (whose runs of one digit
+// are adjacent in the output) share an L2.
+__device__ __forceinline__ int tile_of(int bid, int ntiles) {
+  const int q = ntiles / kXcds, r = ntiles % kXcds;
+  const int x = bid % kXcds, i = bid / kXcds;
+  return x * q + min(x, r) + i;
+}
+
+// Edge e of the list with appended loops, as (source, sort key). Ids < E_in
+// come from edge_index (an out-of-range id is replaced by 0 and flagged), ids
+// >= E_in are the loops (i, i), i = e - E_in. key = target * P + source part.
+struct KeyMap {
+  int64_t E_in, N_src, N;
+  int part_rows, parts;
+  float inv_part_rows;  // 1 / part_rows, for the source-part estimate
+};
+
+// source / part_rows for 0 <= source < 2^31: a float estimate (off by at most
+// one) corrected with exact integer compares.
+__device__ __forceinline__ int source_part(int s, const KeyMap& m) {
+  int q = (int)((float)s * m.inv_part_rows);
+  q = (int64_t)q * m.part_rows > s ? q - 1 : q;
+  q = (int64_t)(q + 1) * m.part_rows <= s ? q + 1 : q;
+  return q;
+}
+
+// Raw ids of edge e (read for every edge, clamped into [0, E_in) so that the
+// loads of a whole tile can be issued together); decode_edge() then applies
+// the range checks and the loop rule.
 template <typename IdxT>
-__device__ __forceinline__ void load_edge(const IdxT* __restrict__ src, const IdxT* __restrict__ tgt,
-                                          int64_t E_in, int64_t N_src, int64_t N, int64_t e,
-                                          int* s, int* t, bool* bad) {
-  if (e < E_in) {
-    int64_t sv = src ? (int64_t)src[e] : 0;
-    int64_t tv = (int64_t)tgt[e];
-    bool sbad = src && (sv < 0 || sv >= N_src);
-    bool tbad = tv < 0 || tv >= N;
-    *bad = sbad || tbad;
-    *s = sbad ? 0 : (int)sv;
-    *t = tbad ? 0 : (int)tv;
-  } else {
-    *bad = false;
-    *s = *t = (int)(e - E_in);
-  }
+__device__ __forceinline__ void load_raw(const IdxT* __restrict__ src, const IdxT* __restrict__ tgt,
+                                         int64_t E_in, int64_t e, IdxT* s, IdxT* t) {
+  const int64_t ec = e < E_in ? e : (E_in > 0 ? E_in - 1 : 0);
+  *s = (src && E_in > 0) ? src[ec] : IdxT(0);
+  *t = E_in > 0 ? tgt[ec] : IdxT(0);
+}
+
+template <typename IdxT>
+__device__ __forceinline__ int decode_source(const KeyMap& m, int64_t e, IdxT s, bool has_src,
+                                             bool* bad) {
+  const bool sbad = has_src && (s < 0 || (int64_t)s >= m.N_src);
+  *bad = sbad;
+  return e < m.E_in ? (sbad ? 0 : (int)s) : (int)(e - m.E_in);
+}
+
+template <typename IdxT>
+__device__ __forceinline__ void decode_edge(const KeyMap& m, int64_t e, IdxT s, IdxT t,
+                                            bool has_src, int* sv, int* key, bool* bad) {
+  const bool in = e < m.E_in;
+  bool sbad;
+  *sv = decode_source(m, e, s, has_src, &sbad);
+  const bool tbad = t < 0 || (int64_t)t >= m.N;
+  *bad = in && (sbad || tbad);
+  const int tv = in ? (tbad ? 0 : (int)t) : (int)(e - m.E_in);
+  *key = m.parts == 1 ? tv : tv * m.parts + source_part(*sv, m);
 }
 
 __global__ void fill_int(int* __restrict__ p, int64_t n, int v) {
@@ -130,66 +179,105 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply(const int* in, int* o
 
 int64_t scan_tiles(int64_t n) { return (n + kScanTile - 1) / kScanTile; }
 
-int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s) {
-  if (n <= 0) return TFG_OK;
-  int64_t nt = scan_tiles(n);
-  scan_tile_sums<<<dim3((unsigned)nt), dim3(kScanThreads), 0, s>>>(in, n, tile_sums);
-  scan_sums<<<1, 1024, 0, s>>>(tile_sums, nt);
-  scan_apply<<<dim3((unsigned)nt), dim3(kScanThreads), 0, s>>>(in, out, n, tile_sums);
-  TFG_LAUNCHED("exclusive scan");
-  return TFG_OK;
-}
-
 // ---------------------------------------------------------------------------
 // Radix sort passes.
 // ---------------------------------------------------------------------------
 
-// First upsweep: validates every edge, counts edges per target (global
-// integer atomics: exact, order-free) and builds the block's digit histogram
-// for the first pass. hist is digit-major: hist[d * nblocks + block].
-template <typename IdxT>
-__global__ __launch_bounds__(kSortThreads) void first_upsweep(
-    const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, int64_t E_in, int64_t N_src,
-    int64_t N, int64_t E, int shift, int dbits, int* __restrict__ cnt, int* __restrict__ hist,
-    int nblocks, int* __restrict__ err) {
+// Digit counts of one tile, written as row `tile` of the block-major table
+// hist[tile * radix + d]. The first pass also validates the ids.
+template <bool FIRST, typename IdxT>
+__global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__ src,
+                                                        const IdxT* __restrict__ tgt, KeyMap m,
+                                                        const int* __restrict__ keys, int64_t E,
+                                                        int shift, int dbits,
+                                                        int* __restrict__ hist,
+                                                        int* __restrict__ err) {
   __shared__ int h[kMaxRadix];
   const int radix = 1 << dbits;
   for (int d = threadIdx.x; d < radix; d += kSortThreads) h[d] = 0;
   __syncthreads();
-  int64_t base = (int64_t)blockIdx.x * kSortTile;
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  IdxT rs[kSortItems], rt[kSortItems];
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
+    if constexpr (FIRST) {
+      load_raw(src, tgt, m.E_in, e, &rs[i], &rt[i]);
+    } else {
+      rt[i] = (IdxT)keys[e < E ? e : E - 1];
+      rs[i] = 0;
+    }
+  }
   bool any_bad = false;
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
-    if (e < E) {
-      int s, t;
+    const int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
+    int k = (int)rt[i];
+    if constexpr (FIRST) {
+      int s;
       bool bad;
-      load_edge(src, tgt, E_in, N_src, N, e, &s, &t, &bad);
-      any_bad |= bad;
-      atomicAdd(&cnt[t], 1);
-      atomicAdd(&h[(t >> shift) & (radix - 1)], 1);
+      decode_edge(m, e, rs[i], rt[i], src != nullptr, &s, &k, &bad);
+      any_bad |= bad && e < E;
     }
+    if (e < E) atomicAdd(&h[(k >> shift) & (radix - 1)], 1);
   }
-  if (any_bad) atomicOr(err, kErrIndex);
+  if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += kSortThreads) hist[(int64_t)d * nblocks + blockIdx.x] = h[d];
+  for (int d = threadIdx.x; d < radix; d += kSortThreads)
+    hist[(int64_t)blockIdx.x * radix + d] = h[d];
 }
 
-__global__ __launch_bounds__(kSortThreads) void upsweep(const int* __restrict__ keys, int64_t E,
-                                                        int shift, int dbits,
-                                                        int* __restrict__ hist, int nblocks) {
-  __shared__ int h[kMaxRadix];
-  const int radix = 1 << dbits;
-  for (int d = threadIdx.x; d < radix; d += kSortThreads) h[d] = 0;
-  __syncthreads();
-  int64_t base = (int64_t)blockIdx.x * kSortTile;
+// Offsets from the digit counts: offset(t, d) = sum over digits d' < d of all
+// counts + sum over tiles t' < t of the counts of d. Tiles are grouped in
+// chunks of kHistChunk: per-chunk column sums, a scan over chunks and digits,
+// then a per-chunk running sum written in place.
+__global__ __launch_bounds__(kMaxRadix) void hist_chunk_sums(const int* __restrict__ hist,
+                                                             int64_t ntiles, int radix,
+                                                             int* __restrict__ csum) {
+  const int d = threadIdx.x;
+  if (d >= radix) return;
+  const int64_t t0 = (int64_t)blockIdx.x * kHistChunk;
+  const int64_t t1 = t0 + kHistChunk < ntiles ? t0 + kHistChunk : ntiles;
+  int s = 0;
+#pragma unroll 8
+  for (int64_t t = t0; t < t1; ++t) s += hist[t * radix + d];
+  csum[(int64_t)blockIdx.x * radix + d] = s;
+}
+
+__global__ __launch_bounds__(kMaxRadix) void hist_chunk_scan(int* __restrict__ csum,
+                                                             int64_t nchunks, int radix) {
+  __shared__ int tmp[kMaxRadix / kWave];
+  const int d = threadIdx.x;
+  int run = 0;
+  if (d < radix)
+    for (int64_t c = 0; c < nchunks; ++c) {
+      const int v = csum[c * radix + d];
+      csum[c * radix + d] = run;
+      run += v;
+    }
+  const int base = block_excl_scan<kMaxRadix / kWave>(d < radix ? run : 0, tmp, nullptr);
+  if (d < radix)
+    for (int64_t c = 0; c < nchunks; ++c) csum[c * radix + d] += base;
+}
+
+__global__ __launch_bounds__(kMaxRadix) void hist_apply(int* __restrict__ hist, int64_t ntiles,
+                                                        int radix, const int* __restrict__ csum) {
+  const int d = threadIdx.x;
+  if (d >= radix) return;
+  const int64_t t0 = (int64_t)blockIdx.x * kHistChunk;
+  const int64_t t1 = t0 + kHistChunk < ntiles ? t0 + kHistChunk : ntiles;
+  int run = csum[(int64_t)blockIdx.x * radix + d];
+  for (int64_t t = t0; t < t1; t += 8) {
+    int v[8];
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
-    if (e < E) atomicAdd(&h[(keys[e] >> shift) & (radix - 1)], 1);
+    for (int j = 0; j < 8; ++j) v[j] = t + j < t1 ? hist[(t + j) * radix + d] : 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (t + j < t1) {
+        hist[(t + j) * radix + d] = run;
+        run += v[j];
+      }
   }
-  __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += kSortThreads) hist[(int64_t)d * nblocks + blockIdx.x] = h[d];
 }
 
 // Stable scatter of one tile by one digit. Wave w owns tile positions
@@ -197,166 +285,265 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const int* __restrict__ 
 // (wave, round, lane) order is the input order. Within a round, lanes with the
 // same digit find each other with one ballot per digit bit; their rank is the
 // number of such lanes below them plus the wave's running count of the digit.
-// The tile is then staged in LDS in digit order and written out so that
-// consecutive threads write consecutive addresses of a digit's run.
-//   FIRST: keys/payloads come from edge_index (payload = edge id, source id)
-//   LAST : writes perm (edge id) and col (source id) only
-template <bool FIRST, bool LAST, typename IdxT>
-__global__ __launch_bounds__(kSortThreads) void scatter(
-    const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, int64_t E_in, int64_t N_src,
-    int64_t N, const int* __restrict__ kin, const int* __restrict__ ein,
-    const int* __restrict__ sin, int64_t E, int shift, int dbits,
-    const int* __restrict__ hist, int nblocks, int* __restrict__ kout, int* __restrict__ eout,
-    int* __restrict__ sout) {
-  __shared__ int wcnt[kSortWaves][kMaxRadix];
+// The tile is then staged in LDS in digit order, one array at a time (keys,
+// edge ids, source ids share one buffer), and written out so that consecutive
+// threads write consecutive addresses of a digit's run.
+//   FIRST: keys and payloads come from edge_index (payload: edge id, source)
+// (16-wave blocks; at most 64 VGPRs so that two blocks fit on a CU)
+template <bool FIRST, typename IdxT>
+__global__ __launch_bounds__(kSortThreads, 8) void scatter(
+    const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, KeyMap m,
+    const int* __restrict__ kin, const int* __restrict__ ein, const int* __restrict__ sin,
+    int64_t E, int shift, int dbits, const int* __restrict__ hist, int ntiles,
+    int* __restrict__ kout, int* __restrict__ eout, int* __restrict__ sout) {
+  __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
   __shared__ int loff[kMaxRadix];
   __shared__ int goff[kMaxRadix];
-  __shared__ int skey[kSortTile];
-  __shared__ int sedge[kSortTile];
-  __shared__ int ssrc[kSortTile];
+  __shared__ int stage[kSortTile];
   __shared__ int tmp[kSortWaves];
 
   const int radix = 1 << dbits;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  const int tile = tile_of((int)blockIdx.x, ntiles);
+  const int64_t base = (int64_t)tile * kSortTile;
   const int tile_n = (int)min<int64_t>(kSortTile, E - base);
   const unsigned long long lt = (1ull << lane) - 1ull;
 
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
   __syncthreads();
 
-  int key[kSortItems], edge[kSortItems], sv[kSortItems], rank[kSortItems];
+  // Only the keys and ranks stay in registers; edge ids and source ids are
+  // fetched again (from L2) when they are staged, which keeps the kernel at
+  // 64 VGPRs (two 16-wave blocks per CU).
+  int key[kSortItems], lpos[kSortItems];
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
-    bool valid = p < tile_n;
-    int64_t e = base + p;
-    if (valid) {
-      if constexpr (FIRST) {
-        bool bad;
-        load_edge(src, tgt, E_in, N_src, N, e, &sv[i], &key[i], &bad);
-        edge[i] = (int)e;
-      } else {
-        key[i] = kin[e];
-        edge[i] = ein[e];
-        sv[i] = sin[e];
-      }
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
+    const int64_t e = base + (p < tile_n ? p : tile_n - 1);
+    if constexpr (FIRST) {
+      IdxT s0, t0;
+      load_raw(src, tgt, m.E_in, e, &s0, &t0);
+      int s;
+      bool bad;
+      decode_edge(m, e, s0, t0, src != nullptr, &s, &key[i], &bad);
     } else {
-      key[i] = 0;
-      edge[i] = 0;
-      sv[i] = 0;
+      key[i] = kin[e];
     }
-    int d = (key[i] >> shift) & (radix - 1);
+  }
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+    const bool valid = p < tile_n;
+    const int d = (key[i] >> shift) & (radix - 1);
     unsigned long long peers = __ballot(valid);
     for (int b = 0; b < dbits; ++b) {
-      int bit = (d >> b) & 1;
-      unsigned long long bb = __ballot(bit);
+      const int bit = (d >> b) & 1;
+      const unsigned long long bb = __ballot(bit);
       peers &= bit ? bb : ~bb;
     }
-    int below = __popcll(peers & lt);
-    int run = valid ? wcnt[wave][d] : 0;
-    rank[i] = run + below;
-    if (valid && below == 0) wcnt[wave][d] = run + __popcll(peers);
+    const int below = __popcll(peers & lt);
+    const int run = valid ? (int)wcnt[wave][d] : 0;
+    lpos[i] = run + below;  // rank within the wave for now
+    if (valid && below == 0) wcnt[wave][d] = (unsigned short)(run + __popcll(peers));
   }
   __syncthreads();
 
-  // Per digit: exclusive offsets of the waves, the block total, the block's
-  // start in LDS (scan over digits) and its start in the output (scanned hist).
+  // Per digit: exclusive offsets of the waves, the tile's start in LDS (scan
+  // over digits) and its start in the output.
   {
-    int d = threadIdx.x;  // kSortThreads == kMaxRadix
+    const int d = threadIdx.x;
     int tot = 0;
     if (d < radix) {
 #pragma unroll
       for (int w = 0; w < kSortWaves; ++w) {
-        int c = wcnt[w][d];
-        wcnt[w][d] = tot;
+        const int c = wcnt[w][d];
+        wcnt[w][d] = (unsigned short)tot;
         tot += c;
       }
     }
-    int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
+    const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
     if (d < radix) {
       loff[d] = ex;
-      goff[d] = hist[(int64_t)d * nblocks + blockIdx.x];
+      goff[d] = hist[(int64_t)tile * radix + d];
     }
   }
   __syncthreads();
 
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    int p = wave * (kWave * kSortItems) + i * kWave + lane;
-    if (p < tile_n) {
-      int d = (key[i] >> shift) & (radix - 1);
-      int lp = loff[d] + wcnt[wave][d] + rank[i];
-      skey[lp] = key[i];
-      sedge[lp] = edge[i];
-      ssrc[lp] = sv[i];
-    }
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+    const int d = (key[i] >> shift) & (radix - 1);
+    // -1 marks positions past the end of the tile
+    lpos[i] = p < tile_n ? lpos[i] + loff[d] + (int)wcnt[wave][d] : -1;
   }
-  __syncthreads();
 
+  // keys: stage, then every thread writes positions threadIdx.x + i * 1024
+  int gpos[kSortItems];
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (lpos[i] >= 0) stage[lpos[i]] = key[i];
+  __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    int p = i * kSortThreads + threadIdx.x;
+    const int p = i * kSortThreads + threadIdx.x;
+    gpos[i] = -1;
     if (p < tile_n) {
-      int k = skey[p];
-      int d = (k >> shift) & (radix - 1);
-      int64_t gp = (int64_t)goff[d] + (p - loff[d]);
+      const int k = stage[p];
+      const int d = (k >> shift) & (radix - 1);
+      const int64_t gp = (int64_t)goff[d] + (p - loff[d]);
       if (gp >= 0 && gp < E) {  // always true for a consistent histogram
-        if constexpr (!LAST) kout[gp] = k;
-        eout[gp] = sedge[p];
-        sout[gp] = ssrc[p];
+        gpos[i] = (int)gp;
+        kout[gp] = k;
       }
     }
   }
+  __syncthreads();
+  // edge ids
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (lpos[i] >= 0) {
+      const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
+      stage[lpos[i]] = FIRST ? (int)e : ein[e];
+    }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (gpos[i] >= 0) eout[gpos[i]] = stage[i * kSortThreads + threadIdx.x];
+  __syncthreads();
+  // source ids
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (lpos[i] >= 0) {
+      const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
+      int s;
+      if constexpr (FIRST) {
+        const int64_t ec = e < m.E_in ? e : (m.E_in > 0 ? m.E_in - 1 : 0);
+        const IdxT s0 = (src && m.E_in > 0) ? src[ec] : IdxT(0);
+        bool bad;
+        s = decode_source(m, e, s0, src != nullptr, &bad);
+      } else {
+        s = sin[e];
+      }
+      stage[lpos[i]] = s;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (gpos[i] >= 0) sout[gpos[i]] = stage[i * kSortThreads + threadIdx.x];
+}
+
+// bounds[v] = first position whose sorted key is >= v (v = 0..K). Position k
+// starts the keys (key[k-1], key[k]]; k = E closes the keys after the last one.
+// Four positions per thread.
+__global__ __launch_bounds__(kBlock) void key_bounds(const int* __restrict__ keys, int64_t E,
+                                                     int64_t K, int* __restrict__ bounds) {
+  const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (k0 > E) return;
+  int64_t cur[5];
+  cur[0] = k0 > 0 ? keys[k0 - 1] : -1;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) cur[j + 1] = k0 + j < E ? keys[k0 + j] : K;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (k0 + j > E) break;
+    for (int64_t v = cur[j] + 1; v <= cur[j + 1]; ++v) bounds[v] = (int)(k0 + j);
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void rows_from_segments(const int* __restrict__ segptr,
+                                                             int64_t N, int parts,
+                                                             int* __restrict__ rowptr) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t <= N) rowptr[t] = segptr[t * parts];
 }
 
 // ---------------------------------------------------------------------------
-// Aggregation work list.
+// Aggregation work lists.
 // ---------------------------------------------------------------------------
 
 // Reserves v entries of *ctr for this lane with one atomic per wave; returns
 // the lane's first entry.
 __device__ __forceinline__ int wave_reserve(int* ctr, int v) {
-  int incl = wave_incl_scan(v);
-  int total = __shfl(incl, kWave - 1);
+  const int incl = wave_incl_scan(v);
+  const int total = __shfl(incl, kWave - 1);
   int base = 0;
   if (lane_id() == kWave - 1 && total > 0) base = atomicAdd(ctr, total);
   base = __shfl(base, kWave - 1);
   return base + incl - v;
 }
 
-// Rows with at most `chunk` edges become one light item; longer rows are cut
-// into ceil(deg / chunk) heavy items whose partial results are combined by
-// the fix-up pass. Item order within each list is arbitrary (it only affects
-// scheduling, never values).
+// Row plan: rows with at most `chunk` edges become one light item; longer
+// rows are cut into ceil(deg / chunk) heavy items whose partial results the
+// fix-up pass combines. Item order within each list is arbitrary (it only
+// affects scheduling, never values).
 __global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__ rowptr, int64_t N,
                                                          int chunk, int* __restrict__ counters,
                                                          WorkItem* __restrict__ heavy,
                                                          WorkItem* __restrict__ light,
                                                          SplitRow* __restrict__ split) {
-  int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int beg = 0, deg = 0;
   if (r < N) {
     beg = rowptr[r];
     deg = rowptr[r + 1] - beg;
   }
-  bool valid = r < N;
-  bool is_split = valid && deg > chunk;
-  int nch = is_split ? (deg + chunk - 1) / chunk : 0;
-  int h0 = wave_reserve(&counters[0], nch);
-  int l0 = wave_reserve(&counters[1], valid && !is_split ? 1 : 0);
-  int s0 = wave_reserve(&counters[2], is_split ? 1 : 0);
+  const bool valid = r < N;
+  const bool is_split = valid && deg > chunk;
+  const int nch = is_split ? (deg + chunk - 1) / chunk : 0;
+  const int h0 = wave_reserve(&counters[0], nch);
+  const int l0 = wave_reserve(&counters[1], valid && !is_split ? 1 : 0);
+  const int s0 = wave_reserve(&counters[2], is_split ? 1 : 0);
   if (!valid) return;
   if (is_split) {
     for (int j = 0; j < nch; ++j) {
-      int kb = beg + j * chunk;
+      const int kb = beg + j * chunk;
       heavy[h0 + j] = WorkItem{(int)r, kb, min(kb + chunk, beg + deg), h0 + j};
     }
     split[s0] = SplitRow{(int)r, h0, nch, deg};
   } else {
     light[l0] = WorkItem{(int)r, beg, beg + deg, -1};
   }
+}
+
+__device__ __forceinline__ int chunks_of(int len, int chunk) { return (len + chunk - 1) / chunk; }
+
+// Part plan, step 1: items per row (all parts) and per (part, row).
+__global__ __launch_bounds__(kBlock) void part_counts(const int* __restrict__ segptr, int64_t N,
+                                                      int parts, int chunk,
+                                                      int* __restrict__ row_items,
+                                                      int* __restrict__ seg_items) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N) return;
+  int tot = 0;
+  for (int p = 0; p < parts; ++p) {
+    const int len = segptr[t * parts + p + 1] - segptr[t * parts + p];
+    const int c = chunks_of(len, chunk);
+    seg_items[(int64_t)p * N + t] = c;
+    tot += c;
+  }
+  row_items[t] = tot;
+}
+
+// Part plan, step 2: items in part-major order (part, row, chunk); the
+// partial slots are numbered row-major so that row t's partials are the
+// contiguous range [row_slot[t], row_slot[t+1]), in part order.
+__global__ __launch_bounds__(kBlock) void part_fill(const int* __restrict__ segptr, int64_t N,
+                                                    int parts, int chunk,
+                                                    const int* __restrict__ row_slot,
+                                                    const int* __restrict__ seg_pos,
+                                                    WorkItem* __restrict__ exec,
+                                                    SplitRow* __restrict__ rows) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N) return;
+  int slot = row_slot[t];
+  const int s0 = slot;
+  for (int p = 0; p < parts; ++p) {
+    const int kb = segptr[t * parts + p], ke = segptr[t * parts + p + 1];
+    int pos = seg_pos[(int64_t)p * N + t];
+    for (int k = kb; k < ke; k += chunk) exec[pos++] = WorkItem{(int)t, k, min(k + chunk, ke), slot++};
+  }
+  rows[t] = SplitRow{(int)t, s0, slot - s0, segptr[(t + 1) * parts] - segptr[t * parts]};
 }
 
 int ceil_log2(int64_t n) {
@@ -367,24 +554,26 @@ int ceil_log2(int64_t n) {
 
 struct SortPlan {
   int bits, passes, dbits;
-  int64_t nblocks;
+  int64_t ntiles, nchunks, keyspace;
 };
 
-SortPlan sort_plan(int64_t E, int64_t N) {
+SortPlan sort_plan(int64_t E, int64_t N, int parts) {
   SortPlan p;
-  p.bits = std::max(1, ceil_log2(std::max<int64_t>(N, 2)));
+  p.keyspace = std::max<int64_t>(N * parts, 1);
+  p.bits = std::max(1, ceil_log2(std::max<int64_t>(p.keyspace, 2)));
   p.passes = (p.bits + kMaxDigitBits - 1) / kMaxDigitBits;
   p.dbits = (p.bits + p.passes - 1) / p.passes;
-  p.nblocks = (E + kSortTile - 1) / kSortTile;
+  p.ntiles = (E + kSortTile - 1) / kSortTile;
+  p.nchunks = (p.ntiles + kHistChunk - 1) / kHistChunk;
   return p;
 }
 
 struct ScratchLayout {
-  size_t cnt, hist, sums, bufA, bufB, total;
+  size_t keys, hist, csum, sums, bufA, bufB, row_items, seg_items, total;
 };
 
-ScratchLayout scratch_layout(int64_t E, int64_t N) {
-  SortPlan p = sort_plan(E, N);
+ScratchLayout scratch_layout(int64_t E, int64_t N, int parts) {
+  SortPlan p = sort_plan(E, N, parts);
   ScratchLayout L;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -392,13 +581,16 @@ ScratchLayout scratch_layout(int64_t E, int64_t N) {
     off = align_up(off + bytes, 256);
     return o;
   };
-  int64_t hist_n = (int64_t)(1 << p.dbits) * p.nblocks;
-  int64_t scan_n = std::max<int64_t>(hist_n, N + 1);
-  L.cnt = take(sizeof(int) * (N + 1));
-  L.hist = take(sizeof(int) * std::max<int64_t>(hist_n, 1));
+  const int64_t radix = int64_t(1) << p.dbits;
+  const int64_t scan_n = std::max<int64_t>(N * parts + 1, N + 1);
+  L.keys = take(sizeof(int) * std::max<int64_t>(E, 1));
+  L.hist = take(sizeof(int) * std::max<int64_t>(radix * p.ntiles, 1));
+  L.csum = take(sizeof(int) * std::max<int64_t>(radix * p.nchunks, 1));
   L.sums = take(sizeof(int) * std::max<int64_t>(scan_tiles(scan_n), 1));
   L.bufA = take(sizeof(int) * 3 * std::max<int64_t>(E, 1));
   L.bufB = take(p.passes >= 3 ? sizeof(int) * 3 * std::max<int64_t>(E, 1) : 0);
+  L.row_items = take(parts > 1 ? sizeof(int) * (N + 1) : 0);
+  L.seg_items = take(parts > 1 ? sizeof(int) * (N * parts + 1) : 0);
   L.total = off;
   return L;
 }
@@ -407,76 +599,125 @@ template <typename IdxT>
 int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const ScratchLayout& L,
                hipStream_t s) {
   const int64_t E = g.E;
-  SortPlan p = sort_plan(E, g.N);
-  int* cnt = reinterpret_cast<int*>(scratch + L.cnt);
+  const SortPlan p = sort_plan(E, g.N, g.parts);
+  const KeyMap m{g.E_in, g.N_src, g.N, (int)g.part_rows, g.parts, 1.0f / (float)g.part_rows};
+  int* keys = reinterpret_cast<int*>(scratch + L.keys);
   int* hist = reinterpret_cast<int*>(scratch + L.hist);
-  int* sums = reinterpret_cast<int*>(scratch + L.sums);
+  int* csum = reinterpret_cast<int*>(scratch + L.csum);
   int* bufs[2][3];
   for (int b = 0; b < 2; ++b) {
     int* base = reinterpret_cast<int*>(scratch + (b == 0 ? L.bufA : L.bufB));
     for (int j = 0; j < 3; ++j) bufs[b][j] = base + j * E;
   }
   int* err = g.counters + 3;
-  const unsigned nb = (unsigned)p.nblocks;
-  const int64_t hist_n = (int64_t)(1 << p.dbits) * p.nblocks;
+  const unsigned nt = (unsigned)p.ntiles;
+  const int radix = 1 << p.dbits;
 
-  fill_int<<<dim3((unsigned)((g.N + 1 + 255) / 256)), dim3(256), 0, s>>>(cnt, g.N + 1, 0);
   if (E > 0) {
-    first_upsweep<IdxT><<<nb, kSortThreads, 0, s>>>(src, tgt, g.E_in, g.N_src, g.N, E, 0, p.dbits,
-                                                    cnt, hist, (int)p.nblocks, err);
-    TFG_LAUNCHED("first_upsweep");
-    int rc = exclusive_scan(hist, hist, hist_n, sums, s);
-    if (rc) return rc;
     int cur = 0;  // which scratch buffer holds the current keys
     for (int pass = 0; pass < p.passes; ++pass) {
       const int shift = pass * p.dbits;
       const bool first = pass == 0, last = pass == p.passes - 1;
-      if (!first) {
-        upsweep<<<nb, kSortThreads, 0, s>>>(bufs[cur][0], E, shift, p.dbits, hist, (int)p.nblocks);
-        rc = exclusive_scan(hist, hist, hist_n, sums, s);
-        if (rc) return rc;
-      }
-      int nxt = first ? 0 : 1 - cur;
-      int* ko = last ? nullptr : bufs[nxt][0];
+      if (first)
+        upsweep<true, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, nullptr, E, shift, p.dbits,
+                                                        hist, err);
+      else
+        upsweep<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, shift,
+                                                         p.dbits, hist, err);
+      hist_chunk_sums<<<(unsigned)p.nchunks, kMaxRadix, 0, s>>>(hist, p.ntiles, radix, csum);
+      hist_chunk_scan<<<1, kMaxRadix, 0, s>>>(csum, p.nchunks, radix);
+      hist_apply<<<(unsigned)p.nchunks, kMaxRadix, 0, s>>>(hist, p.ntiles, radix, csum);
+      TFG_LAUNCHED("radix offsets");
+      const int nxt = first ? 0 : 1 - cur;
+      int* ko = last ? keys : bufs[nxt][0];
       int* eo = last ? g.perm : bufs[nxt][1];
       int* so = last ? g.col : bufs[nxt][2];
       const int *ki = bufs[cur][0], *ei = bufs[cur][1], *si = bufs[cur][2];
-      if (first && last)
-        scatter<true, true, IdxT><<<nb, kSortThreads, 0, s>>>(src, tgt, g.E_in, g.N_src, g.N, ki, ei,
-                                                             si, E, shift, p.dbits, hist,
-                                                             (int)p.nblocks, ko, eo, so);
-      else if (first)
-        scatter<true, false, IdxT><<<nb, kSortThreads, 0, s>>>(src, tgt, g.E_in, g.N_src, g.N, ki, ei,
-                                                              si, E, shift, p.dbits, hist,
-                                                              (int)p.nblocks, ko, eo, so);
-      else if (last)
-        scatter<false, true, IdxT><<<nb, kSortThreads, 0, s>>>(src, tgt, g.E_in, g.N_src, g.N, ki, ei,
-                                                              si, E, shift, p.dbits, hist,
-                                                              (int)p.nblocks, ko, eo, so);
+      if (first)
+        scatter<true, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift, p.dbits,
+                                                        hist, (int)p.ntiles, ko, eo, so);
       else
-        scatter<false, false, IdxT><<<nb, kSortThreads, 0, s>>>(src, tgt, g.E_in, g.N_src, g.N, ki,
-                                                               ei, si, E, shift, p.dbits, hist,
-                                                               (int)p.nblocks, ko, eo, so);
+        scatter<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift,
+                                                         p.dbits, hist, (int)p.ntiles, ko, eo, so);
       TFG_LAUNCHED("radix scatter");
       cur = nxt;
     }
   }
-  // rowptr = exclusive scan of the per-target counts (cnt[N] = 0 gives rowptr[N] = E)
-  return exclusive_scan(cnt, g.rowptr, g.N + 1, sums, s);
+  // segment starts from the boundaries of the sorted keys
+  const int64_t K = g.N * g.parts;
+  key_bounds<<<dim3((unsigned)((E / 4 + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(keys, E, K,
+                                                                                      g.segptr);
+  TFG_LAUNCHED("key_bounds");
+  if (g.parts > 1) {
+    rows_from_segments<<<dim3((unsigned)((g.N + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(
+        g.segptr, g.N, g.parts, g.rowptr);
+    TFG_LAUNCHED("rows_from_segments");
+  }
+  return TFG_OK;
+}
+
+int build_part_plan(Graph& g, char* scratch, const ScratchLayout& L, hipStream_t s) {
+  int* row_items = reinterpret_cast<int*>(scratch + L.row_items);
+  int* seg_items = reinterpret_cast<int*>(scratch + L.seg_items);
+  int* sums = reinterpret_cast<int*>(scratch + L.sums);
+  const unsigned nb = (unsigned)((g.N + kBlock - 1) / kBlock);
+  const int64_t NP = g.N * g.parts;
+  fill_int<<<1, 64, 0, s>>>(row_items + g.N, 1, 0);
+  fill_int<<<1, 64, 0, s>>>(seg_items + NP, 1, 0);
+  part_counts<<<nb, kBlock, 0, s>>>(g.segptr, g.N, g.parts, g.chunk, row_items, seg_items);
+  TFG_LAUNCHED("part_counts");
+  int rc = exclusive_scan(row_items, row_items, g.N + 1, sums, s);
+  if (rc) return rc;
+  rc = exclusive_scan(seg_items, seg_items, NP + 1, sums, s);
+  if (rc) return rc;
+  part_fill<<<nb, kBlock, 0, s>>>(g.segptr, g.N, g.parts, g.chunk, row_items, seg_items, g.pexec,
+                                  g.prows);
+  TFG_LAUNCHED("part_fill");
+  // the number of items, read back with the other counters
+  TFG_HIP(hipMemcpyAsync(g.counters + 4, seg_items + NP, sizeof(int), hipMemcpyDeviceToDevice, s));
+  return TFG_OK;
 }
 
 }  // namespace
 
+int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s) {
+  if (n <= 0) return TFG_OK;
+  const int64_t nt = scan_tiles(n);
+  scan_tile_sums<<<dim3((unsigned)nt), dim3(kScanThreads), 0, s>>>(in, n, tile_sums);
+  scan_sums<<<1, 1024, 0, s>>>(tile_sums, nt);
+  scan_apply<<<dim3((unsigned)nt), dim3(kScanThreads), 0, s>>>(in, out, n, tile_sums);
+  TFG_LAUNCHED("exclusive scan");
+  return TFG_OK;
+}
+
 int default_chunk() {
-  static int chunk = [] {
+  static const int chunk = [] {
     const char* v = std::getenv("TFG_ROW_CHUNK");
-    int c = v ? std::atoi(v) : kDefaultChunk;
+    const int c = v ? std::atoi(v) : kDefaultChunk;
     return c >= 64 ? c : kDefaultChunk;
   }();
   return chunk;
 }
 
-GraphLayout graph_layout(int64_t E, int64_t N, int chunk) {
+int choose_parts(int64_t E, int64_t N, int64_t N_src, int requested) {
+  int P = 1;
+  if (requested >= 1) {
+    P = std::min(requested, kMaxParts);
+  } else {
+    // 512-byte rows (128 float32 features) as the nominal gathered row size
+    const double table = (double)N_src * 512.0;
+    const double avg_deg = N > 0 ? (double)E / (double)N : 0.0;
+    if (table >= 32.0 * (1 << 20)) {
+      P = (int)std::min<double>(kMaxParts, std::ceil(table / (16.0 * (1 << 20))));
+      P = std::min<int>(P, (int)(avg_deg / 16.0));  // keep (row, part) segments long
+    }
+  }
+  P = (int)std::min<int64_t>(P, std::max<int64_t>(N_src, 1));
+  if (P < 1 || N * (int64_t)P >= (int64_t(1) << 31) - 1) P = 1;
+  return P;
+}
+
+GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk) {
   GraphLayout L;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -489,25 +730,33 @@ GraphLayout graph_layout(int64_t E, int64_t N, int chunk) {
   L.cap_split = std::min<int64_t>(N, E / chunk + 1);
   L.cap_heavy = 2 * (E / chunk) + 2;
   L.cap_light = N;
+  // part plan: one item per nonempty (row, part) segment, plus one per
+  // further chunk of a long segment
+  L.cap_pexec = parts > 1 ? std::min<int64_t>(E, N * parts) + E / chunk + 1 : 0;
   L.rowptr = take(sizeof(int) * (N + 1));
+  L.segptr = take(parts > 1 ? sizeof(int) * (N * parts + 1) : 0);
   L.col = take(sizeof(int) * std::max<int64_t>(E, 1));
   L.perm = take(sizeof(int) * std::max<int64_t>(E, 1));
   L.heavy = take(sizeof(WorkItem) * L.cap_heavy);
   L.light = take(sizeof(WorkItem) * std::max<int64_t>(L.cap_light, 1));
   L.split = take(sizeof(SplitRow) * std::max<int64_t>(L.cap_split, 1));
-  L.counters = take(sizeof(int) * 4);
+  L.pexec = take(sizeof(WorkItem) * L.cap_pexec);
+  L.prows = take(parts > 1 ? sizeof(SplitRow) * N : 0);
+  L.counters = take(sizeof(int) * 8);
   L.total = off;
   return L;
 }
 
-size_t graph_scratch_bytes(int64_t E, int64_t N) { return scratch_layout(E, N).total; }
+size_t graph_scratch_bytes(int64_t E, int64_t N, int parts) {
+  return scratch_layout(E, N, parts).total;
+}
 
 int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void* scratch,
                 size_t scratch_bytes, hipStream_t s) {
-  ScratchLayout L = scratch_layout(g.E, g.N);
+  const ScratchLayout L = scratch_layout(g.E, g.N, g.parts);
   if (scratch_bytes < L.total) return fail(TFG_ERR_WORKSPACE, "graph scratch buffer too small");
   char* sc = static_cast<char*>(scratch);
-  fill_int<<<1, 64, 0, s>>>(g.counters, 4, 0);
+  fill_int<<<1, 64, 0, s>>>(g.counters, 8, 0);
   int rc;
   if (index_type == TFG_I64)
     rc = sort_edges<int64_t>(g, static_cast<const int64_t*>(src), static_cast<const int64_t*>(tgt),
@@ -520,14 +769,19 @@ int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void
     build_worklist<<<dim3((unsigned)((g.N + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(
         g.rowptr, g.N, g.chunk, g.counters, g.heavy, g.light, g.split);
     TFG_LAUNCHED("build_worklist");
+    if (g.parts > 1) {
+      rc = build_part_plan(g, sc, L, s);
+      if (rc) return rc;
+    }
   }
-  int host[4];
+  int host[8];
   TFG_HIP(hipMemcpyAsync(host, g.counters, sizeof(host), hipMemcpyDeviceToHost, s));
   TFG_HIP(hipStreamSynchronize(s));
   if (host[3] & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "edge_index holds an id outside [0, N)");
   g.n_heavy = host[0];
   g.n_light = host[1];
   g.n_split = host[2];
+  g.n_pexec = host[4];
   return TFG_OK;
 }
 

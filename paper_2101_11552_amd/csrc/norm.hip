@@ -51,7 +51,8 @@ __global__ __launch_bounds__(kBlock) void degree_weighted(const int* __restrict_
   }
 }
 
-// CSR order: one wavefront per aggregation work item (row or row chunk).
+// CSR order: one wavefront per aggregation work item (row or row chunk); each
+// lane handles four positions per step with their loads issued together.
 __global__ __launch_bounds__(kBlock) void weights_csr(const WorkItem* __restrict__ heavy,
                                                       int n_heavy,
                                                       const WorkItem* __restrict__ light,
@@ -66,14 +67,30 @@ __global__ __launch_bounds__(kBlock) void weights_csr(const WorkItem* __restrict
   const WorkItem* it = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
   const int row = uniform(it->row), kb = uniform(it->kbeg), ke = uniform(it->kend);
   const float dt = dinv[row];
-  for (int k = kb + lane; k < ke; k += kWave) {
-    const float we = w ? edge_w(w, E_in, perm[k]) : 1.0f;
-    const float a = dinv[col[k]] * we;
-    out[k] = a * dt;
+  for (int k0 = kb + lane; k0 < ke; k0 += 4 * kWave) {
+    int c[4];
+    float we[4], ds[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k = k0 + j * kWave < ke ? k0 + j * kWave : k0;
+      c[j] = col[k];
+      we[j] = w ? edge_w(w, E_in, perm[k]) : 1.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ds[j] = dinv[c[j]];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k = k0 + j * kWave;
+      if (k < ke) {
+        const float a = ds[j] * we[j];
+        out[k] = a * dt;
+      }
+    }
   }
 }
 
-// COO order (input edges, then loops), optionally writing the edge list.
+// COO order (input edges, then loops), optionally writing the edge list; four
+// edges per thread, strided by the block size, loads issued together.
 template <typename IdxT>
 __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ src,
                                                       const IdxT* __restrict__ tgt, int64_t E_in,
@@ -82,23 +99,40 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
                                                       const float* __restrict__ dinv,
                                                       int32_t* __restrict__ out_ei,
                                                       float* __restrict__ out_w) {
-  int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= E) return;
-  int s, t;
-  if (e < E_in) {
-    int64_t sv = (int64_t)src[e], tv = (int64_t)tgt[e];
-    s = (sv < 0 || sv >= N) ? 0 : (int)sv;  // ids were validated when the graph was built
-    t = (tv < 0 || tv >= N) ? 0 : (int)tv;
-  } else {
-    s = t = (int)(e - E_in);
-  }
-  if (out_ei) {
-    out_ei[e] = s;
-    out_ei[E + e] = t;
+  const int64_t base = (int64_t)blockIdx.x * (4 * kBlock) + threadIdx.x;
+  int s[4], t[4];
+  float we[4], ds[4], dt[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t e = base + j * kBlock;
+    const int64_t ec = e < E_in ? e : (E_in > 0 ? E_in - 1 : 0);
+    const int64_t sv = E_in > 0 ? (int64_t)src[ec] : 0, tv = E_in > 0 ? (int64_t)tgt[ec] : 0;
+    const bool in = e < E_in;
+    // ids were validated when the graph was built; clamped here all the same
+    s[j] = in ? ((sv < 0 || sv >= N) ? 0 : (int)sv) : (int)(e - E_in);
+    t[j] = in ? ((tv < 0 || tv >= N) ? 0 : (int)tv) : (int)(e - E_in);
+    we[j] = (w != nullptr && in) ? w[ec] : 1.0f;
   }
   if (out_w) {
-    const float a = dinv[s] * edge_w(w, E_in, e);
-    out_w[e] = a * dinv[t];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = base + j * kBlock < E;
+      ds[j] = ok ? dinv[s[j]] : 0.0f;
+      dt[j] = ok ? dinv[t[j]] : 0.0f;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t e = base + j * kBlock;
+    if (e >= E) break;
+    if (out_ei) {
+      out_ei[e] = s[j];
+      out_ei[E + e] = t[j];
+    }
+    if (out_w) {
+      const float a = ds[j] * we[j];
+      out_w[e] = a * dt[j];
+    }
   }
 }
 
@@ -124,7 +158,7 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
     TFG_LAUNCHED("gcn weights (CSR order)");
   }
   if ((out_w || out_edge_index) && g.E > 0) {
-    const unsigned nb = (unsigned)((g.E + kBlock - 1) / kBlock);
+    const unsigned nb = (unsigned)((g.E + 4 * kBlock - 1) / (4 * kBlock));
     if (index_type == TFG_I64) {
       const int64_t* ei = static_cast<const int64_t*>(edge_index);
       weights_coo<int64_t><<<nb, kBlock, 0, s>>>(ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight,

@@ -20,19 +20,28 @@ constexpr int kDefaultChunk = 512; // max edges per aggregation work item
 constexpr int kErrIndex = 1;
 constexpr int kErrUnsorted = 2;
 
-// One aggregation work item, processed by one wavefront: the CSR positions
-// [kbeg, kend) of target `row`. slot < 0: the item covers the whole row and
-// writes the output row; slot >= 0: the row is split, the item writes partial
+// One aggregation work item, processed by one wavefront: the positions
+// [kbeg, kend) (graph order) of target `row`. slot < 0: the item covers the
+// whole row and writes the output row; slot >= 0: the item writes partial
 // result `slot` and a fix-up pass combines the row's partials in order.
 struct WorkItem {
   int row, kbeg, kend, slot;
 };
-// A split row: its partials are slot0 .. slot0 + nchunks - 1, in row order.
+// A row reduced from partials: slots slot0 .. slot0 + nchunks - 1, in order.
 struct SplitRow {
   int row, slot0, nchunks, deg;
 };
 
+constexpr int kMaxParts = 16;
+
 // Host view of a graph; the arrays live in the caller's persistent buffer.
+//
+// Edge order ("graph order"): edges sorted by the key (target, source part),
+// input order kept among equal keys, where source part = source / part_rows.
+// With parts == 1 this is the stable CSR by target. With parts > 1 the edges
+// of each row are grouped by source range, which lets the aggregation visit
+// the whole graph one source range at a time (the gathered rows of one range
+// stay in the L2 caches while it is processed).
 struct Graph {
   int64_t E_in = 0;    // input edges
   int64_t E = 0;       // total edges (input + appended loops)
@@ -40,25 +49,38 @@ struct Graph {
   int64_t N_src = 0;   // sources
   int loops = 0;
   int chunk = kDefaultChunk;
-  int* rowptr = nullptr;  // [N+1]
-  int* col = nullptr;     // [E]
-  int* perm = nullptr;    // [E]
+  int parts = 1;            // source parts P
+  int64_t part_rows = 1;    // sources per part
+  int* rowptr = nullptr;    // [N+1]
+  int* segptr = nullptr;    // [N*P+1]: start of (row, part); == rowptr when P == 1
+  int* col = nullptr;       // [E] source id per position
+  int* perm = nullptr;      // [E] input edge id per position
+  // row plan: one item per row (long rows cut into chunks + fix-up)
   WorkItem* heavy = nullptr;  // chunks of split rows; heavy[i] writes partial i
   WorkItem* light = nullptr;  // whole rows
   SplitRow* split = nullptr;
-  int* counters = nullptr;    // device: [0] heavy, [1] light, [2] split, [3] error flags
   int n_heavy = 0, n_light = 0, n_split = 0;
+  // part plan (P > 1): one item per (part, row) segment chunk, part-major
+  // order; every item writes a partial, prows[t] reduces row t's partials
+  WorkItem* pexec = nullptr;
+  SplitRow* prows = nullptr;
+  int n_pexec = 0;
+  int* counters = nullptr;  // device: [0] heavy, [1] light, [2] split, [3] error flags
   int device = 0;
 };
 
-// Sizes of the persistent / scratch parts of a graph.
+// Sizes of the persistent part of a graph.
 struct GraphLayout {
-  size_t rowptr, col, perm, heavy, light, split, counters, total;
-  int64_t cap_heavy, cap_light, cap_split;
+  size_t rowptr, segptr, col, perm, heavy, light, split, pexec, prows, counters, total;
+  int64_t cap_heavy, cap_light, cap_split, cap_pexec;
 };
-GraphLayout graph_layout(int64_t E, int64_t N, int chunk);
-size_t graph_scratch_bytes(int64_t E, int64_t N);
+GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk);
+size_t graph_scratch_bytes(int64_t E, int64_t N, int parts);
 int default_chunk();
+// Number of source parts for a graph: `requested` if >= 1 (capped), else a
+// choice from the sizes (P > 1 only when the gathered table is much larger
+// than the L2 caches and rows are long enough to be split by source range).
+int choose_parts(int64_t E, int64_t N, int64_t N_src, int requested);
 
 // Thread-local error message.
 void set_error(const std::string& msg);
@@ -83,6 +105,7 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // src may be NULL (a target-only list: col is then all zero).
 int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void* scratch,
                 size_t scratch_bytes, hipStream_t s);
+int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s);
 // norm.hip
 int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                     const float* edge_weight, int32_t* out_edge_index, float* out_w,
@@ -92,6 +115,8 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
                      int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax,
                      void* ws, hipStream_t s);
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce);
+// Whether an aggregation over g with F features uses the part plan.
+bool use_part_plan(const Graph& g, int64_t F);
 // softmax.hip
 int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const float* h,
                       int64_t N, int H, int D, const float* a_src, const float* a_dst,

@@ -50,28 +50,32 @@ def test_status_strings_and_version(lib):
 
 def test_size_queries(lib):
     b, s = ctypes.c_size_t(), ctypes.c_size_t()
-    assert lib.tfg_graph_bytes(1000, 100, 1, ctypes.byref(b), ctypes.byref(s)) == 0
+    assert lib.tfg_graph_bytes(1000, 100, 100, 1, 0, ctypes.byref(b), ctypes.byref(s)) == 0
     assert b.value >= 4 * (101 + 2 * 1100) and s.value >= 3 * 4 * 1100
-    assert lib.tfg_graph_bytes(-1, 100, 0, ctypes.byref(b), ctypes.byref(s)) == 1
-    assert lib.tfg_graph_bytes(2**31, 10, 0, ctypes.byref(b), ctypes.byref(s)) == 4
-    assert lib.tfg_graph_bytes(2**31 - 5, 10, 1, ctypes.byref(b), ctypes.byref(s)) == 4
+    plain = b.value
+    assert lib.tfg_graph_bytes(1000, 100, 100, 1, 4, ctypes.byref(b), ctypes.byref(s)) == 0
+    assert b.value >= plain + 4 * 400  # segment starts of 4 source parts
+    assert lib.tfg_graph_bytes(-1, 100, 100, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 1
+    assert lib.tfg_graph_bytes(2**31, 10, 10, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 4
+    assert lib.tfg_graph_bytes(2**31 - 5, 10, 10, 1, 0, ctypes.byref(b), ctypes.byref(s)) == 4
     assert lib.tfg_segment_pool_ws_bytes(100, 7) >= 8 * 4
-    assert lib.tfg_aggregate_ws_bytes(1000, 100, 64, 2, None) > lib.tfg_aggregate_ws_bytes(
-        1000, 100, 64, 0, None)
+    assert lib.tfg_aggregate_ws_bytes(1000, 100, 100, 64, 2, None) > lib.tfg_aggregate_ws_bytes(
+        1000, 100, 100, 64, 0, None)
 
 
 def test_host_side_argument_errors(lib):
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails its checks first
     h = ctypes.c_void_p()
     # null output handle, bad index type
-    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, fake, 1 << 20, fake, 1 << 20, None, None) == 1
-    assert lib.tfg_graph_create(fake, 7, 10, 5, 5, 0, fake, 1 << 20, fake, 1 << 20, None,
+    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, 0, fake, 1 << 20, fake, 1 << 20, None,
+                                None) == 1
+    assert lib.tfg_graph_create(fake, 7, 10, 5, 5, 0, 0, fake, 1 << 20, fake, 1 << 20, None,
                                 ctypes.byref(h)) == 1
     # self-loops with a rectangular adjacency
-    assert lib.tfg_graph_create(fake, 0, 10, 4, 5, 1, fake, 1 << 20, fake, 1 << 20, None,
+    assert lib.tfg_graph_create(fake, 0, 10, 4, 5, 1, 0, fake, 1 << 20, fake, 1 << 20, None,
                                 ctypes.byref(h)) == 1
     # buffer too small
-    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, fake, 16, fake, 1 << 20, None,
+    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, 0, fake, 16, fake, 1 << 20, None,
                                 ctypes.byref(h)) == 5
     assert b"too small" in lib.tfg_last_error()
     # aggregate: bad reduce, F not a multiple of H, ldx < F, workspace too small

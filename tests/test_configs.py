@@ -119,21 +119,28 @@ def test_power_law_full_size(tfg, orc):
     assert info["E"] == E + n and info["n_rows_split"] > 0
     norm = tfg.tfg_gcn_norm(eid, n, graph=g)
 
-    # CSR: sorted by target, a permutation, input order inside each row -> unique
+    # graph order: sorted by (target, source part), a permutation, input order
+    # among equal keys -> unique
+    P = info["src_parts"]
+    R = -(-n // P)
     rowptr, col, perm = tfg.tfg_graph_csr(g)
-    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)])
-    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)])
-    cnt = torch.bincount(tgt_full.long(), minlength=n)
+    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
+    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
+    cnt = torch.bincount(tgt_full, minlength=n)
     assert torch.equal(rowptr[1:].long() - rowptr[:-1].long(), cnt) and rowptr[0].item() == 0
     pl = perm.long()
     assert torch.equal(torch.bincount(pl, minlength=E + n), torch.ones(E + n, dtype=torch.long,
                                                                      device=pl.device))
-    t_sorted = tgt_full[pl]
-    assert bool((t_sorted[1:] >= t_sorted[:-1]).all())
-    same_row = t_sorted[1:] == t_sorted[:-1]
-    assert bool((pl[1:][same_row] > pl[:-1][same_row]).all())
-    assert torch.equal(col, src_full[pl])
-    del tgt_full, src_full, pl, t_sorted, same_row
+    key = (tgt_full * P + src_full // R)[pl]
+    assert bool((key[1:] >= key[:-1]).all())
+    same_key = key[1:] == key[:-1]
+    assert bool((pl[1:][same_key] > pl[:-1][same_key]).all())
+    assert torch.equal(col.long(), src_full[pl])
+    if P > 1:
+        seg = tfg.tfg_graph_segments(g).long()
+        assert torch.equal(seg[1:] - seg[:-1], torch.bincount(tgt_full * P + src_full // R,
+                                                              minlength=n * P))
+    del tgt_full, src_full, pl, key, same_key
 
     # degrees and weights: bit-exact against the oracle on the whole graph
     oei, ow, odeg = orc.gcn_norm(ei, n)
@@ -142,7 +149,8 @@ def test_power_law_full_size(tfg, orc):
     assert same_bits(host(norm["edge_weight_csr"]), ow[host(perm)])
 
     # aggregation: sampled rows (heaviest rows, split rows, random rows) one by one
-    y = tfg.tfg_aggregate(norm["edge_index"], dev(x), n, "sum",
+    assert info["src_parts"] > 1 and info["n_part_items"] > 0  # the part plan is the one timed
+    y = tfg.tfg_aggregate(None, dev(x), n, "sum",
                           edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
     deg = host(cnt)
     rows = np.unique(np.concatenate([np.argsort(deg)[-40:], np.argsort(deg)[:20],
@@ -157,6 +165,15 @@ def test_power_law_full_size(tfg, orc):
     rel = (ys - s).abs() / s
     assert float(rel.max()) <= 1e-5
     # determinism
-    y2 = tfg.tfg_aggregate(norm["edge_index"], dev(x), n, "sum",
+    y2 = tfg.tfg_aggregate(None, dev(x), n, "sum",
                            edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
     assert torch.equal(y, y2)
+    # the row plan on the same graph agrees within the tolerance
+    import os
+    os.environ["TFG_PART_PLAN"] = "0"
+    try:
+        y3 = tfg.tfg_aggregate(None, dev(x), n, "sum",
+                               edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    finally:
+        del os.environ["TFG_PART_PLAN"]
+    assert_scaled(host(y3)[rows], ref, S, what="c4 sampled rows, row plan")

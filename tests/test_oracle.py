@@ -58,6 +58,24 @@ def test_csr_is_numpy_stable_argsort(orc, seed, n, e):
     assert rowptr[0] == 0 and rowptr[-1] == e
 
 
+@pytest.mark.parametrize("seed,n,n_src,e,parts", [(5, 40, 40, 3000, 2), (6, 300, 77, 9000, 3),
+                                                 (7, 1000, 5000, 20000, 8), (8, 9, 9, 50, 9)])
+def test_csr_by_source_part_is_numpy_stable_argsort(orc, seed, n, n_src, e, parts):
+    ei = graphgen.random_graph(seed, n, e, n_src=n_src)
+    rowptr, col, perm, seg = orc.csr_by_target(ei, n, parts=parts, n_src=n_src)
+    part_rows = -(-n_src // parts)
+    key = ei[1] * parts + ei[0] // part_rows
+    ref = np.argsort(key, kind="stable")
+    np.testing.assert_array_equal(perm, ref)
+    np.testing.assert_array_equal(col, ei[0][ref])
+    np.testing.assert_array_equal(np.diff(seg), np.bincount(key, minlength=n * parts))
+    # rows are the same as in the plain CSR; only the order inside a row changes
+    r1, _, p1 = orc.csr_by_target(ei, n, n_src=n_src)
+    np.testing.assert_array_equal(rowptr, r1)
+    for t in range(0, n, max(1, n // 17)):
+        assert sorted(perm[rowptr[t]:rowptr[t + 1]]) == list(p1[r1[t]:r1[t + 1]])
+
+
 def test_csr_brute_force_tiny(orc):
     ei = graphgen.random_graph(11, 6, 25)
     rowptr, col, perm = orc.csr_by_target(ei, 6)

@@ -66,22 +66,39 @@ def same_bits(a, b):
 # COO -> CSR
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("n,e,loops,idx", [
-    (1, 7, False, np.int64),            # N = 1: a single row
-    (300, 50_000, False, np.int32),     # one radix pass (9 bits), 13 tiles + ragged tail
-    (5_000, 70_001, True, np.int64),    # two passes, loops appended
-    (300_000, 40_000, False, np.int32),  # three passes (19 bits), mostly empty rows
-    (1000, 0, True, np.int32),          # no input edges: loops only
+@pytest.mark.parametrize("n,e,loops,idx,parts", [
+    (1, 7, False, np.int64, 1),            # N = 1: a single row
+    (300, 50_000, False, np.int32, 1),     # one radix pass (9 bits), 7 tiles + ragged tail
+    (5_000, 70_001, True, np.int64, 1),    # two passes, loops appended
+    (300_000, 40_000, False, np.int32, 1),  # three passes (19 bits), mostly empty rows
+    (1000, 0, True, np.int32, 1),          # no input edges: loops only
+    (2000, 90_000, True, np.int32, 8),     # source parts: key (target, part), 3 + 11 bits
+    (300, 50_000, False, np.int64, 3),     # parts that do not divide N
+    (70_000, 200_000, False, np.int32, 16),  # 21-bit keys: three passes
 ])
-def test_csr_bit_exact(tfg, n, e, loops, idx):
+def test_csr_bit_exact(tfg, orc, n, e, loops, idx, parts):
     ei = graphgen.random_graph(e + n, n, e, hub=n // 2, hub_edges=e // 4)
-    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=loops)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=loops, src_parts=parts)
+    assert g.info()["src_parts"] == min(parts, n)
     rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
     full = ei
     if loops:
         full = np.concatenate([ei, np.stack([np.arange(n), np.arange(n)])], axis=1)
-    r, c, p = __import__("oracle").csr_by_target(full, n)
+    ref = orc.csr_by_target(full, n, parts=min(parts, n))
+    r, c, p = ref[:3]
     assert np.array_equal(rowptr, r) and np.array_equal(perm, p) and np.array_equal(col, c)
+    if parts > 1:
+        assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
+
+
+def test_auto_parts(tfg):
+    # small source table: one part; large table with long rows: several
+    ei = graphgen.random_graph(3, 1000, 20_000)
+    assert tfg.tfg_graph_create(dev(ei), 1000).info()["src_parts"] == 1
+    n = 70_000
+    ei = graphgen.random_graph(4, n, 64 * n)  # 35.8 MB of 512-byte rows, average degree 64
+    info = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n).info()
+    assert info["src_parts"] == 3 and info["n_part_items"] > 0
 
 
 def test_csr_rejects_out_of_range(tfg):
@@ -97,19 +114,20 @@ def test_csr_rejects_out_of_range(tfg):
 # GCN normalisation
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("weighted,idx", [(False, np.int32), (True, np.int64)])
-def test_gcn_norm_bit_exact(tfg, orc, weighted, idx):
+@pytest.mark.parametrize("weighted,idx,parts", [(False, np.int32, 1), (True, np.int64, 1),
+                                                (True, np.int32, 6)])
+def test_gcn_norm_bit_exact(tfg, orc, weighted, idx, parts):
     n, e = 4000, 60_000
     ei = graphgen.random_graph(21, n, e, hub=3, hub_edges=5000)  # duplicates, loops, a hub
     w = (np.random.default_rng(3).uniform(0.1, 3.0, ei.shape[1]).astype(np.float32)
          if weighted else None)
-    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=True)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=True, src_parts=parts)
     r = tfg.tfg_gcn_norm(dev(ei.astype(idx)), n, edge_weight=None if w is None else dev(w), graph=g)
     oei, ow, odeg = orc.gcn_norm(ei, n, edge_weight=w)
     assert np.array_equal(host(r["edge_index"]), oei)
     assert same_bits(host(r["deg"]), odeg)
     assert same_bits(host(r["edge_weight"]), ow)
-    _, _, perm = orc.csr_by_target(oei, n)
+    perm = orc.csr_by_target(oei, n, parts=parts)[2]
     assert same_bits(host(r["edge_weight_csr"]), ow[perm])
     # functional path without a handle gives the same bits
     r2 = tfg.tfg_gcn_norm(dev(ei.astype(idx)), n, edge_weight=None if w is None else dev(w))
@@ -151,6 +169,34 @@ def test_aggregate(tfg, orc, n_src, n, e, F, ldx, H, reduce):
     else:
         ref, S = orc.aggregate(ei, x, n, reduce, edge_weight=w, heads=H)
         assert_scaled(host(res), ref, S, what=f"{reduce} F={F}")
+
+
+@pytest.mark.parametrize("F,H", [(128, 1), (64, 1), (32, 4), (5, 1)])
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+@pytest.mark.parametrize("plan", ["0", "1"])
+def test_aggregate_source_parts(tfg, orc, monkeypatch, F, H, reduce, plan):
+    """Graphs ordered by (target, source part); the part plan (partials per
+    source part, reduced in part order) and the row plan on the same graph."""
+    monkeypatch.setenv("TFG_PART_PLAN", plan)
+    n, e, parts = 1500, 60_000, 5
+    ei = graphgen.random_graph(F + H, n, e, hub=17, hub_edges=9000)
+    E = ei.shape[1]
+    x = graphgen.features(F, n, F)
+    w = np.random.default_rng(F).standard_normal((E, H) if H > 1 else E).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n, src_parts=parts)
+    assert g.info()["n_part_items"] > 0
+    _, _, perm, _ = orc.csr_by_target(ei, n, parts=parts)
+    res = tfg.tfg_aggregate(None, dev(x), n, reduce, edge_weight=dev(w[perm]), heads=H,
+                            weight_order="csr", graph=g)
+    coo = tfg.tfg_aggregate(dev(ei), dev(x), n, reduce, edge_weight=dev(w), heads=H, graph=g)
+    if reduce == "max":
+        ref, refarg = orc.aggregate(ei, x, n, "max", edge_weight=w, heads=H)
+        assert same_bits(host(res[0]), ref) and np.array_equal(host(res[1]), refarg)
+        assert same_bits(host(coo[0]), ref) and np.array_equal(host(coo[1]), refarg)
+    else:
+        ref, S = orc.aggregate(ei, x, n, reduce, edge_weight=w, heads=H)
+        assert_scaled(host(res), ref, S, what=f"{reduce} parts plan={plan}")
+        assert same_bits(host(res), host(coo))
 
 
 @pytest.mark.parametrize("reduce", ["sum", "max"])
@@ -229,17 +275,17 @@ def test_gat_scores(tfg, orc, H, D):
     assert_scaled(s, ref, S, what="gat scores")
 
 
-@pytest.mark.parametrize("H", [1, 8, 3])
-def test_segment_softmax(tfg, orc, H):
+@pytest.mark.parametrize("H,parts", [(1, 1), (8, 1), (3, 1), (8, 4)])
+def test_segment_softmax(tfg, orc, H, parts):
     n, e = 5000, 80_000
     ei = graphgen.random_graph(H, n, e, hub=2, hub_edges=6000)
     E = ei.shape[1]
     s = (graphgen.features(77, E, H) * 6).astype(np.float32)
-    g = tfg.tfg_graph_create(dev(ei), n)
+    g = tfg.tfg_graph_create(dev(ei), n, src_parts=parts)
     out, out_csr = tfg.tfg_segment_softmax(dev(s), dev(ei[1]), n, graph=g, out_csr=True)
     ref64, _ = orc.segment_softmax(s, ei[1], n)
     assert_rel(host(out), ref64, what="softmax")
-    _, _, perm = orc.csr_by_target(ei, n)
+    perm = orc.csr_by_target(ei, n, parts=parts)[2]
     assert same_bits(host(out_csr), host(out)[perm])
     plain = tfg.tfg_segment_softmax(dev(s), dev(ei[1]), n)  # no handle
     assert same_bits(host(plain), host(out))
