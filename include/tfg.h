@@ -208,6 +208,26 @@ int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float
                   int32_t *argmax, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Multi-step propagation                                                    */
+/* ------------------------------------------------------------------------ */
+/*
+ * K propagation steps over a square graph (SGC and APPNP, Sec. 2.2):
+ *   Z_0 = x,  Z_{k+1} = (1 - alpha) * A Z_k + alpha * h  (k < K),  out = Z_K
+ * where (A Z)[t] = sum over the edges e entering t of w_e * Z[src_e] (the sum
+ * aggregation of tfg_aggregate). SGC: alpha = 0 (h unused, may be NULL);
+ * APPNP: 0 < alpha <= 1 with h = the initial predictions (often x).
+ * g: a graph with N_src == N; edge_weight: NULL (all ones) or [E'] in
+ * weight_order (TFG_CSR: the graph order, e.g. tfg_gcn_norm's CSR output).
+ * x: [N, F] (leading dimension ldx); h: [N, F] (leading dimension ldh);
+ * out: [N, F]. out must not overlap x or h. Every step is one aggregation
+ * launch whose epilogue applies the update; K = 0 copies x.
+ */
+size_t tfg_propagate_ws_bytes(const tfg_graph *g, int64_t F, int64_t K);
+int tfg_propagate(const tfg_graph *g, const float *edge_weight, int weight_order, const float *x,
+                  int64_t F, int64_t ldx, int64_t K, float alpha, const float *h, int64_t ldh,
+                  float *out, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Attention: edge scores and segment softmax                               */
 /* ------------------------------------------------------------------------ */
 /*
@@ -238,6 +258,24 @@ int tfg_segment_softmax(const float *scores, int64_t E, int64_t H, const void *s
                         int index_type, int64_t N, const tfg_graph *g, float *out,
                         float *out_csr, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
+/*
+ * Fused attention aggregation: the whole GAT workflow of Fig. 5(a) plus the
+ * weighted message aggregation in one pass over the graph, without writing
+ * the [E, H] scores or coefficients:
+ *   s[e, k]     = LeakyReLU(a_src[k] . h[src_e, k] + a_dst[k] . h[tgt_e, k], slope)
+ *   alpha[e, k] = softmax of s[., k] over the edges entering tgt_e
+ *   out[t, k*D + d] = sum over the edges e entering t of alpha[e, k] h[src_e, k*D + d]
+ * Equal (up to rounding) to tfg_gat_edge_scores -> tfg_segment_softmax ->
+ * tfg_aggregate with per-head weights. g: a square graph (N_src == N);
+ * h: [N, H*D]; a_src, a_dst: [H, D]; H <= 64; out: [N, H*D] (a target
+ * without edges gets 0). alpha_out: NULL, or [E', H] to also receive alpha in
+ * the caller's edge order (edge ids as in the graph, loops included).
+ */
+size_t tfg_gat_aggregate_ws_bytes(int64_t N, int64_t H);
+int tfg_gat_aggregate(const tfg_graph *g, const float *h, int64_t H, int64_t D,
+                      const float *a_src, const float *a_dst, float slope, float *out,
+                      float *alpha_out, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Graph pooling                                                             */
 /* ------------------------------------------------------------------------ */
@@ -256,6 +294,30 @@ size_t tfg_segment_pool_ws_bytes(int64_t Nb, int64_t G);
 int tfg_segment_pool(const float *x, int64_t Nb, int64_t F, int64_t ldx, const void *graph_index,
                      int index_type, int64_t G, int reduce, float *out, int32_t *argmax,
                      int validate, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* BatchGraph construction                                                   */
+/* ------------------------------------------------------------------------ */
+/*
+ * Combines G graphs into one BatchGraph (Sec. 2.1.1, Fig. 4): node j of graph
+ * i gets the id j + (number of nodes in graphs 0..i-1), every local edge is
+ * shifted by its graph's offset, and node_graph_index[n] is the graph of node
+ * n (non-decreasing). Node features need no change: they are the per-graph
+ * rows stacked in graph order.
+ * node_counts, edge_counts: [G] (index_type); local_edge_index: [2, E] with
+ * the edges of graph 0, then graph 1, ... (row 0 sources, row 1 targets, ids
+ * local to their graph); E = sum of edge_counts, Nb = sum of node_counts.
+ * Outputs: out_edge_index [2, E] and out_graph_index [Nb] (index_type);
+ * out_node_offsets / out_edge_offsets: NULL or [G + 1] int32.
+ * validate != 0: synchronise and return TFG_ERR_INDEX_RANGE if a count is
+ * negative, a local id is outside its graph, or E / Nb differ from the sums.
+ */
+size_t tfg_batch_graphs_ws_bytes(int64_t G);
+int tfg_batch_graphs(int64_t G, const void *node_counts, const void *edge_counts,
+                     const void *local_edge_index, int index_type, int64_t E, int64_t Nb,
+                     void *out_edge_index, void *out_graph_index, int32_t *out_node_offsets,
+                     int32_t *out_edge_offsets, int validate, void *ws, size_t ws_bytes,
+                     tfg_stream_t stream);
 
 #ifdef __cplusplus
 }

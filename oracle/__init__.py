@@ -51,8 +51,11 @@ def lib():
         _lib.orc_aggregate_rows.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, ctypes.c_int,
                                             p, i64, p, p, p, p]
         _lib.orc_segment_softmax.argtypes = [i64, i64, p, p, i64, p, p]
+        _lib.orc_propagate.argtypes = [i64, p, p, p, p, i64, i64, i64, i64, ctypes.c_double, p,
+                                       p, p]
         _lib.orc_segment_pool.argtypes = [i64, i64, i64, p, p, i64, ctypes.c_int, p, p, p, p]
         _lib.orc_gat_scores.argtypes = [i64, p, p, p, i64, i64, i64, p, p, ctypes.c_float, p, p]
+        _lib.orc_gat_layer.argtypes = [i64, p, p, p, i64, i64, i64, p, p, ctypes.c_float, p, p, p]
         _lib.orc_batch_offsets.argtypes = [i64, p, p]
         _lib.orc_batch_offsets.restype = None
         _lib.orc_batch_graphs.argtypes = [i64, p, p, p, p, p, p]
@@ -158,6 +161,22 @@ def aggregate(edge_index, x, n, reduce="sum", edge_weight=None, heads=1, rows=No
     return (outf, arg) if red == MAX else (out64, scale)
 
 
+def propagate(edge_index, x, K, alpha=0.0, h=None, edge_weight=None):
+    """Z_K of Z_{k+1} = (1 - alpha) A Z_k + alpha h, Z_0 = x: (out64 [N,F], scale [N,F])."""
+    ei = _i64(edge_index)
+    x, ldx = _rows(x)
+    N, F = x.shape
+    hh = None if h is None else np.ascontiguousarray(h, dtype=np.float32).reshape(N, F)
+    src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
+    w = _f32(edge_weight)
+    out64 = np.empty((N, F), np.float64)
+    scale = np.empty((N, F), np.float64)
+    _check(lib().orc_propagate(ei.shape[1], _ptr(src), _ptr(tgt), _ptr(w),
+                               x.ctypes.data_as(ctypes.c_void_p), ldx, N, F, K, float(alpha),
+                               _ptr(hh), _ptr(out64), _ptr(scale)))
+    return out64, scale
+
+
 def segment_softmax(scores, seg, n):
     """Per-segment softmax of float32 scores [E,H] (or [E]) -> (out64, out32)."""
     s = np.ascontiguousarray(scores, dtype=np.float32)
@@ -204,6 +223,24 @@ def gat_scores(edge_index, h, a_src, a_dst, heads, slope=0.2):
     _check(lib().orc_gat_scores(E, _ptr(src), _ptr(tgt), _ptr(h), N, heads, D, _ptr(a_src),
                                 _ptr(a_dst), float(slope), _ptr(out64), _ptr(scale)))
     return out64, scale
+
+
+def gat_layer(edge_index, h, a_src, a_dst, heads, slope=0.2):
+    """Attention layer after the projection: (out64 [N, H*D], alpha64 [E, H], scale [N, H*D])."""
+    ei = _i64(edge_index)
+    h = np.ascontiguousarray(h, dtype=np.float32)
+    N = h.shape[0]
+    D = h.shape[1] // heads
+    a_src = np.ascontiguousarray(a_src, dtype=np.float32).reshape(heads, D)
+    a_dst = np.ascontiguousarray(a_dst, dtype=np.float32).reshape(heads, D)
+    E = ei.shape[1]
+    src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
+    out64 = np.empty((N, heads * D), np.float64)
+    alpha = np.empty((E, heads), np.float64)
+    scale = np.empty((N, heads * D), np.float64)
+    _check(lib().orc_gat_layer(E, _ptr(src), _ptr(tgt), _ptr(h), N, heads, D, _ptr(a_src),
+                               _ptr(a_dst), float(slope), _ptr(out64), _ptr(alpha), _ptr(scale)))
+    return out64, alpha, scale
 
 
 def batch_offsets(sizes):

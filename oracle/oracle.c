@@ -211,6 +211,53 @@ int orc_aggregate_rows(int64_t E, const int64_t *src, const int64_t *tgt, const 
 }
 
 /*
+ * K-step propagation (SGC and APPNP, Sec. 2.2): Z_0 = x and
+ *   Z_{k+1} = (1 - alpha) * A Z_k + alpha * h,   (A Z)[t] = sum over edges e -> t of w_e Z[src_e]
+ * for k < K; out64 = Z_K, all in double (h may be NULL when alpha == 0).
+ * scale receives the same recurrence on absolute values (|w|, |x|, |h|,
+ * |1 - alpha|, |alpha|): the size of the terms behind every output.
+ */
+int orc_propagate(int64_t E, const int64_t *src, const int64_t *tgt, const float *w,
+                  const float *x, int64_t ldx, int64_t N, int64_t F, int64_t K, double alpha,
+                  const float *h, double *out64, double *scale)
+{
+    if (alpha != 0.0 && h == NULL)
+        return ORC_ERR_INVALID_ARG;
+    for (int64_t e = 0; e < E; ++e)
+        if (src[e] < 0 || src[e] >= N || tgt[e] < 0 || tgt[e] >= N)
+            return ORC_ERR_INDEX_RANGE;
+    size_t n = (size_t)(N * F > 0 ? N * F : 1);
+    double *z = (double *)malloc(n * sizeof(double)), *s = (double *)malloc(n * sizeof(double));
+    double *y = (double *)malloc(n * sizeof(double)), *sy = (double *)malloc(n * sizeof(double));
+    for (int64_t i = 0; i < N; ++i)
+        for (int64_t c = 0; c < F; ++c) {
+            z[i * F + c] = (double)x[i * ldx + c];
+            s[i * F + c] = fabs((double)x[i * ldx + c]);
+        }
+    for (int64_t k = 0; k < K; ++k) {
+        memset(y, 0, n * sizeof(double));
+        memset(sy, 0, n * sizeof(double));
+        for (int64_t e = 0; e < E; ++e) {
+            double we = w ? (double)w[e] : 1.0;
+            for (int64_t c = 0; c < F; ++c) {
+                y[tgt[e] * F + c] += we * z[src[e] * F + c];
+                sy[tgt[e] * F + c] += fabs(we) * s[src[e] * F + c];
+            }
+        }
+        for (int64_t i = 0; i < N * F; ++i) {
+            double hv = h ? (double)h[i] : 0.0;
+            z[i] = (1.0 - alpha) * y[i] + alpha * hv;
+            s[i] = fabs(1.0 - alpha) * sy[i] + fabs(alpha) * fabs(hv);
+        }
+    }
+    memcpy(out64, z, (size_t)(N * F) * sizeof(double));
+    if (scale)
+        memcpy(scale, s, (size_t)(N * F) * sizeof(double));
+    free(z); free(s); free(y); free(sy);
+    return ORC_OK;
+}
+
+/*
  * Segment softmax, the map -> reduce -> map workflow of Fig. 5(a), Sec. 2.1.2:
  * for every segment t (the edges with seg[e] = t) and head h,
  *   alpha[e, h] = exp(s[e, h] - m) / sum over the segment of exp(s - m)
@@ -341,6 +388,49 @@ int orc_gat_scores(int64_t E, const int64_t *src, const int64_t *tgt, const floa
     }
     free(as); free(ad); free(as_abs); free(ad_abs);
     return ORC_OK;
+}
+
+/*
+ * A GAT attention layer after the projection: the map -> reduce -> map
+ * workflow of Fig. 5(a) followed by the weighted message aggregation.
+ *   1. scores s[e, k] as orc_gat_scores, rounded to float32 (the map's output);
+ *   2. alpha[e, k] = softmax of s over the edges entering tgt_e (per head);
+ *   3. out[t, k*D + d] = sum over the edges e entering t of alpha[e, k] h[src_e, k*D + d].
+ * Steps 2 and 3 in double. alpha64 ([E, H], may be NULL) receives alpha;
+ * scale[t, c] the sum of |alpha h| (the size of the terms).
+ */
+int orc_gat_layer(int64_t E, const int64_t *src, const int64_t *tgt, const float *h, int64_t N,
+                  int64_t H, int64_t D, const float *a_src, const float *a_dst, float slope,
+                  double *out64, double *alpha64, double *scale)
+{
+    int64_t F = H * D;
+    double *s64 = (double *)malloc((size_t)(E * H > 0 ? E * H : 1) * sizeof(double));
+    float *s32 = (float *)malloc((size_t)(E * H > 0 ? E * H : 1) * sizeof(float));
+    double *al = (double *)malloc((size_t)(E * H > 0 ? E * H : 1) * sizeof(double));
+    int rc = orc_gat_scores(E, src, tgt, h, N, H, D, a_src, a_dst, slope, s64, NULL);
+    if (rc == ORC_OK) {
+        for (int64_t i = 0; i < E * H; ++i)
+            s32[i] = (float)s64[i];
+        rc = orc_segment_softmax(E, H, s32, tgt, N, al, NULL);
+    }
+    if (rc == ORC_OK) {
+        memset(out64, 0, (size_t)(N * F) * sizeof(double));
+        if (scale)
+            memset(scale, 0, (size_t)(N * F) * sizeof(double));
+        for (int64_t e = 0; e < E; ++e)
+            for (int64_t c = 0; c < F; ++c) {
+                double m = al[e * H + c / D] * (double)h[src[e] * F + c];
+                out64[tgt[e] * F + c] += m;
+                if (scale)
+                    scale[tgt[e] * F + c] += fabs(m);
+            }
+        if (alpha64)
+            memcpy(alpha64, al, (size_t)(E * H) * sizeof(double));
+    }
+    free(s64);
+    free(s32);
+    free(al);
+    return rc;
 }
 
 /*

@@ -20,6 +20,7 @@ __all__ = [
     "TfgError", "Graph", "tfg_graph_create", "tfg_graph_csr", "tfg_graph_segments", "tfg_check",
     "tfg_gcn_norm",
     "tfg_aggregate", "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_pool",
+    "tfg_batch_graphs", "tfg_propagate", "tfg_gat_aggregate",
     "library_path", "load",
 ]
 
@@ -87,6 +88,12 @@ def load():
         "tfg_segment_softmax": (ci, [p, i64, i64, p, ci, i64, p, p, p, p, sz, p]),
         "tfg_segment_pool_ws_bytes": (sz, [i64, i64]),
         "tfg_segment_pool": (ci, [p, i64, i64, i64, p, ci, i64, ci, p, p, ci, p, sz, p]),
+        "tfg_batch_graphs_ws_bytes": (sz, [i64]),
+        "tfg_propagate_ws_bytes": (sz, [p, i64, i64]),
+        "tfg_gat_aggregate_ws_bytes": (sz, [i64, i64]),
+        "tfg_gat_aggregate": (ci, [p, p, i64, i64, p, p, ctypes.c_float, p, p, p, sz, p]),
+        "tfg_propagate": (ci, [p, p, ci, p, i64, i64, i64, ctypes.c_float, p, i64, p, p, sz, p]),
+        "tfg_batch_graphs": (ci, [i64, p, p, p, ci, i64, i64, p, p, p, p, ci, p, sz, p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -387,3 +394,79 @@ def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce:
     _check(lib.tfg_segment_pool(_ptr(x), Nb, F, ldx, _ptr(gi), _index_type(gi), G, red, _ptr(out),
                                 _ptr(arg), int(validate), _ptr(ws), ws.numel(), _stream(dev)))
     return (out, arg) if red == 2 else out
+
+
+def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
+                     local_edge_index: torch.Tensor, Nb: int | None = None,
+                     validate: bool = True):
+    """BatchGraph of G graphs: (edge_index [2, E], graph_index [Nb], node_offsets [G+1],
+    edge_offsets [G+1]). local_edge_index holds graph 0's edges, then graph 1's, ...,
+    with ids local to their graph; Nb defaults to node_counts.sum() (one host read)."""
+    lib = load()
+    nc = _dev(node_counts, "node_counts").contiguous()
+    ec = _dev(edge_counts, "edge_counts").contiguous()
+    ei = _edges(local_edge_index)
+    if nc.dtype != ei.dtype or ec.dtype != ei.dtype:
+        raise TypeError("counts and edge_index must share one index dtype")
+    G, E = nc.shape[0], ei.shape[1]
+    if Nb is None:
+        Nb = int(nc.sum().item())
+    dev = ei.device
+    out_ei = torch.empty_like(ei)
+    gi = torch.empty(Nb, dtype=ei.dtype, device=dev)
+    noff = torch.empty(G + 1, dtype=torch.int32, device=dev)
+    eoff = torch.empty(G + 1, dtype=torch.int32, device=dev)
+    ws = _workspace(lib.tfg_batch_graphs_ws_bytes(G), dev)
+    _check(lib.tfg_batch_graphs(G, _ptr(nc), _ptr(ec), _ptr(ei), _index_type(ei), E, Nb,
+                                _ptr(out_ei), _ptr(gi), _ptr(noff), _ptr(eoff), int(validate),
+                                _ptr(ws), ws.numel(), _stream(dev)))
+    return out_ei, gi, noff, eoff
+
+
+def tfg_propagate(graph: Graph, x: torch.Tensor, K: int, alpha: float = 0.0,
+                  h: torch.Tensor | None = None, edge_weight: torch.Tensor | None = None,
+                  weight_order: str = "csr", out: torch.Tensor | None = None,
+                  ws: torch.Tensor | None = None):
+    """K steps of Z <- (1 - alpha) A Z + alpha h from Z = x (SGC: alpha = 0;
+    APPNP: h = x). edge_weight in graph order by default (tfg_gcn_norm's
+    ``edge_weight_csr``)."""
+    lib = load()
+    x, ldx = _rows(x, "x")
+    N, F = x.shape
+    w = _f32(edge_weight, "edge_weight")
+    ldh = 0
+    if h is not None:
+        h, ldh = _rows(h, "h")
+    if out is None:
+        out = torch.empty((N, F), dtype=torch.float32, device=x.device)
+    need = lib.tfg_propagate_ws_bytes(graph.handle, F, K)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, x.device)
+    _check(lib.tfg_propagate(graph.handle, _ptr(w), _ORDER[weight_order], _ptr(x), F, ldx, K,
+                             float(alpha), _ptr(h), ldh, _ptr(out), _ptr(ws), ws.numel(),
+                             _stream(x.device)))
+    return out
+
+
+def tfg_gat_aggregate(graph: Graph, h: torch.Tensor, a_src: torch.Tensor, a_dst: torch.Tensor,
+                      slope: float = 0.2, want_alpha: bool = False,
+                      out: torch.Tensor | None = None):
+    """Fused attention layer after the projection: out [N, H*D] (and alpha
+    [E', H] in the graph's edge order when ``want_alpha``)."""
+    lib = load()
+    h = _f32(h, "h")
+    a_src, a_dst = _f32(a_src, "a_src"), _f32(a_dst, "a_dst")
+    H = a_src.shape[0]
+    D = a_src.numel() // H
+    N = h.shape[0]
+    if h.shape[1] != H * D or a_dst.shape != a_src.shape:
+        raise ValueError("h must be [N, H*D] and a_src, a_dst [H, D]")
+    if out is None:
+        out = torch.empty((N, H * D), dtype=torch.float32, device=h.device)
+    alpha = torch.empty((graph.E, H), dtype=torch.float32, device=h.device) if want_alpha else None
+    ws = _workspace(lib.tfg_gat_aggregate_ws_bytes(N, H), h.device)
+    _check(lib.tfg_gat_aggregate(graph.handle, _ptr(h), H, D, _ptr(a_src), _ptr(a_dst),
+                                 float(slope), _ptr(out), _ptr(alpha), _ptr(ws), ws.numel(),
+                                 _stream(h.device)))
+    return (out, alpha) if want_alpha else out
+

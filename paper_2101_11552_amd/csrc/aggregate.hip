@@ -73,6 +73,27 @@ __device__ __forceinline__ float bcastf(float v, int jbase, int slot) {
   return __int_as_float(bcast<SLOTS>(__float_as_int(v), jbase, slot));
 }
 
+// Output transform of a propagation step: y = scale * sum + alpha * h[row]
+// (APPNP, SGC); the identity (scale 1, no h) for a plain aggregation.
+struct Epilogue {
+  float scale, alpha;
+  const float* h;
+  int64_t ldh;
+};
+
+template <int V>
+__device__ __forceinline__ void apply_epilogue(const Epilogue& ep, int row, int f, float (&v)[V]) {
+  if (ep.h != nullptr) {
+    float t[V];
+    load_row<V>(ep.h + (int64_t)row * ep.ldh + f, t);
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = ep.scale * v[i] + ep.alpha * t[i];
+  } else if (ep.scale != 1.0f) {
+#pragma unroll
+    for (int i = 0; i < V; ++i) v[i] = ep.scale * v[i];
+  }
+}
+
 // Max with the smallest edge id winning ties; arg < 0 marks "no edge yet".
 __device__ __forceinline__ void max_combine(float& v, int& a, float vb, int ab) {
   bool take = ab >= 0 && (a < 0 || vb > v || (vb == v && ab < a));
@@ -94,7 +115,7 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
     int n_light, const int* __restrict__ col, const int* __restrict__ perm,
     const float* __restrict__ w, int w_by_perm, int H, int per_head, const float* __restrict__ x,
     int64_t ldx, int F, int mean, float* __restrict__ out, int* __restrict__ argout,
-    float* __restrict__ part, int* __restrict__ part_arg) {
+    float* __restrict__ part, int* __restrict__ part_arg, Epilogue ep) {
   constexpr int LPS = kWave / SLOTS;  // lanes per edge slot
   constexpr int FC = LPS * V;         // feature columns per pass
   constexpr int U = unroll_for<SLOTS, SHORT>();
@@ -217,6 +238,7 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
           for (int v = 0; v < V; ++v)
             if (arg[0][v] < 0) acc[0][v] = 0.0f;
         }
+        if (!MAX) apply_epilogue<V>(ep, row, f, acc[0]);
         store_row<V>(out + (int64_t)row * F + f, acc[0]);
         if (MAX && argout != nullptr)
 #pragma unroll
@@ -241,7 +263,7 @@ __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict_
                                                      int n_split, const float* __restrict__ part,
                                                      const int* __restrict__ part_arg, int F,
                                                      int mean, float* __restrict__ out,
-                                                     int* __restrict__ argout) {
+                                                     int* __restrict__ argout, Epilogue ep) {
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_split) return;
   const int lane = threadIdx.x & (kWave - 1);
@@ -288,6 +310,7 @@ __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict_
         s[v] = (a4[0][v] + a4[1][v]) + (a4[2][v] + a4[3][v]);
         if (mean && deg > 0) s[v] = s[v] / (float)deg;
       }
+      apply_epilogue<V>(ep, row, f, s);
       store_row<V>(out + (int64_t)row * F + f, s);
     }
   }
@@ -310,13 +333,14 @@ struct RowArgs {
   int* argout;
   float* part;
   int* part_arg;
+  Epilogue ep;
 };
 
 template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT>
 void launch_rows(dim3 grid, hipStream_t s, const RowArgs& a) {
   spmm_rows<V, SLOTS, MAX, HEADS, SHORT><<<grid, dim3(kBlock), 0, s>>>(
       a.heavy, a.n_heavy, a.light, a.n_light, a.col, a.perm, a.w, a.w_by_perm, a.H, a.per_head,
-      a.x, a.ldx, a.F, a.mean, a.out, a.argout, a.part, a.part_arg);
+      a.x, a.ldx, a.F, a.mean, a.out, a.argout, a.part, a.part_arg, a.ep);
 }
 
 template <int V, bool MAX, bool HEADS, bool SHORT>
@@ -371,7 +395,7 @@ bool use_part_plan(const Graph& g, int64_t F) {
 
 int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
                      int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax, void* ws,
-                     hipStream_t s) {
+                     hipStream_t s, float scale, float alpha, const float* h, int64_t ldh) {
   if (g.N == 0 || F == 0) return TFG_OK;
   const bool heads = H > 1 && w != nullptr;
   const int per_head = (int)(F / H);
@@ -400,6 +424,7 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   a.mean = reduce == TFG_MEAN;
   a.out = out;
   a.argout = argmax;
+  a.ep = Epilogue{scale, alpha, h, ldh};
   const int n_partials = part_plan ? g.n_pexec : g.n_heavy;
   a.part = static_cast<float*>(ws);
   a.part_arg = reinterpret_cast<int*>(a.part + (size_t)std::max(n_partials, 1) * F);
@@ -436,13 +461,13 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
     const bool f4 = F % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
     if (mx)
       fixup_rows<true, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
-                                                         a.mean, out, argmax);
+                                                         a.mean, out, argmax, a.ep);
     else if (f4)
       fixup_rows<false, 4><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
-                                                          a.mean, out, argmax);
+                                                          a.mean, out, argmax, a.ep);
     else
       fixup_rows<false, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
-                                                          a.mean, out, argmax);
+                                                          a.mean, out, argmax, a.ep);
     TFG_LAUNCHED("fixup_rows");
   }
   return TFG_OK;

@@ -433,4 +433,123 @@ int tfg_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const v
   return TFG_OK;
 }
 
+size_t tfg_batch_graphs_ws_bytes(int64_t G) { return G < 0 ? 0 : batch_ws_bytes(G); }
+
+int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,
+                     const void* local_edge_index, int index_type, int64_t E, int64_t Nb,
+                     void* out_edge_index, void* out_graph_index, int32_t* out_node_offsets,
+                     int32_t* out_edge_offsets, int validate, void* ws, size_t ws_bytes,
+                     tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E, Nb, 0);
+  if (rc) return rc;
+  if (G < 0 || G >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad G");
+  if (G == 0 && (E > 0 || Nb > 0)) return fail(TFG_ERR_INVALID_ARG, "edges or nodes without graphs");
+  if (G > 0 && (node_counts == nullptr || edge_counts == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL counts");
+  if ((E > 0 && (local_edge_index == nullptr || out_edge_index == nullptr)) ||
+      (Nb > 0 && out_graph_index == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (ws == nullptr || ws_bytes < batch_ws_bytes(G))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  Carver c(ws, ws_bytes);
+  int* node_off = static_cast<int*>(c.take(sizeof(int) * (size_t)(G + 1)));
+  int* edge_off = static_cast<int*>(c.take(sizeof(int) * (size_t)(G + 1)));
+  int* sums = static_cast<int*>(c.take(sizeof(int) * (size_t)std::max<int64_t>((G + 1 + 2047) / 2048, 1)));
+  int* err = static_cast<int*>(c.take(sizeof(int)));
+  if (G == 0) return TFG_OK;
+  rc = launch_batch_graphs(G, node_counts, edge_counts, local_edge_index, index_type, E, Nb,
+                           out_edge_index, out_graph_index, node_off, edge_off, sums, err, s);
+  if (rc) return rc;
+  if (out_node_offsets)
+    TFG_HIP(hipMemcpyAsync(out_node_offsets, node_off, sizeof(int) * (G + 1),
+                           hipMemcpyDeviceToDevice, s));
+  if (out_edge_offsets)
+    TFG_HIP(hipMemcpyAsync(out_edge_offsets, edge_off, sizeof(int) * (G + 1),
+                           hipMemcpyDeviceToDevice, s));
+  if (validate) {
+    int host[3] = {0, 0, 0};
+    TFG_HIP(hipMemcpyAsync(&host[0], err, sizeof(int), hipMemcpyDeviceToHost, s));
+    TFG_HIP(hipMemcpyAsync(&host[1], node_off + G, sizeof(int), hipMemcpyDeviceToHost, s));
+    TFG_HIP(hipMemcpyAsync(&host[2], edge_off + G, sizeof(int), hipMemcpyDeviceToHost, s));
+    TFG_HIP(hipStreamSynchronize(s));
+    if (host[0] & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "a count or local id is out of range");
+    if (host[1] != Nb || host[2] != E)
+      return fail(TFG_ERR_INDEX_RANGE, "node / edge counts do not add up to Nb / E");
+  }
+  return TFG_OK;
+}
+
+size_t tfg_propagate_ws_bytes(const tfg_graph* g, int64_t F, int64_t K) {
+  if (!g || F < 0 || K < 0) return 0;
+  const Graph& gr = g->g;
+  size_t b = aggregate_partial_bytes(partials_needed(gr.E, gr.N, gr.N_src, F, g), F, TFG_SUM);
+  if (K >= 2) b += align_up(sizeof(float) * (size_t)(gr.N * F), 256);
+  return b + 256;
+}
+
+int tfg_propagate(const tfg_graph* g, const float* edge_weight, int weight_order, const float* x,
+                  int64_t F, int64_t ldx, int64_t K, float alpha, const float* h, int64_t ldh,
+                  float* out, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (gr.N != gr.N_src) return fail(TFG_ERR_INVALID_ARG, "propagation needs a square graph");
+  if (F < 0 || F >= kMaxCount || ldx < F || K < 0)
+    return fail(TFG_ERR_INVALID_ARG, "bad F / ldx / K");
+  if (weight_order != TFG_COO && weight_order != TFG_CSR)
+    return fail(TFG_ERR_INVALID_ARG, "bad weight order");
+  if (!(alpha >= 0.0f && alpha <= 1.0f)) return fail(TFG_ERR_INVALID_ARG, "alpha outside [0, 1]");
+  if (alpha != 0.0f && (h == nullptr || ldh < F))
+    return fail(TFG_ERR_INVALID_ARG, "alpha > 0 needs h with ldh >= F");
+  if (gr.N > 0 && F > 0 && (x == nullptr || out == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (ws == nullptr || ws_bytes < tfg_propagate_ws_bytes(g, F, K))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  if (gr.N == 0 || F == 0) return TFG_OK;
+  if (K == 0) {
+    TFG_HIP(hipMemcpy2DAsync(out, sizeof(float) * F, x, sizeof(float) * ldx, sizeof(float) * F,
+                             gr.N, hipMemcpyDeviceToDevice, s));
+    return TFG_OK;
+  }
+  Carver c(ws, ws_bytes);
+  void* part = c.take(aggregate_partial_bytes(partials_needed(gr.E, gr.N, gr.N_src, F, g), F,
+                                              TFG_SUM));
+  float* tmp = K >= 2 ? static_cast<float*>(c.take(sizeof(float) * (size_t)(gr.N * F))) : nullptr;
+  const float* hh = alpha != 0.0f ? h : nullptr;
+  // step k writes Z_{k+1}; the buffers alternate so that Z_K lands in out
+  for (int64_t k = 0; k < K; ++k) {
+    const float* in = k == 0 ? x : ((K - k) % 2 == 0 ? out : tmp);
+    const int64_t ld_in = k == 0 ? ldx : F;
+    float* dst = (K - (k + 1)) % 2 == 0 ? out : tmp;
+    int rc = launch_aggregate(gr, edge_weight, 1, weight_order, in, F, ld_in, TFG_SUM, dst,
+                              nullptr, part, s, 1.0f - alpha, alpha, hh, ldh);
+    if (rc) return rc;
+  }
+  return TFG_OK;
+}
+
+size_t tfg_gat_aggregate_ws_bytes(int64_t N, int64_t H) {
+  if (N < 0 || H < 0) return 0;
+  return gat_aggregate_ws_bytes(N, H);
+}
+
+int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
+                      const float* a_src, const float* a_dst, float slope, float* out,
+                      float* alpha_out, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (gr.N != gr.N_src) return fail(TFG_ERR_INVALID_ARG, "attention needs a square graph");
+  if (H < 1 || H > max_fused_heads() || D < 1 || H * D >= kMaxCount)
+    return fail(TFG_ERR_INVALID_ARG, "need 1 <= H <= 64 and D >= 1");
+  if (gr.N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr || out == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr.N, H))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  return launch_gat_aggregate(gr, h, (int)H, (int)D, a_src, a_dst, slope, out, alpha_out, ws,
+                              as_stream(stream));
+}
+
 }  // extern "C"
+

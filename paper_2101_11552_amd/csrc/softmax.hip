@@ -101,6 +101,15 @@ __global__ __launch_bounds__(kBlock) void softmax_rows(const int* __restrict__ r
 
 }  // namespace
 
+int launch_node_projections(const float* h, int64_t N, int H, int D, const float* a_src,
+                            const float* a_dst, float* as, float* ad, hipStream_t s) {
+  if (N * H == 0) return TFG_OK;
+  node_projections<<<(unsigned)((N * H + kBlock - 1) / kBlock), kBlock, 0, s>>>(h, N, H, D, a_src,
+                                                                               a_dst, as, ad);
+  TFG_LAUNCHED("node_projections");
+  return TFG_OK;
+}
+
 int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const float* h, int64_t N,
                       int H, int D, const float* a_src, const float* a_dst, float slope,
                       float* out, float* proj, int* err, hipStream_t s) {

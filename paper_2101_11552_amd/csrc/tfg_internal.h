@@ -111,9 +111,12 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                     const float* edge_weight, int32_t* out_edge_index, float* out_w,
                     float* out_w_csr, float* out_deg, float* dinv_ws, hipStream_t s);
 // aggregate.hip
+// With h != NULL (or scale != 1) every output row becomes scale * sum +
+// alpha * h[row] (sum reduction only): one propagation step.
 int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
                      int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax,
-                     void* ws, hipStream_t s);
+                     void* ws, hipStream_t s, float scale = 1.0f, float alpha = 0.0f,
+                     const float* h = nullptr, int64_t ldh = 0);
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce);
 // Whether an aggregation over g with F features uses the part plan.
 bool use_part_plan(const Graph& g, int64_t F);
@@ -127,5 +130,21 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
 int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
                         const void* graph_index, int index_type, int64_t G, int reduce,
                         float* out, int32_t* argmax, int* goff_ws, int* err, hipStream_t s);
+
+// softmax.hip: a_s = a_src . h and a_d = a_dst . h per (node, head)
+int launch_node_projections(const float* h, int64_t N, int H, int D, const float* a_src,
+                            const float* a_dst, float* as, float* ad, hipStream_t s);
+// gat.hip
+size_t gat_aggregate_ws_bytes(int64_t N, int64_t H);
+int max_fused_heads();
+int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const float* a_src,
+                         const float* a_dst, float slope, float* out, float* alpha_out, void* ws,
+                         hipStream_t s);
+// batch.hip
+size_t batch_ws_bytes(int64_t G);
+int launch_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,
+                        const void* local_edge_index, int index_type, int64_t E, int64_t Nb,
+                        void* out_edge_index, void* out_graph_index, int* node_off, int* edge_off,
+                        int* sums, int* err, hipStream_t s);
 
 }  // namespace tfg

@@ -177,3 +177,12 @@ def test_power_law_full_size(tfg, orc):
     finally:
         del os.environ["TFG_PART_PLAN"]
     assert_scaled(host(y3)[rows], ref, S, what="c4 sampled rows, row plan")
+
+
+def test_gat_attention_fused(tfg, orc):
+    c = graphgen.config3()
+    ei, h, n, H = c["edge_index"], c["h"], c["N"], c["H"]
+    g = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n)
+    out = tfg.tfg_gat_aggregate(g, dev(h), dev(c["a_src"]), dev(c["a_dst"]), c["slope"])
+    ref, _, S = orc.gat_layer(ei, h, c["a_src"], c["a_dst"], H, slope=np.float32(c["slope"]))
+    assert_scaled(host(out), ref, S, what="c3 fused attention layer")

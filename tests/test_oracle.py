@@ -486,3 +486,95 @@ def test_batch_equals_per_graph(orc):
         loc = np.zeros(n, np.int64)
         for r in ("sum", "mean", "max"):
             assert np.array_equal(orc.segment_pool(hl, loc, 1, r)[0][0], pooled[r][i])
+
+
+# ---------------------------------------------------------------------------
+# Propagation (SGC / APPNP)
+# ---------------------------------------------------------------------------
+
+def test_propagate_dense_closed_form(orc):
+    n, K, alpha = 30, 5, 0.15
+    ei = graphgen.random_graph(41, n, 200)
+    out_ei, w, _ = orc.gcn_norm(ei, n)
+    x = graphgen.features(41, n, 4)
+    h = graphgen.features(42, n, 4)
+    M = (1 - alpha) * dense_adj(out_ei, n, w).T  # messages: y[t] = sum_s A[s, t] z[s]
+    ref = np.linalg.matrix_power(M, K) @ x.astype(np.float64)
+    ref += alpha * sum(np.linalg.matrix_power(M, j) for j in range(K)) @ h.astype(np.float64)
+    z, S = orc.propagate(out_ei, x, K, alpha=alpha, h=h, edge_weight=w)
+    np.testing.assert_allclose(z, ref, rtol=1e-12, atol=1e-12)
+    assert np.all(S >= np.abs(z) - 1e-12)
+
+
+def test_propagate_special_cases(orc):
+    n = 50
+    ei = graphgen.random_graph(43, n, 400)
+    out_ei, w, deg = orc.gcn_norm(ei, n)
+    x = graphgen.features(43, n, 3)
+    h = graphgen.features(44, n, 3)
+    z0, _ = orc.propagate(out_ei, x, 0, edge_weight=w)
+    assert np.array_equal(z0, x.astype(np.float64))  # K = 0
+    z1, _ = orc.propagate(out_ei, x, 4, alpha=1.0, h=h, edge_weight=w)
+    assert np.array_equal(z1, h.astype(np.float64))  # alpha = 1: only the teleport term
+    y, _ = orc.propagate(out_ei, x, 1, edge_weight=w)
+    agg, _ = orc.aggregate(out_ei, x, n, "sum", edge_weight=w)
+    np.testing.assert_allclose(y, agg, rtol=1e-14, atol=1e-15)
+    # sqrt(deg) is a fixed point of A_hat, hence of every APPNP step with h = sqrt(deg)
+    s = np.sqrt(deg.astype(np.float64)).astype(np.float32)[:, None]
+    zs, _ = orc.propagate(out_ei, s, 7, alpha=0.3, h=s, edge_weight=w)
+    np.testing.assert_allclose(zs, s.astype(np.float64), rtol=2e-6)
+
+
+def test_propagate_appnp_limit(orc):
+    # many steps converge to alpha (I - (1 - alpha) A^T)^-1 h
+    n, alpha = 25, 0.2
+    ei = graphgen.random_graph(45, n, 150)
+    out_ei, w, _ = orc.gcn_norm(ei, n)
+    h = graphgen.features(45, n, 2)
+    z, _ = orc.propagate(out_ei, h, 300, alpha=alpha, h=h, edge_weight=w)
+    M = (1 - alpha) * dense_adj(out_ei, n, w).T
+    ref = alpha * np.linalg.solve(np.eye(n) - M, h.astype(np.float64))
+    np.testing.assert_allclose(z, ref, rtol=1e-9, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# GAT layer (scores -> softmax -> weighted aggregation)
+# ---------------------------------------------------------------------------
+
+def test_gat_layer_zero_attention_is_mean(orc):
+    # a_src = a_dst = 0: every score is 0, attention is uniform, output = mean of in-neighbours
+    n, e, H, D = 40, 300, 4, 3
+    ei = graphgen.random_graph(51, n, e)
+    h = graphgen.features(51, n, H * D)
+    z = np.zeros((H, D), np.float32)
+    out, alpha, _ = orc.gat_layer(ei, h, z, z, H)
+    mean, _ = orc.aggregate(ei, h, n, "mean")
+    np.testing.assert_allclose(out, mean, rtol=1e-13, atol=1e-15)
+    cnt = np.bincount(ei[1], minlength=n)
+    np.testing.assert_allclose(alpha[:, 0], 1.0 / cnt[ei[1]], rtol=1e-15)
+
+
+def test_gat_layer_single_edge_and_dense(orc):
+    n, H, D = 12, 2, 3
+    ei = graphgen.random_graph(52, n, 40)
+    h = graphgen.features(52, n, H * D)
+    r = np.random.default_rng(52)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    out, alpha, S = orc.gat_layer(ei, h, a_s, a_d, H, slope=0.2)
+    # dense: per target and head, softmax over the in-edge scores, then the weighted sum
+    h3 = h.astype(np.float64).reshape(n, H, D)
+    z = (np.einsum("nhd,hd->nh", h3, a_s)[ei[0]] + np.einsum("nhd,hd->nh", h3, a_d)[ei[1]])
+    s = np.where(z >= 0, z, np.float64(np.float32(0.2)) * z).astype(np.float32).astype(np.float64)
+    ref = np.zeros((n, H, D))
+    for t in range(n):
+        idx = np.nonzero(ei[1] == t)[0]
+        if idx.size == 0:
+            continue
+        a = np.exp(s[idx] - s[idx].max(0))
+        a /= a.sum(0)
+        ref[t] = np.einsum("eh,ehd->hd", a, h3[ei[0][idx]])
+        if idx.size == 1:
+            assert np.array_equal(out[t], h3[ei[0][idx[0]]].reshape(-1))  # alpha = 1 exactly
+    np.testing.assert_allclose(out, ref.reshape(n, H * D), rtol=1e-12, atol=1e-12)
+    assert np.all(S >= np.abs(out) - 1e-12)

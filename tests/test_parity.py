@@ -333,3 +333,105 @@ def test_segment_pool_errors(tfg):
     empty = host(tfg.tfg_segment_pool(dev(np.zeros((0, 4), np.float32)),
                                       dev(np.zeros(0, np.int64)), 2, "sum"))
     assert np.all(empty == 0)
+
+
+# ---------------------------------------------------------------------------
+# BatchGraph construction
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("idx", [np.int32, np.int64])
+def test_batch_graphs_match_oracle(tfg, orc, idx):
+    sizes, graphs = graphgen.batch_of_small_graphs(55, 300, 10, 60, 0.1)
+    sizes[7] = 0  # an empty graph
+    graphs[7] = np.zeros((2, 0), np.int64)
+    counts = np.array([g.shape[1] for g in graphs])
+    local = np.concatenate(graphs, axis=1)
+    ei, gi, noff, eoff = tfg.tfg_batch_graphs(dev(sizes.astype(idx)), dev(counts.astype(idx)),
+                                              dev(local.astype(idx)), int(sizes.sum()))
+    ref_ei, ref_gi = orc.batch_graphs(sizes, graphs)
+    assert np.array_equal(host(ei), ref_ei) and np.array_equal(host(gi), ref_gi)
+    assert np.array_equal(host(noff), orc.batch_offsets(sizes))
+    assert np.array_equal(host(eoff), orc.batch_offsets(counts))
+
+
+def test_batch_graphs_paper_example(tfg):
+    import json
+    import os
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "batch_reindex_paper_example.json")))
+    sizes = np.array(gold["sizes"])
+    # one edge per graph: its last local node -> its first
+    local = np.array([[n - 1 for n in sizes], [0, 0, 0]])
+    ei, gi, noff, _ = tfg.tfg_batch_graphs(dev(sizes), dev(np.ones(3, np.int64)), dev(local))
+    assert list(host(noff)[1:3]) == gold["offsets_of_graphs_2_and_3"]
+    for ex in gold["one_based_examples"]:
+        assert host(noff)[ex["graph"] - 1] + ex["node"] == ex["batched_index"]
+    assert list(host(gi)) == [0, 0, 0, 0, 1, 1, 2, 2, 2]
+    assert host(ei).tolist() == [[3, 5, 8], [0, 4, 6]]
+
+
+def test_batch_graphs_errors(tfg):
+    sizes = np.array([3, 2])
+    with pytest.raises(IndexError):  # local id 3 in a graph of 3 nodes
+        tfg.tfg_batch_graphs(dev(sizes), dev(np.array([1, 1])), dev(np.array([[3, 0], [0, 1]])))
+    with pytest.raises(IndexError):  # edge counts add up to 3, the list has 2 edges
+        tfg.tfg_batch_graphs(dev(sizes), dev(np.array([2, 1])), dev(np.array([[0, 0], [1, 1]])))
+
+
+# ---------------------------------------------------------------------------
+# Multi-step propagation (SGC / APPNP)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K,alpha,parts,plan", [(1, 0.0, 1, "0"), (3, 0.0, 1, "0"),
+                                                (4, 0.1, 1, "0"), (5, 0.2, 4, "1"),
+                                                (2, 1.0, 4, "1"), (0, 0.0, 1, "0")])
+def test_propagate(tfg, orc, monkeypatch, K, alpha, parts, plan):
+    monkeypatch.setenv("TFG_PART_PLAN", plan)
+    n, e, F = 3000, 80_000, 64
+    ei = graphgen.random_graph(7 + K, n, e, hub=9, hub_edges=4000)
+    x = graphgen.features(K, n, F)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=True, src_parts=parts)
+    norm = tfg.tfg_gcn_norm(dev(ei), n, graph=g)
+    oei, ow, _ = orc.gcn_norm(ei, n)
+    h = x if alpha > 0 else None
+    # stage by stage on the GPU's own intermediate values
+    z = dev(x)
+    for k in range(K):
+        zin = host(z)
+        z = tfg.tfg_propagate(g, z, 1, alpha=alpha, h=dev(x) if alpha > 0 else None,
+                              edge_weight=norm["edge_weight_csr"])
+        ref, S = orc.propagate(oei, zin, 1, alpha=alpha, h=h, edge_weight=ow)
+        assert_scaled(host(z), ref, S, what=f"step {k}")
+    # the K steps in one call, against the double-precision chain
+    zk = tfg.tfg_propagate(g, dev(x), K, alpha=alpha, h=dev(x) if alpha > 0 else None,
+                           edge_weight=norm["edge_weight_csr"])
+    ref, S = orc.propagate(oei, x, K, alpha=alpha, h=h, edge_weight=ow)
+    assert_scaled(host(zk), ref, S + 1e-30, tol=max(K, 1) * 1e-5, what=f"K={K} chain")
+    if K == 0:
+        assert same_bits(host(zk), x)
+
+
+# ---------------------------------------------------------------------------
+# Fused attention aggregation
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("H,D", [(8, 16), (1, 5), (3, 4), (4, 3), (16, 8)])
+def test_gat_aggregate_fused(tfg, orc, H, D):
+    n, e = 3000, 40_000
+    ei = graphgen.random_graph(H * 10 + D, n, e, hub=3, hub_edges=3000)
+    h = graphgen.features(H + D, n, H * D)
+    r = np.random.default_rng(D)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n)
+    out, alpha = tfg.tfg_gat_aggregate(g, dev(h), dev(a_s), dev(a_d), 0.2, want_alpha=True)
+    ref, ref_alpha, S = orc.gat_layer(ei, h, a_s, a_d, H, slope=np.float32(0.2))
+    assert_scaled(host(out), ref, S, what=f"fused GAT H={H} D={D}")
+    has = np.bincount(ei[1], minlength=n)[ei[1]] > 0
+    assert_rel(host(alpha)[has], ref_alpha[has], what="fused GAT alpha")
+    # the unfused chain of the library gives the same layer
+    s = tfg.tfg_gat_edge_scores(dev(ei), dev(h), dev(a_s), dev(a_d), 0.2)
+    _, a_csr = tfg.tfg_segment_softmax(s, dev(ei[1]), n, graph=g, out_csr=True)
+    y = tfg.tfg_aggregate(dev(ei), dev(h), n, "sum", edge_weight=a_csr, heads=H,
+                          weight_order="csr", graph=g)
+    assert_scaled(host(y), ref, S, what="unfused chain")
