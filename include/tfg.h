@@ -134,6 +134,18 @@ int tfg_graph_bytes(int64_t E, int64_t N_src, int64_t N, int add_self_loops, int
 int tfg_graph_create(const void *edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
                      int add_self_loops, int src_parts, void *buf, size_t buf_bytes,
                      void *scratch, size_t scratch_bytes, tfg_stream_t stream, tfg_graph **out);
+/*
+ * tfg_graph_create_transposed: the graph of the reversed edge list (every
+ *   input edge s -> t becomes t -> s): N_src rows (the sources), col holds
+ *   targets, perm the input edge ids (loops: E + i, as above). It carries the
+ *   backward aggregation, whose gradient flows from targets to sources. Size
+ *   its buffers with tfg_graph_bytes(E, N, N_src, ...) (the two node counts
+ *   swapped). Same checks and synchronisation as tfg_graph_create.
+ */
+int tfg_graph_create_transposed(const void *edge_index, int index_type, int64_t E, int64_t N_src,
+                                int64_t N, int add_self_loops, int src_parts, void *buf,
+                                size_t buf_bytes, void *scratch, size_t scratch_bytes,
+                                tfg_stream_t stream, tfg_graph **out);
 int tfg_graph_csr(const tfg_graph *g, int32_t *rowptr, int32_t *col, int32_t *perm,
                   tfg_stream_t stream);
 int tfg_graph_segments(const tfg_graph *g, int32_t *segptr, tfg_stream_t stream);
@@ -208,6 +220,39 @@ int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float
                   int32_t *argmax, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Backward aggregation                                                      */
+/* ------------------------------------------------------------------------ */
+/*
+ * Gradients of tfg_aggregate, for training through graphs built inside the
+ * model: graph construction (Sec. 2.1.1) and batching (Sec. 2.1.3) are
+ * differentiable, so gradients reach the features and the edge weights. Given dy = dL/d out ([N, F],
+ * contiguous), for every edge e = (s -> t) and column c of head k:
+ *   TFG_SUM : dx[s, c] += w_e[k] dy[t, c];   dw[e, k] += dy[t, c] x[s, c]
+ *   TFG_MEAN: the same with dy[t, c] / (number of edges entering t)
+ *   TFG_MAX : only where argmax[t, c] == e (the forward's winning edge).
+ * Nothing is accumulated across calls: dx and dw are overwritten.
+ * g: the forward graph (tfg_graph_create). gt: NULL, or its transpose
+ *   (tfg_graph_create_transposed of the same edge list); required for dx.
+ * edge_weight: NULL (all ones) or [E', H] in weight_order (TFG_CSR: the graph
+ *   order of g). x: [N_src, F] (leading dimension ldx), needed for dw.
+ * argmax: [N, F] int32 from the forward TFG_MAX call (required for TFG_MAX).
+ * dx: NULL or [N_src, F] (a source without edges gets 0).
+ * dw: NULL or [E', H] in dw_order (TFG_COO: the caller's edge order, loops
+ *   after the input edges; TFG_CSR: the graph order of g).
+ * Sums are float32 in a fixed order, as in tfg_aggregate: dx goes through the
+ * same kernel over gt; each dw entry is one dot product over the columns of
+ * its head. Enqueued on `stream`, no synchronisation.
+ */
+size_t tfg_aggregate_backward_ws_bytes(const tfg_graph *g, const tfg_graph *gt, int64_t F,
+                                       int64_t H, int reduce, int weight_order,
+                                       int has_edge_weight);
+int tfg_aggregate_backward(const tfg_graph *g, const tfg_graph *gt, const float *edge_weight,
+                           int64_t H, int weight_order, const float *x, int64_t ldx,
+                           const float *dy, int64_t F, int reduce, const int32_t *argmax,
+                           float *dx, float *dw, int dw_order, void *ws, size_t ws_bytes,
+                           tfg_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Multi-step propagation                                                    */
 /* ------------------------------------------------------------------------ */
 /*
@@ -257,6 +302,19 @@ size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_g
 int tfg_segment_softmax(const float *scores, int64_t E, int64_t H, const void *seg,
                         int index_type, int64_t N, const tfg_graph *g, float *out,
                         float *out_csr, void *ws, size_t ws_bytes, tfg_stream_t stream);
+
+/*
+ * Gradient of tfg_segment_softmax: for alpha = the segment softmax of the
+ * scores and dalpha = dL/d alpha (both [E, H] in the caller's edge order),
+ *   dscores[e, h] = alpha[e, h] * (dalpha[e, h] - sum over the segment of
+ *                   alpha * dalpha at head h)
+ * with the segment sum in double. seg / g as in tfg_segment_softmax.
+ */
+size_t tfg_segment_softmax_backward_ws_bytes(int64_t E, int64_t H, int64_t N,
+                                             const tfg_graph *g);
+int tfg_segment_softmax_backward(const float *alpha, const float *dalpha, int64_t E, int64_t H,
+                                 const void *seg, int index_type, int64_t N, const tfg_graph *g,
+                                 float *dscores, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
 /*
  * Fused attention aggregation: the whole GAT workflow of Fig. 5(a) plus the

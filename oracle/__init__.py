@@ -51,6 +51,9 @@ def lib():
         _lib.orc_aggregate_rows.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, ctypes.c_int,
                                             p, i64, p, p, p, p]
         _lib.orc_segment_softmax.argtypes = [i64, i64, p, p, i64, p, p]
+        _lib.orc_aggregate_backward.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, i64,
+                                                ctypes.c_int, p, p, p, p]
+        _lib.orc_segment_softmax_backward.argtypes = [i64, i64, p, p, p, i64, p]
         _lib.orc_propagate.argtypes = [i64, p, p, p, p, i64, i64, i64, i64, ctypes.c_double, p,
                                        p, p]
         _lib.orc_segment_pool.argtypes = [i64, i64, i64, p, p, i64, ctypes.c_int, p, p, p, p]
@@ -142,6 +145,8 @@ def aggregate(edge_index, x, n, reduce="sum", edge_weight=None, heads=1, rows=No
     red = REDUCE[reduce]
     src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
     w = _f32(edge_weight)
+    if w is not None and w.size != ei.shape[1] * heads:
+        raise ValueError("edge_weight must hold E * heads values")
     n_rows = n if rows is None else len(rows)
     out64 = np.zeros((n_rows, F), np.float64) if red != MAX else None
     scale = np.zeros((n_rows, F), np.float64) if red != MAX else None
@@ -177,6 +182,43 @@ def propagate(edge_index, x, K, alpha=0.0, h=None, edge_weight=None):
     return out64, scale
 
 
+def aggregate_backward(edge_index, x, n, dy, reduce="sum", edge_weight=None, heads=1, arg=None):
+    """Gradients of ``aggregate`` for dL/d out = dy: (dx [N_src, F], dw [E, H]) in float64."""
+    ei = _i64(edge_index)
+    x, ldx = _rows(x)
+    n_src, F = x.shape
+    E = ei.shape[1]
+    src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
+    w = _f32(edge_weight)
+    if w is not None and w.size != E * heads:
+        raise ValueError("edge_weight must hold E * heads values")
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    if dy.shape != (n, F) or (arg is not None and np.shape(arg) != (n, F)):
+        raise ValueError("dy and arg must be [N, F]")
+    a = None if arg is None else _i64(arg)
+    dx = np.empty((n_src, F), np.float64)
+    dw = np.empty((E, heads), np.float64)
+    _check(lib().orc_aggregate_backward(E, _ptr(src), _ptr(tgt), _ptr(w), heads,
+                                        x.ctypes.data_as(ctypes.c_void_p), ldx, F, n_src, n,
+                                        REDUCE[reduce], _ptr(dy), _ptr(a), _ptr(dx), _ptr(dw)))
+    return dx, dw
+
+
+def segment_softmax_backward(alpha, dalpha, seg, n):
+    """dL/d scores for alpha = segment softmax(scores) and dL/d alpha = dalpha (float64)."""
+    a = np.ascontiguousarray(alpha, dtype=np.float32)
+    shape = a.shape
+    a = a.reshape(a.shape[0], -1)
+    da = np.ascontiguousarray(dalpha, dtype=np.float32).reshape(a.shape)
+    seg = _i64(seg)
+    if seg.shape != (a.shape[0],):
+        raise ValueError("seg must hold one id per row")
+    ds = np.empty(a.shape, np.float64)
+    _check(lib().orc_segment_softmax_backward(a.shape[0], a.shape[1], _ptr(a), _ptr(da), _ptr(seg),
+                                              n, _ptr(ds)))
+    return ds.reshape(shape)
+
+
 def segment_softmax(scores, seg, n):
     """Per-segment softmax of float32 scores [E,H] (or [E]) -> (out64, out32)."""
     s = np.ascontiguousarray(scores, dtype=np.float32)
@@ -184,6 +226,8 @@ def segment_softmax(scores, seg, n):
     s2 = s.reshape(s.shape[0], -1)
     E, H = s2.shape
     seg = _i64(seg)
+    if seg.shape != (E,):
+        raise ValueError("seg must hold one id per score row")
     out64 = np.empty((E, H), np.float64)
     outf = np.empty((E, H), np.float32)
     _check(lib().orc_segment_softmax(E, H, _ptr(s2), _ptr(seg), n, _ptr(out64), _ptr(outf)))

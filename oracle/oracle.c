@@ -258,6 +258,73 @@ int orc_propagate(int64_t E, const int64_t *src, const int64_t *tgt, const float
 }
 
 /*
+ * Gradients of orc_aggregate for a loss L with dL/d out = dy ([N, F]):
+ *   sum : dx[s, c] += w_e[head(c)] dy[t, c]            for every edge e = (s -> t)
+ *         dw[e, k] += dy[t, c] x[s, c]                 over the columns c of head k
+ *   mean: the same terms divided by the number of edges entering t
+ *   max : only the terms of edge e at columns c where e is the argmax of (t, c)
+ *         (arg: [N, F] edge ids from the forward max, -1 for empty targets)
+ * dx64 [N_src, F] and dw64 [E, H] (either may be NULL) in double.
+ */
+int orc_aggregate_backward(int64_t E, const int64_t *src, const int64_t *tgt, const float *w,
+                           int64_t H, const float *x, int64_t ldx, int64_t F, int64_t N_src,
+                           int64_t N, int reduce, const float *dy, const int64_t *arg,
+                           double *dx64, double *dw64)
+{
+    if (H < 1 || F % H != 0 || (reduce == ORC_MAX && arg == NULL))
+        return ORC_ERR_INVALID_ARG;
+    int64_t per_head = F / H;
+    int64_t *cnt = (int64_t *)calloc((size_t)(N > 0 ? N : 1), sizeof(int64_t));
+    for (int64_t e = 0; e < E; ++e)
+        cnt[tgt[e]] += 1;
+    if (dx64)
+        memset(dx64, 0, (size_t)(N_src * F) * sizeof(double));
+    if (dw64)
+        memset(dw64, 0, (size_t)(E * H) * sizeof(double));
+    for (int64_t e = 0; e < E; ++e) {
+        int64_t s = src[e], t = tgt[e];
+        for (int64_t c = 0; c < F; ++c) {
+            if (reduce == ORC_MAX && arg[t * F + c] != e)
+                continue;
+            double g = (double)dy[t * F + c];
+            if (reduce == ORC_MEAN)
+                g /= (double)cnt[t];
+            int64_t k = c / per_head;
+            double wv = w ? (double)w[e * H + k] : 1.0;
+            if (dx64)
+                dx64[s * F + c] += wv * g;
+            if (dw64)
+                dw64[e * H + k] += g * (double)x[s * ldx + c];
+        }
+    }
+    free(cnt);
+    return ORC_OK;
+}
+
+/*
+ * Gradient of orc_segment_softmax: with alpha = softmax(s) per (segment, head)
+ * and dL/d alpha = da, dL/d s[e, h] = alpha[e, h] (da[e, h] - sum over the
+ * segment of alpha * da). alpha, da: [E, H] float32; ds64 in double.
+ */
+int orc_segment_softmax_backward(int64_t E, int64_t H, const float *alpha, const float *da,
+                                 const int64_t *seg, int64_t N, double *ds64)
+{
+    for (int64_t e = 0; e < E; ++e)
+        if (seg[e] < 0 || seg[e] >= N)
+            return ORC_ERR_INDEX_RANGE;
+    double *dot = (double *)calloc((size_t)(N * H > 0 ? N * H : 1), sizeof(double));
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t h = 0; h < H; ++h)
+            dot[seg[e] * H + h] += (double)alpha[e * H + h] * (double)da[e * H + h];
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t h = 0; h < H; ++h)
+            ds64[e * H + h] = (double)alpha[e * H + h] *
+                              ((double)da[e * H + h] - dot[seg[e] * H + h]);
+    free(dot);
+    return ORC_OK;
+}
+
+/*
  * Segment softmax, the map -> reduce -> map workflow of Fig. 5(a), Sec. 2.1.2:
  * for every segment t (the edges with seg[e] = t) and head h,
  *   alpha[e, h] = exp(s[e, h] - m) / sum over the segment of exp(s - m)

@@ -94,6 +94,13 @@ def load():
         "tfg_gat_aggregate": (ci, [p, p, i64, i64, p, p, ctypes.c_float, p, p, p, sz, p]),
         "tfg_propagate": (ci, [p, p, ci, p, i64, i64, i64, ctypes.c_float, p, i64, p, p, sz, p]),
         "tfg_batch_graphs": (ci, [i64, p, p, p, ci, i64, i64, p, p, p, p, ci, p, sz, p]),
+        "tfg_graph_create_transposed": (ci, [p, ci, i64, i64, i64, ci, ci, p, sz, p, sz, p,
+                                             ctypes.POINTER(p)]),
+        "tfg_aggregate_backward_ws_bytes": (sz, [p, p, i64, i64, ci, ci, ci]),
+        "tfg_aggregate_backward": (ci, [p, p, p, i64, ci, p, i64, p, i64, ci, p, p, p, ci, p, sz,
+                                        p]),
+        "tfg_segment_softmax_backward_ws_bytes": (sz, [i64, i64, i64, p]),
+        "tfg_segment_softmax_backward": (ci, [p, p, i64, i64, p, ci, i64, p, p, p, sz, p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -205,6 +212,25 @@ def tfg_graph_bytes(E: int, N: int, add_self_loops: bool = False, N_src: int | N
     return b.value, s.value
 
 
+def _create(fn, edge_index, N, N_src, add_self_loops, src_parts, buf, scratch, transposed):
+    ei = _edges(edge_index)
+    E = ei.shape[1]
+    N_src = N if N_src is None else N_src
+    rows, cols = (N_src, N) if transposed else (N, N_src)
+    nb, ns = tfg_graph_bytes(E, rows, add_self_loops, cols, src_parts)
+    dev = ei.device
+    if buf is None or buf.numel() < nb:
+        buf = _workspace(nb, dev)
+    if scratch is None or scratch.numel() < ns:
+        scratch = _workspace(ns, dev)
+    h = ctypes.c_void_p()
+    _check(fn(_ptr(ei), _index_type(ei), E, N_src, N, int(add_self_loops), int(src_parts),
+              _ptr(buf), buf.numel(), _ptr(scratch), scratch.numel(), _stream(dev),
+              ctypes.byref(h)))
+    return Graph(h, buf, E, E + (rows if add_self_loops else 0), rows, cols,
+                 bool(add_self_loops), dev)
+
+
 def tfg_graph_create(edge_index: torch.Tensor, N: int, N_src: int | None = None,
                      add_self_loops: bool = False, src_parts: int = 0,
                      buf: torch.Tensor | None = None,
@@ -212,21 +238,19 @@ def tfg_graph_create(edge_index: torch.Tensor, N: int, N_src: int | None = None,
     """COO -> CSR by (target, source part) (synchronises once; raises
     IndexError on a bad id). src_parts: 0 = chosen by the library, 1 = the
     plain stable CSR by target."""
-    lib = load()
-    ei = _edges(edge_index)
-    E = ei.shape[1]
-    N_src = N if N_src is None else N_src
-    nb, ns = tfg_graph_bytes(E, N, add_self_loops, N_src, src_parts)
-    dev = ei.device
-    if buf is None or buf.numel() < nb:
-        buf = _workspace(nb, dev)
-    if scratch is None or scratch.numel() < ns:
-        scratch = _workspace(ns, dev)
-    h = ctypes.c_void_p()
-    _check(lib.tfg_graph_create(_ptr(ei), _index_type(ei), E, N_src, N, int(add_self_loops),
-                                int(src_parts), _ptr(buf), buf.numel(), _ptr(scratch),
-                                scratch.numel(), _stream(dev), ctypes.byref(h)))
-    return Graph(h, buf, E, E + (N if add_self_loops else 0), N, N_src, bool(add_self_loops), dev)
+    return _create(load().tfg_graph_create, edge_index, N, N_src, add_self_loops, src_parts, buf,
+                   scratch, False)
+
+
+def tfg_graph_create_transposed(edge_index: torch.Tensor, N: int, N_src: int | None = None,
+                                add_self_loops: bool = False, src_parts: int = 0,
+                                buf: torch.Tensor | None = None,
+                                scratch: torch.Tensor | None = None) -> Graph:
+    """The graph of the reversed edges (rows = the N_src sources, col = targets,
+    perm = input edge ids) that carries the backward aggregation. N and N_src
+    are those of the forward edge list; the handle's ``N`` is N_src."""
+    return _create(load().tfg_graph_create_transposed, edge_index, N, N_src, add_self_loops,
+                   src_parts, buf, scratch, True)
 
 
 def tfg_graph_csr(g: Graph):
@@ -315,6 +339,8 @@ def tfg_aggregate(edge_index: torch.Tensor | None, x: torch.Tensor, N: int, redu
     dev = x.device
     N_src, F = x.shape
     w = _f32(edge_weight, "edge_weight")
+    if w is not None and w.numel() != E * heads:
+        raise ValueError(f"edge_weight must hold E * heads = {E * heads} values")
     red = _REDUCE[reduce]
     if out is None:
         out = torch.empty((N, F), dtype=torch.float32, device=dev)
@@ -330,6 +356,72 @@ def tfg_aggregate(edge_index: torch.Tensor | None, x: torch.Tensor, N: int, redu
                              _ptr(argmax) if red == 2 else None, _ptr(ws), ws.numel(),
                              _stream(dev)))
     return (out, argmax) if red == 2 else out
+
+
+def tfg_aggregate_backward(graph: Graph, dy: torch.Tensor, reduce: str = "sum",
+                           graph_t: Graph | None = None, x: torch.Tensor | None = None,
+                           edge_weight: torch.Tensor | None = None, heads: int = 1,
+                           weight_order: str = "coo", argmax: torch.Tensor | None = None,
+                           want_dx: bool = True, want_dw: bool = False, dw_order: str = "coo",
+                           ws: torch.Tensor | None = None):
+    """Gradients of ``tfg_aggregate`` for dy = dL/d out [N, F]. Returns
+    (dx [N_src, F] or None, dw [E', heads] or None); dx needs ``graph_t``
+    (tfg_graph_create_transposed), dw needs ``x``, max needs the forward ``argmax``."""
+    lib = load()
+    dy = _f32(dy, "dy").contiguous()
+    dev = dy.device
+    F = dy.shape[1]
+    if dy.shape[0] != graph.N:
+        raise ValueError("dy must be [N, F]")
+    w = _f32(edge_weight, "edge_weight")
+    if w is not None and w.numel() != graph.E * heads:
+        raise ValueError(f"edge_weight must hold E' * heads = {graph.E * heads} values")
+    xx, ldx = (None, F)
+    if x is not None:
+        xx, ldx = _rows(x, "x")
+        if xx.shape != (graph.N_src, F):
+            raise ValueError("x must be [N_src, F]")
+    if argmax is not None and tuple(argmax.shape) != (graph.N, F):
+        raise ValueError("argmax must be [N, F]")
+    red = _REDUCE[reduce]
+    am = None
+    if argmax is not None:
+        am = _dev(argmax, "argmax").contiguous()
+        if am.dtype != torch.int32:
+            raise TypeError("argmax must be int32")
+    dx = torch.empty((graph.N_src, F), dtype=torch.float32, device=dev) if want_dx else None
+    dw = torch.empty((graph.E, heads), dtype=torch.float32, device=dev) if want_dw else None
+    ht = graph_t.handle if graph_t is not None else None
+    need = lib.tfg_aggregate_backward_ws_bytes(graph.handle, ht, F, heads, red,
+                                               _ORDER[weight_order], int(w is not None))
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    _check(lib.tfg_aggregate_backward(graph.handle, ht, _ptr(w), heads, _ORDER[weight_order],
+                                      _ptr(xx), ldx, _ptr(dy), F, red, _ptr(am), _ptr(dx),
+                                      _ptr(dw), _ORDER[dw_order], _ptr(ws), ws.numel(),
+                                      _stream(dev)))
+    return dx, dw
+
+
+def tfg_segment_softmax_backward(alpha: torch.Tensor, dalpha: torch.Tensor, seg: torch.Tensor,
+                                 N: int, graph: Graph | None = None) -> torch.Tensor:
+    """dL/d scores from alpha = segment softmax(scores) and dalpha = dL/d alpha ([E, H] or [E])."""
+    lib = load()
+    a = _f32(alpha, "alpha")
+    shape = a.shape
+    a2 = a.reshape(a.shape[0], -1)
+    da = _f32(dalpha, "dalpha").reshape(a2.shape)
+    E, H = a2.shape
+    seg = _dev(seg, "seg").contiguous()
+    if seg.numel() != E:
+        raise ValueError("seg must hold one id per edge")
+    dev = a.device
+    ds = torch.empty_like(a2)
+    h = graph.handle if graph is not None else None
+    ws = _workspace(lib.tfg_segment_softmax_backward_ws_bytes(E, H, N, h), dev)
+    _check(lib.tfg_segment_softmax_backward(_ptr(a2), _ptr(da), E, H, _ptr(seg), _index_type(seg),
+                                            N, h, _ptr(ds), _ptr(ws), ws.numel(), _stream(dev)))
+    return ds.reshape(shape)
 
 
 def tfg_gat_edge_scores(edge_index: torch.Tensor, h: torch.Tensor, a_src: torch.Tensor,
@@ -364,6 +456,8 @@ def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
     s2 = s.reshape(s.shape[0], -1)
     E, H = s2.shape
     seg = _dev(seg, "seg").contiguous()
+    if seg.numel() != E:
+        raise ValueError("seg must hold one id per edge")
     dev = s.device
     out = torch.empty_like(s2)
     oc = torch.empty_like(s2) if out_csr else None

@@ -175,9 +175,11 @@ int tfg_graph_bytes(int64_t E, int64_t N_src, int64_t N, int add_self_loops, int
   return TFG_OK;
 }
 
-int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
-                     int add_self_loops, int src_parts, void* buf, size_t buf_bytes, void* scratch,
-                     size_t scratch_bytes, tfg_stream_t stream, tfg_graph** out) {
+namespace {
+
+int create_handle(const void* edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
+                  int add_self_loops, int src_parts, void* buf, size_t buf_bytes, void* scratch,
+                  size_t scratch_bytes, tfg_stream_t stream, bool transposed, tfg_graph** out) {
   if (out == nullptr) return fail(TFG_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
@@ -187,15 +189,37 @@ int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t 
   if (scratch == nullptr) return fail(TFG_ERR_INVALID_ARG, "scratch is NULL");
   tfg_graph* h = new (std::nothrow) tfg_graph;
   if (!h) return fail(TFG_ERR_HIP, "host allocation failed");
-  int rc = create_graph(h->g, edge_index, tgt_row(edge_index, index_type, E), index_type, E, N_src,
-                        N, add_self_loops, src_parts, buf, buf_bytes, scratch, scratch_bytes,
-                        as_stream(stream));
+  const void* src = edge_index;
+  const void* tgt = tgt_row(edge_index, index_type, E);
+  int rc = transposed
+               ? create_graph(h->g, tgt, src, index_type, E, N, N_src, add_self_loops, src_parts,
+                              buf, buf_bytes, scratch, scratch_bytes, as_stream(stream))
+               : create_graph(h->g, src, tgt, index_type, E, N_src, N, add_self_loops, src_parts,
+                              buf, buf_bytes, scratch, scratch_bytes, as_stream(stream));
   if (rc) {
     delete h;
     return rc;
   }
+  h->g.transposed = transposed ? 1 : 0;
   *out = h;
   return TFG_OK;
+}
+
+}  // namespace
+
+int tfg_graph_create(const void* edge_index, int index_type, int64_t E, int64_t N_src, int64_t N,
+                     int add_self_loops, int src_parts, void* buf, size_t buf_bytes, void* scratch,
+                     size_t scratch_bytes, tfg_stream_t stream, tfg_graph** out) {
+  return create_handle(edge_index, index_type, E, N_src, N, add_self_loops, src_parts, buf,
+                       buf_bytes, scratch, scratch_bytes, stream, false, out);
+}
+
+int tfg_graph_create_transposed(const void* edge_index, int index_type, int64_t E, int64_t N_src,
+                                int64_t N, int add_self_loops, int src_parts, void* buf,
+                                size_t buf_bytes, void* scratch, size_t scratch_bytes,
+                                tfg_stream_t stream, tfg_graph** out) {
+  return create_handle(edge_index, index_type, E, N_src, N, add_self_loops, src_parts, buf,
+                       buf_bytes, scratch, scratch_bytes, stream, true, out);
 }
 
 int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* perm,
@@ -392,6 +416,101 @@ int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* s
     if (rc) return rc;
   }
   rc = launch_segment_softmax(*gp, scores, (int)H, out, out_csr, s);
+  if (rc) return rc;
+  if (!g) TFG_HIP(hipStreamSynchronize(s));
+  return TFG_OK;
+}
+
+namespace {
+
+// Checks that g (forward) and gt (transposed, may be NULL) describe one edge list.
+int check_backward_graphs(const tfg_graph* g, const tfg_graph* gt) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "the forward graph is NULL");
+  if (g->g.transposed) return fail(TFG_ERR_INVALID_ARG, "g must be a forward graph");
+  if (gt) {
+    const Graph& a = g->g;
+    const Graph& b = gt->g;
+    if (!b.transposed) return fail(TFG_ERR_INVALID_ARG, "gt must be a transposed graph");
+    if (a.E_in != b.E_in || a.N != b.N_src || a.N_src != b.N || a.loops != b.loops)
+      return fail(TFG_ERR_INVALID_ARG, "gt does not transpose g");
+  }
+  return TFG_OK;
+}
+
+}  // namespace
+
+size_t tfg_aggregate_backward_ws_bytes(const tfg_graph* g, const tfg_graph* gt, int64_t F,
+                                       int64_t H, int reduce, int weight_order,
+                                       int has_edge_weight) {
+  if (!g || F < 0 || H < 1) return 0;
+  return aggregate_backward_ws_bytes(g->g, gt ? &gt->g : nullptr, F, H, reduce, weight_order,
+                                     has_edge_weight != 0);
+}
+
+int tfg_aggregate_backward(const tfg_graph* g, const tfg_graph* gt, const float* edge_weight,
+                           int64_t H, int weight_order, const float* x, int64_t ldx,
+                           const float* dy, int64_t F, int reduce, const int32_t* argmax,
+                           float* dx, float* dw, int dw_order, void* ws, size_t ws_bytes,
+                           tfg_stream_t stream) {
+  int rc = check_backward_graphs(g, gt);
+  if (rc) return rc;
+  if (reduce != TFG_SUM && reduce != TFG_MEAN && reduce != TFG_MAX)
+    return fail(TFG_ERR_INVALID_ARG, "bad reduce");
+  if (weight_order != TFG_COO && weight_order != TFG_CSR)
+    return fail(TFG_ERR_INVALID_ARG, "bad weight order");
+  if (dw_order != TFG_COO && dw_order != TFG_CSR)
+    return fail(TFG_ERR_INVALID_ARG, "bad dw order");
+  if (F < 0 || H < 1 || (F > 0 && F % H != 0) || F > kMaxCount || H > kMaxCount)
+    return fail(TFG_ERR_INVALID_ARG, "bad F or H");
+  const Graph& fg = g->g;
+  if (fg.E * H >= kMaxCount) return fail(TFG_ERR_TOO_LARGE, "E * H does not fit 31-bit indexing");
+  if (fg.N > 0 && F > 0 && dy == nullptr) return fail(TFG_ERR_INVALID_ARG, "dy is NULL");
+  if (dx != nullptr && gt == nullptr) return fail(TFG_ERR_INVALID_ARG, "dx needs gt");
+  if (dw != nullptr && fg.N_src > 0 && F > 0 && x == nullptr)
+    return fail(TFG_ERR_INVALID_ARG, "dw needs x");
+  if (dw != nullptr && ldx < F) return fail(TFG_ERR_INVALID_ARG, "ldx < F");
+  if (reduce == TFG_MAX && argmax == nullptr)
+    return fail(TFG_ERR_INVALID_ARG, "the max gradient needs the forward argmax");
+  const Graph* tg = gt ? &gt->g : nullptr;
+  if (ws == nullptr ||
+      ws_bytes < aggregate_backward_ws_bytes(fg, tg, F, H, reduce, weight_order,
+                                             edge_weight != nullptr))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  return launch_aggregate_backward(fg, dx ? tg : nullptr, edge_weight, (int)H, weight_order, x,
+                                   ldx, dy, F, reduce, argmax, dx, dw, dw_order, ws, s);
+}
+
+size_t tfg_segment_softmax_backward_ws_bytes(int64_t E, int64_t H, int64_t N,
+                                             const tfg_graph* g) {
+  return tfg_segment_softmax_ws_bytes(E, H, N, g);
+}
+
+int tfg_segment_softmax_backward(const float* alpha, const float* dalpha, int64_t E, int64_t H,
+                                 const void* seg, int index_type, int64_t N, const tfg_graph* g,
+                                 float* dscores, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(E, N, 1);
+  if (rc) return rc;
+  if (H < 1 || E * H >= (int64_t(1) << 62)) return fail(TFG_ERR_INVALID_ARG, "bad H");
+  if (E > 0 && (alpha == nullptr || dalpha == nullptr || dscores == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (E > 0 && seg == nullptr && g == nullptr) return fail(TFG_ERR_INVALID_ARG, "seg is NULL");
+  if (ws == nullptr || ws_bytes < tfg_segment_softmax_backward_ws_bytes(E, H, N, g))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  Carver c(ws, ws_bytes);
+  const Graph* gp = nullptr;
+  Graph tmp;
+  if (g) {
+    gp = &g->g;
+    if (gp->transposed || gp->E != E || gp->N != N)
+      return fail(TFG_ERR_INVALID_ARG, "graph handle does not match");
+  } else {
+    rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
+    if (rc) return rc;
+  }
+  rc = launch_segment_softmax_backward(*gp, alpha, dalpha, (int)H, dscores, s);
   if (rc) return rc;
   if (!g) TFG_HIP(hipStreamSynchronize(s));
   return TFG_OK;

@@ -1,0 +1,367 @@
+// Gradients of the aggregation and of the segment softmax (gfx950, wave64).
+//
+// For out = aggregate(w, x) and an incoming gradient dy = dL/d out:
+//   dx  (sum)  = the sum aggregation of dy over the transposed graph (rows are
+//                sources, columns targets) with the same edge weights;
+//   dx  (mean) = the same with w_e / deg(t_e) as weights;
+//   dx  (max)  = the masked gather of spmm_rows: element c of dy[t] reaches
+//                source s only through the edge that won the forward max;
+//   dw[e, k]   = sum over the columns c of head k of g[t_e, c] x[s_e, c] with
+//                g = dy, dy / deg(t) or the masked dy: one dot product per
+//                edge (edge_grad_rows), walking the forward graph so that the
+//                dy row of a target is loaded once.
+// Segment softmax: ds = alpha * (dalpha - sum over the segment of alpha * dalpha)
+// per head, the dot product accumulated in double (softmax_grad_rows).
+// Every result has one writer and a fixed summation order: no atomics.
+#include "spmm.h"
+
+namespace tfg {
+
+namespace rows {
+
+void dispatch_masked(bool part_plan, bool heads, int vec, int slots, dim3 grid, hipStream_t s,
+                     const RowArgs& a) {
+  if (part_plan) {
+    if (heads)
+      dispatch_vec<false, true, true, true>(vec, slots, grid, s, a);
+    else
+      dispatch_vec<false, false, true, true>(vec, slots, grid, s, a);
+  } else {
+    if (heads)
+      dispatch_vec<false, true, false, true>(vec, slots, grid, s, a);
+    else
+      dispatch_vec<false, false, false, true>(vec, slots, grid, s, a);
+  }
+}
+
+}  // namespace rows
+
+namespace {
+
+using namespace rows;
+
+enum { kGradSum = 0, kGradMean = 1, kGradMax = 2 };
+
+// dw for the work items of the forward graph. Lanes are (edge slot, V
+// columns); each lane keeps its V columns of g[t] in registers, and a slot's
+// partial dot products are summed over the G lanes of each head with a
+// shift-down tree (the head's first lane holds the result).
+template <int V, int SLOTS, int MODE>
+__global__ __launch_bounds__(kBlock) void edge_grad_rows(
+    const WorkItem* __restrict__ items, int n_items, const int* __restrict__ rowptr,
+    const int* __restrict__ col, const int* __restrict__ perm, const float* __restrict__ x,
+    int64_t ldx, const float* __restrict__ dy, const int* __restrict__ arg, int F, int H, int G,
+    float* __restrict__ dw, int dw_by_perm) {
+  constexpr int LPS = kWave / SLOTS;
+  constexpr int U = SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_items) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int slot = lane / LPS, sl = lane % LPS;
+  const WorkItem* itp = items + wid;
+  const int row = uniform(itp->row), kbeg = uniform(itp->kbeg), kend = uniform(itp->kend);
+  if (kbeg >= kend) return;
+  const int f = sl * V;
+  const bool fok = f < F;
+  const int r = sl % G, head = sl / G;
+  const bool need_perm = MODE == kGradMax || dw_by_perm;
+
+  float gy[V];
+  int ga[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    gy[v] = 0.0f;
+    ga[v] = -1;
+  }
+  if (fok) {
+    load_row<V>(dy + (int64_t)row * F + f, gy);
+    if constexpr (MODE == kGradMean) {
+      const float cnt = (float)(rowptr[row + 1] - rowptr[row]);
+#pragma unroll
+      for (int v = 0; v < V; ++v) gy[v] = gy[v] / cnt;
+    }
+    if constexpr (MODE == kGradMax) load_irow<V>(arg + (int64_t)row * F + f, ga);
+  }
+
+  for (int kb = kbeg; kb < kend; kb += kWave) {
+    const int n = min(kWave, kend - kb);
+    const bool lok = lane < n;
+    const int cj = lok ? __builtin_nontemporal_load(col + kb + lane) : 0;
+    const int pj = (lok && need_perm) ? __builtin_nontemporal_load(perm + kb + lane) : 0;
+    for (int s0 = 0; s0 < n; s0 += SLOTS * U) {
+      float p[U];
+      int pe[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jb = s0 + u * SLOTS;
+        ok[u] = jb + slot < n;
+        const int c = bcast<SLOTS>(cj, jb, slot);
+        pe[u] = need_perm ? bcast<SLOTS>(pj, jb, slot) : 0;
+        float xv[V];
+        if (ok[u] && fok) {
+          load_row<V>(x + (int64_t)c * ldx + f, xv);
+        } else {
+#pragma unroll
+          for (int v = 0; v < V; ++v) xv[v] = 0.0f;
+        }
+        float acc = 0.0f;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          const float t = (MODE == kGradMax && ga[v] != pe[u]) ? 0.0f : gy[v];
+          acc = __builtin_fmaf(t, xv[v], acc);
+        }
+        p[u] = acc;
+      }
+      for (int off = 1; off < G; off <<= 1)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float o = __shfl_down(p[u], off);
+          if (r + off < G) p[u] += o;
+        }
+      if (r == 0 && fok) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (ok[u]) {
+            const int64_t e = dw_by_perm ? pe[u] : kb + s0 + u * SLOTS + slot;
+            dw[e * H + head] = p[u];
+          }
+      }
+    }
+  }
+}
+
+// Fallback for shapes the lane mapping above does not cover (more than 64
+// vector columns, or heads that are not a whole number of vectors): one
+// thread per (graph position, head), columns in order.
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void edge_grad_simple(
+    const int* __restrict__ rowptr, int64_t N, int64_t E, const int* __restrict__ col,
+    const int* __restrict__ perm, const float* __restrict__ x, int64_t ldx,
+    const float* __restrict__ dy, const int* __restrict__ arg, int F, int H,
+    float* __restrict__ dw, int dw_by_perm) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E * H) return;
+  const int64_t k = i / H;
+  const int h = (int)(i - k * H);
+  int64_t lo = 0, hi = N;  // the row t with rowptr[t] <= k < rowptr[t + 1]
+  while (hi - lo > 1) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (rowptr[mid] <= k) lo = mid; else hi = mid;
+  }
+  const int64_t t = lo, s = col[k], e = perm[k];
+  const int D = F / H;
+  const float cnt = (float)(rowptr[t + 1] - rowptr[t]);
+  float acc = 0.0f;
+  for (int c = h * D; c < (h + 1) * D; ++c) {
+    float g = dy[t * F + c];
+    if (MODE == kGradMean) g = g / cnt;
+    if (MODE == kGradMax && arg[t * F + c] != (int)e) g = 0.0f;
+    acc = __builtin_fmaf(g, x[s * ldx + c], acc);
+  }
+  dw[(dw_by_perm ? e : k) * H + h] = acc;
+}
+
+// Weights of the transposed graph for the mean gradient, in its graph order:
+// wt[k, h] = w[e_k, h] / deg(t_k) (w = 1 when NULL), e_k = perm[k], t_k = col[k].
+__global__ __launch_bounds__(kBlock) void mean_weights(const int* __restrict__ tcol,
+                                                       const int* __restrict__ tperm, int64_t E,
+                                                       int H, const int* __restrict__ rowptr,
+                                                       const float* __restrict__ w,
+                                                       float* __restrict__ wt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E * H) return;
+  const int64_t k = i / H;
+  const int h = (int)(i - k * H);
+  const int t = tcol[k];
+  const float cnt = (float)(rowptr[t + 1] - rowptr[t]);
+  const float wv = w ? w[(int64_t)tperm[k] * H + h] : 1.0f;
+  wt[i] = wv / cnt;
+}
+
+// Graph order -> caller's edge order: out[perm[k], h] = in[k, h].
+__global__ __launch_bounds__(kBlock) void to_edge_order(const int* __restrict__ perm, int64_t E,
+                                                        int H, const float* __restrict__ in,
+                                                        float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E * H) return;
+  const int64_t k = i / H;
+  const int h = (int)(i - k * H);
+  out[(int64_t)perm[k] * H + h] = in[i];
+}
+
+// One wavefront per segment; lanes are (slot, head) pairs as in softmax_rows.
+__global__ __launch_bounds__(kBlock) void softmax_grad_rows(const int* __restrict__ rowptr,
+                                                            const int* __restrict__ perm,
+                                                            int64_t N,
+                                                            const float* __restrict__ alpha,
+                                                            const float* __restrict__ da, int H,
+                                                            int HP, float* __restrict__ ds) {
+  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+  if (t >= N) return;
+  const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
+  if (kb == ke) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  for (int hb = 0; hb < H; hb += HP) {
+    const int h = hb + hh;
+    const bool act = h < H;
+    double dot = 0.0;
+    for (int k = kb + slot; k < ke; k += SL)
+      if (act) {
+        const int64_t i = (int64_t)perm[k] * H + h;
+        dot += (double)alpha[i] * (double)da[i];
+      }
+    for (int off = HP; off < kWave; off <<= 1) dot += __shfl_xor(dot, off);
+    for (int k = kb + slot; k < ke; k += SL)
+      if (act) {
+        const int64_t i = (int64_t)perm[k] * H + h;
+        ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
+      }
+  }
+}
+
+template <int V, int MODE>
+void launch_edge_grad_slots(int slots, dim3 grid, hipStream_t s, const WorkItem* items,
+                            int n_items, const Graph& g, const float* x, int64_t ldx,
+                            const float* dy, const int* arg, int F, int H, int G, float* dw,
+                            int by_perm) {
+#define TFG_EG(SL)                                                                             \
+  edge_grad_rows<V, SL, MODE><<<grid, kBlock, 0, s>>>(items, n_items, g.rowptr, g.col, g.perm, \
+                                                      x, ldx, dy, arg, F, H, G, dw, by_perm)
+  switch (slots) {
+    case 1: TFG_EG(1); break;
+    case 2: TFG_EG(2); break;
+    case 4: TFG_EG(4); break;
+    case 8: TFG_EG(8); break;
+    default: TFG_EG(16); break;
+  }
+#undef TFG_EG
+}
+
+template <int MODE>
+int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* dy,
+                     const int* arg, int64_t F, int H, float* dw, int by_perm, hipStream_t s) {
+  const int D = (int)(F / H);
+  auto fits = [&](int v) {
+    return D % v == 0 && ldx % v == 0 && reinterpret_cast<uintptr_t>(x) % (4 * v) == 0 &&
+           reinterpret_cast<uintptr_t>(dy) % (4 * v) == 0 &&
+           (arg == nullptr || reinterpret_cast<uintptr_t>(arg) % (4 * v) == 0);
+  };
+  const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;
+  if (F / vec > kWave) {
+    const int64_t n = g.E * H;
+    edge_grad_simple<MODE><<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(
+        g.rowptr, g.N, g.E, g.col, g.perm, x, ldx, dy, arg, (int)F, H, dw, by_perm);
+    TFG_LAUNCHED("edge_grad_simple");
+    return TFG_OK;
+  }
+  int p2 = 1;
+  while (p2 < F / vec) p2 <<= 1;
+  const int slots = std::min(kWave / p2, 16);
+  // every edge belongs to exactly one work item of either plan (the row plan
+  // keeps its long-row chunks and its whole rows in two lists)
+  auto run = [&](const WorkItem* it, int n) {
+    if (n <= 0) return;
+    dim3 grid((unsigned)((n + kBlock / kWave - 1) / (kBlock / kWave)));
+    const int G = D / vec;
+    if (vec == 4)
+      launch_edge_grad_slots<4, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
+                                      by_perm);
+    else if (vec == 2)
+      launch_edge_grad_slots<2, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
+                                      by_perm);
+    else
+      launch_edge_grad_slots<1, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
+                                      by_perm);
+  };
+  if (use_part_plan(g, F)) {
+    run(g.pexec, g.n_pexec);
+  } else {
+    run(g.heavy, g.n_heavy);
+    run(g.light, g.n_light);
+  }
+  TFG_LAUNCHED("edge_grad_rows");
+  return TFG_OK;
+}
+
+}  // namespace
+
+size_t aggregate_backward_ws_bytes(const Graph& g, const Graph* gt, int64_t F, int64_t H,
+                                   int reduce, int w_order, bool has_w) {
+  size_t b = 256;
+  if (gt == nullptr) return b;
+  const int64_t parts = use_part_plan(*gt, F) ? gt->n_pexec : gt->n_heavy;
+  b += aggregate_partial_bytes(parts, F, TFG_SUM);
+  const size_t ew = align_up(sizeof(float) * (size_t)std::max<int64_t>(g.E * H, 1), 256);
+  if (has_w && w_order == TFG_CSR) b += ew;  // weights moved to edge order
+  if (reduce == TFG_MEAN) b += ew;           // weights / degree in transposed order
+  return b;
+}
+
+int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, int H, int w_order,
+                              const float* x, int64_t ldx, const float* dy, int64_t F,
+                              int reduce, const int32_t* argmax, float* dx, float* dw,
+                              int dw_order, void* ws, hipStream_t s) {
+  const int64_t EH = g.E * H;
+  const unsigned eb = (unsigned)((EH + kBlock - 1) / kBlock);
+  char* base = static_cast<char*>(ws);
+  size_t off = 256;
+  if (dx != nullptr && gt != nullptr) {
+    const int64_t parts = use_part_plan(*gt, F) ? gt->n_pexec : gt->n_heavy;
+    void* part = base + off;
+    off += aggregate_partial_bytes(parts, F, TFG_SUM);
+    const size_t ew = align_up(sizeof(float) * (size_t)std::max<int64_t>(EH, 1), 256);
+    const float* w_coo = w;
+    if (w != nullptr && w_order == TFG_CSR && EH > 0) {
+      float* t = reinterpret_cast<float*>(base + off);
+      off += ew;
+      to_edge_order<<<eb, kBlock, 0, s>>>(g.perm, g.E, H, w, t);
+      TFG_LAUNCHED("to_edge_order");
+      w_coo = t;
+    }
+    if (gt->N > 0 && F > 0) {
+      int rc;
+      if (reduce == TFG_MEAN) {
+        float* wt = reinterpret_cast<float*>(base + off);
+        off += ew;
+        if (EH > 0) {
+          mean_weights<<<eb, kBlock, 0, s>>>(gt->col, gt->perm, g.E, H, g.rowptr, w_coo, wt);
+          TFG_LAUNCHED("mean_weights");
+        }
+        rc = launch_aggregate(*gt, wt, H, TFG_CSR, dy, F, F, TFG_SUM, dx, nullptr, part, s);
+      } else {
+        rc = launch_aggregate(*gt, w_coo, w_coo ? H : 1, TFG_COO, dy, F, F, TFG_SUM, dx, nullptr,
+                              part, s, 1.0f, 0.0f, nullptr, 0,
+                              reduce == TFG_MAX ? argmax : nullptr);
+      }
+      if (rc) return rc;
+    }
+  }
+  if (dw != nullptr && EH > 0 && F > 0) {
+    const int by_perm = dw_order == TFG_COO ? 1 : 0;
+    int rc;
+    if (reduce == TFG_MEAN)
+      rc = launch_edge_grad<kGradMean>(g, x, ldx, dy, nullptr, F, H, dw, by_perm, s);
+    else if (reduce == TFG_MAX)
+      rc = launch_edge_grad<kGradMax>(g, x, ldx, dy, argmax, F, H, dw, by_perm, s);
+    else
+      rc = launch_edge_grad<kGradSum>(g, x, ldx, dy, nullptr, F, H, dw, by_perm, s);
+    if (rc) return rc;
+  }
+  return TFG_OK;
+}
+
+int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
+                                    int H, float* ds, hipStream_t s) {
+  if (g.N == 0 || g.E == 0 || H == 0) return TFG_OK;
+  int hp = 1;
+  while (hp * 2 <= std::min(H, kWave)) hp *= 2;
+  softmax_grad_rows<<<(unsigned)((g.N + 3) / 4), kBlock, 0, s>>>(g.rowptr, g.perm, g.N, alpha,
+                                                                 dalpha, H, hp, ds);
+  TFG_LAUNCHED("softmax_grad_rows");
+  return TFG_OK;
+}
+
+}  // namespace tfg

@@ -48,6 +48,7 @@ struct Graph {
   int64_t N = 0;       // targets
   int64_t N_src = 0;   // sources
   int loops = 0;
+  int transposed = 0;  // built from the reversed edge list (rows are sources)
   int chunk = kDefaultChunk;
   int parts = 1;            // source parts P
   int64_t part_rows = 1;    // sources per part
@@ -112,11 +113,13 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                     float* out_w_csr, float* out_deg, float* dinv_ws, hipStream_t s);
 // aggregate.hip
 // With h != NULL (or scale != 1) every output row becomes scale * sum +
-// alpha * h[row] (sum reduction only): one propagation step.
+// alpha * h[row] (sum reduction only): one propagation step. With mask != NULL
+// ([rows of x, F] int32, sum only) element c of x[col_k] counts only where
+// mask[col_k, c] == perm[k].
 int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const float* x,
                      int64_t F, int64_t ldx, int reduce, float* out, int32_t* argmax,
                      void* ws, hipStream_t s, float scale = 1.0f, float alpha = 0.0f,
-                     const float* h = nullptr, int64_t ldh = 0);
+                     const float* h = nullptr, int64_t ldh = 0, const int32_t* mask = nullptr);
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce);
 // Whether an aggregation over g with F features uses the part plan.
 bool use_part_plan(const Graph& g, int64_t F);
@@ -134,6 +137,16 @@ int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
 // softmax.hip: a_s = a_src . h and a_d = a_dst . h per (node, head)
 int launch_node_projections(const float* h, int64_t N, int H, int D, const float* a_src,
                             const float* a_dst, float* as, float* ad, hipStream_t s);
+// backward.hip: gradients of launch_aggregate (dx over gt, the transposed
+// graph; dw over g) and of launch_segment_softmax.
+size_t aggregate_backward_ws_bytes(const Graph& g, const Graph* gt, int64_t F, int64_t H,
+                                   int reduce, int w_order, bool has_w);
+int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, int H, int w_order,
+                              const float* x, int64_t ldx, const float* dy, int64_t F,
+                              int reduce, const int32_t* argmax, float* dx, float* dw,
+                              int dw_order, void* ws, hipStream_t s);
+int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
+                                    int H, float* ds, hipStream_t s);
 // gat.hip
 size_t gat_aggregate_ws_bytes(int64_t N, int64_t H);
 int max_fused_heads();

@@ -1,0 +1,222 @@
+"""GPU parity of the backward calls (tfg_aggregate_backward, the transposed
+graph, tfg_segment_softmax_backward) against the oracle's gradients, which
+the CPU tests pin to finite differences of the forward oracle.
+
+Bars: the transposed CSR bit-exact; dx and dw within the float32 summation
+bound scaled by the size of the terms, |y - ref| / sum|terms| <= 1e-5, as for
+the forward sums; the softmax gradient likewise, its terms being alpha * |dalpha|
+and alpha * sum(alpha |dalpha|).
+"""
+
+import numpy as np
+import pytest
+
+import graphgen
+
+from test_parity import TOL, assert_scaled, dev, host, same_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tfg():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm device")
+    import paper_2101_11552_amd as lib
+    lib.load()
+    return lib
+
+
+def with_loops(ei, n):
+    return np.concatenate([ei, np.stack([np.arange(n), np.arange(n)])], axis=1)
+
+
+@pytest.mark.parametrize("n,n_src,e,loops,parts,idx", [
+    (3000, 3000, 40_000, False, 1, np.int32),
+    (2000, 500, 30_001, False, 1, np.int64),   # rectangular: 2000 targets, 500 sources
+    (4000, 4000, 90_000, True, 4, np.int32),   # loops, source parts of the transposed keys
+])
+def test_transposed_csr_bit_exact(tfg, orc, n, n_src, e, loops, parts, idx):
+    ei = graphgen.random_graph(e, n, e, n_src=n_src)
+    gt = tfg.tfg_graph_create_transposed(dev(ei.astype(idx)), n, N_src=n_src,
+                                         add_self_loops=loops, src_parts=parts)
+    assert gt.N == n_src and gt.N_src == n
+    full = with_loops(ei, n) if loops else ei
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(gt))
+    r, c, p = orc.csr_by_target(full[::-1], n_src, parts=parts, n_src=n)[:3]
+    assert np.array_equal(rowptr, r) and np.array_equal(col, c) and np.array_equal(perm, p)
+
+
+def _check_backward(tfg, orc, ei, n, n_src, F, reduce, w=None, heads=1, order="coo",
+                    dw_order="coo", parts=1, loops=False, seed=0):
+    import torch
+    x = graphgen.features(seed + 1, n_src, F)
+    dy = graphgen.features(seed + 2, n, F)
+    full = with_loops(ei, n) if loops else ei
+    E = full.shape[1]
+    g = tfg.tfg_graph_create(dev(ei), n, N_src=n_src, add_self_loops=loops, src_parts=parts)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n, N_src=n_src, add_self_loops=loops,
+                                         src_parts=parts)
+    w_dev = None
+    if w is not None:
+        w_dev = dev(w)
+        if order == "csr":
+            perm = host(tfg.tfg_graph_csr(g)[2])
+            w_dev = dev(w.reshape(E, -1)[perm].reshape(w.shape))
+    arg_dev, arg = None, None
+    if reduce == "max":
+        _, arg = orc.aggregate(full, x, n, "max", edge_weight=w, heads=heads)
+        _, arg_dev = tfg.tfg_aggregate(None, dev(x), n, "max", edge_weight=w_dev, heads=heads,
+                                       weight_order=order, graph=g)
+        assert np.array_equal(host(arg_dev), arg), "forward argmax differs"
+    dx, dw = tfg.tfg_aggregate_backward(g, dev(dy), reduce, graph_t=gt, x=dev(x),
+                                        edge_weight=w_dev, heads=heads, weight_order=order,
+                                        argmax=arg_dev, want_dx=True, want_dw=True,
+                                        dw_order=dw_order)
+    torch.cuda.synchronize()
+    rdx, rdw = orc.aggregate_backward(full, x, n, dy, reduce, edge_weight=w, heads=heads, arg=arg)
+    aw = None if w is None else np.abs(w)
+    sdx, sdw = orc.aggregate_backward(full, np.abs(x), n, np.abs(dy), reduce, edge_weight=aw,
+                                      heads=heads, arg=arg)
+    wdx = assert_scaled(host(dx), rdx, sdx, what=f"dx {reduce}")
+    hdw = host(dw)
+    if dw_order == "csr":
+        perm = host(tfg.tfg_graph_csr(g)[2])
+        back = np.empty_like(hdw)
+        back[perm] = hdw
+        hdw = back
+    wdw = assert_scaled(hdw, rdw, sdw, what=f"dw {reduce}")
+    # reproducible bit for bit
+    dx2, dw2 = tfg.tfg_aggregate_backward(g, dev(dy), reduce, graph_t=gt, x=dev(x),
+                                          edge_weight=w_dev, heads=heads, weight_order=order,
+                                          argmax=arg_dev, want_dx=True, want_dw=True,
+                                          dw_order=dw_order)
+    assert same_bits(host(dx), host(dx2)) and same_bits(host(dw), host(dw2))
+    return wdx, wdw
+
+
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+@pytest.mark.parametrize("F", [64, 33])
+def test_backward_square(tfg, orc, reduce, F):
+    n, e = 3000, 60_000
+    # a target hub (long forward row) and, reversed, a source hub (long transposed row)
+    a = graphgen.random_graph(11, n, e // 2, hub=7, hub_edges=3000)
+    b = graphgen.random_graph(12, n, e // 2, hub=11, hub_edges=3000)[::-1]
+    ei = np.ascontiguousarray(np.concatenate([a, b], axis=1))
+    w = graphgen.rng_for(13, 1).uniform(-1.0, 2.0, ei.shape[1]).astype(np.float32)
+    _check_backward(tfg, orc, ei, n, n, F, reduce, w=w, seed=F)
+
+
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_backward_rectangular_unweighted(tfg, orc, reduce):
+    n, n_src, e = 1500, 700, 25_000
+    ei = graphgen.random_graph(21, n, e, n_src=n_src)
+    _check_backward(tfg, orc, ei, n, n_src, 16, reduce, seed=21)
+
+
+@pytest.mark.parametrize("reduce", ["sum", "max"])
+def test_backward_heads_csr_weights(tfg, orc, reduce):
+    n, e, H, D = 2000, 30_000, 4, 16
+    ei = graphgen.random_graph(31, n, e)
+    w = graphgen.rng_for(31, 2).uniform(0.0, 1.0, (e + n, H)).astype(np.float32)
+    _check_backward(tfg, orc, ei, n, n, H * D, reduce, w=w, heads=H, order="csr",
+                    dw_order="csr", loops=True, seed=31)
+
+
+@pytest.mark.parametrize("plan", ["0", "1"])
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_backward_source_parts(tfg, orc, monkeypatch, plan, reduce):
+    # both graphs in 5 source parts, gathered by the row plan or the part plan
+    monkeypatch.setenv("TFG_PART_PLAN", plan)
+    n, e = 5000, 120_000
+    ei = graphgen.random_graph(41, n, e, hub=3, hub_edges=4000)
+    w = graphgen.rng_for(41, 2).uniform(-1.0, 1.0, ei.shape[1] + n).astype(np.float32)
+    _check_backward(tfg, orc, ei, n, n, 32, reduce, w=w, parts=5, loops=True, seed=41)
+
+
+def test_backward_wide_rows_fallback(tfg, orc):
+    # 300 columns = 75 float4 vectors: the per-edge dot products take the simple kernel
+    n, e = 400, 5000
+    ei = graphgen.random_graph(51, n, e)
+    w = graphgen.rng_for(51, 2).uniform(0.5, 1.5, e).astype(np.float32)
+    _check_backward(tfg, orc, ei, n, n, 300, "mean", w=w, seed=51)
+    _check_backward(tfg, orc, ei, n, n, 300, "max", w=w, seed=52)
+
+
+def test_backward_gcn_chain(tfg, orc):
+    # the GCN layer's aggregation with the normalised weights of tfg_gcn_norm
+    n, e, F = 4000, 50_000, 64
+    ei = graphgen.random_graph(61, n, e, hub=5, hub_edges=2000)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n, add_self_loops=True)
+    norm = tfg.tfg_gcn_norm(dev(ei), n, graph=g)
+    w_coo = host(norm["edge_weight"])
+    x = graphgen.features(61, n, F)
+    dy = graphgen.features(62, n, F)
+    dx, dw = tfg.tfg_aggregate_backward(g, dev(dy), "sum", graph_t=gt, x=dev(x),
+                                        edge_weight=norm["edge_weight_csr"], weight_order="csr",
+                                        want_dw=True)
+    full = with_loops(ei, n)
+    # tfg_gcn_norm's weights equal the oracle's bit for bit (test_gcn_norm_bit_exact)
+    rdx, rdw = orc.aggregate_backward(full, x, n, dy, "sum", edge_weight=w_coo)
+    sdx, sdw = orc.aggregate_backward(full, np.abs(x), n, np.abs(dy), "sum",
+                                      edge_weight=np.abs(w_coo))
+    assert_scaled(host(dx), rdx, sdx, what="dx")
+    assert_scaled(host(dw)[:, 0], rdw[:, 0], sdw[:, 0], what="dw")
+
+
+def test_backward_empty_and_isolated(tfg, orc):
+    import torch
+    # no edges: dx = 0, dw empty
+    n = 50
+    ei = np.zeros((2, 0), np.int64)
+    g = tfg.tfg_graph_create(dev(ei), n)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n)
+    dy = dev(graphgen.features(71, n, 8))
+    dx, dw = tfg.tfg_aggregate_backward(g, dy, "mean", graph_t=gt, x=dy, want_dw=True)
+    torch.cuda.synchronize()
+    assert np.all(host(dx) == 0) and dw.shape == (0, 1)
+    # sources without out-edges get exactly 0
+    ei = np.array([[0, 0, 2], [1, 3, 3]])
+    _check_backward(tfg, orc, ei, 5, 5, 4, "sum")
+
+
+def test_backward_argument_errors(tfg):
+    n = 10
+    ei = dev(np.array([[0, 1], [1, 2]]))
+    g = tfg.tfg_graph_create(ei, n)
+    gt = tfg.tfg_graph_create_transposed(ei, n)
+    dy = dev(np.ones((n, 4), np.float32))
+    with pytest.raises(ValueError):  # dx without the transposed graph
+        tfg.tfg_aggregate_backward(g, dy, "sum")
+    with pytest.raises(ValueError):  # max without the forward argmax
+        tfg.tfg_aggregate_backward(g, dy, "max", graph_t=gt)
+    with pytest.raises(ValueError):  # graphs swapped
+        tfg.tfg_aggregate_backward(gt, dy[:n], "sum", graph_t=g)
+    other = tfg.tfg_graph_create_transposed(dev(np.array([[0], [1]])), n)
+    with pytest.raises(ValueError):  # gt of another edge list
+        tfg.tfg_aggregate_backward(g, dy, "sum", graph_t=other)
+    with pytest.raises(ValueError):  # dw without x
+        tfg.tfg_aggregate_backward(g, dy, "sum", want_dx=False, want_dw=True)
+
+
+@pytest.mark.parametrize("H,with_graph", [(1, True), (3, False), (8, True)])
+def test_softmax_backward(tfg, orc, H, with_graph):
+    import torch
+    n, e = 3000, 50_000
+    ei = graphgen.random_graph(81 + H, n, e, hub=9, hub_edges=5000)
+    seg = ei[1]
+    E = ei.shape[1]
+    s = graphgen.features(81, E, H)
+    da = graphgen.features(82, E, H)
+    a64, a32 = orc.segment_softmax(s, seg, n)
+    g = tfg.tfg_graph_create(dev(ei), n) if with_graph else None
+    ds = tfg.tfg_segment_softmax_backward(dev(a32), dev(da), dev(seg), n, graph=g)
+    torch.cuda.synchronize()
+    ref = orc.segment_softmax_backward(a32, da, seg, n)
+    # terms: alpha |dalpha| and alpha * sum over the segment of alpha |dalpha|
+    dot = np.zeros((n, H))
+    np.add.at(dot, seg, a32.astype(np.float64) * np.abs(da))
+    S = a32 * (np.abs(da) + dot[seg])
+    assert_scaled(host(ds), ref, S, what="dscores")

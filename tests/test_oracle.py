@@ -578,3 +578,84 @@ def test_gat_layer_single_edge_and_dense(orc):
             assert np.array_equal(out[t], h3[ei[0][idx[0]]].reshape(-1))  # alpha = 1 exactly
     np.testing.assert_allclose(out, ref.reshape(n, H * D), rtol=1e-12, atol=1e-12)
     assert np.all(S >= np.abs(out) - 1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Backward: finite differences of the forward oracle
+# ---------------------------------------------------------------------------
+
+def _loss(orc, ei, x, n, dy, reduce, w, heads):
+    if reduce == "max":
+        out, _ = orc.aggregate(ei, x, n, "max", edge_weight=w, heads=heads)
+        return float((out.astype(np.float64) * dy).sum())
+    out, _ = orc.aggregate(ei, x, n, reduce, edge_weight=w, heads=heads)
+    return float((out * dy).sum())
+
+
+@pytest.mark.parametrize("reduce,heads", [("sum", 1), ("mean", 1), ("sum", 2), ("max", 1)])
+def test_aggregate_backward_finite_differences(orc, reduce, heads):
+    n, n_src, e, F = 9, 11, 60, 4
+    ei = graphgen.random_graph(61, n, e, n_src=n_src)
+    rng = np.random.default_rng(61)
+    x = rng.standard_normal((n_src, F)).astype(np.float32)
+    w = rng.uniform(0.5, 2.0, (e, heads) if heads > 1 else e).astype(np.float32)
+    dy = rng.standard_normal((n, F))
+    arg = orc.aggregate(ei, x, n, "max", edge_weight=w, heads=heads)[1] if reduce == "max" else None
+    dx, dw = orc.aggregate_backward(ei, x, n, dy, reduce, edge_weight=w, heads=heads, arg=arg)
+    # the loss is linear (piecewise linear for max) in x and in w; the sums are taken in double,
+    # the max of float32 products, whose rounding (2^-24 relative) over a step of 2^-10 leaves
+    # an error near 2^-14 in the quotient
+    eps = 2.0 ** -10
+    rel = 2e-4 if reduce == "max" else 1e-6
+    for (i, c) in [(0, 0), (3, 2), (n_src - 1, 3), (5, 1)]:
+        xp, xm = x.copy(), x.copy()
+        xp[i, c] += eps
+        xm[i, c] -= eps
+        fd = (_loss(orc, ei, xp, n, dy, reduce, w, heads) -
+              _loss(orc, ei, xm, n, dy, reduce, w, heads)) / (2 * eps)
+        assert fd == pytest.approx(dx[i, c], rel=rel, abs=1e-9)
+    for j in [0, 7, e - 1]:
+        for k in range(heads):
+            wp, wm = w.copy(), w.copy()
+            if heads > 1:
+                wp[j, k] += eps
+                wm[j, k] -= eps
+            else:
+                wp[j] += eps
+                wm[j] -= eps
+            fd = (_loss(orc, ei, x, n, dy, reduce, wp, heads) -
+                  _loss(orc, ei, x, n, dy, reduce, wm, heads)) / (2 * eps)
+            assert fd == pytest.approx(dw[j, k], rel=rel, abs=1e-9 if reduce != "max" else 1e-4)
+
+
+def test_aggregate_backward_is_transpose(orc):
+    # dx of a sum aggregation is the aggregation over the reversed edges
+    n, e, F = 40, 500, 5
+    ei = graphgen.random_graph(62, n, e)
+    w = np.random.default_rng(62).standard_normal(e).astype(np.float32)
+    x = graphgen.features(62, n, F)
+    dy = graphgen.features(63, n, F)
+    dx, _ = orc.aggregate_backward(ei, x, n, dy, "sum", edge_weight=w)
+    rev, _ = orc.aggregate(ei[::-1], dy, n, "sum", edge_weight=w)
+    np.testing.assert_allclose(dx, rev, rtol=1e-12, atol=1e-12)
+
+
+def test_softmax_backward_finite_differences(orc):
+    n, e, H = 6, 40, 2
+    seg = graphgen.random_graph(64, n, e)[1]
+    rng = np.random.default_rng(64)
+    s = rng.standard_normal((e, H)).astype(np.float32)
+    da = rng.standard_normal((e, H)).astype(np.float32)
+    a64, a32 = orc.segment_softmax(s, seg, n)
+    ds = orc.segment_softmax_backward(a64.astype(np.float32), da, seg, n)
+    eps = 1e-3
+    for (i, h) in [(0, 0), (5, 1), (e - 1, 0), (17, 1)]:
+        sp, sm = s.astype(np.float64), s.astype(np.float64)
+        sp = sp.copy(); sm = sm.copy()
+        sp[i, h] += eps
+        sm[i, h] -= eps
+        lp = (orc.segment_softmax(sp.astype(np.float32), seg, n)[0] * da).sum()
+        lm = (orc.segment_softmax(sm.astype(np.float32), seg, n)[0] * da).sum()
+        # float32 perturbed scores: compare with the rounding-aware step
+        step = float(np.float32(s[i, h] + eps)) - float(np.float32(s[i, h] - eps))
+        assert (lp - lm) / step == pytest.approx(ds[i, h], rel=2e-4, abs=1e-6)
