@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "aggregated edges/sec (GE/s) and achieved HBM GB/s for fp32 GCN sum-aggregation"
-AGG_SRC = os.path.join(ROOT, "paper_2101_11552_amd", "csrc", "aggregate.hip")
+AGG_SRC = [os.path.join(ROOT, "paper_2101_11552_amd", "csrc", f) for f in ("spmm.h", "aggregate.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_rows_c4.txt")
 
 
@@ -39,8 +39,11 @@ def algorithmic_bytes(E_total: int, N: int, F: int) -> int:
     return E_total * (8 + 4 * F) + N * 4 * F + 4 * (N + 1)
 
 
-def source_sha(path: str) -> str:
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+def source_sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def stored_traffic():
@@ -88,6 +91,168 @@ def cpu_baseline(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
                       f"{n} nodes, F={x.shape[1]}: gcn_norm + sum aggregation, {dt:.1f} s"}
 
 
+def _timed(torch, fn, reps: int, warm: int = 2) -> float:
+    """Average ms of fn() over reps back-to-back calls, by events on the
+    current stream (the stream the library launches on)."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    a0 = torch.cuda.Event(enable_timing=True)
+    a1 = torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(reps):
+        fn()
+    a1.record()
+    torch.cuda.synchronize()
+    return a0.elapsed_time(a1) / reps
+
+
+def _row(name: str, workload: str, ms: float, edges: int | None, nbytes: int | None, **extra):
+    line = {"row": name, "workload": workload, "ms": round(ms, 4)}
+    if edges is not None:
+        line["GE_per_s"] = round(edges / (ms * 1e-3) / 1e9, 3)
+    if nbytes is not None:
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        line["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBPS,
+                            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBPS, 4),
+                            "algorithmic_bytes_per_launch": int(nbytes)}
+    line.update(extra)
+    print(json.dumps(line), flush=True)
+
+
+def run_suite(args):
+    """One JSON line per measured row of the path besides the headline step:
+    the backward aggregation, multi-step propagation, attention (fused and
+    unfused), segment softmax, BatchGraph construction and pooling, and the
+    GCN step on the two small graphs. Each figure is the average of
+    back-to-back calls on resident inputs."""
+    import torch
+    import graphgen
+    import paper_2101_11552_amd as tfg
+
+    tfg.load()
+    dev = torch.device("cuda:0")
+    reps = max(args.steps, 5)
+
+    # --- the large power-law graph: backward aggregation and propagation
+    ei_np, x_np = load_workload(args.cache)
+    N, F = x_np.shape
+    E = ei_np.shape[1]
+    Ep = E + N
+    ei = torch.from_numpy(ei_np).to(dev)
+    x = torch.from_numpy(x_np).to(dev)
+    g = tfg.tfg_graph_create(ei, N, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(ei, N, add_self_loops=True)
+    norm = tfg.tfg_gcn_norm(ei, N, graph=g)
+    dy = torch.randn((N, F), generator=torch.Generator(device=dev).manual_seed(7), device=dev)
+    wl = f"Chung-Lu power-law graph N={N}, E'={Ep} (with self-loops), F={F}"
+    ws = torch.empty(max(tfg.load().tfg_aggregate_backward_ws_bytes(
+        g.handle, gt.handle, F, 1, 0, 0, 1), 256), dtype=torch.uint8, device=dev)
+    ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
+        g, dy, "sum", graph_t=gt, edge_weight=norm["edge_weight"], weight_order="coo",
+        want_dx=True, ws=ws), reps)
+    # per edge: target id, edge id, the weight (by edge id) and a dy row; per source: a dx row
+    _row("backward dx (transposed sum aggregation)", wl, ms, Ep,
+         Ep * (12 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="spmm_rows over the transposed graph",
+         src_parts=gt.info()["src_parts"])
+    ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
+        g, dy, "sum", x=x, want_dx=False, want_dw=True, dw_order="csr", ws=ws), reps)
+    # per edge: source id, an x row, the dw value; per target: a dy row
+    _row("backward dw (per-edge dot products)", wl, ms, Ep,
+         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="edge_grad_rows")
+    K = 3
+    ms = _timed(torch, lambda: tfg.tfg_propagate(g, x, K, alpha=0.1, h=x,
+                                                edge_weight=norm["edge_weight_csr"]), reps)
+    _row(f"APPNP propagation, K={K}, alpha=0.1", wl, ms, K * Ep,
+         K * (Ep * (8 + 4 * F) + N * 8 * F + 4 * (N + 1)), ms_per_step=round(ms / K, 4))
+    del g, gt, norm, dy, ws, ei, x
+    torch.cuda.empty_cache()
+
+    # --- attention on the preferential-attachment graph
+    c = graphgen.config3()
+    n3, H, D = c["N"], c["H"], c["D"]
+    Fh = H * D
+    ei3 = torch.from_numpy(c["edge_index"].astype(np.int32)).to(dev)
+    E3 = ei3.shape[1]
+    h = torch.from_numpy(c["h"]).to(dev)
+    a_s, a_d = torch.from_numpy(c["a_src"]).to(dev), torch.from_numpy(c["a_dst"]).to(dev)
+    g3 = tfg.tfg_graph_create(ei3, n3)
+    wl3 = f"Barabasi-Albert graph (m=7) N={n3}, E={E3}, H={H} heads x {D} dims"
+    ms_f = _timed(torch, lambda: tfg.tfg_gat_aggregate(g3, h, a_s, a_d, c["slope"]), reps)
+
+    def chain():
+        s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
+        _, a_csr = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3, out_csr=True)
+        return tfg.tfg_aggregate(ei3, h, n3, "sum", edge_weight=a_csr, heads=H,
+                                 weight_order="csr", graph=g3)
+    ms_c = _timed(torch, chain, reps)
+    _row("fused attention aggregation", wl3, ms_f, E3,
+         E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
+         kernel="node_projections + gat_rows", unfused_chain_ms=round(ms_c, 4),
+         speedup_vs_unfused=round(ms_c / ms_f, 3))
+    s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
+    ms = _timed(torch, lambda: tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3), reps)
+    # per edge: edge id, the scores (read twice by the kernel, counted once), alpha
+    _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1), kernel="softmax_rows")
+    alpha = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3)
+    dal = torch.randn_like(alpha)
+    ms = _timed(torch, lambda: tfg.tfg_segment_softmax_backward(alpha, dal, ei3[1], n3, graph=g3),
+                reps)
+    _row("segment softmax backward", wl3, ms, E3, E3 * (4 + 12 * H) + 4 * (n3 + 1),
+         kernel="softmax_grad_rows")
+    del g3, ei3, h, s, alpha, dal
+    torch.cuda.empty_cache()
+
+    # --- mini-batch of small graphs: BatchGraph, 3 GCN layers, pooling
+    c = graphgen.config5()
+    sizes, graphs = c["sizes"], c["graphs"]
+    G, Fb = c["G"], c["F"]
+    nc = torch.from_numpy(sizes.astype(np.int32)).to(dev)
+    ec = torch.from_numpy(np.array([gr.shape[1] for gr in graphs], np.int32)).to(dev)
+    local = torch.from_numpy(np.concatenate(graphs, axis=1).astype(np.int32)).to(dev)
+    Nb = int(sizes.sum())
+    Eb = local.shape[1]
+    xb = torch.from_numpy(c["x"]).to(dev)
+    wl5 = f"{G} graphs, {Nb} nodes, {Eb} edges (+ self-loops), F={Fb}"
+    ms = _timed(torch, lambda: tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False), reps)
+    _row("BatchGraph construction", wl5, ms, Eb,
+         Eb * 16 + G * 8 + Nb * 4, kernel="counts_to_int + scans + reindex_edges + fill_graph_index")
+
+    def batch_step():
+        bei, bgi, _, _ = tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False)
+        gb = tfg.tfg_graph_create(bei, Nb, add_self_loops=True)
+        nb = tfg.tfg_gcn_norm(bei, Nb, graph=gb, out_edge_index=False, out_edge_weight=False,
+                              out_deg=False)
+        hb = xb
+        for _ in range(c["layers"]):
+            hb = tfg.tfg_aggregate(None, hb, Nb, "sum", edge_weight=nb["edge_weight_csr"],
+                                   weight_order="csr", graph=gb)
+        return [tfg.tfg_segment_pool(hb, bgi, G, r, validate=False) for r in ("sum", "mean", "max")]
+    ms = _timed(torch, batch_step, reps)
+    _row("mini-batch step: BatchGraph + CSR + gcn_norm + 3 GCN layers + 3 pools", wl5, ms,
+         3 * (Eb + Nb), None)
+    gi = torch.from_numpy(c["graph_index"].astype(np.int32)).to(dev)
+    ms = _timed(torch, lambda: tfg.tfg_segment_pool(xb, gi, G, "sum", validate=False), reps)
+    _row("segment pool (sum)", wl5, ms, None, Nb * 4 * Fb + Nb * 4 + G * 4 * Fb,
+         kernel="segment_bounds + pool_rows")
+
+    # --- the GCN step on the two small uniform graphs
+    for cfg in (graphgen.config1(), graphgen.config2()):
+        n, Fc = cfg["N"], cfg["F"]
+        eic = torch.from_numpy(cfg["edge_index"].astype(np.int32)).to(dev)
+        xc = torch.from_numpy(cfg["x"]).to(dev)
+        Ec = eic.shape[1] + n
+
+        def gcn_step():
+            gc = tfg.tfg_graph_create(eic, n, add_self_loops=True)
+            nm = tfg.tfg_gcn_norm(eic, n, graph=gc)
+            return tfg.tfg_aggregate(None, xc, n, "sum", edge_weight=nm["edge_weight_csr"],
+                                     weight_order="csr", graph=gc)
+        ms = _timed(torch, gcn_step, reps)
+        _row("GCN step: CSR + gcn_norm + sum aggregation", f"{cfg['name']}: uniform graph N={n}, "
+             f"E'={Ec}, F={Fc}", ms, Ec, None)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -98,11 +263,16 @@ def main():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--cache", default=None, help="npz file to reuse the generated graph")
+    ap.add_argument("--suite", action="store_true",
+                    help="instead of the headline line, one line per other measured row")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported",
               file=sys.stderr)
         sys.exit(2)
+    if args.suite:
+        run_suite(args)
+        return
 
     import torch
     import paper_2101_11552_amd as tfg
