@@ -380,7 +380,7 @@ def main():
                         "N=232965, E=114.6M directed edges + N self-loops, F=128, "
                         "step = COO->CSR + gcn_norm + sum aggregation",
             "N": N, "E": E, "E_total": E_total, "F": F, "seed": 1004,
-            "row_chunk": int(os.environ.get("TFG_ROW_CHUNK", 512)),
+            "row_chunk": int(os.environ.get("TFG_ROW_CHUNK", 128)),
         },
         "stages_ms": {"csr_build": round(avg["create"], 4), "gcn_norm": round(avg["norm"], 4),
                       "aggregate": round(avg["agg"], 4)},

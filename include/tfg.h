@@ -296,7 +296,10 @@ int tfg_gat_edge_scores(const void *edge_index, int index_type, int64_t E, const
  * scores: [E, H]; seg: [E] target ids in [0, N) (normally edge_index + E);
  * out: [E, H] in the caller's edge order; out_csr: NULL or [E, H] in the graph
  * order of g (feeds tfg_aggregate with TFG_CSR weights). g: NULL or a graph
- * whose targets are seg (built from the edge list seg belongs to).
+ * whose targets are seg (built from the edge list seg belongs to). The
+ * maximum and the denominator (double) come out of one online sweep per row;
+ * long rows are cut into chunks whose statistics are combined in chunk order
+ * (workspace: per-chunk statistics, plus the transient graph when g is NULL).
  */
 size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_graph *g);
 int tfg_segment_softmax(const float *scores, int64_t E, int64_t H, const void *seg,
@@ -328,8 +331,13 @@ int tfg_segment_softmax_backward(const float *alpha, const float *dalpha, int64_
  * h: [N, H*D]; a_src, a_dst: [H, D]; H <= 64; out: [N, H*D] (a target
  * without edges gets 0). alpha_out: NULL, or [E', H] to also receive alpha in
  * the caller's edge order (edge ids as in the graph, loops included).
+ * Each row is swept once: the maximum and the denominator (double) are kept
+ * online, rescaled whenever the maximum grows, so the result differs from the
+ * three-step chain only by rounding; rows longer than the graph's chunk are
+ * cut into chunks whose partial results are combined in chunk order.
+ * ws: tfg_gat_aggregate_ws_bytes(g, H, D) bytes.
  */
-size_t tfg_gat_aggregate_ws_bytes(int64_t N, int64_t H);
+size_t tfg_gat_aggregate_ws_bytes(const tfg_graph *g, int64_t H, int64_t D);
 int tfg_gat_aggregate(const tfg_graph *g, const float *h, int64_t H, int64_t D,
                       const float *a_src, const float *a_dst, float slope, float *out,
                       float *alpha_out, void *ws, size_t ws_bytes, tfg_stream_t stream);

@@ -90,7 +90,7 @@ def load():
         "tfg_segment_pool": (ci, [p, i64, i64, i64, p, ci, i64, ci, p, p, ci, p, sz, p]),
         "tfg_batch_graphs_ws_bytes": (sz, [i64]),
         "tfg_propagate_ws_bytes": (sz, [p, i64, i64]),
-        "tfg_gat_aggregate_ws_bytes": (sz, [i64, i64]),
+        "tfg_gat_aggregate_ws_bytes": (sz, [p, i64, i64]),
         "tfg_gat_aggregate": (ci, [p, p, i64, i64, p, p, ctypes.c_float, p, p, p, sz, p]),
         "tfg_propagate": (ci, [p, p, ci, p, i64, i64, i64, ctypes.c_float, p, i64, p, p, sz, p]),
         "tfg_batch_graphs": (ci, [i64, p, p, p, ci, i64, i64, p, p, p, p, ci, p, sz, p]),
@@ -558,7 +558,7 @@ def tfg_gat_aggregate(graph: Graph, h: torch.Tensor, a_src: torch.Tensor, a_dst:
     if out is None:
         out = torch.empty((N, H * D), dtype=torch.float32, device=h.device)
     alpha = torch.empty((graph.E, H), dtype=torch.float32, device=h.device) if want_alpha else None
-    ws = _workspace(lib.tfg_gat_aggregate_ws_bytes(N, H), h.device)
+    ws = _workspace(lib.tfg_gat_aggregate_ws_bytes(graph.handle, H, D), h.device)
     _check(lib.tfg_gat_aggregate(graph.handle, _ptr(h), H, D, _ptr(a_src), _ptr(a_dst),
                                  float(slope), _ptr(out), _ptr(alpha), _ptr(ws), ws.numel(),
                                  _stream(h.device)))

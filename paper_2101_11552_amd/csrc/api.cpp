@@ -387,9 +387,12 @@ int tfg_gat_edge_scores(const void* edge_index, int index_type, int64_t E, const
 }
 
 size_t tfg_segment_softmax_ws_bytes(int64_t E, int64_t H, int64_t N, const tfg_graph* g) {
-  (void)H;
-  if (E < 0 || N < 0) return 0;
-  return g ? 256 : graph_total_bytes(E, N, choose_parts(E, N, 1, 0));
+  if (E < 0 || N < 0 || H < 1) return 0;
+  if (g) return row_stats_bytes(g->g.n_heavy, H) + 256;
+  // a transient graph, then the statistics of its chunks (at most the plan's capacity)
+  const int parts = choose_parts(E, N, 1, 0);
+  const int64_t cap = graph_layout(E, N, parts, default_chunk()).cap_heavy;
+  return graph_total_bytes(E, N, parts) + row_stats_bytes(cap, H) + 256;
 }
 
 int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* seg, int index_type,
@@ -415,7 +418,8 @@ int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* s
     rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
     if (rc) return rc;
   }
-  rc = launch_segment_softmax(*gp, scores, (int)H, out, out_csr, s);
+  void* stats = c.take(row_stats_bytes(gp->n_heavy, H));
+  rc = launch_segment_softmax(*gp, scores, (int)H, out, out_csr, stats, s);
   if (rc) return rc;
   if (!g) TFG_HIP(hipStreamSynchronize(s));
   return TFG_OK;
@@ -510,7 +514,8 @@ int tfg_segment_softmax_backward(const float* alpha, const float* dalpha, int64_
     rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
     if (rc) return rc;
   }
-  rc = launch_segment_softmax_backward(*gp, alpha, dalpha, (int)H, dscores, s);
+  void* stats = c.take(row_stats_bytes(gp->n_heavy, H));
+  rc = launch_segment_softmax_backward(*gp, alpha, dalpha, (int)H, dscores, stats, s);
   if (rc) return rc;
   if (!g) TFG_HIP(hipStreamSynchronize(s));
   return TFG_OK;
@@ -649,9 +654,9 @@ int tfg_propagate(const tfg_graph* g, const float* edge_weight, int weight_order
   return TFG_OK;
 }
 
-size_t tfg_gat_aggregate_ws_bytes(int64_t N, int64_t H) {
-  if (N < 0 || H < 0) return 0;
-  return gat_aggregate_ws_bytes(N, H);
+size_t tfg_gat_aggregate_ws_bytes(const tfg_graph* g, int64_t H, int64_t D) {
+  if (!g || H < 1 || D < 1) return 0;
+  return gat_aggregate_ws_bytes(g->g, H, D);
 }
 
 int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
@@ -664,7 +669,7 @@ int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
     return fail(TFG_ERR_INVALID_ARG, "need 1 <= H <= 64 and D >= 1");
   if (gr.N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr || out == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr.N, H))
+  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr, H, D))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
   return launch_gat_aggregate(gr, h, (int)H, (int)D, a_src, a_dst, slope, out, alpha_out, ws,
                               as_stream(stream));

@@ -11,7 +11,8 @@
 //                edge (edge_grad_rows), walking the forward graph so that the
 //                dy row of a target is loaded once.
 // Segment softmax: ds = alpha * (dalpha - sum over the segment of alpha * dalpha)
-// per head, the dot product accumulated in double (softmax_grad_rows).
+// per head, the sum accumulated in double (softmax_grad_items; long rows in
+// chunks whose sums are added in chunk order).
 // Every result has one writer and a fixed summation order: no atomics.
 #include "spmm.h"
 
@@ -190,16 +191,20 @@ __global__ __launch_bounds__(kBlock) void to_edge_order(const int* __restrict__ 
   out[(int64_t)perm[k] * H + h] = in[i];
 }
 
-// One wavefront per segment; lanes are (slot, head) pairs as in softmax_rows.
-__global__ __launch_bounds__(kBlock) void softmax_grad_rows(const int* __restrict__ rowptr,
-                                                            const int* __restrict__ perm,
-                                                            int64_t N,
-                                                            const float* __restrict__ alpha,
-                                                            const float* __restrict__ da, int H,
-                                                            int HP, float* __restrict__ ds) {
-  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
-  if (t >= N) return;
-  const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
+// Softmax gradient over the work items of the row plan; lanes are (slot,
+// head) pairs as in softmax_items. A whole row sums alpha * dalpha per head
+// (double), then writes ds; a chunk of a long row stores its sum,
+// softmax_grad_merge adds the chunks of each long row in chunk order and
+// softmax_grad_write writes their ds.
+__global__ __launch_bounds__(kBlock) void softmax_grad_items(
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
+    int n_light, const int* __restrict__ perm, const float* __restrict__ alpha,
+    const float* __restrict__ da, int H, int HP, float* __restrict__ ds,
+    double* __restrict__ pdot) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy + n_light) return;
+  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
   if (kb == ke) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
@@ -214,11 +219,51 @@ __global__ __launch_bounds__(kBlock) void softmax_grad_rows(const int* __restric
         dot += (double)alpha[i] * (double)da[i];
       }
     for (int off = HP; off < kWave; off <<= 1) dot += __shfl_xor(dot, off);
+    if (pslot >= 0) {
+      if (slot == 0 && act) pdot[(int64_t)pslot * H + h] = dot;
+      continue;
+    }
     for (int k = kb + slot; k < ke; k += SL)
       if (act) {
         const int64_t i = (int64_t)perm[k] * H + h;
         ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
       }
+  }
+}
+
+// One thread per (long row, head): the chunk sums added in chunk order and
+// written back to every chunk slot of the row.
+__global__ __launch_bounds__(kBlock) void softmax_grad_merge(const SplitRow* __restrict__ split,
+                                                             int n_split, int H,
+                                                             double* __restrict__ pdot) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)n_split * H) return;
+  const int r = (int)(i / H), h = (int)(i - (int64_t)r * H);
+  const int s0 = split[r].slot0, nch = split[r].nchunks;
+  double dot = 0.0;
+  for (int j = 0; j < nch; ++j) dot += pdot[(int64_t)(s0 + j) * H + h];
+  for (int j = 0; j < nch; ++j) pdot[(int64_t)(s0 + j) * H + h] = dot;
+}
+
+__global__ __launch_bounds__(kBlock) void softmax_grad_write(
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
+    const float* __restrict__ alpha, const float* __restrict__ da, int H, int HP,
+    const double* __restrict__ pdot, float* __restrict__ ds) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy) return;
+  const WorkItem* itp = heavy + wid;
+  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  for (int hb = 0; hb < H; hb += HP) {
+    const int h = hb + hh;
+    if (h >= H) continue;
+    const double dot = pdot[(int64_t)pslot * H + h];
+    for (int k = kb + slot; k < ke; k += SL) {
+      const int64_t i = (int64_t)perm[k] * H + h;
+      ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
+    }
   }
 }
 
@@ -354,13 +399,28 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
 }
 
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
-                                    int H, float* ds, hipStream_t s) {
+                                    int H, float* ds, void* ws, hipStream_t s) {
   if (g.N == 0 || g.E == 0 || H == 0) return TFG_OK;
   int hp = 1;
   while (hp * 2 <= std::min(H, kWave)) hp *= 2;
-  softmax_grad_rows<<<(unsigned)((g.N + 3) / 4), kBlock, 0, s>>>(g.rowptr, g.perm, g.N, alpha,
-                                                                 dalpha, H, hp, ds);
-  TFG_LAUNCHED("softmax_grad_rows");
+  // the double part of the per-chunk statistics (row_stats_bytes layout)
+  double* pdot = reinterpret_cast<double*>(
+      static_cast<char*>(ws) +
+      align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
+  const int waves = g.n_heavy + g.n_light;
+  if (waves > 0) {
+    softmax_grad_items<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
+        g.heavy, g.n_heavy, g.light, g.n_light, g.perm, alpha, dalpha, H, hp, ds, pdot);
+    TFG_LAUNCHED("softmax_grad_items");
+  }
+  if (g.n_split > 0) {
+    const int64_t n = (int64_t)g.n_split * H;
+    softmax_grad_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split,
+                                                                               g.n_split, H, pdot);
+    softmax_grad_write<<<(unsigned)((g.n_heavy + 3) / 4), kBlock, 0, s>>>(
+        g.heavy, g.n_heavy, g.perm, alpha, dalpha, H, hp, pdot, ds);
+    TFG_LAUNCHED("softmax_grad_merge / softmax_grad_write");
+  }
   return TFG_OK;
 }
 

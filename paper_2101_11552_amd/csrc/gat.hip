@@ -1,19 +1,22 @@
 // Fused attention aggregation (gfx950): for every target row, the score map,
 // the per-head segment softmax and the weighted per-head sum of Fig. 5(a) in
-// one pass over the row's edges. Nothing per edge is written to memory unless
+// one sweep over the row's edges. Nothing per edge is written to memory unless
 // the attention coefficients are requested.
 //
-// One wavefront per target row:
-//   pass 1  lanes = (edge slot, head): per-head maximum of the scores;
-//   pass 2  lanes = (edge slot, features) as in the aggregation kernel: every
-//           lane gathers its V features of the source row and weights them with
-//           exp(score - max) of its own head; the denominator is summed in
-//           double next to the float32 numerators;
-//   pass 3  (optional) lanes = (edge slot, head): alpha = exp(score - max) / den
-//           written in the caller's edge order.
-// The node projections a_s = a_src . h and a_d = a_dst . h come from
+// One wavefront per work item of the graph's row plan (a whole row, or a
+// chunk of a long row). Lanes are (edge slot, V features) as in the
+// aggregation kernel: every lane gathers its V features of the source row and
+// the source's projection a_s for its own head, forms the score
+// s = LeakyReLU(a_s + a_d[t]) and folds it into a running triple (maximum m,
+// denominator d in double, numerators acc): when the maximum grows, d and acc
+// are rescaled by exp(m_old - m_new). Each lane keeps U independent triples;
+// they are merged pairwise, then across the slots. A whole row writes
+// out = acc / d; a chunk writes its triple and gat_merge combines the chunks
+// of each long row in chunk order. The optional coefficients
+// alpha = exp(s - m) / d are written in a second sweep with lanes = (slot,
+// head). The node projections a_s = a_src . h and a_d = a_dst . h come from
 // node_projections() (softmax.hip) and sit in the workspace.
-#include "tfg_internal.h"
+#include "softmax_stats.h"
 
 namespace tfg {
 namespace {
@@ -22,8 +25,6 @@ typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxHeads = 64;
-
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 template <int V>
 __device__ __forceinline__ void load_row(const float* __restrict__ p, float (&v)[V]) {
@@ -38,142 +39,251 @@ __device__ __forceinline__ void load_row(const float* __restrict__ p, float (&v)
   }
 }
 
+// Value held by lane (jbase + slot); jbase is wave-uniform. Runs with the
+// whole wave active.
+template <int SLOTS>
+__device__ __forceinline__ int bcast(int v, int jbase, int slot) {
+  if constexpr (SLOTS == 1) {
+    return __builtin_amdgcn_readlane(v, jbase);
+  } else if constexpr (SLOTS == 2) {
+    int a = __builtin_amdgcn_readlane(v, jbase);
+    int b = __builtin_amdgcn_readlane(v, jbase + 1);
+    return slot ? b : a;
+  } else {
+    return __shfl(v, jbase + slot);
+  }
+}
+
 __device__ __forceinline__ float leaky(float z, float slope) { return z >= 0.0f ? z : slope * z; }
 
+// Merges the triple (m2, d2, a2) into (m, d, a); an empty triple has m = -inf.
+template <int V>
+__device__ __forceinline__ void triple_merge(float& m, double& d, float (&a)[V], float m2,
+                                             double d2, const float (&a2)[V]) {
+#pragma clang fp contract(off)
+  if (m2 == -__builtin_huge_valf()) return;
+  if (m == -__builtin_huge_valf()) {
+    m = m2;
+    d = d2;
+#pragma unroll
+    for (int v = 0; v < V; ++v) a[v] = a2[v];
+    return;
+  }
+  const float mn = m2 > m ? m2 : m;
+  const float x = expf(m - mn), y = expf(m2 - mn);
+  d = d * (double)x + d2 * (double)y;
+#pragma unroll
+  for (int v = 0; v < V; ++v) a[v] = a[v] * x + a2[v] * y;
+  m = mn;
+}
+
 template <int V, int SLOTS>
-__global__ __launch_bounds__(kBlock) void gat_rows(const int* __restrict__ rowptr,
-                                                   const int* __restrict__ col,
-                                                   const int* __restrict__ perm, int64_t N, int H,
-                                                   int D, int HP, const float* __restrict__ as,
-                                                   const float* __restrict__ ad, float slope,
-                                                   const float* __restrict__ h,
-                                                   float* __restrict__ out,
-                                                   float* __restrict__ alpha_out) {
+__global__ __launch_bounds__(kBlock) void gat_items(
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
+    int n_light, const int* __restrict__ col, const int* __restrict__ perm, int H, int D, int HP,
+    const float* __restrict__ as, const float* __restrict__ ad, float slope,
+    const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out,
+    float* __restrict__ pacc, float* __restrict__ pm, double* __restrict__ pd) {
   constexpr int LPS = kWave / SLOTS;
   constexpr int FC = LPS * V;
   constexpr int U = SLOTS * 4 <= kWave ? 4 : kWave / SLOTS;
   __shared__ float s_max[kBlock / kWave][kMaxHeads];
   __shared__ double s_den[kBlock / kWave][kMaxHeads];
   const int wv = threadIdx.x / kWave;
-  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + wv;
-  if (t >= N) return;
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + wv);
+  if (wid >= n_heavy + n_light) return;
+  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int row = uniform(itp->row), kb = uniform(itp->kbeg), ke = uniform(itp->kend);
+  const int pslot = uniform(itp->slot);
   const int lane = threadIdx.x & (kWave - 1);
   const int F = H * D;
-  const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
-  if (kb == ke) {  // a target without edges: zero output
-    for (int f = lane; f < F; f += kWave) out[t * F + f] = 0.0f;
+  if (kb == ke) {  // a target without edges (never a chunk): zero output
+    for (int f = lane; f < F; f += kWave) out[(int64_t)row * F + f] = 0.0f;
     return;
   }
-
-  // pass 1: per-head maximum
-  {
-    const int SL = kWave / HP;
-    const int slot = lane / HP, hh = lane % HP;
-    const bool act = hh < H;
-    const float adt = act ? ad[t * H + hh] : 0.0f;
-    float m = -__builtin_huge_valf();
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) {
-        const float s = leaky(as[(int64_t)col[k] * H + hh] + adt, slope);
-        m = s > m ? s : m;
-      }
-    for (int off = HP; off < kWave; off <<= 1) {
-      const float o = __shfl_xor(m, off);
-      m = o > m ? o : m;
-    }
-    if (slot == 0 && act) s_max[wv][hh] = m;
-  }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-  // pass 2: weighted per-head sums
   const int slot = lane / LPS, sl = lane % LPS;
   for (int f0 = 0; f0 < F; f0 += FC) {
     const int f = f0 + sl * V;
     const bool fok = f < F;
     const int head = fok ? f / D : 0;
-    const float mh = s_max[wv][head];
-    const float adt = ad[t * H + head];
+    const float adt = ad[(int64_t)row * H + head];
     float acc[U][V];
     double den[U];
+    float mx[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       den[u] = 0.0;
+      mx[u] = -__builtin_huge_valf();
 #pragma unroll
       for (int v = 0; v < V; ++v) acc[u][v] = 0.0f;
     }
-    for (int k0 = kb; k0 < ke; k0 += SLOTS * U) {
-      float xv[U][V];
-      float wgt[U];
+    for (int kc = kb; kc < ke; kc += kWave) {
+      const int n = min(kWave, ke - kc);
+      const int cj = lane < n ? __builtin_nontemporal_load(col + kc + lane) : 0;
+      for (int s0 = 0; s0 < n; s0 += SLOTS * U) {
+        float xv[U][V];
+        float sc[U];
+        bool ok[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = k0 + u * SLOTS + slot;
-        const bool ok = k < ke;
-        const int c = ok ? col[k] : 0;
-        wgt[u] = ok ? expf(leaky(as[(int64_t)c * H + head] + adt, slope) - mh) : 0.0f;
-        if (ok && fok) {
-          load_row<V>(h + (int64_t)c * F + f, xv[u]);
-        } else {
+        for (int u = 0; u < U; ++u) {
+          const int jb = s0 + u * SLOTS;
+          ok[u] = jb + slot < n;
+          const int c = bcast<SLOTS>(cj, jb, slot);
+          sc[u] = ok[u] ? leaky(as[(int64_t)c * H + head] + adt, slope) : 0.0f;
+          if (ok[u] && fok) {
+            load_row<V>(h + (int64_t)c * F + f, xv[u]);
+          } else {
 #pragma unroll
-          for (int v = 0; v < V; ++v) xv[u][v] = 0.0f;
+            for (int v = 0; v < V; ++v) xv[u][v] = 0.0f;
+          }
         }
-      }
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        den[u] += (double)wgt[u];
+        for (int u = 0; u < U; ++u) {
+          // one exponential per edge: t = exp(-|s - m|) is the new edge's
+          // weight when the maximum stays, and the rescale factor of the old
+          // sums when it grows (then the new edge weighs 1); from m = -inf
+          // the factor is 0
+          const float dlt = sc[u] - mx[u];
+          const float t = expf(-__builtin_fabsf(dlt));
+          const bool up = dlt > 0.0f;
+          const float r = ok[u] ? (up ? t : 1.0f) : 1.0f;
+          const float w = ok[u] ? (up ? 1.0f : t) : 0.0f;
+          mx[u] = (ok[u] && up) ? sc[u] : mx[u];
+          den[u] = den[u] * (double)r + (double)w;
 #pragma unroll
-        for (int v = 0; v < V; ++v) acc[u][v] = __builtin_fmaf(wgt[u], xv[u][v], acc[u][v]);
+          for (int v = 0; v < V; ++v) acc[u][v] = __builtin_fmaf(acc[u][v], r, w * xv[u][v]);
+        }
       }
     }
 #pragma unroll
     for (int step = 1; step < U; step <<= 1)
 #pragma unroll
-      for (int u = 0; u + step < U; u += 2 * step) {
-        den[u] += den[u + step];
-#pragma unroll
-        for (int v = 0; v < V; ++v) acc[u][v] += acc[u + step][v];
-      }
+      for (int u = 0; u + step < U; u += 2 * step)
+        triple_merge<V>(mx[u], den[u], acc[u], mx[u + step], den[u + step], acc[u + step]);
 #pragma unroll
     for (int off = LPS; off < kWave; off <<= 1) {
-      den[0] += __shfl_xor(den[0], off);
+      float a2[V];
 #pragma unroll
-      for (int v = 0; v < V; ++v) acc[0][v] += __shfl_xor(acc[0][v], off);
+      for (int v = 0; v < V; ++v) a2[v] = __shfl_xor(acc[0][v], off);
+      const float m2 = __shfl_xor(mx[0], off);
+      const double d2 = __shfl_xor(den[0], off);
+      triple_merge<V>(mx[0], den[0], acc[0], m2, d2, a2);
     }
     if (slot == 0 && fok) {
+      if (pslot < 0) {
 #pragma unroll
-      for (int v = 0; v < V; ++v) out[t * F + f + v] = (float)((double)acc[0][v] / den[0]);
-      if (alpha_out != nullptr && f % D == 0) s_den[wv][head] = den[0];
+        for (int v = 0; v < V; ++v)
+          out[(int64_t)row * F + f + v] = (float)((double)acc[0][v] / den[0]);
+        if (alpha_out != nullptr && f % D == 0) {
+          s_max[wv][head] = mx[0];
+          s_den[wv][head] = den[0];
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < V; ++v) pacc[(int64_t)pslot * F + f + v] = acc[0][v];
+        if (f % D == 0) {
+          pm[(int64_t)pslot * H + head] = mx[0];
+          pd[(int64_t)pslot * H + head] = den[0];
+        }
+      }
     }
   }
-  if (alpha_out == nullptr) return;
+  if (alpha_out == nullptr || pslot >= 0) return;
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-  // pass 3: attention coefficients in the caller's edge order
-  {
-    const int SL = kWave / HP;
-    const int slot3 = lane / HP, hh = lane % HP;
-    if (hh < H) {
-      const float adt = ad[t * H + hh];
-      const float mh = s_max[wv][hh];
-      const double dn = s_den[wv][hh];
-      for (int k = kb + slot3; k < ke; k += SL) {
-        const float w = expf(leaky(as[(int64_t)col[k] * H + hh] + adt, slope) - mh);
-        alpha_out[(int64_t)perm[k] * H + hh] = (float)((double)w / dn);
-      }
+  // attention coefficients of a whole row, in the caller's edge order
+  const int SL = kWave / HP;
+  const int slot3 = lane / HP, hh = lane % HP;
+  if (hh < H) {
+    const float adt = ad[(int64_t)row * H + hh];
+    const float mh = s_max[wv][hh];
+    const double dn = s_den[wv][hh];
+    for (int k = kb + slot3; k < ke; k += SL) {
+      const float w = expf(leaky(as[(int64_t)col[k] * H + hh] + adt, slope) - mh);
+      alpha_out[(int64_t)perm[k] * H + hh] = (float)((double)w / dn);
     }
   }
 }
 
+// One wavefront per long row: the chunks' triples merged in chunk order
+// (lanes over the features, one column each), out = acc / d. With alpha
+// requested the row's (m, d) per head is written back to every chunk slot.
+__global__ __launch_bounds__(kBlock) void gat_merge(const SplitRow* __restrict__ split,
+                                                    int n_split, int H, int D,
+                                                    float* __restrict__ pacc,
+                                                    float* __restrict__ pm,
+                                                    double* __restrict__ pd,
+                                                    float* __restrict__ out, int write_back) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_split) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = uniform(split[wid].row), s0 = uniform(split[wid].slot0);
+  const int nch = uniform(split[wid].nchunks);
+  const int F = H * D;
+  for (int f = lane; f < F; f += kWave) {
+    const int head = f / D;
+    float m = -__builtin_huge_valf();
+    double d = 0.0;
+    float a[1] = {0.0f};
+    for (int j = 0; j < nch; ++j) {
+      const float a2[1] = {pacc[(int64_t)(s0 + j) * F + f]};
+      triple_merge<1>(m, d, a, pm[(int64_t)(s0 + j) * H + head], pd[(int64_t)(s0 + j) * H + head],
+                      a2);
+    }
+    out[(int64_t)row * F + f] = (float)((double)a[0] / d);
+    if (write_back && f % D == 0)
+      for (int j = 0; j < nch; ++j) {
+        pm[(int64_t)(s0 + j) * H + head] = m;
+        pd[(int64_t)(s0 + j) * H + head] = d;
+      }
+  }
+}
+
+// Attention coefficients of the chunks of long rows, from their row's (m, d).
+__global__ __launch_bounds__(kBlock) void gat_alpha_chunks(
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ col,
+    const int* __restrict__ perm, int H, int HP, const float* __restrict__ as,
+    const float* __restrict__ ad, float slope, const float* __restrict__ pm,
+    const double* __restrict__ pd, float* __restrict__ alpha_out) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy) return;
+  const WorkItem* itp = heavy + wid;
+  const int row = uniform(itp->row), kb = uniform(itp->kbeg), ke = uniform(itp->kend);
+  const int pslot = uniform(itp->slot);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  if (hh >= H) return;
+  const float adt = ad[(int64_t)row * H + hh];
+  const float mh = pm[(int64_t)pslot * H + hh];
+  const double dn = pd[(int64_t)pslot * H + hh];
+  for (int k = kb + slot; k < ke; k += SL) {
+    const float w = expf(leaky(as[(int64_t)col[k] * H + hh] + adt, slope) - mh);
+    alpha_out[(int64_t)perm[k] * H + hh] = (float)((double)w / dn);
+  }
+}
+
+struct GatArgs {
+  const Graph* g;
+  int H, D, HP;
+  float *as, *ad;
+  float slope;
+  const float* h;
+  float* out;
+  float* alpha_out;
+  float* pacc;
+  float* pm;
+  double* pd;
+};
+
 template <int V>
-void launch_slots(int slots, dim3 grid, hipStream_t s, const Graph& g, int H, int D, int HP,
-                  const float* as, const float* ad, float slope, const float* h, float* out,
-                  float* alpha_out) {
-#define TFG_GAT(SL)                                                                               \
-  gat_rows<V, SL><<<grid, kBlock, 0, s>>>(g.rowptr, g.col, g.perm, g.N, H, D, HP, as, ad, slope, \
-                                          h, out, alpha_out)
+void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
+  const Graph& g = *a.g;
+#define TFG_GAT(SL)                                                                              \
+  gat_items<V, SL><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, \
+                                           a.H, a.D, a.HP, a.as, a.ad, a.slope, a.h, a.out,       \
+                                           a.alpha_out, a.pacc, a.pm, a.pd)
   switch (slots) {
     case 1: TFG_GAT(1); break;
     case 2: TFG_GAT(2); break;
@@ -184,10 +294,31 @@ void launch_slots(int slots, dim3 grid, hipStream_t s, const Graph& g, int H, in
 #undef TFG_GAT
 }
 
+struct GatLayout {
+  size_t as, ad, pacc, pm, pd, total;
+};
+
+GatLayout gat_layout(int64_t N, int64_t H, int64_t F, int64_t n_chunks) {
+  GatLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  L.as = take(sizeof(float) * (size_t)std::max<int64_t>(N * H, 1));
+  L.ad = take(sizeof(float) * (size_t)std::max<int64_t>(N * H, 1));
+  L.pacc = take(sizeof(float) * (size_t)std::max<int64_t>(n_chunks * F, 1));
+  L.pm = take(sizeof(float) * (size_t)std::max<int64_t>(n_chunks * H, 1));
+  L.pd = take(sizeof(double) * (size_t)std::max<int64_t>(n_chunks * H, 1));
+  L.total = off + 256;
+  return L;
+}
+
 }  // namespace
 
-size_t gat_aggregate_ws_bytes(int64_t N, int64_t H) {
-  return align_up(sizeof(float) * (size_t)std::max<int64_t>(2 * N * H, 1), 256) + 256;
+size_t gat_aggregate_ws_bytes(const Graph& g, int64_t H, int64_t D) {
+  return gat_layout(g.N, H, H * D, g.n_heavy).total;
 }
 
 int max_fused_heads() { return kMaxHeads; }
@@ -196,11 +327,24 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
                          const float* a_dst, float slope, float* out, float* alpha_out, void* ws,
                          hipStream_t s) {
   if (g.N == 0 || H == 0 || D == 0) return TFG_OK;
-  float* as = static_cast<float*>(ws);
-  float* ad = as + g.N * H;
-  int rc = launch_node_projections(h, g.N, H, D, a_src, a_dst, as, ad, s);
-  if (rc) return rc;
   const int64_t F = (int64_t)H * D;
+  const GatLayout L = gat_layout(g.N, H, F, g.n_heavy);
+  char* base = static_cast<char*>(ws);
+  GatArgs a;
+  a.g = &g;
+  a.H = H;
+  a.D = D;
+  a.as = reinterpret_cast<float*>(base + L.as);
+  a.ad = reinterpret_cast<float*>(base + L.ad);
+  a.slope = slope;
+  a.h = h;
+  a.out = out;
+  a.alpha_out = alpha_out;
+  a.pacc = reinterpret_cast<float*>(base + L.pacc);
+  a.pm = reinterpret_cast<float*>(base + L.pm);
+  a.pd = reinterpret_cast<double*>(base + L.pd);
+  int rc = launch_node_projections(h, g.N, H, D, a_src, a_dst, a.as, a.ad, s);
+  if (rc) return rc;
   auto fits = [&](int v) {
     return D % v == 0 && reinterpret_cast<uintptr_t>(h) % (4 * v) == 0 &&
            reinterpret_cast<uintptr_t>(out) % (4 * v) == 0;
@@ -212,14 +356,30 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
   const int slots = std::min(kWave / p2, 16);
   int hp = 1;
   while (hp < H) hp <<= 1;  // heads per pass (a power of two, at most 64)
-  dim3 grid((unsigned)((g.N + kBlock / kWave - 1) / (kBlock / kWave)));
-  if (vec == 4)
-    launch_slots<4>(slots, grid, s, g, H, D, hp, as, ad, slope, h, out, alpha_out);
-  else if (vec == 2)
-    launch_slots<2>(slots, grid, s, g, H, D, hp, as, ad, slope, h, out, alpha_out);
-  else
-    launch_slots<1>(slots, grid, s, g, H, D, hp, as, ad, slope, h, out, alpha_out);
-  TFG_LAUNCHED("gat_rows");
+  a.HP = hp;
+  const int waves = g.n_heavy + g.n_light;
+  if (waves > 0) {
+    dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
+    if (vec == 4)
+      launch_slots<4>(slots, grid, s, a);
+    else if (vec == 2)
+      launch_slots<2>(slots, grid, s, a);
+    else
+      launch_slots<1>(slots, grid, s, a);
+    TFG_LAUNCHED("gat_items");
+  }
+  if (g.n_split > 0) {
+    dim3 mgrid((unsigned)((g.n_split + kBlock / kWave - 1) / (kBlock / kWave)));
+    gat_merge<<<mgrid, kBlock, 0, s>>>(g.split, g.n_split, H, D, a.pacc, a.pm, a.pd, out,
+                                       alpha_out != nullptr ? 1 : 0);
+    TFG_LAUNCHED("gat_merge");
+    if (alpha_out != nullptr) {
+      dim3 agrid((unsigned)((g.n_heavy + kBlock / kWave - 1) / (kBlock / kWave)));
+      gat_alpha_chunks<<<agrid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.col, g.perm, H, hp, a.as,
+                                                a.ad, slope, a.pm, a.pd, alpha_out);
+      TFG_LAUNCHED("gat_alpha_chunks");
+    }
+  }
   return TFG_OK;
 }
 

@@ -4,12 +4,10 @@
 //   w'[e]   = (dinv[src] * w[e]) * dinv[tgt]       (float32, left to right)
 // written in the caller's COO order and/or in the graph's CSR order; both
 // orders use the same operands in the same order, so they are bit-identical.
-#include "tfg_internal.h"
+#include "wave.h"
 
 namespace tfg {
 namespace {
-
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Weight of edge id e in the list with appended loops.
 __device__ __forceinline__ float edge_w(const float* __restrict__ w, int64_t E_in, int64_t e) {

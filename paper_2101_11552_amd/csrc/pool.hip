@@ -1,15 +1,13 @@
 // Graph pooling over a sorted node -> graph index (gfx950): segment bounds
 // from the sorted index (with range and order checks), then one wavefront per
 // graph reducing its contiguous node rows (sum / mean / max + argmax).
-#include "tfg_internal.h"
+#include "wave.h"
 
 namespace tfg {
 namespace {
 
 typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 __global__ void fill_goff(int* __restrict__ goff, int64_t n) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -1,15 +1,17 @@
 // Attention map -> reduce -> map (gfx950):
 //   gat scores: per node and head, the dot products with a_src / a_dst; per
 //               edge, LeakyReLU of their sum (the first map);
-//   segment softmax: per target row and head, the maximum, the sum of the
-//               shifted exponentials (the reduce) and the division (the last
-//               map), one wavefront per row.
-#include "tfg_internal.h"
+//   segment softmax: per target row and head, the maximum and the sum of the
+//               shifted exponentials (the reduce, in one online sweep) and the
+//               division (the last map), one wavefront per work item of the
+//               graph's row plan.
+#include "softmax_stats.h"
 
 namespace tfg {
 namespace {
 
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef float f4 __attribute__((ext_vector_type(4)));
 
 // a_s[n, k] = sum_d a_src[k, d] h[n, k*D + d]; a_d likewise (float32, d ascending).
 __global__ __launch_bounds__(kBlock) void node_projections(const float* __restrict__ h, int64_t N,
@@ -34,6 +36,80 @@ __global__ __launch_bounds__(kBlock) void node_projections(const float* __restri
   ad[i] = y;
 }
 
+// The same projections with lanes = (node, V columns): 64 / LPS nodes per
+// wave, the V-column partial dots summed over the G = D / V lanes of each
+// head with xor butterflies (G a power of two dividing LPS).
+template <int V>
+__global__ __launch_bounds__(kBlock) void node_projections_vec(
+    const float* __restrict__ h, int64_t N, int H, int D, int LPS, int G,
+    const float* __restrict__ a_src, const float* __restrict__ a_dst, float* __restrict__ as,
+    float* __restrict__ ad) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const int64_t n = wave * (kWave / LPS) + lane / LPS;
+  const int sl = lane % LPS;
+  const int F = H * D;
+  const int f = sl * V;
+  const bool ok = n < N && f < F;
+  float x = 0.0f, y = 0.0f;
+  if (ok) {
+    float t[V];
+    const float* hv = h + n * F + f;
+    if constexpr (V == 4) {
+      const f4 q = *reinterpret_cast<const f4*>(hv);
+      t[0] = q.x; t[1] = q.y; t[2] = q.z; t[3] = q.w;
+    } else if constexpr (V == 2) {
+      const f2 q = *reinterpret_cast<const f2*>(hv);
+      t[0] = q.x; t[1] = q.y;
+    } else {
+      t[0] = hv[0];
+    }
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      x = __builtin_fmaf(a_src[f + v], t[v], x);
+      y = __builtin_fmaf(a_dst[f + v], t[v], y);
+    }
+  }
+  for (int off = 1; off < G; off <<= 1) {
+    x += __shfl_xor(x, off);
+    y += __shfl_xor(y, off);
+  }
+  if (ok && sl % G == 0) {
+    as[n * H + sl / G] = x;
+    ad[n * H + sl / G] = y;
+  }
+}
+
+// Launches the vectorised projections when the shape allows, else the simple ones.
+void projections(const float* h, int64_t N, int H, int D, const float* a_src, const float* a_dst,
+                 float* as, float* ad, hipStream_t s) {
+  const int F = H * D;
+  int vec = 1;
+  for (int v : {4, 2}) {
+    if (D % v == 0 && reinterpret_cast<uintptr_t>(h) % (4 * v) == 0) {
+      vec = v;
+      break;
+    }
+  }
+  const int G = D / vec;
+  const int lanes = F / vec;
+  if ((G & (G - 1)) == 0 && lanes <= kWave) {
+    int lps = 1;
+    while (lps < lanes) lps <<= 1;
+    const int64_t waves = (N + kWave / lps - 1) / (kWave / lps);
+    const unsigned nb = (unsigned)((waves * kWave + kBlock - 1) / kBlock);
+    if (vec == 4)
+      node_projections_vec<4><<<nb, kBlock, 0, s>>>(h, N, H, D, lps, G, a_src, a_dst, as, ad);
+    else if (vec == 2)
+      node_projections_vec<2><<<nb, kBlock, 0, s>>>(h, N, H, D, lps, G, a_src, a_dst, as, ad);
+    else
+      node_projections_vec<1><<<nb, kBlock, 0, s>>>(h, N, H, D, lps, G, a_src, a_dst, as, ad);
+  } else {
+    node_projections<<<(unsigned)((N * H + kBlock - 1) / kBlock), kBlock, 0, s>>>(h, N, H, D, a_src,
+                                                                                 a_dst, as, ad);
+  }
+}
+
 template <typename IdxT>
 __global__ __launch_bounds__(kBlock) void edge_scores(const IdxT* __restrict__ src,
                                                       const IdxT* __restrict__ tgt, int64_t E,
@@ -56,18 +132,24 @@ __global__ __launch_bounds__(kBlock) void edge_scores(const IdxT* __restrict__ s
   out[i] = z >= 0.0f ? z : slope * z;
 }
 
-// One wavefront per target row. Lanes are (slot, head) pairs: HP heads (a
-// power of two) per pass and 64 / HP edge slots; reductions across the slots
-// of a head use xor butterflies (all lanes end with the same value). The
-// denominator is accumulated in double.
-__global__ __launch_bounds__(kBlock) void softmax_rows(const int* __restrict__ rowptr,
-                                                       const int* __restrict__ perm, int64_t N,
-                                                       const float* __restrict__ s, int H, int HP,
-                                                       float* __restrict__ out,
-                                                       float* __restrict__ out_csr) {
-  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
-  if (t >= N) return;
-  const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
+// One wavefront per work item of the graph's row plan (a whole row, or a
+// chunk of a long row). Lanes are (slot, head) pairs: HP heads (a power of
+// two) per pass and 64 / HP edge slots. Each lane keeps the maximum m of the
+// scores it has seen and d = sum of exp(s - m) (in double), rescaling d when
+// m grows, so the maximum and the denominator come out of one sweep; the
+// slots are combined with xor butterflies (every lane of a head ends with the
+// same pair). A whole row then writes alpha = exp(s - m) / d; a chunk stores
+// its pair, softmax_merge combines the chunks of each long row in order and
+// softmax_write writes their outputs.
+__global__ __launch_bounds__(kBlock) void softmax_items(
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
+    int n_light, const int* __restrict__ perm, const float* __restrict__ s, int H, int HP,
+    float* __restrict__ out, float* __restrict__ out_csr, float* __restrict__ pm,
+    double* __restrict__ pd) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy + n_light) return;
+  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
   if (kb == ke) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
@@ -76,26 +158,73 @@ __global__ __launch_bounds__(kBlock) void softmax_rows(const int* __restrict__ r
     const int h = hb + hh;
     const bool act = h < H;
     float m = -__builtin_huge_valf();
+    double d = 0.0;
     for (int k = kb + slot; k < ke; k += SL)
-      if (act) {
-        const float v = s[(int64_t)perm[k] * H + h];
-        m = v > m ? v : m;
-      }
+      if (act) stat_add(m, d, s[(int64_t)perm[k] * H + h]);
     for (int off = HP; off < kWave; off <<= 1) {
-      const float o = __shfl_xor(m, off);
-      m = o > m ? o : m;
+      const float m2 = __shfl_xor(m, off);
+      const double d2 = __shfl_xor(d, off);
+      stat_merge(m, d, m2, d2);
     }
-    double den = 0.0;
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) den += (double)expf(s[(int64_t)perm[k] * H + h] - m);
-    for (int off = HP; off < kWave; off <<= 1) den += __shfl_xor(den, off);
+    if (pslot >= 0) {
+      if (slot == 0 && act) {
+        pm[(int64_t)pslot * H + h] = m;
+        pd[(int64_t)pslot * H + h] = d;
+      }
+      continue;
+    }
     for (int k = kb + slot; k < ke; k += SL)
       if (act) {
         const int64_t e = perm[k];
-        const float a = (float)((double)expf(s[e * H + h] - m) / den);
+        const float a = (float)((double)expf(s[e * H + h] - m) / d);
         out[e * H + h] = a;
         if (out_csr) out_csr[(int64_t)k * H + h] = a;
       }
+  }
+}
+
+// One thread per (long row, head): the chunks' pairs combined in chunk order;
+// the row's pair is written back to every chunk slot of the row.
+__global__ __launch_bounds__(kBlock) void softmax_merge(const SplitRow* __restrict__ split,
+                                                        int n_split, int H,
+                                                        float* __restrict__ pm,
+                                                        double* __restrict__ pd) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)n_split * H) return;
+  const int r = (int)(i / H), h = (int)(i - (int64_t)r * H);
+  const int s0 = split[r].slot0, nch = split[r].nchunks;
+  float m = -__builtin_huge_valf();
+  double d = 0.0;
+  for (int j = 0; j < nch; ++j) stat_merge(m, d, pm[(int64_t)(s0 + j) * H + h], pd[(int64_t)(s0 + j) * H + h]);
+  for (int j = 0; j < nch; ++j) {
+    pm[(int64_t)(s0 + j) * H + h] = m;
+    pd[(int64_t)(s0 + j) * H + h] = d;
+  }
+}
+
+// The outputs of the chunks of long rows, from their row's pair.
+__global__ __launch_bounds__(kBlock) void softmax_write(
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
+    const float* __restrict__ s, int H, int HP, const float* __restrict__ pm,
+    const double* __restrict__ pd, float* __restrict__ out, float* __restrict__ out_csr) {
+  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy) return;
+  const WorkItem* itp = heavy + wid;
+  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  for (int hb = 0; hb < H; hb += HP) {
+    const int h = hb + hh;
+    if (h >= H) continue;
+    const float m = pm[(int64_t)pslot * H + h];
+    const double d = pd[(int64_t)pslot * H + h];
+    for (int k = kb + slot; k < ke; k += SL) {
+      const int64_t e = perm[k];
+      const float a = (float)((double)expf(s[e * H + h] - m) / d);
+      out[e * H + h] = a;
+      if (out_csr) out_csr[(int64_t)k * H + h] = a;
+    }
   }
 }
 
@@ -104,8 +233,7 @@ __global__ __launch_bounds__(kBlock) void softmax_rows(const int* __restrict__ r
 int launch_node_projections(const float* h, int64_t N, int H, int D, const float* a_src,
                             const float* a_dst, float* as, float* ad, hipStream_t s) {
   if (N * H == 0) return TFG_OK;
-  node_projections<<<(unsigned)((N * H + kBlock - 1) / kBlock), kBlock, 0, s>>>(h, N, H, D, a_src,
-                                                                               a_dst, as, ad);
+  projections(h, N, H, D, a_src, a_dst, as, ad, s);
   TFG_LAUNCHED("node_projections");
   return TFG_OK;
 }
@@ -116,8 +244,7 @@ int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const f
   float* as = proj;
   float* ad = proj + N * H;
   if (N * H > 0) {
-    node_projections<<<(unsigned)((N * H + kBlock - 1) / kBlock), kBlock, 0, s>>>(h, N, H, D, a_src,
-                                                                                 a_dst, as, ad);
+    projections(h, N, H, D, a_src, a_dst, as, ad, s);
     TFG_LAUNCHED("node_projections");
   }
   if (E * H > 0) {
@@ -134,14 +261,33 @@ int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const f
   return TFG_OK;
 }
 
+size_t row_stats_bytes(int64_t n_chunks, int64_t H) {
+  const size_t n = (size_t)std::max<int64_t>(n_chunks * H, 1);
+  return align_up(sizeof(float) * n, 256) + align_up(sizeof(double) * n, 256);
+}
+
 int launch_segment_softmax(const Graph& g, const float* scores, int H, float* out, float* out_csr,
-                           hipStream_t s) {
+                           void* ws, hipStream_t s) {
   if (g.N == 0 || g.E == 0 || H == 0) return TFG_OK;
   int hp = 1;
   while (hp * 2 <= std::min(H, kWave)) hp *= 2;
-  softmax_rows<<<(unsigned)((g.N + 3) / 4), kBlock, 0, s>>>(g.rowptr, g.perm, g.N, scores, H, hp,
-                                                            out, out_csr);
-  TFG_LAUNCHED("softmax_rows");
+  float* pm = static_cast<float*>(ws);
+  double* pd = reinterpret_cast<double*>(
+      static_cast<char*>(ws) + align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
+  const int waves = g.n_heavy + g.n_light;
+  if (waves > 0) {
+    softmax_items<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
+        g.heavy, g.n_heavy, g.light, g.n_light, g.perm, scores, H, hp, out, out_csr, pm, pd);
+    TFG_LAUNCHED("softmax_items");
+  }
+  if (g.n_split > 0) {
+    const int64_t n = (int64_t)g.n_split * H;
+    softmax_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split, g.n_split, H,
+                                                                          pm, pd);
+    softmax_write<<<(unsigned)((g.n_heavy + 3) / 4), kBlock, 0, s>>>(
+        g.heavy, g.n_heavy, g.perm, scores, H, hp, pm, pd, out, out_csr);
+    TFG_LAUNCHED("softmax_merge / softmax_write");
+  }
   return TFG_OK;
 }
 

@@ -16,7 +16,7 @@
 // every output is reproducible bit for bit.
 #pragma once
 
-#include "tfg_internal.h"
+#include "wave.h"
 
 namespace tfg {
 namespace rows {
@@ -64,8 +64,6 @@ __device__ __forceinline__ void store_row(float* __restrict__ p, const float (&v
     __builtin_nontemporal_store(v[0], p);
   }
 }
-
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Value held by lane (jbase + slot); jbase is wave-uniform.
 template <int SLOTS>

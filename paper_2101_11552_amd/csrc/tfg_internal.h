@@ -14,7 +14,7 @@ namespace tfg {
 
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per block for most kernels (4 waves)
-constexpr int kDefaultChunk = 512; // max edges per aggregation work item
+constexpr int kDefaultChunk = 128; // max edges per work item of the row plan
 
 // Device error flag bits (graph->err and the pooling workspace flag).
 constexpr int kErrIndex = 1;
@@ -127,8 +127,11 @@ bool use_part_plan(const Graph& g, int64_t F);
 int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const float* h,
                       int64_t N, int H, int D, const float* a_src, const float* a_dst,
                       float slope, float* out, float* proj_ws, int* err, hipStream_t s);
+// Per-chunk softmax statistics of the long rows: [n_chunks, H] float maxima
+// and double sums (the workspace of the softmax launches).
+size_t row_stats_bytes(int64_t n_chunks, int64_t H);
 int launch_segment_softmax(const Graph& g, const float* scores, int H, float* out,
-                           float* out_csr, hipStream_t s);
+                           float* out_csr, void* ws, hipStream_t s);
 // pool.hip
 int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
                         const void* graph_index, int index_type, int64_t G, int reduce,
@@ -146,9 +149,9 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
                               int reduce, const int32_t* argmax, float* dx, float* dw,
                               int dw_order, void* ws, hipStream_t s);
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
-                                    int H, float* ds, hipStream_t s);
+                                    int H, float* ds, void* ws, hipStream_t s);
 // gat.hip
-size_t gat_aggregate_ws_bytes(int64_t N, int64_t H);
+size_t gat_aggregate_ws_bytes(const Graph& g, int64_t H, int64_t D);
 int max_fused_heads();
 int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const float* a_src,
                          const float* a_dst, float slope, float* out, float* alpha_out, void* ws,
