@@ -148,13 +148,19 @@ def run_suite(args):
     wl = f"Chung-Lu power-law graph N={N}, E'={Ep} (with self-loops), F={F}"
     ws = torch.empty(max(tfg.load().tfg_aggregate_backward_ws_bytes(
         g.handle, gt.handle, F, 1, 0, 0, 1), 256), dtype=torch.uint8, device=dev)
+    # the normalised weights in the transposed graph's order, cached once per graph
+    w_t = tfg.tfg_edge_reorder(norm["edge_weight_csr"], src=g, dst=gt)
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
+        g, dy, "sum", graph_t=gt, edge_weight=w_t, weight_order="csr_t", want_dx=True, ws=ws),
+        reps)
+    ms_coo = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", graph_t=gt, edge_weight=norm["edge_weight"], weight_order="coo",
         want_dx=True, ws=ws), reps)
-    # per edge: target id, edge id, the weight (by edge id) and a dy row; per source: a dx row
+    # per edge: target id, the weight and a dy row; per source: a dx row
     _row("backward dx (transposed sum aggregation)", wl, ms, Ep,
-         Ep * (12 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="spmm_rows over the transposed graph",
-         src_parts=gt.info()["src_parts"])
+         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="spmm_rows over the transposed graph",
+         src_parts=gt.info()["src_parts"], weights="transposed graph order",
+         ms_with_edge_order_weights=round(ms_coo, 4))
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", x=x, want_dx=False, want_dw=True, dw_order="csr", ws=ws), reps)
     # per edge: source id, an x row, the dw value; per target: a dy row

@@ -69,9 +69,11 @@ typedef enum {
 
 typedef enum { TFG_SUM = 0, TFG_MEAN = 1, TFG_MAX = 2 } tfg_reduce;
 typedef enum { TFG_I32 = 0, TFG_I64 = 1 } tfg_index_type;
-/* Order of a per-edge array: the caller's COO edge order, or the graph order
- * of a graph handle (edges grouped by target; see tfg_graph_create). */
-typedef enum { TFG_COO = 0, TFG_CSR = 1 } tfg_edge_order;
+/* Order of a per-edge array: the caller's COO edge order, the graph order of
+ * a graph handle (edges grouped by target; see tfg_graph_create), or, where a
+ * call takes a transposed graph too, that graph's order (edges grouped by
+ * source; see tfg_graph_create_transposed). */
+typedef enum { TFG_COO = 0, TFG_CSR = 1, TFG_CSR_T = 2 } tfg_edge_order;
 
 typedef void *tfg_stream_t; /* hipStream_t */
 
@@ -148,6 +150,19 @@ int tfg_graph_create_transposed(const void *edge_index, int index_type, int64_t 
                                 tfg_stream_t stream, tfg_graph **out);
 int tfg_graph_csr(const tfg_graph *g, int32_t *rowptr, int32_t *col, int32_t *perm,
                   tfg_stream_t stream);
+/*
+ * tfg_edge_reorder: moves a per-edge array [E', H] from the order of `from`
+ *   to the order of `to` (NULL = the caller's COO order, else a graph handle;
+ *   both handles, or the handle and the COO array, must describe the same E'
+ *   edges, e.g. a graph and its transpose). Gathers through the target order's
+ *   perm; graph -> graph goes through COO order in `ws` (E' * H floats, query
+ *   with tfg_edge_reorder_ws_bytes). Per-edge values that depend only on the
+ *   graph structure (normalised weights) are reordered once and cached, like
+ *   the graph itself. out must not overlap in.
+ */
+size_t tfg_edge_reorder_ws_bytes(const tfg_graph *from, const tfg_graph *to, int64_t H);
+int tfg_edge_reorder(const tfg_graph *from, const tfg_graph *to, const float *in, int64_t H,
+                     float *out, void *ws, size_t ws_bytes, tfg_stream_t stream);
 int tfg_graph_segments(const tfg_graph *g, int32_t *segptr, tfg_stream_t stream);
 int tfg_graph_info(const tfg_graph *g, int64_t *E_total, int64_t *N, int64_t *N_src,
                    int64_t *src_parts, int64_t *n_chunks, int64_t *n_rows_split,
@@ -234,7 +249,9 @@ int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float
  * g: the forward graph (tfg_graph_create). gt: NULL, or its transpose
  *   (tfg_graph_create_transposed of the same edge list); required for dx.
  * edge_weight: NULL (all ones) or [E', H] in weight_order (TFG_CSR: the graph
- *   order of g). x: [N_src, F] (leading dimension ldx), needed for dw.
+ *   order of g; TFG_CSR_T: the graph order of gt, which the dx gather reads
+ *   sequentially, see tfg_edge_reorder). x: [N_src, F] (leading dimension
+ *   ldx), needed for dw.
  * argmax: [N, F] int32 from the forward TFG_MAX call (required for TFG_MAX).
  * dx: NULL or [N_src, F] (a source without edges gets 0).
  * dw: NULL or [E', H] in dw_order (TFG_COO: the caller's edge order, loops

@@ -30,7 +30,7 @@ LIB_PATH = os.path.join(_HERE, "libtfg.so")
 TFG_OK, TFG_ERR_INVALID_ARG, TFG_ERR_INDEX_RANGE, TFG_ERR_UNSORTED = 0, 1, 2, 3
 TFG_ERR_TOO_LARGE, TFG_ERR_WORKSPACE, TFG_ERR_HIP = 4, 5, 6
 _REDUCE = {"sum": 0, "mean": 1, "max": 2}
-_ORDER = {"coo": 0, "csr": 1}
+_ORDER = {"coo": 0, "csr": 1, "csr_t": 2}
 
 _lib = None
 
@@ -101,6 +101,8 @@ def load():
                                         p]),
         "tfg_segment_softmax_backward_ws_bytes": (sz, [i64, i64, i64, p]),
         "tfg_segment_softmax_backward": (ci, [p, p, i64, i64, p, ci, i64, p, p, p, sz, p]),
+        "tfg_edge_reorder_ws_bytes": (sz, [p, p, i64]),
+        "tfg_edge_reorder": (ci, [p, p, p, i64, p, p, sz, p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -260,6 +262,27 @@ def tfg_graph_csr(g: Graph):
     perm = torch.empty(g.E, dtype=torch.int32, device=g.device)
     _check(load().tfg_graph_csr(g.handle, _ptr(rowptr), _ptr(col), _ptr(perm), _stream(g.device)))
     return rowptr, col, perm
+
+
+def tfg_edge_reorder(values: torch.Tensor, src: Graph | None = None,
+                     dst: Graph | None = None) -> torch.Tensor:
+    """A per-edge array [E'] or [E', H] moved from the order of ``src`` to the
+    order of ``dst`` (None = the caller's COO edge order)."""
+    lib = load()
+    v = _f32(values, "values")
+    g = src if src is not None else dst
+    if g is None:
+        raise ValueError("at least one graph is needed")
+    H = v.numel() // max(g.E, 1) if g.E else 1
+    if v.numel() != g.E * H:
+        raise ValueError("values must hold E' * H entries")
+    out = torch.empty_like(v)
+    hs = src.handle if src is not None else None
+    hd = dst.handle if dst is not None else None
+    ws = _workspace(lib.tfg_edge_reorder_ws_bytes(hs, hd, H), v.device)
+    _check(lib.tfg_edge_reorder(hs, hd, _ptr(v), H, _ptr(out), _ptr(ws), ws.numel(),
+                                _stream(v.device)))
+    return out
 
 
 def tfg_graph_segments(g: Graph):

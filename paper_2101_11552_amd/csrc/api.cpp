@@ -236,6 +236,28 @@ int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* pe
   return TFG_OK;
 }
 
+size_t tfg_edge_reorder_ws_bytes(const tfg_graph* from, const tfg_graph* to, int64_t H) {
+  if (H < 1) return 0;
+  const int64_t E = from ? from->g.E : (to ? to->g.E : 0);
+  return (from && to) ? align_up(sizeof(float) * (size_t)std::max<int64_t>(E * H, 1), 256) + 256
+                      : 256;
+}
+
+int tfg_edge_reorder(const tfg_graph* from, const tfg_graph* to, const float* in, int64_t H,
+                     float* out, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!from && !to) return fail(TFG_ERR_INVALID_ARG, "no graph handle");
+  if (from && to && (from->g.E != to->g.E || from->g.E_in != to->g.E_in))
+    return fail(TFG_ERR_INVALID_ARG, "the graphs describe different edge lists");
+  const int64_t E = from ? from->g.E : to->g.E;
+  if (H < 1 || E * H >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad H");
+  if (E > 0 && (in == nullptr || out == nullptr)) return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (E > 0 && in == out) return fail(TFG_ERR_INVALID_ARG, "out overlaps in");
+  if (ws == nullptr || ws_bytes < tfg_edge_reorder_ws_bytes(from, to, H))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  return launch_edge_reorder(from ? from->g.perm : nullptr, to ? to->g.perm : nullptr, E, (int)H,
+                             in, out, static_cast<float*>(ws), as_stream(stream));
+}
+
 int tfg_graph_info(const tfg_graph* h, int64_t* E_total, int64_t* N, int64_t* N_src,
                    int64_t* src_parts, int64_t* n_chunks, int64_t* n_rows_split,
                    int64_t* n_part_items) {
@@ -460,8 +482,10 @@ int tfg_aggregate_backward(const tfg_graph* g, const tfg_graph* gt, const float*
   if (rc) return rc;
   if (reduce != TFG_SUM && reduce != TFG_MEAN && reduce != TFG_MAX)
     return fail(TFG_ERR_INVALID_ARG, "bad reduce");
-  if (weight_order != TFG_COO && weight_order != TFG_CSR)
+  if (weight_order != TFG_COO && weight_order != TFG_CSR && weight_order != TFG_CSR_T)
     return fail(TFG_ERR_INVALID_ARG, "bad weight order");
+  if (weight_order == TFG_CSR_T && edge_weight != nullptr && gt == nullptr)
+    return fail(TFG_ERR_INVALID_ARG, "TFG_CSR_T weights need gt");
   if (dw_order != TFG_COO && dw_order != TFG_CSR)
     return fail(TFG_ERR_INVALID_ARG, "bad dw order");
   if (F < 0 || H < 1 || (F > 0 && F % H != 0) || F > kMaxCount || H > kMaxCount)

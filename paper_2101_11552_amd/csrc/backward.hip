@@ -164,11 +164,13 @@ __global__ __launch_bounds__(kBlock) void edge_grad_simple(
 }
 
 // Weights of the transposed graph for the mean gradient, in its graph order:
-// wt[k, h] = w[e_k, h] / deg(t_k) (w = 1 when NULL), e_k = perm[k], t_k = col[k].
+// wt[k, h] = w[e, h] / deg(t_k) (w = 1 when NULL) with e = perm[k] for
+// weights in edge order, e = k for weights already in the transposed order;
+// t_k = col[k].
 __global__ __launch_bounds__(kBlock) void mean_weights(const int* __restrict__ tcol,
                                                        const int* __restrict__ tperm, int64_t E,
                                                        int H, const int* __restrict__ rowptr,
-                                                       const float* __restrict__ w,
+                                                       const float* __restrict__ w, int by_perm,
                                                        float* __restrict__ wt) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= E * H) return;
@@ -176,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void mean_weights(const int* __restrict__ t
   const int h = (int)(i - k * H);
   const int t = tcol[k];
   const float cnt = (float)(rowptr[t + 1] - rowptr[t]);
-  const float wv = w ? w[(int64_t)tperm[k] * H + h] : 1.0f;
+  const float wv = w ? w[(by_perm ? (int64_t)tperm[k] : k) * H + h] : 1.0f;
   wt[i] = wv / cnt;
 }
 
@@ -189,6 +191,17 @@ __global__ __launch_bounds__(kBlock) void to_edge_order(const int* __restrict__ 
   const int64_t k = i / H;
   const int h = (int)(i - k * H);
   out[(int64_t)perm[k] * H + h] = in[i];
+}
+
+// Caller's edge order -> graph order: out[k, h] = in[perm[k], h].
+__global__ __launch_bounds__(kBlock) void to_graph_order(const int* __restrict__ perm, int64_t E,
+                                                         int H, const float* __restrict__ in,
+                                                         float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E * H) return;
+  const int64_t k = i / H;
+  const int h = (int)(i - k * H);
+  out[i] = in[(int64_t)perm[k] * H + h];
 }
 
 // Softmax gradient over the work items of the row plan; lanes are (slot,
@@ -333,6 +346,23 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
 
 }  // namespace
 
+int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
+                        const float* in, float* out, float* tmp, hipStream_t s) {
+  const int64_t n = E * H;
+  if (n == 0) return TFG_OK;
+  const unsigned nb = (unsigned)((n + kBlock - 1) / kBlock);
+  if (perm_from != nullptr && perm_to != nullptr) {
+    to_edge_order<<<nb, kBlock, 0, s>>>(perm_from, E, H, in, tmp);
+    to_graph_order<<<nb, kBlock, 0, s>>>(perm_to, E, H, tmp, out);
+  } else if (perm_from != nullptr) {
+    to_edge_order<<<nb, kBlock, 0, s>>>(perm_from, E, H, in, out);
+  } else {
+    to_graph_order<<<nb, kBlock, 0, s>>>(perm_to, E, H, in, out);
+  }
+  TFG_LAUNCHED("edge reorder");
+  return TFG_OK;
+}
+
 size_t aggregate_backward_ws_bytes(const Graph& g, const Graph* gt, int64_t F, int64_t H,
                                    int reduce, int w_order, bool has_w) {
   size_t b = 256;
@@ -358,13 +388,16 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
     void* part = base + off;
     off += aggregate_partial_bytes(parts, F, TFG_SUM);
     const size_t ew = align_up(sizeof(float) * (size_t)std::max<int64_t>(EH, 1), 256);
-    const float* w_coo = w;
+    // weights for the gather over gt: in edge order (read through gt's perm)
+    // or already in gt's order (read in sequence)
+    const float* wg = w;
+    int wg_order = w_order == TFG_CSR_T ? TFG_CSR : TFG_COO;
     if (w != nullptr && w_order == TFG_CSR && EH > 0) {
       float* t = reinterpret_cast<float*>(base + off);
       off += ew;
       to_edge_order<<<eb, kBlock, 0, s>>>(g.perm, g.E, H, w, t);
       TFG_LAUNCHED("to_edge_order");
-      w_coo = t;
+      wg = t;
     }
     if (gt->N > 0 && F > 0) {
       int rc;
@@ -372,14 +405,14 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
         float* wt = reinterpret_cast<float*>(base + off);
         off += ew;
         if (EH > 0) {
-          mean_weights<<<eb, kBlock, 0, s>>>(gt->col, gt->perm, g.E, H, g.rowptr, w_coo, wt);
+          mean_weights<<<eb, kBlock, 0, s>>>(gt->col, gt->perm, g.E, H, g.rowptr, wg,
+                                             wg_order == TFG_COO ? 1 : 0, wt);
           TFG_LAUNCHED("mean_weights");
         }
         rc = launch_aggregate(*gt, wt, H, TFG_CSR, dy, F, F, TFG_SUM, dx, nullptr, part, s);
       } else {
-        rc = launch_aggregate(*gt, w_coo, w_coo ? H : 1, TFG_COO, dy, F, F, TFG_SUM, dx, nullptr,
-                              part, s, 1.0f, 0.0f, nullptr, 0,
-                              reduce == TFG_MAX ? argmax : nullptr);
+        rc = launch_aggregate(*gt, wg, wg ? H : 1, wg_order, dy, F, F, TFG_SUM, dx, nullptr, part,
+                              s, 1.0f, 0.0f, nullptr, 0, reduce == TFG_MAX ? argmax : nullptr);
       }
       if (rc) return rc;
     }

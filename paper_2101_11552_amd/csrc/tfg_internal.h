@@ -148,6 +148,10 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
                               const float* x, int64_t ldx, const float* dy, int64_t F,
                               int reduce, const int32_t* argmax, float* dx, float* dw,
                               int dw_order, void* ws, hipStream_t s);
+// out[k] = in[perm_to[k]] (COO -> graph), out[perm_from[k]] = in[k] (graph ->
+// COO), or both through tmp ([E, H] floats); either perm may be NULL.
+int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
+                        const float* in, float* out, float* tmp, hipStream_t s);
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
                                     int H, float* ds, void* ws, hipStream_t s);
 // gat.hip

@@ -135,6 +135,45 @@ def test_backward_source_parts(tfg, orc, monkeypatch, plan, reduce):
     _check_backward(tfg, orc, ei, n, n, 32, reduce, w=w, parts=5, loops=True, seed=41)
 
 
+def test_edge_reorder(tfg, orc):
+    n, e, H = 3000, 40_000, 3
+    ei = graphgen.random_graph(91, n, e, hub=4, hub_edges=2000)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n, add_self_loops=True)
+    full = with_loops(ei, n)
+    v = graphgen.features(91, full.shape[1], H)
+    p = orc.csr_by_target(full, n)[2]
+    pt = orc.csr_by_target(full[::-1], n)[2]
+    vg = tfg.tfg_edge_reorder(dev(v), dst=g)                 # COO -> graph order
+    assert same_bits(host(vg), v[p])
+    vt = tfg.tfg_edge_reorder(vg, src=g, dst=gt)              # graph -> transposed order
+    assert same_bits(host(vt), v[pt])
+    back = tfg.tfg_edge_reorder(vt, src=gt)                   # transposed -> COO order
+    assert same_bits(host(back), v)
+
+
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_backward_transposed_order_weights(tfg, orc, reduce):
+    # weights already in the transposed graph's order give the same gradients
+    import torch
+    n, e = 3000, 50_000
+    ei = graphgen.random_graph(92, n, e, hub=6, hub_edges=2500)
+    w = graphgen.rng_for(92, 2).uniform(-1.0, 1.0, ei.shape[1] + n).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n, add_self_loops=True)
+    x = dev(graphgen.features(93, n, 32))
+    dy = dev(graphgen.features(94, n, 32))
+    arg = tfg.tfg_aggregate(None, x, n, "max", edge_weight=dev(w), graph=g)[1] \
+        if reduce == "max" else None
+    wt = tfg.tfg_edge_reorder(dev(w), dst=gt)
+    a, _ = tfg.tfg_aggregate_backward(g, dy, reduce, graph_t=gt, edge_weight=dev(w), argmax=arg)
+    b, _ = tfg.tfg_aggregate_backward(g, dy, reduce, graph_t=gt, edge_weight=wt,
+                                      weight_order="csr_t", argmax=arg)
+    torch.cuda.synchronize()
+    # the same products in the same order: the same bits
+    assert same_bits(host(a), host(b))
+
+
 def test_backward_wide_rows_fallback(tfg, orc):
     # 300 columns = 75 float4 vectors: the per-edge dot products take the simple kernel
     n, e = 400, 5000
