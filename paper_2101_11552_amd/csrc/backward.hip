@@ -43,18 +43,54 @@ using namespace rows;
 
 enum { kGradSum = 0, kGradMean = 1, kGradMax = 2 };
 
+// Sums each of the U values of a lane over the LPS lanes of its slot, U <= LPS
+// (powers of two), with log2(LPS) xor exchanges in which the values are also
+// transposed: at an exchange over offset o while c > 1 values remain, the
+// lane with bit o set keeps the upper half of its values and sends the lower
+// half (the partner the reverse), so c halves. After log2(U) such steps each
+// lane holds one value, the sum for index sl / (LPS / U) over its group; the
+// remaining exchanges are plain butterflies. log2(LPS) + U - 1 shuffles in
+// all, against U * log2(LPS) for U separate trees.
+template <int U, int LPS>
+__device__ __forceinline__ float transpose_sum(float (&p)[U], int sl) {
+  int cnt = U;
+#pragma unroll
+  for (int o = LPS / 2; o >= 1; o >>= 1) {
+    if (cnt > 1) {
+      const bool up = (sl & o) != 0;
+      const int half = cnt / 2;
+#pragma unroll
+      for (int j = 0; j < U / 2; ++j) {
+        if (j < half) {
+          const float send = up ? p[j] : p[j + half];
+          const float keep = up ? p[j + half] : p[j];
+          p[j] = keep + __shfl_xor(send, o);
+        }
+      }
+      cnt = half;
+    } else {
+      p[0] += __shfl_xor(p[0], o);
+    }
+  }
+  return p[0];
+}
+
 // dw for the work items of the forward graph. Lanes are (edge slot, V
-// columns); each lane keeps its V columns of g[t] in registers, and a slot's
-// partial dot products are summed over the G lanes of each head with a
-// shift-down tree (the head's first lane holds the result).
-template <int V, int SLOTS, int MODE>
+// columns); each lane keeps its V columns of g[t] in registers. With one head
+// (WHOLE) the U partial dot products of a lane are summed over the slot with
+// transpose_sum; with several heads they are summed over the G lanes of each
+// head with a shift-down tree (the head's first lane holds the result).
+template <int V, int SLOTS, int MODE, bool WHOLE>
 __global__ __launch_bounds__(kBlock) void edge_grad_rows(
     const WorkItem* __restrict__ items, int n_items, const int* __restrict__ rowptr,
     const int* __restrict__ col, const int* __restrict__ perm, const float* __restrict__ x,
     int64_t ldx, const float* __restrict__ dy, const int* __restrict__ arg, int F, int H, int G,
     float* __restrict__ dw, int dw_by_perm) {
   constexpr int LPS = kWave / SLOTS;
-  constexpr int U = SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
+  // 4 gathers in flight per slot with the transposing reduction keeps the
+  // kernel within 64 VGPRs (8 waves per SIMD); 8 would need 79
+  constexpr int UMAX = WHOLE ? 4 : 8;
+  constexpr int U = SLOTS * UMAX <= kWave ? UMAX : kWave / SLOTS;
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_items) return;
   const int lane = threadIdx.x & (kWave - 1);
@@ -114,19 +150,32 @@ __global__ __launch_bounds__(kBlock) void edge_grad_rows(
         }
         p[u] = acc;
       }
-      for (int off = 1; off < G; off <<= 1)
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const float o = __shfl_down(p[u], off);
-          if (r + off < G) p[u] += o;
+      if constexpr (WHOLE) {
+        // lane sl ends with the dot product of edge slot u = sl / (LPS / U)
+        constexpr int STRIDE = LPS / U;
+        const int u = sl / STRIDE;
+        const int j = s0 + u * SLOTS + slot;
+        const int pu = need_perm ? __shfl(pj, j & (kWave - 1)) : 0;
+        const float val = transpose_sum<U, LPS>(p, sl);
+        if (sl % STRIDE == 0 && j < n) {
+          const int64_t e = dw_by_perm ? pu : kb + j;
+          dw[e] = val;
         }
-      if (r == 0 && fok) {
+      } else {
+        for (int off = 1; off < G; off <<= 1)
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (ok[u]) {
-            const int64_t e = dw_by_perm ? pe[u] : kb + s0 + u * SLOTS + slot;
-            dw[e * H + head] = p[u];
+          for (int u = 0; u < U; ++u) {
+            const float o = __shfl_down(p[u], off);
+            if (r + off < G) p[u] += o;
           }
+        if (r == 0 && fok) {
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            if (ok[u]) {
+              const int64_t e = dw_by_perm ? pe[u] : kb + s0 + u * SLOTS + slot;
+              dw[e * H + head] = p[u];
+            }
+        }
       }
     }
   }
@@ -280,14 +329,14 @@ __global__ __launch_bounds__(kBlock) void softmax_grad_write(
   }
 }
 
-template <int V, int MODE>
+template <int V, int MODE, bool WHOLE>
 void launch_edge_grad_slots(int slots, dim3 grid, hipStream_t s, const WorkItem* items,
                             int n_items, const Graph& g, const float* x, int64_t ldx,
                             const float* dy, const int* arg, int F, int H, int G, float* dw,
                             int by_perm) {
-#define TFG_EG(SL)                                                                             \
-  edge_grad_rows<V, SL, MODE><<<grid, kBlock, 0, s>>>(items, n_items, g.rowptr, g.col, g.perm, \
-                                                      x, ldx, dy, arg, F, H, G, dw, by_perm)
+#define TFG_EG(SL)                                                                      \
+  edge_grad_rows<V, SL, MODE, WHOLE><<<grid, kBlock, 0, s>>>(                           \
+      items, n_items, g.rowptr, g.col, g.perm, x, ldx, dy, arg, F, H, G, dw, by_perm)
   switch (slots) {
     case 1: TFG_EG(1); break;
     case 2: TFG_EG(2); break;
@@ -324,15 +373,27 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
     if (n <= 0) return;
     dim3 grid((unsigned)((n + kBlock / kWave - 1) / (kBlock / kWave)));
     const int G = D / vec;
-    if (vec == 4)
-      launch_edge_grad_slots<4, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
-                                      by_perm);
-    else if (vec == 2)
-      launch_edge_grad_slots<2, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
-                                      by_perm);
-    else
-      launch_edge_grad_slots<1, MODE>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F, H, G, dw,
-                                      by_perm);
+    if (H == 1) {
+      if (vec == 4)
+        launch_edge_grad_slots<4, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                              H, G, dw, by_perm);
+      else if (vec == 2)
+        launch_edge_grad_slots<2, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                              H, G, dw, by_perm);
+      else
+        launch_edge_grad_slots<1, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                              H, G, dw, by_perm);
+    } else {
+      if (vec == 4)
+        launch_edge_grad_slots<4, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                               H, G, dw, by_perm);
+      else if (vec == 2)
+        launch_edge_grad_slots<2, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                               H, G, dw, by_perm);
+      else
+        launch_edge_grad_slots<1, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
+                                               H, G, dw, by_perm);
+    }
   };
   if (use_part_plan(g, F)) {
     run(g.pexec, g.n_pexec);
