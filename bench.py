@@ -39,6 +39,13 @@ def algorithmic_bytes(E_total: int, N: int, F: int) -> int:
     return E_total * (8 + 4 * F) + N * 4 * F + 4 * (N + 1)
 
 
+def row_chunk() -> int:
+    """Edges per work item of the row plan (the library's default unless
+    TFG_ROW_CHUNK overrides it)."""
+    v = os.environ.get("TFG_ROW_CHUNK")
+    return int(v) if v and int(v) >= 64 else 128
+
+
 def source_sha(paths) -> str:
     h = hashlib.sha256()
     for p in paths:
@@ -57,6 +64,8 @@ def stored_traffic():
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("kernel_source_sha256_16") != source_sha(AGG_SRC):
+        return None
+    if vals.get("row_chunk") != str(row_chunk()):
         return None
     try:
         return int(float(vals["hbm_bytes_per_launch"]))
@@ -194,18 +203,19 @@ def run_suite(args):
     ms_c = _timed(torch, chain, reps)
     _row("fused attention aggregation", wl3, ms_f, E3,
          E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
-         kernel="node_projections + gat_rows", unfused_chain_ms=round(ms_c, 4),
+         kernel="node_projections_vec + gat_items + gat_merge", unfused_chain_ms=round(ms_c, 4),
          speedup_vs_unfused=round(ms_c / ms_f, 3))
     s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3), reps)
     # per edge: edge id, the scores (read twice by the kernel, counted once), alpha
-    _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1), kernel="softmax_rows")
+    _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1),
+         kernel="softmax_items + softmax_merge + softmax_write")
     alpha = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3)
     dal = torch.randn_like(alpha)
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax_backward(alpha, dal, ei3[1], n3, graph=g3),
                 reps)
     _row("segment softmax backward", wl3, ms, E3, E3 * (4 + 12 * H) + 4 * (n3 + 1),
-         kernel="softmax_grad_rows")
+         kernel="softmax_grad_items + softmax_grad_merge + softmax_grad_write")
     del g3, ei3, h, s, alpha, dal
     torch.cuda.empty_cache()
 
@@ -386,7 +396,7 @@ def main():
                         "N=232965, E=114.6M directed edges + N self-loops, F=128, "
                         "step = COO->CSR + gcn_norm + sum aggregation",
             "N": N, "E": E, "E_total": E_total, "F": F, "seed": 1004,
-            "row_chunk": int(os.environ.get("TFG_ROW_CHUNK", 128)),
+            "row_chunk": row_chunk(),
         },
         "stages_ms": {"csr_build": round(avg["create"], 4), "gcn_norm": round(avg["norm"], 4),
                       "aggregate": round(avg["agg"], 4)},

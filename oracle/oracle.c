@@ -23,8 +23,9 @@
  *
  * Parity pins: every function is pinned in the CPU tests against values fixed
  * by the paper or by mathematics (dense brute force, closed forms, library
- * routines, invariants, the paper's worked BatchGraph example); see the test
- * module for the oracle.
+ * routines, invariants, the paper's worked BatchGraph example; the gradients
+ * by central differences of the forward functions and the transpose
+ * identity); see the test module for the oracle.
  */
 #include <math.h>
 #include <stdint.h>
