@@ -279,6 +279,8 @@ def main():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--cache", default=None, help="npz file to reuse the generated graph")
+    ap.add_argument("--src-parts", type=int, default=0,
+                    help="source parts of the graph (0: the library's choice)")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the headline line, one line per other measured row")
     args = ap.parse_args()
@@ -305,7 +307,7 @@ def main():
 
     ei = torch.from_numpy(ei_np).to(dev)
     x = torch.from_numpy(x_np).to(dev)
-    nb, ns = tfg.tfg_graph_bytes(E, N, True)  # source parts chosen by the library
+    nb, ns = tfg.tfg_graph_bytes(E, N, True, src_parts=args.src_parts)
     buf = torch.empty(nb, dtype=torch.uint8, device=dev)
     scratch = torch.empty(ns, dtype=torch.uint8, device=dev)
     out = torch.empty((N, F), dtype=torch.float32, device=dev)
@@ -329,7 +331,8 @@ def main():
         e2 = torch.cuda.Event(enable_timing=True)
         e3 = torch.cuda.Event(enable_timing=True)
         e0.record()
-        g = tfg.tfg_graph_create(ei, N, add_self_loops=True, buf=buf, scratch=scratch)
+        g = tfg.tfg_graph_create(ei, N, add_self_loops=True, src_parts=args.src_parts, buf=buf,
+                                 scratch=scratch)
         e1.record()
         norm = tfg.tfg_gcn_norm(ei, N, graph=g)
         e2.record()

@@ -104,7 +104,8 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
   for (int j = 0; j < 4; ++j) {
     const int64_t e = base + j * kBlock;
     const int64_t ec = e < E_in ? e : (E_in > 0 ? E_in - 1 : 0);
-    const int64_t sv = E_in > 0 ? (int64_t)src[ec] : 0, tv = E_in > 0 ? (int64_t)tgt[ec] : 0;
+    const int64_t sv = E_in > 0 ? (int64_t)__builtin_nontemporal_load(src + ec) : 0;
+    const int64_t tv = E_in > 0 ? (int64_t)__builtin_nontemporal_load(tgt + ec) : 0;
     const bool in = e < E_in;
     // ids were validated when the graph was built; clamped here all the same
     s[j] = in ? ((sv < 0 || sv >= N) ? 0 : (int)sv) : (int)(e - E_in);
@@ -124,12 +125,12 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
     const int64_t e = base + j * kBlock;
     if (e >= E) break;
     if (out_ei) {
-      out_ei[e] = s[j];
-      out_ei[E + e] = t[j];
+      __builtin_nontemporal_store(s[j], out_ei + e);
+      __builtin_nontemporal_store(t[j], out_ei + E + e);
     }
     if (out_w) {
       const float a = ds[j] * we[j];
-      out_w[e] = a * dt[j];
+      __builtin_nontemporal_store(a * dt[j], out_w + e);
     }
   }
 }

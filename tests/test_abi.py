@@ -104,6 +104,32 @@ def test_host_side_argument_errors(lib):
     # gat scores: bad heads
     assert lib.tfg_gat_edge_scores(fake, 0, 10, fake, 5, 0, 4, fake, fake, 0.2, fake, fake,
                                    1 << 20, None) == 1
+    # transposed graph: the same checks as the forward one
+    assert lib.tfg_graph_create_transposed(fake, 0, 10, 4, 5, 1, 0, fake, 1 << 20, fake,
+                                           1 << 20, None, ctypes.byref(h)) == 1
+    assert lib.tfg_graph_create_transposed(fake, 9, 10, 5, 5, 0, 0, fake, 1 << 20, fake,
+                                           1 << 20, None, ctypes.byref(h)) == 1
+    # backward without a forward graph; size query without a graph
+    assert lib.tfg_aggregate_backward(None, None, None, 1, 0, fake, 8, fake, 8, 0, None, fake,
+                                      None, 0, fake, 1 << 20, None) == 1
+    assert lib.tfg_aggregate_backward_ws_bytes(None, None, 8, 1, 0, 0, 0) == 0
+    # reorder with no graph at all
+    assert lib.tfg_edge_reorder(None, None, fake, 1, fake, fake, 1 << 20, None) == 1
+    assert lib.tfg_edge_reorder_ws_bytes(None, None, 0) == 0
+    # softmax gradient: bad H, NULL inputs
+    assert lib.tfg_segment_softmax_backward(fake, fake, 10, 0, fake, 0, 5, None, fake, fake,
+                                            1 << 30, None) == 1
+    assert lib.tfg_segment_softmax_backward(None, fake, 10, 2, fake, 0, 5, None, fake, fake,
+                                            1 << 30, None) == 1
+    # fused attention without a graph
+    assert lib.tfg_gat_aggregate(None, fake, 8, 16, fake, fake, 0.2, fake, None, fake, 1 << 20,
+                                 None) == 1
+    assert lib.tfg_gat_aggregate_ws_bytes(None, 8, 16) == 0
+    # propagation and BatchGraph
+    assert lib.tfg_propagate(None, None, 0, fake, 8, 8, 2, 0.0, None, 0, fake, fake, 1 << 20,
+                             None) == 1
+    assert lib.tfg_batch_graphs(-1, fake, fake, fake, 0, 0, 0, fake, fake, None, None, 1, fake,
+                                1 << 20, None) == 1
 
 
 def test_python_binding_rejects_host_tensors():
