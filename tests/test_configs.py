@@ -107,10 +107,15 @@ def test_batched_pooling(tfg, orc):
     assert same_bits(host(p), ref) and np.array_equal(host(arg), rarg)
 
 
+@pytest.fixture(scope="module")
+def c4():
+    return graphgen.config4(dtype=np.int32)
+
+
 @pytest.mark.timeout(900)
-def test_power_law_full_size(tfg, orc):
+def test_power_law_full_size(tfg, orc, c4):
     import torch
-    c = graphgen.config4(dtype=np.int32)
+    c = c4
     ei, x, n = c["edge_index"], c["x"], c["N"]
     E = ei.shape[1]
     eid = dev(ei)
@@ -186,3 +191,71 @@ def test_gat_attention_fused(tfg, orc):
     out = tfg.tfg_gat_aggregate(g, dev(h), dev(c["a_src"]), dev(c["a_dst"]), c["slope"])
     ref, _, S = orc.gat_layer(ei, h, c["a_src"], c["a_dst"], H, slope=np.float32(c["slope"]))
     assert_scaled(host(out), ref, S, what="c3 fused attention layer")
+
+
+@pytest.mark.timeout(900)
+def test_power_law_backward_and_propagation_full_size(tfg, orc, c4):
+    """The backward aggregation and APPNP propagation at full size, as timed
+    by the benchmark: dx over the transposed graph with the normalised
+    weights in its order, dw in graph order, APPNP K = 3."""
+    import torch
+    ei, x, n = c4["edge_index"], c4["x"], c4["N"]
+    E = ei.shape[1]
+    eid = dev(ei)
+    g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(eid, n, add_self_loops=True)
+    norm = tfg.tfg_gcn_norm(eid, n, graph=g)
+    oei, ow, _ = orc.gcn_norm(ei, n)
+
+    # the transposed graph: rows are sources, stable order of (source, target part)
+    P = gt.info()["src_parts"]
+    R = -(-n // P)
+    trow, tcol, tperm = tfg.tfg_graph_csr(gt)
+    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
+    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
+    assert torch.equal(trow[1:].long() - trow[:-1].long(), torch.bincount(src_full, minlength=n))
+    pl = tperm.long()
+    key = (src_full * P + tgt_full // R)[pl]
+    assert bool((key[1:] >= key[:-1]).all())
+    same_key = key[1:] == key[:-1]
+    assert bool((pl[1:][same_key] > pl[:-1][same_key]).all())
+    assert torch.equal(tcol.long(), tgt_full[pl])
+    del src_full, tgt_full, pl, key, same_key
+
+    w_t = tfg.tfg_edge_reorder(norm["edge_weight_csr"], src=g, dst=gt)
+    assert same_bits(host(w_t), ow[host(tperm)])
+    dy = graphgen.features(2004, n, x.shape[1])
+    xd, dyd = dev(x), dev(dy)
+    dx, _ = tfg.tfg_aggregate_backward(g, dyd, "sum", graph_t=gt, edge_weight=w_t,
+                                       weight_order="csr_t")
+    _, dw = tfg.tfg_aggregate_backward(g, dyd, "sum", x=xd, want_dx=False, want_dw=True,
+                                       dw_order="csr")
+    torch.cuda.synchronize()
+    outdeg = np.bincount(np.concatenate([ei[0], np.arange(n)]), minlength=n)
+    rows = np.unique(np.concatenate([np.argsort(outdeg)[-30:],
+                                     np.random.default_rng(1).choice(n, 1000, replace=False)]))
+    # dx of a sum aggregation is the aggregation over the reversed edges (pinned on the CPU)
+    ref, S = orc.aggregate(oei[::-1], dy, n, "sum", edge_weight=ow, rows=rows)
+    assert_scaled(host(dx)[rows], ref, S, what="c4 dx sampled sources")
+    # dw: sampled graph positions, each a dot product of two rows
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    ks = np.random.default_rng(2).choice(E + n, 4000, replace=False)
+    ts = np.searchsorted(rowptr, ks, side="right") - 1
+    terms = dy[ts].astype(np.float64) * x[col[ks]].astype(np.float64)
+    assert_scaled(host(dw)[ks, 0], terms.sum(1), np.abs(terms).sum(1), what="c4 dw sampled edges")
+
+    # APPNP, K = 3, alpha = 0.1: the K-step call equals three chained steps bit for bit,
+    # and the first step matches the oracle on sampled rows
+    alpha = 0.1
+    w_csr = norm["edge_weight_csr"]
+    z3 = tfg.tfg_propagate(g, xd, 3, alpha=alpha, h=xd, edge_weight=w_csr)
+    z = xd
+    for k in range(3):
+        z = tfg.tfg_propagate(g, z, 1, alpha=alpha, h=xd, edge_weight=w_csr)
+        if k == 0:
+            z1 = host(z)
+    assert same_bits(host(z3), host(z))
+    agg, S = orc.aggregate(oei, x, n, "sum", edge_weight=ow, rows=rows)
+    ref = (1 - np.float64(np.float32(alpha))) * agg + np.float64(np.float32(alpha)) * x[rows]
+    S = (1 - alpha) * S + alpha * np.abs(x[rows])
+    assert_scaled(z1[rows], ref, S, what="c4 APPNP first step")
