@@ -608,14 +608,9 @@ int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts
   int* err = static_cast<int*>(c.take(sizeof(int)));
   if (G == 0) return TFG_OK;
   rc = launch_batch_graphs(G, node_counts, edge_counts, local_edge_index, index_type, E, Nb,
-                           out_edge_index, out_graph_index, node_off, edge_off, sums, err, s);
+                           out_edge_index, out_graph_index, node_off, edge_off, out_node_offsets,
+                           out_edge_offsets, sums, err, s);
   if (rc) return rc;
-  if (out_node_offsets)
-    TFG_HIP(hipMemcpyAsync(out_node_offsets, node_off, sizeof(int) * (G + 1),
-                           hipMemcpyDeviceToDevice, s));
-  if (out_edge_offsets)
-    TFG_HIP(hipMemcpyAsync(out_edge_offsets, edge_off, sizeof(int) * (G + 1),
-                           hipMemcpyDeviceToDevice, s));
   if (validate) {
     int host[3] = {0, 0, 0};
     TFG_HIP(hipMemcpyAsync(&host[0], err, sizeof(int), hipMemcpyDeviceToHost, s));

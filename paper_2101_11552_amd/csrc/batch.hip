@@ -2,7 +2,9 @@
 // per-graph counts (exclusive scans), every local edge id shifted by its
 // graph's node offset, and the node -> graph index. Each edge and node finds
 // its graph by binary search over the offsets (G + 1 entries, L2 resident).
-#include "tfg_internal.h"
+// Up to 16,383 graphs the offsets come from one block and the edges and nodes
+// from one more launch; larger batches use the device-wide scan.
+#include "wave.h"
 
 namespace tfg {
 namespace {
@@ -66,6 +68,100 @@ __global__ __launch_bounds__(kBlock) void fill_graph_index(int64_t Nb, int64_t G
 
 __global__ void zero_flag(int* __restrict__ p) { *p = 0; }
 
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallItems = 16;
+constexpr int64_t kSmallMax = (int64_t)kSmallThreads * kSmallItems;  // G + 1 entries at most
+
+// Both offset arrays of up to kSmallMax - 1 graphs in one block: thread i
+// holds entries [16 i, 16 i + 16), sums them, and a block scan gives its start.
+// Also clears the error word (every later check of the launch ORs into it).
+template <typename IdxT>
+__global__ __launch_bounds__(kSmallThreads) void batch_offsets_small(
+    const IdxT* __restrict__ nodes, const IdxT* __restrict__ edges, int64_t G,
+    int* __restrict__ node_off, int* __restrict__ edge_off, int* __restrict__ out_node_off,
+    int* __restrict__ out_edge_off, int* __restrict__ err) {
+  __shared__ int tmp[kSmallThreads / kWave];
+  const int64_t base = (int64_t)threadIdx.x * kSmallItems;
+  int nv[kSmallItems], ev[kSmallItems];
+  int ns = 0, es = 0;
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i) {
+    const int64_t g = base + i;
+    int64_t n = 0, e = 0;
+    if (g < G) {
+      n = (int64_t)nodes[g];
+      e = (int64_t)edges[g];
+    }
+    const bool b = n < 0 || e < 0 || n >= (int64_t(1) << 31) || e >= (int64_t(1) << 31);
+    bad |= b;
+    nv[i] = b ? 0 : (int)n;
+    ev[i] = b ? 0 : (int)e;
+    ns += nv[i];
+    es += ev[i];
+  }
+  const bool any_bad = __syncthreads_or(bad);
+  int nrun = block_excl_scan<kSmallThreads / kWave>(ns, tmp, nullptr);
+  int erun = block_excl_scan<kSmallThreads / kWave>(es, tmp, nullptr);
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i) {
+    const int64_t g = base + i;
+    if (g <= G) {
+      node_off[g] = nrun;
+      edge_off[g] = erun;
+      if (out_node_off) out_node_off[g] = nrun;
+      if (out_edge_off) out_edge_off[g] = erun;
+    }
+    nrun += nv[i];
+    erun += ev[i];
+  }
+  if (threadIdx.x == 0) *err = any_bad ? kErrIndex : 0;
+}
+
+// Edges and nodes in one launch: thread i reindexes edge i and labels node i.
+template <typename IdxT>
+__global__ __launch_bounds__(kBlock) void batch_fill(const IdxT* __restrict__ src,
+                                                     const IdxT* __restrict__ tgt, int64_t E,
+                                                     int64_t Nb, int64_t G,
+                                                     const int* __restrict__ node_off,
+                                                     const int* __restrict__ edge_off,
+                                                     IdxT* __restrict__ out_src,
+                                                     IdxT* __restrict__ out_tgt,
+                                                     IdxT* __restrict__ gi,
+                                                     int* __restrict__ err) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < E) {
+    const int g = graph_of(edge_off, G, i);
+    const int64_t off = node_off[g], n = (int64_t)node_off[g + 1] - off;
+    const int64_t s = (int64_t)src[i], t = (int64_t)tgt[i];
+    if (s < 0 || s >= n || t < 0 || t >= n) atomicOr(err, kErrIndex);
+    out_src[i] = (IdxT)(s + off);
+    out_tgt[i] = (IdxT)(t + off);
+  }
+  if (i < Nb) gi[i] = (IdxT)graph_of(node_off, G, i);
+}
+
+template <typename IdxT>
+int launch_small(int64_t G, const void* node_counts, const void* edge_counts,
+                 const void* local_edge_index, int64_t E, int64_t Nb, void* out_edge_index,
+                 void* out_graph_index, int* node_off, int* edge_off, int* out_node_off,
+                 int* out_edge_off, int* err, hipStream_t s) {
+  batch_offsets_small<IdxT><<<1, kSmallThreads, 0, s>>>(
+      static_cast<const IdxT*>(node_counts), static_cast<const IdxT*>(edge_counts), G, node_off,
+      edge_off, out_node_off, out_edge_off, err);
+  TFG_LAUNCHED("batch_offsets_small");
+  const int64_t n = std::max(E, Nb);
+  if (n > 0) {
+    const IdxT* ei = static_cast<const IdxT*>(local_edge_index);
+    IdxT* oi = static_cast<IdxT*>(out_edge_index);
+    batch_fill<IdxT><<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(
+        ei, ei + E, E, Nb, G, node_off, edge_off, oi, oi + E, static_cast<IdxT*>(out_graph_index),
+        err);
+    TFG_LAUNCHED("batch_fill");
+  }
+  return TFG_OK;
+}
+
 }  // namespace
 
 size_t batch_ws_bytes(int64_t G) {
@@ -77,7 +173,17 @@ size_t batch_ws_bytes(int64_t G) {
 int launch_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,
                         const void* local_edge_index, int index_type, int64_t E, int64_t Nb,
                         void* out_edge_index, void* out_graph_index, int* node_off, int* edge_off,
-                        int* sums, int* err, hipStream_t s) {
+                        int* out_node_off, int* out_edge_off, int* sums, int* err,
+                        hipStream_t s) {
+  if (G + 1 <= kSmallMax) {
+    if (index_type == TFG_I64)
+      return launch_small<int64_t>(G, node_counts, edge_counts, local_edge_index, E, Nb,
+                                   out_edge_index, out_graph_index, node_off, edge_off,
+                                   out_node_off, out_edge_off, err, s);
+    return launch_small<int32_t>(G, node_counts, edge_counts, local_edge_index, E, Nb,
+                                 out_edge_index, out_graph_index, node_off, edge_off, out_node_off,
+                                 out_edge_off, err, s);
+  }
   zero_flag<<<1, 1, 0, s>>>(err);
   const unsigned gb = (unsigned)((G + 1 + kBlock - 1) / kBlock);
   const unsigned eb = (unsigned)((E + kBlock - 1) / kBlock);
@@ -116,6 +222,12 @@ int launch_batch_graphs(int64_t G, const void* node_counts, const void* edge_cou
                                                        static_cast<int32_t*>(out_graph_index));
   }
   TFG_LAUNCHED("reindex_edges / fill_graph_index");
+  if (out_node_off)
+    TFG_HIP(hipMemcpyAsync(out_node_off, node_off, sizeof(int) * (G + 1), hipMemcpyDeviceToDevice,
+                           s));
+  if (out_edge_off)
+    TFG_HIP(hipMemcpyAsync(out_edge_off, edge_off, sizeof(int) * (G + 1), hipMemcpyDeviceToDevice,
+                           s));
   return TFG_OK;
 }
 

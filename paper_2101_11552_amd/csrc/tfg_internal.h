@@ -162,9 +162,11 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
                          hipStream_t s);
 // batch.hip
 size_t batch_ws_bytes(int64_t G);
+// out_node_off / out_edge_off: NULL or [G + 1] copies of the offsets.
 int launch_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,
                         const void* local_edge_index, int index_type, int64_t E, int64_t Nb,
                         void* out_edge_index, void* out_graph_index, int* node_off, int* edge_off,
-                        int* sums, int* err, hipStream_t s);
+                        int* out_node_off, int* out_edge_off, int* sums, int* err,
+                        hipStream_t s);
 
 }  // namespace tfg

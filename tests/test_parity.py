@@ -359,6 +359,31 @@ def test_batch_graphs_match_oracle(tfg, orc, idx):
     assert np.array_equal(host(eoff), orc.batch_offsets(counts))
 
 
+@pytest.mark.parametrize("G", [16383, 16384, 40000])
+def test_batch_graphs_one_block_and_device_scan(tfg, orc, G):
+    # up to 16,383 graphs the offsets come from one block, above from the device-wide scan
+    rng = graphgen.rng_for(56, 0)
+    sizes = rng.integers(0, 6, G)
+    graphs = []
+    for n in sizes:
+        m = int(rng.integers(0, 2 * n + 1)) if n > 0 else 0
+        graphs.append(rng.integers(0, max(n, 1), (2, m)))
+    counts = np.array([g.shape[1] for g in graphs])
+    local = np.concatenate(graphs, axis=1)
+    ei, gi, noff, eoff = tfg.tfg_batch_graphs(dev(sizes.astype(np.int32)),
+                                              dev(counts.astype(np.int32)),
+                                              dev(local.astype(np.int32)), int(sizes.sum()))
+    ref_ei, ref_gi = orc.batch_graphs(sizes, graphs)
+    assert np.array_equal(host(ei), ref_ei) and np.array_equal(host(gi), ref_gi)
+    assert np.array_equal(host(noff), orc.batch_offsets(sizes))
+    assert np.array_equal(host(eoff), orc.batch_offsets(counts))
+    bad = sizes.copy()
+    bad[G // 2] = -1  # a negative count is reported, whichever path runs
+    with pytest.raises(IndexError):
+        tfg.tfg_batch_graphs(dev(bad.astype(np.int32)), dev(counts.astype(np.int32)),
+                             dev(local.astype(np.int32)), int(sizes.sum()))
+
+
 def test_batch_graphs_paper_example(tfg):
     import json
     import os
