@@ -230,7 +230,11 @@ def run_suite(args):
     Eb = local.shape[1]
     xb = torch.from_numpy(c["x"]).to(dev)
     wl5 = f"{G} graphs, {Nb} nodes, {Eb} edges (+ self-loops), F={Fb}"
-    ms = _timed(torch, lambda: tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False), reps)
+    bout = tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False)
+    bws = torch.empty(max(tfg.load().tfg_batch_graphs_ws_bytes(G), 256), dtype=torch.uint8,
+                      device=dev)
+    ms = _timed(torch, lambda: tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False, out=bout,
+                                                    ws=bws), reps)
     _row("BatchGraph construction", wl5, ms, Eb,
          Eb * 16 + G * 8 + Nb * 4, kernel="counts_to_int + scans + reindex_edges + fill_graph_index")
 
@@ -248,7 +252,11 @@ def run_suite(args):
     _row("mini-batch step: BatchGraph + CSR + gcn_norm + 3 GCN layers + 3 pools", wl5, ms,
          3 * (Eb + Nb), None)
     gi = torch.from_numpy(c["graph_index"].astype(np.int32)).to(dev)
-    ms = _timed(torch, lambda: tfg.tfg_segment_pool(xb, gi, G, "sum", validate=False), reps)
+    pout = torch.empty((G, Fb), dtype=torch.float32, device=dev)
+    pws = torch.empty(max(tfg.load().tfg_segment_pool_ws_bytes(Nb, G), 256), dtype=torch.uint8,
+                      device=dev)
+    ms = _timed(torch, lambda: tfg.tfg_segment_pool(xb, gi, G, "sum", validate=False, out=pout,
+                                                    ws=pws), reps)
     _row("segment pool (sum)", wl5, ms, None, Nb * 4 * Fb + Nb * 4 + G * 4 * Fb,
          kernel="segment_bounds + pool_rows")
 

@@ -495,7 +495,8 @@ def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
 
 
 def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce: str = "sum",
-                     validate: bool = True, out: torch.Tensor | None = None):
+                     validate: bool = True, out: torch.Tensor | None = None,
+                     argmax: torch.Tensor | None = None, ws: torch.Tensor | None = None):
     """Pools node rows x [Nb, F] into G graphs by the sorted graph_index [Nb].
     Returns out [G, F] (and argmax node ids [G, F] for ``reduce="max"``)."""
     lib = load()
@@ -506,8 +507,12 @@ def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce:
     dev = x.device
     if out is None:
         out = torch.empty((G, F), dtype=torch.float32, device=dev)
-    arg = torch.empty((G, F), dtype=torch.int32, device=dev) if red == 2 else None
-    ws = _workspace(lib.tfg_segment_pool_ws_bytes(Nb, G), dev)
+    arg = None
+    if red == 2:
+        arg = argmax if argmax is not None else torch.empty((G, F), dtype=torch.int32, device=dev)
+    need = lib.tfg_segment_pool_ws_bytes(Nb, G)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
     _check(lib.tfg_segment_pool(_ptr(x), Nb, F, ldx, _ptr(gi), _index_type(gi), G, red, _ptr(out),
                                 _ptr(arg), int(validate), _ptr(ws), ws.numel(), _stream(dev)))
     return (out, arg) if red == 2 else out
@@ -515,7 +520,7 @@ def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce:
 
 def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
                      local_edge_index: torch.Tensor, Nb: int | None = None,
-                     validate: bool = True):
+                     validate: bool = True, out=None, ws: torch.Tensor | None = None):
     """BatchGraph of G graphs: (edge_index [2, E], graph_index [Nb], node_offsets [G+1],
     edge_offsets [G+1]). local_edge_index holds graph 0's edges, then graph 1's, ...,
     with ids local to their graph; Nb defaults to node_counts.sum() (one host read)."""
@@ -529,11 +534,18 @@ def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
     if Nb is None:
         Nb = int(nc.sum().item())
     dev = ei.device
-    out_ei = torch.empty_like(ei)
-    gi = torch.empty(Nb, dtype=ei.dtype, device=dev)
-    noff = torch.empty(G + 1, dtype=torch.int32, device=dev)
-    eoff = torch.empty(G + 1, dtype=torch.int32, device=dev)
-    ws = _workspace(lib.tfg_batch_graphs_ws_bytes(G), dev)
+    if out is not None:  # (edge_index, graph_index, node_offsets, edge_offsets) from a prior call
+        out_ei, gi, noff, eoff = out
+    else:
+        out_ei = torch.empty_like(ei)
+        gi = torch.empty(Nb, dtype=ei.dtype, device=dev)
+        noff = torch.empty(G + 1, dtype=torch.int32, device=dev)
+        eoff = torch.empty(G + 1, dtype=torch.int32, device=dev)
+    if out_ei.shape != ei.shape or gi.numel() != Nb or noff.numel() != G + 1 or eoff.numel() != G + 1:
+        raise ValueError("out does not match the batch")
+    need = lib.tfg_batch_graphs_ws_bytes(G)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
     _check(lib.tfg_batch_graphs(G, _ptr(nc), _ptr(ec), _ptr(ei), _index_type(ei), E, Nb,
                                 _ptr(out_ei), _ptr(gi), _ptr(noff), _ptr(eoff), int(validate),
                                 _ptr(ws), ws.numel(), _stream(dev)))

@@ -450,7 +450,9 @@ __global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__
                                                          int chunk, int* __restrict__ counters,
                                                          WorkItem* __restrict__ heavy,
                                                          WorkItem* __restrict__ light,
-                                                         SplitRow* __restrict__ split) {
+                                                         SplitRow* __restrict__ split,
+                                                         int* __restrict__ short_rows,
+                                                         int* __restrict__ long_rows) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int beg = 0, deg = 0;
   if (r < N) {
@@ -463,7 +465,14 @@ __global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__
   const int h0 = wave_reserve(&counters[0], nch);
   const int l0 = wave_reserve(&counters[1], valid && !is_split ? 1 : 0);
   const int s0 = wave_reserve(&counters[2], is_split ? 1 : 0);
+  const bool is_short = valid && deg <= kShortRow;
+  const int q0 = wave_reserve(&counters[5], is_short ? 1 : 0);
+  const int m0 = wave_reserve(&counters[6], valid && !is_split && !is_short ? 1 : 0);
   if (!valid) return;
+  if (is_short)
+    short_rows[q0] = (int)r;
+  else if (!is_split)
+    long_rows[m0] = (int)r;
   if (is_split) {
     for (int j = 0; j < nch; ++j) {
       const int kb = beg + j * chunk;
@@ -711,6 +720,8 @@ GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk) {
   L.split = take(sizeof(SplitRow) * std::max<int64_t>(L.cap_split, 1));
   L.pexec = take(sizeof(WorkItem) * L.cap_pexec);
   L.prows = take(parts > 1 ? sizeof(SplitRow) * N : 0);
+  L.short_rows = take(sizeof(int) * std::max<int64_t>(N, 1));
+  L.long_rows = take(sizeof(int) * std::max<int64_t>(N, 1));
   L.counters = take(sizeof(int) * 8);
   L.total = off;
   return L;
@@ -736,7 +747,8 @@ int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void
   if (rc) return rc;
   if (g.N > 0) {
     build_worklist<<<dim3((unsigned)((g.N + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(
-        g.rowptr, g.N, g.chunk, g.counters, g.heavy, g.light, g.split);
+        g.rowptr, g.N, g.chunk, g.counters, g.heavy, g.light, g.split, g.short_rows,
+        g.long_rows);
     TFG_LAUNCHED("build_worklist");
     if (g.parts > 1) {
       rc = build_part_plan(g, sc, L, s);
@@ -751,6 +763,8 @@ int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void
   g.n_light = host[1];
   g.n_split = host[2];
   g.n_pexec = host[4];
+  g.n_short = host[5];
+  g.n_long = host[6];
   return TFG_OK;
 }
 

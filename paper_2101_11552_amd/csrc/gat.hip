@@ -3,8 +3,10 @@
 // one sweep over the row's edges. Nothing per edge is written to memory unless
 // the attention coefficients are requested.
 //
-// One wavefront per work item of the graph's row plan (a whole row, or a
-// chunk of a long row). Lanes are (edge slot, V features) as in the
+// Rows of at most kShortRow edges go one per edge slot (several per
+// wavefront), with every gather of the row in flight at once. Otherwise one
+// wavefront per work item of the graph's row plan (a whole row, or a chunk of
+// a long row). Lanes are (edge slot, V features) as in the
 // aggregation kernel: every lane gathers its V features of the source row and
 // the source's projection a_s for its own head, forms the score
 // s = LeakyReLU(a_s + a_d[t]) and folds it into a running triple (maximum m,
@@ -77,13 +79,90 @@ __device__ __forceinline__ void triple_merge(float& m, double& d, float (&a)[V],
   m = mn;
 }
 
+// A short row (at most kShortRow edges) per edge slot: the slot's lanes load
+// the row's column ids, scores and feature rows at once, take the maximum,
+// then the weighted sums (denominator in double) in graph order.
+template <int V>
+__device__ __forceinline__ void gat_short_row(int t, int sl, int LPS, const int* __restrict__ rowptr,
+                                              const int* __restrict__ col,
+                                              const int* __restrict__ perm, int H, int D,
+                                              const float* __restrict__ as,
+                                              const float* __restrict__ ad, float slope,
+                                              const float* __restrict__ h, float* __restrict__ out,
+                                              float* __restrict__ alpha_out) {
+  const int F = H * D;
+  const int kb = rowptr[t], n = rowptr[t + 1] - kb;  // 0 <= n <= kShortRow
+  int c[kShortRow];
+#pragma unroll
+  for (int j = 0; j < kShortRow; ++j) c[j] = j < n ? col[kb + j] : 0;
+  for (int f0 = 0; f0 < F; f0 += LPS * V) {
+    const int f = f0 + sl * V;
+    if (f >= F) continue;
+    const int head = f / D;
+    const float adt = ad[(int64_t)t * H + head];
+    float sc[kShortRow], xv[kShortRow][V];
+    float m = -__builtin_huge_valf();
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j) {
+      if (j < n) {
+        sc[j] = leaky(as[(int64_t)c[j] * H + head] + adt, slope);
+        load_row<V>(h + (int64_t)c[j] * F + f, xv[j]);
+        m = sc[j] > m ? sc[j] : m;
+      } else {
+        sc[j] = 0.0f;
+#pragma unroll
+        for (int v = 0; v < V; ++v) xv[j][v] = 0.0f;
+      }
+    }
+    double d = 0.0;
+    float acc[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) acc[v] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j) {
+      sc[j] = j < n ? expf(sc[j] - m) : 0.0f;
+      d += (double)sc[j];
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[v] = __builtin_fmaf(sc[j], xv[j][v], acc[v]);
+    }
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      out[(int64_t)t * F + f + v] = n > 0 ? (float)((double)acc[v] / d) : 0.0f;
+    if (alpha_out != nullptr && f % D == 0)
+#pragma unroll
+      for (int j = 0; j < kShortRow; ++j)
+        if (j < n) alpha_out[(int64_t)perm[kb + j] * H + head] = (float)((double)sc[j] / d);
+  }
+}
+
+// SLOTS short rows per wavefront, one per edge slot (gat_short_row). A kernel
+// of its own: holding a whole short row in registers takes more of them than
+// the sweep of gat_items, whose occupancy it would otherwise lower.
+template <int V, int SLOTS>
+__global__ __launch_bounds__(kBlock) void gat_short(
+    const int* __restrict__ short_rows, int n_short, const int* __restrict__ rowptr,
+    const int* __restrict__ col, const int* __restrict__ perm, int H, int D,
+    const float* __restrict__ as, const float* __restrict__ ad, float slope,
+    const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out) {
+  constexpr int LPS = kWave / SLOTS;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const int64_t i = wave * SLOTS + lane / LPS;
+  if (i < n_short)
+    gat_short_row<V>(short_rows[i], lane % LPS, LPS, rowptr, col, perm, H, D, as, ad, slope, h,
+                     out, alpha_out);
+}
+
+// Wavefronts [0, n_heavy) take the chunks of long rows, [n_heavy, n_heavy +
+// n_long) one other light row each, with the running-triple sweep.
 template <int V, int SLOTS>
 __global__ __launch_bounds__(kBlock) void gat_items(
-    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
-    int n_light, const int* __restrict__ col, const int* __restrict__ perm, int H, int D, int HP,
-    const float* __restrict__ as, const float* __restrict__ ad, float slope,
-    const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out,
-    float* __restrict__ pacc, float* __restrict__ pm, double* __restrict__ pd) {
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ long_rows,
+    int n_long, const int* __restrict__ rowptr, const int* __restrict__ col,
+    const int* __restrict__ perm, int H, int D, int HP, const float* __restrict__ as,
+    const float* __restrict__ ad, float slope, const float* __restrict__ h,
+    float* __restrict__ out, float* __restrict__ alpha_out, float* __restrict__ pacc,
+    float* __restrict__ pm, double* __restrict__ pd) {
   constexpr int LPS = kWave / SLOTS;
   constexpr int FC = LPS * V;
   constexpr int U = SLOTS * 4 <= kWave ? 4 : kWave / SLOTS;
@@ -91,17 +170,22 @@ __global__ __launch_bounds__(kBlock) void gat_items(
   __shared__ double s_den[kBlock / kWave][kMaxHeads];
   const int wv = threadIdx.x / kWave;
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + wv);
-  if (wid >= n_heavy + n_light) return;
-  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
-  const int row = uniform(itp->row), kb = uniform(itp->kbeg), ke = uniform(itp->kend);
-  const int pslot = uniform(itp->slot);
+  if (wid >= n_heavy + n_long) return;
   const int lane = threadIdx.x & (kWave - 1);
-  const int F = H * D;
-  if (kb == ke) {  // a target without edges (never a chunk): zero output
-    for (int f = lane; f < F; f += kWave) out[(int64_t)row * F + f] = 0.0f;
-    return;
-  }
   const int slot = lane / LPS, sl = lane % LPS;
+  int row, kb, ke, pslot;
+  if (wid < n_heavy) {
+    row = uniform(heavy[wid].row);
+    kb = uniform(heavy[wid].kbeg);
+    ke = uniform(heavy[wid].kend);
+    pslot = uniform(heavy[wid].slot);
+  } else {
+    row = uniform(long_rows[wid - n_heavy]);
+    kb = uniform(rowptr[row]);
+    ke = uniform(rowptr[row + 1]);
+    pslot = -1;
+  }
+  const int F = H * D;
   for (int f0 = 0; f0 < F; f0 += FC) {
     const int f = f0 + sl * V;
     const bool fok = f < F;
@@ -280,10 +364,21 @@ struct GatArgs {
 template <int V>
 void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
   const Graph& g = *a.g;
-#define TFG_GAT(SL)                                                                              \
-  gat_items<V, SL><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, \
-                                           a.H, a.D, a.HP, a.as, a.ad, a.slope, a.h, a.out,       \
-                                           a.alpha_out, a.pacc, a.pm, a.pd)
+  const int waves = g.n_heavy + g.n_long;
+  const int64_t short_waves = (g.n_short + slots - 1) / slots;
+  const dim3 sgrid((unsigned)((short_waves + kBlock / kWave - 1) / (kBlock / kWave)));
+#define TFG_GAT(SL)                                                                            \
+  do {                                                                                         \
+    if (g.n_short > 0)                                                                         \
+      gat_short<V, SL><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.rowptr, g.col,      \
+                                                g.perm, a.H, a.D, a.as, a.ad, a.slope, a.h,    \
+                                                a.out, a.alpha_out);                           \
+    if (waves > 0)                                                                             \
+      gat_items<V, SL><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows, g.n_long,      \
+                                               g.rowptr, g.col, g.perm, a.H, a.D, a.HP, a.as,  \
+                                               a.ad, a.slope, a.h, a.out, a.alpha_out, a.pacc, \
+                                               a.pm, a.pd);                                    \
+  } while (0)
   switch (slots) {
     case 1: TFG_GAT(1); break;
     case 2: TFG_GAT(2); break;
@@ -357,9 +452,9 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
   int hp = 1;
   while (hp < H) hp <<= 1;  // heads per pass (a power of two, at most 64)
   a.HP = hp;
-  const int waves = g.n_heavy + g.n_light;
-  if (waves > 0) {
-    dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
+  const int waves = g.n_heavy + g.n_long;
+  if (waves > 0 || g.n_short > 0) {
+    dim3 grid((unsigned)((std::max(waves, 1) + kBlock / kWave - 1) / (kBlock / kWave)));
     if (vec == 4)
       launch_slots<4>(slots, grid, s, a);
     else if (vec == 2)

@@ -132,28 +132,88 @@ __global__ __launch_bounds__(kBlock) void edge_scores(const IdxT* __restrict__ s
   out[i] = z >= 0.0f ? z : slope * z;
 }
 
-// One wavefront per work item of the graph's row plan (a whole row, or a
-// chunk of a long row). Lanes are (slot, head) pairs: HP heads (a power of
-// two) per pass and 64 / HP edge slots. Each lane keeps the maximum m of the
-// scores it has seen and d = sum of exp(s - m) (in double), rescaling d when
-// m grows, so the maximum and the denominator come out of one sweep; the
-// slots are combined with xor butterflies (every lane of a head ends with the
-// same pair). A whole row then writes alpha = exp(s - m) / d; a chunk stores
-// its pair, softmax_merge combines the chunks of each long row in order and
-// softmax_write writes their outputs.
+// Short rows (at most kShortRow edges), 64 / HP per wavefront: lane (r, hh)
+// takes row short_rows[i] and heads hh, hh + HP, ...; the row's scores are
+// loaded at once and kept in registers: maximum, then the sum of exp(s - m)
+// in double in graph order, then alpha. No cross-lane traffic.
+__device__ __forceinline__ void softmax_short_row(const int* __restrict__ rowptr,
+                                                  const int* __restrict__ perm, int t,
+                                                  const float* __restrict__ s, int H, int hh,
+                                                  int HP, float* __restrict__ out,
+                                                  float* __restrict__ out_csr) {
+  const int kb = rowptr[t], n = rowptr[t + 1] - kb;  // 0 <= n <= kShortRow
+  int e[kShortRow];
+#pragma unroll
+  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? perm[kb + j] : 0;
+  for (int h = hh; h < H; h += HP) {
+    float v[kShortRow];
+    float m = -__builtin_huge_valf();
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j) {
+      v[j] = j < n ? s[(int64_t)e[j] * H + h] : 0.0f;
+      if (j < n) m = v[j] > m ? v[j] : m;
+    }
+    double d = 0.0;
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j) {
+      v[j] = expf(v[j] - m);
+      if (j < n) d += (double)v[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j)
+      if (j < n) {
+        const float a = (float)((double)v[j] / d);
+        out[(int64_t)e[j] * H + h] = a;
+        if (out_csr) out_csr[(int64_t)(kb + j) * H + h] = a;
+      }
+  }
+}
+
+// Short rows, 64 / HP per wavefront (a kernel of its own: its registers would
+// lower the occupancy of the sweep below).
+__global__ __launch_bounds__(kBlock) void softmax_short(const int* __restrict__ short_rows,
+                                                        int n_short,
+                                                        const int* __restrict__ rowptr,
+                                                        const int* __restrict__ perm,
+                                                        const float* __restrict__ s, int H, int HP,
+                                                        float* __restrict__ out,
+                                                        float* __restrict__ out_csr) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const int64_t i = wave * (kWave / HP) + lane / HP;
+  if (i < n_short) softmax_short_row(rowptr, perm, short_rows[i], s, H, lane % HP, HP, out, out_csr);
+}
+
+// The other buckets of the row plan: wavefronts [0, n_heavy) take the chunks
+// of long rows, the rest one other light row each. Lanes are (slot, head) pairs: HP
+// heads (a power of two) per pass and 64 / HP edge slots; each lane keeps the
+// maximum m of the scores it has seen and d = sum of exp(s - m) (in double),
+// rescaling d when m grows, so the maximum and the denominator come out of
+// one sweep; the slots are combined with xor butterflies (every lane of a
+// head ends with the same pair). A whole row then writes alpha = exp(s - m) /
+// d; a chunk stores its pair, softmax_merge combines the chunks of each long
+// row in order and softmax_write writes their outputs.
 __global__ __launch_bounds__(kBlock) void softmax_items(
-    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
-    int n_light, const int* __restrict__ perm, const float* __restrict__ s, int H, int HP,
-    float* __restrict__ out, float* __restrict__ out_csr, float* __restrict__ pm,
-    double* __restrict__ pd) {
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ long_rows,
+    int n_long, const int* __restrict__ rowptr, const int* __restrict__ perm,
+    const float* __restrict__ s, int H, int HP, float* __restrict__ out,
+    float* __restrict__ out_csr, float* __restrict__ pm, double* __restrict__ pd) {
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
-  if (wid >= n_heavy + n_light) return;
-  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
-  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
-  if (kb == ke) return;
+  if (wid >= n_heavy + n_long) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
   const int slot = lane / HP, hh = lane % HP;
+  int kb, ke, pslot;
+  if (wid < n_heavy) {
+    kb = uniform(heavy[wid].kbeg);
+    ke = uniform(heavy[wid].kend);
+    pslot = uniform(heavy[wid].slot);
+  } else {
+    const int t = uniform(long_rows[wid - n_heavy]);
+    kb = uniform(rowptr[t]);
+    ke = uniform(rowptr[t + 1]);
+    pslot = -1;
+  }
   for (int hb = 0; hb < H; hb += HP) {
     const int h = hb + hh;
     const bool act = h < H;
@@ -274,10 +334,17 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
   float* pm = static_cast<float*>(ws);
   double* pd = reinterpret_cast<double*>(
       static_cast<char*>(ws) + align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
-  const int waves = g.n_heavy + g.n_light;
+  const int64_t short_waves = (g.n_short + kWave / hp - 1) / (kWave / hp);
+  if (short_waves > 0) {
+    softmax_short<<<(unsigned)((short_waves + 3) / 4), kBlock, 0, s>>>(
+        g.short_rows, g.n_short, g.rowptr, g.perm, scores, H, hp, out, out_csr);
+    TFG_LAUNCHED("softmax_short");
+  }
+  const int waves = g.n_heavy + g.n_long;
   if (waves > 0) {
     softmax_items<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.light, g.n_light, g.perm, scores, H, hp, out, out_csr, pm, pd);
+        g.heavy, g.n_heavy, g.long_rows, g.n_long, g.rowptr, g.perm, scores, H, hp, out, out_csr,
+        pm, pd);
     TFG_LAUNCHED("softmax_items");
   }
   if (g.n_split > 0) {

@@ -15,6 +15,7 @@ namespace tfg {
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per block for most kernels (4 waves)
 constexpr int kDefaultChunk = 128; // max edges per work item of the row plan
+constexpr int kShortRow = 8;       // rows of at most this many edges are "short"
 
 // Device error flag bits (graph->err and the pooling workspace flag).
 constexpr int kErrIndex = 1;
@@ -61,18 +62,26 @@ struct Graph {
   WorkItem* light = nullptr;  // whole rows
   SplitRow* split = nullptr;
   int n_heavy = 0, n_light = 0, n_split = 0;
+  // the light rows again, by length: short (0..kShortRow edges, several per
+  // wavefront in the attention kernels) and the rest (one per wavefront)
+  int* short_rows = nullptr;
+  int* long_rows = nullptr;
+  int n_short = 0, n_long = 0;
   // part plan (P > 1): one item per (part, row) segment chunk, part-major
   // order; every item writes a partial, prows[t] reduces row t's partials
   WorkItem* pexec = nullptr;
   SplitRow* prows = nullptr;
   int n_pexec = 0;
-  int* counters = nullptr;  // device: [0] heavy, [1] light, [2] split, [3] error flags
+  // device: [0] heavy, [1] light, [2] split, [3] error flags, [4] part items,
+  // [5] short rows, [6] other light rows
+  int* counters = nullptr;
   int device = 0;
 };
 
 // Sizes of the persistent part of a graph.
 struct GraphLayout {
-  size_t rowptr, segptr, col, perm, heavy, light, split, pexec, prows, counters, total;
+  size_t rowptr, segptr, col, perm, heavy, light, split, pexec, prows, short_rows, long_rows,
+      counters, total;
   int64_t cap_heavy, cap_light, cap_split, cap_pexec;
 };
 GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk);
