@@ -130,6 +130,9 @@ int tfg_abi_version(void);
  * tfg_check: synchronises `stream` and returns TFG_ERR_INDEX_RANGE if any
  *   device-side check on this graph failed, else TFG_OK.
  * tfg_graph_destroy: frees the host struct (not `buf`).
+ *
+ * A handle belongs to the device that was current when it was created; every
+ * call that reads it fails with TFG_ERR_INVALID_ARG on another device.
  */
 int tfg_graph_bytes(int64_t E, int64_t N_src, int64_t N, int add_self_loops, int src_parts,
                     size_t *buf_bytes, size_t *scratch_bytes);

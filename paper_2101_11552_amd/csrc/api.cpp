@@ -93,6 +93,17 @@ int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int
   return build_graph(g, src, tgt, index_type, scratch, scratch_bytes, s);
 }
 
+// A handle's device arrays live on the device that was current when it was
+// built; every call that reads them must run there.
+int check_device(const Graph& g) {
+  int d = 0;
+  TFG_HIP(hipGetDevice(&d));
+  if (d != g.device) return fail(TFG_ERR_INVALID_ARG, "the graph lives on another device");
+  return TFG_OK;
+}
+
+int check_device(const tfg_graph* h) { return h ? check_device(h->g) : TFG_OK; }
+
 const void* tgt_row(const void* edge_index, int index_type, int64_t E) {
   if (edge_index == nullptr) return nullptr;
   return index_type == TFG_I64 ? static_cast<const void*>(static_cast<const int64_t*>(edge_index) + E)
@@ -108,7 +119,8 @@ int graph_or_transient(const tfg_graph* handle, Graph& tmp, const Graph*& g, con
     g = &handle->g;
     if (g->E_in != E || g->N != N || g->N_src != N_src || g->loops != (loops ? 1 : 0))
       return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
-    return TFG_OK;
+    if (g->transposed) return fail(TFG_ERR_INVALID_ARG, "a transposed graph cannot serve here");
+    return check_device(*g);
   }
   const int64_t Ep = E + (loops ? N : 0);
   const int parts = choose_parts(Ep, N, N_src, 0);
@@ -227,6 +239,7 @@ int tfg_graph_create_transposed(const void* edge_index, int index_type, int64_t 
 int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* perm,
                   tfg_stream_t stream) {
   if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  if (int rc = check_device(h)) return rc;
   const Graph& g = h->g;
   hipStream_t s = as_stream(stream);
   if (rowptr)
@@ -256,6 +269,8 @@ int tfg_edge_reorder(const tfg_graph* from, const tfg_graph* to, const float* in
   if (E > 0 && in == out) return fail(TFG_ERR_INVALID_ARG, "out overlaps in");
   if (ws == nullptr || ws_bytes < tfg_edge_reorder_ws_bytes(from, to, H))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int rc = check_device(from)) return rc;
+  if (int rc = check_device(to)) return rc;
   return launch_edge_reorder(from ? from->g.perm : nullptr, to ? to->g.perm : nullptr, E, (int)H,
                              in, out, static_cast<float*>(ws), as_stream(stream));
 }
@@ -276,6 +291,7 @@ int tfg_graph_info(const tfg_graph* h, int64_t* E_total, int64_t* N, int64_t* N_
 
 int tfg_graph_segments(const tfg_graph* h, int32_t* segptr, tfg_stream_t stream) {
   if (!h || !segptr) return fail(TFG_ERR_INVALID_ARG, "NULL argument");
+  if (int rc = check_device(h)) return rc;
   const Graph& g = h->g;
   TFG_HIP(hipMemcpyAsync(segptr, g.segptr, sizeof(int) * (g.N * g.parts + 1),
                          hipMemcpyDeviceToDevice, as_stream(stream)));
@@ -284,6 +300,7 @@ int tfg_graph_segments(const tfg_graph* h, int32_t* segptr, tfg_stream_t stream)
 
 int tfg_check(const tfg_graph* h, tfg_stream_t stream) {
   if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  if (int rc = check_device(h)) return rc;
   int flags = 0;
   hipStream_t s = as_stream(stream);
   TFG_HIP(hipMemcpyAsync(&flags, h->g.counters + 3, sizeof(int), hipMemcpyDeviceToHost, s));
@@ -372,6 +389,7 @@ int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float
     gp = &g->g;
     if (gp->E != E || gp->N != N || gp->N_src != N_src)
       return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
+    if (int e = check_device(*gp)) return e;
   } else {
     rc = graph_or_transient(nullptr, tmp, gp, edge_index, tgt_row(edge_index, index_type, E),
                             index_type, E, N_src, N, 0, c, s);
@@ -438,6 +456,7 @@ int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* s
   if (g) {
     gp = &g->g;
     if (gp->E != E || gp->N != N) return fail(TFG_ERR_INVALID_ARG, "graph handle does not match");
+    if (int e = check_device(*gp)) return e;
   } else {
     rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
     if (rc) return rc;
@@ -506,6 +525,8 @@ int tfg_aggregate_backward(const tfg_graph* g, const tfg_graph* gt, const float*
       ws_bytes < aggregate_backward_ws_bytes(fg, tg, F, H, reduce, weight_order,
                                              edge_weight != nullptr))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int e = check_device(g)) return e;
+  if (int e = check_device(gt)) return e;
   hipStream_t s = as_stream(stream);
   return launch_aggregate_backward(fg, dx ? tg : nullptr, edge_weight, (int)H, weight_order, x,
                                    ldx, dy, F, reduce, argmax, dx, dw, dw_order, ws, s);
@@ -536,6 +557,7 @@ int tfg_segment_softmax_backward(const float* alpha, const float* dalpha, int64_
     gp = &g->g;
     if (gp->transposed || gp->E != E || gp->N != N)
       return fail(TFG_ERR_INVALID_ARG, "graph handle does not match");
+    if (int e = check_device(*gp)) return e;
   } else {
     rc = graph_or_transient(nullptr, tmp, gp, nullptr, seg, index_type, E, 1, N, 0, c, s);
     if (rc) return rc;
@@ -651,6 +673,7 @@ int tfg_propagate(const tfg_graph* g, const float* edge_weight, int weight_order
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (ws == nullptr || ws_bytes < tfg_propagate_ws_bytes(g, F, K))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int e = check_device(gr)) return e;
   hipStream_t s = as_stream(stream);
   if (gr.N == 0 || F == 0) return TFG_OK;
   if (K == 0) {
@@ -692,6 +715,7 @@ int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr, H, D))
     return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int e = check_device(gr)) return e;
   return launch_gat_aggregate(gr, h, (int)H, (int)D, a_src, a_dst, slope, out, alpha_out, ws,
                               as_stream(stream));
 }
