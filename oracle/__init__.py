@@ -54,6 +54,9 @@ def lib():
         _lib.orc_aggregate_backward.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, i64,
                                                 ctypes.c_int, p, p, p, p]
         _lib.orc_segment_softmax_backward.argtypes = [i64, i64, p, p, p, i64, p]
+        _lib.orc_dot_scores.argtypes = [i64, p, p, p, p, i64, i64, i64, i64, ctypes.c_double, p]
+        _lib.orc_dot_layer.argtypes = [i64, p, p, p, p, p, i64, i64, i64, i64, ctypes.c_double,
+                                       p, p, p]
         _lib.orc_propagate.argtypes = [i64, p, p, p, p, i64, i64, i64, i64, ctypes.c_double, p,
                                        p, p]
         _lib.orc_segment_pool.argtypes = [i64, i64, i64, p, p, i64, ctypes.c_int, p, p, p, p]
@@ -180,6 +183,43 @@ def propagate(edge_index, x, K, alpha=0.0, h=None, edge_weight=None):
                                x.ctypes.data_as(ctypes.c_void_p), ldx, N, F, K, float(alpha),
                                _ptr(hh), _ptr(out64), _ptr(scale)))
     return out64, scale
+
+
+def dot_scores(edge_index, q, key, heads, scale):
+    """Scaled dot-product scores [E, H] in float64: scale * <q[tgt], key[src]> per head."""
+    ei = _i64(edge_index)
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    key = np.ascontiguousarray(key, dtype=np.float32)
+    n, F = q.shape
+    n_src = key.shape[0]
+    if key.shape[1] != F or F % heads:
+        raise ValueError("q and key must be [*, H*D]")
+    E = ei.shape[1]
+    src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
+    s = np.empty((E, heads), np.float64)
+    _check(lib().orc_dot_scores(E, _ptr(src), _ptr(tgt), _ptr(q), _ptr(key), n, n_src, heads,
+                                F // heads, float(scale), _ptr(s)))
+    return s
+
+
+def dot_layer(edge_index, q, key, v, heads, scale):
+    """Transformer-style attention layer: (out64 [N, H*D], alpha64 [E, H], scale [N, H*D])."""
+    ei = _i64(edge_index)
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    key = np.ascontiguousarray(key, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    n, F = q.shape
+    n_src = key.shape[0]
+    if key.shape[1] != F or v.shape != key.shape or F % heads:
+        raise ValueError("q, key and v must be [*, H*D]")
+    E = ei.shape[1]
+    src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
+    out = np.empty((n, F), np.float64)
+    alpha = np.empty((E, heads), np.float64)
+    S = np.empty((n, F), np.float64)
+    _check(lib().orc_dot_layer(E, _ptr(src), _ptr(tgt), _ptr(q), _ptr(key), _ptr(v), n, n_src,
+                               heads, F // heads, float(scale), _ptr(out), _ptr(alpha), _ptr(S)))
+    return out, alpha, S
 
 
 def aggregate_backward(edge_index, x, n, dy, reduce="sum", edge_weight=None, heads=1, arg=None):

@@ -502,6 +502,70 @@ int orc_gat_layer(int64_t E, const int64_t *src, const int64_t *tgt, const float
 }
 
 /*
+ * Transformer-style attention (the GAT variant of the paper's library, Sec.
+ * 4.2), scaled dot-product scores per edge and head:
+ *   s[e, k] = scale * sum_d q[tgt_e, k*D + d] * key[src_e, k*D + d]
+ * q: [N, H*D] (targets), key: [N_src, H*D] (sources); s64: [E, H] in double.
+ */
+int orc_dot_scores(int64_t E, const int64_t *src, const int64_t *tgt, const float *q,
+                   const float *key, int64_t N, int64_t N_src, int64_t H, int64_t D,
+                   double scale, double *s64)
+{
+    if (orc_check_edges(E, src, tgt, N_src, N) != ORC_OK)
+        return ORC_ERR_INDEX_RANGE;
+    int64_t F = H * D;
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t k = 0; k < H; ++k) {
+            double acc = 0.0;
+            for (int64_t d = 0; d < D; ++d)
+                acc += (double)q[tgt[e] * F + k * D + d] * (double)key[src[e] * F + k * D + d];
+            s64[e * H + k] = scale * acc;
+        }
+    return ORC_OK;
+}
+
+/*
+ * The whole layer: scores as above (rounded to float32, as a float32 kernel
+ * would hold them), the segment softmax per target and head, and
+ * out[t, k*D + d] = sum over the edges e entering t of alpha[e, k] v[src_e, k*D + d].
+ * v: [N_src, H*D]. out64 / scale: [N, H*D]; alpha64: [E, H] or NULL.
+ */
+int orc_dot_layer(int64_t E, const int64_t *src, const int64_t *tgt, const float *q,
+                  const float *key, const float *v, int64_t N, int64_t N_src, int64_t H,
+                  int64_t D, double scale, double *out64, double *alpha64, double *S)
+{
+    int64_t F = H * D;
+    size_t n = (size_t)(E * H > 0 ? E * H : 1);
+    double *s64 = (double *)malloc(n * sizeof(double));
+    float *s32 = (float *)malloc(n * sizeof(float));
+    double *al = (double *)malloc(n * sizeof(double));
+    int rc = orc_dot_scores(E, src, tgt, q, key, N, N_src, H, D, scale, s64);
+    if (rc == ORC_OK) {
+        for (int64_t i = 0; i < E * H; ++i)
+            s32[i] = (float)s64[i];
+        rc = orc_segment_softmax(E, H, s32, tgt, N, al, NULL);
+    }
+    if (rc == ORC_OK) {
+        memset(out64, 0, (size_t)(N * F) * sizeof(double));
+        if (S)
+            memset(S, 0, (size_t)(N * F) * sizeof(double));
+        for (int64_t e = 0; e < E; ++e)
+            for (int64_t c = 0; c < F; ++c) {
+                double m = al[e * H + c / D] * (double)v[src[e] * F + c];
+                out64[tgt[e] * F + c] += m;
+                if (S)
+                    S[tgt[e] * F + c] += fabs(m);
+            }
+        if (alpha64)
+            memcpy(alpha64, al, (size_t)(E * H) * sizeof(double));
+    }
+    free(s64);
+    free(s32);
+    free(al);
+    return rc;
+}
+
+/*
  * BatchGraph reindexing (Sec. 2.1.1, Fig. 4): node j of graph i becomes
  * j + offset[i], where offset[i] is the number of nodes in graphs 0..i-1.
  * offsets has G + 1 entries (the last one is the total node count).

@@ -659,3 +659,71 @@ def test_softmax_backward_finite_differences(orc):
         # float32 perturbed scores: compare with the rounding-aware step
         step = float(np.float32(s[i, h] + eps)) - float(np.float32(s[i, h] - eps))
         assert (lp - lm) / step == pytest.approx(ds[i, h], rel=2e-4, abs=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Transformer-style attention (scaled dot-product scores)
+# ---------------------------------------------------------------------------
+
+def test_dot_scores_brute_force(orc):
+    n, e, H, D = 7, 30, 3, 4
+    ei = graphgen.random_graph(71, n, e)
+    rng = np.random.default_rng(71)
+    q = rng.standard_normal((n, H * D)).astype(np.float32)
+    k = rng.standard_normal((n, H * D)).astype(np.float32)
+    s = orc.dot_scores(ei, q, k, H, 0.5)
+    q3 = q.astype(np.float64).reshape(n, H, D)
+    k3 = k.astype(np.float64).reshape(n, H, D)
+    for j in range(e):
+        for h in range(H):
+            ref = 0.5 * sum(q3[ei[1, j], h, d] * k3[ei[0, j], h, d] for d in range(D))
+            assert s[j, h] == pytest.approx(ref, rel=1e-14, abs=1e-14)
+
+
+def test_dot_layer_zero_query_is_mean(orc):
+    # q = 0: every score is 0, the attention is uniform, the output is the mean of v
+    n, e, H, D = 30, 200, 2, 4
+    ei = graphgen.random_graph(72, n, e)
+    k = graphgen.features(72, n, H * D)
+    v = graphgen.features(73, n, H * D)
+    out, alpha, _ = orc.dot_layer(ei, np.zeros_like(k), k, v, H, 0.25)
+    mean, _ = orc.aggregate(ei, v, n, "mean")
+    np.testing.assert_allclose(out, mean, rtol=1e-13, atol=1e-15)
+    cnt = np.bincount(ei[1], minlength=n)
+    np.testing.assert_allclose(alpha[:, 1], 1.0 / cnt[ei[1]], rtol=1e-15)
+
+
+def test_dot_layer_dense(orc):
+    # a dense check: per target and head, softmax of the float32 scores, then the weighted sum
+    n, H, D = 9, 2, 3
+    ei = graphgen.random_graph(74, n, 35)
+    rng = np.random.default_rng(74)
+    q, k, v = (rng.standard_normal((n, H * D)).astype(np.float32) for _ in range(3))
+    scale = 1 / np.sqrt(D)
+    out, alpha, _ = orc.dot_layer(ei, q, k, v, H, scale)
+    s = np.einsum("ehd,ehd->eh", q.astype(np.float64).reshape(n, H, D)[ei[1]],
+                  k.astype(np.float64).reshape(n, H, D)[ei[0]]) * scale
+    s = s.astype(np.float32).astype(np.float64)
+    ref = np.zeros((n, H, D))
+    for t in range(n):
+        m = ei[1] == t
+        if not m.any():
+            continue
+        a = np.exp(s[m] - s[m].max(0))
+        a /= a.sum(0)
+        ref[t] = np.einsum("eh,ehd->hd", a, v.astype(np.float64).reshape(n, H, D)[ei[0][m]])
+    np.testing.assert_allclose(out, ref.reshape(n, H * D), rtol=1e-12, atol=1e-13)
+    tot = np.zeros((n, H))
+    np.add.at(tot, ei[1], alpha)
+    has = np.bincount(ei[1], minlength=n) > 0
+    np.testing.assert_allclose(tot[has], 1.0, rtol=1e-13)
+
+
+def test_dot_layer_single_edge_copies_value(orc):
+    # a target with one in-edge gets exactly the value row of its source
+    ei = np.array([[3, 1, 2], [0, 2, 2]])
+    rng = np.random.default_rng(75)
+    q, k, v = (rng.standard_normal((4, 8)).astype(np.float32) for _ in range(3))
+    out, alpha, _ = orc.dot_layer(ei, q, k, v, 2, 0.5)
+    np.testing.assert_array_equal(out[0], v[3].astype(np.float64))
+    assert np.all(out[[1, 3]] == 0) and np.all(alpha[0] == 1.0)
