@@ -205,6 +205,22 @@ def run_suite(args):
          E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
          kernel="node_projections_vec + gat_items + gat_merge", unfused_chain_ms=round(ms_c, 4),
          speedup_vs_unfused=round(ms_c / ms_f, 3))
+    # the Transformer-style variant: q, key, v of the same shape as h
+    gen = torch.Generator(device=dev).manual_seed(3)
+    qd, kd, vd = (torch.randn((n3, Fh), generator=gen, device=dev) for _ in range(3))
+    ms_f = _timed(torch, lambda: tfg.tfg_gat_dot_aggregate(g3, qd, kd, vd, H), reps)
+
+    def dot_chain():
+        s = tfg.tfg_edge_dot_scores(g3, qd, kd, H)
+        _, a_csr = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3, out_csr=True)
+        return tfg.tfg_aggregate(ei3, vd, n3, "sum", edge_weight=a_csr, heads=H,
+                                 weight_order="csr", graph=g3)
+    ms_c = _timed(torch, dot_chain, reps)
+    # per edge: source id, the key and value rows; per node: q row, output row
+    _row("fused Transformer-style attention (scaled dot product)", wl3, ms_f, E3,
+         E3 * (4 + 8 * Fh) + n3 * (8 * Fh + 4), kernel="gat_short + gat_items (dot) + gat_merge",
+         unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3))
+    del qd, kd, vd
     s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3), reps)
     # per edge: edge id, the scores (read twice by the kernel, counted once), alpha
@@ -236,7 +252,7 @@ def run_suite(args):
     ms = _timed(torch, lambda: tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False, out=bout,
                                                     ws=bws), reps)
     _row("BatchGraph construction", wl5, ms, Eb,
-         Eb * 16 + G * 8 + Nb * 4, kernel="counts_to_int + scans + reindex_edges + fill_graph_index")
+         Eb * 16 + G * 8 + Nb * 4, kernel="batch_offsets_small + batch_fill")
 
     def batch_step():
         bei, bgi, _, _ = tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False)

@@ -362,6 +362,31 @@ int tfg_gat_aggregate(const tfg_graph *g, const float *h, int64_t H, int64_t D,
                       const float *a_src, const float *a_dst, float slope, float *out,
                       float *alpha_out, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
+/*
+ * Transformer-style attention, the GAT variant the paper's library uses (Sec.
+ * 4.2): per edge e = (s -> t) and head k, the scaled dot product
+ *   s[e, k] = scale * sum_d q[t, k*D + d] * key[s, k*D + d]
+ * (scale usually 1/sqrt(D)), the softmax of s[., k] over the edges entering
+ * each target, and out[t, k*D + d] = sum over those edges of alpha[e, k] *
+ * v[s, k*D + d]. q: [N, H*D] (one row per target), key, v: [N_src, H*D] (per
+ * source); all contiguous. The query, key and value projections are dense
+ * layers outside this library.
+ * tfg_edge_dot_scores: the scores alone, [E', H] in `order` (TFG_COO: edge
+ *   ids of g, loops after the input edges; TFG_CSR: the graph order); they
+ *   feed tfg_segment_softmax and tfg_aggregate (the unfused chain). Any D.
+ * tfg_gat_dot_aggregate: the whole layer in one sweep per row, as
+ *   tfg_gat_aggregate (online maximum and denominator, chunks of long rows
+ *   merged in order); D a power of two, at most 64; H <= 64. alpha_out: NULL
+ *   or [E', H] in edge-id order. ws: tfg_gat_dot_aggregate_ws_bytes(g, H, D).
+ */
+int tfg_edge_dot_scores(const tfg_graph *g, const float *q, const float *key, int64_t H,
+                        int64_t D, float scale, float *out_scores, int order,
+                        tfg_stream_t stream);
+size_t tfg_gat_dot_aggregate_ws_bytes(const tfg_graph *g, int64_t H, int64_t D);
+int tfg_gat_dot_aggregate(const tfg_graph *g, const float *q, const float *key, const float *v,
+                          int64_t H, int64_t D, float scale, float *out, float *alpha_out,
+                          void *ws, size_t ws_bytes, tfg_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Graph pooling                                                             */
 /* ------------------------------------------------------------------------ */

@@ -102,6 +102,9 @@ def load():
         "tfg_segment_softmax_backward_ws_bytes": (sz, [i64, i64, i64, p]),
         "tfg_segment_softmax_backward": (ci, [p, p, i64, i64, p, ci, i64, p, p, p, sz, p]),
         "tfg_edge_reorder_ws_bytes": (sz, [p, p, i64]),
+        "tfg_edge_dot_scores": (ci, [p, p, p, i64, i64, ctypes.c_float, p, ci, p]),
+        "tfg_gat_dot_aggregate_ws_bytes": (sz, [p, i64, i64]),
+        "tfg_gat_dot_aggregate": (ci, [p, p, p, p, i64, i64, ctypes.c_float, p, p, p, sz, p]),
         "tfg_edge_reorder": (ci, [p, p, p, i64, p, p, sz, p]),
     }
     for name, (res, args) in sig.items():
@@ -599,3 +602,48 @@ def tfg_gat_aggregate(graph: Graph, h: torch.Tensor, a_src: torch.Tensor, a_dst:
                                  _stream(h.device)))
     return (out, alpha) if want_alpha else out
 
+
+
+def tfg_edge_dot_scores(graph: Graph, q: torch.Tensor, key: torch.Tensor, heads: int,
+                        scale: float | None = None, order: str = "coo",
+                        out: torch.Tensor | None = None) -> torch.Tensor:
+    """Scaled dot-product scores [E', heads]: scale * <q[tgt], key[src]> per head
+    (scale defaults to 1/sqrt(D))."""
+    lib = load()
+    q, key = _f32(q, "q"), _f32(key, "key")
+    F = q.shape[1]
+    D = F // heads
+    if q.shape[0] != graph.N or key.shape != (graph.N_src, F) or F % heads:
+        raise ValueError("q must be [N, H*D] and key [N_src, H*D]")
+    if scale is None:
+        scale = 1.0 / (D ** 0.5)
+    if out is None:
+        out = torch.empty((graph.E, heads), dtype=torch.float32, device=q.device)
+    _check(lib.tfg_edge_dot_scores(graph.handle, _ptr(q), _ptr(key), heads, D, float(scale),
+                                   _ptr(out), _ORDER[order], _stream(q.device)))
+    return out
+
+
+def tfg_gat_dot_aggregate(graph: Graph, q: torch.Tensor, key: torch.Tensor, v: torch.Tensor,
+                          heads: int, scale: float | None = None, want_alpha: bool = False,
+                          out: torch.Tensor | None = None):
+    """Transformer-style attention layer in one sweep: out [N, H*D] (and alpha
+    [E', H] in edge-id order with ``want_alpha``)."""
+    lib = load()
+    q, key, v = _f32(q, "q"), _f32(key, "key"), _f32(v, "v")
+    F = q.shape[1]
+    D = F // heads
+    if (q.shape[0] != graph.N or key.shape != (graph.N_src, F) or v.shape != key.shape
+            or F % heads):
+        raise ValueError("q must be [N, H*D], key and v [N_src, H*D]")
+    if scale is None:
+        scale = 1.0 / (D ** 0.5)
+    dev = q.device
+    if out is None:
+        out = torch.empty((graph.N, F), dtype=torch.float32, device=dev)
+    alpha = torch.empty((graph.E, heads), dtype=torch.float32, device=dev) if want_alpha else None
+    ws = _workspace(lib.tfg_gat_dot_aggregate_ws_bytes(graph.handle, heads, D), dev)
+    _check(lib.tfg_gat_dot_aggregate(graph.handle, _ptr(q), _ptr(key), _ptr(v), heads, D,
+                                     float(scale), _ptr(out), _ptr(alpha), _ptr(ws), ws.numel(),
+                                     _stream(dev)))
+    return (out, alpha) if want_alpha else out

@@ -720,5 +720,42 @@ int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
                               as_stream(stream));
 }
 
+size_t tfg_gat_dot_aggregate_ws_bytes(const tfg_graph* g, int64_t H, int64_t D) {
+  return tfg_gat_aggregate_ws_bytes(g, H, D);
+}
+
+int tfg_gat_dot_aggregate(const tfg_graph* g, const float* q, const float* key, const float* v,
+                          int64_t H, int64_t D, float scale, float* out, float* alpha_out,
+                          void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (H < 1 || H > max_fused_heads() || !dot_attention_shape_ok(D))
+    return fail(TFG_ERR_INVALID_ARG, "need 1 <= H <= 64 and D a power of two <= 64");
+  if (gr.N > 0 && (q == nullptr || out == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (gr.E > 0 && (key == nullptr || v == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr, H, D))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int e = check_device(gr)) return e;
+  return launch_gat_dot_aggregate(gr, q, key, v, (int)H, (int)D, scale, out, alpha_out, ws,
+                                  as_stream(stream));
+}
+
+int tfg_edge_dot_scores(const tfg_graph* g, const float* q, const float* key, int64_t H,
+                        int64_t D, float scale, float* out_scores, int order,
+                        tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (H < 1 || D < 1 || H * D >= kMaxCount || gr.E * H >= kMaxCount)
+    return fail(TFG_ERR_INVALID_ARG, "bad H or D");
+  if (order != TFG_COO && order != TFG_CSR) return fail(TFG_ERR_INVALID_ARG, "bad order");
+  if (gr.E > 0 && (q == nullptr || key == nullptr || out_scores == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (int e = check_device(gr)) return e;
+  return launch_edge_dot(gr, q, key, H * D, H * D, (int)H, scale, out_scores,
+                         order == TFG_COO ? 1 : 0, as_stream(stream));
+}
+
 }  // extern "C"
 

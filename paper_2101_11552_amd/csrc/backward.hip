@@ -85,7 +85,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_rows(
     const WorkItem* __restrict__ items, int n_items, const int* __restrict__ rowptr,
     const int* __restrict__ col, const int* __restrict__ perm, const float* __restrict__ x,
     int64_t ldx, const float* __restrict__ dy, const int* __restrict__ arg, int F, int H, int G,
-    float* __restrict__ dw, int dw_by_perm) {
+    float* __restrict__ dw, int dw_by_perm, float scale) {
   constexpr int LPS = kWave / SLOTS;
   // 4 gathers in flight per slot with the transposing reduction keeps the
   // kernel within 64 VGPRs (8 waves per SIMD); 8 would need 79
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_rows(
         const float val = transpose_sum<U, LPS>(p, sl);
         if (sl % STRIDE == 0 && j < n) {
           const int64_t e = dw_by_perm ? pu : kb + j;
-          dw[e] = val;
+          dw[e] = val * scale;
         }
       } else {
         for (int off = 1; off < G; off <<= 1)
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_rows(
           for (int u = 0; u < U; ++u)
             if (ok[u]) {
               const int64_t e = dw_by_perm ? pe[u] : kb + s0 + u * SLOTS + slot;
-              dw[e * H + head] = p[u];
+              dw[e * H + head] = p[u] * scale;
             }
         }
       }
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_simple(
     const int* __restrict__ rowptr, int64_t N, int64_t E, const int* __restrict__ col,
     const int* __restrict__ perm, const float* __restrict__ x, int64_t ldx,
     const float* __restrict__ dy, const int* __restrict__ arg, int F, int H,
-    float* __restrict__ dw, int dw_by_perm) {
+    float* __restrict__ dw, int dw_by_perm, float scale) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= E * H) return;
   const int64_t k = i / H;
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_simple(
     if (MODE == kGradMax && arg[t * F + c] != (int)e) g = 0.0f;
     acc = __builtin_fmaf(g, x[s * ldx + c], acc);
   }
-  dw[(dw_by_perm ? e : k) * H + h] = acc;
+  dw[(dw_by_perm ? e : k) * H + h] = acc * scale;
 }
 
 // Weights of the transposed graph for the mean gradient, in its graph order:
@@ -334,10 +334,10 @@ template <int V, int MODE, bool WHOLE>
 void launch_edge_grad_slots(int slots, dim3 grid, hipStream_t s, const WorkItem* items,
                             int n_items, const Graph& g, const float* x, int64_t ldx,
                             const float* dy, const int* arg, int F, int H, int G, float* dw,
-                            int by_perm) {
+                            int by_perm, float scale) {
 #define TFG_EG(SL)                                                                      \
   edge_grad_rows<V, SL, MODE, WHOLE><<<grid, kBlock, 0, s>>>(                           \
-      items, n_items, g.rowptr, g.col, g.perm, x, ldx, dy, arg, F, H, G, dw, by_perm)
+      items, n_items, g.rowptr, g.col, g.perm, x, ldx, dy, arg, F, H, G, dw, by_perm, scale)
   switch (slots) {
     case 1: TFG_EG(1); break;
     case 2: TFG_EG(2); break;
@@ -350,7 +350,8 @@ void launch_edge_grad_slots(int slots, dim3 grid, hipStream_t s, const WorkItem*
 
 template <int MODE>
 int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* dy,
-                     const int* arg, int64_t F, int H, float* dw, int by_perm, hipStream_t s) {
+                     const int* arg, int64_t F, int H, float* dw, int by_perm, hipStream_t s,
+                     float scale = 1.0f) {
   const int D = (int)(F / H);
   auto fits = [&](int v) {
     return D % v == 0 && ldx % v == 0 && reinterpret_cast<uintptr_t>(x) % (4 * v) == 0 &&
@@ -361,7 +362,7 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
   if (F / vec > kWave) {
     const int64_t n = g.E * H;
     edge_grad_simple<MODE><<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(
-        g.rowptr, g.N, g.E, g.col, g.perm, x, ldx, dy, arg, (int)F, H, dw, by_perm);
+        g.rowptr, g.N, g.E, g.col, g.perm, x, ldx, dy, arg, (int)F, H, dw, by_perm, scale);
     TFG_LAUNCHED("edge_grad_simple");
     return TFG_OK;
   }
@@ -377,23 +378,23 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
     if (H == 1) {
       if (vec == 4)
         launch_edge_grad_slots<4, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                              H, G, dw, by_perm);
+                                              H, G, dw, by_perm, scale);
       else if (vec == 2)
         launch_edge_grad_slots<2, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                              H, G, dw, by_perm);
+                                              H, G, dw, by_perm, scale);
       else
         launch_edge_grad_slots<1, MODE, true>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                              H, G, dw, by_perm);
+                                              H, G, dw, by_perm, scale);
     } else {
       if (vec == 4)
         launch_edge_grad_slots<4, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                               H, G, dw, by_perm);
+                                               H, G, dw, by_perm, scale);
       else if (vec == 2)
         launch_edge_grad_slots<2, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                               H, G, dw, by_perm);
+                                               H, G, dw, by_perm, scale);
       else
         launch_edge_grad_slots<1, MODE, false>(slots, grid, s, it, n, g, x, ldx, dy, arg, (int)F,
-                                               H, G, dw, by_perm);
+                                               H, G, dw, by_perm, scale);
     }
   };
   if (use_part_plan(g, F)) {
@@ -407,6 +408,12 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
 }
 
 }  // namespace
+
+int launch_edge_dot(const Graph& g, const float* q, const float* key, int64_t ldk, int64_t F,
+                    int H, float scale, float* out, int by_perm, hipStream_t s) {
+  if (g.E == 0 || F == 0) return TFG_OK;
+  return launch_edge_grad<kGradSum>(g, key, ldk, q, nullptr, F, H, out, by_perm, s, scale);
+}
 
 int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
                         const float* in, float* out, float* tmp, hipStream_t s) {

@@ -8,16 +8,20 @@
 // wavefront per work item of the graph's row plan (a whole row, or a chunk of
 // a long row). Lanes are (edge slot, V features) as in the
 // aggregation kernel: every lane gathers its V features of the source row and
-// the source's projection a_s for its own head, forms the score
-// s = LeakyReLU(a_s + a_d[t]) and folds it into a running triple (maximum m,
+// what its head's score needs (the source's projection a_s for the additive
+// GAT score, its V columns of the key row for the scaled dot product), forms
+// the score and folds it into a running triple (maximum m,
 // denominator d in double, numerators acc): when the maximum grows, d and acc
 // are rescaled by exp(m_old - m_new). Each lane keeps U independent triples;
 // they are merged pairwise, then across the slots. A whole row writes
 // out = acc / d; a chunk writes its triple and gat_merge combines the chunks
 // of each long row in chunk order. The optional coefficients
 // alpha = exp(s - m) / d are written in a second sweep with lanes = (slot,
-// head). The node projections a_s = a_src . h and a_d = a_dst . h come from
-// node_projections() (softmax.hip) and sit in the workspace.
+// head). For the additive score the node projections a_s = a_src . h and
+// a_d = a_dst . h come from node_projections() (softmax.hip) and sit in the
+// workspace.
+#include <initializer_list>
+
 #include "softmax_stats.h"
 
 namespace tfg {
@@ -79,40 +83,107 @@ __device__ __forceinline__ void triple_merge(float& m, double& d, float (&a)[V],
   m = mn;
 }
 
+// The two score maps. Additive (GAT): s = LeakyReLU(a_s[src, k] + a_d[t, k])
+// from the node projections. Scaled dot product (the Transformer-style GAT,
+// Sec. 4.2): s = scale * <q[t, k], key[src, k]> over the D columns of head k;
+// a lane holds V of them, and the partial products are summed over the G =
+// D / V lanes of the head with xor shuffles (every lane of the head gets the
+// score).
+struct Scores {
+  const float* as;  // additive: [N, H]
+  const float* ad;
+  float slope;
+  const float* q;  // dot product: [N, H*D]
+  const float* key;
+  float scale;
+  int G;  // lanes per head (dot product)
+};
+
+template <bool DOT>
+__device__ __forceinline__ float group_sum(float v, int G) {
+  for (int o = 1; o < G; o <<= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Score of edge (c -> t) at head k for one lane holding all D columns (the
+// coefficient sweeps, lanes = (slot, head)).
+template <bool DOT>
+__device__ __forceinline__ float lane_score(const Scores& sc, int64_t c, int64_t t, int k, int H,
+                                            int D) {
+  if constexpr (DOT) {
+    const int64_t F = (int64_t)H * D;
+    const float* qa = sc.q + t * F + (int64_t)k * D;
+    const float* ka = sc.key + c * F + (int64_t)k * D;
+    float acc = 0.0f;
+    for (int d = 0; d < D; ++d) acc = __builtin_fmaf(qa[d], ka[d], acc);
+    return sc.scale * acc;
+  } else {
+    return leaky(sc.as[c * H + k] + sc.ad[t * H + k], sc.slope);
+  }
+}
+
 // A short row (at most kShortRow edges) per edge slot: the slot's lanes load
 // the row's column ids, scores and feature rows at once, take the maximum,
-// then the weighted sums (denominator in double) in graph order.
-template <int V>
-__device__ __forceinline__ void gat_short_row(int t, int sl, int LPS, const int* __restrict__ rowptr,
+// then the weighted sums (denominator in double) in graph order. valid = false
+// (a slot past the list) runs the same steps on no edges, so that the
+// shuffles of the dot-product scores see the whole wave.
+template <int V, bool DOT>
+__device__ __forceinline__ void gat_short_row(bool valid, int t, int sl, int LPS,
+                                              const int* __restrict__ rowptr,
                                               const int* __restrict__ col,
                                               const int* __restrict__ perm, int H, int D,
-                                              const float* __restrict__ as,
-                                              const float* __restrict__ ad, float slope,
-                                              const float* __restrict__ h, float* __restrict__ out,
+                                              const Scores& S, const float* __restrict__ h,
+                                              float* __restrict__ out,
                                               float* __restrict__ alpha_out) {
   const int F = H * D;
-  const int kb = rowptr[t], n = rowptr[t + 1] - kb;  // 0 <= n <= kShortRow
+  const int kb = valid ? rowptr[t] : 0;
+  const int n = valid ? rowptr[t + 1] - kb : 0;  // 0 <= n <= kShortRow
   int c[kShortRow];
 #pragma unroll
   for (int j = 0; j < kShortRow; ++j) c[j] = j < n ? col[kb + j] : 0;
   for (int f0 = 0; f0 < F; f0 += LPS * V) {
     const int f = f0 + sl * V;
-    if (f >= F) continue;
-    const int head = f / D;
-    const float adt = ad[(int64_t)t * H + head];
+    const bool fok = f < F;
+    const int head = fok ? f / D : 0;
+    float qv[V];
+    float adt = 0.0f;
+    if constexpr (DOT) {
+      if (fok && n > 0) {
+        load_row<V>(S.q + (int64_t)t * F + f, qv);
+      } else {
+#pragma unroll
+        for (int v = 0; v < V; ++v) qv[v] = 0.0f;
+      }
+    } else {
+      adt = n > 0 ? S.ad[(int64_t)t * H + head] : 0.0f;
+    }
     float sc[kShortRow], xv[kShortRow][V];
     float m = -__builtin_huge_valf();
 #pragma unroll
     for (int j = 0; j < kShortRow; ++j) {
-      if (j < n) {
-        sc[j] = leaky(as[(int64_t)c[j] * H + head] + adt, slope);
+      const bool use = j < n && fok;
+      if (use) {
         load_row<V>(h + (int64_t)c[j] * F + f, xv[j]);
-        m = sc[j] > m ? sc[j] : m;
       } else {
-        sc[j] = 0.0f;
 #pragma unroll
         for (int v = 0; v < V; ++v) xv[j][v] = 0.0f;
       }
+      if constexpr (DOT) {
+        float kv[V];
+        if (use) {
+          load_row<V>(S.key + (int64_t)c[j] * F + f, kv);
+        } else {
+#pragma unroll
+          for (int v = 0; v < V; ++v) kv[v] = 0.0f;
+        }
+        float p = 0.0f;
+#pragma unroll
+        for (int v = 0; v < V; ++v) p = __builtin_fmaf(qv[v], kv[v], p);
+        sc[j] = S.scale * group_sum<DOT>(p, S.G);
+      } else {
+        sc[j] = j < n ? leaky(S.as[(int64_t)c[j] * H + head] + adt, S.slope) : 0.0f;
+      }
+      if (j < n) m = sc[j] > m ? sc[j] : m;
     }
     double d = 0.0;
     float acc[V];
@@ -125,42 +196,42 @@ __device__ __forceinline__ void gat_short_row(int t, int sl, int LPS, const int*
 #pragma unroll
       for (int v = 0; v < V; ++v) acc[v] = __builtin_fmaf(sc[j], xv[j][v], acc[v]);
     }
+    if (valid && fok) {
 #pragma unroll
-    for (int v = 0; v < V; ++v)
-      out[(int64_t)t * F + f + v] = n > 0 ? (float)((double)acc[v] / d) : 0.0f;
-    if (alpha_out != nullptr && f % D == 0)
+      for (int v = 0; v < V; ++v)
+        out[(int64_t)t * F + f + v] = n > 0 ? (float)((double)acc[v] / d) : 0.0f;
+      if (alpha_out != nullptr && f % D == 0)
 #pragma unroll
-      for (int j = 0; j < kShortRow; ++j)
-        if (j < n) alpha_out[(int64_t)perm[kb + j] * H + head] = (float)((double)sc[j] / d);
+        for (int j = 0; j < kShortRow; ++j)
+          if (j < n) alpha_out[(int64_t)perm[kb + j] * H + head] = (float)((double)sc[j] / d);
+    }
   }
 }
 
 // SLOTS short rows per wavefront, one per edge slot (gat_short_row). A kernel
 // of its own: holding a whole short row in registers takes more of them than
 // the sweep of gat_items, whose occupancy it would otherwise lower.
-template <int V, int SLOTS>
+template <int V, int SLOTS, bool DOT>
 __global__ __launch_bounds__(kBlock) void gat_short(
     const int* __restrict__ short_rows, int n_short, const int* __restrict__ rowptr,
-    const int* __restrict__ col, const int* __restrict__ perm, int H, int D,
-    const float* __restrict__ as, const float* __restrict__ ad, float slope,
+    const int* __restrict__ col, const int* __restrict__ perm, int H, int D, Scores S,
     const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out) {
   constexpr int LPS = kWave / SLOTS;
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const int64_t i = wave * SLOTS + lane / LPS;
-  if (i < n_short)
-    gat_short_row<V>(short_rows[i], lane % LPS, LPS, rowptr, col, perm, H, D, as, ad, slope, h,
-                     out, alpha_out);
+  const bool valid = i < n_short;
+  gat_short_row<V, DOT>(valid, valid ? short_rows[i] : 0, lane % LPS, LPS, rowptr, col, perm, H,
+                        D, S, h, out, alpha_out);
 }
 
 // Wavefronts [0, n_heavy) take the chunks of long rows, [n_heavy, n_heavy +
 // n_long) one other light row each, with the running-triple sweep.
-template <int V, int SLOTS>
+template <int V, int SLOTS, bool DOT>
 __global__ __launch_bounds__(kBlock) void gat_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ col,
-    const int* __restrict__ perm, int H, int D, int HP, const float* __restrict__ as,
-    const float* __restrict__ ad, float slope, const float* __restrict__ h,
+    const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ h,
     float* __restrict__ out, float* __restrict__ alpha_out, float* __restrict__ pacc,
     float* __restrict__ pm, double* __restrict__ pd) {
   constexpr int LPS = kWave / SLOTS;
@@ -190,7 +261,18 @@ __global__ __launch_bounds__(kBlock) void gat_items(
     const int f = f0 + sl * V;
     const bool fok = f < F;
     const int head = fok ? f / D : 0;
-    const float adt = ad[(int64_t)row * H + head];
+    float qv[V];
+    float adt = 0.0f;
+    if constexpr (DOT) {
+      if (fok) {
+        load_row<V>(S.q + (int64_t)row * F + f, qv);
+      } else {
+#pragma unroll
+        for (int v = 0; v < V; ++v) qv[v] = 0.0f;
+      }
+    } else {
+      adt = S.ad[(int64_t)row * H + head];
+    }
     float acc[U][V];
     double den[U];
     float mx[U];
@@ -213,12 +295,27 @@ __global__ __launch_bounds__(kBlock) void gat_items(
           const int jb = s0 + u * SLOTS;
           ok[u] = jb + slot < n;
           const int c = bcast<SLOTS>(cj, jb, slot);
-          sc[u] = ok[u] ? leaky(as[(int64_t)c * H + head] + adt, slope) : 0.0f;
-          if (ok[u] && fok) {
+          const bool use = ok[u] && fok;
+          if (use) {
             load_row<V>(h + (int64_t)c * F + f, xv[u]);
           } else {
 #pragma unroll
             for (int v = 0; v < V; ++v) xv[u][v] = 0.0f;
+          }
+          if constexpr (DOT) {
+            float kv[V];
+            if (use) {
+              load_row<V>(S.key + (int64_t)c * F + f, kv);
+            } else {
+#pragma unroll
+              for (int v = 0; v < V; ++v) kv[v] = 0.0f;
+            }
+            float p = 0.0f;
+#pragma unroll
+            for (int v = 0; v < V; ++v) p = __builtin_fmaf(qv[v], kv[v], p);
+            sc[u] = S.scale * group_sum<DOT>(p, S.G);
+          } else {
+            sc[u] = ok[u] ? leaky(S.as[(int64_t)c * H + head] + adt, S.slope) : 0.0f;
           }
         }
 #pragma unroll
@@ -280,11 +377,10 @@ __global__ __launch_bounds__(kBlock) void gat_items(
   const int SL = kWave / HP;
   const int slot3 = lane / HP, hh = lane % HP;
   if (hh < H) {
-    const float adt = ad[(int64_t)row * H + hh];
     const float mh = s_max[wv][hh];
     const double dn = s_den[wv][hh];
     for (int k = kb + slot3; k < ke; k += SL) {
-      const float w = expf(leaky(as[(int64_t)col[k] * H + hh] + adt, slope) - mh);
+      const float w = expf(lane_score<DOT>(S, col[k], row, hh, H, D) - mh);
       alpha_out[(int64_t)perm[k] * H + hh] = (float)((double)w / dn);
     }
   }
@@ -325,10 +421,10 @@ __global__ __launch_bounds__(kBlock) void gat_merge(const SplitRow* __restrict__
 }
 
 // Attention coefficients of the chunks of long rows, from their row's (m, d).
+template <bool DOT>
 __global__ __launch_bounds__(kBlock) void gat_alpha_chunks(
     const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ col,
-    const int* __restrict__ perm, int H, int HP, const float* __restrict__ as,
-    const float* __restrict__ ad, float slope, const float* __restrict__ pm,
+    const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ pm,
     const double* __restrict__ pd, float* __restrict__ alpha_out) {
   const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
@@ -339,11 +435,10 @@ __global__ __launch_bounds__(kBlock) void gat_alpha_chunks(
   const int SL = kWave / HP;
   const int slot = lane / HP, hh = lane % HP;
   if (hh >= H) return;
-  const float adt = ad[(int64_t)row * H + hh];
   const float mh = pm[(int64_t)pslot * H + hh];
   const double dn = pd[(int64_t)pslot * H + hh];
   for (int k = kb + slot; k < ke; k += SL) {
-    const float w = expf(leaky(as[(int64_t)col[k] * H + hh] + adt, slope) - mh);
+    const float w = expf(lane_score<DOT>(S, col[k], row, hh, H, D) - mh);
     alpha_out[(int64_t)perm[k] * H + hh] = (float)((double)w / dn);
   }
 }
@@ -351,9 +446,8 @@ __global__ __launch_bounds__(kBlock) void gat_alpha_chunks(
 struct GatArgs {
   const Graph* g;
   int H, D, HP;
-  float *as, *ad;
-  float slope;
-  const float* h;
+  Scores S;
+  const float* h;  // the rows that are summed (h, or the values)
   float* out;
   float* alpha_out;
   float* pacc;
@@ -361,23 +455,23 @@ struct GatArgs {
   double* pd;
 };
 
-template <int V>
+template <int V, bool DOT>
 void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
   const Graph& g = *a.g;
   const int waves = g.n_heavy + g.n_long;
   const int64_t short_waves = (g.n_short + slots - 1) / slots;
   const dim3 sgrid((unsigned)((short_waves + kBlock / kWave - 1) / (kBlock / kWave)));
-#define TFG_GAT(SL)                                                                            \
-  do {                                                                                         \
-    if (g.n_short > 0)                                                                         \
-      gat_short<V, SL><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.rowptr, g.col,      \
-                                                g.perm, a.H, a.D, a.as, a.ad, a.slope, a.h,    \
-                                                a.out, a.alpha_out);                           \
-    if (waves > 0)                                                                             \
-      gat_items<V, SL><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows, g.n_long,      \
-                                               g.rowptr, g.col, g.perm, a.H, a.D, a.HP, a.as,  \
-                                               a.ad, a.slope, a.h, a.out, a.alpha_out, a.pacc, \
-                                               a.pm, a.pd);                                    \
+#define TFG_GAT(SL)                                                                              \
+  do {                                                                                           \
+    if (g.n_short > 0)                                                                           \
+      gat_short<V, SL, DOT><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.rowptr, g.col,   \
+                                                     g.perm, a.H, a.D, a.S, a.h, a.out,          \
+                                                     a.alpha_out);                               \
+    if (waves > 0)                                                                               \
+      gat_items<V, SL, DOT><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows, g.n_long,   \
+                                                    g.rowptr, g.col, g.perm, a.H, a.D, a.HP, a.S, \
+                                                    a.h, a.out, a.alpha_out, a.pacc, a.pm,       \
+                                                    a.pd);                                       \
   } while (0)
   switch (slots) {
     case 1: TFG_GAT(1); break;
@@ -418,33 +512,23 @@ size_t gat_aggregate_ws_bytes(const Graph& g, int64_t H, int64_t D) {
 
 int max_fused_heads() { return kMaxHeads; }
 
-int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const float* a_src,
-                         const float* a_dst, float slope, float* out, float* alpha_out, void* ws,
-                         hipStream_t s) {
-  if (g.N == 0 || H == 0 || D == 0) return TFG_OK;
+namespace {
+
+// Vector width for rows of D columns at these addresses (every row read or
+// written with V-wide accesses).
+int gat_vec(int D, std::initializer_list<const float*> ptrs) {
+  for (int v : {4, 2}) {
+    bool ok = D % v == 0;
+    for (const float* p : ptrs) ok = ok && reinterpret_cast<uintptr_t>(p) % (4 * v) == 0;
+    if (ok) return v;
+  }
+  return 1;
+}
+
+template <bool DOT>
+int run_attention(const Graph& g, GatArgs& a, int vec, hipStream_t s) {
+  const int H = a.H, D = a.D;
   const int64_t F = (int64_t)H * D;
-  const GatLayout L = gat_layout(g.N, H, F, g.n_heavy);
-  char* base = static_cast<char*>(ws);
-  GatArgs a;
-  a.g = &g;
-  a.H = H;
-  a.D = D;
-  a.as = reinterpret_cast<float*>(base + L.as);
-  a.ad = reinterpret_cast<float*>(base + L.ad);
-  a.slope = slope;
-  a.h = h;
-  a.out = out;
-  a.alpha_out = alpha_out;
-  a.pacc = reinterpret_cast<float*>(base + L.pacc);
-  a.pm = reinterpret_cast<float*>(base + L.pm);
-  a.pd = reinterpret_cast<double*>(base + L.pd);
-  int rc = launch_node_projections(h, g.N, H, D, a_src, a_dst, a.as, a.ad, s);
-  if (rc) return rc;
-  auto fits = [&](int v) {
-    return D % v == 0 && reinterpret_cast<uintptr_t>(h) % (4 * v) == 0 &&
-           reinterpret_cast<uintptr_t>(out) % (4 * v) == 0;
-  };
-  const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;
   const int lanes = (int)std::min<int64_t>((F + vec - 1) / vec, kWave);
   int p2 = 1;
   while (p2 < lanes) p2 <<= 1;
@@ -456,26 +540,74 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
   if (waves > 0 || g.n_short > 0) {
     dim3 grid((unsigned)((std::max(waves, 1) + kBlock / kWave - 1) / (kBlock / kWave)));
     if (vec == 4)
-      launch_slots<4>(slots, grid, s, a);
+      launch_slots<4, DOT>(slots, grid, s, a);
     else if (vec == 2)
-      launch_slots<2>(slots, grid, s, a);
+      launch_slots<2, DOT>(slots, grid, s, a);
     else
-      launch_slots<1>(slots, grid, s, a);
+      launch_slots<1, DOT>(slots, grid, s, a);
     TFG_LAUNCHED("gat_items");
   }
   if (g.n_split > 0) {
     dim3 mgrid((unsigned)((g.n_split + kBlock / kWave - 1) / (kBlock / kWave)));
-    gat_merge<<<mgrid, kBlock, 0, s>>>(g.split, g.n_split, H, D, a.pacc, a.pm, a.pd, out,
-                                       alpha_out != nullptr ? 1 : 0);
+    gat_merge<<<mgrid, kBlock, 0, s>>>(g.split, g.n_split, H, D, a.pacc, a.pm, a.pd, a.out,
+                                       a.alpha_out != nullptr ? 1 : 0);
     TFG_LAUNCHED("gat_merge");
-    if (alpha_out != nullptr) {
+    if (a.alpha_out != nullptr) {
       dim3 agrid((unsigned)((g.n_heavy + kBlock / kWave - 1) / (kBlock / kWave)));
-      gat_alpha_chunks<<<agrid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.col, g.perm, H, hp, a.as,
-                                                a.ad, slope, a.pm, a.pd, alpha_out);
+      gat_alpha_chunks<DOT><<<agrid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.col, g.perm, H, D, hp,
+                                                     a.S, a.pm, a.pd, a.alpha_out);
       TFG_LAUNCHED("gat_alpha_chunks");
     }
   }
   return TFG_OK;
+}
+
+GatArgs make_args(const Graph& g, int H, int D, float* out, float* alpha_out, void* ws) {
+  const GatLayout L = gat_layout(g.N, H, (int64_t)H * D, g.n_heavy);
+  char* base = static_cast<char*>(ws);
+  GatArgs a{};
+  a.g = &g;
+  a.H = H;
+  a.D = D;
+  a.out = out;
+  a.alpha_out = alpha_out;
+  a.pacc = reinterpret_cast<float*>(base + L.pacc);
+  a.pm = reinterpret_cast<float*>(base + L.pm);
+  a.pd = reinterpret_cast<double*>(base + L.pd);
+  a.S.as = reinterpret_cast<float*>(base + L.as);
+  a.S.ad = reinterpret_cast<float*>(base + L.ad);
+  return a;
+}
+
+}  // namespace
+
+int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const float* a_src,
+                         const float* a_dst, float slope, float* out, float* alpha_out, void* ws,
+                         hipStream_t s) {
+  if (g.N == 0 || H == 0 || D == 0) return TFG_OK;
+  GatArgs a = make_args(g, H, D, out, alpha_out, ws);
+  a.S.slope = slope;
+  a.h = h;
+  int rc = launch_node_projections(h, g.N, H, D, a_src, a_dst, const_cast<float*>(a.S.as),
+                                   const_cast<float*>(a.S.ad), s);
+  if (rc) return rc;
+  return run_attention<false>(g, a, gat_vec(D, {h, out}), s);
+}
+
+bool dot_attention_shape_ok(int64_t D) { return D >= 1 && D <= 64 && (D & (D - 1)) == 0; }
+
+int launch_gat_dot_aggregate(const Graph& g, const float* q, const float* key, const float* v,
+                             int H, int D, float scale, float* out, float* alpha_out, void* ws,
+                             hipStream_t s) {
+  if (g.N == 0 || H == 0 || D == 0) return TFG_OK;
+  GatArgs a = make_args(g, H, D, out, alpha_out, ws);
+  a.h = v;
+  a.S.q = q;
+  a.S.key = key;
+  a.S.scale = scale;
+  const int vec = gat_vec(D, {q, key, v, out});
+  a.S.G = D / vec;  // lanes of one head, a power of two that divides the slot width
+  return run_attention<true>(g, a, vec, s);
 }
 
 }  // namespace tfg

@@ -165,6 +165,15 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
                                     int H, float* ds, void* ws, hipStream_t s);
 // gat.hip
 size_t gat_aggregate_ws_bytes(const Graph& g, int64_t H, int64_t D);
+// Scaled dot-product variant: D a power of two, at most 64.
+bool dot_attention_shape_ok(int64_t D);
+int launch_gat_dot_aggregate(const Graph& g, const float* q, const float* key, const float* v,
+                             int H, int D, float scale, float* out, float* alpha_out, void* ws,
+                             hipStream_t s);
+// backward.hip: out[e, k] = scale * <q[t_e], key[s_e]> over the columns of
+// head k, in COO (by_perm) or graph order.
+int launch_edge_dot(const Graph& g, const float* q, const float* key, int64_t ldk, int64_t F,
+                    int H, float scale, float* out, int by_perm, hipStream_t s);
 int max_fused_heads();
 int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const float* a_src,
                          const float* a_dst, float slope, float* out, float* alpha_out, void* ws,

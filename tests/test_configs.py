@@ -259,3 +259,23 @@ def test_power_law_backward_and_propagation_full_size(tfg, orc, c4):
     ref = (1 - np.float64(np.float32(alpha))) * agg + np.float64(np.float32(alpha)) * x[rows]
     S = (1 - alpha) * S + alpha * np.abs(x[rows])
     assert_scaled(z1[rows], ref, S, what="c4 APPNP first step")
+
+
+def test_transformer_attention_full_size(tfg, orc):
+    """The Transformer-style attention layer (scaled dot-product scores) on the
+    attention workload's graph, fused and as the unfused chain, as timed."""
+    import torch
+    c = graphgen.config3()
+    ei, n, H, D = c["edge_index"], c["N"], c["H"], c["D"]
+    r = graphgen.rng_for(3003, 1)
+    q, k, v = (r.standard_normal((n, H * D), dtype=np.float32) for _ in range(3))
+    scale = 1.0 / np.sqrt(D)
+    g = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n)
+    out = tfg.tfg_gat_dot_aggregate(g, dev(q), dev(k), dev(v), H, scale=scale)
+    torch.cuda.synchronize()
+    ref, _, S = orc.dot_layer(ei, q, k, v, H, np.float32(scale))
+    assert_scaled(host(out), ref, S, what="c3 fused dot attention")
+    s = tfg.tfg_edge_dot_scores(g, dev(q), dev(k), H, scale=scale)
+    rs = orc.dot_scores(ei, q, k, H, np.float32(scale))
+    assert_scaled(host(s), rs, orc.dot_scores(ei, np.abs(q), np.abs(k), H, np.float32(scale)),
+                  what="c3 dot scores")

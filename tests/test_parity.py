@@ -465,3 +465,62 @@ def test_gat_aggregate_fused(tfg, orc, H, D):
     y = tfg.tfg_aggregate(dev(ei), dev(h), n, "sum", edge_weight=a_csr, heads=H,
                           weight_order="csr", graph=g)
     assert_scaled(host(y), ref, S, what="unfused chain")
+
+
+# ---------------------------------------------------------------------------
+# Transformer-style attention (scaled dot-product scores)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("H,D,order,rect", [(1, 16, "coo", False), (4, 8, "csr", False),
+                                            (3, 5, "coo", True), (8, 16, "csr", True)])
+def test_edge_dot_scores(tfg, orc, H, D, order, rect):
+    n, n_src, e = 2000, (1500 if rect else 2000), 30_000
+    ei = graphgen.random_graph(H * 7 + D, n, e, n_src=n_src, hub=4, hub_edges=1000)
+    q = graphgen.features(H + 1, n, H * D)
+    k = graphgen.features(H + 2, n_src, H * D)
+    g = tfg.tfg_graph_create(dev(ei), n, N_src=n_src)
+    s = tfg.tfg_edge_dot_scores(g, dev(q), dev(k), H, scale=0.25, order=order)
+    ref = orc.dot_scores(ei, q, k, H, 0.25)
+    S = orc.dot_scores(ei, np.abs(q), np.abs(k), H, 0.25)
+    got = host(s)
+    if order == "csr":
+        perm = host(tfg.tfg_graph_csr(g)[2])
+        back = np.empty_like(got)
+        back[perm] = got
+        got = back
+    assert_scaled(got, ref, S, what=f"dot scores H={H} D={D}")
+
+
+@pytest.mark.parametrize("H,D,rect", [(8, 16, False), (1, 4, False), (4, 8, True), (2, 64, False),
+                                      (16, 2, False), (3, 1, True)])
+def test_gat_dot_aggregate_fused(tfg, orc, H, D, rect):
+    import torch
+    n, n_src, e = 3000, (2200 if rect else 3000), 40_000
+    ei = graphgen.random_graph(H * 11 + D, n, e, n_src=n_src, hub=3, hub_edges=3000)
+    q = graphgen.features(H + 5, n, H * D)
+    k = graphgen.features(H + 6, n_src, H * D)
+    v = graphgen.features(H + 7, n_src, H * D)
+    scale = 1.0 / np.sqrt(D)
+    g = tfg.tfg_graph_create(dev(ei), n, N_src=n_src)
+    out, alpha = tfg.tfg_gat_dot_aggregate(g, dev(q), dev(k), dev(v), H, scale=scale,
+                                           want_alpha=True)
+    torch.cuda.synchronize()
+    ref, ref_alpha, S = orc.dot_layer(ei, q, k, v, H, np.float32(scale))
+    assert_scaled(host(out), ref, S, what=f"fused dot attention H={H} D={D}")
+    assert_rel(host(alpha), ref_alpha, tol=2e-5, what="fused dot attention alpha")
+    empty = np.bincount(ei[1], minlength=n) == 0
+    assert np.all(host(out)[empty] == 0)
+    # the unfused chain of the library gives the same layer
+    s = tfg.tfg_edge_dot_scores(g, dev(q), dev(k), H, scale=scale)
+    _, a_csr = tfg.tfg_segment_softmax(s, dev(ei[1]), n, graph=g, out_csr=True)
+    y = tfg.tfg_aggregate(dev(ei), dev(v), n, "sum", edge_weight=a_csr, heads=H,
+                          weight_order="csr", graph=g)
+    assert_scaled(host(y), ref, S, what="unfused dot chain")
+
+
+def test_gat_dot_rejects_shapes(tfg):
+    ei = dev(np.array([[0, 1], [1, 2]]))
+    g = tfg.tfg_graph_create(ei, 4)
+    x = dev(np.ones((4, 12), np.float32))
+    with pytest.raises(ValueError):  # D = 3 is not a power of two
+        tfg.tfg_gat_dot_aggregate(g, x, x, x, 4)
