@@ -138,3 +138,12 @@ def test_python_binding_rejects_host_tensors():
     ei = torch.zeros((2, 3), dtype=torch.int64)
     with pytest.raises(ValueError):
         tfg.tfg_graph_create(ei, 4)
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    # no CPU fallback: without the built library every call raises
+    import paper_2101_11552_amd as tfg
+    monkeypatch.setattr(tfg, "LIB_PATH", str(tmp_path / "libtfg.so"))
+    monkeypatch.setattr(tfg, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        tfg.load()
