@@ -54,6 +54,7 @@ def lib():
         _lib.orc_aggregate_backward.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, i64,
                                                 ctypes.c_int, p, p, p, p]
         _lib.orc_segment_softmax_backward.argtypes = [i64, i64, p, p, p, i64, p]
+        _lib.orc_segment_pool_backward.argtypes = [i64, i64, p, i64, ctypes.c_int, p, p, p]
         _lib.orc_dot_scores.argtypes = [i64, p, p, p, p, i64, i64, i64, i64, ctypes.c_double, p]
         _lib.orc_dot_layer.argtypes = [i64, p, p, p, p, p, i64, i64, i64, i64, ctypes.c_double,
                                        p, p, p]
@@ -183,6 +184,19 @@ def propagate(edge_index, x, K, alpha=0.0, h=None, edge_weight=None):
                                x.ctypes.data_as(ctypes.c_void_p), ldx, N, F, K, float(alpha),
                                _ptr(hh), _ptr(out64), _ptr(scale)))
     return out64, scale
+
+
+def segment_pool_backward(dy, graph_index, G, reduce="sum", arg=None):
+    """Gradient of ``segment_pool`` for dL/d out = dy [G, F]: dx [Nb, F] in float64."""
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    gi = _i64(graph_index)
+    if dy.shape[0] != G or (arg is not None and np.shape(arg) != dy.shape):
+        raise ValueError("dy and arg must be [G, F]")
+    a = None if arg is None else _i64(arg)
+    dx = np.empty((gi.shape[0], dy.shape[1]), np.float64)
+    _check(lib().orc_segment_pool_backward(gi.shape[0], dy.shape[1], _ptr(gi), G, REDUCE[reduce],
+                                           _ptr(dy), _ptr(a), _ptr(dx)))
+    return dx
 
 
 def dot_scores(edge_index, q, key, heads, scale):

@@ -417,6 +417,41 @@ int orc_segment_pool(int64_t Nb, int64_t F, int64_t ldx, const float *x, const i
 }
 
 /*
+ * Gradient of orc_segment_pool for dL/d out = dy ([G, F]): node n of graph g
+ * receives dy[g, c] (sum), dy[g, c] / (nodes of g) (mean), or dy[g, c] only
+ * where it was the argmax of (g, c) (max; arg as the forward returned it).
+ * dx64: [Nb, F] in double.
+ */
+int orc_segment_pool_backward(int64_t Nb, int64_t F, const int64_t *gi, int64_t G, int reduce,
+                              const float *dy, const int64_t *arg, double *dx64)
+{
+    for (int64_t n = 0; n < Nb; ++n) {
+        if (gi[n] < 0 || gi[n] >= G)
+            return ORC_ERR_INDEX_RANGE;
+        if (n > 0 && gi[n] < gi[n - 1])
+            return ORC_ERR_UNSORTED;
+    }
+    if (reduce == ORC_MAX && arg == NULL)
+        return ORC_ERR_INVALID_ARG;
+    int64_t *cnt = (int64_t *)calloc((size_t)(G > 0 ? G : 1), sizeof(int64_t));
+    for (int64_t n = 0; n < Nb; ++n)
+        cnt[gi[n]] += 1;
+    for (int64_t n = 0; n < Nb; ++n) {
+        int64_t g = gi[n];
+        for (int64_t c = 0; c < F; ++c) {
+            double v = (double)dy[g * F + c];
+            if (reduce == ORC_MEAN)
+                v /= (double)cnt[g];
+            if (reduce == ORC_MAX && arg[g * F + c] != n)
+                v = 0.0;
+            dx64[n * F + c] = v;
+        }
+    }
+    free(cnt);
+    return ORC_OK;
+}
+
+/*
  * GAT attention scores, the first map of Fig. 5(a): with heads laid out as
  * h[n, k*D + d] (head k, dim d),
  *   a_s[n, k] = sum_d a_src[k, d] h[n, k, d],  a_d[n, k] = sum_d a_dst[k, d] h[n, k, d]

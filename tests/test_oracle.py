@@ -727,3 +727,38 @@ def test_dot_layer_single_edge_copies_value(orc):
     out, alpha, _ = orc.dot_layer(ei, q, k, v, 2, 0.5)
     np.testing.assert_array_equal(out[0], v[3].astype(np.float64))
     assert np.all(out[[1, 3]] == 0) and np.all(alpha[0] == 1.0)
+
+
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_pool_backward_finite_differences(orc, reduce):
+    sizes = np.array([3, 1, 4, 2])
+    gi = np.repeat(np.arange(4), sizes)
+    Nb, F, G = gi.shape[0], 3, 4
+    rng = np.random.default_rng(81)
+    x = rng.standard_normal((Nb, F)).astype(np.float32)
+    dy = rng.standard_normal((G, F))
+    arg = orc.segment_pool(x, gi, G, "max")[1] if reduce == "max" else None
+    dx = orc.segment_pool_backward(dy, gi, G, reduce, arg=arg)
+
+    def loss(xx):
+        out = orc.segment_pool(xx, gi, G, reduce)[0]
+        return float((np.asarray(out, np.float64) * dy).sum())
+    eps = 2.0 ** -10  # the pooled values are exact sums / copies at these magnitudes
+    for n in range(Nb):
+        for c in range(F):
+            xp, xm = x.copy(), x.copy()
+            xp[n, c] += eps
+            xm[n, c] -= eps
+            fd = (loss(xp) - loss(xm)) / (2 * eps)
+            assert fd == pytest.approx(dx[n, c], rel=1e-6, abs=1e-9)
+
+
+def test_pool_backward_mean_sums_to_dy(orc):
+    # every graph's mean gradient adds back up to its dy row
+    sizes = np.array([5, 2, 7])
+    gi = np.repeat(np.arange(3), sizes)
+    dy = np.random.default_rng(82).standard_normal((3, 4)).astype(np.float32)
+    dx = orc.segment_pool_backward(dy, gi, 3, "mean")
+    tot = np.zeros((3, 4))
+    np.add.at(tot, gi, dx)
+    np.testing.assert_allclose(tot, dy.astype(np.float64), rtol=1e-14)
