@@ -406,6 +406,20 @@ int tfg_segment_pool(const float *x, int64_t Nb, int64_t F, int64_t ldx, const v
                      int index_type, int64_t G, int reduce, float *out, int32_t *argmax,
                      int validate, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
+/*
+ * Gradient of tfg_segment_pool, for training graph-level models through the
+ * pooling (Sec. 4.1): given dy = dL/d out ([G, F], contiguous), node n of
+ * graph g receives dx[n, c] = dy[g, c] (TFG_SUM), dy[g, c] / (nodes of g)
+ * (TFG_MEAN), or dy[g, c] if argmax[g, c] == n and 0 otherwise (TFG_MAX;
+ * argmax as the forward call returned it). dx: [Nb, F] with leading
+ * dimension ldx, overwritten. graph_index, validate and ws as in
+ * tfg_segment_pool (same workspace size).
+ */
+int tfg_segment_pool_backward(const float *dy, int64_t G, int64_t F, const void *graph_index,
+                              int index_type, int64_t Nb, int reduce, const int32_t *argmax,
+                              float *dx, int64_t ldx, int validate, void *ws, size_t ws_bytes,
+                              tfg_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* BatchGraph construction                                                   */
 /* ------------------------------------------------------------------------ */

@@ -103,6 +103,7 @@ def load():
         "tfg_segment_softmax_backward": (ci, [p, p, i64, i64, p, ci, i64, p, p, p, sz, p]),
         "tfg_edge_reorder_ws_bytes": (sz, [p, p, i64]),
         "tfg_edge_dot_scores": (ci, [p, p, p, i64, i64, ctypes.c_float, p, ci, p]),
+        "tfg_segment_pool_backward": (ci, [p, i64, i64, p, ci, i64, ci, p, p, i64, ci, p, sz, p]),
         "tfg_gat_dot_aggregate_ws_bytes": (sz, [p, i64, i64]),
         "tfg_gat_dot_aggregate": (ci, [p, p, p, p, i64, i64, ctypes.c_float, p, p, p, sz, p]),
         "tfg_edge_reorder": (ci, [p, p, p, i64, p, p, sz, p]),
@@ -519,6 +520,29 @@ def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce:
     _check(lib.tfg_segment_pool(_ptr(x), Nb, F, ldx, _ptr(gi), _index_type(gi), G, red, _ptr(out),
                                 _ptr(arg), int(validate), _ptr(ws), ws.numel(), _stream(dev)))
     return (out, arg) if red == 2 else out
+
+
+def tfg_segment_pool_backward(dy: torch.Tensor, graph_index: torch.Tensor, reduce: str = "sum",
+                              argmax: torch.Tensor | None = None, validate: bool = True,
+                              out: torch.Tensor | None = None) -> torch.Tensor:
+    """Gradient of ``tfg_segment_pool`` for dy = dL/d out [G, F]: dx [Nb, F]."""
+    lib = load()
+    dy = _f32(dy, "dy")
+    G, F = dy.shape
+    gi = _dev(graph_index, "graph_index").contiguous()
+    Nb = gi.shape[0]
+    red = _REDUCE[reduce]
+    am = None
+    if argmax is not None:
+        am = _dev(argmax, "argmax").contiguous()
+        if am.dtype != torch.int32 or am.shape != dy.shape:
+            raise ValueError("argmax must be int32 [G, F]")
+    dx = out if out is not None else torch.empty((Nb, F), dtype=torch.float32, device=dy.device)
+    ws = _workspace(lib.tfg_segment_pool_ws_bytes(Nb, G), dy.device)
+    _check(lib.tfg_segment_pool_backward(_ptr(dy), G, F, _ptr(gi), _index_type(gi), Nb, red,
+                                         _ptr(am), _ptr(dx), F, int(validate), _ptr(ws),
+                                         ws.numel(), _stream(dy.device)))
+    return dx
 
 
 def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,

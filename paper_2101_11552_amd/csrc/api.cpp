@@ -605,6 +605,39 @@ int tfg_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const v
   return TFG_OK;
 }
 
+int tfg_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void* graph_index,
+                              int index_type, int64_t Nb, int reduce, const int32_t* argmax,
+                              float* dx, int64_t ldx, int validate, void* ws, size_t ws_bytes,
+                              tfg_stream_t stream) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  int rc = check_counts(0, Nb, 0);
+  if (rc) return rc;
+  if (G < 0 || G >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad G");
+  if (F < 0 || F >= kMaxCount || ldx < F) return fail(TFG_ERR_INVALID_ARG, "bad F / ldx");
+  if (reduce != TFG_SUM && reduce != TFG_MEAN && reduce != TFG_MAX)
+    return fail(TFG_ERR_INVALID_ARG, "bad reduce");
+  if (Nb > 0 && F > 0 && (graph_index == nullptr || dx == nullptr || (G > 0 && dy == nullptr)))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (reduce == TFG_MAX && Nb > 0 && F > 0 && G > 0 && argmax == nullptr)
+    return fail(TFG_ERR_INVALID_ARG, "the max gradient needs the forward argmax");
+  if (ws == nullptr || ws_bytes < tfg_segment_pool_ws_bytes(Nb, G))
+    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  hipStream_t s = as_stream(stream);
+  int* goff = static_cast<int*>(ws);
+  int* err = reinterpret_cast<int*>(static_cast<char*>(ws) + align_up(sizeof(int) * (size_t)(G + 1), 256));
+  rc = launch_segment_pool_backward(dy, G, F, graph_index, index_type, Nb, reduce, argmax, dx, ldx,
+                                    goff, err, s);
+  if (rc) return rc;
+  if (validate) {
+    int flags = 0;
+    TFG_HIP(hipMemcpyAsync(&flags, err, sizeof(int), hipMemcpyDeviceToHost, s));
+    TFG_HIP(hipStreamSynchronize(s));
+    if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "graph_index holds an id outside [0, G)");
+    if (flags & kErrUnsorted) return fail(TFG_ERR_UNSORTED, "graph_index is not non-decreasing");
+  }
+  return TFG_OK;
+}
+
 size_t tfg_batch_graphs_ws_bytes(int64_t G) { return G < 0 ? 0 : batch_ws_bytes(G); }
 
 int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,

@@ -1,6 +1,7 @@
 // Graph pooling over a sorted node -> graph index (gfx950): segment bounds
 // from the sorted index (with range and order checks), then one wavefront per
-// graph reducing its contiguous node rows (sum / mean / max + argmax).
+// graph reducing its contiguous node rows (sum / mean / max + argmax); and its
+// gradient, one thread per node and column vector.
 #include "wave.h"
 
 namespace tfg {
@@ -182,6 +183,89 @@ void launch_pool_vec(int vec, int slots, dim3 grid, hipStream_t s, const float* 
 }
 
 }  // namespace
+
+namespace {
+
+// Gradient of the pooling: one thread per (node, V columns) writes
+// dx[n, c] = dy[g, c] (sum), dy[g, c] / count(g) (mean), or dy[g, c] where
+// node n won the forward max of (g, c), else 0. g = the clamped graph id; the
+// counts come from the segment bounds.
+template <typename IdxT, int V>
+__global__ __launch_bounds__(kBlock) void pool_grad(const float* __restrict__ dy, int64_t G,
+                                                    int F, const IdxT* __restrict__ gi,
+                                                    int64_t Nb, const int* __restrict__ goff,
+                                                    int reduce, const int* __restrict__ arg,
+                                                    float* __restrict__ dx, int64_t ldx) {
+  const int cols = F / V;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= Nb * cols) return;
+  const int64_t n = i / cols;
+  const int f = (int)(i - n * cols) * V;
+  const int64_t g = clamp_gid((int64_t)gi[n], G);
+  float v[V];
+  if (g < 0) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) v[j] = 0.0f;
+  } else {
+    load_row<V>(dy + g * F + f, v);
+    if (reduce == TFG_MEAN) {
+      const float cnt = (float)(goff[g + 1] - goff[g]);
+#pragma unroll
+      for (int j = 0; j < V; ++j) v[j] = cnt > 0.0f ? v[j] / cnt : 0.0f;
+    } else if (reduce == TFG_MAX) {
+#pragma unroll
+      for (int j = 0; j < V; ++j) v[j] = arg[g * F + f + j] == (int)n ? v[j] : 0.0f;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < V; ++j) dx[n * ldx + f + j] = v[j];
+}
+
+template <typename IdxT>
+void launch_pool_grad(int vec, const float* dy, int64_t G, int F, const void* gi, int64_t Nb,
+                      const int* goff, int reduce, const int* arg, float* dx, int64_t ldx,
+                      hipStream_t s) {
+  const int64_t n = Nb * (F / vec);
+  const unsigned nb = (unsigned)((n + kBlock - 1) / kBlock);
+  const IdxT* g = static_cast<const IdxT*>(gi);
+  if (vec == 4)
+    pool_grad<IdxT, 4><<<nb, kBlock, 0, s>>>(dy, G, F, g, Nb, goff, reduce, arg, dx, ldx);
+  else if (vec == 2)
+    pool_grad<IdxT, 2><<<nb, kBlock, 0, s>>>(dy, G, F, g, Nb, goff, reduce, arg, dx, ldx);
+  else
+    pool_grad<IdxT, 1><<<nb, kBlock, 0, s>>>(dy, G, F, g, Nb, goff, reduce, arg, dx, ldx);
+}
+
+}  // namespace
+
+int launch_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void* graph_index,
+                                 int index_type, int64_t Nb, int reduce, const int32_t* argmax,
+                                 float* dx, int64_t ldx, int* goff, int* err, hipStream_t s) {
+  fill_goff<<<1, 64, 0, s>>>(err, 1);
+  if (Nb == 0 || F == 0) return TFG_OK;
+  fill_goff<<<(unsigned)((G + 1 + kBlock - 1) / kBlock), kBlock, 0, s>>>(goff, G + 1);
+  const unsigned nb = (unsigned)((Nb + 1 + kBlock - 1) / kBlock);
+  if (index_type == TFG_I64)
+    segment_bounds<int64_t><<<nb, kBlock, 0, s>>>(static_cast<const int64_t*>(graph_index), Nb, G,
+                                                   goff, err);
+  else
+    segment_bounds<int32_t><<<nb, kBlock, 0, s>>>(static_cast<const int32_t*>(graph_index), Nb, G,
+                                                   goff, err);
+  TFG_LAUNCHED("segment_bounds");
+  auto fits = [&](int v) {
+    return F % v == 0 && ldx % v == 0 && reinterpret_cast<uintptr_t>(dx) % (4 * v) == 0 &&
+           reinterpret_cast<uintptr_t>(dy) % (4 * v) == 0;
+  };
+  const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;
+  if (index_type == TFG_I64)
+    launch_pool_grad<int64_t>(vec, dy, G, (int)F, graph_index, Nb, goff, reduce, argmax, dx, ldx,
+                              s);
+  else
+    launch_pool_grad<int32_t>(vec, dy, G, (int)F, graph_index, Nb, goff, reduce, argmax, dx, ldx,
+                              s);
+  TFG_LAUNCHED("pool_grad");
+  return TFG_OK;
+}
 
 int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const void* graph_index,
                         int index_type, int64_t G, int reduce, float* out, int32_t* argmax,

@@ -146,6 +146,10 @@ int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
                         const void* graph_index, int index_type, int64_t G, int reduce,
                         float* out, int32_t* argmax, int* goff_ws, int* err, hipStream_t s);
 
+int launch_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void* graph_index,
+                                 int index_type, int64_t Nb, int reduce, const int32_t* argmax,
+                                 float* dx, int64_t ldx, int* goff, int* err, hipStream_t s);
+
 // softmax.hip: a_s = a_src . h and a_d = a_dst . h per (node, head)
 int launch_node_projections(const float* h, int64_t N, int H, int D, const float* a_src,
                             const float* a_dst, float* as, float* ad, hipStream_t s);

@@ -259,3 +259,36 @@ def test_softmax_backward(tfg, orc, H, with_graph):
     np.add.at(dot, seg, a32.astype(np.float64) * np.abs(da))
     S = a32 * (np.abs(da) + dot[seg])
     assert_scaled(host(ds), ref, S, what="dscores")
+
+
+@pytest.mark.parametrize("reduce,idx", [("sum", np.int32), ("mean", np.int64), ("max", np.int32)])
+def test_pool_backward(tfg, orc, reduce, idx):
+    import torch
+    sizes = graphgen.rng_for(95, 0).integers(0, 40, 300)  # some graphs without nodes
+    gi = np.repeat(np.arange(300), sizes)
+    Nb, F, G = gi.shape[0], 24, 300
+    x = graphgen.features(95, Nb, F)
+    dy = graphgen.features(96, G, F)
+    arg_dev, arg = None, None
+    if reduce == "max":
+        _, arg_dev = tfg.tfg_segment_pool(dev(x), dev(gi.astype(idx)), G, "max")
+        _, arg = orc.segment_pool(x, gi, G, "max")
+        assert np.array_equal(host(arg_dev), arg)
+    dx = tfg.tfg_segment_pool_backward(dev(dy), dev(gi.astype(idx)), reduce, argmax=arg_dev)
+    torch.cuda.synchronize()
+    ref = orc.segment_pool_backward(dy, gi, G, reduce, arg=arg)
+    # sum and max copy dy exactly; mean divides once in float32 (dy / count)
+    if reduce == "mean":
+        cnt = np.bincount(gi, minlength=G)[gi][:, None]
+        assert same_bits(host(dx), (dy[gi] / cnt.astype(np.float32)).astype(np.float32))
+        np.testing.assert_allclose(host(dx), ref, rtol=1e-6)
+    else:
+        assert same_bits(host(dx), ref.astype(np.float32))
+
+
+def test_pool_backward_rejects_bad_index(tfg):
+    dy = dev(np.ones((3, 4), np.float32))
+    with pytest.raises(ValueError):  # decreasing ids (TfgValueError for TFG_ERR_UNSORTED)
+        tfg.tfg_segment_pool_backward(dy, dev(np.array([0, 2, 1], np.int32)))
+    with pytest.raises(IndexError):
+        tfg.tfg_segment_pool_backward(dy, dev(np.array([0, 1, 3], np.int32)))
