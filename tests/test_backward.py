@@ -292,3 +292,24 @@ def test_pool_backward_rejects_bad_index(tfg):
         tfg.tfg_segment_pool_backward(dy, dev(np.array([0, 2, 1], np.int32)))
     with pytest.raises(IndexError):
         tfg.tfg_segment_pool_backward(dy, dev(np.array([0, 1, 3], np.int32)))
+
+
+def test_new_calls_on_empty_inputs(tfg):
+    import torch
+    n = 20
+    ei = dev(np.zeros((2, 0), np.int64))
+    g = tfg.tfg_graph_create(ei, n)
+    gt = tfg.tfg_graph_create_transposed(ei, n)
+    x = dev(graphgen.features(97, n, 16))
+    # attention over a graph without edges: zero output, nothing to score
+    out = tfg.tfg_gat_dot_aggregate(g, x, x, x, 4)
+    s = tfg.tfg_edge_dot_scores(g, x, x, 4)
+    # reordering an empty per-edge array, pooling gradient without nodes
+    r = tfg.tfg_edge_reorder(torch.zeros((0, 2), device=x.device), src=g, dst=gt)
+    dxp = tfg.tfg_segment_pool_backward(dev(np.ones((3, 4), np.float32)),
+                                        dev(np.zeros(0, np.int32)))
+    # F = 0 features
+    dx0, _ = tfg.tfg_aggregate_backward(g, dev(np.zeros((n, 0), np.float32)), "sum", graph_t=gt)
+    torch.cuda.synchronize()
+    assert np.all(host(out) == 0) and s.shape == (0, 4) and r.shape == (0, 2)
+    assert dxp.shape == (0, 4) and dx0.shape == (n, 0)
