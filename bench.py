@@ -116,6 +116,17 @@ def _timed(torch, fn, reps: int, warm: int = 2) -> float:
     return a0.elapsed_time(a1) / reps
 
 
+def _oracle(fn, units: int, unit: str, sample: str):
+    """The oracle on the host (one thread), timed on a bounded sample: the rate
+    in `unit` (units per second, scaled like the GPU figure)."""
+    t0 = time.perf_counter()
+    fn()
+    dt = time.perf_counter() - t0
+    scale = 1e9 if unit == "GE/s" else 1.0
+    return {"value": round(units / dt / scale, 6), "unit": unit, "cores": 1, "kind": "oracle",
+            "sample": f"{sample}, {dt:.2f} s"}
+
+
 def _row(name: str, workload: str, ms: float, edges: int | None, nbytes: int | None, **extra):
     line = {"row": name, "workload": workload, "ms": round(ms, 4)}
     if edges is not None:
@@ -165,21 +176,37 @@ def run_suite(args):
     ms_coo = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", graph_t=gt, edge_weight=norm["edge_weight"], weight_order="coo",
         want_dx=True, ws=ws), reps)
+    import oracle
+    cpu = {}
+    if not args.no_cpu_baseline:
+        m = 4_000_000
+        sub = np.ascontiguousarray(ei_np[:, :m].astype(np.int64))
+        w_sub = np.random.default_rng(7).uniform(0.1, 1.0, m).astype(np.float32)
+        dy_h = dy.cpu().numpy()
+        cpu["bw"] = _oracle(lambda: oracle.aggregate_backward(sub, x_np, N, dy_h, "sum",
+                                                              edge_weight=w_sub),
+                            m, "GE/s", f"first {m} edges, all {N} nodes, F={F}: dx and dw together")
+        cpu["appnp"] = _oracle(lambda: oracle.propagate(sub, x_np, 3, alpha=0.1, h=x_np,
+                                                        edge_weight=w_sub),
+                               3 * m, "GE/s", f"first {m} edges, all {N} nodes, F={F}, K=3")
+        del sub, dy_h
     # per edge: target id, the weight and a dy row; per source: a dx row
     _row("backward dx (transposed sum aggregation)", wl, ms, Ep,
          Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="spmm_rows over the transposed graph",
          src_parts=gt.info()["src_parts"], weights="transposed graph order",
-         ms_with_edge_order_weights=round(ms_coo, 4))
+         ms_with_edge_order_weights=round(ms_coo, 4), cpu_baseline=cpu.get("bw"))
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", x=x, want_dx=False, want_dw=True, dw_order="csr", ws=ws), reps)
     # per edge: source id, an x row, the dw value; per target: a dy row
     _row("backward dw (per-edge dot products)", wl, ms, Ep,
-         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="edge_grad_rows")
+         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="edge_grad_rows",
+         cpu_baseline=cpu.get("bw"))
     K = 3
     ms = _timed(torch, lambda: tfg.tfg_propagate(g, x, K, alpha=0.1, h=x,
                                                 edge_weight=norm["edge_weight_csr"]), reps)
     _row(f"APPNP propagation, K={K}, alpha=0.1", wl, ms, K * Ep,
-         K * (Ep * (8 + 4 * F) + N * 8 * F + 4 * (N + 1)), ms_per_step=round(ms / K, 4))
+         K * (Ep * (8 + 4 * F) + N * 8 * F + 4 * (N + 1)), ms_per_step=round(ms / K, 4),
+         cpu_baseline=cpu.get("appnp"))
     del g, gt, norm, dy, ws, ei, x
     torch.cuda.empty_cache()
 
@@ -201,10 +228,16 @@ def run_suite(args):
         return tfg.tfg_aggregate(ei3, h, n3, "sum", edge_weight=a_csr, heads=H,
                                  weight_order="csr", graph=g3)
     ms_c = _timed(torch, chain, reps)
+    ei3_np = c["edge_index"]
+    if not args.no_cpu_baseline:
+        cpu["gat"] = _oracle(lambda: oracle.gat_layer(ei3_np, c["h"], c["a_src"], c["a_dst"], H,
+                                                      slope=np.float32(c["slope"])),
+                             E3, "GE/s", "the whole attention graph")
     _row("fused attention aggregation", wl3, ms_f, E3,
          E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
-         kernel="node_projections_vec + gat_items + gat_merge", unfused_chain_ms=round(ms_c, 4),
-         speedup_vs_unfused=round(ms_c / ms_f, 3))
+         kernel="node_projections_vec + gat_short + gat_items + gat_merge",
+         unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
+         cpu_baseline=cpu.get("gat"))
     # the Transformer-style variant: q, key, v of the same shape as h
     gen = torch.Generator(device=dev).manual_seed(3)
     qd, kd, vd = (torch.randn((n3, Fh), generator=gen, device=dev) for _ in range(3))
@@ -216,22 +249,38 @@ def run_suite(args):
         return tfg.tfg_aggregate(ei3, vd, n3, "sum", edge_weight=a_csr, heads=H,
                                  weight_order="csr", graph=g3)
     ms_c = _timed(torch, dot_chain, reps)
+    if not args.no_cpu_baseline:
+        qh, kh, vh = (t.cpu().numpy() for t in (qd, kd, vd))
+        cpu["dot"] = _oracle(lambda: oracle.dot_layer(ei3_np, qh, kh, vh, H, 1.0 / np.sqrt(c["D"])),
+                             E3, "GE/s", "the whole attention graph")
+        del qh, kh, vh
     # per edge: source id, the key and value rows; per node: q row, output row
     _row("fused Transformer-style attention (scaled dot product)", wl3, ms_f, E3,
          E3 * (4 + 8 * Fh) + n3 * (8 * Fh + 4), kernel="gat_short + gat_items (dot) + gat_merge",
-         unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3))
+         unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
+         cpu_baseline=cpu.get("dot"))
     del qd, kd, vd
     s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3), reps)
     # per edge: edge id, the scores (read twice by the kernel, counted once), alpha
+    if not args.no_cpu_baseline:
+        s_h = s.cpu().numpy()
+        cpu["sm"] = _oracle(lambda: oracle.segment_softmax(s_h, ei3_np[1], n3), E3, "GE/s",
+                            "the whole attention graph")
     _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1),
-         kernel="softmax_items + softmax_merge + softmax_write")
+         kernel="softmax_short + softmax_items + softmax_merge + softmax_write",
+         cpu_baseline=cpu.get("sm"))
     alpha = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3)
     dal = torch.randn_like(alpha)
+    if not args.no_cpu_baseline:
+        a_h, d_h = alpha.cpu().numpy(), dal.cpu().numpy()
+        cpu["smb"] = _oracle(lambda: oracle.segment_softmax_backward(a_h, d_h, ei3_np[1], n3), E3,
+                             "GE/s", "the whole attention graph")
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax_backward(alpha, dal, ei3[1], n3, graph=g3),
                 reps)
     _row("segment softmax backward", wl3, ms, E3, E3 * (4 + 12 * H) + 4 * (n3 + 1),
-         kernel="softmax_grad_items + softmax_grad_merge + softmax_grad_write")
+         kernel="softmax_grad_items + softmax_grad_merge + softmax_grad_write",
+         cpu_baseline=cpu.get("smb"))
     del g3, ei3, h, s, alpha, dal
     torch.cuda.empty_cache()
 
@@ -251,8 +300,23 @@ def run_suite(args):
                       device=dev)
     ms = _timed(torch, lambda: tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False, out=bout,
                                                     ws=bws), reps)
+    if not args.no_cpu_baseline:
+        cpu["batch"] = _oracle(lambda: oracle.batch_graphs(sizes, graphs), Eb, "GE/s",
+                               "the whole batch")
+
+        def oracle_step():
+            oei, ow, _ = oracle.gcn_norm(c["edge_index"], Nb)
+            hb = c["x"]
+            for _ in range(c["layers"]):
+                hb = oracle.aggregate(oei, hb, Nb, "sum", edge_weight=ow)[0].astype(np.float32)
+            return [oracle.segment_pool(hb, c["graph_index"], G, r) for r in ("sum", "mean", "max")]
+        cpu["mb"] = _oracle(oracle_step, 3 * (Eb + Nb), "GE/s",
+                            "the whole batch (normalisation, 3 layers, 3 pools)")
+        cpu["pool"] = _oracle(lambda: oracle.segment_pool(c["x"], c["graph_index"], G, "sum"),
+                              Nb, "nodes/s", "the whole batch")
     _row("BatchGraph construction", wl5, ms, Eb,
-         Eb * 16 + G * 8 + Nb * 4, kernel="batch_offsets_small + batch_fill")
+         Eb * 16 + G * 8 + Nb * 4, kernel="batch_offsets_small + batch_fill",
+         cpu_baseline=cpu.get("batch"))
 
     def batch_step():
         bei, bgi, _, _ = tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False)
@@ -266,7 +330,7 @@ def run_suite(args):
         return [tfg.tfg_segment_pool(hb, bgi, G, r, validate=False) for r in ("sum", "mean", "max")]
     ms = _timed(torch, batch_step, reps)
     _row("mini-batch step: BatchGraph + CSR + gcn_norm + 3 GCN layers + 3 pools", wl5, ms,
-         3 * (Eb + Nb), None)
+         3 * (Eb + Nb), None, cpu_baseline=cpu.get("mb"))
     gi = torch.from_numpy(c["graph_index"].astype(np.int32)).to(dev)
     pout = torch.empty((G, Fb), dtype=torch.float32, device=dev)
     pws = torch.empty(max(tfg.load().tfg_segment_pool_ws_bytes(Nb, G), 256), dtype=torch.uint8,
@@ -274,7 +338,8 @@ def run_suite(args):
     ms = _timed(torch, lambda: tfg.tfg_segment_pool(xb, gi, G, "sum", validate=False, out=pout,
                                                     ws=pws), reps)
     _row("segment pool (sum)", wl5, ms, None, Nb * 4 * Fb + Nb * 4 + G * 4 * Fb,
-         kernel="segment_bounds + pool_rows")
+         kernel="segment_bounds + pool_rows", nodes_per_s=round(Nb / (ms * 1e-3), 1),
+         cpu_baseline=cpu.get("pool"))
 
     # --- the GCN step on the two small uniform graphs
     for cfg in (graphgen.config1(), graphgen.config2()):
@@ -289,8 +354,14 @@ def run_suite(args):
             return tfg.tfg_aggregate(None, xc, n, "sum", edge_weight=nm["edge_weight_csr"],
                                      weight_order="csr", graph=gc)
         ms = _timed(torch, gcn_step, reps)
+        cb = None
+        if not args.no_cpu_baseline:
+            def oracle_gcn():
+                oei, ow, _ = oracle.gcn_norm(cfg["edge_index"], n)
+                return oracle.aggregate(oei, cfg["x"], n, "sum", edge_weight=ow)
+            cb = _oracle(oracle_gcn, Ec, "GE/s", "the whole graph")
         _row("GCN step: CSR + gcn_norm + sum aggregation", f"{cfg['name']}: uniform graph N={n}, "
-             f"E'={Ec}, F={Fc}", ms, Ec, None)
+             f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb)
 
 
 def main():
