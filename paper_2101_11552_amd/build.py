@@ -14,8 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libtfg.so")
-SOURCES = ["csr.hip", "norm.hip", "aggregate.hip", "softmax.hip", "gat.hip", "pool.hip",
-           "batch.hip", "backward.hip", "api.cpp"]
+SOURCES = ["csr.hip", "norm.hip", "aggregate.hip", "aggregate_short.hip", "softmax.hip",
+           "gat.hip", "pool.hip", "batch.hip", "backward.hip", "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -123,6 +123,7 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   const int slots = std::min(kWave / p2, 16);
   const bool mx = reduce == TFG_MAX;
   const bool part_plan = use_part_plan(g, F);
+  const bool short_rows = !part_plan && mask == nullptr && !heads && g.n_short > 0;
 
   RowArgs a;
   a.col = g.col;
@@ -155,10 +156,20 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   } else {
     a.heavy = g.heavy;
     a.n_heavy = g.n_heavy;
-    a.light = g.light;
-    a.n_light = g.n_light;
     rows = g.split;
     n_rows = g.n_split;
+    if (short_rows) {
+      // rows of at most kShortRow edges several per wavefront, the rest one each
+      a.light = g.long_rows;
+      a.n_light = g.n_long;
+    } else {
+      a.light = g.light;
+      a.n_light = g.n_light;
+    }
+  }
+  if (short_rows) {
+    dispatch_short(mx, vec, slots, g, a, s);
+    TFG_LAUNCHED("spmm_short");
   }
   const int waves = a.n_heavy + a.n_light;
   if (waves > 0) {

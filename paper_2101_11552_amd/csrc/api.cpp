@@ -87,7 +87,7 @@ int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int
   g.pexec = reinterpret_cast<WorkItem*>(b + L.pexec);
   g.prows = reinterpret_cast<SplitRow*>(b + L.prows);
   g.short_rows = reinterpret_cast<int*>(b + L.short_rows);
-  g.long_rows = reinterpret_cast<int*>(b + L.long_rows);
+  g.long_rows = reinterpret_cast<WorkItem*>(b + L.long_rows);
   g.counters = reinterpret_cast<int*>(b + L.counters);
   TFG_HIP(hipGetDevice(&g.device));
   return build_graph(g, src, tgt, index_type, scratch, scratch_bytes, s);

@@ -452,7 +452,7 @@ __global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__
                                                          WorkItem* __restrict__ light,
                                                          SplitRow* __restrict__ split,
                                                          int* __restrict__ short_rows,
-                                                         int* __restrict__ long_rows) {
+                                                         WorkItem* __restrict__ long_rows) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int beg = 0, deg = 0;
   if (r < N) {
@@ -472,7 +472,7 @@ __global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__
   if (is_short)
     short_rows[q0] = (int)r;
   else if (!is_split)
-    long_rows[m0] = (int)r;
+    long_rows[m0] = WorkItem{(int)r, beg, beg + deg, -1};
   if (is_split) {
     for (int j = 0; j < nch; ++j) {
       const int kb = beg + j * chunk;
@@ -721,7 +721,7 @@ GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk) {
   L.pexec = take(sizeof(WorkItem) * L.cap_pexec);
   L.prows = take(parts > 1 ? sizeof(SplitRow) * N : 0);
   L.short_rows = take(sizeof(int) * std::max<int64_t>(N, 1));
-  L.long_rows = take(sizeof(int) * std::max<int64_t>(N, 1));
+  L.long_rows = take(sizeof(WorkItem) * std::max<int64_t>(N, 1));
   L.counters = take(sizeof(int) * 8);
   L.total = off;
   return L;

@@ -229,7 +229,7 @@ __global__ __launch_bounds__(kBlock) void gat_short(
 // n_long) one other light row each, with the running-triple sweep.
 template <int V, int SLOTS, bool DOT>
 __global__ __launch_bounds__(kBlock) void gat_items(
-    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ long_rows,
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ col,
     const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ h,
     float* __restrict__ out, float* __restrict__ alpha_out, float* __restrict__ pacc,
@@ -251,9 +251,10 @@ __global__ __launch_bounds__(kBlock) void gat_items(
     ke = uniform(heavy[wid].kend);
     pslot = uniform(heavy[wid].slot);
   } else {
-    row = uniform(long_rows[wid - n_heavy]);
-    kb = uniform(rowptr[row]);
-    ke = uniform(rowptr[row + 1]);
+    const WorkItem* it = long_rows + (wid - n_heavy);
+    row = uniform(it->row);
+    kb = uniform(it->kbeg);
+    ke = uniform(it->kend);
     pslot = -1;
   }
   const int F = H * D;

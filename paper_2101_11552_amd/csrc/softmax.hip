@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kBlock) void softmax_short(const int* __restrict__ 
 // d; a chunk stores its pair, softmax_merge combines the chunks of each long
 // row in order and softmax_write writes their outputs.
 __global__ __launch_bounds__(kBlock) void softmax_items(
-    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ long_rows,
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ perm,
     const float* __restrict__ s, int H, int HP, float* __restrict__ out,
     float* __restrict__ out_csr, float* __restrict__ pm, double* __restrict__ pd) {
@@ -209,9 +209,8 @@ __global__ __launch_bounds__(kBlock) void softmax_items(
     ke = uniform(heavy[wid].kend);
     pslot = uniform(heavy[wid].slot);
   } else {
-    const int t = uniform(long_rows[wid - n_heavy]);
-    kb = uniform(rowptr[t]);
-    ke = uniform(rowptr[t + 1]);
+    kb = uniform(long_rows[wid - n_heavy].kbeg);
+    ke = uniform(long_rows[wid - n_heavy].kend);
     pslot = -1;
   }
   for (int hb = 0; hb < H; hb += HP) {

@@ -330,6 +330,10 @@ void dispatch_vec(int vec, int slots, dim3 grid, hipStream_t s, const RowArgs& a
     dispatch_slots<1, MAX, HEADS, SHORT, MASK>(slots, grid, s, a);
 }
 
+// Short rows of the row plan, one per edge slot (aggregate_short.hip).
+void dispatch_short(bool mx, int vec, int slots, const Graph& g, const RowArgs& a,
+                    hipStream_t s);
+
 // Masked sum gathers (backward.hip).
 void dispatch_masked(bool part_plan, bool heads, int vec, int slots, dim3 grid, hipStream_t s,
                      const RowArgs& a);

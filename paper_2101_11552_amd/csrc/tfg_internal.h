@@ -62,10 +62,10 @@ struct Graph {
   WorkItem* light = nullptr;  // whole rows
   SplitRow* split = nullptr;
   int n_heavy = 0, n_light = 0, n_split = 0;
-  // the light rows again, by length: short (0..kShortRow edges, several per
-  // wavefront in the attention kernels) and the rest (one per wavefront)
+  // the light rows again, by length: short (0..kShortRow edges, row ids,
+  // several per wavefront) and the rest (whole-row items, one per wavefront)
   int* short_rows = nullptr;
-  int* long_rows = nullptr;
+  WorkItem* long_rows = nullptr;
   int n_short = 0, n_long = 0;
   // part plan (P > 1): one item per (part, row) segment chunk, part-major
   // order; every item writes a partial, prows[t] reduces row t's partials
