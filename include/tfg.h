@@ -7,7 +7,12 @@
  * node — and graph pooling — reduce the node vectors of each graph of a
  * BatchGraph into one vector per graph. Around them sit the GCN normalisation
  * the paper caches per graph (Sec. 3) and the map -> reduce -> map softmax
- * workflow for attention scores (Sec. 2.1.2, Fig. 5).
+ * workflow for attention scores (Sec. 2.1.2, Fig. 5). Built on them: fused
+ * attention layers (the additive GAT score and the Transformer-style scaled
+ * dot product of Sec. 4.2), multi-step propagation (SGC, APPNP; Sec. 2.2),
+ * BatchGraph construction (Sec. 2.1.1, 2.1.3), and the gradients of the
+ * aggregation, the softmax and the pooling for training through graphs built
+ * inside a model.
  *
  * Conventions shared by every call
  * --------------------------------
