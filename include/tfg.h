@@ -68,7 +68,7 @@ typedef enum {
     TFG_ERR_INDEX_RANGE = 2, /* an edge id outside [0, N_src) / [0, N), a graph id outside [0, G) */
     TFG_ERR_UNSORTED = 3,    /* graph_index is not non-decreasing */
     TFG_ERR_TOO_LARGE = 4,   /* a count does not fit the 31-bit internal indexing */
-    TFG_ERR_WORKSPACE = 5,   /* buffer smaller than the size the matching query returned */
+    TFG_ERR_WORKSPACE = 5,   /* buffer smaller than the size the matching query returned, or not 256-byte aligned */
     TFG_ERR_HIP = 6          /* the HIP runtime reported an error; see tfg_last_error() */
 } tfg_status;
 

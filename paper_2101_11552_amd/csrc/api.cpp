@@ -48,6 +48,15 @@ struct Carver {
   }
 };
 
+// A caller workspace: present, 256-byte aligned (kernels read it with wide
+// loads) and at least `need` bytes.
+int check_ws(const void* ws, size_t bytes, size_t need) {
+  if (ws == nullptr || bytes < need) return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return fail(TFG_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  return TFG_OK;
+}
+
 size_t graph_total_bytes(int64_t E, int64_t N, int parts) {
   return graph_layout(E, N, parts, default_chunk()).total + graph_scratch_bytes(E, N, parts);
 }
@@ -76,11 +85,14 @@ int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int
   GraphLayout L = graph_layout(g.E, N, g.parts, g.chunk);
   if (buf == nullptr || buf_bytes < L.total)
     return fail(TFG_ERR_WORKSPACE, "graph buffer too small");
+  if (reinterpret_cast<uintptr_t>(buf) % 256 != 0 || reinterpret_cast<uintptr_t>(scratch) % 256 != 0)
+    return fail(TFG_ERR_WORKSPACE, "graph buffer or scratch not 256-byte aligned");
   char* b = static_cast<char*>(buf);
   g.rowptr = reinterpret_cast<int*>(b + L.rowptr);
   g.segptr = g.parts > 1 ? reinterpret_cast<int*>(b + L.segptr) : g.rowptr;
   g.col = reinterpret_cast<int*>(b + L.col);
   g.perm = reinterpret_cast<int*>(b + L.perm);
+  g.key = reinterpret_cast<int*>(b + L.key);
   g.heavy = reinterpret_cast<WorkItem*>(b + L.heavy);
   g.light = reinterpret_cast<WorkItem*>(b + L.light);
   g.split = reinterpret_cast<SplitRow*>(b + L.split);
@@ -267,8 +279,7 @@ int tfg_edge_reorder(const tfg_graph* from, const tfg_graph* to, const float* in
   if (H < 1 || E * H >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad H");
   if (E > 0 && (in == nullptr || out == nullptr)) return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (E > 0 && in == out) return fail(TFG_ERR_INVALID_ARG, "out overlaps in");
-  if (ws == nullptr || ws_bytes < tfg_edge_reorder_ws_bytes(from, to, H))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_edge_reorder_ws_bytes(from, to, H))) return wrc;
   if (int rc = check_device(from)) return rc;
   if (int rc = check_device(to)) return rc;
   return launch_edge_reorder(from ? from->g.perm : nullptr, to ? to->g.perm : nullptr, E, (int)H,
@@ -332,8 +343,7 @@ int tfg_gcn_norm(const void* edge_index, int index_type, int64_t E, const float*
   int rc = check_counts(E + (add_self_loops ? N : 0), N, N);
   if (rc) return rc;
   if (E > 0 && edge_index == nullptr) return fail(TFG_ERR_INVALID_ARG, "edge_index is NULL");
-  if (ws == nullptr || ws_bytes < tfg_gcn_norm_ws_bytes(E, N, add_self_loops, g))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_gcn_norm_ws_bytes(E, N, add_self_loops, g))) return wrc;
   if (out_edge_weight_csr && !g)
     return fail(TFG_ERR_INVALID_ARG, "CSR-order output needs a graph handle");
   hipStream_t s = as_stream(stream);
@@ -377,8 +387,7 @@ int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float
   if (weight_order == TFG_CSR && edge_weight && !g)
     return fail(TFG_ERR_INVALID_ARG, "CSR-order weights need a graph handle");
   if (H > 1 && !edge_weight) H = 1;
-  if (ws == nullptr || ws_bytes < aggregate_ws_needed(E, N, N_src, F, reduce, g))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, aggregate_ws_needed(E, N, N_src, F, reduce, g))) return wrc;
   hipStream_t s = as_stream(stream);
   Carver c(ws, ws_bytes);
   Graph tmp;
@@ -419,8 +428,7 @@ int tfg_gat_edge_scores(const void* edge_index, int index_type, int64_t E, const
       (N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr)))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (E > 0 && N == 0) return fail(TFG_ERR_INDEX_RANGE, "edges on a graph without nodes");
-  if (ws == nullptr || ws_bytes < tfg_gat_edge_scores_ws_bytes(N, H))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_gat_edge_scores_ws_bytes(N, H))) return wrc;
   float* proj = static_cast<float*>(ws);
   int* err = reinterpret_cast<int*>(static_cast<char*>(ws) +
                                     align_up(sizeof(float) * (size_t)std::max<int64_t>(2 * N * H, 1), 256));
@@ -447,8 +455,7 @@ int tfg_segment_softmax(const float* scores, int64_t E, int64_t H, const void* s
   if (E > 0 && (scores == nullptr || out == nullptr)) return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (E > 0 && seg == nullptr && g == nullptr) return fail(TFG_ERR_INVALID_ARG, "seg is NULL");
   if (out_csr && !g) return fail(TFG_ERR_INVALID_ARG, "CSR-order output needs a graph handle");
-  if (ws == nullptr || ws_bytes < tfg_segment_softmax_ws_bytes(E, H, N, g))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_softmax_ws_bytes(E, H, N, g))) return wrc;
   hipStream_t s = as_stream(stream);
   Carver c(ws, ws_bytes);
   const Graph* gp = nullptr;
@@ -521,10 +528,10 @@ int tfg_aggregate_backward(const tfg_graph* g, const tfg_graph* gt, const float*
   if (reduce == TFG_MAX && argmax == nullptr)
     return fail(TFG_ERR_INVALID_ARG, "the max gradient needs the forward argmax");
   const Graph* tg = gt ? &gt->g : nullptr;
-  if (ws == nullptr ||
-      ws_bytes < aggregate_backward_ws_bytes(fg, tg, F, H, reduce, weight_order,
-                                             edge_weight != nullptr))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes,
+                         aggregate_backward_ws_bytes(fg, tg, F, H, reduce, weight_order,
+                                                     edge_weight != nullptr)))
+    return wrc;
   if (int e = check_device(g)) return e;
   if (int e = check_device(gt)) return e;
   hipStream_t s = as_stream(stream);
@@ -547,8 +554,7 @@ int tfg_segment_softmax_backward(const float* alpha, const float* dalpha, int64_
   if (E > 0 && (alpha == nullptr || dalpha == nullptr || dscores == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (E > 0 && seg == nullptr && g == nullptr) return fail(TFG_ERR_INVALID_ARG, "seg is NULL");
-  if (ws == nullptr || ws_bytes < tfg_segment_softmax_backward_ws_bytes(E, H, N, g))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_softmax_backward_ws_bytes(E, H, N, g))) return wrc;
   hipStream_t s = as_stream(stream);
   Carver c(ws, ws_bytes);
   const Graph* gp = nullptr;
@@ -588,8 +594,7 @@ int tfg_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const v
   if ((Nb > 0 && (graph_index == nullptr || (F > 0 && x == nullptr))) ||
       (G > 0 && F > 0 && out == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < tfg_segment_pool_ws_bytes(Nb, G))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_pool_ws_bytes(Nb, G))) return wrc;
   hipStream_t s = as_stream(stream);
   int* goff = static_cast<int*>(ws);
   int* err = reinterpret_cast<int*>(static_cast<char*>(ws) + align_up(sizeof(int) * (size_t)(G + 1), 256));
@@ -620,8 +625,7 @@ int tfg_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void*
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (reduce == TFG_MAX && Nb > 0 && F > 0 && G > 0 && argmax == nullptr)
     return fail(TFG_ERR_INVALID_ARG, "the max gradient needs the forward argmax");
-  if (ws == nullptr || ws_bytes < tfg_segment_pool_ws_bytes(Nb, G))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_pool_ws_bytes(Nb, G))) return wrc;
   hipStream_t s = as_stream(stream);
   int* goff = static_cast<int*>(ws);
   int* err = reinterpret_cast<int*>(static_cast<char*>(ws) + align_up(sizeof(int) * (size_t)(G + 1), 256));
@@ -655,8 +659,7 @@ int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts
   if ((E > 0 && (local_edge_index == nullptr || out_edge_index == nullptr)) ||
       (Nb > 0 && out_graph_index == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < batch_ws_bytes(G))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, batch_ws_bytes(G))) return wrc;
   hipStream_t s = as_stream(stream);
   Carver c(ws, ws_bytes);
   int* node_off = static_cast<int*>(c.take(sizeof(int) * (size_t)(G + 1)));
@@ -704,8 +707,7 @@ int tfg_propagate(const tfg_graph* g, const float* edge_weight, int weight_order
     return fail(TFG_ERR_INVALID_ARG, "alpha > 0 needs h with ldh >= F");
   if (gr.N > 0 && F > 0 && (x == nullptr || out == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < tfg_propagate_ws_bytes(g, F, K))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_propagate_ws_bytes(g, F, K))) return wrc;
   if (int e = check_device(gr)) return e;
   hipStream_t s = as_stream(stream);
   if (gr.N == 0 || F == 0) return TFG_OK;
@@ -746,8 +748,7 @@ int tfg_gat_aggregate(const tfg_graph* g, const float* h, int64_t H, int64_t D,
     return fail(TFG_ERR_INVALID_ARG, "need 1 <= H <= 64 and D >= 1");
   if (gr.N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr || out == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr, H, D))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, gat_aggregate_ws_bytes(gr, H, D))) return wrc;
   if (int e = check_device(gr)) return e;
   return launch_gat_aggregate(gr, h, (int)H, (int)D, a_src, a_dst, slope, out, alpha_out, ws,
                               as_stream(stream));
@@ -768,8 +769,7 @@ int tfg_gat_dot_aggregate(const tfg_graph* g, const float* q, const float* key, 
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
   if (gr.E > 0 && (key == nullptr || v == nullptr))
     return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
-  if (ws == nullptr || ws_bytes < gat_aggregate_ws_bytes(gr, H, D))
-    return fail(TFG_ERR_WORKSPACE, "workspace too small");
+  if (int wrc = check_ws(ws, ws_bytes, gat_aggregate_ws_bytes(gr, H, D))) return wrc;
   if (int e = check_device(gr)) return e;
   return launch_gat_dot_aggregate(gr, q, key, v, (int)H, (int)D, scale, out, alpha_out, ws,
                                   as_stream(stream));

@@ -547,7 +547,7 @@ SortPlan sort_plan(int64_t E, int64_t N, int parts) {
 }
 
 struct ScratchLayout {
-  size_t keys, hist, csum, sums, bufA, bufB, row_items, seg_items, total;
+  size_t hist, csum, sums, bufA, bufB, row_items, seg_items, total;
 };
 
 ScratchLayout scratch_layout(int64_t E, int64_t N, int parts) {
@@ -561,7 +561,6 @@ ScratchLayout scratch_layout(int64_t E, int64_t N, int parts) {
   };
   const int64_t radix = int64_t(1) << p.dbits;
   const int64_t scan_n = std::max<int64_t>(N * parts + 1, N + 1);
-  L.keys = take(sizeof(int) * std::max<int64_t>(E, 1));
   L.hist = take(sizeof(int) * std::max<int64_t>(radix * p.ntiles, 1));
   L.csum = take(sizeof(int) * std::max<int64_t>(radix * p.nchunks, 1));
   L.sums = take(sizeof(int) * std::max<int64_t>(scan_tiles(scan_n), 1));
@@ -579,7 +578,7 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
   const int64_t E = g.E;
   const SortPlan p = sort_plan(E, g.N, g.parts);
   const KeyMap m{g.E_in, g.N_src, g.N, (int)g.part_rows, g.parts, 1.0f / (float)g.part_rows};
-  int* keys = reinterpret_cast<int*>(scratch + L.keys);
+  int* keys = g.key;  // the last pass leaves the sorted keys in the graph
   int* hist = reinterpret_cast<int*>(scratch + L.hist);
   int* csum = reinterpret_cast<int*>(scratch + L.csum);
   int* bufs[2][3];
@@ -715,6 +714,7 @@ GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk) {
   L.segptr = take(parts > 1 ? sizeof(int) * (N * parts + 1) : 0);
   L.col = take(sizeof(int) * std::max<int64_t>(E, 1));
   L.perm = take(sizeof(int) * std::max<int64_t>(E, 1));
+  L.key = take(sizeof(int) * std::max<int64_t>(E, 1));
   L.heavy = take(sizeof(WorkItem) * L.cap_heavy);
   L.light = take(sizeof(WorkItem) * std::max<int64_t>(L.cap_light, 1));
   L.split = take(sizeof(SplitRow) * std::max<int64_t>(L.cap_split, 1));

@@ -4,6 +4,8 @@
 //   w'[e]   = (dinv[src] * w[e]) * dinv[tgt]       (float32, left to right)
 // written in the caller's COO order and/or in the graph's CSR order; both
 // orders use the same operands in the same order, so they are bit-identical.
+#include <cstdlib>
+
 #include "wave.h"
 
 namespace tfg {
@@ -135,6 +137,232 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
   }
 }
 
+// dinv from LDS instead of L2. Gathering one float per endpoint from L2 moves
+// a whole cache line per lane, and that line traffic, not HBM, bounds the two
+// kernels above. Here a block keeps the node ids of its edges in registers and
+// walks dinv in slices that fit in LDS; each endpoint picks up its value in
+// the slice that holds it. Every block reads all of dinv once (4 N bytes from
+// L2 in full lines, copied straight into LDS) in exchange for one or two
+// random line reads per edge, so the tile per block is made as large as the
+// registers allow: one register per endpoint, holding the node id until the
+// endpoint's slice is seen and then its dinv value, marked by the sign bit
+// (dinv >= 0, ids >= 0). The products are the same ones, in the same order,
+// as in weights_coo / weights_csr, so the kernels agree bit for bit.
+constexpr int kSlThreads = 1024;                  // 16 waves, one block per CU
+constexpr int kSlice = 40960;                     // floats per LDS slice (160 KB)
+constexpr int kSlPiece = kWave * 4;               // floats per wave-wide 16-byte copy
+constexpr int kCooItems = 24;                     // edges per thread (2 registers each)
+constexpr int kCsrItems = 32;                     // positions per thread (1 register each)
+constexpr int kCooTile = kSlThreads * kCooItems;  // 24576 edges per block
+constexpr int kCsrTile = kSlThreads * kCsrItems;  // 32768 positions per block
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// Starts copying d[0, len) (16-byte aligned) into slice: whole 1 KB pieces as
+// direct memory-to-LDS loads (lane l of a wave moves bytes 16 l .. 16 l + 15
+// of a piece), the remainder through registers. The caller waits for the
+// copies (wait_slice) before the barrier that publishes the slice.
+__device__ __forceinline__ void fill_slice(float* slice, const float* __restrict__ d, int len) {
+  const int lane = lane_id();
+  const int wave = uniform((int)threadIdx.x / kWave);
+  const int pieces = len / kSlPiece;
+  for (int c = wave; c < pieces; c += kSlThreads / kWave)
+    __builtin_amdgcn_global_load_lds(d + c * kSlPiece + lane * 4, (lds_ptr)(slice + c * kSlPiece),
+                                     16, 0, 0);
+  for (int i = pieces * kSlPiece + (int)threadIdx.x; i < len; i += kSlThreads) slice[i] = d[i];
+}
+
+// All of this wave's memory operations done (the LDS copies included).
+__device__ __forceinline__ void wait_slice() { __builtin_amdgcn_s_waitcnt(0); }
+
+// An endpoint register: a node id (>= 0, or -1 for no edge) until resolved,
+// then the dinv value with the sign bit set. A resolved value never matches a
+// later slice: as unsigned, (value - lo) >= 2^31 - lo > 2^30 (N <= 2^30).
+__device__ __forceinline__ int resolved(float v) { return __float_as_int(v) | INT_MIN; }
+__device__ __forceinline__ float value_of(int r) { return __int_as_float(r & INT_MAX); }
+
+// Resolves the endpoints of one slice [lo, lo + len): reads in groups of 8,
+// issued together, then used.
+template <int ITEMS>
+__device__ __forceinline__ void resolve(int (&r)[ITEMS], const float* slice, int lo, int len) {
+#pragma unroll
+  for (int j0 = 0; j0 < ITEMS; j0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8 && j0 + j < ITEMS; ++j) {
+      const unsigned u = (unsigned)(r[j0 + j] - lo);
+      v[j] = u < (unsigned)len ? slice[u] : -1.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8 && j0 + j < ITEMS; ++j)
+      r[j0 + j] = v[j] >= 0.0f ? resolved(v[j]) : r[j0 + j];
+  }
+}
+
+// Walks dinv[0, N) slice by slice, resolving every register of the block.
+// The first slice was started (fill_slice) by the caller.
+template <int ITEMS>
+__device__ __forceinline__ void walk_slices(int (&r)[ITEMS], float* slice,
+                                            const float* __restrict__ dinv, int64_t N) {
+  for (int64_t lo = 0; lo < N; lo += kSlice) {
+    const int len = (int)min<int64_t>(kSlice, N - lo);
+    if (lo > 0) {
+      __syncthreads();  // the previous slice is no longer read
+      fill_slice(slice, dinv + lo, len);
+    }
+    wait_slice();
+    __syncthreads();
+    resolve(r, slice, (int)lo, len);
+  }
+}
+
+// (Block-relative pointers with 32-bit offsets keep one address register per
+// thread for all items.)
+template <typename IdxT>
+__global__ __launch_bounds__(kSlThreads, 4) void weights_coo_sliced(
+    const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, int64_t E_in, int64_t E, int64_t N,
+    const float* __restrict__ w, const float* __restrict__ dinv, int32_t* __restrict__ out_ei,
+    float* __restrict__ out_w) {
+  __shared__ float slice[kSlice];
+  fill_slice(slice, dinv, (int)min<int64_t>(kSlice, N));  // overlaps the edge loads
+  const int64_t b0 = (int64_t)blockIdx.x * kCooTile;
+  const int n_in = (int)max<int64_t>(0, min<int64_t>(kCooTile, E_in - b0));  // input edges here
+  const int n_all = (int)min<int64_t>(kCooTile, E - b0);                     // with the loops
+  int st[2 * kCooItems];  // [0, ITEMS): sources, [ITEMS, 2 ITEMS): targets
+  {
+    // every load issued before the first use
+    const IdxT* sb = src + b0;
+    const IdxT* tb = tgt + b0;
+    // 32-bit ids: all loads straight into the registers, then the checks;
+    // 64-bit ids: groups of 8 edges (two registers per raw id)
+    constexpr int G = sizeof(IdxT) == 4 ? kCooItems : 8;
+#pragma unroll
+    for (int j0 = 0; j0 < kCooItems; j0 += G) {
+      IdxT rs[G], rt[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
+        rs[j] = p < n_in ? __builtin_nontemporal_load(sb + p) : IdxT(0);
+        rt[j] = p < n_in ? __builtin_nontemporal_load(tb + p) : IdxT(0);
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        // ids were validated when the graph was built; clamped here all the
+        // same. Loops (i, i) follow the input edges; positions past E get the
+        // id -1, which no slice holds.
+        const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
+        const int64_t s0 = (int64_t)rs[j], t0 = (int64_t)rt[j];
+        const int loop = p < n_all ? (int)(b0 + p - E_in) : -1;
+        const bool in = p < n_in;
+        st[j0 + j] = in ? ((s0 < 0 || s0 >= N) ? 0 : (int)s0) : loop;
+        st[kCooItems + j0 + j] = in ? ((t0 < 0 || t0 >= N) ? 0 : (int)t0) : loop;
+      }
+    }
+  }
+  if (out_ei) {
+    int32_t* os = out_ei + b0;
+    int32_t* ot = out_ei + E + b0;
+#pragma unroll
+    for (int j = 0; j < kCooItems; ++j) {
+      const int p = j * kSlThreads + (int)threadIdx.x;
+      if (p < n_all) {
+        __builtin_nontemporal_store(st[j], os + p);
+        __builtin_nontemporal_store(st[kCooItems + j], ot + p);
+      }
+    }
+  }
+  walk_slices(st, slice, dinv, N);
+  // all loads (the weights) before the first store: a wait for a load also
+  // waits for the stores issued before it
+  float* ow = out_w + b0;
+  float o[kCooItems];
+  if (w != nullptr) {
+    const float* wb = w + b0;
+#pragma unroll
+    for (int j = 0; j < kCooItems; ++j)  // loops weigh 1
+      o[j] = j * kSlThreads + (int)threadIdx.x < n_in ? wb[j * kSlThreads + threadIdx.x] : 1.0f;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kCooItems; ++j) o[j] = 1.0f;
+  }
+#pragma unroll
+  for (int j = 0; j < kCooItems; ++j)
+    o[j] = (value_of(st[j]) * o[j]) * value_of(st[kCooItems + j]);  // (dinv[s] * w) * dinv[t]
+#pragma unroll
+  for (int j = 0; j < kCooItems; ++j) {
+    const int p = j * kSlThreads + (int)threadIdx.x;
+    if (p < n_all) __builtin_nontemporal_store(o[j], ow + p);
+  }
+}
+
+// CSR order: blocks take kCsrTile consecutive positions and only the source
+// side goes through the slices; the target of a position comes from its sort
+// key (target * parts + part) at the end, and neighbouring positions share it,
+// so dinv[target] is read directly, as are the weights.
+template <bool HAS_W>
+__global__ __launch_bounds__(kSlThreads, 4) void weights_csr_sliced(
+    const int* __restrict__ key, int parts, const int* __restrict__ col,
+    const int* __restrict__ perm, const float* __restrict__ w, int64_t E_in, int64_t E, int64_t N,
+    const float* __restrict__ dinv, float* __restrict__ out) {
+  __shared__ float slice[kSlice];
+  fill_slice(slice, dinv, (int)min<int64_t>(kSlice, N));
+  const int64_t b0 = (int64_t)blockIdx.x * kCsrTile;
+  const int n = (int)min<int64_t>(kCsrTile, E - b0);
+  int c[kCsrItems];
+  {
+    const int* cb = col + b0;
+#pragma unroll
+    for (int j = 0; j < kCsrItems; ++j) {
+      const int p = j * kSlThreads + (int)threadIdx.x;
+      c[j] = p < n ? cb[p] : -1;  // -1: no slice holds it
+    }
+  }
+  walk_slices(c, slice, dinv, N);
+  // keys (and edge ids), then the targets' dinv (and the weights), then the
+  // products: all loads before the first store, since a wait for a load also
+  // waits for the stores issued before it
+  const int* kb = key + b0;
+  float* ob = out + b0;
+  int kv[kCsrItems];
+#pragma unroll
+  for (int j = 0; j < kCsrItems; ++j)
+    kv[j] = j * kSlThreads + (int)threadIdx.x < n ? kb[j * kSlThreads + threadIdx.x] : 0;
+  float o[kCsrItems];
+#pragma unroll
+  for (int j = 0; j < kCsrItems; ++j) o[j] = 1.0f;
+  if constexpr (HAS_W) {  // edge ids, then weights, in groups (loops weigh 1)
+    const int* pb = perm + b0;
+#pragma unroll
+    for (int j0 = 0; j0 < kCsrItems; j0 += 8) {
+      int pe[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
+        pe[j] = p < n ? pb[p] : (int)E_in;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j0 + j] = pe[j] < E_in ? w[pe[j]] : 1.0f;
+    }
+  }
+  float dt[kCsrItems];
+#pragma unroll
+  for (int j = 0; j < kCsrItems; ++j) dt[j] = dinv[parts == 1 ? kv[j] : kv[j] / parts];
+#pragma unroll
+  for (int j = 0; j < kCsrItems; ++j) {
+    const int p = j * kSlThreads + (int)threadIdx.x;
+    if (p < n) ob[p] = (value_of(c[j]) * o[j]) * dt[j];  // (dinv[col] * w) * dinv[row]
+  }
+}
+
+// The sliced kernels pay 4 N bytes of L2 reads per block against one or two
+// gathered lines per edge; they are chosen while that fill stays below one
+// line per edge and the grid still covers the chip.
+bool use_sliced(int64_t E, int64_t N) {
+  if (N > (int64_t(1) << 30)) return false;  // see resolved()
+  if (const char* v = std::getenv("TFG_NORM_SLICED")) return v[0] == '1';
+  return N * 4 <= (int64_t)kCooTile * 128 && E >= (int64_t)256 * kCooTile;
+}
+
 }  // namespace
 
 int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
@@ -150,13 +378,38 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
   }
   TFG_LAUNCHED("gcn degree");
   const int waves = g.n_heavy + g.n_light;
-  if (out_w_csr && waves > 0) {
+  if (out_w_csr && g.E > 0 && use_sliced(g.E, g.N)) {
+    const unsigned nbs = (unsigned)((g.E + kCsrTile - 1) / kCsrTile);
+    if (edge_weight)
+      weights_csr_sliced<true><<<nbs, kSlThreads, 0, s>>>(g.key, g.parts, g.col, g.perm,
+                                                          edge_weight, g.E_in, g.E, g.N, dinv,
+                                                          out_w_csr);
+    else
+      weights_csr_sliced<false><<<nbs, kSlThreads, 0, s>>>(g.key, g.parts, g.col, g.perm,
+                                                           nullptr, g.E_in, g.E, g.N, dinv,
+                                                           out_w_csr);
+    TFG_LAUNCHED("gcn weights (CSR order, sliced)");
+  } else if (out_w_csr && waves > 0) {
     weights_csr<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
         g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, edge_weight, g.E_in, dinv,
         out_w_csr);
     TFG_LAUNCHED("gcn weights (CSR order)");
   }
   if ((out_w || out_edge_index) && g.E > 0) {
+    if (out_w && use_sliced(g.E, g.N)) {
+      const unsigned nbs = (unsigned)((g.E + kCooTile - 1) / kCooTile);
+      if (index_type == TFG_I64) {
+        const int64_t* ei = static_cast<const int64_t*>(edge_index);
+        weights_coo_sliced<int64_t><<<nbs, kSlThreads, 0, s>>>(
+            ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+      } else {
+        const int32_t* ei = static_cast<const int32_t*>(edge_index);
+        weights_coo_sliced<int32_t><<<nbs, kSlThreads, 0, s>>>(
+            ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+      }
+      TFG_LAUNCHED("gcn weights (COO order, sliced)");
+      return TFG_OK;
+    }
     const unsigned nb = (unsigned)((g.E + 4 * kBlock - 1) / (4 * kBlock));
     if (index_type == TFG_I64) {
       const int64_t* ei = static_cast<const int64_t*>(edge_index);

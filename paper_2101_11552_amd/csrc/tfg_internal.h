@@ -57,6 +57,7 @@ struct Graph {
   int* segptr = nullptr;    // [N*P+1]: start of (row, part); == rowptr when P == 1
   int* col = nullptr;       // [E] source id per position
   int* perm = nullptr;      // [E] input edge id per position
+  int* key = nullptr;       // [E] sort key per position: target * parts + source part
   // row plan: one item per row (long rows cut into chunks + fix-up)
   WorkItem* heavy = nullptr;  // chunks of split rows; heavy[i] writes partial i
   WorkItem* light = nullptr;  // whole rows
@@ -80,7 +81,7 @@ struct Graph {
 
 // Sizes of the persistent part of a graph.
 struct GraphLayout {
-  size_t rowptr, segptr, col, perm, heavy, light, split, pexec, prows, short_rows, long_rows,
+  size_t rowptr, segptr, col, perm, key, heavy, light, split, pexec, prows, short_rows, long_rows,
       counters, total;
   int64_t cap_heavy, cap_light, cap_split, cap_pexec;
 };

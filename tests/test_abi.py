@@ -78,19 +78,24 @@ def test_host_side_argument_errors(lib):
     assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, 0, fake, 16, fake, 1 << 20, None,
                                 ctypes.byref(h)) == 5
     assert b"too small" in lib.tfg_last_error()
+    assert lib.tfg_graph_create(fake, 0, 10, 5, 5, 0, 0, ctypes.c_void_p(0x1080), 1 << 20, fake,
+                                1 << 20, None, ctypes.byref(h)) == 5
+    assert b"aligned" in lib.tfg_last_error()
     # aggregate: bad reduce, F not a multiple of H, ldx < F, workspace too small
     args = dict(E=10, w=None, H=1, order=0, x=fake, N_src=5, F=8, ldx=8, N=5, red=0)
 
     def agg(**kw):
         a = {**args, **kw}
         return lib.tfg_aggregate(fake, 0, a["E"], a["w"], a["H"], a["order"], a["x"], a["N_src"],
-                                 a["F"], a["ldx"], a["N"], a["red"], None, fake, None, fake,
-                                 kw.get("ws", 1 << 30), None)
+                                 a["F"], a["ldx"], a["N"], a["red"], None, fake, None,
+                                 kw.get("wsp", fake), kw.get("ws", 1 << 30), None)
     assert agg(red=3) == 1
     assert agg(w=fake, H=3) == 1
     assert agg(ldx=4) == 1
     assert agg(order=1, w=fake) == 1  # CSR-order weights need a graph
     assert agg(ws=8) == 5
+    assert agg(wsp=ctypes.c_void_p(0x1004)) == 5  # workspace not 256-byte aligned
+    assert b"aligned" in lib.tfg_last_error()
     assert agg(E=-1) == 1
     assert agg(N=2**31) == 4
     # pooling: bad reduce, ldx < F

@@ -134,6 +134,37 @@ def test_gcn_norm_bit_exact(tfg, orc, weighted, idx, parts):
     assert same_bits(host(r2["edge_weight"]), ow)
 
 
+NORM_SLICE_CASES = [
+    # n, e, weighted, idx, parts, loops
+    (4000, 60_000, False, np.int32, 1, True),    # one LDS slice
+    (4000, 60_000, True, np.int64, 6, True),     # key / parts for the row
+    (100_003, 300_000, False, np.int32, 1, True),  # three slices, N % 4 == 3 (tail)
+    (100_003, 300_000, True, np.int32, 5, False),  # no loops: E' == E
+    (90_001, 50_000, False, np.int64, 1, True),  # int64 ids, more nodes than edges
+]
+
+
+@pytest.mark.parametrize("n,e,weighted,idx,parts,loops", NORM_SLICE_CASES)
+def test_gcn_norm_sliced_and_direct(tfg, orc, monkeypatch, n, e, weighted, idx, parts, loops):
+    # the LDS-sliced and the direct-gather weight kernels, each forced, both
+    # equal to the oracle bit for bit (COO and CSR order)
+    ei = graphgen.random_graph(23, n, e, hub=11, hub_edges=e // 10)
+    w = (np.random.default_rng(5).uniform(0.1, 3.0, ei.shape[1]).astype(np.float32)
+         if weighted else None)
+    oei, ow, odeg = orc.gcn_norm(ei, n, edge_weight=w, add_self_loops=loops)
+    perm = orc.csr_by_target(oei, n, parts=parts)[2]
+    eid = dev(ei.astype(idx))
+    g = tfg.tfg_graph_create(eid, n, add_self_loops=loops, src_parts=parts)
+    for mode in ("1", "0"):
+        monkeypatch.setenv("TFG_NORM_SLICED", mode)
+        r = tfg.tfg_gcn_norm(eid, n, edge_weight=None if w is None else dev(w),
+                             add_self_loops=loops, graph=g)
+        assert np.array_equal(host(r["edge_index"]), oei), mode
+        assert same_bits(host(r["deg"]), odeg), mode
+        assert same_bits(host(r["edge_weight"]), ow), mode
+        assert same_bits(host(r["edge_weight_csr"]), ow[perm]), mode
+
+
 # ---------------------------------------------------------------------------
 # Aggregation
 # ---------------------------------------------------------------------------
