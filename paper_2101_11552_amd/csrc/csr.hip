@@ -31,7 +31,6 @@ constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 edges per tile
 constexpr int kSortWaves = kSortThreads / kWave;
 constexpr int kMaxDigitBits = 9;
 constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 512
-constexpr int kHistChunk = 256;                       // tiles per offset chunk
 constexpr int kXcds = 8;
 
 // Blocks are dispatched round-robin over the XCDs; tile_of() gives each XCD a
@@ -152,8 +151,10 @@ int64_t scan_tiles(int64_t n) { return (n + kScanTile - 1) / kScanTile; }
 // Radix sort passes.
 // ---------------------------------------------------------------------------
 
-// Digit counts of one tile, written as row `tile` of the block-major table
-// hist[tile * radix + d]. The first pass also validates the ids.
+// Digit counts of one tile, written as column `tile` of the digit-major table
+// hist[d * ntiles + tile]; an exclusive scan of the whole table then gives
+// every (digit, tile) its output offset. The first pass also validates the
+// ids.
 template <bool FIRST, typename IdxT>
 __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__ src,
                                                         const IdxT* __restrict__ tgt, KeyMap m,
@@ -193,60 +194,7 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
   if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
   for (int d = threadIdx.x; d < radix; d += kSortThreads)
-    hist[(int64_t)blockIdx.x * radix + d] = h[d];
-}
-
-// Offsets from the digit counts: offset(t, d) = sum over digits d' < d of all
-// counts + sum over tiles t' < t of the counts of d. Tiles are grouped in
-// chunks of kHistChunk: per-chunk column sums, a scan over chunks and digits,
-// then a per-chunk running sum written in place.
-__global__ __launch_bounds__(kMaxRadix) void hist_chunk_sums(const int* __restrict__ hist,
-                                                             int64_t ntiles, int radix,
-                                                             int* __restrict__ csum) {
-  const int d = threadIdx.x;
-  if (d >= radix) return;
-  const int64_t t0 = (int64_t)blockIdx.x * kHistChunk;
-  const int64_t t1 = t0 + kHistChunk < ntiles ? t0 + kHistChunk : ntiles;
-  int s = 0;
-#pragma unroll 8
-  for (int64_t t = t0; t < t1; ++t) s += hist[t * radix + d];
-  csum[(int64_t)blockIdx.x * radix + d] = s;
-}
-
-__global__ __launch_bounds__(kMaxRadix) void hist_chunk_scan(int* __restrict__ csum,
-                                                             int64_t nchunks, int radix) {
-  __shared__ int tmp[kMaxRadix / kWave];
-  const int d = threadIdx.x;
-  int run = 0;
-  if (d < radix)
-    for (int64_t c = 0; c < nchunks; ++c) {
-      const int v = csum[c * radix + d];
-      csum[c * radix + d] = run;
-      run += v;
-    }
-  const int base = block_excl_scan<kMaxRadix / kWave>(d < radix ? run : 0, tmp, nullptr);
-  if (d < radix)
-    for (int64_t c = 0; c < nchunks; ++c) csum[c * radix + d] += base;
-}
-
-__global__ __launch_bounds__(kMaxRadix) void hist_apply(int* __restrict__ hist, int64_t ntiles,
-                                                        int radix, const int* __restrict__ csum) {
-  const int d = threadIdx.x;
-  if (d >= radix) return;
-  const int64_t t0 = (int64_t)blockIdx.x * kHistChunk;
-  const int64_t t1 = t0 + kHistChunk < ntiles ? t0 + kHistChunk : ntiles;
-  int run = csum[(int64_t)blockIdx.x * radix + d];
-  for (int64_t t = t0; t < t1; t += 8) {
-    int v[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = t + j < t1 ? hist[(t + j) * radix + d] : 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (t + j < t1) {
-        hist[(t + j) * radix + d] = run;
-        run += v[j];
-      }
-  }
+    hist[(int64_t)d * gridDim.x + blockIdx.x] = h[d];
 }
 
 // Stable scatter of one tile by one digit. Wave w owns tile positions
@@ -282,10 +230,11 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
   __syncthreads();
 
-  // Only the keys and ranks stay in registers; edge ids and source ids are
-  // fetched again (from L2) when they are staged, which keeps the kernel at
-  // 64 VGPRs (two 16-wave blocks per CU).
-  int key[kSortItems], lpos[kSortItems];
+  // Later passes load keys and payloads together up front (one round of
+  // memory latency per tile). The first pass keeps only the keys: its edge
+  // id is the position, and its source id is decoded again from edge_index
+  // (an L2 hit) when staged, which keeps that kernel within 64 VGPRs.
+  int key[kSortItems], lpos[kSortItems], pe[FIRST ? 1 : kSortItems], ps[FIRST ? 1 : kSortItems];
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
@@ -293,11 +242,13 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
     if constexpr (FIRST) {
       IdxT s0, t0;
       load_raw(src, tgt, m.E_in, e, &s0, &t0);
-      int s;
+      int sv;
       bool bad;
-      decode_edge(m, e, s0, t0, src != nullptr, &s, &key[i], &bad);
+      decode_edge(m, e, s0, t0, src != nullptr, &sv, &key[i], &bad);
     } else {
       key[i] = kin[e];
+      pe[i] = ein[e];
+      ps[i] = sin[e];
     }
   }
 #pragma unroll
@@ -334,7 +285,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
     const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
     if (d < radix) {
       loff[d] = ex;
-      goff[d] = hist[(int64_t)tile * radix + d];
+      goff[d] = hist[(int64_t)d * ntiles + tile];
     }
   }
   __syncthreads();
@@ -372,8 +323,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
     if (lpos[i] >= 0) {
-      const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
-      stage[lpos[i]] = FIRST ? (int)e : ein[e];
+      if constexpr (FIRST)
+        stage[lpos[i]] = (int)(base + wave * (kWave * kSortItems) + i * kWave + lane);
+      else
+        stage[lpos[i]] = pe[i];
     }
   __syncthreads();
 #pragma unroll
@@ -384,17 +337,15 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
     if (lpos[i] >= 0) {
-      const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
-      int s;
       if constexpr (FIRST) {
+        const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
         const int64_t ec = e < m.E_in ? e : (m.E_in > 0 ? m.E_in - 1 : 0);
         const IdxT s0 = (src && m.E_in > 0) ? src[ec] : IdxT(0);
         bool bad;
-        s = decode_source(m, e, s0, src != nullptr, &bad);
+        stage[lpos[i]] = decode_source(m, e, s0, src != nullptr, &bad);
       } else {
-        s = sin[e];
+        stage[lpos[i]] = ps[i];
       }
-      stage[lpos[i]] = s;
     }
   __syncthreads();
 #pragma unroll
@@ -404,19 +355,32 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 
 // bounds[v] = first position whose sorted key is >= v (v = 0..K). Position k
 // starts the keys (key[k-1], key[k]]; k = E closes the keys after the last one.
-// Four positions per thread.
+// Four positions per thread, read with one 16-byte load; the key before them
+// comes from the neighbouring lane.
 __global__ __launch_bounds__(kBlock) void key_bounds(const int* __restrict__ keys, int64_t E,
                                                      int64_t K, int* __restrict__ bounds) {
   const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (k0 > E) return;
-  int64_t cur[5];
-  cur[0] = k0 > 0 ? keys[k0 - 1] : -1;
+  int c[4];
+  if (k0 + 4 <= E) {
+    const int4 v = *reinterpret_cast<const int4*>(keys + k0);
+    c[0] = v.x;
+    c[1] = v.y;
+    c[2] = v.z;
+    c[3] = v.w;
+  } else {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) cur[j + 1] = k0 + j < E ? keys[k0 + j] : K;
+    for (int j = 0; j < 4; ++j) c[j] = k0 + j < E ? keys[k0 + j] : (int)K;
+  }
+  // lane l - 1 holds keys[k0 - 1] whenever this lane has positions to close
+  int prev = __shfl_up(c[3], 1);
+  if (lane_id() == 0) prev = (k0 > 0 && k0 <= E) ? keys[k0 - 1] : -1;
+  if (k0 > E) return;
+  int64_t cur = prev;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     if (k0 + j > E) break;
-    for (int64_t v = cur[j] + 1; v <= cur[j + 1]; ++v) bounds[v] = (int)(k0 + j);
+    for (int64_t v = cur + 1; v <= c[j]; ++v) bounds[v] = (int)(k0 + j);
+    cur = c[j];
   }
 }
 
@@ -431,56 +395,93 @@ __global__ __launch_bounds__(kBlock) void rows_from_segments(const int* __restri
 // Aggregation work lists.
 // ---------------------------------------------------------------------------
 
-// Reserves v entries of *ctr for this lane with one atomic per wave; returns
-// the lane's first entry.
-__device__ __forceinline__ int wave_reserve(int* ctr, int v) {
-  const int incl = wave_incl_scan(v);
-  const int total = __shfl(incl, kWave - 1);
-  int base = 0;
-  if (lane_id() == kWave - 1 && total > 0) base = atomicAdd(ctr, total);
-  base = __shfl(base, kWave - 1);
-  return base + incl - v;
-}
-
 // Row plan: rows with at most `chunk` edges become one light item; longer
 // rows are cut into ceil(deg / chunk) heavy items whose partial results the
-// fix-up pass combines. Item order within each list is arbitrary (it only
-// affects scheduling, never values).
-__global__ __launch_bounds__(kBlock) void build_worklist(const int* __restrict__ rowptr, int64_t N,
-                                                         int chunk, int* __restrict__ counters,
-                                                         WorkItem* __restrict__ heavy,
-                                                         WorkItem* __restrict__ light,
-                                                         SplitRow* __restrict__ split,
-                                                         int* __restrict__ short_rows,
-                                                         WorkItem* __restrict__ long_rows) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int beg = 0, deg = 0;
+// fix-up pass combines. The light rows are listed again by length (short:
+// at most kShortRow edges; long: the others). Every list is in row order:
+// per-block counts, one scan of them, then a fill pass (no atomics).
+constexpr int kWlThreads = 1024;  // rows per block of the work-list kernels
+constexpr int kLists = 5;         // heavy chunks, light, split, short, long
+__constant__ const int kListCounter[kLists] = {0, 1, 2, 5, 6};  // their slots in counters
+
+__device__ __forceinline__ void row_entries(const int* __restrict__ rowptr, int64_t N, int chunk,
+                                            int64_t r, int* beg, int* deg, int (&c)[kLists]) {
+  *beg = 0;
+  *deg = 0;
   if (r < N) {
-    beg = rowptr[r];
-    deg = rowptr[r + 1] - beg;
+    *beg = rowptr[r];
+    *deg = rowptr[r + 1] - *beg;
   }
   const bool valid = r < N;
-  const bool is_split = valid && deg > chunk;
-  const int nch = is_split ? (deg + chunk - 1) / chunk : 0;
-  const int h0 = wave_reserve(&counters[0], nch);
-  const int l0 = wave_reserve(&counters[1], valid && !is_split ? 1 : 0);
-  const int s0 = wave_reserve(&counters[2], is_split ? 1 : 0);
-  const bool is_short = valid && deg <= kShortRow;
-  const int q0 = wave_reserve(&counters[5], is_short ? 1 : 0);
-  const int m0 = wave_reserve(&counters[6], valid && !is_split && !is_short ? 1 : 0);
-  if (!valid) return;
-  if (is_short)
-    short_rows[q0] = (int)r;
-  else if (!is_split)
-    long_rows[m0] = WorkItem{(int)r, beg, beg + deg, -1};
-  if (is_split) {
-    for (int j = 0; j < nch; ++j) {
+  const bool split = valid && *deg > chunk;
+  const bool shrt = valid && *deg <= kShortRow;
+  c[0] = split ? (*deg + chunk - 1) / chunk : 0;
+  c[1] = valid && !split;
+  c[2] = split;
+  c[3] = shrt;
+  c[4] = valid && !split && !shrt;
+}
+
+// Entries per list of each block of rows: block_sums[list * nb + block].
+__global__ __launch_bounds__(kWlThreads) void worklist_count(const int* __restrict__ rowptr,
+                                                             int64_t N, int chunk,
+                                                             int* __restrict__ block_sums, int nb) {
+  __shared__ int tmp[kWlThreads / kWave];
+  int beg, deg, c[kLists];
+  row_entries(rowptr, N, chunk, (int64_t)blockIdx.x * kWlThreads + threadIdx.x, &beg, &deg, c);
+#pragma unroll
+  for (int i = 0; i < kLists; ++i) {
+    int tot;
+    block_excl_scan<kWlThreads / kWave>(c[i], tmp, &tot);
+    if (threadIdx.x == 0) block_sums[i * nb + blockIdx.x] = tot;
+  }
+}
+
+// One block: exclusive scan of each list's block sums in place; the list
+// lengths go to the counters.
+__global__ __launch_bounds__(1024) void worklist_offsets(int* __restrict__ block_sums, int nb,
+                                                         int* __restrict__ counters) {
+  __shared__ int tmp[1024 / kWave];
+  for (int i = 0; i < kLists; ++i) {
+    int* b = block_sums + (int64_t)i * nb;
+    int carry = 0;
+    for (int base = 0; base < nb; base += 1024) {
+      const int k = base + (int)threadIdx.x;
+      const int v = k < nb ? b[k] : 0;
+      int total;
+      const int ex = block_excl_scan<1024 / kWave>(v, tmp, &total);
+      if (k < nb) b[k] = carry + ex;
+      carry += total;
+    }
+    if (threadIdx.x == 0) counters[kListCounter[i]] = carry;
+  }
+}
+
+__global__ __launch_bounds__(kWlThreads) void worklist_fill(
+    const int* __restrict__ rowptr, int64_t N, int chunk, const int* __restrict__ block_sums,
+    int nb, WorkItem* __restrict__ heavy, WorkItem* __restrict__ light,
+    SplitRow* __restrict__ split, int* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
+  __shared__ int tmp[kWlThreads / kWave];
+  const int64_t r = (int64_t)blockIdx.x * kWlThreads + threadIdx.x;
+  int beg, deg, c[kLists], o[kLists];
+  row_entries(rowptr, N, chunk, r, &beg, &deg, c);
+#pragma unroll
+  for (int i = 0; i < kLists; ++i)
+    o[i] = block_sums[i * nb + blockIdx.x] + block_excl_scan<kWlThreads / kWave>(c[i], tmp, nullptr);
+  if (r >= N) return;
+  if (c[3])
+    short_rows[o[3]] = (int)r;
+  else if (c[4])
+    long_rows[o[4]] = WorkItem{(int)r, beg, beg + deg, -1};
+  if (c[2]) {
+    const int h0 = o[0];
+    for (int j = 0; j < c[0]; ++j) {
       const int kb = beg + j * chunk;
       heavy[h0 + j] = WorkItem{(int)r, kb, min(kb + chunk, beg + deg), h0 + j};
     }
-    split[s0] = SplitRow{(int)r, h0, nch, deg};
+    split[o[2]] = SplitRow{(int)r, h0, c[0], deg};
   } else {
-    light[l0] = WorkItem{(int)r, beg, beg + deg, -1};
+    light[o[1]] = WorkItem{(int)r, beg, beg + deg, -1};
   }
 }
 
@@ -532,7 +533,7 @@ int ceil_log2(int64_t n) {
 
 struct SortPlan {
   int bits, passes, dbits;
-  int64_t ntiles, nchunks, keyspace;
+  int64_t ntiles, keyspace;
 };
 
 SortPlan sort_plan(int64_t E, int64_t N, int parts) {
@@ -542,12 +543,11 @@ SortPlan sort_plan(int64_t E, int64_t N, int parts) {
   p.passes = (p.bits + kMaxDigitBits - 1) / kMaxDigitBits;
   p.dbits = (p.bits + p.passes - 1) / p.passes;
   p.ntiles = (E + kSortTile - 1) / kSortTile;
-  p.nchunks = (p.ntiles + kHistChunk - 1) / kHistChunk;
   return p;
 }
 
 struct ScratchLayout {
-  size_t hist, csum, sums, bufA, bufB, row_items, seg_items, total;
+  size_t hist, sums, bufA, bufB, wl_sums, row_items, seg_items, total;
 };
 
 ScratchLayout scratch_layout(int64_t E, int64_t N, int parts) {
@@ -560,12 +560,12 @@ ScratchLayout scratch_layout(int64_t E, int64_t N, int parts) {
     return o;
   };
   const int64_t radix = int64_t(1) << p.dbits;
-  const int64_t scan_n = std::max<int64_t>(N * parts + 1, N + 1);
+  const int64_t scan_n = std::max<int64_t>({N * parts + 1, N + 1, radix * p.ntiles});
   L.hist = take(sizeof(int) * std::max<int64_t>(radix * p.ntiles, 1));
-  L.csum = take(sizeof(int) * std::max<int64_t>(radix * p.nchunks, 1));
   L.sums = take(sizeof(int) * std::max<int64_t>(scan_tiles(scan_n), 1));
   L.bufA = take(sizeof(int) * 3 * std::max<int64_t>(E, 1));
   L.bufB = take(p.passes >= 3 ? sizeof(int) * 3 * std::max<int64_t>(E, 1) : 0);
+  L.wl_sums = take(sizeof(int) * kLists * std::max<int64_t>((N + kWlThreads - 1) / kWlThreads, 1));
   L.row_items = take(parts > 1 ? sizeof(int) * (N + 1) : 0);
   L.seg_items = take(parts > 1 ? sizeof(int) * (N * parts + 1) : 0);
   L.total = off;
@@ -580,7 +580,7 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
   const KeyMap m{g.E_in, g.N_src, g.N, (int)g.part_rows, g.parts, 1.0f / (float)g.part_rows};
   int* keys = g.key;  // the last pass leaves the sorted keys in the graph
   int* hist = reinterpret_cast<int*>(scratch + L.hist);
-  int* csum = reinterpret_cast<int*>(scratch + L.csum);
+  int* sums = reinterpret_cast<int*>(scratch + L.sums);
   int* bufs[2][3];
   for (int b = 0; b < 2; ++b) {
     int* base = reinterpret_cast<int*>(scratch + (b == 0 ? L.bufA : L.bufB));
@@ -601,9 +601,8 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
       else
         upsweep<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, shift,
                                                          p.dbits, hist, err);
-      hist_chunk_sums<<<(unsigned)p.nchunks, kMaxRadix, 0, s>>>(hist, p.ntiles, radix, csum);
-      hist_chunk_scan<<<1, kMaxRadix, 0, s>>>(csum, p.nchunks, radix);
-      hist_apply<<<(unsigned)p.nchunks, kMaxRadix, 0, s>>>(hist, p.ntiles, radix, csum);
+      const int rc = exclusive_scan(hist, hist, radix * p.ntiles, sums, s);
+      if (rc) return rc;
       TFG_LAUNCHED("radix offsets");
       const int nxt = first ? 0 : 1 - cur;
       int* ko = last ? keys : bufs[nxt][0];
@@ -746,10 +745,13 @@ int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void
                              sc, L, s);
   if (rc) return rc;
   if (g.N > 0) {
-    build_worklist<<<dim3((unsigned)((g.N + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(
-        g.rowptr, g.N, g.chunk, g.counters, g.heavy, g.light, g.split, g.short_rows,
-        g.long_rows);
-    TFG_LAUNCHED("build_worklist");
+    const int nb = (int)((g.N + kWlThreads - 1) / kWlThreads);
+    int* wl = reinterpret_cast<int*>(sc + L.wl_sums);
+    worklist_count<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb);
+    worklist_offsets<<<1, 1024, 0, s>>>(wl, nb, g.counters);
+    worklist_fill<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb, g.heavy, g.light,
+                                            g.split, g.short_rows, g.long_rows);
+    TFG_LAUNCHED("work lists");
     if (g.parts > 1) {
       rc = build_part_plan(g, sc, L, s);
       if (rc) return rc;
