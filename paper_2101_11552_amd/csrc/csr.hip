@@ -162,10 +162,12 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
                                                         int shift, int dbits,
                                                         int* __restrict__ hist,
                                                         int* __restrict__ err) {
-  __shared__ int h[kMaxRadix];
+  // one histogram per wave: equal digits (a hub target's edges) then contend
+  // only within a wave
+  __shared__ int h[kSortWaves][kMaxRadix];
   const int radix = 1 << dbits;
-  for (int d = threadIdx.x; d < radix; d += kSortThreads) h[d] = 0;
-  __syncthreads();
+  const int wave = threadIdx.x / kWave;
+  for (int d = lane_id(); d < radix; d += kWave) h[wave][d] = 0;
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
   IdxT rs[kSortItems], rt[kSortItems];
 #pragma unroll
@@ -189,12 +191,16 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
       decode_edge(m, e, rs[i], rt[i], src != nullptr, &s, &k, &bad);
       any_bad |= bad && e < E;
     }
-    if (e < E) atomicAdd(&h[(k >> shift) & (radix - 1)], 1);
+    if (e < E) atomicAdd(&h[wave][(k >> shift) & (radix - 1)], 1);
   }
   if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += kSortThreads)
-    hist[(int64_t)d * gridDim.x + blockIdx.x] = h[d];
+  for (int d = threadIdx.x; d < radix; d += kSortThreads) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kSortWaves; ++w) c += h[w][d];
+    hist[(int64_t)d * gridDim.x + blockIdx.x] = c;
+  }
 }
 
 // Stable scatter of one tile by one digit. Wave w owns tile positions
