@@ -163,11 +163,15 @@ def test_gcn_norm_sliced_and_direct(tfg, orc, monkeypatch, n, e, weighted, idx, 
         assert same_bits(host(r["deg"]), odeg), mode
         assert same_bits(host(r["edge_weight"]), ow), mode
         assert same_bits(host(r["edge_weight_csr"]), ow[perm]), mode
-        # without the edge list the COO kernel keeps fewer registers per edge
+        # one order at a time (the sliced path then runs one kernel per order)
         r = tfg.tfg_gcn_norm(eid, n, edge_weight=None if w is None else dev(w),
                              add_self_loops=loops, graph=g, out_edge_index=False,
                              out_edge_weight_csr=False, out_deg=False)
         assert same_bits(host(r["edge_weight"]), ow), mode
+        r = tfg.tfg_gcn_norm(eid, n, edge_weight=None if w is None else dev(w),
+                             add_self_loops=loops, graph=g, out_edge_index=False,
+                             out_edge_weight=False, out_deg=False)
+        assert same_bits(host(r["edge_weight_csr"]), ow[perm]), mode
 
 
 # ---------------------------------------------------------------------------
