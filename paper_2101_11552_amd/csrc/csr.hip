@@ -5,13 +5,13 @@
 // keeps the input order among equal keys (bit-identical to a sequential
 // counting sort). With one source part this is the CSR by target.
 //
-// Per radix pass: an upsweep counts the digits of every 8192-edge tile
-// (block-major histogram, coalesced), three small kernels turn the counts
-// into output offsets, and a scatter ranks each tile stably (one ballot per
-// digit bit per 64 edges), stages it in LDS in digit order and writes every
-// digit's run with consecutive addresses. Row pointers come from the run
-// boundaries of the sorted keys; the aggregation work lists from the row
-// pointers.
+// Per radix pass: an upsweep counts the digits of every 8192-edge tile into
+// one column of a digit-major table, one device-wide exclusive scan of the
+// table turns the counts into output offsets, and a scatter ranks each tile
+// stably (one ballot per digit bit per 64 edges), stages it in LDS in digit
+// order and writes every digit's run with consecutive addresses. Row pointers
+// come from the run boundaries of the sorted keys; the aggregation work lists
+// from the row pointers (per-block counts and a scan, no atomics).
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
