@@ -236,11 +236,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
   __syncthreads();
 
-  // Later passes load keys and payloads together up front (one round of
-  // memory latency per tile). The first pass keeps only the keys: its edge
-  // id is the position, and its source id is decoded again from edge_index
-  // (an L2 hit) when staged, which keeps that kernel within 64 VGPRs.
-  int key[kSortItems], lpos[kSortItems], pe[FIRST ? 1 : kSortItems], ps[FIRST ? 1 : kSortItems];
+  // Keys and payloads are loaded together up front (one round of memory
+  // latency per tile). In the first pass the edge id is the position itself
+  // and the source id comes out of the key's decoding.
+  int key[kSortItems], lpos[kSortItems], pe[FIRST ? 1 : kSortItems], ps[kSortItems];
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
@@ -248,9 +247,8 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
     if constexpr (FIRST) {
       IdxT s0, t0;
       load_raw(src, tgt, m.E_in, e, &s0, &t0);
-      int sv;
       bool bad;
-      decode_edge(m, e, s0, t0, src != nullptr, &sv, &key[i], &bad);
+      decode_edge(m, e, s0, t0, src != nullptr, &ps[i], &key[i], &bad);
     } else {
       key[i] = kin[e];
       pe[i] = ein[e];
@@ -343,15 +341,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
     if (lpos[i] >= 0) {
-      if constexpr (FIRST) {
-        const int64_t e = base + wave * (kWave * kSortItems) + i * kWave + lane;
-        const int64_t ec = e < m.E_in ? e : (m.E_in > 0 ? m.E_in - 1 : 0);
-        const IdxT s0 = (src && m.E_in > 0) ? src[ec] : IdxT(0);
-        bool bad;
-        stage[lpos[i]] = decode_source(m, e, s0, src != nullptr, &bad);
-      } else {
-        stage[lpos[i]] = ps[i];
-      }
+      stage[lpos[i]] = ps[i];
     }
   __syncthreads();
 #pragma unroll
