@@ -29,7 +29,7 @@ constexpr int kSortThreads = 1024;                    // 16 waves
 constexpr int kSortItems = 8;                         // items per thread
 constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 edges per tile
 constexpr int kSortWaves = kSortThreads / kWave;
-constexpr int kMaxDigitBits = 9;
+constexpr int kMaxDigitBits = 8;
 constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 512
 constexpr int kXcds = 8;
 
@@ -208,8 +208,8 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
 // (wave, round, lane) order is the input order. Within a round, lanes with the
 // same digit find each other with one ballot per digit bit; their rank is the
 // number of such lanes below them plus the wave's running count of the digit.
-// The tile is then staged in LDS in digit order, one array at a time (keys,
-// edge ids, source ids share one buffer), and written out so that consecutive
+// The tile is then staged in LDS in digit order in two rounds (keys with edge
+// ids in two buffers, then source ids) and written out so that consecutive
 // threads write consecutive addresses of a digit's run.
 //   FIRST: keys and payloads come from edge_index (payload: edge id, source)
 // (16-wave blocks; at most 64 VGPRs so that two blocks fit on a CU)
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
   __shared__ int loff[kMaxRadix];
   __shared__ int goff[kMaxRadix];
-  __shared__ int stage[kSortTile];
+  __shared__ int stage[2][kSortTile];
   __shared__ int tmp[kSortWaves];
 
   const int radix = 1 << dbits;
@@ -302,51 +302,43 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
     lpos[i] = p < tile_n ? lpos[i] + loff[d] + (int)wcnt[wave][d] : -1;
   }
 
-  // keys: stage, then every thread writes positions threadIdx.x + i * 1024
+  // keys and edge ids: stage both, then every thread writes positions
+  // threadIdx.x + i * 1024 of each
   int gpos[kSortItems];
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
-    if (lpos[i] >= 0) stage[lpos[i]] = key[i];
+    if (lpos[i] >= 0) {
+      stage[0][lpos[i]] = key[i];
+      if constexpr (FIRST)
+        stage[1][lpos[i]] = (int)(base + wave * (kWave * kSortItems) + i * kWave + lane);
+      else
+        stage[1][lpos[i]] = pe[i];
+    }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = i * kSortThreads + threadIdx.x;
     gpos[i] = -1;
     if (p < tile_n) {
-      const int k = stage[p];
+      const int k = stage[0][p];
       const int d = (k >> shift) & (radix - 1);
       const int64_t gp = (int64_t)goff[d] + (p - loff[d]);
       if (gp >= 0 && gp < E) {  // always true for a consistent histogram
         gpos[i] = (int)gp;
         kout[gp] = k;
+        eout[gp] = stage[1][p];
       }
     }
   }
   __syncthreads();
-  // edge ids
-#pragma unroll
-  for (int i = 0; i < kSortItems; ++i)
-    if (lpos[i] >= 0) {
-      if constexpr (FIRST)
-        stage[lpos[i]] = (int)(base + wave * (kWave * kSortItems) + i * kWave + lane);
-      else
-        stage[lpos[i]] = pe[i];
-    }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kSortItems; ++i)
-    if (gpos[i] >= 0) eout[gpos[i]] = stage[i * kSortThreads + threadIdx.x];
-  __syncthreads();
   // source ids
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
-    if (lpos[i] >= 0) {
-      stage[lpos[i]] = ps[i];
-    }
+    if (lpos[i] >= 0) stage[0][lpos[i]] = ps[i];
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
-    if (gpos[i] >= 0) sout[gpos[i]] = stage[i * kSortThreads + threadIdx.x];
+    if (gpos[i] >= 0) sout[gpos[i]] = stage[0][i * kSortThreads + threadIdx.x];
 }
 
 // bounds[v] = first position whose sorted key is >= v (v = 0..K). Position k
