@@ -174,6 +174,23 @@ def test_gcn_norm_sliced_and_direct(tfg, orc, monkeypatch, n, e, weighted, idx, 
         assert same_bits(host(r["edge_weight_csr"]), ow[perm]), mode
 
 
+@pytest.mark.parametrize("idx", [np.int32, np.int64])
+def test_gcn_norm_sliced_hub_row(tfg, orc, monkeypatch, idx):
+    # a target with more than 65535 in-edges (a row longer than any 16-bit
+    # count) through the sliced kernels
+    n = 3000
+    ei = graphgen.random_graph(29, n, 10_000, hub=5, hub_edges=70_000)
+    oei, ow, odeg = orc.gcn_norm(ei, n)
+    assert odeg.max() > 65535
+    perm = orc.csr_by_target(oei, n)[2]
+    eid = dev(ei.astype(idx))
+    g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+    monkeypatch.setenv("TFG_NORM_SLICED", "1")
+    r = tfg.tfg_gcn_norm(eid, n, graph=g)
+    assert same_bits(host(r["edge_weight"]), ow)
+    assert same_bits(host(r["edge_weight_csr"]), ow[perm])
+
+
 # ---------------------------------------------------------------------------
 # Aggregation
 # ---------------------------------------------------------------------------
