@@ -126,6 +126,32 @@ __global__ __launch_bounds__(1024) void scan_sums(int* __restrict__ sums, int64_
   }
 }
 
+// In-place exclusive scan of a short array by one block, 8 consecutive
+// values per thread (for the small tables of small graphs: one launch
+// instead of three).
+constexpr int kSmallScan = 32768;
+__global__ __launch_bounds__(1024) void scan_small(int* __restrict__ a, int64_t n) {
+  __shared__ int tmp[1024 / kWave];
+  int carry = 0;
+  for (int64_t base = 0; base < n; base += 1024 * 8) {
+    const int64_t i0 = base + (int64_t)threadIdx.x * 8;
+    int v[8], t = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = i0 + j < n ? a[i0 + j] : 0;
+      t += v[j];
+    }
+    int total;
+    int run = carry + block_excl_scan<1024 / kWave>(t, tmp, &total);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (i0 + j < n) a[i0 + j] = run;
+      run += v[j];
+    }
+    carry += total;
+  }
+}
+
 __global__ __launch_bounds__(kScanThreads) void scan_apply(const int* in, int* out, int64_t n,
                                                            const int* __restrict__ sums) {
   __shared__ int tmp[kScanThreads / kWave];
@@ -445,6 +471,47 @@ __global__ __launch_bounds__(1024) void worklist_offsets(int* __restrict__ block
   }
 }
 
+// The three steps in one block, for graphs of at most kWlSingle rows: the
+// rows go in chunks of kWlThreads, each chunk's entries placed after the
+// previous chunks' (the same lists, in the same order).
+constexpr int kWlSingle = 32 * kWlThreads;
+__global__ __launch_bounds__(kWlThreads) void worklist_single(
+    const int* __restrict__ rowptr, int64_t N, int chunk, int* __restrict__ counters,
+    WorkItem* __restrict__ heavy, WorkItem* __restrict__ light, SplitRow* __restrict__ split,
+    int* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
+  __shared__ int tmp[kWlThreads / kWave];
+  int carry[kLists] = {0, 0, 0, 0, 0};
+  for (int64_t r0 = 0; r0 < N; r0 += kWlThreads) {
+    const int64_t r = r0 + threadIdx.x;
+    int beg, deg, c[kLists], o[kLists];
+    row_entries(rowptr, N, chunk, r, &beg, &deg, c);
+#pragma unroll
+    for (int i = 0; i < kLists; ++i) {
+      int tot;
+      o[i] = carry[i] + block_excl_scan<kWlThreads / kWave>(c[i], tmp, &tot);
+      carry[i] += tot;
+    }
+    if (r < N) {
+      if (c[3])
+        short_rows[o[3]] = (int)r;
+      else if (c[4])
+        long_rows[o[4]] = WorkItem{(int)r, beg, beg + deg, -1};
+      if (c[2]) {
+        for (int j = 0; j < c[0]; ++j) {
+          const int kb = beg + j * chunk;
+          heavy[o[0] + j] = WorkItem{(int)r, kb, min(kb + chunk, beg + deg), o[0] + j};
+        }
+        split[o[2]] = SplitRow{(int)r, o[0], c[0], deg};
+      } else {
+        light[o[1]] = WorkItem{(int)r, beg, beg + deg, -1};
+      }
+    }
+  }
+  if (threadIdx.x == 0)
+#pragma unroll
+    for (int i = 0; i < kLists; ++i) counters[kListCounter[i]] = carry[i];
+}
+
 __global__ __launch_bounds__(kWlThreads) void worklist_fill(
     const int* __restrict__ rowptr, int64_t N, int chunk, const int* __restrict__ block_sums,
     int nb, WorkItem* __restrict__ heavy, WorkItem* __restrict__ light,
@@ -646,6 +713,11 @@ int build_part_plan(Graph& g, char* scratch, const ScratchLayout& L, hipStream_t
 
 int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s) {
   if (n <= 0) return TFG_OK;
+  if (in == out && n <= kSmallScan) {
+    scan_small<<<1, 1024, 0, s>>>(out, n);
+    TFG_LAUNCHED("exclusive scan (one block)");
+    return TFG_OK;
+  }
   const int64_t nt = scan_tiles(n);
   scan_tile_sums<<<dim3((unsigned)nt), dim3(kScanThreads), 0, s>>>(in, n, tile_sums);
   scan_sums<<<1, 1024, 0, s>>>(tile_sums, nt);
@@ -735,10 +807,15 @@ int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void
   if (g.N > 0) {
     const int nb = (int)((g.N + kWlThreads - 1) / kWlThreads);
     int* wl = reinterpret_cast<int*>(sc + L.wl_sums);
-    worklist_count<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb);
-    worklist_offsets<<<1, 1024, 0, s>>>(wl, nb, g.counters);
-    worklist_fill<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb, g.heavy, g.light,
-                                            g.split, g.short_rows, g.long_rows);
+    if (g.N <= kWlSingle) {
+      worklist_single<<<1, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, g.counters, g.heavy,
+                                               g.light, g.split, g.short_rows, g.long_rows);
+    } else {
+      worklist_count<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb);
+      worklist_offsets<<<1, 1024, 0, s>>>(wl, nb, g.counters);
+      worklist_fill<<<nb, kWlThreads, 0, s>>>(g.rowptr, g.N, g.chunk, wl, nb, g.heavy, g.light,
+                                              g.split, g.short_rows, g.long_rows);
+    }
     TFG_LAUNCHED("work lists");
     if (g.parts > 1) {
       rc = build_part_plan(g, sc, L, s);
