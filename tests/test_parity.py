@@ -68,13 +68,16 @@ def same_bits(a, b):
 
 @pytest.mark.parametrize("n,e,loops,idx,parts", [
     (1, 7, False, np.int64, 1),            # N = 1: a single row
-    (300, 50_000, False, np.int32, 1),     # one radix pass (9 bits), 7 tiles + ragged tail
+    (200, 30_000, False, np.int32, 1),     # one radix pass (8 bits), 4 tiles + ragged tail
+    (300, 50_000, False, np.int32, 1),     # two passes (9 bits), 7 tiles + ragged tail
     (5_000, 70_001, True, np.int64, 1),    # two passes, loops appended
     (300_000, 40_000, False, np.int32, 1),  # three passes (19 bits), mostly empty rows
     (1000, 0, True, np.int32, 1),          # no input edges: loops only
     (2000, 90_000, True, np.int32, 8),     # source parts: key (target, part), 3 + 11 bits
     (300, 50_000, False, np.int64, 3),     # parts that do not divide N
     (70_000, 200_000, False, np.int32, 16),  # 21-bit keys: three passes
+    (60_000, 500_000, True, np.int32, 1),  # digit tables of 21.5k counts: one-block scan
+    (20_000, 1_500_000, False, np.int32, 1),  # digit tables of 58.6k counts: three-kernel scan
 ])
 def test_csr_bit_exact(tfg, orc, n, e, loops, idx, parts):
     ei = graphgen.random_graph(e + n, n, e, hub=n // 2, hub_edges=e // 4)
