@@ -54,8 +54,9 @@ def source_sha(paths) -> str:
 
 
 def stored_traffic():
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current aggregation source."""
+    """Bytes per launch that the L2s request from the fabric (Infinity Cache
+    and HBM together), from the committed rocprofv3 counter summary, if it was
+    taken on the current aggregation source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
