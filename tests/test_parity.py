@@ -76,6 +76,8 @@ def same_bits(a, b):
     (2000, 90_000, True, np.int32, 8),     # source parts: key (target, part), 3 + 11 bits
     (300, 50_000, False, np.int64, 3),     # parts that do not divide N
     (70_000, 200_000, False, np.int32, 16),  # 21-bit keys: three passes
+    (32_768, 40_000, True, np.int32, 1),   # 32768 rows: one-block work lists (largest)
+    (32_769, 40_000, True, np.int32, 1),   # one row more: work lists from per-block counts
     (60_000, 500_000, True, np.int32, 1),  # digit tables of 21.5k counts: one-block scan
     (20_000, 1_500_000, False, np.int32, 1),  # digit tables of 58.6k counts: three-kernel scan
 ])
@@ -90,6 +92,12 @@ def test_csr_bit_exact(tfg, orc, n, e, loops, idx, parts):
     ref = orc.csr_by_target(full, n, parts=min(parts, n))
     r, c, p = ref[:3]
     assert np.array_equal(rowptr, r) and np.array_equal(perm, p) and np.array_equal(col, c)
+    # the row plan's lists: rows longer than 128 edges are cut into chunks
+    deg = np.diff(r)
+    long_rows = deg[deg > 128]
+    info = g.info()
+    assert info["n_rows_split"] == long_rows.size
+    assert info["n_chunks"] == int(((long_rows + 127) // 128).sum())
     if parts > 1:
         assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
 
