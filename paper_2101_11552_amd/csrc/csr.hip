@@ -474,7 +474,7 @@ __global__ __launch_bounds__(1024) void worklist_offsets(int* __restrict__ block
 // The three steps in one block, for graphs of at most kWlSingle rows: the
 // rows go in chunks of kWlThreads, each chunk's entries placed after the
 // previous chunks' (the same lists, in the same order).
-constexpr int kWlSingle = 32 * kWlThreads;
+constexpr int kWlSingle = 4 * kWlThreads;
 __global__ __launch_bounds__(kWlThreads) void worklist_single(
     const int* __restrict__ rowptr, int64_t N, int chunk, int* __restrict__ counters,
     WorkItem* __restrict__ heavy, WorkItem* __restrict__ light, SplitRow* __restrict__ split,

@@ -76,8 +76,8 @@ def same_bits(a, b):
     (2000, 90_000, True, np.int32, 8),     # source parts: key (target, part), 3 + 11 bits
     (300, 50_000, False, np.int64, 3),     # parts that do not divide N
     (70_000, 200_000, False, np.int32, 16),  # 21-bit keys: three passes
-    (32_768, 40_000, True, np.int32, 1),   # 32768 rows: one-block work lists (largest)
-    (32_769, 40_000, True, np.int32, 1),   # one row more: work lists from per-block counts
+    (4_096, 40_000, True, np.int32, 1),    # 4096 rows: one-block work lists (largest)
+    (4_097, 40_000, True, np.int32, 1),    # one row more: work lists from per-block counts
     (60_000, 500_000, True, np.int32, 1),  # digit tables of 21.5k counts: one-block scan
     (20_000, 1_500_000, False, np.int32, 1),  # digit tables of 58.6k counts: three-kernel scan
 ])
