@@ -184,6 +184,22 @@ __global__ __launch_bounds__(kBlock) void softmax_short(const int* __restrict__ 
   if (i < n_short) softmax_short_row(rowptr, perm, short_rows[i], s, H, lane % HP, HP, out, out_csr);
 }
 
+// kSmSteps slot steps (positions k0, k0 + SL, ...) at a time: the edge ids,
+// then the scores, issued together (e < 0: past the item or an inactive head).
+constexpr int kSmSteps = 4;
+__device__ __forceinline__ void load_steps(const int* __restrict__ perm,
+                                           const float* __restrict__ s, int H, int h, bool act,
+                                           int k0, int SL, int ke, int64_t (&e)[kSmSteps],
+                                           float (&v)[kSmSteps]) {
+#pragma unroll
+  for (int u = 0; u < kSmSteps; ++u) {
+    const int k = k0 + u * SL;
+    e[u] = (act && k < ke) ? (int64_t)perm[k] : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < kSmSteps; ++u) v[u] = e[u] >= 0 ? s[e[u] * H + h] : 0.0f;
+}
+
 // The other buckets of the row plan: wavefronts [0, n_heavy) take the chunks
 // of long rows, the rest one other light row each. Lanes are (slot, head) pairs: HP
 // heads (a power of two) per pass and 64 / HP edge slots; each lane keeps the
@@ -218,8 +234,14 @@ __global__ __launch_bounds__(kBlock) void softmax_items(
     const bool act = h < H;
     float m = -__builtin_huge_valf();
     double d = 0.0;
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) stat_add(m, d, s[(int64_t)perm[k] * H + h]);
+    for (int k0 = kb + slot; k0 < ke; k0 += kSmSteps * SL) {
+      int64_t e[kSmSteps];
+      float v[kSmSteps];
+      load_steps(perm, s, H, h, act, k0, SL, ke, e, v);
+#pragma unroll
+      for (int u = 0; u < kSmSteps; ++u)
+        if (e[u] >= 0) stat_add(m, d, v[u]);
+    }
     for (int off = HP; off < kWave; off <<= 1) {
       const float m2 = __shfl_xor(m, off);
       const double d2 = __shfl_xor(d, off);
@@ -232,13 +254,18 @@ __global__ __launch_bounds__(kBlock) void softmax_items(
       }
       continue;
     }
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) {
-        const int64_t e = perm[k];
-        const float a = (float)((double)expf(s[e * H + h] - m) / d);
-        out[e * H + h] = a;
-        if (out_csr) out_csr[(int64_t)k * H + h] = a;
-      }
+    for (int k0 = kb + slot; k0 < ke; k0 += kSmSteps * SL) {
+      int64_t e[kSmSteps];
+      float v[kSmSteps];
+      load_steps(perm, s, H, h, act, k0, SL, ke, e, v);
+#pragma unroll
+      for (int u = 0; u < kSmSteps; ++u)
+        if (e[u] >= 0) {
+          const float a = (float)((double)expf(v[u] - m) / d);
+          out[e[u] * H + h] = a;
+          if (out_csr) out_csr[(int64_t)(k0 + u * SL) * H + h] = a;
+        }
+    }
   }
 }
 
@@ -278,11 +305,17 @@ __global__ __launch_bounds__(kBlock) void softmax_write(
     if (h >= H) continue;
     const float m = pm[(int64_t)pslot * H + h];
     const double d = pd[(int64_t)pslot * H + h];
-    for (int k = kb + slot; k < ke; k += SL) {
-      const int64_t e = perm[k];
-      const float a = (float)((double)expf(s[e * H + h] - m) / d);
-      out[e * H + h] = a;
-      if (out_csr) out_csr[(int64_t)k * H + h] = a;
+    for (int k0 = kb + slot; k0 < ke; k0 += kSmSteps * SL) {
+      int64_t e[kSmSteps];
+      float v[kSmSteps];
+      load_steps(perm, s, H, h, true, k0, SL, ke, e, v);
+#pragma unroll
+      for (int u = 0; u < kSmSteps; ++u)
+        if (e[u] >= 0) {
+          const float a = (float)((double)expf(v[u] - m) / d);
+          out[e[u] * H + h] = a;
+          if (out_csr) out_csr[(int64_t)(k0 + u * SL) * H + h] = a;
+        }
     }
   }
 }
