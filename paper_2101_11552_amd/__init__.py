@@ -17,10 +17,15 @@ import os
 import torch
 
 __all__ = [
-    "TfgError", "Graph", "tfg_graph_create", "tfg_graph_csr", "tfg_graph_segments", "tfg_check",
+    "TfgError", "TfgIndexError", "TfgValueError", "Graph",
+    "tfg_graph_bytes", "tfg_graph_create", "tfg_graph_create_transposed", "tfg_graph_csr",
+    "tfg_edge_reorder", "tfg_graph_segments", "tfg_check",
     "tfg_gcn_norm",
-    "tfg_aggregate", "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_pool",
+    "tfg_aggregate_ws_bytes", "tfg_aggregate", "tfg_aggregate_backward",
+    "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_softmax_backward",
+    "tfg_segment_pool", "tfg_segment_pool_backward",
     "tfg_batch_graphs", "tfg_propagate", "tfg_gat_aggregate",
+    "tfg_edge_dot_scores", "tfg_gat_dot_aggregate",
     "library_path", "load",
 ]
 
