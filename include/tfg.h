@@ -23,8 +23,11 @@
  * Messages flow source -> target and are reduced by the target id, the reduce
  * key of the paper's reducer (Sec. 2.1.2).
  *
- * Index arrays are int32 (TFG_I32) or int64 (TFG_I64); node and edge counts
- * must stay below 2^31 (else TFG_ERR_TOO_LARGE). Floating-point data is
+ * Index arrays are int32 (TFG_I32) or int64 (TFG_I64). Node counts, edge
+ * counts (including appended self-loops), E * H and feature counts must stay
+ * below 2^31 - 2^20 = 2,146,435,072 (else TFG_ERR_TOO_LARGE): positions are
+ * 32-bit inside the kernels, with a margin for the strides that step through
+ * them. Floating-point data is
  * float32, row-major; a feature matrix has a leading dimension ldx >= F (in
  * elements). Outputs are dense row-major with leading dimension F.
  *
@@ -67,7 +70,7 @@ typedef enum {
     TFG_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad enum, F % H != 0, mismatch with a graph */
     TFG_ERR_INDEX_RANGE = 2, /* an edge id outside [0, N_src) / [0, N), a graph id outside [0, G) */
     TFG_ERR_UNSORTED = 3,    /* graph_index is not non-decreasing */
-    TFG_ERR_TOO_LARGE = 4,   /* a count does not fit the 31-bit internal indexing */
+    TFG_ERR_TOO_LARGE = 4,   /* a count is not below 2^31 - 2^20 (32-bit internal positions) */
     TFG_ERR_WORKSPACE = 5,   /* buffer smaller than the size the matching query returned, or not 256-byte aligned */
     TFG_ERR_HIP = 6          /* the HIP runtime reported an error; see tfg_last_error() */
 } tfg_status;

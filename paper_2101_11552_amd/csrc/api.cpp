@@ -15,7 +15,11 @@ namespace tfg {
 
 namespace {
 thread_local std::string g_last_error;
-constexpr int64_t kMaxCount = (int64_t(1) << 31) - 1;
+// Counts (nodes, edges with their appended loops, E * H, features, graphs)
+// stay below 2^31 - 2^20: kernels keep positions in 32-bit ints and step
+// through them in strides of up to a work item (at most 2^16 positions), so
+// the margin keeps every position plus a stride representable.
+constexpr int64_t kMaxCount = (int64_t(1) << 31) - (int64_t(1) << 20);
 }  // namespace
 
 void set_error(const std::string& msg) { g_last_error = msg; }
@@ -63,8 +67,8 @@ size_t graph_total_bytes(int64_t E, int64_t N, int parts) {
 
 int check_counts(int64_t E, int64_t N, int64_t N_src) {
   if (E < 0 || N < 0 || N_src < 0) return fail(TFG_ERR_INVALID_ARG, "negative size");
-  if (E > kMaxCount || N >= kMaxCount || N_src >= kMaxCount)
-    return fail(TFG_ERR_TOO_LARGE, "edge or node count does not fit 31-bit indexing");
+  if (E >= kMaxCount || N >= kMaxCount || N_src >= kMaxCount)
+    return fail(TFG_ERR_TOO_LARGE, "edge or node count not below 2^31 - 2^20");
   return TFG_OK;
 }
 
@@ -516,10 +520,10 @@ int tfg_aggregate_backward(const tfg_graph* g, const tfg_graph* gt, const float*
     return fail(TFG_ERR_INVALID_ARG, "TFG_CSR_T weights need gt");
   if (dw_order != TFG_COO && dw_order != TFG_CSR)
     return fail(TFG_ERR_INVALID_ARG, "bad dw order");
-  if (F < 0 || H < 1 || (F > 0 && F % H != 0) || F > kMaxCount || H > kMaxCount)
+  if (F < 0 || H < 1 || (F > 0 && F % H != 0) || F >= kMaxCount || H >= kMaxCount)
     return fail(TFG_ERR_INVALID_ARG, "bad F or H");
   const Graph& fg = g->g;
-  if (fg.E * H >= kMaxCount) return fail(TFG_ERR_TOO_LARGE, "E * H does not fit 31-bit indexing");
+  if (fg.E * H >= kMaxCount) return fail(TFG_ERR_TOO_LARGE, "E * H not below 2^31 - 2^20");
   if (fg.N > 0 && F > 0 && dy == nullptr) return fail(TFG_ERR_INVALID_ARG, "dy is NULL");
   if (dx != nullptr && gt == nullptr) return fail(TFG_ERR_INVALID_ARG, "dx needs gt");
   if (dw != nullptr && fg.N_src > 0 && F > 0 && x == nullptr)

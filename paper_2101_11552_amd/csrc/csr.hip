@@ -730,7 +730,7 @@ int default_chunk() {
   static const int chunk = [] {
     const char* v = std::getenv("TFG_ROW_CHUNK");
     const int c = v ? std::atoi(v) : kDefaultChunk;
-    return c >= 64 ? c : kDefaultChunk;
+    return c >= 64 && c <= kMaxChunk ? c : kDefaultChunk;
   }();
   return chunk;
 }

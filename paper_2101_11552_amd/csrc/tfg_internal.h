@@ -15,6 +15,7 @@ namespace tfg {
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per block for most kernels (4 waves)
 constexpr int kDefaultChunk = 128; // max edges per work item of the row plan
+constexpr int kMaxChunk = 1 << 16;  // largest chunk the tuning knob may set
 constexpr int kShortRow = 8;       // rows of at most this many edges are "short"
 
 // Device error flag bits (graph->err and the pooling workspace flag).

@@ -58,6 +58,14 @@ def test_size_queries(lib):
     assert lib.tfg_graph_bytes(-1, 100, 100, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 1
     assert lib.tfg_graph_bytes(2**31, 10, 10, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 4
     assert lib.tfg_graph_bytes(2**31 - 5, 10, 10, 1, 0, ctypes.byref(b), ctypes.byref(s)) == 4
+    # the largest accepted count is 2^31 - 2^20 - 1, appended loops included
+    top = 2**31 - 2**20 - 1
+    assert lib.tfg_graph_bytes(top, 10, 10, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 0
+    assert b.value >= 3 * 4 * top
+    assert lib.tfg_graph_bytes(top + 1, 10, 10, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 4
+    assert lib.tfg_graph_bytes(top - 10, 10, 10, 1, 0, ctypes.byref(b), ctypes.byref(s)) == 0
+    assert lib.tfg_graph_bytes(top - 9, 10, 10, 1, 0, ctypes.byref(b), ctypes.byref(s)) == 4
+    assert lib.tfg_graph_bytes(100, 10, top + 1, 0, 0, ctypes.byref(b), ctypes.byref(s)) == 4
     assert lib.tfg_segment_pool_ws_bytes(100, 7) >= 8 * 4
     assert lib.tfg_aggregate_ws_bytes(1000, 100, 100, 64, 2, None) > lib.tfg_aggregate_ws_bytes(
         1000, 100, 100, 64, 0, None)
@@ -98,6 +106,7 @@ def test_host_side_argument_errors(lib):
     assert b"aligned" in lib.tfg_last_error()
     assert agg(E=-1) == 1
     assert agg(N=2**31) == 4
+    assert agg(N=2**31 - 2**20) == 4
     # pooling: bad reduce, ldx < F
     assert lib.tfg_segment_pool(fake, 10, 4, 4, fake, 0, 3, 5, fake, None, 1, fake, 1 << 20,
                                 None) == 1
