@@ -518,7 +518,7 @@ def main():
     info = g.info()
     a0 = torch.cuda.Event(enable_timing=True)
     a1 = torch.cuda.Event(enable_timing=True)
-    reps = max(args.steps, 5)
+    reps = max(args.steps, 20)
     a0.record()
     for _ in range(reps):
         tfg.tfg_aggregate(None, x, N, "sum", edge_weight=norm["edge_weight_csr"],
@@ -526,6 +526,15 @@ def main():
     a1.record()
     torch.cuda.synchronize()
     agg_ms = a0.elapsed_time(a1) / reps
+    # the same launches one by one (events around each): median and minimum
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    marks[0].record()
+    for i in range(reps):
+        tfg.tfg_aggregate(None, x, N, "sum", edge_weight=norm["edge_weight_csr"],
+                          weight_order="csr", graph=g, out=out, ws=agg_ws)
+        marks[i + 1].record()
+    torch.cuda.synchronize()
+    each = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(reps))
 
     B = algorithmic_bytes(E_total, N, F)
     achieved = B / (agg_ms * 1e-3) / 1e9
@@ -560,6 +569,8 @@ def main():
         "stages_ms": {"csr_build": round(avg["create"], 4), "gcn_norm": round(avg["norm"], 4),
                       "aggregate": round(avg["agg"], 4)},
         "aggregate_cached_graph": {"ms": round(agg_ms, 4),
+                                   "ms_median": round(each[len(each) // 2], 4),
+                                   "ms_min": round(each[0], 4), "launches": reps,
                                    "GE_per_s": round(E_total / (agg_ms * 1e-3) / 1e9, 3),
                                    "src_parts": info["src_parts"],
                                    "n_part_items": info["n_part_items"],
