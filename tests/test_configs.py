@@ -184,6 +184,27 @@ def test_power_law_full_size(tfg, orc, c4):
     assert_scaled(host(y3)[rows], ref, S, what="c4 sampled rows, row plan")
 
 
+def test_power_law_int64_ids_match_int32(tfg, c4):
+    """The 64-bit index kernels (loads of two registers per id in the sort's
+    first pass and in the COO-order normalisation) at full size: the graph
+    and the normalisation from int64 ids equal those from int32 ids bit for
+    bit."""
+    import torch
+    ei, n = c4["edge_index"], c4["N"]
+    outs = []
+    for dt in (np.int32, np.int64):
+        eid = dev(ei.astype(dt))
+        g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+        norm = tfg.tfg_gcn_norm(eid, n, graph=g)
+        rowptr, col, perm = tfg.tfg_graph_csr(g)
+        outs.append([rowptr, col, perm, tfg.tfg_graph_segments(g), norm["edge_index"],
+                     norm["edge_weight"].view(torch.int32),
+                     norm["edge_weight_csr"].view(torch.int32), norm["deg"].view(torch.int32)])
+        del g, norm, eid
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_gat_attention_fused(tfg, orc):
     c = graphgen.config3()
     ei, h, n, H = c["edge_index"], c["h"], c["N"], c["H"]
