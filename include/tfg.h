@@ -35,7 +35,9 @@
  * the caller. The library never allocates device memory: callers query the
  * workspace size (tfg_*_ws_bytes) and pass a buffer of at least that many
  * bytes (256-byte aligned). Inputs are only read; outputs must not overlap
- * inputs. The only host allocation is the small tfg_graph struct.
+ * inputs. Host allocations: the small tfg_graph struct, and 32 bytes of
+ * pinned host memory per calling thread (allocated on its first synchronising
+ * call, kept until the process ends) into which counters are read back.
  *
  * Streams: every call enqueues its kernels on `stream` (a hipStream_t; NULL is
  * the null stream) and returns without waiting, except where a call is

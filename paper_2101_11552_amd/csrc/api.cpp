@@ -61,6 +61,19 @@ int check_ws(const void* ws, size_t bytes, size_t need) {
   return TFG_OK;
 }
 
+// Reads n (<= 8) ints from device addresses into `to`, through the calling
+// thread's pinned buffer when there is one, and synchronises the stream.
+int read_back(hipStream_t s, int n, const int* const* from, int* to) {
+  int* pin = readback_buffer();
+  int* buf = pin ? pin : to;
+  for (int i = 0; i < n; ++i)
+    TFG_HIP(hipMemcpyAsync(buf + i, from[i], sizeof(int), hipMemcpyDeviceToHost, s));
+  TFG_HIP(hipStreamSynchronize(s));
+  if (pin)
+    for (int i = 0; i < n; ++i) to[i] = pin[i];
+  return TFG_OK;
+}
+
 size_t graph_total_bytes(int64_t E, int64_t N, int parts) {
   return graph_layout(E, N, parts, default_chunk()).total + graph_scratch_bytes(E, N, parts);
 }
@@ -317,9 +330,8 @@ int tfg_check(const tfg_graph* h, tfg_stream_t stream) {
   if (!h) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
   if (int rc = check_device(h)) return rc;
   int flags = 0;
-  hipStream_t s = as_stream(stream);
-  TFG_HIP(hipMemcpyAsync(&flags, h->g.counters + 3, sizeof(int), hipMemcpyDeviceToHost, s));
-  TFG_HIP(hipStreamSynchronize(s));
+  const int* from[1] = {h->g.counters + 3};
+  if (int rc = read_back(as_stream(stream), 1, from, &flags)) return rc;
   if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "an id was out of range");
   return TFG_OK;
 }
@@ -606,8 +618,8 @@ int tfg_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const v
   if (rc) return rc;
   if (validate) {
     int flags = 0;
-    TFG_HIP(hipMemcpyAsync(&flags, err, sizeof(int), hipMemcpyDeviceToHost, s));
-    TFG_HIP(hipStreamSynchronize(s));
+    const int* from[1] = {err};
+    if (int rrc = read_back(s, 1, from, &flags)) return rrc;
     if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "graph_index holds an id outside [0, G)");
     if (flags & kErrUnsorted) return fail(TFG_ERR_UNSORTED, "graph_index is not non-decreasing");
   }
@@ -638,8 +650,8 @@ int tfg_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void*
   if (rc) return rc;
   if (validate) {
     int flags = 0;
-    TFG_HIP(hipMemcpyAsync(&flags, err, sizeof(int), hipMemcpyDeviceToHost, s));
-    TFG_HIP(hipStreamSynchronize(s));
+    const int* from[1] = {err};
+    if (int rrc = read_back(s, 1, from, &flags)) return rrc;
     if (flags & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "graph_index holds an id outside [0, G)");
     if (flags & kErrUnsorted) return fail(TFG_ERR_UNSORTED, "graph_index is not non-decreasing");
   }
@@ -677,10 +689,8 @@ int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts
   if (rc) return rc;
   if (validate) {
     int host[3] = {0, 0, 0};
-    TFG_HIP(hipMemcpyAsync(&host[0], err, sizeof(int), hipMemcpyDeviceToHost, s));
-    TFG_HIP(hipMemcpyAsync(&host[1], node_off + G, sizeof(int), hipMemcpyDeviceToHost, s));
-    TFG_HIP(hipMemcpyAsync(&host[2], edge_off + G, sizeof(int), hipMemcpyDeviceToHost, s));
-    TFG_HIP(hipStreamSynchronize(s));
+    const int* from[3] = {err, node_off + G, edge_off + G};
+    if (int rrc = read_back(s, 3, from, host)) return rrc;
     if (host[0] & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "a count or local id is out of range");
     if (host[1] != Nb || host[2] != E)
       return fail(TFG_ERR_INDEX_RANGE, "node / edge counts do not add up to Nb / E");

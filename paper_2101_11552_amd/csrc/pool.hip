@@ -10,9 +10,9 @@ namespace {
 typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-__global__ void fill_goff(int* __restrict__ goff, int64_t n) {
+__global__ void zero_ints(int* __restrict__ p, int64_t n) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) goff[i] = 0;
+  if (i < n) p[i] = 0;
 }
 
 __device__ __forceinline__ int64_t clamp_gid(int64_t g, int64_t G) {
@@ -21,8 +21,11 @@ __device__ __forceinline__ int64_t clamp_gid(int64_t g, int64_t G) {
 
 // goff[g] = first node of graph g, goff[G] = Nb. Node n writes the starts of
 // the graphs (gi[n-1], gi[n]]; the thread n = Nb writes the empty tail graphs.
-// With valid sorted input every entry is written exactly once; otherwise the
-// error flag is set and the (clamped) entries stay inside [0, Nb].
+// With valid sorted input every entry is written exactly once. Otherwise the
+// error flag is set, and every entry is still written (so goff needs no
+// clearing first) with a value in [0, Nb]: the clamped ids run from -1 (before
+// node 0) to G (after node Nb - 1), so each g in [0, G] lies in (prev, cur] for
+// the first n whose cur reaches g.
 template <typename IdxT>
 __global__ __launch_bounds__(kBlock) void segment_bounds(const IdxT* __restrict__ gi, int64_t Nb,
                                                          int64_t G, int* __restrict__ goff,
@@ -241,9 +244,8 @@ void launch_pool_grad(int vec, const float* dy, int64_t G, int F, const void* gi
 int launch_segment_pool_backward(const float* dy, int64_t G, int64_t F, const void* graph_index,
                                  int index_type, int64_t Nb, int reduce, const int32_t* argmax,
                                  float* dx, int64_t ldx, int* goff, int* err, hipStream_t s) {
-  fill_goff<<<1, 64, 0, s>>>(err, 1);
+  zero_ints<<<1, 64, 0, s>>>(err, 1);
   if (Nb == 0 || F == 0) return TFG_OK;
-  fill_goff<<<(unsigned)((G + 1 + kBlock - 1) / kBlock), kBlock, 0, s>>>(goff, G + 1);
   const unsigned nb = (unsigned)((Nb + 1 + kBlock - 1) / kBlock);
   if (index_type == TFG_I64)
     segment_bounds<int64_t><<<nb, kBlock, 0, s>>>(static_cast<const int64_t*>(graph_index), Nb, G,
@@ -270,9 +272,8 @@ int launch_segment_pool_backward(const float* dy, int64_t G, int64_t F, const vo
 int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, const void* graph_index,
                         int index_type, int64_t G, int reduce, float* out, int32_t* argmax,
                         int* goff, int* err, hipStream_t s) {
-  fill_goff<<<1, 64, 0, s>>>(err, 1);
+  zero_ints<<<1, 64, 0, s>>>(err, 1);
   if (G == 0 || F == 0) return TFG_OK;
-  fill_goff<<<(unsigned)((G + 1 + kBlock - 1) / kBlock), kBlock, 0, s>>>(goff, G + 1);
   const unsigned nb = (unsigned)((Nb + 1 + kBlock - 1) / kBlock);
   if (index_type == TFG_I64)
     segment_bounds<int64_t><<<nb, kBlock, 0, s>>>(static_cast<const int64_t*>(graph_index), Nb, G,

@@ -89,6 +89,8 @@ struct GraphLayout {
 GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk);
 size_t graph_scratch_bytes(int64_t E, int64_t N, int parts);
 int default_chunk();
+// Pinned host ints (8) of the calling thread for counter readbacks, or NULL.
+int* readback_buffer();
 // Number of source parts for a graph: `requested` if >= 1 (capped), else a
 // choice from the sizes (P > 1 only when the gathered table is much larger
 // than the L2 caches and rows are long enough to be split by source range).
