@@ -579,6 +579,12 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
+                     # the bytes the L2s move to and from memory (Infinity Cache and HBM
+                     # together) per launch, as a rate against the same peak
+                     "traffic_GBps": (round(traffic / (agg_ms * 1e-3) / 1e9, 1)
+                                      if traffic else None),
+                     "traffic_frac": (round(traffic / (agg_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)
+                                      if traffic else None),
                      "kernel": "tfg_aggregate (spmm_rows + fixup_rows)",
                      "algorithmic_bytes_per_launch": B},
         "cpu_baseline": cpu,
