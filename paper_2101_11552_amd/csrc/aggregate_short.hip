@@ -15,8 +15,8 @@ namespace {
 
 template <int V, int SLOTS, bool MAX>
 __global__ __launch_bounds__(kBlock) void spmm_short(
-    const int* __restrict__ short_rows, int n_short, const int* __restrict__ rowptr,
-    const int* __restrict__ col, const int* __restrict__ perm, const float* __restrict__ w,
+    const WorkItem* __restrict__ short_rows, int n_short, const int* __restrict__ col,
+    const int* __restrict__ perm, const float* __restrict__ w,
     int w_by_perm, const float* __restrict__ x, int64_t ldx, int F, int mean,
     float* __restrict__ out, int* __restrict__ argout, Epilogue ep) {
   constexpr int LPS = kWave / SLOTS;
@@ -26,8 +26,8 @@ __global__ __launch_bounds__(kBlock) void spmm_short(
   const int64_t i = wave * SLOTS + lane / LPS;
   if (i >= n_short) return;  // nothing crosses lanes: a lane may leave early
   const int sl = lane % LPS;
-  const int t = short_rows[i];
-  const int kb = rowptr[t], n = rowptr[t + 1] - kb;  // 0 <= n <= kShortRow
+  const WorkItem it = short_rows[i];
+  const int t = it.row, kb = it.kbeg, n = it.kend - it.kbeg;  // 0 <= n <= kShortRow
   const bool need_perm = MAX || w_by_perm;
   int c[kShortRow], e[kShortRow];
   float wr[kShortRow];
@@ -97,7 +97,7 @@ template <int V, int SLOTS, bool MAX>
 void run(const Graph& g, const RowArgs& a, hipStream_t s) {
   const int64_t waves = (g.n_short + SLOTS - 1) / SLOTS;
   const dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
-  spmm_short<V, SLOTS, MAX><<<grid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.rowptr, a.col,
+  spmm_short<V, SLOTS, MAX><<<grid, kBlock, 0, s>>>(g.short_rows, g.n_short, a.col,
                                                     a.perm, a.w, a.w_by_perm, a.x, a.ldx, a.F,
                                                     a.mean, a.out, a.argout, a.ep);
 }

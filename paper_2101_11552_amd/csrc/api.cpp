@@ -115,7 +115,7 @@ int create_graph(Graph& g, const void* src, const void* tgt, int index_type, int
   g.split = reinterpret_cast<SplitRow*>(b + L.split);
   g.pexec = reinterpret_cast<WorkItem*>(b + L.pexec);
   g.prows = reinterpret_cast<SplitRow*>(b + L.prows);
-  g.short_rows = reinterpret_cast<int*>(b + L.short_rows);
+  g.short_rows = reinterpret_cast<WorkItem*>(b + L.short_rows);
   g.long_rows = reinterpret_cast<WorkItem*>(b + L.long_rows);
   g.counters = reinterpret_cast<int*>(b + L.counters);
   TFG_HIP(hipGetDevice(&g.device));

@@ -478,7 +478,7 @@ constexpr int kWlSingle = 4 * kWlThreads;
 __global__ __launch_bounds__(kWlThreads) void worklist_single(
     const int* __restrict__ rowptr, int64_t N, int chunk, int* __restrict__ counters,
     WorkItem* __restrict__ heavy, WorkItem* __restrict__ light, SplitRow* __restrict__ split,
-    int* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
+    WorkItem* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
   __shared__ int tmp[kWlThreads / kWave];
   int carry[kLists] = {0, 0, 0, 0, 0};
   for (int64_t r0 = 0; r0 < N; r0 += kWlThreads) {
@@ -493,7 +493,7 @@ __global__ __launch_bounds__(kWlThreads) void worklist_single(
     }
     if (r < N) {
       if (c[3])
-        short_rows[o[3]] = (int)r;
+        short_rows[o[3]] = WorkItem{(int)r, beg, beg + deg, -1};
       else if (c[4])
         long_rows[o[4]] = WorkItem{(int)r, beg, beg + deg, -1};
       if (c[2]) {
@@ -515,7 +515,7 @@ __global__ __launch_bounds__(kWlThreads) void worklist_single(
 __global__ __launch_bounds__(kWlThreads) void worklist_fill(
     const int* __restrict__ rowptr, int64_t N, int chunk, const int* __restrict__ block_sums,
     int nb, WorkItem* __restrict__ heavy, WorkItem* __restrict__ light,
-    SplitRow* __restrict__ split, int* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
+    SplitRow* __restrict__ split, WorkItem* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
   __shared__ int tmp[kWlThreads / kWave];
   const int64_t r = (int64_t)blockIdx.x * kWlThreads + threadIdx.x;
   int beg, deg, c[kLists], o[kLists];
@@ -525,7 +525,7 @@ __global__ __launch_bounds__(kWlThreads) void worklist_fill(
     o[i] = block_sums[i * nb + blockIdx.x] + block_excl_scan<kWlThreads / kWave>(c[i], tmp, nullptr);
   if (r >= N) return;
   if (c[3])
-    short_rows[o[3]] = (int)r;
+    short_rows[o[3]] = WorkItem{(int)r, beg, beg + deg, -1};
   else if (c[4])
     long_rows[o[4]] = WorkItem{(int)r, beg, beg + deg, -1};
   if (c[2]) {
@@ -795,7 +795,7 @@ GraphLayout graph_layout(int64_t E, int64_t N, int parts, int chunk) {
   L.split = take(sizeof(SplitRow) * std::max<int64_t>(L.cap_split, 1));
   L.pexec = take(sizeof(WorkItem) * L.cap_pexec);
   L.prows = take(parts > 1 ? sizeof(SplitRow) * N : 0);
-  L.short_rows = take(sizeof(int) * std::max<int64_t>(N, 1));
+  L.short_rows = take(sizeof(WorkItem) * std::max<int64_t>(N, 1));
   L.long_rows = take(sizeof(WorkItem) * std::max<int64_t>(N, 1));
   L.counters = take(sizeof(int) * 8);
   L.total = off;

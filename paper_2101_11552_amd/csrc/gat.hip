@@ -128,16 +128,13 @@ __device__ __forceinline__ float lane_score(const Scores& sc, int64_t c, int64_t
 // (a slot past the list) runs the same steps on no edges, so that the
 // shuffles of the dot-product scores see the whole wave.
 template <int V, bool DOT>
-__device__ __forceinline__ void gat_short_row(bool valid, int t, int sl, int LPS,
-                                              const int* __restrict__ rowptr,
+__device__ __forceinline__ void gat_short_row(bool valid, int t, int kb, int n, int sl, int LPS,
                                               const int* __restrict__ col,
                                               const int* __restrict__ perm, int H, int D,
                                               const Scores& S, const float* __restrict__ h,
                                               float* __restrict__ out,
                                               float* __restrict__ alpha_out) {
-  const int F = H * D;
-  const int kb = valid ? rowptr[t] : 0;
-  const int n = valid ? rowptr[t + 1] - kb : 0;  // 0 <= n <= kShortRow
+  const int F = H * D;  // 0 <= n <= kShortRow (0 when !valid)
   int c[kShortRow];
 #pragma unroll
   for (int j = 0; j < kShortRow; ++j) c[j] = j < n ? col[kb + j] : 0;
@@ -213,7 +210,7 @@ __device__ __forceinline__ void gat_short_row(bool valid, int t, int sl, int LPS
 // the sweep of gat_items, whose occupancy it would otherwise lower.
 template <int V, int SLOTS, bool DOT>
 __global__ __launch_bounds__(kBlock) void gat_short(
-    const int* __restrict__ short_rows, int n_short, const int* __restrict__ rowptr,
+    const WorkItem* __restrict__ short_rows, int n_short,
     const int* __restrict__ col, const int* __restrict__ perm, int H, int D, Scores S,
     const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out) {
   constexpr int LPS = kWave / SLOTS;
@@ -221,7 +218,8 @@ __global__ __launch_bounds__(kBlock) void gat_short(
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const int64_t i = wave * SLOTS + lane / LPS;
   const bool valid = i < n_short;
-  gat_short_row<V, DOT>(valid, valid ? short_rows[i] : 0, lane % LPS, LPS, rowptr, col, perm, H,
+  const WorkItem it = valid ? short_rows[i] : WorkItem{0, 0, 0, -1};
+  gat_short_row<V, DOT>(valid, it.row, it.kbeg, it.kend - it.kbeg, lane % LPS, LPS, col, perm, H,
                         D, S, h, out, alpha_out);
 }
 
@@ -465,7 +463,7 @@ void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
 #define TFG_GAT(SL)                                                                              \
   do {                                                                                           \
     if (g.n_short > 0)                                                                           \
-      gat_short<V, SL, DOT><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.rowptr, g.col,   \
+      gat_short<V, SL, DOT><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.col,             \
                                                      g.perm, a.H, a.D, a.S, a.h, a.out,          \
                                                      a.alpha_out);                               \
     if (waves > 0)                                                                               \

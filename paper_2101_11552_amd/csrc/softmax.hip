@@ -136,12 +136,12 @@ __global__ __launch_bounds__(kBlock) void edge_scores(const IdxT* __restrict__ s
 // takes row short_rows[i] and heads hh, hh + HP, ...; the row's scores are
 // loaded at once and kept in registers: maximum, then the sum of exp(s - m)
 // in double in graph order, then alpha. No cross-lane traffic.
-__device__ __forceinline__ void softmax_short_row(const int* __restrict__ rowptr,
-                                                  const int* __restrict__ perm, int t,
+__device__ __forceinline__ void softmax_short_row(const WorkItem& it,
+                                                  const int* __restrict__ perm,
                                                   const float* __restrict__ s, int H, int hh,
                                                   int HP, float* __restrict__ out,
                                                   float* __restrict__ out_csr) {
-  const int kb = rowptr[t], n = rowptr[t + 1] - kb;  // 0 <= n <= kShortRow
+  const int kb = it.kbeg, n = it.kend - it.kbeg;  // 0 <= n <= kShortRow
   int e[kShortRow];
 #pragma unroll
   for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? perm[kb + j] : 0;
@@ -171,9 +171,8 @@ __device__ __forceinline__ void softmax_short_row(const int* __restrict__ rowptr
 
 // Short rows, 64 / HP per wavefront (a kernel of its own: its registers would
 // lower the occupancy of the sweep below).
-__global__ __launch_bounds__(kBlock) void softmax_short(const int* __restrict__ short_rows,
+__global__ __launch_bounds__(kBlock) void softmax_short(const WorkItem* __restrict__ short_rows,
                                                         int n_short,
-                                                        const int* __restrict__ rowptr,
                                                         const int* __restrict__ perm,
                                                         const float* __restrict__ s, int H, int HP,
                                                         float* __restrict__ out,
@@ -181,7 +180,7 @@ __global__ __launch_bounds__(kBlock) void softmax_short(const int* __restrict__ 
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const int64_t i = wave * (kWave / HP) + lane / HP;
-  if (i < n_short) softmax_short_row(rowptr, perm, short_rows[i], s, H, lane % HP, HP, out, out_csr);
+  if (i < n_short) softmax_short_row(short_rows[i], perm, s, H, lane % HP, HP, out, out_csr);
 }
 
 // kSmSteps slot steps (positions k0, k0 + SL, ...) at a time: the edge ids,
@@ -369,7 +368,7 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
   const int64_t short_waves = (g.n_short + kWave / hp - 1) / (kWave / hp);
   if (short_waves > 0) {
     softmax_short<<<(unsigned)((short_waves + 3) / 4), kBlock, 0, s>>>(
-        g.short_rows, g.n_short, g.rowptr, g.perm, scores, H, hp, out, out_csr);
+        g.short_rows, g.n_short, g.perm, scores, H, hp, out, out_csr);
     TFG_LAUNCHED("softmax_short");
   }
   const int waves = g.n_heavy + g.n_long;

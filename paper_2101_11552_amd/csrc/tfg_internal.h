@@ -66,7 +66,7 @@ struct Graph {
   int n_heavy = 0, n_light = 0, n_split = 0;
   // the light rows again, by length: short (0..kShortRow edges, row ids,
   // several per wavefront) and the rest (whole-row items, one per wavefront)
-  int* short_rows = nullptr;
+  WorkItem* short_rows = nullptr;  // (row, kbeg, kend, -1): one load gives a row's extent
   WorkItem* long_rows = nullptr;
   int n_short = 0, n_long = 0;
   // part plan (P > 1): one item per (part, row) segment chunk, part-major
