@@ -152,13 +152,16 @@ NORM_SLICE_CASES = [
     (100_003, 300_000, False, np.int32, 1, True),  # three slices, N % 4 == 3 (tail)
     (100_003, 300_000, True, np.int32, 5, False),  # no loops: E' == E
     (90_001, 50_000, False, np.int64, 1, True),  # int64 ids, more nodes than edges
+    (100_003, 400_000, False, np.int32, 7, True),  # graph order by source part, 7 parts
+    (4000, 60_000, False, np.int64, 3, False),   # blocks of items straddling two parts
 ]
 
 
 @pytest.mark.parametrize("n,e,weighted,idx,parts,loops", NORM_SLICE_CASES)
 def test_gcn_norm_sliced_and_direct(tfg, orc, monkeypatch, n, e, weighted, idx, parts, loops):
-    # the LDS-sliced and the direct-gather weight kernels, each forced, both
-    # equal to the oracle bit for bit (COO and CSR order)
+    # the LDS-sliced, the direct-gather and (unit weights, several source
+    # parts) the part-range weight kernels, each forced, all equal to the
+    # oracle bit for bit (COO and CSR order)
     ei = graphgen.random_graph(23, n, e, hub=11, hub_edges=e // 10)
     w = (np.random.default_rng(5).uniform(0.1, 3.0, ei.shape[1]).astype(np.float32)
          if weighted else None)
@@ -166,8 +169,10 @@ def test_gcn_norm_sliced_and_direct(tfg, orc, monkeypatch, n, e, weighted, idx, 
     perm = orc.csr_by_target(oei, n, parts=parts)[2]
     eid = dev(ei.astype(idx))
     g = tfg.tfg_graph_create(eid, n, add_self_loops=loops, src_parts=parts)
-    for mode in ("1", "0"):
+    for mode, by_part in (("1", "0"), ("0", "0"), ("0", "1")):
         monkeypatch.setenv("TFG_NORM_SLICED", mode)
+        monkeypatch.setenv("TFG_NORM_PARTS", by_part)
+        mode = f"sliced={mode} parts={by_part}"
         r = tfg.tfg_gcn_norm(eid, n, edge_weight=None if w is None else dev(w),
                              add_self_loops=loops, graph=g)
         assert np.array_equal(host(r["edge_index"]), oei), mode
