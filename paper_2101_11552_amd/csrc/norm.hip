@@ -1,4 +1,5 @@
-// GCN normalisation on the CSR-by-target graph (gfx950):
+// GCN normalisation on the CSR-by-target graph (gfx950): the propagation
+// matrix of GCN (Sec. 2.2), computed once per graph and cached (Sec. 3):
 //   deg[t]  = sum of the weights entering t (loops included when appended)
 //   dinv[t] = deg > 0 ? 1 / sqrt(deg) : 0         (IEEE sqrt, IEEE divide)
 //   w'[e]   = (dinv[src] * w[e]) * dinv[tgt]       (float32, left to right)
