@@ -14,7 +14,8 @@ namespace {
 using namespace rows;
 
 // Combines the partial results of each split row in chunk order: sums with
-// four interleaved accumulators combined pairwise, maxima with the tie rule.
+// kFixAcc interleaved accumulators combined pairwise, maxima with the tie rule.
+constexpr int kFixAcc = 8;
 // Lanes cover V consecutive features each.
 template <bool MAX, int V>
 __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict__ split,
@@ -41,31 +42,38 @@ __global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict_
         if (argout != nullptr) argout[(int64_t)row * F + f + v] = a;
       }
     } else {
-      float a4[4][V];
+      // kFixAcc partial rows in flight, one accumulator each
+      float a4[kFixAcc][V];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kFixAcc; ++i)
 #pragma unroll
         for (int v = 0; v < V; ++v) a4[i][v] = 0.0f;
-      int j = 0;
-      for (; j + 4 <= nch; j += 4) {
+      for (int j = 0; j < nch; j += kFixAcc) {
+        float t[kFixAcc][V];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float t[V];
-          load_row<V>(part + (int64_t)(slot0 + j + i) * F + f, t);
+        for (int i = 0; i < kFixAcc; ++i) {
+          if (j + i < nch) {
+            load_row<V>(part + (int64_t)(slot0 + j + i) * F + f, t[i]);
+          } else {
 #pragma unroll
-          for (int v = 0; v < V; ++v) a4[i][v] += t[v];
+            for (int v = 0; v < V; ++v) t[i][v] = 0.0f;
+          }
         }
-      }
-      for (int i = 0; j < nch; ++j, ++i) {
-        float t[V];
-        load_row<V>(part + (int64_t)(slot0 + j) * F + f, t);
 #pragma unroll
-        for (int v = 0; v < V; ++v) a4[i][v] += t[v];
+        for (int i = 0; i < kFixAcc; ++i)
+#pragma unroll
+          for (int v = 0; v < V; ++v) a4[i][v] += t[i][v];
       }
+#pragma unroll
+      for (int step = 1; step < kFixAcc; step <<= 1)
+#pragma unroll
+        for (int i = 0; i + step < kFixAcc; i += 2 * step)
+#pragma unroll
+          for (int v = 0; v < V; ++v) a4[i][v] += a4[i + step][v];
       float s[V];
 #pragma unroll
       for (int v = 0; v < V; ++v) {
-        s[v] = (a4[0][v] + a4[1][v]) + (a4[2][v] + a4[3][v]);
+        s[v] = a4[0][v];
         if (mean && deg > 0) s[v] = s[v] / (float)deg;
       }
       apply_epilogue<V>(ep, row, f, s);
