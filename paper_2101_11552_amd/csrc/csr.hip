@@ -726,16 +726,16 @@ int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream
   return TFG_OK;
 }
 
-// Eight ints of pinned host memory per calling thread, allocated on first use
-// and kept for the life of the process, for the few counters that the
-// synchronising calls read back: a copy into pinned memory goes straight to
-// the host, without the runtime's staging copy (a graph build of 13,264 edges:
-// 0.165 -> 0.137 ms). NULL if the allocation fails (the caller then reads into
-// pageable memory).
+// Eight ints of pinned host memory per calling thread (portable: usable with
+// any device's stream), allocated on first use and kept for the life of the
+// process, for the few counters that the synchronising calls read back: a
+// copy into pinned memory goes straight to the host, without the runtime's
+// staging copy (a graph build of 13,264 edges: 0.165 -> 0.137 ms). NULL if
+// the allocation fails (the caller then reads into pageable memory).
 int* readback_buffer() {
   thread_local int* p = [] {
     void* q = nullptr;
-    return hipHostMalloc(&q, sizeof(int) * 8, hipHostMallocDefault) == hipSuccess
+    return hipHostMalloc(&q, sizeof(int) * 8, hipHostMallocPortable) == hipSuccess
                ? static_cast<int*>(q)
                : nullptr;
   }();
