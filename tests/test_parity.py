@@ -597,3 +597,53 @@ def test_gat_dot_rejects_shapes(tfg):
     x = dev(np.ones((4, 12), np.float32))
     with pytest.raises(ValueError):  # D = 3 is not a power of two
         tfg.tfg_gat_dot_aggregate(g, x, x, x, 4)
+
+
+_CHUNK_SCRIPT = r"""
+import os
+import sys
+import numpy as np
+sys.path.insert(0, sys.argv[1])
+sys.path.insert(0, sys.argv[1] + "/tests")
+import torch
+import graphgen
+import oracle
+import paper_2101_11552_amd as tfg
+from test_parity import assert_scaled, same_bits
+n, parts = 5000, 4
+ei = graphgen.random_graph(41, n, 150_000, hub=9, hub_edges=20_000)
+eid = torch.from_numpy(ei.astype(np.int32)).cuda()
+g = tfg.tfg_graph_create(eid, n, add_self_loops=True, src_parts=parts)
+assert g.info()["src_parts"] == parts
+oei, ow, _ = oracle.gcn_norm(ei, n)
+perm = oracle.csr_by_target(oei, n, parts=parts)[2]
+x = graphgen.features(41, n, 32)
+for by_part in ("1", "0"):
+    os.environ["TFG_NORM_PARTS"] = by_part
+    r = tfg.tfg_gcn_norm(eid, n, graph=g)
+    assert same_bits(r["edge_weight_csr"].cpu().numpy(), ow[perm]), by_part
+    assert same_bits(r["edge_weight"].cpu().numpy(), ow), by_part
+for plan in ("1", "0"):
+    os.environ["TFG_PART_PLAN"] = plan
+    y = tfg.tfg_aggregate(None, torch.from_numpy(x).cuda(), n, "sum",
+                          edge_weight=r["edge_weight_csr"], weight_order="csr", graph=g)
+    ref, S = oracle.aggregate(oei, x, n, "sum", edge_weight=ow)
+    assert_scaled(y.cpu().numpy(), ref, S, what="chunk knob, plan " + plan)
+print("chunk knob ok")
+"""
+
+
+def test_row_chunk_knob_in_a_fresh_process(tfg):
+    """TFG_ROW_CHUNK is read once per process, so a longer work item (300
+    edges, beyond two rounds of lanes) runs in a child process: normalised
+    weights in both orders (part-range kernel on and off) and the sum
+    aggregation (both plans) against the oracle."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, TFG_ROW_CHUNK="300", TFG_NORM_SLICED="0")
+    r = subprocess.run([sys.executable, "-c", _CHUNK_SCRIPT, root], env=env,
+                       capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
+    assert "chunk knob ok" in r.stdout
