@@ -99,7 +99,7 @@ def cpu_baseline(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
     return {"value": round(e_total / dt / 1e9, 6), "unit": "GE/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n_edges} of the {ei.shape[1]} edges (+{n} self-loops), all "
                       f"{n} nodes, F={x.shape[1]}: gcn_norm + sum aggregation, {dt:.1f} s",
-            "cpu_model": cpu_model()}
+            "cpu_model": cpu_model(), "nproc": os.cpu_count()}
 
 
 def host_threads() -> int:
@@ -157,7 +157,7 @@ def cpu_baseline_threads(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
             "kind": "oracle",
             "sample": f"the single-thread sample, aggregation rows split over {threads} "
                       f"threads, {dt:.1f} s",
-            "cpu_model": cpu_model()}
+            "cpu_model": cpu_model(), "nproc": os.cpu_count()}
 
 
 def _timed(torch, fn, reps: int, warm: int = 2) -> float:
