@@ -52,41 +52,37 @@ __global__ __launch_bounds__(kBlock) void degree_weighted(const int* __restrict_
   }
 }
 
-// CSR order: one wavefront per aggregation work item (row or row chunk); each
-// lane handles four positions per step with their loads issued together.
-__global__ __launch_bounds__(kBlock) void weights_csr(const WorkItem* __restrict__ heavy,
-                                                      int n_heavy,
-                                                      const WorkItem* __restrict__ light,
-                                                      int n_light, const int* __restrict__ col,
+// CSR order, one position per thread (four per thread, strided by the block):
+// the target comes from the stored sort key (target * parts + part), so the
+// source's and the target's dinv are gathered side by side, with no work list.
+template <bool HAS_W>
+__global__ __launch_bounds__(kBlock) void weights_csr(const int* __restrict__ key, int parts,
+                                                      const int* __restrict__ col,
                                                       const int* __restrict__ perm,
                                                       const float* __restrict__ w, int64_t E_in,
-                                                      const float* __restrict__ dinv,
+                                                      int64_t E, const float* __restrict__ dinv,
                                                       float* __restrict__ out) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
-  if (wid >= n_heavy + n_light) return;
-  const int lane = threadIdx.x & (kWave - 1);
-  const WorkItem* it = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
-  const int row = uniform(it->row), kb = uniform(it->kbeg), ke = uniform(it->kend);
-  const float dt = dinv[row];
-  for (int k0 = kb + lane; k0 < ke; k0 += 4 * kWave) {
-    int c[4];
-    float we[4], ds[4];
+  const int64_t b = (int64_t)blockIdx.x * (4 * kBlock) + threadIdx.x;
+  int c[4], t[4], e[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int k = k0 + j * kWave < ke ? k0 + j * kWave : k0;
-      c[j] = col[k];
-      we[j] = w ? edge_w(w, E_in, perm[k]) : 1.0f;
-    }
+  for (int j = 0; j < 4; ++j) {
+    const int64_t k = b + j * kBlock;
+    const bool ok = k < E;
+    c[j] = ok ? col[k] : 0;
+    t[j] = ok ? key[k] : 0;
+    e[j] = (HAS_W && ok) ? perm[k] : 0;
+  }
+  float we[4], ds[4], dt[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) ds[j] = dinv[c[j]];
+  for (int j = 0; j < 4; ++j) {
+    we[j] = HAS_W ? edge_w(w, E_in, e[j]) : 1.0f;
+    ds[j] = dinv[c[j]];
+    dt[j] = dinv[parts == 1 ? t[j] : t[j] / parts];
+  }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int k = k0 + j * kWave;
-      if (k < ke) {
-        const float a = ds[j] * we[j];
-        out[k] = a * dt;
-      }
-    }
+  for (int j = 0; j < 4; ++j) {
+    const int64_t k = b + j * kBlock;
+    if (k < E) out[k] = (ds[j] * we[j]) * dt[j];  // (dinv[s] * w) * dinv[t]
   }
 }
 
@@ -466,7 +462,6 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                                                                  g.E_in, g.N, out_deg, dinv);
   }
   TFG_LAUNCHED("gcn degree");
-  const int waves = g.n_heavy + g.n_light;
   if (out_w_csr && g.E > 0 && edge_weight == nullptr && use_part_ranges(g)) {
     weights_csr_parts<<<(unsigned)((g.n_pexec + kPartItems - 1) / kPartItems), kSlThreads, 0, s>>>(
         g.pexec, g.n_pexec, (int)g.part_rows, g.col, g.N, dinv, out_w_csr);
@@ -482,10 +477,14 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                                                            nullptr, g.E_in, g.E, g.N, dinv,
                                                            out_w_csr);
     TFG_LAUNCHED("gcn weights (CSR order, sliced)");
-  } else if (out_w_csr && waves > 0) {
-    weights_csr<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.light, g.n_light, g.col, g.perm, edge_weight, g.E_in, dinv,
-        out_w_csr);
+  } else if (out_w_csr && g.E > 0) {
+    const unsigned nb = (unsigned)((g.E + 4 * kBlock - 1) / (4 * kBlock));
+    if (edge_weight)
+      weights_csr<true><<<nb, kBlock, 0, s>>>(g.key, g.parts, g.col, g.perm, edge_weight, g.E_in,
+                                              g.E, dinv, out_w_csr);
+    else
+      weights_csr<false><<<nb, kBlock, 0, s>>>(g.key, g.parts, g.col, g.perm, nullptr, g.E_in,
+                                               g.E, dinv, out_w_csr);
     TFG_LAUNCHED("gcn weights (CSR order)");
   }
   if ((out_w || out_edge_index) && g.E > 0) {
