@@ -29,6 +29,8 @@ constexpr int kSortThreads = 1024;                    // 16 waves
 constexpr int kSortItems = 8;                         // items per thread
 constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 edges per tile
 constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kUpThreads = 512;                       // counting pass: threads per tile
+constexpr int kUpItems = kSortTile / kUpThreads;
 constexpr int kMaxDigitBits = 8;
 constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 512
 constexpr int kXcds = 8;
@@ -182,7 +184,7 @@ int64_t scan_tiles(int64_t n) { return (n + kScanTile - 1) / kScanTile; }
 // every (digit, tile) its output offset. The first pass also validates the
 // ids.
 template <bool FIRST, typename IdxT>
-__global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__ src,
+__global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ src,
                                                         const IdxT* __restrict__ tgt, KeyMap m,
                                                         const int* __restrict__ keys, int64_t E,
                                                         int shift, int dbits,
@@ -190,15 +192,15 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
                                                         int* __restrict__ err) {
   // one histogram per wave: equal digits (a hub target's edges) then contend
   // only within a wave
-  __shared__ int h[kSortWaves][kMaxRadix];
+  __shared__ int h[kUpThreads / kWave][kMaxRadix];
   const int radix = 1 << dbits;
   const int wave = threadIdx.x / kWave;
   for (int d = lane_id(); d < radix; d += kWave) h[wave][d] = 0;
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
-  IdxT rs[kSortItems], rt[kSortItems];
+  IdxT rs[kUpItems], rt[kUpItems];
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
+  for (int i = 0; i < kUpItems; ++i) {
+    const int64_t e = base + (int64_t)i * kUpThreads + threadIdx.x;
     if constexpr (FIRST) {
       load_raw(src, tgt, m.E_in, e, &rs[i], &rt[i]);
     } else {
@@ -208,8 +210,8 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
   }
   bool any_bad = false;
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t e = base + (int64_t)i * kSortThreads + threadIdx.x;
+  for (int i = 0; i < kUpItems; ++i) {
+    const int64_t e = base + (int64_t)i * kUpThreads + threadIdx.x;
     int k = (int)rt[i];
     if constexpr (FIRST) {
       int s;
@@ -221,10 +223,10 @@ __global__ __launch_bounds__(kSortThreads) void upsweep(const IdxT* __restrict__
   }
   if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += kSortThreads) {
+  for (int d = threadIdx.x; d < radix; d += kUpThreads) {
     int c = 0;
 #pragma unroll
-    for (int w = 0; w < kSortWaves; ++w) c += h[w][d];
+    for (int w = 0; w < kUpThreads / kWave; ++w) c += h[w][d];
     hist[(int64_t)d * gridDim.x + blockIdx.x] = c;
   }
 }
@@ -651,10 +653,10 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
       const int shift = pass * p.dbits;
       const bool first = pass == 0, last = pass == p.passes - 1;
       if (first)
-        upsweep<true, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, nullptr, E, shift, p.dbits,
+        upsweep<true, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, nullptr, E, shift, p.dbits,
                                                         hist, err);
       else
-        upsweep<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, shift,
+        upsweep<false, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, shift,
                                                          p.dbits, hist, err);
       const int rc = exclusive_scan(hist, hist, radix * p.ntiles, sums, s);
       if (rc) return rc;
