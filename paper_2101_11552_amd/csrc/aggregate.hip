@@ -181,7 +181,7 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   }
   const int waves = a.n_heavy + a.n_light;
   if (waves > 0) {
-    dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
+    dim3 grid((unsigned)((waves + kRowBlock / kWave - 1) / (kRowBlock / kWave)));
     if (mask != nullptr)
       dispatch_masked(part_plan, heads, vec, slots, grid, s, a);
     else if (part_plan)

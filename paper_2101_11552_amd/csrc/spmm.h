@@ -128,8 +128,11 @@ constexpr int unroll_for() {
 // MASK (sum only): element c of the gathered row x[col_k] counts only where
 // mask[col_k, c] equals the edge id perm[k] (the gradient of a max
 // aggregation, gathered over the transposed graph).
+// Threads per block of the row kernel (wavefronts are independent).
+constexpr int kRowBlock = 256;
+
 template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT, bool MASK>
-__global__ __launch_bounds__(kBlock) void spmm_rows(
+__global__ __launch_bounds__(kRowBlock) void spmm_rows(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
     int n_light, const int* __restrict__ col, const int* __restrict__ perm,
     const float* __restrict__ w, int w_by_perm, int H, int per_head, const float* __restrict__ x,
@@ -139,7 +142,7 @@ __global__ __launch_bounds__(kBlock) void spmm_rows(
   constexpr int LPS = kWave / SLOTS;  // lanes per edge slot
   constexpr int FC = LPS * V;         // feature columns per pass
   constexpr int U = unroll_for<SLOTS, SHORT>();
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kRowBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy + n_light) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int slot = lane / LPS, sl = lane % LPS;
@@ -304,7 +307,7 @@ struct RowArgs {
 
 template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT, bool MASK>
 void launch_rows(dim3 grid, hipStream_t s, const RowArgs& a) {
-  spmm_rows<V, SLOTS, MAX, HEADS, SHORT, MASK><<<grid, dim3(kBlock), 0, s>>>(
+  spmm_rows<V, SLOTS, MAX, HEADS, SHORT, MASK><<<grid, dim3(kRowBlock), 0, s>>>(
       a.heavy, a.n_heavy, a.light, a.n_light, a.col, a.perm, a.w, a.w_by_perm, a.H, a.per_head,
       a.x, a.ldx, a.mask, a.F, a.mean, a.out, a.argout, a.part, a.part_arg, a.ep);
 }
