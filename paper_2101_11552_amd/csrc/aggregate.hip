@@ -18,12 +18,12 @@ using namespace rows;
 constexpr int kFixAcc = 8;
 // Lanes cover V consecutive features each.
 template <bool MAX, int V>
-__global__ __launch_bounds__(kBlock) void fixup_rows(const SplitRow* __restrict__ split,
+__global__ __launch_bounds__(kItemBlock) void fixup_rows(const SplitRow* __restrict__ split,
                                                      int n_split, const float* __restrict__ part,
                                                      const int* __restrict__ part_arg, int F,
                                                      int mean, float* __restrict__ out,
                                                      int* __restrict__ argout, Epilogue ep) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_split) return;
   const int lane = threadIdx.x & (kWave - 1);
   const SplitRow* sr = split + wid;
@@ -191,17 +191,17 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
     TFG_LAUNCHED("spmm_rows");
   }
   if (n_rows > 0) {
-    dim3 fgrid((unsigned)((n_rows + kBlock / kWave - 1) / (kBlock / kWave)));
+    dim3 fgrid((unsigned)((n_rows + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
     // partials are dense [slot, F] rows: 16-byte accesses when F is a multiple of 4
     const bool f4 = F % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
     if (mx)
-      fixup_rows<true, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+      fixup_rows<true, 1><<<fgrid, dim3(kItemBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
                                                          a.mean, out, argmax, a.ep);
     else if (f4)
-      fixup_rows<false, 4><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+      fixup_rows<false, 4><<<fgrid, dim3(kItemBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
                                                           a.mean, out, argmax, a.ep);
     else
-      fixup_rows<false, 1><<<fgrid, dim3(kBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
+      fixup_rows<false, 1><<<fgrid, dim3(kItemBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
                                                           a.mean, out, argmax, a.ep);
     TFG_LAUNCHED("fixup_rows");
   }

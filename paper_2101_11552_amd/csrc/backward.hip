@@ -81,7 +81,7 @@ __device__ __forceinline__ float transpose_sum(float (&p)[U], int sl) {
 // transpose_sum; with several heads they are summed over the G lanes of each
 // head with a shift-down tree (the head's first lane holds the result).
 template <int V, int SLOTS, int MODE, bool WHOLE>
-__global__ __launch_bounds__(kBlock) void edge_grad_rows(
+__global__ __launch_bounds__(kItemBlock) void edge_grad_rows(
     const WorkItem* __restrict__ items, int n_items, const int* __restrict__ rowptr,
     const int* __restrict__ col, const int* __restrict__ perm, const float* __restrict__ x,
     int64_t ldx, const float* __restrict__ dy, const int* __restrict__ arg, int F, int H, int G,
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(kBlock) void edge_grad_rows(
   // kernel within 64 VGPRs (8 waves per SIMD); 8 would need 79
   constexpr int UMAX = WHOLE ? 4 : 8;
   constexpr int U = SLOTS * UMAX <= kWave ? UMAX : kWave / SLOTS;
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_items) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int slot = lane / LPS, sl = lane % LPS;
@@ -336,7 +336,7 @@ void launch_edge_grad_slots(int slots, dim3 grid, hipStream_t s, const WorkItem*
                             const float* dy, const int* arg, int F, int H, int G, float* dw,
                             int by_perm, float scale) {
 #define TFG_EG(SL)                                                                      \
-  edge_grad_rows<V, SL, MODE, WHOLE><<<grid, kBlock, 0, s>>>(                           \
+  edge_grad_rows<V, SL, MODE, WHOLE><<<grid, kItemBlock, 0, s>>>(                       \
       items, n_items, g.rowptr, g.col, g.perm, x, ldx, dy, arg, F, H, G, dw, by_perm, scale)
   switch (slots) {
     case 1: TFG_EG(1); break;
@@ -373,7 +373,7 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
   // keeps its long-row chunks and its whole rows in two lists)
   auto run = [&](const WorkItem* it, int n) {
     if (n <= 0) return;
-    dim3 grid((unsigned)((n + kBlock / kWave - 1) / (kBlock / kWave)));
+    dim3 grid((unsigned)((n + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
     const int G = D / vec;
     if (H == 1) {
       if (vec == 4)

@@ -125,11 +125,15 @@ constexpr int unroll_for() {
   return SHORT && u > 4 ? 4 : u;
 }
 
+// Threads per block of the row kernel: one wavefront. Its wavefronts are
+// independent, and single-wavefront blocks let a CU start the next item as
+// soon as any wavefront ends (aggregation on the power-law graph: 3.60 ms,
+// against 3.65 / 3.71 / 4.10 / 4.98 ms with 128- to 1024-thread blocks).
+constexpr int kRowBlock = kItemBlock;
+
 // MASK (sum only): element c of the gathered row x[col_k] counts only where
 // mask[col_k, c] equals the edge id perm[k] (the gradient of a max
 // aggregation, gathered over the transposed graph).
-// Threads per block of the row kernel (wavefronts are independent).
-constexpr int kRowBlock = 256;
 
 template <int V, int SLOTS, bool MAX, bool HEADS, bool SHORT, bool MASK>
 __global__ __launch_bounds__(kRowBlock) void spmm_rows(

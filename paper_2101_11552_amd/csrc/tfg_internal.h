@@ -14,6 +14,9 @@ namespace tfg {
 
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per block for most kernels (4 waves)
+// Kernels whose wavefronts each take their own work items run one wavefront
+// per block, so that a CU starts the next item as soon as any wavefront ends.
+constexpr int kItemBlock = 64;
 constexpr int kDefaultChunk = 128; // max edges per work item of the row plan
 constexpr int kMaxChunk = 1 << 16;  // largest chunk the tuning knob may set
 constexpr int kShortRow = 8;       // rows of at most this many edges are "short"
