@@ -14,7 +14,7 @@ namespace rows {
 namespace {
 
 template <int V, int SLOTS, bool MAX>
-__global__ __launch_bounds__(kBlock) void spmm_short(
+__global__ __launch_bounds__(kItemBlock) void spmm_short(
     const WorkItem* __restrict__ short_rows, int n_short, const int* __restrict__ col,
     const int* __restrict__ perm, const float* __restrict__ w,
     int w_by_perm, const float* __restrict__ x, int64_t ldx, int F, int mean,
@@ -96,8 +96,8 @@ __global__ __launch_bounds__(kBlock) void spmm_short(
 template <int V, int SLOTS, bool MAX>
 void run(const Graph& g, const RowArgs& a, hipStream_t s) {
   const int64_t waves = (g.n_short + SLOTS - 1) / SLOTS;
-  const dim3 grid((unsigned)((waves + kBlock / kWave - 1) / (kBlock / kWave)));
-  spmm_short<V, SLOTS, MAX><<<grid, kBlock, 0, s>>>(g.short_rows, g.n_short, a.col,
+  const dim3 grid((unsigned)((waves + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
+  spmm_short<V, SLOTS, MAX><<<grid, kItemBlock, 0, s>>>(g.short_rows, g.n_short, a.col,
                                                     a.perm, a.w, a.w_by_perm, a.x, a.ldx, a.F,
                                                     a.mean, a.out, a.argout, a.ep);
 }

@@ -259,12 +259,12 @@ __global__ __launch_bounds__(kBlock) void to_graph_order(const int* __restrict__
 // softmax_grad_merge adds the chunks of each long row in chunk order and
 // softmax_grad_write writes their ds. (A bucket of short rows, as the softmax
 // has, measured no faster here: the sweep has no exponentials.)
-__global__ __launch_bounds__(kBlock) void softmax_grad_items(
+__global__ __launch_bounds__(kItemBlock) void softmax_grad_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
     int n_light, const int* __restrict__ perm, const float* __restrict__ alpha,
     const float* __restrict__ da, int H, int HP, float* __restrict__ ds,
     double* __restrict__ pdot) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy + n_light) return;
   const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
   const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
@@ -308,11 +308,11 @@ __global__ __launch_bounds__(kBlock) void softmax_grad_merge(const SplitRow* __r
   for (int j = 0; j < nch; ++j) pdot[(int64_t)(s0 + j) * H + h] = dot;
 }
 
-__global__ __launch_bounds__(kBlock) void softmax_grad_write(
+__global__ __launch_bounds__(kItemBlock) void softmax_grad_write(
     const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
     const float* __restrict__ alpha, const float* __restrict__ da, int H, int HP,
     const double* __restrict__ pdot, float* __restrict__ ds) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
   const WorkItem* itp = heavy + wid;
   const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
@@ -511,7 +511,7 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
       align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
   const int waves = g.n_heavy + g.n_light;
   if (waves > 0) {
-    softmax_grad_items<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
+    softmax_grad_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.heavy, g.n_heavy, g.light, g.n_light, g.perm, alpha, dalpha, H, hp, ds, pdot);
     TFG_LAUNCHED("softmax_grad_items");
   }
@@ -519,7 +519,7 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
     const int64_t n = (int64_t)g.n_split * H;
     softmax_grad_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split,
                                                                                g.n_split, H, pdot);
-    softmax_grad_write<<<(unsigned)((g.n_heavy + 3) / 4), kBlock, 0, s>>>(
+    softmax_grad_write<<<(unsigned)((g.n_heavy + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.heavy, g.n_heavy, g.perm, alpha, dalpha, H, hp, pdot, ds);
     TFG_LAUNCHED("softmax_grad_merge / softmax_grad_write");
   }

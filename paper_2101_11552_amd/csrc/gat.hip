@@ -209,7 +209,7 @@ __device__ __forceinline__ void gat_short_row(bool valid, int t, int kb, int n, 
 // of its own: holding a whole short row in registers takes more of them than
 // the sweep of gat_items, whose occupancy it would otherwise lower.
 template <int V, int SLOTS, bool DOT>
-__global__ __launch_bounds__(kBlock) void gat_short(
+__global__ __launch_bounds__(kItemBlock) void gat_short(
     const WorkItem* __restrict__ short_rows, int n_short,
     const int* __restrict__ col, const int* __restrict__ perm, int H, int D, Scores S,
     const float* __restrict__ h, float* __restrict__ out, float* __restrict__ alpha_out) {
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kBlock) void gat_short(
 // Wavefronts [0, n_heavy) take the chunks of long rows, [n_heavy, n_heavy +
 // n_long) one other light row each, with the running-triple sweep.
 template <int V, int SLOTS, bool DOT>
-__global__ __launch_bounds__(kBlock) void gat_items(
+__global__ __launch_bounds__(kItemBlock) void gat_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ col,
     const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ h,
@@ -235,10 +235,10 @@ __global__ __launch_bounds__(kBlock) void gat_items(
   constexpr int LPS = kWave / SLOTS;
   constexpr int FC = LPS * V;
   constexpr int U = SLOTS * 4 <= kWave ? 4 : kWave / SLOTS;
-  __shared__ float s_max[kBlock / kWave][kMaxHeads];
-  __shared__ double s_den[kBlock / kWave][kMaxHeads];
+  __shared__ float s_max[kItemBlock / kWave][kMaxHeads];
+  __shared__ double s_den[kItemBlock / kWave][kMaxHeads];
   const int wv = threadIdx.x / kWave;
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + wv);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + wv);
   if (wid >= n_heavy + n_long) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int slot = lane / LPS, sl = lane % LPS;
@@ -421,11 +421,11 @@ __global__ __launch_bounds__(kBlock) void gat_merge(const SplitRow* __restrict__
 
 // Attention coefficients of the chunks of long rows, from their row's (m, d).
 template <bool DOT>
-__global__ __launch_bounds__(kBlock) void gat_alpha_chunks(
+__global__ __launch_bounds__(kItemBlock) void gat_alpha_chunks(
     const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ col,
     const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ pm,
     const double* __restrict__ pd, float* __restrict__ alpha_out) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
   const WorkItem* itp = heavy + wid;
   const int row = uniform(itp->row), kb = uniform(itp->kbeg), ke = uniform(itp->kend);
@@ -459,18 +459,18 @@ void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
   const Graph& g = *a.g;
   const int waves = g.n_heavy + g.n_long;
   const int64_t short_waves = (g.n_short + slots - 1) / slots;
-  const dim3 sgrid((unsigned)((short_waves + kBlock / kWave - 1) / (kBlock / kWave)));
+  const dim3 sgrid((unsigned)((short_waves + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
 #define TFG_GAT(SL)                                                                              \
   do {                                                                                           \
     if (g.n_short > 0)                                                                           \
-      gat_short<V, SL, DOT><<<sgrid, kBlock, 0, s>>>(g.short_rows, g.n_short, g.col,             \
+      gat_short<V, SL, DOT><<<sgrid, kItemBlock, 0, s>>>(g.short_rows, g.n_short, g.col,         \
                                                      g.perm, a.H, a.D, a.S, a.h, a.out,          \
                                                      a.alpha_out);                               \
     if (waves > 0)                                                                               \
-      gat_items<V, SL, DOT><<<grid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows, g.n_long,   \
-                                                    g.rowptr, g.col, g.perm, a.H, a.D, a.HP, a.S, \
-                                                    a.h, a.out, a.alpha_out, a.pacc, a.pm,       \
-                                                    a.pd);                                       \
+      gat_items<V, SL, DOT><<<grid, kItemBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows,         \
+                                                    g.n_long, g.rowptr, g.col, g.perm, a.H,      \
+                                                    a.D, a.HP, a.S, a.h, a.out, a.alpha_out,     \
+                                                    a.pacc, a.pm, a.pd);                         \
   } while (0)
   switch (slots) {
     case 1: TFG_GAT(1); break;
@@ -537,7 +537,7 @@ int run_attention(const Graph& g, GatArgs& a, int vec, hipStream_t s) {
   a.HP = hp;
   const int waves = g.n_heavy + g.n_long;
   if (waves > 0 || g.n_short > 0) {
-    dim3 grid((unsigned)((std::max(waves, 1) + kBlock / kWave - 1) / (kBlock / kWave)));
+    dim3 grid((unsigned)((std::max(waves, 1) + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
     if (vec == 4)
       launch_slots<4, DOT>(slots, grid, s, a);
     else if (vec == 2)
@@ -552,8 +552,8 @@ int run_attention(const Graph& g, GatArgs& a, int vec, hipStream_t s) {
                                        a.alpha_out != nullptr ? 1 : 0);
     TFG_LAUNCHED("gat_merge");
     if (a.alpha_out != nullptr) {
-      dim3 agrid((unsigned)((g.n_heavy + kBlock / kWave - 1) / (kBlock / kWave)));
-      gat_alpha_chunks<DOT><<<agrid, kBlock, 0, s>>>(g.heavy, g.n_heavy, g.col, g.perm, H, D, hp,
+      dim3 agrid((unsigned)((g.n_heavy + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
+      gat_alpha_chunks<DOT><<<agrid, kItemBlock, 0, s>>>(g.heavy, g.n_heavy, g.col, g.perm, H, D, hp,
                                                      a.S, a.pm, a.pd, a.alpha_out);
       TFG_LAUNCHED("gat_alpha_chunks");
     }

@@ -69,14 +69,14 @@ __device__ __forceinline__ void max_combine(float& v, int& a, float vb, int ab) 
 // One wavefront per graph; SLOTS node slots of 64/SLOTS lanes, U nodes in
 // flight per slot, pairwise combination (as in the aggregation kernel).
 template <int V, int SLOTS, bool MAX>
-__global__ __launch_bounds__(kBlock) void pool_rows(const float* __restrict__ x, int64_t ldx,
+__global__ __launch_bounds__(kItemBlock) void pool_rows(const float* __restrict__ x, int64_t ldx,
                                                     int F, const int* __restrict__ goff, int64_t G,
                                                     int64_t Nb, int mean, float* __restrict__ out,
                                                     int* __restrict__ argout) {
   constexpr int LPS = kWave / SLOTS;
   constexpr int FC = LPS * V;
   constexpr int U = SLOTS * 8 <= kWave ? 8 : kWave / SLOTS;
-  const int64_t g = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+  const int64_t g = (int64_t)blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave;
   if (g >= G) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int slot = lane / LPS, sl = lane % LPS;
@@ -165,11 +165,11 @@ template <int V, bool MAX>
 void launch_pool_slots(int slots, dim3 grid, hipStream_t s, const float* x, int64_t ldx, int F,
                        const int* goff, int64_t G, int64_t Nb, int mean, float* out, int* argout) {
   switch (slots) {
-    case 1: pool_rows<V, 1, MAX><<<grid, kBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
-    case 2: pool_rows<V, 2, MAX><<<grid, kBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
-    case 4: pool_rows<V, 4, MAX><<<grid, kBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
-    case 8: pool_rows<V, 8, MAX><<<grid, kBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
-    default: pool_rows<V, 16, MAX><<<grid, kBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
+    case 1: pool_rows<V, 1, MAX><<<grid, kItemBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
+    case 2: pool_rows<V, 2, MAX><<<grid, kItemBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
+    case 4: pool_rows<V, 4, MAX><<<grid, kItemBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
+    case 8: pool_rows<V, 8, MAX><<<grid, kItemBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
+    default: pool_rows<V, 16, MAX><<<grid, kItemBlock, 0, s>>>(x, ldx, F, goff, G, Nb, mean, out, argout); break;
   }
 }
 
@@ -290,7 +290,7 @@ int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx, cons
   int p2 = 1;
   while (p2 < lanes) p2 <<= 1;
   const int slots = std::min(kWave / p2, 16);
-  dim3 grid((unsigned)((G + 3) / 4));
+  dim3 grid((unsigned)((G + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
   if (reduce == TFG_MAX)
     launch_pool_vec<true>(vec, slots, grid, s, x, ldx, (int)F, goff, G, Nb, 0, out, argmax);
   else

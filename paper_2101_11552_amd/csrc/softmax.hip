@@ -171,7 +171,7 @@ __device__ __forceinline__ void softmax_short_row(const WorkItem& it,
 
 // Short rows, 64 / HP per wavefront (a kernel of its own: its registers would
 // lower the occupancy of the sweep below).
-__global__ __launch_bounds__(kBlock) void softmax_short(const WorkItem* __restrict__ short_rows,
+__global__ __launch_bounds__(kItemBlock) void softmax_short(const WorkItem* __restrict__ short_rows,
                                                         int n_short,
                                                         const int* __restrict__ perm,
                                                         const float* __restrict__ s, int H, int HP,
@@ -208,12 +208,12 @@ __device__ __forceinline__ void load_steps(const int* __restrict__ perm,
 // head ends with the same pair). A whole row then writes alpha = exp(s - m) /
 // d; a chunk stores its pair, softmax_merge combines the chunks of each long
 // row in order and softmax_write writes their outputs.
-__global__ __launch_bounds__(kBlock) void softmax_items(
+__global__ __launch_bounds__(kItemBlock) void softmax_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ perm,
     const float* __restrict__ s, int H, int HP, float* __restrict__ out,
     float* __restrict__ out_csr, float* __restrict__ pm, double* __restrict__ pd) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy + n_long) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
@@ -288,11 +288,11 @@ __global__ __launch_bounds__(kBlock) void softmax_merge(const SplitRow* __restri
 }
 
 // The outputs of the chunks of long rows, from their row's pair.
-__global__ __launch_bounds__(kBlock) void softmax_write(
+__global__ __launch_bounds__(kItemBlock) void softmax_write(
     const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
     const float* __restrict__ s, int H, int HP, const float* __restrict__ pm,
     const double* __restrict__ pd, float* __restrict__ out, float* __restrict__ out_csr) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
   const WorkItem* itp = heavy + wid;
   const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
@@ -367,13 +367,13 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
       static_cast<char*>(ws) + align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
   const int64_t short_waves = (g.n_short + kWave / hp - 1) / (kWave / hp);
   if (short_waves > 0) {
-    softmax_short<<<(unsigned)((short_waves + 3) / 4), kBlock, 0, s>>>(
+    softmax_short<<<(unsigned)((short_waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.short_rows, g.n_short, g.perm, scores, H, hp, out, out_csr);
     TFG_LAUNCHED("softmax_short");
   }
   const int waves = g.n_heavy + g.n_long;
   if (waves > 0) {
-    softmax_items<<<(unsigned)((waves + 3) / 4), kBlock, 0, s>>>(
+    softmax_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.heavy, g.n_heavy, g.long_rows, g.n_long, g.rowptr, g.perm, scores, H, hp, out, out_csr,
         pm, pd);
     TFG_LAUNCHED("softmax_items");
@@ -382,7 +382,7 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
     const int64_t n = (int64_t)g.n_split * H;
     softmax_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split, g.n_split, H,
                                                                           pm, pd);
-    softmax_write<<<(unsigned)((g.n_heavy + 3) / 4), kBlock, 0, s>>>(
+    softmax_write<<<(unsigned)((g.n_heavy + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.heavy, g.n_heavy, g.perm, scores, H, hp, pm, pd, out, out_csr);
     TFG_LAUNCHED("softmax_merge / softmax_write");
   }
