@@ -388,13 +388,13 @@ __global__ __launch_bounds__(kItemBlock) void gat_items(
 // One wavefront per long row: the chunks' triples merged in chunk order
 // (lanes over the features, one column each), out = acc / d. With alpha
 // requested the row's (m, d) per head is written back to every chunk slot.
-__global__ __launch_bounds__(kBlock) void gat_merge(const SplitRow* __restrict__ split,
+__global__ __launch_bounds__(kItemBlock) void gat_merge(const SplitRow* __restrict__ split,
                                                     int n_split, int H, int D,
                                                     float* __restrict__ pacc,
                                                     float* __restrict__ pm,
                                                     double* __restrict__ pd,
                                                     float* __restrict__ out, int write_back) {
-  const int wid = uniform(blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_split) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int row = uniform(split[wid].row), s0 = uniform(split[wid].slot0);
@@ -547,8 +547,8 @@ int run_attention(const Graph& g, GatArgs& a, int vec, hipStream_t s) {
     TFG_LAUNCHED("gat_items");
   }
   if (g.n_split > 0) {
-    dim3 mgrid((unsigned)((g.n_split + kBlock / kWave - 1) / (kBlock / kWave)));
-    gat_merge<<<mgrid, kBlock, 0, s>>>(g.split, g.n_split, H, D, a.pacc, a.pm, a.pd, a.out,
+    dim3 mgrid((unsigned)((g.n_split + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)));
+    gat_merge<<<mgrid, kItemBlock, 0, s>>>(g.split, g.n_split, H, D, a.pacc, a.pm, a.pd, a.out,
                                        a.alpha_out != nullptr ? 1 : 0);
     TFG_LAUNCHED("gat_merge");
     if (a.alpha_out != nullptr) {

@@ -31,13 +31,13 @@ __global__ __launch_bounds__(kBlock) void degree_unit(const int* __restrict__ ro
 
 // General weights: one wavefront per row, each lane summing a strided part of
 // the row in double, then a fixed-order tree across the lanes.
-__global__ __launch_bounds__(kBlock) void degree_weighted(const int* __restrict__ rowptr,
+__global__ __launch_bounds__(kItemBlock) void degree_weighted(const int* __restrict__ rowptr,
                                                           const int* __restrict__ perm,
                                                           const float* __restrict__ w,
                                                           int64_t E_in, int64_t N,
                                                           float* __restrict__ deg,
                                                           float* __restrict__ dinv) {
-  const int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+  const int64_t t = (int64_t)blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave;
   if (t >= N) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int kb = uniform(rowptr[t]), ke = uniform(rowptr[t + 1]);
@@ -458,8 +458,8 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
   if (edge_weight == nullptr) {
     degree_unit<<<nb_rows, kBlock, 0, s>>>(g.rowptr, g.N, out_deg, dinv);
   } else {
-    degree_weighted<<<(unsigned)((g.N + 3) / 4), kBlock, 0, s>>>(g.rowptr, g.perm, edge_weight,
-                                                                 g.E_in, g.N, out_deg, dinv);
+    degree_weighted<<<(unsigned)((g.N + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
+        g.rowptr, g.perm, edge_weight, g.E_in, g.N, out_deg, dinv);
   }
   TFG_LAUNCHED("gcn degree");
   if (out_w_csr && g.E > 0 && edge_weight == nullptr && use_part_ranges(g)) {
