@@ -373,7 +373,8 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 // starts the keys (key[k-1], key[k]]; k = E closes the keys after the last one.
 // Four positions per thread, read with one 16-byte load; the key before them
 // comes from the neighbouring lane.
-__global__ __launch_bounds__(kBlock) void key_bounds(const int* __restrict__ keys, int64_t E,
+constexpr int kKbThreads = 256;  // threads per block of key_bounds
+__global__ __launch_bounds__(kKbThreads) void key_bounds(const int* __restrict__ keys, int64_t E,
                                                      int64_t K, int* __restrict__ bounds) {
   const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   int c[4];
@@ -678,8 +679,8 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
   }
   // segment starts from the boundaries of the sorted keys
   const int64_t K = g.N * g.parts;
-  key_bounds<<<dim3((unsigned)((E / 4 + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(keys, E, K,
-                                                                                      g.segptr);
+  key_bounds<<<dim3((unsigned)((E / 4 + 1 + kKbThreads - 1) / kKbThreads)), dim3(kKbThreads), 0, s>>>(
+      keys, E, K, g.segptr);
   TFG_LAUNCHED("key_bounds");
   if (g.parts > 1) {
     rows_from_segments<<<dim3((unsigned)((g.N + 1 + kBlock - 1) / kBlock)), dim3(kBlock), 0, s>>>(
