@@ -647,3 +647,71 @@ def test_row_chunk_knob_in_a_fresh_process(tfg):
                        capture_output=True, text=True, timeout=240)
     assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
     assert "chunk knob ok" in r.stdout
+
+
+# ---------------------------------------------------------------------------
+# Seeded random configurations: graph size and shape, source parts, plan,
+# normalisation kernels, index type, feature width, leading dimension, heads
+# and reducer drawn together, each case checked against the oracle.
+# ---------------------------------------------------------------------------
+
+def _random_case(seed):
+    r = np.random.default_rng([9001, seed])
+    n = int(r.integers(1, 3000))
+    n_src = n if r.random() < 0.7 else int(r.integers(1, 3000))
+    e = int(r.integers(0, 40_000))
+    H = int(r.choice([1, 1, 2, 4]))
+    F = H * int(r.choice([1, 3, 4, 16, 32]))
+    return dict(n=n, n_src=n_src, e=e, H=H, F=F, ldx=F + int(r.choice([0, 0, 3])),
+                parts=int(r.choice([0, 1, 2, 5, 16])), plan=str(r.choice(["0", "1"])),
+                reduce=str(r.choice(["sum", "mean", "max"])),
+                idx=np.int64 if r.random() < 0.3 else np.int32,
+                hub_edges=int(r.choice([0, 0, 500, 5000])),
+                sliced=str(r.choice(["0", "1"])), by_part=str(r.choice(["0", "1"])),
+                weighted=bool(r.random() < 0.5))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_configurations(tfg, orc, monkeypatch, seed):
+    c = _random_case(seed)
+    monkeypatch.setenv("TFG_PART_PLAN", c["plan"])
+    monkeypatch.setenv("TFG_NORM_SLICED", c["sliced"])
+    monkeypatch.setenv("TFG_NORM_PARTS", c["by_part"])
+    n, n_src, H, F = c["n"], c["n_src"], c["H"], c["F"]
+    hub = 0 if c["hub_edges"] else None
+    ei = graphgen.random_graph(100 + seed, n, c["e"], n_src=n_src, hub=hub,
+                               hub_edges=c["hub_edges"])
+    E = ei.shape[1]
+    what = f"seed {seed}: {c}"
+    eid = dev(ei.astype(c["idx"]))
+    g = tfg.tfg_graph_create(eid, n, N_src=n_src, src_parts=c["parts"])
+    rowptr, col, perm = tfg.tfg_graph_csr(g)
+    parts = g.info()["src_parts"]
+    ref_rowptr, ref_col, ref_perm = orc.csr_by_target(ei, n, parts=parts, n_src=n_src)[:3]
+    assert np.array_equal(host(perm), ref_perm), what
+    assert np.array_equal(host(col), ref_col) and np.array_equal(host(rowptr), ref_rowptr), what
+    # the aggregation, weighted per edge (or per head) or not
+    big = graphgen.features(200 + seed, n_src, c["ldx"])
+    x = big[:, :F]
+    w = (np.random.default_rng(seed).standard_normal((E, H) if H > 1 else E).astype(np.float32)
+         if c["weighted"] else None)
+    heads = H if w is not None else 1
+    res = tfg.tfg_aggregate(eid, dev(big)[:, :F], n, reduce=c["reduce"],
+                            edge_weight=None if w is None else dev(w), heads=heads, graph=g)
+    if c["reduce"] == "max":
+        out, arg = (host(t) for t in res)
+        ref, refarg = orc.aggregate(ei, x, n, "max", edge_weight=w, heads=heads)
+        assert same_bits(out, ref) and np.array_equal(arg, refarg), what
+    else:
+        ref, S = orc.aggregate(ei, x, n, c["reduce"], edge_weight=w, heads=heads)
+        assert_scaled(host(res), ref, S, what=what)
+    # the normalisation of the square part of the graph (with loops)
+    if n_src == n:
+        gl = tfg.tfg_graph_create(eid, n, add_self_loops=True, src_parts=c["parts"])
+        wn = None if w is None else np.abs(w if H == 1 else w[:, 0]).astype(np.float32) + 0.1
+        r = tfg.tfg_gcn_norm(eid, n, edge_weight=None if wn is None else dev(wn), graph=gl)
+        oei, ow, odeg = orc.gcn_norm(ei, n, edge_weight=wn)
+        assert same_bits(host(r["deg"]), odeg), what
+        assert same_bits(host(r["edge_weight"]), ow), what
+        lperm = orc.csr_by_target(oei, n, parts=gl.info()["src_parts"])[2]
+        assert same_bits(host(r["edge_weight_csr"]), ow[lperm]), what
