@@ -715,3 +715,46 @@ def test_random_configurations(tfg, orc, monkeypatch, seed):
         assert same_bits(host(r["edge_weight"]), ow), what
         lperm = orc.csr_by_target(oei, n, parts=gl.info()["src_parts"])[2]
         assert same_bits(host(r["edge_weight_csr"]), ow[lperm]), what
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_random_attention_and_pooling(tfg, orc, seed):
+    """Seeded random attention layers (heads, head width, graph shape, hub
+    rows, source parts) through the fused layer and the unfused chain, and
+    random pooling batches (graph sizes including empty graphs, width,
+    leading dimension, reducer), against the oracle."""
+    r = np.random.default_rng([9002, seed])
+    n = int(r.integers(2, 3000))
+    H = int(r.choice([1, 2, 4, 8]))
+    D = int(r.choice([1, 4, 8, 16]))
+    hub_edges = int(r.choice([0, 300, 4000]))
+    ei = graphgen.random_graph(300 + seed, n, int(r.integers(1, 30_000)),
+                               hub=0 if hub_edges else None, hub_edges=hub_edges)
+    h = graphgen.features(400 + seed, n, H * D)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n, src_parts=int(r.choice([0, 1, 3])))
+    out = tfg.tfg_gat_aggregate(g, dev(h), dev(a_s), dev(a_d), 0.2)
+    ref, ref_alpha, S = orc.gat_layer(ei, h, a_s, a_d, H, slope=np.float32(0.2))
+    what = f"seed {seed}: n={n} H={H} D={D} E={ei.shape[1]}"
+    assert_scaled(host(out), ref, S, what=what)
+    s = tfg.tfg_gat_edge_scores(dev(ei), dev(h), dev(a_s), dev(a_d), 0.2)
+    alpha = tfg.tfg_segment_softmax(s, dev(ei[1]), n, graph=g)
+    has = np.bincount(ei[1], minlength=n)[ei[1]] > 0
+    assert_rel(host(alpha)[has], ref_alpha[has], what=what + " softmax")
+    # pooling
+    G = int(r.integers(1, 800))
+    sizes = r.integers(0, 30, G)
+    gi = np.repeat(np.arange(G), sizes)
+    F = int(r.choice([1, 3, 16, 64, 130]))
+    ldx = F + int(r.choice([0, 1, 4]))
+    reduce = str(r.choice(["sum", "mean", "max"]))
+    if gi.size:
+        big = graphgen.features(500 + seed, gi.shape[0], ldx)
+        res = tfg.tfg_segment_pool(dev(big)[:, :F], dev(gi.astype(np.int32)), G, reduce)
+        if reduce == "max":
+            pref, parg = orc.segment_pool(big[:, :F], gi, G, "max")
+            assert same_bits(host(res[0]), pref) and np.array_equal(host(res[1]), parg), what
+        else:
+            pref, pS = orc.segment_pool(big[:, :F], gi, G, reduce)
+            assert_scaled(host(res), pref, pS, what=what + f" pool {reduce}")
