@@ -313,3 +313,27 @@ def test_new_calls_on_empty_inputs(tfg):
     torch.cuda.synchronize()
     assert np.all(host(out) == 0) and s.shape == (0, 4) and r.shape == (0, 2)
     assert dxp.shape == (0, 4) and dx0.shape == (n, 0)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_random_backward_configurations(tfg, orc, seed):
+    """Seeded random backward cases: graph shape (square with or without
+    loops, rectangular), hub rows on either side, source parts, reducer,
+    heads, weight order and gradient order, against the oracle."""
+    r = np.random.default_rng([9003, seed])
+    n = int(r.integers(2, 2500))
+    square = r.random() < 0.6
+    n_src = n if square else int(r.integers(2, 2500))
+    heads = int(r.choice([1, 1, 2, 4]))
+    F = heads * int(r.choice([1, 4, 16, 32]))
+    reduce = str(r.choice(["sum", "mean", "max"]))
+    a = graphgen.random_graph(600 + seed, n, int(r.integers(1, 20_000)), n_src=n_src,
+                              hub=0, hub_edges=int(r.choice([0, 2000])))
+    loops = bool(square and r.random() < 0.5)
+    E = a.shape[1] + (n if loops else 0)
+    w = (graphgen.rng_for(700 + seed, 1).uniform(-1.0, 2.0, (E, heads) if heads > 1 else E)
+         .astype(np.float32))
+    order = str(r.choice(["coo", "csr"]))
+    dw_order = str(r.choice(["coo", "csr"]))
+    _check_backward(tfg, orc, a, n, n_src, F, reduce, w=w, heads=heads, order=order,
+                    dw_order=dw_order, parts=int(r.choice([1, 2, 4])), loops=loops, seed=seed)
