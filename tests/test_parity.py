@@ -758,3 +758,43 @@ def test_random_attention_and_pooling(tfg, orc, seed):
         else:
             pref, pS = orc.segment_pool(big[:, :F], gi, G, reduce)
             assert_scaled(host(res), pref, pS, what=what + f" pool {reduce}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_propagation_and_batching(tfg, orc, monkeypatch, seed):
+    """Seeded random multi-step propagation (steps, teleport weight, width,
+    source parts, plan) one step at a time on the library's own intermediate
+    values, and random BatchGraph construction (graph count, sizes, edge
+    density, index type) against the oracle."""
+    r = np.random.default_rng([9004, seed])
+    monkeypatch.setenv("TFG_PART_PLAN", str(r.choice(["0", "1"])))
+    n = int(r.integers(2, 2500))
+    F = int(r.choice([1, 8, 32, 64]))
+    K = int(r.integers(1, 4))
+    alpha = float(r.choice([0.0, 0.1, 0.5]))
+    ei = graphgen.random_graph(800 + seed, n, int(r.integers(1, 25_000)), hub=0,
+                               hub_edges=int(r.choice([0, 3000])))
+    x = graphgen.features(900 + seed, n, F)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=True, src_parts=int(r.choice([0, 1, 3])))
+    norm = tfg.tfg_gcn_norm(dev(ei), n, graph=g)
+    oei, ow, _ = orc.gcn_norm(ei, n)
+    z = dev(x)
+    for k in range(K):
+        zin = host(z)
+        z = tfg.tfg_propagate(g, z, 1, alpha=alpha, h=dev(x) if alpha > 0 else None,
+                              edge_weight=norm["edge_weight_csr"])
+        ref, S = orc.propagate(oei, zin, 1, alpha=alpha, h=x if alpha > 0 else None,
+                               edge_weight=ow)
+        assert_scaled(host(z), ref, S, what=f"seed {seed} step {k}")
+    # BatchGraph construction
+    idx = np.int64 if r.random() < 0.3 else np.int32
+    G = int(r.integers(1, 2000))
+    sizes, graphs = graphgen.batch_of_small_graphs(1000 + seed, G, 0, 40, float(r.uniform(0, 0.3)))
+    counts = np.array([gr.shape[1] for gr in graphs])
+    local = (np.concatenate(graphs, axis=1) if counts.sum() else np.zeros((2, 0), np.int64))
+    bei, bgi, noff, eoff = tfg.tfg_batch_graphs(dev(sizes.astype(idx)), dev(counts.astype(idx)),
+                                                dev(local.astype(idx)), int(sizes.sum()))
+    ref_ei, ref_gi = orc.batch_graphs(sizes, graphs)
+    assert np.array_equal(host(bei), ref_ei) and np.array_equal(host(bgi), ref_gi), seed
+    assert np.array_equal(host(noff), orc.batch_offsets(sizes)), seed
+    assert np.array_equal(host(eoff), orc.batch_offsets(counts)), seed
