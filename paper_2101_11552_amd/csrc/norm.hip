@@ -141,9 +141,9 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
 // the slice that holds it. Every block reads all of dinv once (4 N bytes from
 // L2 in full lines, copied straight into LDS) in exchange for one or two
 // random line reads per edge, so the tile per block is made as large as the
-// registers allow: one register per endpoint, holding the node id until the
-// endpoint's slice is seen and then its dinv value, marked by the sign bit
-// (dinv >= 0, ids >= 0). The products are the same ones, in the same order,
+// registers allow: one register per endpoint, holding the node id (as a byte
+// offset, 4 * id) until the endpoint's slice is seen and then its dinv value,
+// marked by the sign bit (dinv >= 0, offsets >= 0). The products are the same ones, in the same order,
 // as in weights_coo / weights_csr, so the kernels agree bit for bit.
 constexpr int kSlThreads = 1024;                  // 16 waves, one block per CU
 constexpr int kSlice = 40960;                     // floats per LDS slice (160 KB)
@@ -172,9 +172,9 @@ __device__ __forceinline__ void fill_slice(float* slice, const float* __restrict
 // All of this wave's memory operations done (the LDS copies included).
 __device__ __forceinline__ void wait_slice() { __builtin_amdgcn_s_waitcnt(0); }
 
-// An endpoint register: a node id (>= 0, or -1 for no edge) until resolved,
+// An endpoint register: 4 * node id (>= 0, or -1 for no edge) until resolved,
 // then the dinv value with the sign bit set. A resolved value never matches a
-// later slice: as unsigned, (value - lo) >= 2^31 - lo > 2^30 (N <= 2^30).
+// later slice: as unsigned, (value - 4 lo) >= 2^31 - 2^30 > 4 len (N <= 2^28).
 __device__ __forceinline__ int resolved(float v) { return __float_as_int(v) | INT_MIN; }
 __device__ __forceinline__ float value_of(int r) { return __int_as_float(r & INT_MAX); }
 
@@ -182,13 +182,16 @@ __device__ __forceinline__ float value_of(int r) { return __int_as_float(r & INT
 // issued together, then used.
 template <int ITEMS>
 __device__ __forceinline__ void resolve(int (&r)[ITEMS], const float* slice, int lo, int len) {
+  // unresolved registers hold byte offsets (4 * id): the difference is the
+  // LDS byte address itself
+  const char* sb = reinterpret_cast<const char*>(slice);
 #pragma unroll
   for (int j0 = 0; j0 < ITEMS; j0 += 8) {
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8 && j0 + j < ITEMS; ++j) {
-      const unsigned u = (unsigned)(r[j0 + j] - lo);
-      v[j] = u < (unsigned)len ? slice[u] : -1.0f;
+      const unsigned u = (unsigned)(r[j0 + j] - 4 * lo);
+      v[j] = u < 4u * (unsigned)len ? *reinterpret_cast<const float*>(sb + u) : -1.0f;
     }
 #pragma unroll
     for (int j = 0; j < 8 && j0 + j < ITEMS; ++j)
@@ -268,6 +271,8 @@ __global__ __launch_bounds__(kSlThreads, 4) void weights_coo_sliced(
       }
     }
   }
+#pragma unroll
+  for (int j = 0; j < 2 * kCooItems; ++j) st[j] = st[j] >= 0 ? 4 * st[j] : st[j];  // byte offsets
   walk_slices(st, slice, dinv, N);
   // all loads (the weights) before the first store: a wait for a load also
   // waits for the stores issued before it
@@ -311,7 +316,7 @@ __global__ __launch_bounds__(kSlThreads, 4) void weights_csr_sliced(
 #pragma unroll
     for (int j = 0; j < kCsrItems; ++j) {
       const int p = j * kSlThreads + (int)threadIdx.x;
-      c[j] = p < n ? cb[p] : -1;  // -1: no slice holds it
+      c[j] = p < n ? 4 * cb[p] : -1;  // byte offset; -1: no slice holds it
     }
   }
   walk_slices(c, slice, dinv, N);
@@ -435,7 +440,7 @@ __global__ __launch_bounds__(kSlThreads) void weights_csr_parts(
 // gathered lines per edge; they are chosen while that fill stays below one
 // line per edge and the grid still covers the chip.
 bool use_sliced(int64_t E, int64_t N) {
-  if (N > (int64_t(1) << 30)) return false;  // see resolved()
+  if (N > (int64_t(1) << 28)) return false;  // see resolved()
   if (const char* v = std::getenv("TFG_NORM_SLICED")) return v[0] == '1';
   return N * 4 <= (int64_t)kCooTile * 128 && E >= (int64_t)256 * kCooTile;
 }
