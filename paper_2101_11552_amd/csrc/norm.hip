@@ -5,6 +5,7 @@
 //   w'[e]   = (dinv[src] * w[e]) * dinv[tgt]       (float32, left to right)
 // written in the caller's COO order and/or in the graph's CSR order; both
 // orders use the same operands in the same order, so they are bit-identical.
+#include <algorithm>
 #include <cstdlib>
 
 #include "wave.h"
@@ -358,78 +359,88 @@ __global__ __launch_bounds__(kSlThreads, 4) void weights_csr_sliced(
 
 // Graph order over the part plan's items (unit weights). The items come part
 // by part and the sources of a (row, part) item all lie in that part's node
-// range, so a block copies that range of dinv into LDS once (or the two
-// ranges its items straddle) and every position reads its source's value
-// there: one copy of a part per block instead of a walk over all of dinv.
+// range. A block takes a contiguous run of items (one block per CU, in chunks
+// of kPartItems), copies a part's range of dinv into LDS when its items reach
+// that part (once, or twice where the run straddles two parts) and every
+// position reads its source's value there: one copy of a part per block
+// instead of a walk over all of dinv.
 // A position is written in the round of its source's part only, so exactly
 // once. Same products as weights_coo, in the same order.
-constexpr int kPartItems = 512;             // items per block
+constexpr int kPartItems = 512;             // items per chunk (descriptors in LDS)
 constexpr int kPartU = 8;                   // items in flight per wavefront
 constexpr int kPartSlice = 36864;           // floats of LDS for one part (144 KB)
+constexpr int kPartBlocks = 256;            // blocks: one per CU
 
 __global__ __launch_bounds__(kSlThreads) void weights_csr_parts(
-    const WorkItem* __restrict__ items, int n_items, int part_rows,
+    const WorkItem* __restrict__ items, int n_items, int per_block, int part_rows,
     const int* __restrict__ col, int64_t N, const float* __restrict__ dinv,
     float* __restrict__ out) {
   __shared__ float slice[kPartSlice];
-  __shared__ int4 it[kPartItems];  // (row, kbeg, kend, -) of the block's items
+  __shared__ int4 it[kPartItems];  // (row, kbeg, kend, -) of the current chunk of items
   __shared__ int prange[2];
-  const int i0 = blockIdx.x * kPartItems;
-  const int ni = min(kPartItems, n_items - i0);
-  for (int j = threadIdx.x; j < ni; j += kSlThreads) {
-    const WorkItem w = items[i0 + j];
-    it[j] = make_int4(w.row, w.kbeg, w.kend, 0);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    // parts of the first and the last item's first source (items are part-major)
-    prange[0] = col[it[0].y] / part_rows;
-    prange[1] = col[it[ni - 1].y] / part_rows;
-  }
-  __syncthreads();
-  const int p0 = prange[0], p1 = prange[1];
+  const int ib = blockIdx.x * per_block;
+  const int ie = min(ib + per_block, n_items);
   const int wave = uniform((int)threadIdx.x / kWave), lane = lane_id();
-  for (int p = p0; p <= p1; ++p) {
-    // part p holds sources [base, base + cnt); the copy starts 16-byte aligned
-    const int64_t base = (int64_t)p * part_rows;
-    const int cnt = (int)min<int64_t>(part_rows, N - base);
-    const int64_t lo = base & ~int64_t(3);
-    const int off = (int)(base - lo);
-    const int len = cnt + off;
-    if (p > p0) __syncthreads();  // the previous range is no longer read
-    fill_slice(slice, dinv + lo, len);
-    __builtin_amdgcn_s_waitcnt(0);
+  int loaded = -1;  // the part whose range the slice holds (the same in every thread)
+  for (int c0 = ib; c0 < ie; c0 += kPartItems) {
+    const int ni = min(kPartItems, ie - c0);
+    __syncthreads();  // the previous chunk's items and part range are no longer read
+    for (int j = threadIdx.x; j < ni; j += kSlThreads) {
+      const WorkItem w = items[c0 + j];
+      it[j] = make_int4(w.row, w.kbeg, w.kend, 0);
+    }
     __syncthreads();
-    for (int jb = wave * kPartU; jb < ni; jb += (kSlThreads / kWave) * kPartU) {
-      int kb[kPartU], ke[kPartU], c[kPartU][2];
-      float dt[kPartU];
-#pragma unroll
-      for (int u = 0; u < kPartU; ++u) {
-        const bool ok = jb + u < ni;
-        const int4 d = it[ok ? jb + u : 0];
-        kb[u] = ok ? d.y : 0;
-        ke[u] = ok ? d.z : 0;
-        dt[u] = ok ? dinv[d.x] : 0.0f;
+    if (threadIdx.x == 0) {
+      // parts of the chunk's first and last item (items are part-major)
+      prange[0] = col[it[0].y] / part_rows;
+      prange[1] = col[it[ni - 1].y] / part_rows;
+    }
+    __syncthreads();
+    const int p0 = prange[0], p1 = prange[1];
+    for (int p = p0; p <= p1; ++p) {
+      // part p holds sources [base, base + cnt); the copy starts 16-byte aligned
+      const int64_t base = (int64_t)p * part_rows;
+      const int cnt = (int)min<int64_t>(part_rows, N - base);
+      const int64_t lo = base & ~int64_t(3);
+      const int off = (int)(base - lo);
+      if (p != loaded) {
+        __syncthreads();  // the previous range is no longer read
+        fill_slice(slice, dinv + lo, cnt + off);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        loaded = p;
       }
+      for (int jb = wave * kPartU; jb < ni; jb += (kSlThreads / kWave) * kPartU) {
+        int kb[kPartU], ke[kPartU], c[kPartU][2];
+        float dt[kPartU];
 #pragma unroll
-      for (int u = 0; u < kPartU; ++u)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int k = kb[u] + h * kWave + lane;
-          c[u][h] = k < ke[u] ? col[k] : -1;
+        for (int u = 0; u < kPartU; ++u) {
+          const bool ok = jb + u < ni;
+          const int4 d = it[ok ? jb + u : 0];
+          kb[u] = ok ? d.y : 0;
+          ke[u] = ok ? d.z : 0;
+          dt[u] = ok ? dinv[d.x] : 0.0f;
         }
 #pragma unroll
-      for (int u = 0; u < kPartU; ++u) {
+        for (int u = 0; u < kPartU; ++u)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int k = kb[u] + h * kWave + lane;
-          const unsigned q = (unsigned)(c[u][h] - (int)base);
-          if (k < ke[u] && q < (unsigned)cnt) out[k] = (slice[off + q] * 1.0f) * dt[u];
-        }
-        // items longer than two rounds of lanes (a row-chunk setting above 128)
-        for (int k = kb[u] + 2 * kWave + lane; k < ke[u]; k += kWave) {
-          const unsigned q = (unsigned)(col[k] - (int)base);
-          if (q < (unsigned)cnt) out[k] = (slice[off + q] * 1.0f) * dt[u];
+          for (int h = 0; h < 2; ++h) {
+            const int k = kb[u] + h * kWave + lane;
+            c[u][h] = k < ke[u] ? col[k] : -1;
+          }
+#pragma unroll
+        for (int u = 0; u < kPartU; ++u) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int k = kb[u] + h * kWave + lane;
+            const unsigned q = (unsigned)(c[u][h] - (int)base);
+            if (k < ke[u] && q < (unsigned)cnt) out[k] = (slice[off + q] * 1.0f) * dt[u];
+          }
+          // items longer than two rounds of lanes (a row-chunk setting above 128)
+          for (int k = kb[u] + 2 * kWave + lane; k < ke[u]; k += kWave) {
+            const unsigned q = (unsigned)(col[k] - (int)base);
+            if (q < (unsigned)cnt) out[k] = (slice[off + q] * 1.0f) * dt[u];
+          }
         }
       }
     }
@@ -468,8 +479,11 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
   }
   TFG_LAUNCHED("gcn degree");
   if (out_w_csr && g.E > 0 && edge_weight == nullptr && use_part_ranges(g)) {
-    weights_csr_parts<<<(unsigned)((g.n_pexec + kPartItems - 1) / kPartItems), kSlThreads, 0, s>>>(
-        g.pexec, g.n_pexec, (int)g.part_rows, g.col, g.N, dinv, out_w_csr);
+    // one block per CU, each over a contiguous run of items (at most two part
+    // ranges to copy), or blocks of kPartItems items on small graphs
+    const int per_block = std::max(kPartItems, (g.n_pexec + kPartBlocks - 1) / kPartBlocks);
+    weights_csr_parts<<<(unsigned)((g.n_pexec + per_block - 1) / per_block), kSlThreads, 0, s>>>(
+        g.pexec, g.n_pexec, per_block, (int)g.part_rows, g.col, g.N, dinv, out_w_csr);
     TFG_LAUNCHED("gcn weights (graph order, by source part)");
   } else if (out_w_csr && g.E > 0 && use_sliced(g.E, g.N)) {
     const unsigned nbs = (unsigned)((g.E + kCsrTile - 1) / kCsrTile);
