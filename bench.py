@@ -102,15 +102,6 @@ def cpu_baseline(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
             "cpu_model": cpu_model(), "nproc": os.cpu_count()}
 
 
-def host_threads() -> int:
-    """Host threads this process may use: OMP_NUM_THREADS when set (the
-    machine's share for this job), else the CPUs of the affinity mask."""
-    env = os.environ.get("OMP_NUM_THREADS", "")
-    if env.isdigit() and int(env) > 0:
-        return int(env)
-    return len(os.sched_getaffinity(0))
-
-
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -122,35 +113,16 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def oracle_sum_by_row_ranges(oei, ow, x, n: int, threads: int):
-    """The oracle's sum aggregation split over host threads by target range:
-    thread i computes rows [n*i/T, n*(i+1)/T), scanning every edge in input
-    order and skipping the other targets, so each row is summed in the same
-    order as in one thread and the result is bit-identical. Returns the [n, F]
-    double sums."""
-    import oracle
-    from concurrent.futures import ThreadPoolExecutor
-    bounds = [n * i // threads for i in range(threads + 1)]
-
-    def part(i):
-        rows = np.arange(bounds[i], bounds[i + 1], dtype=np.int64)
-        return oracle.aggregate(oei, x, n, "sum", edge_weight=ow, rows=rows)[0]
-
-    with ThreadPoolExecutor(threads) as pool:  # the oracle's C calls release the GIL
-        parts = list(pool.map(part, range(threads)))
-    return np.concatenate(parts, axis=0)
-
-
 def cpu_baseline_threads(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
     """The same sample with the aggregation over all host threads (rows split
     by target range, bit-identical to one thread); the normalisation, about
     1% of the work, stays on one thread."""
     import oracle
-    threads = host_threads()
+    threads = oracle.host_threads()
     sub = np.ascontiguousarray(ei[:, :n_edges].astype(np.int64))
     t0 = time.perf_counter()
     oei, ow, _ = oracle.gcn_norm(sub, n)
-    oracle_sum_by_row_ranges(oei, ow, x, n, threads)
+    oracle.aggregate_by_row_ranges(oei, x, n, "sum", edge_weight=ow, threads=threads)
     dt = time.perf_counter() - t0
     e_total = n_edges + n
     return {"value": round(e_total / dt / 1e9, 6), "unit": "GE/s", "cores": threads,

@@ -441,12 +441,25 @@ int tfg_segment_pool_backward(const float *dy, int64_t G, int64_t F, const void 
  * rows stacked in graph order.
  * node_counts, edge_counts: [G] (index_type); local_edge_index: [2, E] with
  * the edges of graph 0, then graph 1, ... (row 0 sources, row 1 targets, ids
- * local to their graph); E = sum of edge_counts, Nb = sum of node_counts.
+ * local to their graph); E = sum of edge_counts, Nb = sum of node_counts (both
+ * from tfg_batch_graphs_totals when the caller does not know them).
  * Outputs: out_edge_index [2, E] and out_graph_index [Nb] (index_type);
  * out_node_offsets / out_edge_offsets: NULL or [G + 1] int32.
  * validate != 0: synchronise and return TFG_ERR_INDEX_RANGE if a count is
  * negative, a local id is outside its graph, or E / Nb differ from the sums.
  */
+/*
+ * The sizes of a BatchGraph before it is built (Sec. 2.1.1): *Nb = sum of
+ * node_counts and *E = sum of edge_counts ([G], index_type, device memory),
+ * summed on the device in 64 bits. ws: tfg_batch_graphs_ws_bytes(G) bytes,
+ * 256-byte aligned. Synchronises the stream once to read the totals back.
+ * Errors: TFG_ERR_INVALID_ARG (bad G or index type, NULL pointer),
+ * TFG_ERR_INDEX_RANGE (a negative count), TFG_ERR_WORKSPACE.
+ */
+int tfg_batch_graphs_totals(int64_t G, const void *node_counts, const void *edge_counts,
+                            int index_type, void *ws, size_t ws_bytes, tfg_stream_t stream,
+                            int64_t *Nb, int64_t *E);
+
 size_t tfg_batch_graphs_ws_bytes(int64_t G);
 int tfg_batch_graphs(int64_t G, const void *node_counts, const void *edge_counts,
                      const void *local_edge_index, int index_type, int64_t E, int64_t Nb,

@@ -42,8 +42,6 @@ def lib():
         _lib.orc_check_edges.argtypes = [i64, p, p, i64, i64]
         _lib.orc_csr_by_target.argtypes = [i64, i64, p, p, p, p, p]
         _lib.orc_csr_by_target.restype = None
-        _lib.orc_csr_by_key.argtypes = [i64, i64, i64, i64, p, p, p, p, p]
-        _lib.orc_csr_by_key.restype = None
         _lib.orc_gcn_norm.argtypes = [i64, i64, p, p, p, ctypes.c_int, p, p, p, p]
         _lib.orc_gcn_norm.restype = i64
         _lib.orc_aggregate.argtypes = [i64, p, p, p, i64, p, i64, i64, i64, ctypes.c_int,
@@ -101,25 +99,19 @@ def check_edges(edge_index, n_src, n):
     return lib().orc_check_edges(ei.shape[1], _ptr(ei[0]), _ptr(ei[1]), n_src, n)
 
 
-def csr_by_target(edge_index, n, parts=1, n_src=None):
-    """Stable counting sort by (target, source part): (rowptr [N+1], col [E],
-    perm [E]); with ``parts`` > 1 also returns seg [N*parts+1] (the start of
-    every (target, part) key). Source part = source // ceil(n_src / parts)."""
+def csr_by_target(edge_index, n, n_src=None):
+    """Stable counting sort by target: (rowptr [N+1], col [E], perm [E]), input
+    order kept within a row."""
     ei = _i64(edge_index)
     E = ei.shape[1]
     n_src = n if n_src is None else n_src
     _check(check_edges(ei, n_src, n))
-    part_rows = max(-(-n_src // parts), 1)
-    seg = np.empty(n * parts + 1, np.int64)
+    rowptr = np.empty(n + 1, np.int64)
     col = np.empty(E, np.int64)
     perm = np.empty(E, np.int64)
     src, tgt = np.ascontiguousarray(ei[0]), np.ascontiguousarray(ei[1])
-    lib().orc_csr_by_key(E, n, parts, part_rows, _ptr(src), _ptr(tgt), _ptr(seg), _ptr(col),
-                         _ptr(perm))
-    rowptr = np.ascontiguousarray(seg[::parts])
-    if parts == 1:
-        return rowptr, col, perm
-    return rowptr, col, perm, seg
+    lib().orc_csr_by_target(E, n, _ptr(src), _ptr(tgt), _ptr(rowptr), _ptr(col), _ptr(perm))
+    return rowptr, col, perm
 
 
 def gcn_norm(edge_index, n, edge_weight=None, add_self_loops=True):
@@ -168,6 +160,36 @@ def aggregate(edge_index, x, n, reduce="sum", edge_weight=None, heads=1, rows=No
                                         _ptr(arg), _ptr(scale))
     _check(code)
     return (outf, arg) if red == MAX else (out64, scale)
+
+
+def host_threads() -> int:
+    """Host threads this process may use: OMP_NUM_THREADS when set (the
+    machine's share for this job), else the CPUs of the affinity mask."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return int(env)
+    return len(os.sched_getaffinity(0))
+
+
+def aggregate_by_row_ranges(edge_index, x, n, reduce="sum", edge_weight=None, heads=1,
+                            threads=None):
+    """``aggregate`` over all N targets, split over host threads by target
+    range: thread i computes rows [n*i/T, n*(i+1)/T), scanning every edge in
+    input order and skipping the other targets, so every row is reduced in the
+    same order as in one thread and the result is bit-identical."""
+    from concurrent.futures import ThreadPoolExecutor
+    threads = max(1, min(threads or host_threads(), max(n, 1)))
+    ei = _i64(edge_index)
+    x, _ = _rows(x)
+    bounds = [n * i // threads for i in range(threads + 1)]
+
+    def part(i):
+        rows = np.arange(bounds[i], bounds[i + 1], dtype=np.int64)
+        return aggregate(ei, x, n, reduce, edge_weight=edge_weight, heads=heads, rows=rows)
+
+    with ThreadPoolExecutor(threads) as pool:  # the C calls release the GIL
+        parts = list(pool.map(part, range(threads)))
+    return tuple(np.concatenate([p[j] for p in parts], axis=0) for j in range(2))
 
 
 def propagate(edge_index, x, K, alpha=0.0, h=None, edge_weight=None):

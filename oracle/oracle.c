@@ -45,36 +45,28 @@ int orc_check_edges(int64_t E, const int64_t *src, const int64_t *tgt, int64_t n
 }
 
 /*
- * CSR by target (the reduce key): a stable counting sort of the edge list by
- * the key (target, source part), source part = source / part_rows, with
- * `parts` parts (parts = 1: by target only). seg[v] .. seg[v+1] are the
- * positions of key v = target * parts + part (N * parts + 1 entries; with
- * parts = 1 this is the row pointer); within a key the edges keep their input
- * order. perm[k] is the input edge id at position k, col[k] its source id.
+ * CSR by target (the reduce key of Sec. 2.1.2 is the target node index): a
+ * stable counting sort of the edge list by target. rowptr[t] .. rowptr[t+1]
+ * are the positions of the edges entering t (N + 1 entries); within a row the
+ * edges keep their input order. perm[k] is the input edge id at position k,
+ * col[k] its source id.
  */
-void orc_csr_by_key(int64_t E, int64_t N, int64_t parts, int64_t part_rows, const int64_t *src,
-                    const int64_t *tgt, int64_t *seg, int64_t *col, int64_t *perm)
+void orc_csr_by_target(int64_t E, int64_t N, const int64_t *src, const int64_t *tgt,
+                       int64_t *rowptr, int64_t *col, int64_t *perm)
 {
-    int64_t K = N * parts;
-    memset(seg, 0, (size_t)(K + 1) * sizeof(int64_t));
+    memset(rowptr, 0, (size_t)(N + 1) * sizeof(int64_t));
     for (int64_t e = 0; e < E; ++e)
-        seg[tgt[e] * parts + src[e] / part_rows + 1] += 1;
-    for (int64_t v = 0; v < K; ++v)
-        seg[v + 1] += seg[v];
-    int64_t *cursor = (int64_t *)malloc((size_t)(K > 0 ? K : 1) * sizeof(int64_t));
-    memcpy(cursor, seg, (size_t)K * sizeof(int64_t));
+        rowptr[tgt[e] + 1] += 1;
+    for (int64_t t = 0; t < N; ++t)
+        rowptr[t + 1] += rowptr[t];
+    int64_t *cursor = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    memcpy(cursor, rowptr, (size_t)N * sizeof(int64_t));
     for (int64_t e = 0; e < E; ++e) {
-        int64_t k = cursor[tgt[e] * parts + src[e] / part_rows]++;
+        int64_t k = cursor[tgt[e]]++;
         perm[k] = e;
         col[k] = src[e];
     }
     free(cursor);
-}
-
-void orc_csr_by_target(int64_t E, int64_t N, const int64_t *src, const int64_t *tgt,
-                       int64_t *rowptr, int64_t *col, int64_t *perm)
-{
-    orc_csr_by_key(E, N, 1, 1, src, tgt, rowptr, col, perm);
 }
 
 /*

@@ -24,7 +24,7 @@ __all__ = [
     "tfg_aggregate_ws_bytes", "tfg_aggregate", "tfg_aggregate_backward",
     "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_softmax_backward",
     "tfg_segment_pool", "tfg_segment_pool_backward",
-    "tfg_batch_graphs", "tfg_propagate", "tfg_gat_aggregate",
+    "tfg_batch_graphs", "tfg_batch_graphs_totals", "tfg_propagate", "tfg_gat_aggregate",
     "tfg_edge_dot_scores", "tfg_gat_dot_aggregate",
     "library_path", "load",
 ]
@@ -94,6 +94,8 @@ def load():
         "tfg_segment_pool_ws_bytes": (sz, [i64, i64]),
         "tfg_segment_pool": (ci, [p, i64, i64, i64, p, ci, i64, ci, p, p, ci, p, sz, p]),
         "tfg_batch_graphs_ws_bytes": (sz, [i64]),
+        "tfg_batch_graphs_totals": (ci, [i64, p, p, ci, p, sz, p, ctypes.POINTER(i64),
+                                         ctypes.POINTER(i64)]),
         "tfg_propagate_ws_bytes": (sz, [p, i64, i64]),
         "tfg_gat_aggregate_ws_bytes": (sz, [p, i64, i64]),
         "tfg_gat_aggregate": (ci, [p, p, i64, i64, p, p, ctypes.c_float, p, p, p, sz, p]),
@@ -150,10 +152,41 @@ def _index_type(t: torch.Tensor) -> int:
     raise TypeError(f"index tensor must be int32 or int64, got {t.dtype}")
 
 
-def _dev(t: torch.Tensor, what: str) -> torch.Tensor:
-    if not t.is_cuda:
+def _dev(t: torch.Tensor, what: str, device=None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise ValueError(f"{what} must be a device tensor")
+    if device is not None and t.device != torch.device(device):
+        raise ValueError(f"{what} is on {t.device}, the call runs on {device}")
     return t
+
+
+def _out(t: torch.Tensor, shape, dtype, device, what: str) -> torch.Tensor:
+    """A caller-supplied output: on the call's device, of the right dtype,
+    exactly `shape` and contiguous (the kernels write it densely by row)."""
+    _dev(t, what, device)
+    if t.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def _ws(ws: torch.Tensor | None, need: int, device, what: str = "ws") -> torch.Tensor:
+    """The caller's workspace if it is a contiguous device buffer of at least
+    `need` bytes on the call's device, else a new one."""
+    if ws is not None:
+        _dev(ws, what, device)
+        if not ws.is_contiguous():
+            raise ValueError(f"{what} must be contiguous")
+        if _nbytes(ws) >= max(int(need), 1):
+            return ws
+    return _workspace(need, device)
 
 
 def _edges(edge_index: torch.Tensor) -> torch.Tensor:
@@ -163,18 +196,18 @@ def _edges(edge_index: torch.Tensor) -> torch.Tensor:
     return edge_index.contiguous()
 
 
-def _f32(t: torch.Tensor | None, what: str) -> torch.Tensor | None:
+def _f32(t: torch.Tensor | None, what: str, device=None) -> torch.Tensor | None:
     if t is None:
         return None
-    _dev(t, what)
+    _dev(t, what, device)
     if t.dtype != torch.float32:
         raise TypeError(f"{what} must be float32")
     return t.contiguous()
 
 
-def _rows(x: torch.Tensor, what: str):
+def _rows(x: torch.Tensor, what: str, device=None):
     """float32 2-D device tensor with unit column stride; returns (x, ldx)."""
-    _dev(x, what)
+    _dev(x, what, device)
     if x.dtype != torch.float32 or x.dim() != 2:
         raise TypeError(f"{what} must be a float32 matrix")
     if x.stride(1) != 1 or x.stride(0) < x.shape[1]:
@@ -230,13 +263,11 @@ def _create(fn, edge_index, N, N_src, add_self_loops, src_parts, buf, scratch, t
     rows, cols = (N_src, N) if transposed else (N, N_src)
     nb, ns = tfg_graph_bytes(E, rows, add_self_loops, cols, src_parts)
     dev = ei.device
-    if buf is None or buf.numel() < nb:
-        buf = _workspace(nb, dev)
-    if scratch is None or scratch.numel() < ns:
-        scratch = _workspace(ns, dev)
+    buf = _ws(buf, nb, dev, "buf")
+    scratch = _ws(scratch, ns, dev, "scratch")
     h = ctypes.c_void_p()
     _check(fn(_ptr(ei), _index_type(ei), E, N_src, N, int(add_self_loops), int(src_parts),
-              _ptr(buf), buf.numel(), _ptr(scratch), scratch.numel(), _stream(dev),
+              _ptr(buf), _nbytes(buf), _ptr(scratch), _nbytes(scratch), _stream(dev),
               ctypes.byref(h)))
     return Graph(h, buf, E, E + (rows if add_self_loops else 0), rows, cols,
                  bool(add_self_loops), dev)
@@ -278,10 +309,10 @@ def tfg_edge_reorder(values: torch.Tensor, src: Graph | None = None,
     """A per-edge array [E'] or [E', H] moved from the order of ``src`` to the
     order of ``dst`` (None = the caller's COO edge order)."""
     lib = load()
-    v = _f32(values, "values")
     g = src if src is not None else dst
     if g is None:
         raise ValueError("at least one graph is needed")
+    v = _f32(values, "values", g.device)
     H = v.numel() // max(g.E, 1) if g.E else 1
     if v.numel() != g.E * H:
         raise ValueError("values must hold E' * H entries")
@@ -289,7 +320,7 @@ def tfg_edge_reorder(values: torch.Tensor, src: Graph | None = None,
     hs = src.handle if src is not None else None
     hd = dst.handle if dst is not None else None
     ws = _workspace(lib.tfg_edge_reorder_ws_bytes(hs, hd, H), v.device)
-    _check(lib.tfg_edge_reorder(hs, hd, _ptr(v), H, _ptr(out), _ptr(ws), ws.numel(),
+    _check(lib.tfg_edge_reorder(hs, hd, _ptr(v), H, _ptr(out), _ptr(ws), _nbytes(ws),
                                 _stream(v.device)))
     return out
 
@@ -320,7 +351,11 @@ def tfg_gcn_norm(edge_index: torch.Tensor, N: int, edge_weight: torch.Tensor | N
     ei = _edges(edge_index)
     E = ei.shape[1]
     dev = ei.device
-    w = _f32(edge_weight, "edge_weight")
+    w = _f32(edge_weight, "edge_weight", dev)
+    if w is not None and w.numel() != E:
+        raise ValueError(f"edge_weight must hold E = {E} values")
+    if graph is not None and graph.device != dev:
+        raise ValueError("graph and edge_index are on different devices")
     Ep = E + (N if add_self_loops else 0)
     if out_edge_weight_csr is None:
         out_edge_weight_csr = graph is not None
@@ -334,13 +369,11 @@ def tfg_gcn_norm(edge_index: torch.Tensor, N: int, edge_weight: torch.Tensor | N
     if out_deg:
         res["deg"] = torch.empty(N, dtype=torch.float32, device=dev)
     h = graph.handle if graph is not None else None
-    need = lib.tfg_gcn_norm_ws_bytes(E, N, int(add_self_loops), h)
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, dev)
+    ws = _ws(ws, lib.tfg_gcn_norm_ws_bytes(E, N, int(add_self_loops), h), dev)
     _check(lib.tfg_gcn_norm(_ptr(ei), _index_type(ei), E, _ptr(w), N, int(add_self_loops), h,
                             _ptr(res.get("edge_index")), _ptr(res.get("edge_weight")),
                             _ptr(res.get("edge_weight_csr")), _ptr(res.get("deg")), _ptr(ws),
-                            ws.numel(), _stream(dev)))
+                            _nbytes(ws), _stream(dev)))
     return res
 
 
@@ -369,23 +402,28 @@ def tfg_aggregate(edge_index: torch.Tensor | None, x: torch.Tensor, N: int, redu
         E = ei.shape[1]
     x, ldx = _rows(x, "x")
     dev = x.device
+    if ei is not None and ei.device != dev:
+        raise ValueError("edge_index and x are on different devices")
+    if graph is not None and graph.device != dev:
+        raise ValueError("graph and x are on different devices")
     N_src, F = x.shape
-    w = _f32(edge_weight, "edge_weight")
+    w = _f32(edge_weight, "edge_weight", dev)
     if w is not None and w.numel() != E * heads:
         raise ValueError(f"edge_weight must hold E * heads = {E * heads} values")
     red = _REDUCE[reduce]
     if out is None:
         out = torch.empty((N, F), dtype=torch.float32, device=dev)
-    if red == 2 and argmax is None:
-        argmax = torch.empty((N, F), dtype=torch.int32, device=dev)
+    _out(out, (N, F), torch.float32, dev, "out")
+    if red == 2:
+        if argmax is None:
+            argmax = torch.empty((N, F), dtype=torch.int32, device=dev)
+        _out(argmax, (N, F), torch.int32, dev, "argmax")
     h = graph.handle if graph is not None else None
-    need = lib.tfg_aggregate_ws_bytes(E, N_src, N, F, red, h)
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, dev)
+    ws = _ws(ws, lib.tfg_aggregate_ws_bytes(E, N_src, N, F, red, h), dev)
     _check(lib.tfg_aggregate(_ptr(ei), _index_type(ei) if ei is not None else 0, E, _ptr(w), heads,
                              _ORDER[weight_order],
                              _ptr(x), N_src, F, ldx, N, red, h, _ptr(out),
-                             _ptr(argmax) if red == 2 else None, _ptr(ws), ws.numel(),
+                             _ptr(argmax) if red == 2 else None, _ptr(ws), _nbytes(ws),
                              _stream(dev)))
     return (out, argmax) if red == 2 else out
 
@@ -400,17 +438,19 @@ def tfg_aggregate_backward(graph: Graph, dy: torch.Tensor, reduce: str = "sum",
     (dx [N_src, F] or None, dw [E', heads] or None); dx needs ``graph_t``
     (tfg_graph_create_transposed), dw needs ``x``, max needs the forward ``argmax``."""
     lib = load()
-    dy = _f32(dy, "dy").contiguous()
+    dy = _f32(dy, "dy", graph.device).contiguous()
     dev = dy.device
-    F = dy.shape[1]
-    if dy.shape[0] != graph.N:
+    if dy.dim() != 2 or dy.shape[0] != graph.N:
         raise ValueError("dy must be [N, F]")
-    w = _f32(edge_weight, "edge_weight")
+    F = dy.shape[1]
+    if graph_t is not None and graph_t.device != dev:
+        raise ValueError("graph_t is on another device")
+    w = _f32(edge_weight, "edge_weight", dev)
     if w is not None and w.numel() != graph.E * heads:
         raise ValueError(f"edge_weight must hold E' * heads = {graph.E * heads} values")
     xx, ldx = (None, F)
     if x is not None:
-        xx, ldx = _rows(x, "x")
+        xx, ldx = _rows(x, "x", dev)
         if xx.shape != (graph.N_src, F):
             raise ValueError("x must be [N_src, F]")
     if argmax is not None and tuple(argmax.shape) != (graph.N, F):
@@ -418,7 +458,7 @@ def tfg_aggregate_backward(graph: Graph, dy: torch.Tensor, reduce: str = "sum",
     red = _REDUCE[reduce]
     am = None
     if argmax is not None:
-        am = _dev(argmax, "argmax").contiguous()
+        am = _dev(argmax, "argmax", dev).contiguous()
         if am.dtype != torch.int32:
             raise TypeError("argmax must be int32")
     dx = torch.empty((graph.N_src, F), dtype=torch.float32, device=dev) if want_dx else None
@@ -426,11 +466,10 @@ def tfg_aggregate_backward(graph: Graph, dy: torch.Tensor, reduce: str = "sum",
     ht = graph_t.handle if graph_t is not None else None
     need = lib.tfg_aggregate_backward_ws_bytes(graph.handle, ht, F, heads, red,
                                                _ORDER[weight_order], int(w is not None))
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, dev)
+    ws = _ws(ws, need, dev)
     _check(lib.tfg_aggregate_backward(graph.handle, ht, _ptr(w), heads, _ORDER[weight_order],
                                       _ptr(xx), ldx, _ptr(dy), F, red, _ptr(am), _ptr(dx),
-                                      _ptr(dw), _ORDER[dw_order], _ptr(ws), ws.numel(),
+                                      _ptr(dw), _ORDER[dw_order], _ptr(ws), _nbytes(ws),
                                       _stream(dev)))
     return dx, dw
 
@@ -442,9 +481,12 @@ def tfg_segment_softmax_backward(alpha: torch.Tensor, dalpha: torch.Tensor, seg:
     a = _f32(alpha, "alpha")
     shape = a.shape
     a2 = a.reshape(a.shape[0], -1)
-    da = _f32(dalpha, "dalpha").reshape(a2.shape)
+    da = _f32(dalpha, "dalpha", a.device)
+    if da.numel() != a2.numel():
+        raise ValueError("dalpha must have the shape of alpha")
+    da = da.reshape(a2.shape)
     E, H = a2.shape
-    seg = _dev(seg, "seg").contiguous()
+    seg = _dev(seg, "seg", a.device).contiguous()
     if seg.numel() != E:
         raise ValueError("seg must hold one id per edge")
     dev = a.device
@@ -452,7 +494,7 @@ def tfg_segment_softmax_backward(alpha: torch.Tensor, dalpha: torch.Tensor, seg:
     h = graph.handle if graph is not None else None
     ws = _workspace(lib.tfg_segment_softmax_backward_ws_bytes(E, H, N, h), dev)
     _check(lib.tfg_segment_softmax_backward(_ptr(a2), _ptr(da), E, H, _ptr(seg), _index_type(seg),
-                                            N, h, _ptr(ds), _ptr(ws), ws.numel(), _stream(dev)))
+                                            N, h, _ptr(ds), _ptr(ws), _nbytes(ws), _stream(dev)))
     return ds.reshape(shape)
 
 
@@ -462,18 +504,19 @@ def tfg_gat_edge_scores(edge_index: torch.Tensor, h: torch.Tensor, a_src: torch.
     lib = load()
     ei = _edges(edge_index)
     E = ei.shape[1]
-    h = _f32(h, "h")
+    h = _f32(h, "h", ei.device)
     N = h.shape[0]
-    a_src, a_dst = _f32(a_src, "a_src"), _f32(a_dst, "a_dst")
+    a_src, a_dst = _f32(a_src, "a_src", ei.device), _f32(a_dst, "a_dst", ei.device)
     H = a_src.shape[0]
     D = a_src.numel() // H
-    if h.shape[1] != H * D or a_dst.shape != a_src.shape:
+    if h.dim() != 2 or h.shape[1] != H * D or a_dst.shape != a_src.shape:
         raise ValueError("h must be [N, H*D] and a_src, a_dst [H, D]")
     if out is None:
         out = torch.empty((E, H), dtype=torch.float32, device=h.device)
+    _out(out, (E, H), torch.float32, h.device, "out")
     ws = _workspace(lib.tfg_gat_edge_scores_ws_bytes(N, H), h.device)
     _check(lib.tfg_gat_edge_scores(_ptr(ei), _index_type(ei), E, _ptr(h), N, H, D, _ptr(a_src),
-                                   _ptr(a_dst), float(slope), _ptr(out), _ptr(ws), ws.numel(),
+                                   _ptr(a_dst), float(slope), _ptr(out), _ptr(ws), _nbytes(ws),
                                    _stream(h.device)))
     return out
 
@@ -487,16 +530,18 @@ def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
     squeeze = s.dim() == 1
     s2 = s.reshape(s.shape[0], -1)
     E, H = s2.shape
-    seg = _dev(seg, "seg").contiguous()
+    seg = _dev(seg, "seg", s.device).contiguous()
     if seg.numel() != E:
         raise ValueError("seg must hold one id per edge")
     dev = s.device
+    if graph is not None and graph.device != dev:
+        raise ValueError("graph and scores are on different devices")
     out = torch.empty_like(s2)
     oc = torch.empty_like(s2) if out_csr else None
     h = graph.handle if graph is not None else None
     ws = _workspace(lib.tfg_segment_softmax_ws_bytes(E, H, N, h), dev)
     _check(lib.tfg_segment_softmax(_ptr(s2), E, H, _ptr(seg), _index_type(seg), N, h, _ptr(out),
-                                   _ptr(oc), _ptr(ws), ws.numel(), _stream(dev)))
+                                   _ptr(oc), _ptr(ws), _nbytes(ws), _stream(dev)))
     if squeeze:
         out = out.reshape(E)
         oc = oc.reshape(E) if oc is not None else None
@@ -511,19 +556,21 @@ def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce:
     lib = load()
     x, ldx = _rows(x, "x")
     Nb, F = x.shape
-    gi = _dev(graph_index, "graph_index").contiguous()
-    red = _REDUCE[reduce]
     dev = x.device
+    gi = _dev(graph_index, "graph_index", dev).contiguous()
+    if gi.dim() != 1 or gi.shape[0] != Nb:
+        raise ValueError("graph_index must hold one id per row of x")
+    red = _REDUCE[reduce]
     if out is None:
         out = torch.empty((G, F), dtype=torch.float32, device=dev)
+    _out(out, (G, F), torch.float32, dev, "out")
     arg = None
     if red == 2:
         arg = argmax if argmax is not None else torch.empty((G, F), dtype=torch.int32, device=dev)
-    need = lib.tfg_segment_pool_ws_bytes(Nb, G)
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, dev)
+        _out(arg, (G, F), torch.int32, dev, "argmax")
+    ws = _ws(ws, lib.tfg_segment_pool_ws_bytes(Nb, G), dev)
     _check(lib.tfg_segment_pool(_ptr(x), Nb, F, ldx, _ptr(gi), _index_type(gi), G, red, _ptr(out),
-                                _ptr(arg), int(validate), _ptr(ws), ws.numel(), _stream(dev)))
+                                _ptr(arg), int(validate), _ptr(ws), _nbytes(ws), _stream(dev)))
     return (out, arg) if red == 2 else out
 
 
@@ -533,21 +580,40 @@ def tfg_segment_pool_backward(dy: torch.Tensor, graph_index: torch.Tensor, reduc
     """Gradient of ``tfg_segment_pool`` for dy = dL/d out [G, F]: dx [Nb, F]."""
     lib = load()
     dy = _f32(dy, "dy")
+    if dy.dim() != 2:
+        raise ValueError("dy must be [G, F]")
     G, F = dy.shape
-    gi = _dev(graph_index, "graph_index").contiguous()
+    gi = _dev(graph_index, "graph_index", dy.device).contiguous()
     Nb = gi.shape[0]
     red = _REDUCE[reduce]
     am = None
     if argmax is not None:
-        am = _dev(argmax, "argmax").contiguous()
+        am = _dev(argmax, "argmax", dy.device).contiguous()
         if am.dtype != torch.int32 or am.shape != dy.shape:
             raise ValueError("argmax must be int32 [G, F]")
     dx = out if out is not None else torch.empty((Nb, F), dtype=torch.float32, device=dy.device)
+    _out(dx, (Nb, F), torch.float32, dy.device, "out")
     ws = _workspace(lib.tfg_segment_pool_ws_bytes(Nb, G), dy.device)
     _check(lib.tfg_segment_pool_backward(_ptr(dy), G, F, _ptr(gi), _index_type(gi), Nb, red,
                                          _ptr(am), _ptr(dx), F, int(validate), _ptr(ws),
-                                         ws.numel(), _stream(dy.device)))
+                                         _nbytes(ws), _stream(dy.device)))
     return dx
+
+
+def tfg_batch_graphs_totals(node_counts: torch.Tensor, edge_counts: torch.Tensor):
+    """(Nb, E): the node and edge totals of a batch, summed on the device."""
+    lib = load()
+    nc = _dev(node_counts, "node_counts").contiguous()
+    ec = _dev(edge_counts, "edge_counts").contiguous()
+    if nc.dtype != ec.dtype or nc.shape != ec.shape or nc.dim() != 1:
+        raise ValueError("node_counts and edge_counts must be [G] of one index dtype")
+    G = nc.shape[0]
+    ws = _workspace(lib.tfg_batch_graphs_ws_bytes(G), nc.device)
+    nb, eb = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib.tfg_batch_graphs_totals(G, _ptr(nc), _ptr(ec), _index_type(nc), _ptr(ws),
+                                       _nbytes(ws), _stream(nc.device), ctypes.byref(nb),
+                                       ctypes.byref(eb)))
+    return nb.value, eb.value
 
 
 def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
@@ -555,17 +621,25 @@ def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
                      validate: bool = True, out=None, ws: torch.Tensor | None = None):
     """BatchGraph of G graphs: (edge_index [2, E], graph_index [Nb], node_offsets [G+1],
     edge_offsets [G+1]). local_edge_index holds graph 0's edges, then graph 1's, ...,
-    with ids local to their graph; Nb defaults to node_counts.sum() (one host read)."""
+    with ids local to their graph; Nb defaults to the node total, which
+    tfg_batch_graphs_totals sums on the device (one wait on the stream)."""
     lib = load()
-    nc = _dev(node_counts, "node_counts").contiguous()
-    ec = _dev(edge_counts, "edge_counts").contiguous()
     ei = _edges(local_edge_index)
+    dev = ei.device
+    nc = _dev(node_counts, "node_counts", dev).contiguous()
+    ec = _dev(edge_counts, "edge_counts", dev).contiguous()
     if nc.dtype != ei.dtype or ec.dtype != ei.dtype:
         raise TypeError("counts and edge_index must share one index dtype")
+    if nc.dim() != 1 or nc.shape != ec.shape:
+        raise ValueError("node_counts and edge_counts must be [G]")
     G, E = nc.shape[0], ei.shape[1]
+    ws = _ws(ws, lib.tfg_batch_graphs_ws_bytes(G), dev)
     if Nb is None:
-        Nb = int(nc.sum().item())
-    dev = ei.device
+        nb, eb = ctypes.c_int64(), ctypes.c_int64()
+        _check(lib.tfg_batch_graphs_totals(G, _ptr(nc), _ptr(ec), _index_type(ei), _ptr(ws),
+                                           _nbytes(ws), _stream(dev), ctypes.byref(nb),
+                                           ctypes.byref(eb)))
+        Nb = nb.value
     if out is not None:  # (edge_index, graph_index, node_offsets, edge_offsets) from a prior call
         out_ei, gi, noff, eoff = out
     else:
@@ -573,14 +647,13 @@ def tfg_batch_graphs(node_counts: torch.Tensor, edge_counts: torch.Tensor,
         gi = torch.empty(Nb, dtype=ei.dtype, device=dev)
         noff = torch.empty(G + 1, dtype=torch.int32, device=dev)
         eoff = torch.empty(G + 1, dtype=torch.int32, device=dev)
-    if out_ei.shape != ei.shape or gi.numel() != Nb or noff.numel() != G + 1 or eoff.numel() != G + 1:
-        raise ValueError("out does not match the batch")
-    need = lib.tfg_batch_graphs_ws_bytes(G)
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, dev)
+    _out(out_ei, tuple(ei.shape), ei.dtype, dev, "out edge_index")
+    _out(gi, (Nb,), ei.dtype, dev, "out graph_index")
+    _out(noff, (G + 1,), torch.int32, dev, "out node_offsets")
+    _out(eoff, (G + 1,), torch.int32, dev, "out edge_offsets")
     _check(lib.tfg_batch_graphs(G, _ptr(nc), _ptr(ec), _ptr(ei), _index_type(ei), E, Nb,
                                 _ptr(out_ei), _ptr(gi), _ptr(noff), _ptr(eoff), int(validate),
-                                _ptr(ws), ws.numel(), _stream(dev)))
+                                _ptr(ws), _nbytes(ws), _stream(dev)))
     return out_ei, gi, noff, eoff
 
 
@@ -592,19 +665,24 @@ def tfg_propagate(graph: Graph, x: torch.Tensor, K: int, alpha: float = 0.0,
     APPNP: h = x). edge_weight in graph order by default (tfg_gcn_norm's
     ``edge_weight_csr``)."""
     lib = load()
-    x, ldx = _rows(x, "x")
+    x, ldx = _rows(x, "x", graph.device)
     N, F = x.shape
-    w = _f32(edge_weight, "edge_weight")
+    if N != graph.N:
+        raise ValueError("x must be [N, F]")
+    w = _f32(edge_weight, "edge_weight", x.device)
+    if w is not None and w.numel() != graph.E:
+        raise ValueError(f"edge_weight must hold E' = {graph.E} values")
     ldh = 0
     if h is not None:
-        h, ldh = _rows(h, "h")
+        h, ldh = _rows(h, "h", x.device)
+        if h.shape != (N, F):
+            raise ValueError("h must be [N, F]")
     if out is None:
         out = torch.empty((N, F), dtype=torch.float32, device=x.device)
-    need = lib.tfg_propagate_ws_bytes(graph.handle, F, K)
-    if ws is None or ws.numel() < need:
-        ws = _workspace(need, x.device)
+    _out(out, (N, F), torch.float32, x.device, "out")
+    ws = _ws(ws, lib.tfg_propagate_ws_bytes(graph.handle, F, K), x.device)
     _check(lib.tfg_propagate(graph.handle, _ptr(w), _ORDER[weight_order], _ptr(x), F, ldx, K,
-                             float(alpha), _ptr(h), ldh, _ptr(out), _ptr(ws), ws.numel(),
+                             float(alpha), _ptr(h), ldh, _ptr(out), _ptr(ws), _nbytes(ws),
                              _stream(x.device)))
     return out
 
@@ -615,19 +693,22 @@ def tfg_gat_aggregate(graph: Graph, h: torch.Tensor, a_src: torch.Tensor, a_dst:
     """Fused attention layer after the projection: out [N, H*D] (and alpha
     [E', H] in the graph's edge order when ``want_alpha``)."""
     lib = load()
-    h = _f32(h, "h")
-    a_src, a_dst = _f32(a_src, "a_src"), _f32(a_dst, "a_dst")
+    h = _f32(h, "h", graph.device)
+    a_src, a_dst = _f32(a_src, "a_src", h.device), _f32(a_dst, "a_dst", h.device)
     H = a_src.shape[0]
     D = a_src.numel() // H
     N = h.shape[0]
-    if h.shape[1] != H * D or a_dst.shape != a_src.shape:
+    if h.dim() != 2 or h.shape[1] != H * D or a_dst.shape != a_src.shape:
         raise ValueError("h must be [N, H*D] and a_src, a_dst [H, D]")
+    if N != graph.N or graph.N_src != graph.N:
+        raise ValueError("h must be [N, H*D] for a square graph")
     if out is None:
         out = torch.empty((N, H * D), dtype=torch.float32, device=h.device)
+    _out(out, (N, H * D), torch.float32, h.device, "out")
     alpha = torch.empty((graph.E, H), dtype=torch.float32, device=h.device) if want_alpha else None
     ws = _workspace(lib.tfg_gat_aggregate_ws_bytes(graph.handle, H, D), h.device)
     _check(lib.tfg_gat_aggregate(graph.handle, _ptr(h), H, D, _ptr(a_src), _ptr(a_dst),
-                                 float(slope), _ptr(out), _ptr(alpha), _ptr(ws), ws.numel(),
+                                 float(slope), _ptr(out), _ptr(alpha), _ptr(ws), _nbytes(ws),
                                  _stream(h.device)))
     return (out, alpha) if want_alpha else out
 
@@ -639,7 +720,9 @@ def tfg_edge_dot_scores(graph: Graph, q: torch.Tensor, key: torch.Tensor, heads:
     """Scaled dot-product scores [E', heads]: scale * <q[tgt], key[src]> per head
     (scale defaults to 1/sqrt(D))."""
     lib = load()
-    q, key = _f32(q, "q"), _f32(key, "key")
+    q, key = _f32(q, "q", graph.device), _f32(key, "key", graph.device)
+    if q.dim() != 2:
+        raise ValueError("q must be [N, H*D]")
     F = q.shape[1]
     D = F // heads
     if q.shape[0] != graph.N or key.shape != (graph.N_src, F) or F % heads:
@@ -648,6 +731,7 @@ def tfg_edge_dot_scores(graph: Graph, q: torch.Tensor, key: torch.Tensor, heads:
         scale = 1.0 / (D ** 0.5)
     if out is None:
         out = torch.empty((graph.E, heads), dtype=torch.float32, device=q.device)
+    _out(out, (graph.E, heads), torch.float32, q.device, "out")
     _check(lib.tfg_edge_dot_scores(graph.handle, _ptr(q), _ptr(key), heads, D, float(scale),
                                    _ptr(out), _ORDER[order], _stream(q.device)))
     return out
@@ -659,7 +743,10 @@ def tfg_gat_dot_aggregate(graph: Graph, q: torch.Tensor, key: torch.Tensor, v: t
     """Transformer-style attention layer in one sweep: out [N, H*D] (and alpha
     [E', H] in edge-id order with ``want_alpha``)."""
     lib = load()
-    q, key, v = _f32(q, "q"), _f32(key, "key"), _f32(v, "v")
+    q, key, v = (_f32(q, "q", graph.device), _f32(key, "key", graph.device),
+                 _f32(v, "v", graph.device))
+    if q.dim() != 2:
+        raise ValueError("q must be [N, H*D]")
     F = q.shape[1]
     D = F // heads
     if (q.shape[0] != graph.N or key.shape != (graph.N_src, F) or v.shape != key.shape
@@ -670,9 +757,10 @@ def tfg_gat_dot_aggregate(graph: Graph, q: torch.Tensor, key: torch.Tensor, v: t
     dev = q.device
     if out is None:
         out = torch.empty((graph.N, F), dtype=torch.float32, device=dev)
+    _out(out, (graph.N, F), torch.float32, dev, "out")
     alpha = torch.empty((graph.E, heads), dtype=torch.float32, device=dev) if want_alpha else None
     ws = _workspace(lib.tfg_gat_dot_aggregate_ws_bytes(graph.handle, heads, D), dev)
     _check(lib.tfg_gat_dot_aggregate(graph.handle, _ptr(q), _ptr(key), _ptr(v), heads, D,
-                                     float(scale), _ptr(out), _ptr(alpha), _ptr(ws), ws.numel(),
+                                     float(scale), _ptr(out), _ptr(alpha), _ptr(ws), _nbytes(ws),
                                      _stream(dev)))
     return (out, alpha) if want_alpha else out

@@ -119,9 +119,11 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   if (mask != nullptr && reduce != TFG_SUM) return fail(TFG_ERR_INVALID_ARG, "masked max");
   const bool heads = H > 1 && w != nullptr;
   const int per_head = (int)(F / H);
+  // every row of x, out (and h, mask) is read or written with v-wide accesses
   auto fits = [&](int v) {
     return F % v == 0 && ldx % v == 0 && reinterpret_cast<uintptr_t>(x) % (4 * v) == 0 &&
-           (!heads || per_head % v == 0) &&
+           reinterpret_cast<uintptr_t>(out) % (4 * v) == 0 && (!heads || per_head % v == 0) &&
+           (h == nullptr || (ldh % v == 0 && reinterpret_cast<uintptr_t>(h) % (4 * v) == 0)) &&
            (mask == nullptr || reinterpret_cast<uintptr_t>(mask) % (4 * v) == 0);
   };
   const int vec = fits(4) ? 4 : fits(2) ? 2 : 1;

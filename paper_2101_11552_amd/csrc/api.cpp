@@ -698,6 +698,30 @@ int tfg_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts
   return TFG_OK;
 }
 
+int tfg_batch_graphs_totals(int64_t G, const void* node_counts, const void* edge_counts,
+                            int index_type, void* ws, size_t ws_bytes, tfg_stream_t stream,
+                            int64_t* Nb, int64_t* E) {
+  if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
+  if (G < 0 || G >= kMaxCount) return fail(TFG_ERR_INVALID_ARG, "bad G");
+  if (Nb == nullptr || E == nullptr) return fail(TFG_ERR_INVALID_ARG, "NULL result pointer");
+  if (G > 0 && (node_counts == nullptr || edge_counts == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL counts");
+  if (int wrc = check_ws(ws, ws_bytes, batch_ws_bytes(G))) return wrc;
+  *Nb = 0;
+  *E = 0;
+  if (G == 0) return TFG_OK;
+  hipStream_t s = as_stream(stream);
+  int* out = static_cast<int*>(ws);
+  if (int rc = launch_batch_totals(G, node_counts, edge_counts, index_type, out, s)) return rc;
+  int host[5];
+  const int* from[5] = {out, out + 1, out + 2, out + 3, out + 4};
+  if (int rrc = read_back(s, 5, from, host)) return rrc;
+  if (host[4] & kErrIndex) return fail(TFG_ERR_INDEX_RANGE, "a node or edge count is negative");
+  *Nb = (int64_t)(uint32_t)host[0] | ((int64_t)host[1] << 32);
+  *E = (int64_t)(uint32_t)host[2] | ((int64_t)host[3] << 32);
+  return TFG_OK;
+}
+
 size_t tfg_propagate_ws_bytes(const tfg_graph* g, int64_t F, int64_t K) {
   if (!g || F < 0 || K < 0) return 0;
   const Graph& gr = g->g;

@@ -118,6 +118,49 @@ __global__ __launch_bounds__(kSmallThreads) void batch_offsets_small(
   if (threadIdx.x == 0) *err = any_bad ? kErrIndex : 0;
 }
 
+// Totals of both count arrays (one block, 64-bit sums): out[0..1] = the node
+// total as (low, high) 32-bit halves, out[2..3] the edge total, out[4] the
+// error flag (a negative count). The caller reads the five ints back.
+constexpr int kTotalThreads = 1024;
+template <typename IdxT>
+__global__ __launch_bounds__(kTotalThreads) void count_totals(const IdxT* __restrict__ nodes,
+                                                              const IdxT* __restrict__ edges,
+                                                              int64_t G, int* __restrict__ out) {
+  __shared__ long long part[2][kTotalThreads / kWave];
+  long long ns = 0, es = 0;
+  bool bad = false;
+  for (int64_t g = threadIdx.x; g < G; g += kTotalThreads) {
+    const long long n = (long long)nodes[g], e = (long long)edges[g];
+    bad |= n < 0 || e < 0;
+    ns += n;
+    es += e;
+  }
+  const bool any_bad = __syncthreads_or(bad);
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+    ns += __shfl_down(ns, off);
+    es += __shfl_down(es, off);
+  }
+  const int wave = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    part[0][wave] = ns;
+    part[1][wave] = es;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long tn = 0, te = 0;
+    for (int w = 0; w < kTotalThreads / kWave; ++w) {
+      tn += part[0][w];
+      te += part[1][w];
+    }
+    out[0] = (int)(unsigned)(tn & 0xffffffffll);
+    out[1] = (int)(tn >> 32);
+    out[2] = (int)(unsigned)(te & 0xffffffffll);
+    out[3] = (int)(te >> 32);
+    out[4] = any_bad ? kErrIndex : 0;
+  }
+}
+
 // Edges and nodes in one launch: thread i reindexes edge i and labels node i.
 template <typename IdxT>
 __global__ __launch_bounds__(kBlock) void batch_fill(const IdxT* __restrict__ src,
@@ -163,6 +206,20 @@ int launch_small(int64_t G, const void* node_counts, const void* edge_counts,
 }
 
 }  // namespace
+
+int launch_batch_totals(int64_t G, const void* node_counts, const void* edge_counts,
+                        int index_type, int* out, hipStream_t s) {
+  if (index_type == TFG_I64)
+    count_totals<int64_t><<<1, kTotalThreads, 0, s>>>(static_cast<const int64_t*>(node_counts),
+                                                       static_cast<const int64_t*>(edge_counts),
+                                                       G, out);
+  else
+    count_totals<int32_t><<<1, kTotalThreads, 0, s>>>(static_cast<const int32_t*>(node_counts),
+                                                       static_cast<const int32_t*>(edge_counts),
+                                                       G, out);
+  TFG_LAUNCHED("count_totals");
+  return TFG_OK;
+}
 
 size_t batch_ws_bytes(int64_t G) {
   const int64_t tiles = (G + 1 + 2047) / 2048;

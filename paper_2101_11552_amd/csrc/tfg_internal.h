@@ -191,6 +191,10 @@ int launch_gat_aggregate(const Graph& g, const float* h, int H, int D, const flo
                          hipStream_t s);
 // batch.hip
 size_t batch_ws_bytes(int64_t G);
+// Node and edge totals of the counts and a negative-count flag: five ints
+// (node total low, high; edge total low, high; flag) at `out`.
+int launch_batch_totals(int64_t G, const void* node_counts, const void* edge_counts,
+                        int index_type, int* out, hipStream_t s);
 // out_node_off / out_edge_off: NULL or [G + 1] copies of the offsets.
 int launch_batch_graphs(int64_t G, const void* node_counts, const void* edge_counts,
                         const void* local_edge_index, int index_type, int64_t E, int64_t Nb,

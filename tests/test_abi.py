@@ -147,11 +147,28 @@ def test_host_side_argument_errors(lib):
 
 
 def test_python_binding_rejects_host_tensors():
+    """Host tensors never reach a C call: every entry point of the binding
+    refuses them first."""
     import torch
     import paper_2101_11552_amd as tfg
     ei = torch.zeros((2, 3), dtype=torch.int64)
+    x = torch.zeros((4, 8))
     with pytest.raises(ValueError):
         tfg.tfg_graph_create(ei, 4)
+    with pytest.raises(ValueError):
+        tfg.tfg_aggregate(ei, x, 4)
+    with pytest.raises(ValueError):
+        tfg.tfg_gcn_norm(ei, 4)
+    with pytest.raises(ValueError):
+        tfg.tfg_segment_pool(x, torch.zeros(4, dtype=torch.int64), 1)
+    with pytest.raises(ValueError):
+        tfg.tfg_segment_softmax(torch.zeros(3), ei[1], 4)
+    with pytest.raises(ValueError):
+        tfg.tfg_batch_graphs(torch.ones(1, dtype=torch.int64), torch.ones(1, dtype=torch.int64),
+                             ei[:, :1])
+    with pytest.raises(ValueError):
+        tfg.tfg_batch_graphs_totals(torch.ones(1, dtype=torch.int64),
+                                    torch.ones(1, dtype=torch.int64))
 
 
 def test_missing_library_fails_loudly(tmp_path, monkeypatch):

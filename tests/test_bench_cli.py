@@ -5,6 +5,8 @@ import os
 import subprocess
 import sys
 
+import pytest
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
@@ -16,21 +18,21 @@ def test_bench_refuses_several_gpus():
     assert r.stdout == ""
 
 
-def test_threaded_oracle_baseline_is_bit_identical():
-    """The threaded CPU baseline splits target rows over threads; every row is
-    still summed over its edges in input order, so the result equals the
-    single-thread oracle bit for bit (ragged split: 97 rows over 5 threads)."""
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_threaded_oracle_is_bit_identical(reduce):
+    """The oracle split over threads by target range (the benchmark's threaded
+    CPU baseline and the full-size GPU checks) reduces every row over its
+    edges in input order, so it equals the single-thread oracle bit for bit
+    (ragged split: 97 rows over 5 threads)."""
     import numpy as np
     sys.path.insert(0, ROOT)
-    import bench
     import oracle
     rng = np.random.default_rng(7)
     n, E, F = 97, 2_000, 16
     ei = rng.integers(0, n, size=(2, E), dtype=np.int64)
     x = rng.standard_normal((n, F)).astype(np.float32)
     oei, ow, _ = oracle.gcn_norm(ei, n)
-    one, _ = oracle.aggregate(oei, x, n, "sum", edge_weight=ow)
+    one = oracle.aggregate(oei, x, n, reduce, edge_weight=ow)
     for threads in (1, 5, 8):
-        many = bench.oracle_sum_by_row_ranges(oei, ow, x, n, threads)
-        assert many.dtype == np.float64 and many.shape == (n, F)
-        assert np.array_equal(many, one)
+        many = oracle.aggregate_by_row_ranges(oei, x, n, reduce, edge_weight=ow, threads=threads)
+        assert all(m.dtype == o.dtype and np.array_equal(m, o) for m, o in zip(many, one))

@@ -4,15 +4,17 @@ the benchmark uses (graph handle with self-loops, CSR-order weights).
 Each stage is checked on its own: the oracle of a stage consumes the GPU's
 output of the previous stage (bit-identical inputs), so every stage is gated
 on its own error and argmax stays checkable bit for bit. The largest graph is
-checked on all normalised weights and degrees (bit-exact), on the full CSR
-permutation through properties that determine it uniquely, and on a sample of
-output rows that the oracle computes one by one.
+checked in full: the graph order, degrees and normalised weights bit for bit,
+and every output row of the aggregation, of its gradients and of the first
+propagation step against the oracle (threads split the oracle's rows or edges;
+the results are bit-identical to one thread).
 """
 
 import numpy as np
 import pytest
 
 import graphgen
+from graph_order import expected_graph
 from test_parity import assert_rel, assert_scaled, dev, host, same_bits
 
 pytestmark = pytest.mark.gpu
@@ -112,76 +114,110 @@ def c4():
     return graphgen.config4(dtype=np.int32)
 
 
-@pytest.mark.timeout(900)
-def test_power_law_full_size(tfg, orc, c4):
-    import torch
-    c = c4
-    ei, x, n = c["edge_index"], c["x"], c["N"]
-    E = ei.shape[1]
-    eid = dev(ei)
+@pytest.fixture(scope="module")
+def c4_norm_ref(orc, c4):
+    """The oracle's normalisation of the whole power-law graph: (edge_index'
+    [2, E'] with the self-loops appended, w' [E'], deg [N])."""
+    return orc.gcn_norm(c4["edge_index"], c4["N"])
+
+
+@pytest.fixture(scope="module")
+def c4_graph(tfg, c4):
+    """The graph handle and normalisation in the launch configuration the
+    benchmark times: self-loops, the library's source-part choice."""
+    eid = dev(c4["edge_index"])
+    n = c4["N"]
     g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
-    info = g.info()
-    assert info["E"] == E + n and info["n_rows_split"] > 0
     norm = tfg.tfg_gcn_norm(eid, n, graph=g)
+    return eid, g, norm
 
-    # graph order: sorted by (target, source part), a permutation, input order
-    # among equal keys -> unique
+
+@pytest.fixture(scope="module")
+def c4_sum_ref(orc, c4, c4_norm_ref):
+    """The oracle's sum aggregation A_hat x over every row (threads split the
+    rows; bit-identical to one thread): (out64, scale)."""
+    oei, ow, _ = c4_norm_ref
+    return orc.aggregate_by_row_ranges(oei, c4["x"], c4["N"], "sum", edge_weight=ow)
+
+
+@pytest.mark.timeout(900)
+def test_power_law_plain_csr_bit_exact(tfg, orc, c4, c4_norm_ref):
+    """One source part: the stable CSR by target (the paper's reduce key),
+    every rowptr, col and perm entry against the oracle at full size."""
+    n = c4["N"]
+    oei = c4_norm_ref[0]
+    g = tfg.tfg_graph_create(dev(c4["edge_index"]), n, add_self_loops=True, src_parts=1)
+    assert g.info()["src_parts"] == 1 and g.info()["E"] == oei.shape[1]
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    del g
+    r, c, p = orc.csr_by_target(oei, n)
+    assert np.array_equal(rowptr, r)
+    assert np.array_equal(perm, p)
+    assert np.array_equal(col, c)
+
+
+@pytest.mark.timeout(900)
+def test_power_law_graph_order_and_norm(tfg, orc, c4, c4_norm_ref, c4_graph):
+    """The timed handle (several source parts): its order equals the oracle's
+    plain CSR regrouped by source part inside each row, bit for bit; degrees
+    and normalised weights (COO and graph order) bit-exact on the whole graph."""
+    n = c4["N"]
+    oei, ow, odeg = c4_norm_ref
+    _, g, norm = c4_graph
+    info = g.info()
+    assert info["E"] == oei.shape[1] and info["n_rows_split"] > 0
     P = info["src_parts"]
-    R = -(-n // P)
-    rowptr, col, perm = tfg.tfg_graph_csr(g)
-    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
-    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
-    cnt = torch.bincount(tgt_full, minlength=n)
-    assert torch.equal(rowptr[1:].long() - rowptr[:-1].long(), cnt) and rowptr[0].item() == 0
-    pl = perm.long()
-    assert torch.equal(torch.bincount(pl, minlength=E + n), torch.ones(E + n, dtype=torch.long,
-                                                                     device=pl.device))
-    key = (tgt_full * P + src_full // R)[pl]
-    assert bool((key[1:] >= key[:-1]).all())
-    same_key = key[1:] == key[:-1]
-    assert bool((pl[1:][same_key] > pl[:-1][same_key]).all())
-    assert torch.equal(col.long(), src_full[pl])
-    if P > 1:
-        seg = tfg.tfg_graph_segments(g).long()
-        assert torch.equal(seg[1:] - seg[:-1], torch.bincount(tgt_full * P + src_full // R,
-                                                              minlength=n * P))
-    del tgt_full, src_full, pl, key, same_key
-
-    # degrees and weights: bit-exact against the oracle on the whole graph
-    oei, ow, odeg = orc.gcn_norm(ei, n)
+    assert P > 1 and info["n_part_items"] > 0  # the part plan is the one timed
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    r, c, p, seg = expected_graph(orc, oei, n, parts=P)
+    assert np.array_equal(rowptr, r)
+    assert np.array_equal(perm, p)
+    assert np.array_equal(col, c)
+    assert np.array_equal(host(tfg.tfg_graph_segments(g)), seg)
+    del r, c, seg
+    assert np.array_equal(host(norm["edge_index"]), oei)
     assert same_bits(host(norm["deg"]), odeg)
     assert same_bits(host(norm["edge_weight"]), ow)
-    assert same_bits(host(norm["edge_weight_csr"]), ow[host(perm)])
+    assert same_bits(host(norm["edge_weight_csr"]), ow[perm])
 
-    # aggregation: sampled rows (heaviest rows, split rows, random rows) one by one
-    assert info["src_parts"] > 1 and info["n_part_items"] > 0  # the part plan is the one timed
-    y = tfg.tfg_aggregate(None, dev(x), n, "sum",
-                          edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
-    deg = host(cnt)
-    rows = np.unique(np.concatenate([np.argsort(deg)[-40:], np.argsort(deg)[:20],
-                                     np.random.default_rng(0).choice(n, 1500, replace=False)]))
-    ref, S = orc.aggregate(oei, x, n, "sum", edge_weight=ow, rows=rows)
-    assert_scaled(host(y)[rows], ref, S, what="c4 sampled rows")
 
-    # invariant at full size: A_hat sqrt(deg) = sqrt(deg)
-    s = torch.sqrt(norm["deg"]).reshape(n, 1).repeat(1, 4).contiguous()
-    ys = tfg.tfg_aggregate(norm["edge_index"], s, n, "sum", edge_weight=norm["edge_weight_csr"],
+@pytest.mark.timeout(900)
+def test_power_law_aggregate_every_row(tfg, c4, c4_graph, c4_sum_ref):
+    """The timed aggregation (part plan, weights in graph order) on all
+    232,965 x 128 outputs against the oracle; the row plan on the same graph
+    likewise; the same call twice gives the same bits."""
+    import os
+    import torch
+    n = c4["N"]
+    _, g, norm = c4_graph
+    ref, S = c4_sum_ref
+    xd = dev(c4["x"])
+    kw = dict(edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
+    y = tfg.tfg_aggregate(None, xd, n, "sum", **kw)
+    assert_scaled(host(y), ref, S, what="c4 every row, part plan")
+    y2 = tfg.tfg_aggregate(None, xd, n, "sum", **kw)
+    assert torch.equal(y, y2)
+    os.environ["TFG_PART_PLAN"] = "0"
+    try:
+        y3 = tfg.tfg_aggregate(None, xd, n, "sum", **kw)
+    finally:
+        del os.environ["TFG_PART_PLAN"]
+    assert_scaled(host(y3), ref, S, what="c4 every row, row plan")
+
+
+@pytest.mark.timeout(900)
+def test_power_law_sqrt_deg_fixed_point(tfg, c4, c4_graph):
+    """A_hat sqrt(deg) = sqrt(deg) on every row, at F = 128 so that the
+    gathered table (119 MB) takes the part plan, as timed."""
+    import torch
+    n = c4["N"]
+    _, g, norm = c4_graph
+    s = torch.sqrt(norm["deg"]).reshape(n, 1).repeat(1, c4["x"].shape[1]).contiguous()
+    assert s.numel() * 4 >= 32 << 20
+    ys = tfg.tfg_aggregate(None, s, n, "sum", edge_weight=norm["edge_weight_csr"],
                            weight_order="csr", graph=g)
     rel = (ys - s).abs() / s
     assert float(rel.max()) <= 1e-5
-    # determinism
-    y2 = tfg.tfg_aggregate(None, dev(x), n, "sum",
-                           edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
-    assert torch.equal(y, y2)
-    # the row plan on the same graph agrees within the tolerance
-    import os
-    os.environ["TFG_PART_PLAN"] = "0"
-    try:
-        y3 = tfg.tfg_aggregate(None, dev(x), n, "sum",
-                               edge_weight=norm["edge_weight_csr"], weight_order="csr", graph=g)
-    finally:
-        del os.environ["TFG_PART_PLAN"]
-    assert_scaled(host(y3)[rows], ref, S, what="c4 sampled rows, row plan")
 
 
 def test_power_law_int64_ids_match_int32(tfg, c4):
@@ -214,59 +250,67 @@ def test_gat_attention_fused(tfg, orc):
     assert_scaled(host(out), ref, S, what="c3 fused attention layer")
 
 
+def _dw_by_edge_ranges(orc, edge_index, x, n, dy, threads):
+    """The oracle's dw of a sum aggregation for every edge, and its error
+    scale (the same dot products over |x| and |dy|), computed over ranges of
+    edges in threads: an edge's gradient depends on that edge alone."""
+    from concurrent.futures import ThreadPoolExecutor
+    E = edge_index.shape[1]
+    bounds = [E * i // threads for i in range(threads + 1)]
+    ax, ady = np.abs(x), np.abs(dy)
+
+    def chunk(i):
+        sub = np.ascontiguousarray(edge_index[:, bounds[i]:bounds[i + 1]])
+        d = orc.aggregate_backward(sub, x, n, dy, "sum")[1][:, 0]
+        sc = orc.aggregate_backward(sub, ax, n, ady, "sum")[1][:, 0]
+        return d, sc
+
+    with ThreadPoolExecutor(threads) as pool:
+        parts = list(pool.map(chunk, range(threads)))
+    return np.concatenate([q[0] for q in parts]), np.concatenate([q[1] for q in parts])
+
+
 @pytest.mark.timeout(900)
-def test_power_law_backward_and_propagation_full_size(tfg, orc, c4):
+def test_power_law_backward_and_propagation_full_size(tfg, orc, c4, c4_norm_ref, c4_graph,
+                                                       c4_sum_ref):
     """The backward aggregation and APPNP propagation at full size, as timed
     by the benchmark: dx over the transposed graph with the normalised
-    weights in its order, dw in graph order, APPNP K = 3."""
-    import torch
-    ei, x, n = c4["edge_index"], c4["x"], c4["N"]
-    E = ei.shape[1]
-    eid = dev(ei)
-    g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+    weights in its order (every source row), dw in graph order (every
+    position), APPNP K = 3 (the first step on every row; the K-step call
+    equals three chained steps bit for bit)."""
+    x, n = c4["x"], c4["N"]
+    oei, ow, _ = c4_norm_ref
+    eid, g, norm = c4_graph
     gt = tfg.tfg_graph_create_transposed(eid, n, add_self_loops=True)
-    norm = tfg.tfg_gcn_norm(eid, n, graph=g)
-    oei, ow, _ = orc.gcn_norm(ei, n)
 
-    # the transposed graph: rows are sources, stable order of (source, target part)
+    # the transposed graph: the oracle's plain CSR of the reversed edges,
+    # regrouped by target part inside each source row
     P = gt.info()["src_parts"]
-    R = -(-n // P)
-    trow, tcol, tperm = tfg.tfg_graph_csr(gt)
-    src_full = torch.cat([eid[0], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
-    tgt_full = torch.cat([eid[1], torch.arange(n, device=eid.device, dtype=torch.int32)]).long()
-    assert torch.equal(trow[1:].long() - trow[:-1].long(), torch.bincount(src_full, minlength=n))
-    pl = tperm.long()
-    key = (src_full * P + tgt_full // R)[pl]
-    assert bool((key[1:] >= key[:-1]).all())
-    same_key = key[1:] == key[:-1]
-    assert bool((pl[1:][same_key] > pl[:-1][same_key]).all())
-    assert torch.equal(tcol.long(), tgt_full[pl])
-    del src_full, tgt_full, pl, key, same_key
+    trow, tcol, tperm = (host(t) for t in tfg.tfg_graph_csr(gt))
+    r, c, p, _ = expected_graph(orc, oei[::-1], n, parts=P)
+    assert np.array_equal(trow, r) and np.array_equal(tperm, p) and np.array_equal(tcol, c)
+    del r, c, p, trow, tcol
 
     w_t = tfg.tfg_edge_reorder(norm["edge_weight_csr"], src=g, dst=gt)
-    assert same_bits(host(w_t), ow[host(tperm)])
+    assert same_bits(host(w_t), ow[tperm])
+    del tperm
     dy = graphgen.features(2004, n, x.shape[1])
     xd, dyd = dev(x), dev(dy)
     dx, _ = tfg.tfg_aggregate_backward(g, dyd, "sum", graph_t=gt, edge_weight=w_t,
                                        weight_order="csr_t")
     _, dw = tfg.tfg_aggregate_backward(g, dyd, "sum", x=xd, want_dx=False, want_dw=True,
                                        dw_order="csr")
-    torch.cuda.synchronize()
-    outdeg = np.bincount(np.concatenate([ei[0], np.arange(n)]), minlength=n)
-    rows = np.unique(np.concatenate([np.argsort(outdeg)[-30:],
-                                     np.random.default_rng(1).choice(n, 1000, replace=False)]))
     # dx of a sum aggregation is the aggregation over the reversed edges (pinned on the CPU)
-    ref, S = orc.aggregate(oei[::-1], dy, n, "sum", edge_weight=ow, rows=rows)
-    assert_scaled(host(dx)[rows], ref, S, what="c4 dx sampled sources")
-    # dw: sampled graph positions, each a dot product of two rows
-    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
-    ks = np.random.default_rng(2).choice(E + n, 4000, replace=False)
-    ts = np.searchsorted(rowptr, ks, side="right") - 1
-    terms = dy[ts].astype(np.float64) * x[col[ks]].astype(np.float64)
-    assert_scaled(host(dw)[ks, 0], terms.sum(1), np.abs(terms).sum(1), what="c4 dw sampled edges")
+    ref, S = orc.aggregate_by_row_ranges(oei[::-1], dy, n, "sum", edge_weight=ow)
+    assert_scaled(host(dx), ref, S, what="c4 dx, every source row")
+    del ref, S, dx
+    # dw: every graph position, each a dot product of a dy row and an x row
+    perm = host(tfg.tfg_graph_csr(g)[2])
+    ref_dw, S_dw = _dw_by_edge_ranges(orc, oei, x, n, dy, orc.host_threads())
+    assert_scaled(host(dw)[:, 0], ref_dw[perm], S_dw[perm], what="c4 dw, every position")
+    del ref_dw, S_dw, dw, perm
 
-    # APPNP, K = 3, alpha = 0.1: the K-step call equals three chained steps bit for bit,
-    # and the first step matches the oracle on sampled rows
+    # APPNP, K = 3, alpha = 0.1
     alpha = 0.1
     w_csr = norm["edge_weight_csr"]
     z3 = tfg.tfg_propagate(g, xd, 3, alpha=alpha, h=xd, edge_weight=w_csr)
@@ -276,10 +320,11 @@ def test_power_law_backward_and_propagation_full_size(tfg, orc, c4):
         if k == 0:
             z1 = host(z)
     assert same_bits(host(z3), host(z))
-    agg, S = orc.aggregate(oei, x, n, "sum", edge_weight=ow, rows=rows)
-    ref = (1 - np.float64(np.float32(alpha))) * agg + np.float64(np.float32(alpha)) * x[rows]
-    S = (1 - alpha) * S + alpha * np.abs(x[rows])
-    assert_scaled(z1[rows], ref, S, what="c4 APPNP first step")
+    agg, S = c4_sum_ref
+    a32 = np.float64(np.float32(alpha))
+    ref = (1 - a32) * agg + a32 * x
+    S = (1 - a32) * S + a32 * np.abs(x)
+    assert_scaled(z1, ref, S, what="c4 APPNP first step, every row")
 
 
 def test_transformer_attention_full_size(tfg, orc):

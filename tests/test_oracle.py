@@ -60,16 +60,20 @@ def test_csr_is_numpy_stable_argsort(orc, seed, n, e):
 
 @pytest.mark.parametrize("seed,n,n_src,e,parts", [(5, 40, 40, 3000, 2), (6, 300, 77, 9000, 3),
                                                  (7, 1000, 5000, 20000, 8), (8, 9, 9, 50, 9)])
-def test_csr_by_source_part_is_numpy_stable_argsort(orc, seed, n, n_src, e, parts):
+def test_part_order_from_plain_csr(orc, seed, n, n_src, e, parts):
+    """The tests' regrouping of the oracle's plain CSR into the (target, source
+    part) order of a handle with several source parts equals numpy's stable
+    argsort of that composite key over the edge list."""
+    from graph_order import expected_graph, part_rows
     ei = graphgen.random_graph(seed, n, e, n_src=n_src)
-    rowptr, col, perm, seg = orc.csr_by_target(ei, n, parts=parts, n_src=n_src)
-    part_rows = -(-n_src // parts)
-    key = ei[1] * parts + ei[0] // part_rows
+    rowptr, col, perm, seg = expected_graph(orc, ei, n, parts=parts, n_src=n_src)
+    key = ei[1] * parts + ei[0] // part_rows(n_src, parts)
     ref = np.argsort(key, kind="stable")
     np.testing.assert_array_equal(perm, ref)
     np.testing.assert_array_equal(col, ei[0][ref])
     np.testing.assert_array_equal(np.diff(seg), np.bincount(key, minlength=n * parts))
-    # rows are the same as in the plain CSR; only the order inside a row changes
+    np.testing.assert_array_equal(rowptr, seg[::parts])
+    # the rows are those of the plain CSR; only the order inside a row changes
     r1, _, p1 = orc.csr_by_target(ei, n, n_src=n_src)
     np.testing.assert_array_equal(rowptr, r1)
     for t in range(0, n, max(1, n // 17)):
