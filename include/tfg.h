@@ -247,6 +247,27 @@ int tfg_aggregate(const void *edge_index, int index_type, int64_t E, const float
                   int64_t ldx, int64_t N, int reduce, const tfg_graph *g, float *out,
                   int32_t *argmax, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * aggregation as tfg_aggregate on a cached graph, with the same kernels and
+ * bit-identical results, but no workspace argument. The partial rows that
+ * tfg_aggregate keeps in `ws` go to a static device array of the library,
+ * TFG_NOALLOC_SCRATCH_BYTES bytes on every GPU it runs on, held until the
+ * process ends. The call allocates nothing and does not synchronise.
+ * g is required (the functional form would need a transient graph); the other
+ * arguments are those of tfg_aggregate. A graph and width whose partial rows
+ * (the workspace tfg_aggregate_ws_bytes reports, for that handle) exceed the
+ * limit give TFG_ERR_WORKSPACE before any launch.
+ * Calls that overlap on one GPU (two streams, two threads) share the one
+ * array and race: order them on one stream, or use tfg_aggregate.
+ */
+#define TFG_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int tfg_aggregate_noalloc(const void *edge_index, int index_type, int64_t E,
+                          const float *edge_weight, int64_t H, int weight_order, const float *x,
+                          int64_t N_src, int64_t F, int64_t ldx, int64_t N, int reduce,
+                          const tfg_graph *g, float *out, int32_t *argmax, tfg_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Backward aggregation                                                      */
 /* ------------------------------------------------------------------------ */

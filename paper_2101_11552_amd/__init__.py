@@ -21,7 +21,7 @@ __all__ = [
     "tfg_graph_bytes", "tfg_graph_create", "tfg_graph_create_transposed", "tfg_graph_csr",
     "tfg_edge_reorder", "tfg_graph_segments", "tfg_check",
     "tfg_gcn_norm",
-    "tfg_aggregate_ws_bytes", "tfg_aggregate", "tfg_aggregate_backward",
+    "tfg_aggregate_ws_bytes", "tfg_aggregate", "tfg_aggregate_noalloc", "tfg_aggregate_backward",
     "tfg_gat_edge_scores", "tfg_segment_softmax", "tfg_segment_softmax_backward",
     "tfg_segment_pool", "tfg_segment_pool_backward",
     "tfg_batch_graphs", "tfg_batch_graphs_totals", "tfg_propagate", "tfg_gat_aggregate",
@@ -86,6 +86,8 @@ def load():
         "tfg_aggregate_ws_bytes": (sz, [i64, i64, i64, i64, ci, p]),
         "tfg_aggregate": (ci, [p, ci, i64, p, i64, ci, p, i64, i64, i64, i64, ci, p, p, p, p,
                                sz, p]),
+        "tfg_aggregate_noalloc": (ci, [p, ci, i64, p, i64, ci, p, i64, i64, i64, i64, ci, p, p,
+                                       p, p]),
         "tfg_gat_edge_scores_ws_bytes": (sz, [i64, i64]),
         "tfg_gat_edge_scores": (ci, [p, ci, i64, p, i64, i64, i64, p, p, ctypes.c_float, p, p,
                                      sz, p]),
@@ -425,6 +427,43 @@ def tfg_aggregate(edge_index: torch.Tensor | None, x: torch.Tensor, N: int, redu
                              _ptr(x), N_src, F, ldx, N, red, h, _ptr(out),
                              _ptr(argmax) if red == 2 else None, _ptr(ws), _nbytes(ws),
                              _stream(dev)))
+    return (out, argmax) if red == 2 else out
+
+
+def tfg_aggregate_noalloc(edge_index: torch.Tensor | None, x: torch.Tensor, N: int,
+                          graph: Graph, reduce: str = "sum",
+                          edge_weight: torch.Tensor | None = None, heads: int = 1,
+                          weight_order: str = "coo", out: torch.Tensor | None = None,
+                          argmax: torch.Tensor | None = None):
+    """``tfg_aggregate`` on a cached graph through the entry point that
+    allocates nothing: its partial rows live in the library's static device
+    scratch (TFG_NOALLOC_SCRATCH_BYTES per GPU). Pass ``out`` (and ``argmax``
+    for max) to keep the call free of allocations on this side too."""
+    lib = load()
+    if graph is None:
+        raise ValueError("the no-allocation aggregation needs a graph handle")
+    x, ldx = _rows(x, "x", graph.device)
+    dev = x.device
+    ei = None
+    if edge_index is not None:
+        ei = _edges(edge_index)
+        _dev(ei, "edge_index", dev)
+    N_src, F = x.shape
+    w = _f32(edge_weight, "edge_weight", dev)
+    if w is not None and w.numel() != graph.E * heads:
+        raise ValueError(f"edge_weight must hold E * heads = {graph.E * heads} values")
+    red = _REDUCE[reduce]
+    if out is None:
+        out = torch.empty((N, F), dtype=torch.float32, device=dev)
+    _out(out, (N, F), torch.float32, dev, "out")
+    if red == 2:
+        if argmax is None:
+            argmax = torch.empty((N, F), dtype=torch.int32, device=dev)
+        _out(argmax, (N, F), torch.int32, dev, "argmax")
+    _check(lib.tfg_aggregate_noalloc(_ptr(ei), _index_type(ei) if ei is not None else 0, graph.E,
+                                     _ptr(w), heads, _ORDER[weight_order], _ptr(x), N_src, F,
+                                     ldx, N, red, graph.handle, _ptr(out),
+                                     _ptr(argmax) if red == 2 else None, _stream(dev)))
     return (out, argmax) if red == 2 else out
 
 

@@ -5,11 +5,23 @@
 // fixup_rows combines in a fixed order. No floating-point atomics: every
 // output is reproducible bit for bit.
 #include <cstdlib>
+#include <mutex>
 
 #include "spmm.h"
 
 namespace tfg {
 namespace {
+
+// Device memory of the no-allocation aggregation (tfg_aggregate_noalloc): the
+// partial rows that tfg_aggregate keeps in its workspace. Every GPU the
+// library runs on holds its own copy until the process ends. In host code the
+// name only stands for the symbol: kernels get the device address that
+// hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) unsigned char scratch[TFG_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
 
 using namespace rows;
 
@@ -96,6 +108,21 @@ void dispatch_kind(bool mx, bool heads, int vec, int slots, dim3 grid, hipStream
 }
 
 }  // namespace
+
+int noalloc_scratch(void** ptr) {
+  int dev = 0;
+  TFG_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(TFG_ERR_INVALID_ARG, "device id out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    TFG_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return fail(TFG_ERR_HIP, "no device address for the static scratch");
+    g_scratch_addr[dev] = p;
+  }
+  *ptr = g_scratch_addr[dev];
+  return TFG_OK;
+}
 
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce) {
   size_t per = sizeof(float) + (reduce == TFG_MAX ? sizeof(int) : 0);

@@ -382,10 +382,16 @@ size_t tfg_aggregate_ws_bytes(int64_t E, int64_t N_src, int64_t N, int64_t F, in
   return aggregate_ws_needed(E, N, N_src, F, reduce, g);
 }
 
-int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float* edge_weight,
-                  int64_t H, int weight_order, const float* x, int64_t N_src, int64_t F,
-                  int64_t ldx, int64_t N, int reduce, const tfg_graph* g, float* out,
-                  int32_t* argmax, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+}  // extern "C"
+
+namespace tfg {
+namespace {
+
+// The host-side argument checks of tfg_aggregate and tfg_aggregate_noalloc.
+int check_aggregate_args(const void* edge_index, int index_type, int64_t E,
+                         const float* edge_weight, int64_t H, int weight_order, const float* x,
+                         int64_t N_src, int64_t F, int64_t ldx, int64_t N, int reduce,
+                         const tfg_graph* g, const float* out) {
   if (bad_index_type(index_type)) return fail(TFG_ERR_INVALID_ARG, "bad index type");
   int rc = check_counts(E, N, N_src);
   if (rc) return rc;
@@ -402,6 +408,52 @@ int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float
   if (E > 0 && F > 0 && x == nullptr) return fail(TFG_ERR_INVALID_ARG, "x is NULL");
   if (weight_order == TFG_CSR && edge_weight && !g)
     return fail(TFG_ERR_INVALID_ARG, "CSR-order weights need a graph handle");
+  (void)edge_weight;
+  return TFG_OK;
+}
+
+// A handle built with loops describes the E' = E_in + N edges of this list.
+int check_handle_sizes(const Graph& g, int64_t E, int64_t N, int64_t N_src) {
+  if (g.E != E || g.N != N || g.N_src != N_src)
+    return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
+  return check_device(g);
+}
+
+}  // namespace
+}  // namespace tfg
+
+extern "C" {
+
+int tfg_aggregate_noalloc(const void* edge_index, int index_type, int64_t E,
+                          const float* edge_weight, int64_t H, int weight_order, const float* x,
+                          int64_t N_src, int64_t F, int64_t ldx, int64_t N, int reduce,
+                          const tfg_graph* g, float* out, int32_t* argmax, tfg_stream_t stream) {
+  int rc = check_aggregate_args(edge_index, index_type, E, edge_weight, H, weight_order, x, N_src,
+                                F, ldx, N, reduce, g, out);
+  if (rc) return rc;
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "the no-allocation aggregation needs a graph handle");
+  if (H > 1 && !edge_weight) H = 1;
+  const Graph& gr = g->g;
+  if ((rc = check_handle_sizes(gr, E, N, N_src))) return rc;
+  const size_t need = aggregate_partial_bytes(partials_needed(E, N, N_src, F, g), F, reduce);
+  if (need > (size_t)TFG_NOALLOC_SCRATCH_BYTES)
+    return fail(TFG_ERR_WORKSPACE, "the partial rows of this graph (" + std::to_string(need) +
+                                       " bytes) exceed the static scratch (" +
+                                       std::to_string((size_t)TFG_NOALLOC_SCRATCH_BYTES) +
+                                       " bytes); use tfg_aggregate with a workspace");
+  void* part = nullptr;
+  if ((rc = noalloc_scratch(&part))) return rc;
+  return launch_aggregate(gr, edge_weight, (int)H, weight_order, x, F, ldx, reduce, out, argmax,
+                          part, as_stream(stream));
+}
+
+int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float* edge_weight,
+                  int64_t H, int weight_order, const float* x, int64_t N_src, int64_t F,
+                  int64_t ldx, int64_t N, int reduce, const tfg_graph* g, float* out,
+                  int32_t* argmax, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  int rc = check_aggregate_args(edge_index, index_type, E, edge_weight, H, weight_order, x, N_src,
+                                F, ldx, N, reduce, g, out);
+  if (rc) return rc;
   if (H > 1 && !edge_weight) H = 1;
   if (int wrc = check_ws(ws, ws_bytes, aggregate_ws_needed(E, N, N_src, F, reduce, g))) return wrc;
   hipStream_t s = as_stream(stream);
@@ -410,11 +462,8 @@ int tfg_aggregate(const void* edge_index, int index_type, int64_t E, const float
   const Graph* gp = nullptr;
   void* part = c.take(aggregate_partial_bytes(partials_needed(E, N, N_src, F, g), F, reduce));
   if (g) {
-    // a handle built with loops describes the E' = E_in + N edges of this list
     gp = &g->g;
-    if (gp->E != E || gp->N != N || gp->N_src != N_src)
-      return fail(TFG_ERR_INVALID_ARG, "graph handle does not match the edge list sizes");
-    if (int e = check_device(*gp)) return e;
+    if ((rc = check_handle_sizes(*gp, E, N, N_src))) return rc;
   } else {
     rc = graph_or_transient(nullptr, tmp, gp, edge_index, tgt_row(edge_index, index_type, E),
                             index_type, E, N_src, N, 0, c, s);

@@ -137,6 +137,9 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
                      void* ws, hipStream_t s, float scale = 1.0f, float alpha = 0.0f,
                      const float* h = nullptr, int64_t ldh = 0, const int32_t* mask = nullptr);
 size_t aggregate_partial_bytes(int64_t n_partials, int64_t F, int reduce);
+// Device address, on the current device, of the library's static scratch
+// (TFG_NOALLOC_SCRATCH_BYTES bytes); looked up once per device.
+int noalloc_scratch(void** ptr);
 // Whether an aggregation over g with F features uses the part plan.
 bool use_part_plan(const Graph& g, int64_t F);
 // softmax.hip
