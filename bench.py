@@ -39,6 +39,94 @@ def algorithmic_bytes(E_total: int, N: int, F: int) -> int:
     return E_total * (8 + 4 * F) + N * 4 * F + 4 * (N + 1)
 
 
+def compulsory_bytes(E_total: int, N: int, N_src: int, F: int, n_items: int) -> int:
+    """Bytes one aggregation launch must move to or from memory at least: the
+    column index and weight of every edge, x once, the output, the row or
+    segment pointers and the work items (16 bytes each). Gathered rows that
+    the caches serve again are not counted, nor the part plan's partial rows
+    (reported apart)."""
+    return E_total * 8 + N_src * 4 * F + N * 4 * F + 4 * (N + 1) + 16 * n_items
+
+
+def part_plan_items(segptr: np.ndarray, N: int, P: int, chunk: int) -> np.ndarray:
+    """(kbeg, kend) of the part plan's work items in dispatch order: part by
+    part, row by row, each (row, part) segment cut into chunks of `chunk`."""
+    seg = segptr.astype(np.int64)
+    start = seg[:-1].reshape(N, P).T.reshape(-1)  # part-major
+    end = seg[1:].reshape(N, P).T.reshape(-1)
+    length = end - start
+    nch = (length + chunk - 1) // chunk
+    first = np.repeat(start, nch)
+    idx = np.arange(first.size) - np.repeat(np.cumsum(nch) - nch, nch)
+    kb = first + idx * chunk
+    ke = np.minimum(kb + chunk, np.repeat(end, nch))
+    return np.stack([kb, ke], axis=1).astype(np.int32)
+
+
+def probe_lib():
+    import ctypes
+    path = os.path.join(ROOT, "paper_2101_11552_amd", "libtfg_probe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    p, i64 = ctypes.c_void_p, ctypes.c_int64
+    lib.tfg_probe_gather_window.argtypes = [p, i64, i64, i64, i64, p, p]
+    lib.tfg_probe_gather_items.argtypes = [p, p, p, i64, p, p]
+    return lib
+
+
+def gather_ceiling(torch, x, items=None, col=None, reps: int = 5):
+    """Rates (GB/s of 512-byte rows) of bare row gathers from x, the
+    aggregation's table: E' rows drawn uniformly from a window that moves
+    every E'/P gathers, for windows from the whole table down to 256 rows;
+    with (items, col), also the part plan's own row stream. Each figure is
+    the best of `reps` timed launches (HIP events on the launch stream)."""
+    import ctypes
+    lib = probe_lib()
+    N, F = x.shape
+    assert F == 128
+    n = int(items.shape[0]) if items is not None else 0
+    n_gathers = int(col.shape[0]) if col is not None else 114_832_965
+    sink = torch.empty(max((n_gathers + 127) // 128, n, 1), dtype=torch.float32, device=x.device)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {}
+
+    def best(fn):
+        ts = []
+        for _ in range(reps + 1):
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record()
+            rc = fn()
+            a1.record()
+            assert rc == 0, rc
+            torch.cuda.synchronize()
+            ts.append(a0.elapsed_time(a1))
+        return min(ts[1:])
+
+    for name, wr in (("table", N), ("table/8", -(-N // 8)), ("table/16", -(-N // 16)),
+                     ("table/32", -(-N // 32)), ("table/64", -(-N // 64)),
+                     ("table/128", -(-N // 128)), ("1024 rows", 1024), ("256 rows", 256)):
+        windows = -(-N // wr)
+        per = -(-n_gathers // windows)
+        per = -(-per // 128) * 128
+        ms = best(lambda: lib.tfg_probe_gather_window(ctypes.c_void_p(x.data_ptr()), N, wr,
+                                                      n_gathers, per,
+                                                      ctypes.c_void_p(sink.data_ptr()), stream))
+        out[name] = {"ms": round(ms, 4), "GBps": round(n_gathers * 4 * F / (ms * 1e-3) / 1e9, 1),
+                     "window_rows": wr}
+    if items is not None:
+        it = torch.from_numpy(items).to(x.device)
+        ms = best(lambda: lib.tfg_probe_gather_items(ctypes.c_void_p(x.data_ptr()),
+                                                     ctypes.c_void_p(col.data_ptr()),
+                                                     ctypes.c_void_p(it.data_ptr()), n,
+                                                     ctypes.c_void_p(sink.data_ptr()), stream))
+        out["part plan stream"] = {"ms": round(ms, 4),
+                                   "GBps": round(n_gathers * 4 * F / (ms * 1e-3) / 1e9, 1),
+                                   "items": n}
+    return out
+
+
 def row_chunk() -> int:
     """Edges per work item of the row plan (the library's default unless
     TFG_ROW_CHUNK overrides it)."""
@@ -396,6 +484,30 @@ def run_suite(args):
              f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb)
 
 
+def run_ceiling(args):
+    """The gather probes on the power-law workload's table and graph, with
+    more repetitions than the headline run takes: one JSON line."""
+    import torch
+    import paper_2101_11552_amd as tfg
+    tfg.load()
+    dev = torch.device("cuda:0")
+    ei_np, x_np = load_workload(args.cache)
+    N, F = x_np.shape
+    ei = torch.from_numpy(ei_np).to(dev)
+    x = torch.from_numpy(x_np).to(dev)
+    g = tfg.tfg_graph_create(ei, N, add_self_loops=True, src_parts=args.src_parts)
+    info = g.info()
+    P = info["src_parts"]
+    items = col = None
+    if P > 1:
+        items = part_plan_items(tfg.tfg_graph_segments(g).cpu().numpy(), N, P, row_chunk())
+        col = tfg.tfg_graph_csr(g)[1]
+    res = gather_ceiling(torch, x, items, col, reps=max(args.steps, 5))
+    print(json.dumps({"row": "gather ceiling", "workload": f"power-law table [{N}, {F}] float32, "
+                      f"{info['E']} gathers of 512-byte rows", "src_parts": P, "probes": res}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -410,6 +522,8 @@ def main():
                     help="source parts of the graph (0: the library's choice)")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the headline line, one line per other measured row")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="instead of the headline line, the gather-ceiling probes (one line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: runs on one GPU only; --gpus {args.gpus} is not supported",
@@ -417,6 +531,9 @@ def main():
         sys.exit(2)
     if args.suite:
         run_suite(args)
+        return
+    if args.ceiling:
+        run_ceiling(args)
         return
 
     import torch
@@ -509,9 +626,26 @@ def main():
     each = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(reps))
 
     B = algorithmic_bytes(E_total, N, F)
-    achieved = B / (agg_ms * 1e-3) / 1e9
     value = E_total / (ms_step * 1e-3) / 1e9
     traffic = stored_traffic()
+    P = info["src_parts"]
+    n_items = info["n_part_items"] if P > 1 else info["n_chunks"] + N
+    n_partials = info["n_part_items"] if P > 1 else info["n_chunks"]
+    C = compulsory_bytes(E_total, N, N, F, n_items)
+    partial_bytes = 2 * n_partials * 4 * F  # written once, read once by the fix-up
+    achieved = C / (agg_ms * 1e-3) / 1e9
+    gathered = E_total * 4 * F
+    gather_rate = gathered / (agg_ms * 1e-3) / 1e9
+    # the gather ceiling, measured in this run: bare gathers of the same number
+    # of rows from the same table (random windows, and the part plan's stream)
+    items = col = None
+    if P > 1:
+        seg = tfg.tfg_graph_segments(g).cpu().numpy()
+        items = part_plan_items(seg, N, P, row_chunk())
+        col = tfg.tfg_graph_csr(g)[1]
+    ceil = gather_ceiling(torch, x, items, col)
+    del col
+    ceiling_name, ceiling = max(((k, v["GBps"]) for k, v in ceil.items()), key=lambda kv: kv[1])
 
     cpu = cpu_mt = None
     if not args.no_cpu_baseline:
@@ -548,17 +682,29 @@ def main():
                                    "n_part_items": info["n_part_items"],
                                    "n_chunks": info["n_chunks"],
                                    "n_rows_split": info["n_rows_split"]},
+        # achieved / frac: the bytes the aggregation must move to or from HBM (col,
+        # weights, x once, out, pointers, work items) per call against 8 TB/s. The
+        # gathered rows (one 512-byte row per edge) are served by the L2s and the
+        # Infinity Cache: their rate is set against the measured gather ceiling.
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
-                     # the bytes the L2s move to and from memory (Infinity Cache and HBM
-                     # together) per launch, as a rate against the same peak
+                     "traffic_source": ("stored: profiles/traffic_spmm_rows_c4.txt, rocprofv3 "
+                                        "FETCH_SIZE + WRITE_SIZE per launch, taken on the "
+                                        "current kernel source" if traffic else None),
                      "traffic_GBps": (round(traffic / (agg_ms * 1e-3) / 1e9, 1)
                                       if traffic else None),
-                     "traffic_frac": (round(traffic / (agg_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)
-                                      if traffic else None),
                      "kernel": "tfg_aggregate (spmm_rows + fixup_rows)",
-                     "algorithmic_bytes_per_launch": B},
+                     "compulsory_bytes_per_launch": C,
+                     "partial_row_bytes_per_launch": partial_bytes,
+                     "frac_with_partials": round((C + partial_bytes) / (agg_ms * 1e-3) / 1e9
+                                                 / PEAK_HBM_GBPS, 4),
+                     "gather": {"bytes_per_launch": gathered, "achieved": round(gather_rate, 1),
+                                "ceiling": ceiling, "ceiling_from": ceiling_name,
+                                "frac": round(gather_rate / ceiling, 4), "unit": "GB/s",
+                                "probes": ceil},
+                     "algorithmic_bytes_per_launch": B,
+                     "algorithmic_GBps": round(B / (agg_ms * 1e-3) / 1e9, 1)},
         "cpu_baseline": cpu,
         "cpu_baseline_threads": cpu_mt,
     }

@@ -1,4 +1,5 @@
-"""Builds libtfg.so (the HIP library behind include/tfg.h) for gfx950 in-tree.
+"""Builds libtfg.so (the HIP library behind include/tfg.h) and libtfg_probe.so
+(the benchmark's gather probes, include/tfg_probe.h) for gfx950 in-tree.
 
 Every translation unit is compiled by hipcc to an object file (in parallel),
 then linked into a shared library next to this file.
@@ -16,6 +17,9 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libtfg.so")
 SOURCES = ["csr.hip", "norm.hip", "aggregate.hip", "aggregate_short.hip", "softmax.hip",
            "gat.hip", "pool.hip", "batch.hip", "backward.hip", "api.cpp"]
+# measurement probes for the benchmark (include/tfg_probe.h), a library of their own
+PROBE_LIB = os.path.join(HERE, "libtfg_probe.so")
+PROBE_SOURCES = ["probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [
@@ -36,18 +40,25 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str) -> None:
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(_compile, srcs))
+    _link(objs[:len(SOURCES)], LIB)
+    _link(objs[len(SOURCES):], PROBE_LIB)
     if verbose:
         print(LIB)
+        print(PROBE_LIB)
     return LIB
 
 

@@ -1,0 +1,126 @@
+// Gather probes (libtfg_probe.so, declared in include/tfg_probe.h): the row
+// gathers of the sum aggregation with nothing else, to measure their ceiling.
+// Lane layout of the aggregation at F = 128: two edge slots of 32 lanes per
+// wavefront, each lane a 16-byte piece of the row.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/tfg_probe.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kSlots = 2;
+constexpr int kItem = 128;  // gathers per wavefront (one row-plan work item)
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t mix(uint32_t v) {
+  // an integer hash (xorshift-multiply rounds) giving a uniform 32-bit value
+  v ^= v >> 16;
+  v *= 0x7feb352dU;
+  v ^= v >> 15;
+  v *= 0x846ca68bU;
+  v ^= v >> 16;
+  return v;
+}
+
+template <int U>
+__global__ __launch_bounds__(kWave) void gather_window(const float* __restrict__ x, int64_t rows,
+                                                       int64_t window_rows, int64_t n_gathers,
+                                                       int64_t per_window, float* __restrict__ sink) {
+  const int64_t item = blockIdx.x;
+  const int lane = threadIdx.x, slot = lane / 32, sl = lane % 32;
+  const int64_t e0 = item * kItem;
+  const int n = (int)min<int64_t>(kItem, n_gathers - e0);
+  // per_window is a multiple of kItem: one window per wavefront
+  const int64_t windows = (rows + window_rows - 1) / window_rows;
+  const int64_t base = ((e0 / per_window) % windows) * window_rows;
+  const uint32_t span = (uint32_t)min<int64_t>(window_rows, rows - base);
+  const float* __restrict__ xb = x + base * 128 + sl * 4;
+  f4 acc[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) acc[u] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < n; j0 += kSlots * U) {
+    f4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * kSlots + slot;
+      const uint32_t r = __umulhi(mix((uint32_t)(e0 + j)), span);  // uniform in [0, span)
+      v[u] = j < n ? *reinterpret_cast<const f4*>(xb + (int64_t)r * 128) : f4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc[u] += v[u];
+  }
+#pragma unroll
+  for (int u = 1; u < U; ++u) acc[0] += acc[u];
+  const float t = acc[0].x + acc[0].y + acc[0].z + acc[0].w;
+  if (lane == 0) sink[item] = t;
+}
+
+template <int U>
+__global__ __launch_bounds__(kWave) void gather_items(const float* __restrict__ x,
+                                                      const int32_t* __restrict__ col,
+                                                      const int32_t* __restrict__ items,
+                                                      int64_t n_items, float* __restrict__ sink) {
+  const int64_t item = blockIdx.x;
+  const int lane = threadIdx.x, slot = lane / 32, sl = lane % 32;
+  const int kb = items[2 * item], ke = items[2 * item + 1];
+  f4 acc[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) acc[u] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = kb; k0 < ke; k0 += kWave) {
+    const int n = min(kWave, ke - k0);
+    const int cj = lane < n ? __builtin_nontemporal_load(col + k0 + lane) : 0;
+    for (int s0 = 0; s0 < n; s0 += kSlots * U) {
+      f4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = s0 + u * kSlots;
+        const int a = __builtin_amdgcn_readlane(cj, j);
+        const int b = __builtin_amdgcn_readlane(cj, j + 1 < kWave ? j + 1 : j);
+        const int c = slot ? b : a;
+        v[u] = j + slot < n ? *reinterpret_cast<const f4*>(x + (int64_t)c * 128 + sl * 4)
+                            : f4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) acc[u] += v[u];
+    }
+  }
+#pragma unroll
+  for (int u = 1; u < U; ++u) acc[0] += acc[u];
+  const float t = acc[0].x + acc[0].y + acc[0].z + acc[0].w;
+  if (lane == 0) sink[item] = t;
+}
+
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int tfg_probe_gather_window(const float* x, int64_t rows, int64_t window_rows,
+                            int64_t n_gathers, int64_t per_window, float* sink, void* stream) {
+  if (x == nullptr || sink == nullptr || !aligned16(x) || rows < 1 || window_rows < 1 ||
+      window_rows > rows || n_gathers < 0 || per_window < 1 || per_window % kItem != 0 ||
+      (n_gathers + kItem - 1) / kItem >= (int64_t(1) << 31) || rows >= (int64_t(1) << 32))
+    return 1;
+  if (n_gathers == 0) return 0;
+  const unsigned grid = (unsigned)((n_gathers + kItem - 1) / kItem);
+  gather_window<8><<<grid, kWave, 0, static_cast<hipStream_t>(stream)>>>(
+      x, rows, window_rows, n_gathers, per_window, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 6;
+}
+
+int tfg_probe_gather_items(const float* x, const int32_t* col, const int32_t* items,
+                           int64_t n_items, float* sink, void* stream) {
+  if (x == nullptr || col == nullptr || items == nullptr || sink == nullptr || !aligned16(x) ||
+      n_items < 0 || n_items >= (int64_t(1) << 31))
+    return 1;
+  if (n_items == 0) return 0;
+  gather_items<4><<<(unsigned)n_items, kWave, 0, static_cast<hipStream_t>(stream)>>>(
+      x, col, items, n_items, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 6;
+}
+
+}  // extern "C"
