@@ -247,6 +247,36 @@ def _oracle(fn, units: int, unit: str, sample: str):
             "sample": f"{sample}, {dt:.2f} s"}
 
 
+def _oracle_threads(fn, units: int, unit: str, sample: str):
+    """As _oracle, for a callable that splits the oracle's work over
+    oracle.host_threads() threads by target range (each range's results are
+    bit-identical to one thread's)."""
+    import oracle
+    threads = oracle.host_threads()
+    t0 = time.perf_counter()
+    fn(threads)
+    dt = time.perf_counter() - t0
+    scale = 1e9 if unit == "GE/s" else 1.0
+    return {"value": round(units / dt / scale, 6), "unit": unit, "cores": threads,
+            "kind": "oracle", "sample": f"{sample}, split over {threads} threads by target "
+                                        f"range, {dt:.2f} s"}
+
+
+def _by_target_range(fn, edge_index, n, threads):
+    """Runs fn(sub_edge_index) for the edges of each target range [n*i/T,
+    n*(i+1)/T) in parallel threads (input order kept inside a range)."""
+    from concurrent.futures import ThreadPoolExecutor
+    tgt = edge_index[1]
+    bounds = [n * i // threads for i in range(threads + 1)]
+
+    def part(i):
+        m = (tgt >= bounds[i]) & (tgt < bounds[i + 1])
+        return fn(np.ascontiguousarray(edge_index[:, m]))
+
+    with ThreadPoolExecutor(threads) as pool:
+        return list(pool.map(part, range(threads)))
+
+
 def _row(name: str, workload: str, ms: float, edges: int | None, nbytes: int | None, **extra):
     line = {"row": name, "workload": workload, "ms": round(ms, 4)}
     if edges is not None:
@@ -353,11 +383,15 @@ def run_suite(args):
         cpu["gat"] = _oracle(lambda: oracle.gat_layer(ei3_np, c["h"], c["a_src"], c["a_dst"], H,
                                                       slope=np.float32(c["slope"])),
                              E3, "GE/s", "the whole attention graph")
+        cpu["gat_t"] = _oracle_threads(
+            lambda T: _by_target_range(lambda sub: oracle.gat_layer(
+                sub, c["h"], c["a_src"], c["a_dst"], H, slope=np.float32(c["slope"])),
+                ei3_np, n3, T), E3, "GE/s", "the whole attention graph")
     _row("fused attention aggregation", wl3, ms_f, E3,
          E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
          kernel="node_projections_vec + gat_short + gat_items + gat_merge",
          unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
-         cpu_baseline=cpu.get("gat"))
+         cpu_baseline=cpu.get("gat"), cpu_baseline_threads=cpu.get("gat_t"))
     # the Transformer-style variant: q, key, v of the same shape as h
     gen = torch.Generator(device=dev).manual_seed(3)
     qd, kd, vd = (torch.randn((n3, Fh), generator=gen, device=dev) for _ in range(3))
@@ -432,6 +466,17 @@ def run_suite(args):
             return [oracle.segment_pool(hb, c["graph_index"], G, r) for r in ("sum", "mean", "max")]
         cpu["mb"] = _oracle(oracle_step, 3 * (Eb + Nb), "GE/s",
                             "the whole batch (normalisation, 3 layers, 3 pools)")
+
+        def oracle_step_threads(T):
+            oei, ow, _ = oracle.gcn_norm(c["edge_index"], Nb)
+            hb = c["x"]
+            for _ in range(c["layers"]):
+                hb = oracle.aggregate_by_row_ranges(oei, hb, Nb, "sum", edge_weight=ow,
+                                                    threads=T)[0].astype(np.float32)
+            return [oracle.segment_pool(hb, c["graph_index"], G, r) for r in ("sum", "mean", "max")]
+        cpu["mb_t"] = _oracle_threads(oracle_step_threads, 3 * (Eb + Nb), "GE/s",
+                                      "the whole batch (normalisation and pools on one thread, "
+                                      "the 3 layers)")
         cpu["pool"] = _oracle(lambda: oracle.segment_pool(c["x"], c["graph_index"], G, "sum"),
                               Nb, "nodes/s", "the whole batch")
     _row("BatchGraph construction", wl5, ms, Eb,
@@ -450,7 +495,7 @@ def run_suite(args):
         return [tfg.tfg_segment_pool(hb, bgi, G, r, validate=False) for r in ("sum", "mean", "max")]
     ms = _timed(torch, batch_step, reps)
     _row("mini-batch step: BatchGraph + CSR + gcn_norm + 3 GCN layers + 3 pools", wl5, ms,
-         3 * (Eb + Nb), None, cpu_baseline=cpu.get("mb"))
+         3 * (Eb + Nb), None, cpu_baseline=cpu.get("mb"), cpu_baseline_threads=cpu.get("mb_t"))
     gi = torch.from_numpy(c["graph_index"].astype(np.int32)).to(dev)
     pout = torch.empty((G, Fb), dtype=torch.float32, device=dev)
     pws = torch.empty(max(tfg.load().tfg_segment_pool_ws_bytes(Nb, G), 256), dtype=torch.uint8,
@@ -474,14 +519,21 @@ def run_suite(args):
             return tfg.tfg_aggregate(None, xc, n, "sum", edge_weight=nm["edge_weight_csr"],
                                      weight_order="csr", graph=gc)
         ms = _timed(torch, gcn_step, reps)
-        cb = None
+        cb = cbt = None
         if not args.no_cpu_baseline:
             def oracle_gcn():
                 oei, ow, _ = oracle.gcn_norm(cfg["edge_index"], n)
                 return oracle.aggregate(oei, cfg["x"], n, "sum", edge_weight=ow)
+
+            def oracle_gcn_threads(T):
+                oei, ow, _ = oracle.gcn_norm(cfg["edge_index"], n)
+                return oracle.aggregate_by_row_ranges(oei, cfg["x"], n, "sum", edge_weight=ow,
+                                                      threads=T)
             cb = _oracle(oracle_gcn, Ec, "GE/s", "the whole graph")
+            cbt = _oracle_threads(oracle_gcn_threads, Ec, "GE/s",
+                                  "the whole graph (normalisation on one thread)")
         _row("GCN step: CSR + gcn_norm + sum aggregation", f"{cfg['name']}: uniform graph N={n}, "
-             f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb)
+             f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb, cpu_baseline_threads=cbt)
 
 
 def run_ceiling(args):

@@ -32,7 +32,7 @@ constexpr int kSortWaves = kSortThreads / kWave;
 constexpr int kUpThreads = 512;                       // counting pass: threads per tile
 constexpr int kUpItems = kSortTile / kUpThreads;
 constexpr int kMaxDigitBits = 8;
-constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 512
+constexpr int kMaxRadix = 1 << kMaxDigitBits;         // 256
 constexpr int kXcds = 8;
 
 // Blocks are dispatched round-robin over the XCDs; tile_of() gives each XCD a
