@@ -277,15 +277,32 @@ def _by_target_range(fn, edge_index, n, threads):
         return list(pool.map(part, range(threads)))
 
 
-def _row(name: str, workload: str, ms: float, edges: int | None, nbytes: int | None, **extra):
+def _row(name: str, workload: str, ms: float, edges: int | None, nbytes: int | None,
+         compulsory: int | None = None, gathered: int | None = None,
+         ceiling: tuple | None = None, **extra):
+    """One suite line. nbytes: the algorithmic bytes of the row (one gathered
+    row per edge where the kernel gathers). For gathering kernels whose rows
+    the caches serve, `compulsory` (bytes that must cross HBM) is set against
+    8 TB/s and `gathered` (the row bytes) against the measured gather ceiling
+    (name, GB/s)."""
     line = {"row": name, "workload": workload, "ms": round(ms, 4)}
     if edges is not None:
         line["GE_per_s"] = round(edges / (ms * 1e-3) / 1e9, 3)
     if nbytes is not None:
-        gbs = nbytes / (ms * 1e-3) / 1e9
-        line["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBPS,
-                            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBPS, 4),
-                            "algorithmic_bytes_per_launch": int(nbytes)}
+        t = ms * 1e-3
+        hbm = compulsory if compulsory is not None else nbytes
+        gbs = hbm / t / 1e9
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBPS, 4), "algorithmic_bytes_per_launch": int(nbytes),
+                "algorithmic_GBps": round(nbytes / t / 1e9, 1)}
+        if compulsory is not None:
+            roof["compulsory_bytes_per_launch"] = int(compulsory)
+        if gathered is not None and ceiling is not None:
+            rate = gathered / t / 1e9
+            roof["gather"] = {"bytes_per_launch": int(gathered), "achieved": round(rate, 1),
+                              "ceiling": ceiling[1], "ceiling_from": ceiling[0],
+                              "frac": round(rate / ceiling[1], 4), "unit": "GB/s"}
+        line["roofline"] = roof
     line.update(extra)
     print(json.dumps(line), flush=True)
 
@@ -320,6 +337,14 @@ def run_suite(args):
         g.handle, gt.handle, F, 1, 0, 0, 1), 256), dtype=torch.uint8, device=dev)
     # the normalised weights in the transposed graph's order, cached once per graph
     w_t = tfg.tfg_edge_reorder(norm["edge_weight_csr"], src=g, dst=gt)
+    # the gather ceiling on this table (the rows gathered by dx, dw and APPNP)
+    ceil = gather_ceiling(torch, x, reps=5)
+    ceiling = max(((k, v["GBps"]) for k, v in ceil.items()), key=lambda kv: kv[1])
+    info_f, info_t = g.info(), gt.info()
+
+    def items(inf):
+        return inf["n_part_items"] if inf["src_parts"] > 1 else inf["n_chunks"] + N
+
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", graph_t=gt, edge_weight=w_t, weight_order="csr_t", want_dx=True, ws=ws),
         reps)
@@ -342,20 +367,26 @@ def run_suite(args):
         del sub, dy_h
     # per edge: target id, the weight and a dy row; per source: a dx row
     _row("backward dx (transposed sum aggregation)", wl, ms, Ep,
-         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="spmm_rows over the transposed graph",
+         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1),
+         compulsory=compulsory_bytes(Ep, N, N, F, items(info_t)), gathered=Ep * 4 * F,
+         ceiling=ceiling, kernel="spmm_rows over the transposed graph",
          src_parts=gt.info()["src_parts"], weights="transposed graph order",
          ms_with_edge_order_weights=round(ms_coo, 4), cpu_baseline=cpu.get("bw"))
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
         g, dy, "sum", x=x, want_dx=False, want_dw=True, dw_order="csr", ws=ws), reps)
     # per edge: source id, an x row, the dw value; per target: a dy row
     _row("backward dw (per-edge dot products)", wl, ms, Ep,
-         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1), kernel="edge_grad_rows",
+         Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1),
+         compulsory=Ep * 8 + 2 * N * 4 * F + 4 * (N + 1) + 16 * items(info_f),
+         gathered=Ep * 4 * F, ceiling=ceiling, kernel="edge_grad_rows",
          cpu_baseline=cpu.get("bw"))
     K = 3
     ms = _timed(torch, lambda: tfg.tfg_propagate(g, x, K, alpha=0.1, h=x,
                                                 edge_weight=norm["edge_weight_csr"]), reps)
     _row(f"APPNP propagation, K={K}, alpha=0.1", wl, ms, K * Ep,
-         K * (Ep * (8 + 4 * F) + N * 8 * F + 4 * (N + 1)), ms_per_step=round(ms / K, 4),
+         K * (Ep * (8 + 4 * F) + N * 8 * F + 4 * (N + 1)),
+         compulsory=K * (compulsory_bytes(Ep, N, N, F, items(info_f)) + N * 4 * F),
+         gathered=K * Ep * 4 * F, ceiling=ceiling, ms_per_step=round(ms / K, 4),
          cpu_baseline=cpu.get("appnp"))
     del g, gt, norm, dy, ws, ei, x
     torch.cuda.empty_cache()
