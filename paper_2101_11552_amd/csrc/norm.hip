@@ -142,17 +142,23 @@ __global__ __launch_bounds__(kBlock) void weights_coo(const IdxT* __restrict__ s
 // the slice that holds it. Every block reads all of dinv once (4 N bytes from
 // L2 in full lines, copied straight into LDS) in exchange for one or two
 // random line reads per edge, so the tile per block is made as large as the
-// registers allow: one register per endpoint, holding the node id (as a byte
-// offset, 4 * id) until the endpoint's slice is seen and then its dinv value,
-// marked by the sign bit (dinv >= 0, offsets >= 0). The products are the same ones, in the same order,
-// as in weights_coo / weights_csr, so the kernels agree bit for bit.
+// registers allow: one register per endpoint, holding the node id until the
+// endpoint's slice is seen and then its dinv value. The products are the same
+// ones, in the same order, as in weights_coo / weights_csr, so the kernels
+// agree bit for bit.
 constexpr int kSlThreads = 1024;                  // 16 waves, one block per CU
-constexpr int kSlice = 40960;                     // floats per LDS slice (160 KB)
 constexpr int kSlPiece = kWave * 4;               // floats per wave-wide 16-byte copy
-constexpr int kCooItems = 24;                     // edges per thread (2 registers each)
-constexpr int kCsrItems = 32;                     // positions per thread (1 register each)
-constexpr int kCooTile = kSlThreads * kCooItems;  // 24576 edges per block
-constexpr int kCsrTile = kSlThreads * kCsrItems;  // 32768 positions per block
+constexpr int kSlice = 159 * kSlPiece;            // floats per LDS slice (159 KB)
+constexpr int kSlLds = kSlice + kSlPiece;         // the slice, then the sentinel word
+// edges per thread in COO order (2 registers each; 64-bit ids and weights
+// need registers of their own)
+template <typename IdxT, bool HAS_W>
+constexpr int coo_items() { return sizeof(IdxT) == 4 && !HAS_W ? 28 : 24; }
+constexpr int kCooTile = kSlThreads * coo_items<int32_t, false>();  // 28672 edges per block
+// positions per thread in graph order (1 register each; general weights need
+// registers for their edge ids and weights)
+template <bool HAS_W>
+constexpr int csr_items() { return HAS_W ? 24 : 32; }
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -173,37 +179,38 @@ __device__ __forceinline__ void fill_slice(float* slice, const float* __restrict
 // All of this wave's memory operations done (the LDS copies included).
 __device__ __forceinline__ void wait_slice() { __builtin_amdgcn_s_waitcnt(0); }
 
-// An endpoint register: 4 * node id (>= 0, or -1 for no edge) until resolved,
-// then the dinv value with the sign bit set. A resolved value never matches a
-// later slice: as unsigned, (value - 4 lo) >= 2^31 - 2^30 > 4 len (N <= 2^28).
-__device__ __forceinline__ int resolved(float v) { return __float_as_int(v) | INT_MIN; }
-__device__ __forceinline__ float value_of(int r) { return __int_as_float(r & INT_MAX); }
+// An endpoint register, as unsigned: 0x80000000 | (4 * node id) until it is
+// resolved (0xFFFFFFFC for no edge, which no slice holds), then the bits of
+// its dinv value, which are below 0x80000000 (dinv >= 0). The word after the
+// slice holds the sentinel 0xFFFFFFFF. For the slice of nodes [lo, lo + len)
+// a register's offset is u = r - (0x80000000 + 4 lo): below 4 len for an id
+// in the slice, and at least 4 kSlice for every other register (a later id,
+// a resolved value, no edge; earlier ids were resolved by earlier slices;
+// N <= 2^28). So min(u, 4 kSlice) addresses either the value or the sentinel,
+// and min(r, word read) resolves the register or leaves it as it was: three
+// ALU operations and one LDS read per register and slice, with no branch.
+__device__ __forceinline__ unsigned unresolved(int id) { return 0x80000000u | (4u * (unsigned)id); }
+__device__ __forceinline__ float value_of(unsigned r) { return __uint_as_float(r); }
+__device__ __forceinline__ void put_sentinel(float* slice) {
+  if (threadIdx.x == 0) reinterpret_cast<unsigned*>(slice)[kSlice] = 0xFFFFFFFFu;
+}
 
-// Resolves the endpoints of one slice [lo, lo + len): reads in groups of 8,
-// issued together, then used.
 template <int ITEMS>
-__device__ __forceinline__ void resolve(int (&r)[ITEMS], const float* slice, int lo, int len) {
-  // unresolved registers hold byte offsets (4 * id): the difference is the
-  // LDS byte address itself
+__device__ __forceinline__ void resolve(unsigned (&r)[ITEMS], const float* slice, int64_t lo) {
   const char* sb = reinterpret_cast<const char*>(slice);
+  const unsigned b = 0x80000000u + 4u * (unsigned)lo;
 #pragma unroll
-  for (int j0 = 0; j0 < ITEMS; j0 += 8) {
-    float v[8];
-#pragma unroll
-    for (int j = 0; j < 8 && j0 + j < ITEMS; ++j) {
-      const unsigned u = (unsigned)(r[j0 + j] - 4 * lo);
-      v[j] = u < 4u * (unsigned)len ? *reinterpret_cast<const float*>(sb + u) : -1.0f;
-    }
-#pragma unroll
-    for (int j = 0; j < 8 && j0 + j < ITEMS; ++j)
-      r[j0 + j] = v[j] >= 0.0f ? resolved(v[j]) : r[j0 + j];
+  for (int j = 0; j < ITEMS; ++j) {
+    const unsigned a = min(r[j] - b, 4u * (unsigned)kSlice);
+    r[j] = min(r[j], *reinterpret_cast<const unsigned*>(sb + a));
   }
 }
 
 // Walks dinv[0, N) slice by slice, resolving every register of the block.
-// The first slice was started (fill_slice) by the caller.
+// The first slice and the sentinel were started (fill_slice, put_sentinel) by
+// the caller.
 template <int ITEMS>
-__device__ __forceinline__ void walk_slices(int (&r)[ITEMS], float* slice,
+__device__ __forceinline__ void walk_slices(unsigned (&r)[ITEMS], float* slice,
                                             const float* __restrict__ dinv, int64_t N) {
   for (int64_t lo = 0; lo < N; lo += kSlice) {
     const int len = (int)min<int64_t>(kSlice, N - lo);
@@ -213,73 +220,83 @@ __device__ __forceinline__ void walk_slices(int (&r)[ITEMS], float* slice,
     }
     wait_slice();
     __syncthreads();
-    resolve(r, slice, (int)lo, len);
+    resolve(r, slice, lo);
   }
 }
 
 // (Block-relative pointers with 32-bit offsets keep one address register per
-// thread for all items.)
-template <typename IdxT>
+// thread for all items. The weights are a template choice: a run-time branch
+// on them costs the unweighted kernel 13% in spilled scalar registers.)
+template <typename IdxT, bool HAS_W>
 __global__ __launch_bounds__(kSlThreads, 4) void weights_coo_sliced(
     const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, int64_t E_in, int64_t E, int64_t N,
     const float* __restrict__ w, const float* __restrict__ dinv, int32_t* __restrict__ out_ei,
     float* __restrict__ out_w) {
-  __shared__ float slice[kSlice];
+  constexpr int kCooItems = coo_items<IdxT, HAS_W>();
+  constexpr int kTile = kSlThreads * kCooItems;
+  __shared__ float slice[kSlLds];
   fill_slice(slice, dinv, (int)min<int64_t>(kSlice, N));  // overlaps the edge loads
-  const int64_t b0 = (int64_t)blockIdx.x * kCooTile;
-  const int n_in = (int)max<int64_t>(0, min<int64_t>(kCooTile, E_in - b0));  // input edges here
-  const int n_all = (int)min<int64_t>(kCooTile, E - b0);                     // with the loops
-  int st[2 * kCooItems];  // [0, ITEMS): sources, [ITEMS, 2 ITEMS): targets
-  {
-    // every load issued before the first use
-    const IdxT* sb = src + b0;
-    const IdxT* tb = tgt + b0;
-    // 32-bit ids: all loads straight into the registers, then the checks;
-    // 64-bit ids: groups of 8 edges (two registers per raw id)
-    constexpr int G = sizeof(IdxT) == 4 ? kCooItems : 8;
+  put_sentinel(slice);
+  const int64_t b0 = (int64_t)blockIdx.x * kTile;
+  const int n_in = (int)max<int64_t>(0, min<int64_t>(kTile, E_in - b0));  // input edges here
+  const int n_all = (int)min<int64_t>(kTile, E - b0);                     // with the loops
+  // [0, ITEMS): sources, [ITEMS, 2 ITEMS): targets. 32-bit ids are loaded
+  // straight into these registers (every load issued before the first use);
+  // 64-bit ids go through groups of 8 edges.
+  unsigned st[2 * kCooItems];
+  const IdxT* sb = src + b0;
+  const IdxT* tb = tgt + b0;
+  constexpr int G = sizeof(IdxT) == 4 ? kCooItems : 8;
 #pragma unroll
-    for (int j0 = 0; j0 < kCooItems; j0 += G) {
-      IdxT rs[G], rt[G];
+  for (int j0 = 0; j0 < kCooItems; j0 += G) {
+    IdxT rs[sizeof(IdxT) == 4 ? 1 : G], rt[sizeof(IdxT) == 4 ? 1 : G];
 #pragma unroll
-      for (int j = 0; j < G; ++j) {
-        const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
-        rs[j] = p < n_in ? __builtin_nontemporal_load(sb + p) : IdxT(0);
-        rt[j] = p < n_in ? __builtin_nontemporal_load(tb + p) : IdxT(0);
+    for (int j = 0; j < G; ++j) {
+      const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
+      const IdxT a = p < n_in ? __builtin_nontemporal_load(sb + p) : IdxT(0);
+      const IdxT b = p < n_in ? __builtin_nontemporal_load(tb + p) : IdxT(0);
+      if constexpr (sizeof(IdxT) == 4) {
+        st[j0 + j] = (unsigned)a;
+        st[kCooItems + j0 + j] = (unsigned)b;
+      } else {
+        rs[j] = a;
+        rt[j] = b;
       }
+    }
+    if constexpr (sizeof(IdxT) != 4) {
+      // ids out of the 32-bit range become N (clamped below)
 #pragma unroll
       for (int j = 0; j < G; ++j) {
-        // ids were validated when the graph was built; clamped here all the
-        // same. Loops (i, i) follow the input edges; positions past E get the
-        // id -1, which no slice holds.
-        const int p = (j0 + j) * kSlThreads + (int)threadIdx.x;
-        const int64_t s0 = (int64_t)rs[j], t0 = (int64_t)rt[j];
-        const int loop = p < n_all ? (int)(b0 + p - E_in) : -1;
-        const bool in = p < n_in;
-        st[j0 + j] = in ? ((s0 < 0 || s0 >= N) ? 0 : (int)s0) : loop;
-        st[kCooItems + j0 + j] = in ? ((t0 < 0 || t0 >= N) ? 0 : (int)t0) : loop;
+        st[j0 + j] = (rs[j] < 0 || rs[j] >= N) ? (unsigned)N : (unsigned)rs[j];
+        st[kCooItems + j0 + j] = (rt[j] < 0 || rt[j] >= N) ? (unsigned)N : (unsigned)rt[j];
       }
     }
   }
-  if (out_ei) {
-    int32_t* os = out_ei + b0;
-    int32_t* ot = out_ei + E + b0;
+  int32_t* os = out_ei == nullptr ? nullptr : out_ei + b0;
+  int32_t* ot = out_ei == nullptr ? nullptr : out_ei + E + b0;
 #pragma unroll
-    for (int j = 0; j < kCooItems; ++j) {
-      const int p = j * kSlThreads + (int)threadIdx.x;
-      if (p < n_all) {
-        __builtin_nontemporal_store(st[j], os + p);
-        __builtin_nontemporal_store(st[kCooItems + j], ot + p);
-      }
+  for (int j = 0; j < kCooItems; ++j) {
+    // ids were validated when the graph was built; clamped here all the same
+    // (as unsigned, so that negative ids are caught too). Loops (i, i) follow
+    // the input edges; positions past E get no edge.
+    const int p = j * kSlThreads + (int)threadIdx.x;
+    const bool in = p < n_in;
+    const int loop = (int)(b0 + p - E_in);
+    const int sv = in ? (st[j] >= (unsigned)N ? 0 : (int)st[j]) : loop;
+    const int tv = in ? (st[kCooItems + j] >= (unsigned)N ? 0 : (int)st[kCooItems + j]) : loop;
+    if (os != nullptr && p < n_all) {
+      __builtin_nontemporal_store(sv, os + p);
+      __builtin_nontemporal_store(tv, ot + p);
     }
+    st[j] = p < n_all ? unresolved(sv) : unresolved(-1);
+    st[kCooItems + j] = p < n_all ? unresolved(tv) : unresolved(-1);
   }
-#pragma unroll
-  for (int j = 0; j < 2 * kCooItems; ++j) st[j] = st[j] >= 0 ? 4 * st[j] : st[j];  // byte offsets
   walk_slices(st, slice, dinv, N);
   // all loads (the weights) before the first store: a wait for a load also
   // waits for the stores issued before it
   float* ow = out_w + b0;
   float o[kCooItems];
-  if (w != nullptr) {
+  if constexpr (HAS_W) {
     const float* wb = w + b0;
 #pragma unroll
     for (int j = 0; j < kCooItems; ++j)  // loops weigh 1
@@ -307,33 +324,31 @@ __global__ __launch_bounds__(kSlThreads, 4) void weights_csr_sliced(
     const int* __restrict__ key, int parts, const int* __restrict__ col,
     const int* __restrict__ perm, const float* __restrict__ w, int64_t E_in, int64_t E, int64_t N,
     const float* __restrict__ dinv, float* __restrict__ out) {
-  __shared__ float slice[kSlice];
+  constexpr int kCsrItems = csr_items<HAS_W>();
+  constexpr int kCsrTile = kSlThreads * kCsrItems;
+  __shared__ float slice[kSlLds];
   fill_slice(slice, dinv, (int)min<int64_t>(kSlice, N));
+  put_sentinel(slice);
   const int64_t b0 = (int64_t)blockIdx.x * kCsrTile;
   const int n = (int)min<int64_t>(kCsrTile, E - b0);
-  int c[kCsrItems];
+  unsigned c[kCsrItems];
   {
     const int* cb = col + b0;
 #pragma unroll
     for (int j = 0; j < kCsrItems; ++j) {
       const int p = j * kSlThreads + (int)threadIdx.x;
-      c[j] = p < n ? 4 * cb[p] : -1;  // byte offset; -1: no slice holds it
+      c[j] = unresolved(p < n ? cb[p] : -1);
     }
   }
   walk_slices(c, slice, dinv, N);
-  // keys (and edge ids), then the targets' dinv (and the weights), then the
-  // products: all loads before the first store, since a wait for a load also
-  // waits for the stores issued before it
-  const int* kb = key + b0;
-  float* ob = out + b0;
-  int kv[kCsrItems];
-#pragma unroll
-  for (int j = 0; j < kCsrItems; ++j)
-    kv[j] = j * kSlThreads + (int)threadIdx.x < n ? kb[j * kSlThreads + threadIdx.x] : 0;
+  // The sources' values replace their registers; then the weights (edge ids
+  // first, in groups), the keys and the targets' dinv: all loads before the
+  // first store, since a wait for a load also waits for the stores issued
+  // before it.
   float o[kCsrItems];
 #pragma unroll
-  for (int j = 0; j < kCsrItems; ++j) o[j] = 1.0f;
-  if constexpr (HAS_W) {  // edge ids, then weights, in groups (loops weigh 1)
+  for (int j = 0; j < kCsrItems; ++j) o[j] = value_of(c[j]);
+  if constexpr (HAS_W) {  // dinv[col] * w (loops weigh 1)
     const int* pb = perm + b0;
 #pragma unroll
     for (int j0 = 0; j0 < kCsrItems; j0 += 8) {
@@ -344,16 +359,23 @@ __global__ __launch_bounds__(kSlThreads, 4) void weights_csr_sliced(
         pe[j] = p < n ? pb[p] : (int)E_in;
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) o[j0 + j] = pe[j] < E_in ? w[pe[j]] : 1.0f;
+      for (int j = 0; j < 8; ++j) o[j0 + j] = o[j0 + j] * (pe[j] < E_in ? w[pe[j]] : 1.0f);
     }
   }
+  // (unit weights: dinv[col] * 1 is dinv[col] itself)
+  const int* kb = key + b0;
+  float* ob = out + b0;
+  int kv[kCsrItems];
+#pragma unroll
+  for (int j = 0; j < kCsrItems; ++j)
+    kv[j] = j * kSlThreads + (int)threadIdx.x < n ? kb[j * kSlThreads + threadIdx.x] : 0;
   float dt[kCsrItems];
 #pragma unroll
   for (int j = 0; j < kCsrItems; ++j) dt[j] = dinv[parts == 1 ? kv[j] : kv[j] / parts];
 #pragma unroll
   for (int j = 0; j < kCsrItems; ++j) {
     const int p = j * kSlThreads + (int)threadIdx.x;
-    if (p < n) ob[p] = (value_of(c[j]) * o[j]) * dt[j];  // (dinv[col] * w) * dinv[row]
+    if (p < n) ob[p] = o[j] * dt[j];  // (dinv[col] * w) * dinv[row]
   }
 }
 
@@ -486,15 +508,15 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
         g.pexec, g.n_pexec, per_block, (int)g.part_rows, g.col, g.N, dinv, out_w_csr);
     TFG_LAUNCHED("gcn weights (graph order, by source part)");
   } else if (out_w_csr && g.E > 0 && use_sliced(g.E, g.N)) {
-    const unsigned nbs = (unsigned)((g.E + kCsrTile - 1) / kCsrTile);
-    if (edge_weight)
-      weights_csr_sliced<true><<<nbs, kSlThreads, 0, s>>>(g.key, g.parts, g.col, g.perm,
-                                                          edge_weight, g.E_in, g.E, g.N, dinv,
-                                                          out_w_csr);
-    else
-      weights_csr_sliced<false><<<nbs, kSlThreads, 0, s>>>(g.key, g.parts, g.col, g.perm,
-                                                           nullptr, g.E_in, g.E, g.N, dinv,
-                                                           out_w_csr);
+    if (edge_weight) {
+      constexpr int64_t tile = kSlThreads * csr_items<true>();
+      weights_csr_sliced<true><<<(unsigned)((g.E + tile - 1) / tile), kSlThreads, 0, s>>>(
+          g.key, g.parts, g.col, g.perm, edge_weight, g.E_in, g.E, g.N, dinv, out_w_csr);
+    } else {
+      constexpr int64_t tile = kSlThreads * csr_items<false>();
+      weights_csr_sliced<false><<<(unsigned)((g.E + tile - 1) / tile), kSlThreads, 0, s>>>(
+          g.key, g.parts, g.col, g.perm, nullptr, g.E_in, g.E, g.N, dinv, out_w_csr);
+    }
     TFG_LAUNCHED("gcn weights (CSR order, sliced)");
   } else if (out_w_csr && g.E > 0) {
     const unsigned nb = (unsigned)((g.E + 4 * kBlock - 1) / (4 * kBlock));
@@ -508,15 +530,23 @@ int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
   }
   if ((out_w || out_edge_index) && g.E > 0) {
     if (out_w && use_sliced(g.E, g.N)) {
-      const unsigned nbs = (unsigned)((g.E + kCooTile - 1) / kCooTile);
+      auto blocks = [&](int items) { return (unsigned)((g.E + kSlThreads * items - 1) / (kSlThreads * items)); };
       if (index_type == TFG_I64) {
         const int64_t* ei = static_cast<const int64_t*>(edge_index);
-        weights_coo_sliced<int64_t><<<nbs, kSlThreads, 0, s>>>(
-            ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+        if (edge_weight)
+          weights_coo_sliced<int64_t, true><<<blocks(coo_items<int64_t, true>()), kSlThreads, 0, s>>>(
+              ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+        else
+          weights_coo_sliced<int64_t, false><<<blocks(coo_items<int64_t, false>()), kSlThreads, 0, s>>>(
+              ei, ei + g.E_in, g.E_in, g.E, g.N, nullptr, dinv, out_edge_index, out_w);
       } else {
         const int32_t* ei = static_cast<const int32_t*>(edge_index);
-        weights_coo_sliced<int32_t><<<nbs, kSlThreads, 0, s>>>(
-            ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+        if (edge_weight)
+          weights_coo_sliced<int32_t, true><<<blocks(coo_items<int32_t, true>()), kSlThreads, 0, s>>>(
+              ei, ei + g.E_in, g.E_in, g.E, g.N, edge_weight, dinv, out_edge_index, out_w);
+        else
+          weights_coo_sliced<int32_t, false><<<blocks(coo_items<int32_t, false>()), kSlThreads, 0, s>>>(
+              ei, ei + g.E_in, g.E_in, g.E, g.N, nullptr, dinv, out_edge_index, out_w);
       }
       TFG_LAUNCHED("gcn weights (COO order, sliced)");
       return TFG_OK;

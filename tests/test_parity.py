@@ -155,6 +155,7 @@ NORM_SLICE_CASES = [
     (90_001, 50_000, False, np.int64, 1, True),  # int64 ids, more nodes than edges
     (100_003, 400_000, False, np.int32, 7, True),  # graph order by source part, 7 parts
     (4000, 60_000, False, np.int64, 3, False),   # blocks of items straddling two parts
+    (81_409, 200_000, False, np.int32, 1, True),  # two full 159 KB slices and one node
 ]
 
 
