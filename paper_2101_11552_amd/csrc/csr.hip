@@ -50,46 +50,54 @@ __device__ __forceinline__ int tile_of(int bid, int ntiles) {
 struct KeyMap {
   int64_t E_in, N_src, N;
   int part_rows, parts;
-  float inv_part_rows;  // 1 / part_rows, for the source-part estimate
+  double inv_part_rows, half_inv_part_rows;  // 1 / part_rows and 0.5 / part_rows
 };
 
-// source / part_rows for 0 <= source < 2^31: a float estimate (off by at most
-// one) corrected with exact integer compares.
+// floor(s / part_rows) for 0 <= s < 2^31, as the truncation of
+// (s + 1/2) / part_rows in double: the fraction of s / part_rows is at most
+// (part_rows - 1) / part_rows, so adding 1 / (2 part_rows) never reaches the
+// next integer, and the double's relative error (a few 2^-53) is far below
+// that margin of 1 / (2 part_rows) for every s < 2^51.
 __device__ __forceinline__ int source_part(int s, const KeyMap& m) {
-  int q = (int)((float)s * m.inv_part_rows);
-  q = (int64_t)q * m.part_rows > s ? q - 1 : q;
-  q = (int64_t)(q + 1) * m.part_rows <= s ? q + 1 : q;
-  return q;
+  return (int)fma((double)s, m.inv_part_rows, m.half_inv_part_rows);
 }
 
-// Raw ids of edge e (read for every edge, clamped into [0, E_in) so that the
-// loads of a whole tile can be issued together); decode_edge() then applies
-// the range checks and the loop rule.
-template <typename IdxT>
-__device__ __forceinline__ void load_raw(const IdxT* __restrict__ src, const IdxT* __restrict__ tgt,
-                                         int64_t E_in, int64_t e, IdxT* s, IdxT* t) {
-  const int64_t ec = e < E_in ? e : (E_in > 0 ? E_in - 1 : 0);
-  *s = (src && E_in > 0) ? src[ec] : IdxT(0);
-  *t = E_in > 0 ? tgt[ec] : IdxT(0);
+// Edges are addressed inside a tile: position p is edge base + p, and
+// d = E_in - base (the tile's count of input edges when 0 <= d <= tile size)
+// makes the input / loop test and the loop id 32-bit: p < d is an input
+// edge, otherwise the loop on node p - d.
+__device__ __forceinline__ int input_edges_before(int64_t E_in, int64_t base) {
+  return (int)(E_in - base);  // |E_in - base| < 2^31: both below 2^31
 }
 
+// Raw ids of tile position p, read for every position (clamped to the tile's
+// last input edge, or not read when the tile has none) so that the loads of
+// a whole tile can be issued together; decode_edge() then applies the range
+// checks and the loop rule.
 template <typename IdxT>
-__device__ __forceinline__ int decode_source(const KeyMap& m, int64_t e, IdxT s, bool has_src,
-                                             bool* bad) {
-  const bool sbad = has_src && (s < 0 || (int64_t)s >= m.N_src);
-  *bad = sbad;
-  return e < m.E_in ? (sbad ? 0 : (int)s) : (int)(e - m.E_in);
+__device__ __forceinline__ void load_raw(const IdxT* __restrict__ sb, const IdxT* __restrict__ tb,
+                                         int p, int d, IdxT* s, IdxT* t) {
+  const int q = p < d ? p : d - 1;
+  *s = (sb && d > 0) ? sb[q] : IdxT(0);
+  *t = d > 0 ? tb[q] : IdxT(0);
 }
 
 template <typename IdxT>
-__device__ __forceinline__ void decode_edge(const KeyMap& m, int64_t e, IdxT s, IdxT t,
+__device__ __forceinline__ void decode_edge(const KeyMap& m, int p, int d, IdxT s, IdxT t,
                                             bool has_src, int* sv, int* key, bool* bad) {
-  const bool in = e < m.E_in;
-  bool sbad;
-  *sv = decode_source(m, e, s, has_src, &sbad);
-  const bool tbad = t < 0 || (int64_t)t >= m.N;
+  const bool in = p < d;
+  bool sbad, tbad;
+  if constexpr (sizeof(IdxT) == 4) {  // counts are below 2^31: one unsigned compare
+    sbad = has_src && (unsigned)s >= (unsigned)m.N_src;
+    tbad = (unsigned)t >= (unsigned)m.N;
+  } else {
+    sbad = has_src && (s < 0 || (int64_t)s >= m.N_src);
+    tbad = t < 0 || (int64_t)t >= m.N;
+  }
+  const int loop = p - d;
+  *sv = in ? (sbad ? 0 : (int)s) : loop;
+  const int tv = in ? (tbad ? 0 : (int)t) : loop;
   *bad = in && (sbad || tbad);
-  const int tv = in ? (tbad ? 0 : (int)t) : (int)(e - m.E_in);
   *key = m.parts == 1 ? tv : tv * m.parts + source_part(*sv, m);
 }
 
@@ -197,29 +205,33 @@ __global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ s
   const int wave = threadIdx.x / kWave;
   for (int d = lane_id(); d < radix; d += kWave) h[wave][d] = 0;
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  const int tile_n = (int)min<int64_t>(kSortTile, E - base);
+  const int d = input_edges_before(m.E_in, base);
+  const IdxT* sb = src ? src + base : nullptr;
+  const IdxT* tb = tgt + base;
   IdxT rs[kUpItems], rt[kUpItems];
 #pragma unroll
   for (int i = 0; i < kUpItems; ++i) {
-    const int64_t e = base + (int64_t)i * kUpThreads + threadIdx.x;
+    const int p = i * kUpThreads + (int)threadIdx.x;
     if constexpr (FIRST) {
-      load_raw(src, tgt, m.E_in, e, &rs[i], &rt[i]);
+      load_raw(sb, tb, p, d, &rs[i], &rt[i]);
     } else {
-      rt[i] = (IdxT)keys[e < E ? e : E - 1];
+      rt[i] = (IdxT)keys[base + (p < tile_n ? p : tile_n - 1)];
       rs[i] = 0;
     }
   }
   bool any_bad = false;
 #pragma unroll
   for (int i = 0; i < kUpItems; ++i) {
-    const int64_t e = base + (int64_t)i * kUpThreads + threadIdx.x;
+    const int p = i * kUpThreads + (int)threadIdx.x;
     int k = (int)rt[i];
     if constexpr (FIRST) {
-      int s;
+      int sv;
       bool bad;
-      decode_edge(m, e, rs[i], rt[i], src != nullptr, &s, &k, &bad);
-      any_bad |= bad && e < E;
+      decode_edge(m, p, d, rs[i], rt[i], sb != nullptr, &sv, &k, &bad);
+      any_bad |= bad && p < tile_n;
     }
-    if (e < E) atomicAdd(&h[wave][(k >> shift) & (radix - 1)], 1);
+    if (p < tile_n) atomicAdd(&h[wave][(k >> shift) & (radix - 1)], 1);
   }
   if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
@@ -268,19 +280,22 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   // latency per tile). In the first pass the edge id is the position itself
   // and the source id comes out of the key's decoding.
   int key[kSortItems], lpos[kSortItems], pe[FIRST ? 1 : kSortItems], ps[kSortItems];
+  const int d = input_edges_before(m.E_in, base);
+  const IdxT* sb = src ? src + base : nullptr;
+  const IdxT* tb = tgt + base;
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
-    const int64_t e = base + (p < tile_n ? p : tile_n - 1);
+    const int q = p < tile_n ? p : tile_n - 1;
     if constexpr (FIRST) {
       IdxT s0, t0;
-      load_raw(src, tgt, m.E_in, e, &s0, &t0);
+      load_raw(sb, tb, q, d, &s0, &t0);
       bool bad;
-      decode_edge(m, e, s0, t0, src != nullptr, &ps[i], &key[i], &bad);
+      decode_edge(m, q, d, s0, t0, sb != nullptr, &ps[i], &key[i], &bad);
     } else {
-      key[i] = kin[e];
-      pe[i] = ein[e];
-      ps[i] = sin[e];
+      key[i] = kin[base + q];
+      pe[i] = ein[base + q];
+      ps[i] = sin[base + q];
     }
   }
 #pragma unroll
@@ -635,7 +650,8 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
                hipStream_t s) {
   const int64_t E = g.E;
   const SortPlan p = sort_plan(E, g.N, g.parts);
-  const KeyMap m{g.E_in, g.N_src, g.N, (int)g.part_rows, g.parts, 1.0f / (float)g.part_rows};
+  const KeyMap m{g.E_in, g.N_src, g.N, (int)g.part_rows, g.parts, 1.0 / (double)g.part_rows,
+                 0.5 / (double)g.part_rows};
   int* keys = g.key;  // the last pass leaves the sorted keys in the graph
   int* hist = reinterpret_cast<int*>(scratch + L.hist);
   int* sums = reinterpret_cast<int*>(scratch + L.sums);
