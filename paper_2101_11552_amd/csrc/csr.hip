@@ -231,7 +231,8 @@ __global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ s
       decode_edge(m, p, d, rs[i], rt[i], sb != nullptr, &sv, &k, &bad);
       any_bad |= bad && p < tile_n;
     }
-    if (p < tile_n) atomicAdd(&h[wave][(k >> shift) & (radix - 1)], 1);
+    // (a logical shift: packed words use the sign bit)
+    if (p < tile_n) atomicAdd(&h[wave][(int)((unsigned)k >> shift) & (radix - 1)], 1);
   }
   if (FIRST && any_bad) atomicOr(err, kErrIndex);
   __syncthreads();
@@ -382,6 +383,162 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i)
     if (gpos[i] >= 0) sout[gpos[i]] = stage[0][i * kSortThreads + threadIdx.x];
+}
+
+// Packed payloads. When P is a power of two (key = target << log2 P | source
+// part) and the ids and positions fit in 64 bits, an edge travels between
+// the passes as two words instead of three,
+//   A = target << (32 - bt) | source >> sl,
+//   B = (source mod 2^sl) << be | edge id,
+// with bt, bs, be the bit widths of target, source and position and
+// sl = max(0, bs - (32 - bt)) (so sl + be <= 32). The key's digits above the
+// source part are bits of A; the first pass's digit and the last pass's key
+// are recomputed from the unpacked ids. The middle passes then move 8 bytes
+// per edge instead of 12 and stage two words in LDS instead of three.
+struct PackMap {
+  int bt, sl, be, lp;  // target bits, source bits kept in B, position bits, log2 P
+};
+
+__device__ __forceinline__ unsigned pack_a(int t, int sv, const PackMap& q) {
+  return ((unsigned)t << (32 - q.bt)) | ((unsigned)sv >> q.sl);
+}
+__device__ __forceinline__ unsigned pack_b(int sv, int e, const PackMap& q) {
+  return (q.sl > 0 ? ((unsigned)sv & ((1u << q.sl) - 1u)) << q.be : 0u) | (unsigned)e;
+}
+__device__ __forceinline__ int unpack_t(unsigned a, const PackMap& q) {
+  return (int)(a >> (32 - q.bt));
+}
+__device__ __forceinline__ int unpack_s(unsigned a, unsigned b, const PackMap& q) {
+  const unsigned hi = (a & ((1u << (32 - q.bt)) - 1u)) << q.sl;
+  return (int)(q.sl > 0 ? hi | (b >> q.be) : hi);
+}
+__device__ __forceinline__ int unpack_e(unsigned b, const PackMap& q) {
+  return (int)(b & ((1u << q.be) - 1u));
+}
+__device__ __forceinline__ int packed_key(unsigned a, unsigned b, const KeyMap& m,
+                                          const PackMap& q) {
+  return (unpack_t(a, q) << q.lp) | source_part(unpack_s(a, b, q), m);
+}
+
+// The scatter of one pass over packed payloads; the ranking and staging are
+// those of scatter() above. MODE 0: the first pass (reads edge_index, writes
+// A and B); 1: a middle pass (A and B to A and B); 2: the last pass (A and B
+// to the sorted key, edge id and source). `shift` is the digit's position in
+// the key (first pass) or in A (the other passes).
+template <int MODE, typename IdxT>
+__global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
+    const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, KeyMap m, PackMap q,
+    const unsigned* __restrict__ ain, const unsigned* __restrict__ bin, int64_t E, int shift,
+    int dbits, const int* __restrict__ hist, int ntiles, int* __restrict__ o0,
+    int* __restrict__ o1, int* __restrict__ o2) {
+  __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
+  __shared__ int loff[kMaxRadix];
+  __shared__ int goff[kMaxRadix];
+  __shared__ unsigned stage[2][kSortTile];
+  __shared__ int tmp[kSortWaves];
+
+  const int radix = 1 << dbits;
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int tile = tile_of((int)blockIdx.x, ntiles);
+  const int64_t base = (int64_t)tile * kSortTile;
+  const int tile_n = (int)min<int64_t>(kSortTile, E - base);
+  const unsigned long long lt = (1ull << lane) - 1ull;
+
+  for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
+  __syncthreads();
+
+  unsigned va[kSortItems], vb[kSortItems];
+  int dig[kSortItems], lpos[kSortItems];
+  {
+    const int d = input_edges_before(m.E_in, base);
+    const IdxT* sb = src ? src + base : nullptr;
+    const IdxT* tb = tgt + base;
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+      const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
+      const int c = p < tile_n ? p : tile_n - 1;
+      if constexpr (MODE == 0) {
+        IdxT s0, t0;
+        load_raw(sb, tb, c, d, &s0, &t0);
+        int sv, key;
+        bool bad;
+        decode_edge(m, c, d, s0, t0, sb != nullptr, &sv, &key, &bad);
+        va[i] = pack_a(key >> q.lp, sv, q);
+        vb[i] = pack_b(sv, (int)(base + c), q);
+        dig[i] = key & (radix - 1);
+      } else {
+        va[i] = ain[base + c];
+        vb[i] = bin[base + c];
+        dig[i] = (int)(va[i] >> shift) & (radix - 1);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+    const bool valid = p < tile_n;
+    const int d = dig[i];
+    unsigned long long peers = __ballot(valid);
+    for (int b = 0; b < dbits; ++b) {
+      const int bit = (d >> b) & 1;
+      const unsigned long long bb = __ballot(bit);
+      peers &= bit ? bb : ~bb;
+    }
+    const int below = __popcll(peers & lt);
+    const int run = valid ? (int)wcnt[wave][d] : 0;
+    lpos[i] = run + below;
+    if (valid && below == 0) wcnt[wave][d] = (unsigned short)(run + __popcll(peers));
+  }
+  __syncthreads();
+  {
+    const int d = threadIdx.x;
+    int tot = 0;
+    if (d < radix) {
+#pragma unroll
+      for (int w = 0; w < kSortWaves; ++w) {
+        const int c = wcnt[w][d];
+        wcnt[w][d] = (unsigned short)tot;
+        tot += c;
+      }
+    }
+    const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
+    if (d < radix) {
+      loff[d] = ex;
+      goff[d] = hist[(int64_t)d * ntiles + tile];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+    if (p < tile_n) {
+      const int l = lpos[i] + loff[dig[i]] + (int)wcnt[wave][dig[i]];
+      stage[0][l] = va[i];
+      stage[1][l] = vb[i];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int p = i * kSortThreads + threadIdx.x;
+    if (p < tile_n) {
+      const unsigned a = stage[0][p], b = stage[1][p];
+      const int d = MODE == 0 ? packed_key(a, b, m, q) & (radix - 1)
+                              : (int)(a >> shift) & (radix - 1);
+      const int64_t gp = (int64_t)goff[d] + (p - loff[d]);
+      if (gp >= 0 && gp < E) {  // always true for a consistent histogram
+        if constexpr (MODE == 2) {
+          o0[gp] = packed_key(a, b, m, q);
+          o1[gp] = unpack_e(b, q);
+          o2[gp] = unpack_s(a, b, q);
+        } else {
+          o0[gp] = (int)a;
+          o1[gp] = (int)b;
+        }
+      }
+    }
+  }
 }
 
 // bounds[v] = first position whose sorted key is >= v (v = 0..K). Position k
@@ -664,16 +821,27 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
   const unsigned nt = (unsigned)p.ntiles;
   const int radix = 1 << p.dbits;
 
+  // packed payloads (scatter_packed): P a power of two, ids and positions in 64 bits
+  const int lp = ceil_log2(g.parts);
+  const int bt = ceil_log2(g.N), bs = ceil_log2(g.N_src), be = ceil_log2(E);
+  const int sl = std::max(0, bs - (32 - bt));
+  bool packed = p.passes >= 2 && (int64_t(1) << lp) == g.parts && bt >= 1 && bt <= 31 &&
+                be <= 31 && sl + be <= 32 && p.dbits >= lp;
+  if (const char* v = std::getenv("TFG_SORT_PACKED")) packed = packed && v[0] != '0';
+  const PackMap q{bt, sl, be, lp};
+
   if (E > 0) {
     int cur = 0;  // which scratch buffer holds the current keys
     for (int pass = 0; pass < p.passes; ++pass) {
       const int shift = pass * p.dbits;
       const bool first = pass == 0, last = pass == p.passes - 1;
+      // packed passes after the first find their digit in A
+      const int dshift = (packed && !first) ? 32 - bt + shift - lp : shift;
       if (first)
         upsweep<true, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, nullptr, E, shift, p.dbits,
                                                         hist, err);
       else
-        upsweep<false, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, shift,
+        upsweep<false, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, dshift,
                                                          p.dbits, hist, err);
       const int rc = exclusive_scan(hist, hist, radix * p.ntiles, sums, s);
       if (rc) return rc;
@@ -683,12 +851,28 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
       int* eo = last ? g.perm : bufs[nxt][1];
       int* so = last ? g.col : bufs[nxt][2];
       const int *ki = bufs[cur][0], *ei = bufs[cur][1], *si = bufs[cur][2];
-      if (first)
+      if (packed) {
+        const unsigned* ai = reinterpret_cast<const unsigned*>(ki);
+        const unsigned* bi = reinterpret_cast<const unsigned*>(ei);
+        if (first)
+          scatter_packed<0, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
+                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
+                                                              so);
+        else if (last)
+          scatter_packed<2, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
+                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
+                                                              so);
+        else
+          scatter_packed<1, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
+                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
+                                                              so);
+      } else if (first) {
         scatter<true, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift, p.dbits,
                                                         hist, (int)p.ntiles, ko, eo, so);
-      else
+      } else {
         scatter<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift,
                                                          p.dbits, hist, (int)p.ntiles, ko, eo, so);
+      }
       TFG_LAUNCHED("radix scatter");
       cur = nxt;
     }

@@ -103,6 +103,32 @@ def test_csr_bit_exact(tfg, orc, n, e, loops, idx, parts):
         assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
 
 
+@pytest.mark.parametrize("n,n_src,e,loops,idx,parts,packed", [
+    (300_000, 300_000, 40_000, False, np.int32, 1, "0"),  # three passes, three-word payloads
+    (70_000, 70_000, 200_000, True, np.int64, 16, "0"),   # 21-bit keys, three-word payloads
+    (2000, 2000, 90_000, True, np.int32, 8, "0"),         # two passes, three-word payloads
+    (150_000, 300_000, 120_000, False, np.int32, 4, "1"),  # rectangular: source bits in both words
+    (300_000, 5_000, 60_000, False, np.int64, 2, "1"),    # rectangular: every source bit in A
+])
+def test_csr_packed_and_unpacked_payloads(tfg, orc, monkeypatch, n, n_src, e, loops, idx, parts,
+                                          packed):
+    # the radix passes carry (key, edge id, source) as three words, or, with
+    # a power-of-two part count, packed into two; both give the oracle's order
+    monkeypatch.setenv("TFG_SORT_PACKED", packed)
+    ei = graphgen.random_graph(e + n + 1, n, e, n_src=n_src, hub=n // 3, hub_edges=e // 5)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, N_src=n_src, add_self_loops=loops,
+                             src_parts=parts)
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    full = ei
+    if loops:
+        full = np.concatenate([ei, np.stack([np.arange(n), np.arange(n)])], axis=1)
+    ref = expected_graph(orc, full, n, parts=g.info()["src_parts"], n_src=n_src)
+    assert np.array_equal(rowptr, ref[0]) and np.array_equal(perm, ref[2])
+    assert np.array_equal(col, ref[1])
+    if g.info()["src_parts"] > 1:
+        assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
+
+
 def test_auto_parts(tfg):
     # small source table: one part; large table with long rows: several
     ei = graphgen.random_graph(3, 1000, 20_000)
