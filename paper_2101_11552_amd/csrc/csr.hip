@@ -70,16 +70,33 @@ __device__ __forceinline__ int input_edges_before(int64_t E_in, int64_t base) {
   return (int)(E_in - base);  // |E_in - base| < 2^31: both below 2^31
 }
 
-// Raw ids of tile position p, read for every position (clamped to the tile's
-// last input edge, or not read when the tile has none) so that the loads of
-// a whole tile can be issued together; decode_edge() then applies the range
-// checks and the loop rule.
-template <typename IdxT>
-__device__ __forceinline__ void load_raw(const IdxT* __restrict__ sb, const IdxT* __restrict__ tb,
-                                         int p, int d, IdxT* s, IdxT* t) {
-  const int q = p < d ? p : d - 1;
-  *s = (sb && d > 0) ? sb[q] : IdxT(0);
-  *t = d > 0 ? tb[q] : IdxT(0);
+// The raw ids of N tile positions pos[i], every load issued before any is
+// used (the branches are uniform: they depend on the tile only).
+template <int N, typename IdxT>
+__device__ __forceinline__ void load_raw_all(const IdxT* __restrict__ sb,
+                                             const IdxT* __restrict__ tb, const int (&pos)[N],
+                                             int d, IdxT (&s)[N], IdxT (&t)[N]) {
+  if (d <= 0) {  // loops only
+#pragma unroll
+    for (int i = 0; i < N; ++i) s[i] = t[i] = IdxT(0);
+    return;
+  }
+  int q[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) q[i] = pos[i] < d ? pos[i] : d - 1;
+  if (sb != nullptr) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      s[i] = sb[q[i]];
+      t[i] = tb[q[i]];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      s[i] = IdxT(0);
+      t[i] = tb[q[i]];
+    }
+  }
 }
 
 template <typename IdxT>
@@ -210,12 +227,20 @@ __global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ s
   const IdxT* sb = src ? src + base : nullptr;
   const IdxT* tb = tgt + base;
   IdxT rs[kUpItems], rt[kUpItems];
+  if constexpr (FIRST) {
+    // read for every position (clamped to the tile's last input edge, or not
+    // read when the tile has none), so that all loads are issued together
 #pragma unroll
-  for (int i = 0; i < kUpItems; ++i) {
-    const int p = i * kUpThreads + (int)threadIdx.x;
-    if constexpr (FIRST) {
-      load_raw(sb, tb, p, d, &rs[i], &rt[i]);
-    } else {
+    for (int i = 0; i < kUpItems; ++i) {
+      const int p = i * kUpThreads + (int)threadIdx.x;
+      const int c = p < d ? p : d - 1;
+      rs[i] = (sb && d > 0) ? sb[c] : IdxT(0);
+      rt[i] = d > 0 ? tb[c] : IdxT(0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kUpItems; ++i) {
+      const int p = i * kUpThreads + (int)threadIdx.x;
       rt[i] = (IdxT)keys[base + (p < tile_n ? p : tile_n - 1)];
       rs[i] = 0;
     }
@@ -284,19 +309,26 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   const int d = input_edges_before(m.E_in, base);
   const IdxT* sb = src ? src + base : nullptr;
   const IdxT* tb = tgt + base;
+  int c[kSortItems];  // positions in the tile (clamped to its last)
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
-    const int q = p < tile_n ? p : tile_n - 1;
-    if constexpr (FIRST) {
-      IdxT s0, t0;
-      load_raw(sb, tb, q, d, &s0, &t0);
+    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+    c[i] = p < tile_n ? p : tile_n - 1;
+  }
+  if constexpr (FIRST) {
+    IdxT rs[kSortItems], rt[kSortItems];
+    load_raw_all(sb, tb, c, d, rs, rt);
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
       bool bad;
-      decode_edge(m, q, d, s0, t0, sb != nullptr, &ps[i], &key[i], &bad);
-    } else {
-      key[i] = kin[base + q];
-      pe[i] = ein[base + q];
-      ps[i] = sin[base + q];
+      decode_edge(m, c[i], d, rs[i], rt[i], sb != nullptr, &ps[i], &key[i], &bad);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+      key[i] = kin[base + c[i]];
+      pe[i] = ein[base + c[i]];
+      ps[i] = sin[base + c[i]];
     }
   }
 #pragma unroll
@@ -454,24 +486,32 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
     const int d = input_edges_before(m.E_in, base);
     const IdxT* sb = src ? src + base : nullptr;
     const IdxT* tb = tgt + base;
+    int c[kSortItems];  // positions in the tile (clamped to its last)
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-      const int p = wave * (kWave * kSortItems) + i * kWave + lane;  // position in tile
-      const int c = p < tile_n ? p : tile_n - 1;
-      if constexpr (MODE == 0) {
-        IdxT s0, t0;
-        load_raw(sb, tb, c, d, &s0, &t0);
+      const int p = wave * (kWave * kSortItems) + i * kWave + lane;
+      c[i] = p < tile_n ? p : tile_n - 1;
+    }
+    if constexpr (MODE == 0) {
+      IdxT rs[kSortItems], rt[kSortItems];
+      load_raw_all(sb, tb, c, d, rs, rt);
+#pragma unroll
+      for (int i = 0; i < kSortItems; ++i) {
         int sv, key;
         bool bad;
-        decode_edge(m, c, d, s0, t0, sb != nullptr, &sv, &key, &bad);
+        decode_edge(m, c[i], d, rs[i], rt[i], sb != nullptr, &sv, &key, &bad);
         va[i] = pack_a(key >> q.lp, sv, q);
-        vb[i] = pack_b(sv, (int)(base + c), q);
+        vb[i] = pack_b(sv, (int)(base + c[i]), q);
         dig[i] = key & (radix - 1);
-      } else {
-        va[i] = ain[base + c];
-        vb[i] = bin[base + c];
-        dig[i] = (int)(va[i] >> shift) & (radix - 1);
       }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kSortItems; ++i) {
+        va[i] = ain[base + c[i]];
+        vb[i] = bin[base + c[i]];
+      }
+#pragma unroll
+      for (int i = 0; i < kSortItems; ++i) dig[i] = (int)(va[i] >> shift) & (radix - 1);
     }
   }
 #pragma unroll
@@ -512,20 +552,28 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;
-    if (p < tile_n) {
-      const int l = lpos[i] + loff[dig[i]] + (int)wcnt[wave][dig[i]];
-      stage[0][l] = va[i];
-      stage[1][l] = vb[i];
-    }
+    lpos[i] = p < tile_n ? lpos[i] + loff[dig[i]] + (int)wcnt[wave][dig[i]] : -1;
   }
+  // The first pass's digit is not a field of A: once every position is known
+  // (the barrier), the per-wave counters' LDS (exactly one byte per tile
+  // position) holds the digit of every staged position instead.
+  unsigned char* sdig = reinterpret_cast<unsigned char*>(&wcnt[0][0]);
+  static_assert(sizeof(wcnt) >= kSortTile, "one byte per tile position");
+  if constexpr (MODE == 0) __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i)
+    if (lpos[i] >= 0) {
+      stage[0][lpos[i]] = va[i];
+      stage[1][lpos[i]] = vb[i];
+      if constexpr (MODE == 0) sdig[lpos[i]] = (unsigned char)dig[i];
+    }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = i * kSortThreads + threadIdx.x;
     if (p < tile_n) {
       const unsigned a = stage[0][p], b = stage[1][p];
-      const int d = MODE == 0 ? packed_key(a, b, m, q) & (radix - 1)
-                              : (int)(a >> shift) & (radix - 1);
+      const int d = MODE == 0 ? (int)sdig[p] : (int)(a >> shift) & (radix - 1);
       const int64_t gp = (int64_t)goff[d] + (p - loff[d]);
       if (gp >= 0 && gp < E) {  // always true for a consistent histogram
         if constexpr (MODE == 2) {
