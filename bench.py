@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "aggregated edges/sec (GE/s) and achieved HBM GB/s for fp32 GCN sum-aggregation"
 AGG_SRC = [os.path.join(ROOT, "paper_2101_11552_amd", "csrc", f) for f in ("spmm.h", "aggregate.hip")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_rows_c4.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_rows_powerlaw.txt")
 
 
 def algorithmic_bytes(E_total: int, N: int, F: int) -> int:
@@ -167,7 +167,7 @@ def load_workload(cache: str | None):
     if cache and os.path.exists(cache):
         z = np.load(cache)
         return z["edge_index"], z["x"]
-    c = graphgen.config4(dtype=np.int32)
+    c = graphgen.power_law(dtype=np.int32)
     if cache:
         np.savez(cache, edge_index=c["edge_index"], x=c["x"])
     return c["edge_index"], c["x"]
@@ -392,7 +392,7 @@ def run_suite(args):
     torch.cuda.empty_cache()
 
     # --- attention on the preferential-attachment graph
-    c = graphgen.config3()
+    c = graphgen.attention_graph()
     n3, H, D = c["N"], c["H"], c["D"]
     Fh = H * D
     ei3 = torch.from_numpy(c["edge_index"].astype(np.int32)).to(dev)
@@ -470,7 +470,7 @@ def run_suite(args):
     torch.cuda.empty_cache()
 
     # --- mini-batch of small graphs: BatchGraph, 3 GCN layers, pooling
-    c = graphgen.config5()
+    c = graphgen.graph_batch()
     sizes, graphs = c["sizes"], c["graphs"]
     G, Fb = c["G"], c["F"]
     nc = torch.from_numpy(sizes.astype(np.int32)).to(dev)
@@ -538,7 +538,7 @@ def run_suite(args):
          cpu_baseline=cpu.get("pool"))
 
     # --- the GCN step on the two small uniform graphs
-    for cfg in (graphgen.config1(), graphgen.config2()):
+    for cfg in (graphgen.uniform_small(), graphgen.uniform_medium()):
         n, Fc = cfg["N"], cfg["F"]
         eic = torch.from_numpy(cfg["edge_index"].astype(np.int32)).to(dev)
         xc = torch.from_numpy(cfg["x"]).to(dev)
@@ -563,7 +563,7 @@ def run_suite(args):
             cb = _oracle(oracle_gcn, Ec, "GE/s", "the whole graph")
             cbt = _oracle_threads(oracle_gcn_threads, Ec, "GE/s",
                                   "the whole graph (normalisation on one thread)")
-        _row("GCN step: CSR + gcn_norm + sum aggregation", f"{cfg['name']}: uniform graph N={n}, "
+        _row("GCN step: CSR + gcn_norm + sum aggregation", f"uniform graph N={n}, "
              f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb, cpu_baseline_threads=cbt)
 
 
@@ -772,7 +772,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
-                     "traffic_source": ("stored: profiles/traffic_spmm_rows_c4.txt, rocprofv3 "
+                     "traffic_source": ("stored: profiles/traffic_spmm_rows_powerlaw.txt, rocprofv3 "
                                         "FETCH_SIZE + WRITE_SIZE per launch, taken on the "
                                         "current kernel source" if traffic else None),
                      "traffic_GBps": (round(traffic / (agg_ms * 1e-3) / 1e9, 1)

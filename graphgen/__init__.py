@@ -16,14 +16,14 @@ The five workloads mirror the shapes of the paper's evaluation graphs (the
 paper's own datasets are not available here, so these stand in for their
 sizes and degree structure):
 
-* ``config1`` — 2,708 nodes, 5,278 distinct undirected pairs (citation-graph
+* ``uniform_small`` — 2,708 nodes, 5,278 distinct undirected pairs (citation-graph
   sized), F = 64.
-* ``config2`` — 19,717 nodes, 44,324 distinct undirected pairs, F = 128.
-* ``config3`` — 169,343 nodes, Barabási–Albert preferential attachment with
+* ``uniform_medium`` — 19,717 nodes, 44,324 distinct undirected pairs, F = 128.
+* ``attention_graph`` — 169,343 nodes, Barabási–Albert preferential attachment with
   m = 7 (directed new -> old), 8 heads x 16 dims.
-* ``config4`` — 232,965 nodes, Chung–Lu power law (gamma = 2), 114.6M directed
+* ``power_law`` — 232,965 nodes, Chung–Lu power law (gamma = 2), 114.6M directed
   edges, F = 128.
-* ``config5`` — 4,096 small graphs of 10..60 nodes, G(n, 0.1), batched into one
+* ``graph_batch`` — 4,096 small graphs of 10..60 nodes, G(n, 0.1), batched into one
   disjoint graph with a sorted graph index, F = 64.
 
 Edge lists are int64 arrays of shape [2, E]: row 0 holds source ids, row 1
@@ -215,25 +215,25 @@ def stack_batch(sizes: np.ndarray, graphs: list[np.ndarray]):
 # The five workloads
 # ---------------------------------------------------------------------------
 
-def config1():
+def uniform_small():
     s = SEED_BASE + 1
     n = 2708
-    return {"name": "c1", "N": n, "F": 64, "edge_index": uniform_pairs(s, n, 5278),
+    return {"name": "uniform-2708", "N": n, "F": 64, "edge_index": uniform_pairs(s, n, 5278),
             "x": features(s, n, 64)}
 
 
-def config2():
+def uniform_medium():
     s = SEED_BASE + 2
     n = 19717
-    return {"name": "c2", "N": n, "F": 128, "edge_index": uniform_pairs(s, n, 44324),
+    return {"name": "uniform-19717", "N": n, "F": 128, "edge_index": uniform_pairs(s, n, 44324),
             "x": features(s, n, 128)}
 
 
-def config3():
+def attention_graph():
     s = SEED_BASE + 3
     n, heads, dims = 169343, 8, 16
     ra = rng_for(s, 2)
-    return {"name": "c3", "N": n, "H": heads, "D": dims,
+    return {"name": "ba-169343", "N": n, "H": heads, "D": dims,
             "edge_index": barabasi_albert(s, n, 7),
             "h": features(s, n, heads * dims),
             "a_src": ra.standard_normal((heads, dims), dtype=np.float32),
@@ -241,22 +241,23 @@ def config3():
             "slope": 0.2}
 
 
-def config4(n_pairs: int = 57_300_000, dtype=np.int64):
+def power_law(n_pairs: int = 57_300_000, dtype=np.int64):
     s = SEED_BASE + 4
     n = 232965
-    return {"name": "c4", "N": n, "F": 128,
+    return {"name": "powerlaw-232965", "N": n, "F": 128,
             "edge_index": chung_lu(s, n, n_pairs, dtype=dtype),
             "x": features(s, n, 128)}
 
 
-def config5():
+def graph_batch():
     s = SEED_BASE + 5
     sizes, graphs = batch_of_small_graphs(s, 4096, 10, 60, 0.1)
     edge_index, graph_index = stack_batch(sizes, graphs)
     nb = int(sizes.sum())
-    return {"name": "c5", "N": nb, "F": 64, "G": 4096, "layers": 3,
+    return {"name": "batch-4096", "N": nb, "F": 64, "G": 4096, "layers": 3,
             "sizes": sizes, "graphs": graphs, "edge_index": edge_index,
             "graph_index": graph_index, "x": features(s, nb, 64)}
 
 
-CONFIGS = {"c1": config1, "c2": config2, "c3": config3, "c4": config4, "c5": config5}
+WORKLOADS = {"uniform-2708": uniform_small, "uniform-19717": uniform_medium, "ba-169343": attention_graph,
+             "powerlaw-232965": power_law, "batch-4096": graph_batch}
