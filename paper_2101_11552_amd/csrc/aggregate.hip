@@ -65,7 +65,7 @@ __global__ __launch_bounds__(kItemBlock) void fixup_rows(const SplitRow* __restr
 #pragma unroll
         for (int i = 0; i < kFixAcc; ++i) {
           if (j + i < nch) {
-            load_row<V>(part + (int64_t)(slot0 + j + i) * F + f, t[i]);
+            load_row_once<V>(part + (int64_t)(slot0 + j + i) * F + f, t[i]);
           } else {
 #pragma unroll
             for (int v = 0; v < V; ++v) t[i][v] = 0.0f;

@@ -87,14 +87,14 @@ __device__ __forceinline__ void load_raw_all(const IdxT* __restrict__ sb,
   if (sb != nullptr) {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      s[i] = sb[q[i]];
-      t[i] = tb[q[i]];
+      s[i] = __builtin_nontemporal_load(sb + q[i]);
+      t[i] = __builtin_nontemporal_load(tb + q[i]);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       s[i] = IdxT(0);
-      t[i] = tb[q[i]];
+      t[i] = __builtin_nontemporal_load(tb + q[i]);
     }
   }
 }
@@ -234,14 +234,14 @@ __global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ s
     for (int i = 0; i < kUpItems; ++i) {
       const int p = i * kUpThreads + (int)threadIdx.x;
       const int c = p < d ? p : d - 1;
-      rs[i] = (sb && d > 0) ? sb[c] : IdxT(0);
-      rt[i] = d > 0 ? tb[c] : IdxT(0);
+      rs[i] = (sb && d > 0) ? __builtin_nontemporal_load(sb + c) : IdxT(0);
+      rt[i] = d > 0 ? __builtin_nontemporal_load(tb + c) : IdxT(0);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < kUpItems; ++i) {
       const int p = i * kUpThreads + (int)threadIdx.x;
-      rt[i] = (IdxT)keys[base + (p < tile_n ? p : tile_n - 1)];
+      rt[i] = (IdxT)__builtin_nontemporal_load(keys + base + (p < tile_n ? p : tile_n - 1));
       rs[i] = 0;
     }
   }
@@ -599,7 +599,8 @@ __global__ __launch_bounds__(kKbThreads) void key_bounds(const int* __restrict__
   const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   int c[4];
   if (k0 + 4 <= E) {
-    const int4 v = *reinterpret_cast<const int4*>(keys + k0);
+    typedef int i4 __attribute__((ext_vector_type(4)));
+    const i4 v = __builtin_nontemporal_load(reinterpret_cast<const i4*>(keys + k0));
     c[0] = v.x;
     c[1] = v.y;
     c[2] = v.z;

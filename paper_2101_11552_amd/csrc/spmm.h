@@ -39,6 +39,20 @@ __device__ __forceinline__ void load_row(const float* __restrict__ p, float (&v)
   }
 }
 
+// The same, for data read once (streamed past the L2).
+template <int V>
+__device__ __forceinline__ void load_row_once(const float* __restrict__ p, float (&v)[V]) {
+  if constexpr (V == 4) {
+    f4 t = __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else if constexpr (V == 2) {
+    f2 t = __builtin_nontemporal_load(reinterpret_cast<const f2*>(p));
+    v[0] = t.x; v[1] = t.y;
+  } else {
+    v[0] = __builtin_nontemporal_load(p);
+  }
+}
+
 template <int V>
 __device__ __forceinline__ void load_irow(const int* __restrict__ p, int (&v)[V]) {
   if constexpr (V == 4) {
@@ -277,9 +291,9 @@ __global__ __launch_bounds__(kRowBlock) void spmm_rows(
 #pragma unroll
           for (int v = 0; v < V; ++v) argout[(int64_t)row * F + f + v] = arg[0][v];
       } else {
-        float* p = part + (int64_t)pslot * F + f;
-#pragma unroll
-        for (int v = 0; v < V; ++v) p[v] = acc[0][v];
+        // partial rows are read back once, by the fix-up, long after: streamed
+        // past the L2, which they would otherwise share with the gathered rows
+        store_row<V>(part + (int64_t)pslot * F + f, acc[0]);
         if (MAX)
 #pragma unroll
           for (int v = 0; v < V; ++v) part_arg[(int64_t)pslot * F + f + v] = arg[0][v];
