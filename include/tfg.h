@@ -168,8 +168,10 @@ int tfg_graph_csr(const tfg_graph *g, int32_t *rowptr, int32_t *col, int32_t *pe
  *   to the order of `to` (NULL = the caller's COO order, else a graph handle;
  *   both handles, or the handle and the COO array, must describe the same E'
  *   edges, e.g. a graph and its transpose). Gathers through the target order's
- *   perm; graph -> graph goes through COO order in `ws` (E' * H floats, query
- *   with tfg_edge_reorder_ws_bytes). Per-edge values that depend only on the
+ *   perm; leaving a graph order scatters through the source order's perm
+ *   (with one value per edge on graphs of 2^20 edges or more, through buckets
+ *   of destinations in `ws`); graph -> graph goes through COO order in `ws`.
+ *   Query the workspace with tfg_edge_reorder_ws_bytes. Per-edge values that depend only on the
  *   graph structure (normalised weights) are reordered once and cached, like
  *   the graph itself. out must not overlap in.
  */

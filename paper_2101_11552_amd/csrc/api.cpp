@@ -283,8 +283,7 @@ int tfg_graph_csr(const tfg_graph* h, int32_t* rowptr, int32_t* col, int32_t* pe
 size_t tfg_edge_reorder_ws_bytes(const tfg_graph* from, const tfg_graph* to, int64_t H) {
   if (H < 1) return 0;
   const int64_t E = from ? from->g.E : (to ? to->g.E : 0);
-  return (from && to) ? align_up(sizeof(float) * (size_t)std::max<int64_t>(E * H, 1), 256) + 256
-                      : 256;
+  return edge_reorder_ws_bytes(E, (int)H, from != nullptr, to != nullptr) + 256;
 }
 
 int tfg_edge_reorder(const tfg_graph* from, const tfg_graph* to, const float* in, int64_t H,
@@ -300,7 +299,7 @@ int tfg_edge_reorder(const tfg_graph* from, const tfg_graph* to, const float* in
   if (int rc = check_device(from)) return rc;
   if (int rc = check_device(to)) return rc;
   return launch_edge_reorder(from ? from->g.perm : nullptr, to ? to->g.perm : nullptr, E, (int)H,
-                             in, out, static_cast<float*>(ws), as_stream(stream));
+                             in, out, ws, ws_bytes, as_stream(stream));
 }
 
 int tfg_graph_info(const tfg_graph* h, int64_t* E_total, int64_t* N, int64_t* N_src,

@@ -14,6 +14,8 @@
 // per head, the sum accumulated in double (softmax_grad_items; long rows in
 // chunks whose sums are added in chunk order).
 // Every result has one writer and a fixed summation order: no atomics.
+#include <cstdlib>
+
 #include "spmm.h"
 
 namespace tfg {
@@ -242,6 +244,115 @@ __global__ __launch_bounds__(kBlock) void to_edge_order(const int* __restrict__ 
   out[(int64_t)perm[k] * H + h] = in[i];
 }
 
+// The same scatter for one value per edge on large graphs, in two passes
+// through buckets of 2^kPermBits consecutive destinations (a random 4-byte
+// store moves a whole line; these passes move whole lines):
+//   perm_count   per tile of kPermTile positions, the count of each bucket
+//                (one column of a bucket-major table);
+//   (exclusive scan of the table: every (bucket, tile) its place)
+//   perm_bucket  each position's (destination mod 2^kPermBits, value) pair
+//                to its bucket's place for this tile, slots taken with LDS
+//                atomics (the order inside a bucket does not matter);
+//   perm_place   one block per bucket: the pairs into LDS at their offsets,
+//                then the bucket's 2^kPermBits destinations written in order.
+// perm is a permutation, so every destination of a bucket is written once.
+constexpr int kPermBits = 15;                         // destinations per bucket (128 KB of LDS)
+constexpr int kPermThreads = 1024;
+constexpr int kPermItems = 64;                        // positions per thread and tile
+constexpr int kPermTile = kPermThreads * kPermItems;  // 65536
+constexpr int kPermMaxBuckets = 8192;                 // LDS counters (32 KB)
+constexpr int kPermXcds = 8;
+
+// tiles in XCD-contiguous order (blocks are dispatched round-robin over the
+// XCDs), so that the bucket runs of neighbouring tiles meet in one L2
+__device__ __forceinline__ int perm_tile_of(int bid, int ntiles) {
+  const int q = ntiles / kPermXcds, r = ntiles % kPermXcds;
+  const int x = bid % kPermXcds, i = bid / kPermXcds;
+  return x * q + min(x, r) + i;
+}
+
+__global__ __launch_bounds__(kPermThreads) void perm_count(const int* __restrict__ perm, int64_t E,
+                                                       int nbuckets, int ntiles,
+                                                       int* __restrict__ table) {
+  __shared__ int cnt[kPermMaxBuckets];
+  for (int b = threadIdx.x; b < nbuckets; b += kPermThreads) cnt[b] = 0;
+  __syncthreads();
+  const int tile = perm_tile_of((int)blockIdx.x, ntiles);
+  const int64_t base = (int64_t)tile * kPermTile;
+  const int n = (int)min<int64_t>(kPermTile, E - base);
+  for (int i0 = 0; i0 < kPermItems; i0 += 16) {
+    int d[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int p = (i0 + i) * kPermThreads + (int)threadIdx.x;
+      d[i] = p < n ? __builtin_nontemporal_load(perm + base + p) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (d[i] >= 0) atomicAdd(&cnt[d[i] >> kPermBits], 1);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < nbuckets; b += kPermThreads)
+    table[(int64_t)b * ntiles + tile] = cnt[b];
+}
+
+__global__ __launch_bounds__(kPermThreads) void perm_bucket(const int* __restrict__ perm,
+                                                        const float* __restrict__ in, int64_t E,
+                                                        int nbuckets, int ntiles,
+                                                        const int* __restrict__ table,
+                                                        int2* __restrict__ pairs) {
+  __shared__ int cur[kPermMaxBuckets];
+  const int tile = perm_tile_of((int)blockIdx.x, ntiles);
+  for (int b = threadIdx.x; b < nbuckets; b += kPermThreads)
+    cur[b] = table[(int64_t)b * ntiles + tile];
+  __syncthreads();
+  const int64_t base = (int64_t)tile * kPermTile;
+  const int n = (int)min<int64_t>(kPermTile, E - base);
+  for (int i0 = 0; i0 < kPermItems; i0 += 16) {
+    int d[16];
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int p = (i0 + i) * kPermThreads + (int)threadIdx.x;
+      d[i] = p < n ? __builtin_nontemporal_load(perm + base + p) : -1;
+      v[i] = p < n ? __builtin_nontemporal_load(in + base + p) : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (d[i] >= 0) {
+        const int slot = atomicAdd(&cur[d[i] >> kPermBits], 1);
+        pairs[slot] = make_int2(d[i] & ((1 << kPermBits) - 1), __float_as_int(v[i]));
+      }
+  }
+}
+
+__global__ __launch_bounds__(kPermThreads) void perm_place(const int2* __restrict__ pairs,
+                                                       const int* __restrict__ table, int ntiles,
+                                                       int64_t E, int nbuckets,
+                                                       float* __restrict__ out) {
+  __shared__ float buf[1 << kPermBits];
+  const int b = (int)blockIdx.x;
+  const int64_t start = table[(int64_t)b * ntiles];
+  const int64_t end = b + 1 < nbuckets ? table[(int64_t)(b + 1) * ntiles] : E;
+  typedef int i2v __attribute__((ext_vector_type(2)));
+  const i2v* pv = reinterpret_cast<const i2v*>(pairs);
+  for (int64_t j0 = start; j0 < end; j0 += 8 * kPermThreads) {
+    i2v pr[8];  // eight loads in flight per thread
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t j = j0 + u * kPermThreads + threadIdx.x;
+      pr[u] = j < end ? __builtin_nontemporal_load(pv + j) : i2v{-1, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (pr[u].x >= 0) buf[pr[u].x] = __int_as_float(pr[u].y);
+  }
+  __syncthreads();
+  const int64_t o = (int64_t)b << kPermBits;
+  const int n = (int)min<int64_t>(int64_t(1) << kPermBits, E - o);
+  for (int j = threadIdx.x; j < n; j += kPermThreads) __builtin_nontemporal_store(buf[j], out + o + j);
+}
+
 // Caller's edge order -> graph order: out[k, h] = in[perm[k], h].
 __global__ __launch_bounds__(kBlock) void to_graph_order(const int* __restrict__ perm, int64_t E,
                                                          int H, const float* __restrict__ in,
@@ -409,22 +520,79 @@ int launch_edge_grad(const Graph& g, const float* x, int64_t ldx, const float* d
 
 }  // namespace
 
+// Bytes of the bucketed scatter's scratch (pairs, bucket table, scan sums);
+// 0 where the plain scatter runs (several values per edge, small or very
+// large graphs).
+size_t perm_scatter_ws_bytes(int64_t E, int H) {
+  if (H != 1 || E < (int64_t(1) << 20)) return 0;
+  if (const char* v = std::getenv("TFG_PERM_BUCKETS"))  // "0": the plain scatter
+    if (v[0] == '0') return 0;
+  const int64_t nbuckets = (E + (int64_t(1) << kPermBits) - 1) >> kPermBits;
+  if (nbuckets > kPermMaxBuckets) return 0;
+  const int64_t ntiles = (E + kPermTile - 1) / kPermTile;
+  const int64_t entries = nbuckets * ntiles;
+  return align_up(sizeof(int2) * (size_t)E, 256) + align_up(sizeof(int) * (size_t)entries, 256) +
+         align_up(sizeof(int) * (size_t)exclusive_scan_sums(entries), 256);
+}
+
+// out[perm[k], h] = in[k, h]; bucketed when ws holds perm_scatter_ws_bytes.
+int launch_perm_scatter(const int* perm, int64_t E, int H, const float* in, float* out, void* ws,
+                        size_t ws_bytes, hipStream_t s) {
+  const int64_t n = E * H;
+  if (n == 0) return TFG_OK;
+  const size_t need = perm_scatter_ws_bytes(E, H);
+  if (need == 0 || ws == nullptr || ws_bytes < need) {
+    to_edge_order<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(perm, E, H, in, out);
+    TFG_LAUNCHED("to_edge_order");
+    return TFG_OK;
+  }
+  const int nbuckets = (int)((E + (int64_t(1) << kPermBits) - 1) >> kPermBits);
+  const int ntiles = (int)((E + kPermTile - 1) / kPermTile);
+  const int64_t entries = (int64_t)nbuckets * ntiles;
+  char* c = static_cast<char*>(ws);
+  int2* pairs = reinterpret_cast<int2*>(c);
+  c += align_up(sizeof(int2) * (size_t)E, 256);
+  int* table = reinterpret_cast<int*>(c);
+  c += align_up(sizeof(int) * (size_t)entries, 256);
+  int* sums = reinterpret_cast<int*>(c);
+  perm_count<<<ntiles, kPermThreads, 0, s>>>(perm, E, nbuckets, ntiles, table);
+  TFG_LAUNCHED("perm_count");
+  if (int rc = exclusive_scan(table, table, entries, sums, s)) return rc;
+  perm_bucket<<<ntiles, kPermThreads, 0, s>>>(perm, in, E, nbuckets, ntiles, table, pairs);
+  TFG_LAUNCHED("perm_bucket");
+  perm_place<<<nbuckets, kPermThreads, 0, s>>>(pairs, table, ntiles, E, nbuckets, out);
+  TFG_LAUNCHED("perm_place");
+  return TFG_OK;
+}
+
+
 int launch_edge_dot(const Graph& g, const float* q, const float* key, int64_t ldk, int64_t F,
                     int H, float scale, float* out, int by_perm, hipStream_t s) {
   if (g.E == 0 || F == 0) return TFG_OK;
   return launch_edge_grad<kGradSum>(g, key, ldk, q, nullptr, F, H, out, by_perm, s, scale);
 }
 
+// Graph -> graph goes through edge order in the first E * H floats of ws;
+// the scatter's scratch follows.
+size_t edge_reorder_ws_bytes(int64_t E, int H, bool from, bool to) {
+  const size_t tmp = (from && to) ? align_up(sizeof(float) * (size_t)std::max<int64_t>(E * H, 1), 256) : 0;
+  return tmp + (from ? perm_scatter_ws_bytes(E, H) : 0);
+}
+
 int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
-                        const float* in, float* out, float* tmp, hipStream_t s) {
+                        const float* in, float* out, void* ws, size_t ws_bytes, hipStream_t s) {
   const int64_t n = E * H;
   if (n == 0) return TFG_OK;
   const unsigned nb = (unsigned)((n + kBlock - 1) / kBlock);
   if (perm_from != nullptr && perm_to != nullptr) {
-    to_edge_order<<<nb, kBlock, 0, s>>>(perm_from, E, H, in, tmp);
+    const size_t tb = align_up(sizeof(float) * (size_t)n, 256);
+    float* tmp = static_cast<float*>(ws);
+    const int rc = launch_perm_scatter(perm_from, E, H, in, tmp, static_cast<char*>(ws) + tb,
+                                       ws_bytes > tb ? ws_bytes - tb : 0, s);
+    if (rc) return rc;
     to_graph_order<<<nb, kBlock, 0, s>>>(perm_to, E, H, tmp, out);
   } else if (perm_from != nullptr) {
-    to_edge_order<<<nb, kBlock, 0, s>>>(perm_from, E, H, in, out);
+    return launch_perm_scatter(perm_from, E, H, in, out, ws, ws_bytes, s);
   } else {
     to_graph_order<<<nb, kBlock, 0, s>>>(perm_to, E, H, in, out);
   }
@@ -439,7 +607,8 @@ size_t aggregate_backward_ws_bytes(const Graph& g, const Graph* gt, int64_t F, i
   const int64_t parts = use_part_plan(*gt, F) ? gt->n_pexec : gt->n_heavy;
   b += aggregate_partial_bytes(parts, F, TFG_SUM);
   const size_t ew = align_up(sizeof(float) * (size_t)std::max<int64_t>(g.E * H, 1), 256);
-  if (has_w && w_order == TFG_CSR) b += ew;  // weights moved to edge order
+  // weights moved to edge order (and the bucketed scatter's scratch)
+  if (has_w && w_order == TFG_CSR) b += ew + perm_scatter_ws_bytes(g.E, (int)H);
   if (reduce == TFG_MEAN) b += ew;           // weights / degree in transposed order
   return b;
 }
@@ -464,8 +633,10 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
     if (w != nullptr && w_order == TFG_CSR && EH > 0) {
       float* t = reinterpret_cast<float*>(base + off);
       off += ew;
-      to_edge_order<<<eb, kBlock, 0, s>>>(g.perm, g.E, H, w, t);
-      TFG_LAUNCHED("to_edge_order");
+      const size_t sb = perm_scatter_ws_bytes(g.E, H);
+      const int rc = launch_perm_scatter(g.perm, g.E, H, w, t, sb ? base + off : nullptr, sb, s);
+      if (rc) return rc;
+      off += sb;
       wg = t;
     }
     if (gt->N > 0 && F > 0) {

@@ -963,6 +963,8 @@ int build_part_plan(Graph& g, char* scratch, const ScratchLayout& L, hipStream_t
 
 }  // namespace
 
+int64_t exclusive_scan_sums(int64_t n) { return std::max<int64_t>(scan_tiles(n), 1); }
+
 int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s) {
   if (n <= 0) return TFG_OK;
   if (in == out && n <= kSmallScan) {

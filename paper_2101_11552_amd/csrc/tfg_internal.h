@@ -122,7 +122,9 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // src may be NULL (a target-only list: col is then all zero).
 int build_graph(Graph& g, const void* src, const void* tgt, int index_type, void* scratch,
                 size_t scratch_bytes, hipStream_t s);
+// tile_sums: exclusive_scan_sums(n) ints of scratch
 int exclusive_scan(const int* in, int* out, int64_t n, int* tile_sums, hipStream_t s);
+int64_t exclusive_scan_sums(int64_t n);
 // norm.hip
 int launch_gcn_norm(const Graph& g, const void* edge_index, int index_type,
                     const float* edge_weight, int32_t* out_edge_index, float* out_w,
@@ -173,8 +175,14 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
                               int dw_order, void* ws, hipStream_t s);
 // out[k] = in[perm_to[k]] (COO -> graph), out[perm_from[k]] = in[k] (graph ->
 // COO), or both through tmp ([E, H] floats); either perm may be NULL.
+// out[perm[k], h] = in[k, h], bucketed on large graphs when ws holds
+// perm_scatter_ws_bytes(E, H) (0: the plain scatter, no scratch)
+size_t perm_scatter_ws_bytes(int64_t E, int H);
+int launch_perm_scatter(const int* perm, int64_t E, int H, const float* in, float* out, void* ws,
+                        size_t ws_bytes, hipStream_t s);
+size_t edge_reorder_ws_bytes(int64_t E, int H, bool from, bool to);
 int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
-                        const float* in, float* out, float* tmp, hipStream_t s);
+                        const float* in, float* out, void* ws, size_t ws_bytes, hipStream_t s);
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
                                     int H, float* ds, void* ws, hipStream_t s);
 // gat.hip

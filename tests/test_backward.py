@@ -153,6 +153,36 @@ def test_edge_reorder(tfg, orc):
     assert same_bits(host(back), v)
 
 
+@pytest.mark.parametrize("idx", [np.int32, np.int64])
+def test_edge_reorder_bucketed(tfg, orc, idx):
+    # one value per edge on a graph of more than 2^20 edges: graph order ->
+    # edge order runs through buckets of destinations (a ragged last bucket
+    # and tile); every path back and forth gives the same bits
+    import torch
+    n, e = 200_003, 3_000_000
+    ei = graphgen.random_graph(95, n, e, hub=7, hub_edges=40_000)
+    g = tfg.tfg_graph_create(dev(ei.astype(idx)), n, add_self_loops=True)
+    gt = tfg.tfg_graph_create_transposed(dev(ei.astype(idx)), n, add_self_loops=True)
+    full = with_loops(ei, n)
+    v = graphgen.features(95, full.shape[1], 1)[:, 0].copy()
+    p = orc.csr_by_target(full, n)[2]
+    pt = orc.csr_by_target(full[::-1], n)[2]
+    vg = tfg.tfg_edge_reorder(dev(v), dst=g)
+    assert same_bits(host(vg), v[p])
+    back = tfg.tfg_edge_reorder(vg, src=g)                    # bucketed scatter
+    assert same_bits(host(back), v)
+    vt = tfg.tfg_edge_reorder(vg, src=g, dst=gt)              # bucketed scatter, then gather
+    assert same_bits(host(vt), v[pt])
+    # the backward with weights in the forward graph's order moves them to
+    # edge order the same way: the same gradient as with weights in edge order
+    dy = dev(graphgen.features(97, n, 16))
+    a, _ = tfg.tfg_aggregate_backward(g, dy, "sum", graph_t=gt, edge_weight=dev(v))
+    b, _ = tfg.tfg_aggregate_backward(g, dy, "sum", graph_t=gt, edge_weight=vg,
+                                      weight_order="csr")
+    torch.cuda.synchronize()
+    assert same_bits(host(a), host(b))
+
+
 @pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
 def test_backward_transposed_order_weights(tfg, orc, reduce):
     # weights already in the transposed graph's order give the same gradients
