@@ -367,8 +367,8 @@ __global__ __launch_bounds__(kBlock) void to_graph_order(const int* __restrict__
 // Softmax gradient over the work items of the row plan; lanes are (slot,
 // head) pairs as in softmax_items. A whole row sums alpha * dalpha per head
 // (double), then writes ds; a chunk of a long row stores its sum,
-// softmax_grad_merge adds the chunks of each long row in chunk order and
-// softmax_grad_write writes their ds. (A bucket of short rows, as the softmax
+// softmax_grad_write adds the chunks of each long row in chunk order and
+// writes their ds. (A bucket of short rows, as the softmax
 // has, measured no faster here: the sweep has no exponentials.)
 __global__ __launch_bounds__(kItemBlock) void softmax_grad_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
@@ -407,33 +407,27 @@ __global__ __launch_bounds__(kItemBlock) void softmax_grad_items(
 
 // One thread per (long row, head): the chunk sums added in chunk order and
 // written back to every chunk slot of the row.
-__global__ __launch_bounds__(kBlock) void softmax_grad_merge(const SplitRow* __restrict__ split,
-                                                             int n_split, int H,
-                                                             double* __restrict__ pdot) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)n_split * H) return;
-  const int r = (int)(i / H), h = (int)(i - (int64_t)r * H);
-  const int s0 = split[r].slot0, nch = split[r].nchunks;
-  double dot = 0.0;
-  for (int j = 0; j < nch; ++j) dot += pdot[(int64_t)(s0 + j) * H + h];
-  for (int j = 0; j < nch; ++j) pdot[(int64_t)(s0 + j) * H + h] = dot;
-}
-
+// The chunks of long rows: each adds the sums of all chunks of its row in
+// chunk order (consecutive slots of `chunk` edges each), then writes its ds.
 __global__ __launch_bounds__(kItemBlock) void softmax_grad_write(
-    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
-    const float* __restrict__ alpha, const float* __restrict__ da, int H, int HP,
-    const double* __restrict__ pdot, float* __restrict__ ds) {
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ rowptr, int chunk,
+    const int* __restrict__ perm, const float* __restrict__ alpha, const float* __restrict__ da,
+    int H, int HP, const double* __restrict__ pdot, float* __restrict__ ds) {
   const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
   const WorkItem* itp = heavy + wid;
   const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
+  const int row = uniform(itp->row);
+  const int rb = uniform(rowptr[row]), re = uniform(rowptr[row + 1]);
+  const int s0 = pslot - (kb - rb) / chunk, nch = (re - rb + chunk - 1) / chunk;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
   const int slot = lane / HP, hh = lane % HP;
   for (int hb = 0; hb < H; hb += HP) {
     const int h = hb + hh;
     if (h >= H) continue;
-    const double dot = pdot[(int64_t)pslot * H + h];
+    double dot = 0.0;
+    for (int j = 0; j < nch; ++j) dot += pdot[(int64_t)(s0 + j) * H + h];
     for (int k = kb + slot; k < ke; k += SL) {
       const int64_t i = (int64_t)perm[k] * H + h;
       ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
@@ -687,12 +681,9 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
     TFG_LAUNCHED("softmax_grad_items");
   }
   if (g.n_split > 0) {
-    const int64_t n = (int64_t)g.n_split * H;
-    softmax_grad_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split,
-                                                                               g.n_split, H, pdot);
     softmax_grad_write<<<(unsigned)((g.n_heavy + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.perm, alpha, dalpha, H, hp, pdot, ds);
-    TFG_LAUNCHED("softmax_grad_merge / softmax_grad_write");
+        g.heavy, g.n_heavy, g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, pdot, ds);
+    TFG_LAUNCHED("softmax_grad_write");
   }
   return TFG_OK;
 }

@@ -206,8 +206,8 @@ __device__ __forceinline__ void load_steps(const int* __restrict__ perm,
 // rescaling d when m grows, so the maximum and the denominator come out of
 // one sweep; the slots are combined with xor butterflies (every lane of a
 // head ends with the same pair). A whole row then writes alpha = exp(s - m) /
-// d; a chunk stores its pair, softmax_merge combines the chunks of each long
-// row in order and softmax_write writes their outputs.
+// d; a chunk stores its pair, and softmax_write combines the pairs of each
+// long row in chunk order and writes the chunk's outputs.
 __global__ __launch_bounds__(kItemBlock) void softmax_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
     int n_long, const int* __restrict__ rowptr, const int* __restrict__ perm,
@@ -268,42 +268,32 @@ __global__ __launch_bounds__(kItemBlock) void softmax_items(
   }
 }
 
-// One thread per (long row, head): the chunks' pairs combined in chunk order;
-// the row's pair is written back to every chunk slot of the row.
-__global__ __launch_bounds__(kBlock) void softmax_merge(const SplitRow* __restrict__ split,
-                                                        int n_split, int H,
-                                                        float* __restrict__ pm,
-                                                        double* __restrict__ pd) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)n_split * H) return;
-  const int r = (int)(i / H), h = (int)(i - (int64_t)r * H);
-  const int s0 = split[r].slot0, nch = split[r].nchunks;
-  float m = -__builtin_huge_valf();
-  double d = 0.0;
-  for (int j = 0; j < nch; ++j) stat_merge(m, d, pm[(int64_t)(s0 + j) * H + h], pd[(int64_t)(s0 + j) * H + h]);
-  for (int j = 0; j < nch; ++j) {
-    pm[(int64_t)(s0 + j) * H + h] = m;
-    pd[(int64_t)(s0 + j) * H + h] = d;
-  }
-}
-
-// The outputs of the chunks of long rows, from their row's pair.
+// The outputs of the chunks of long rows. Each chunk combines the pairs of
+// all chunks of its row in chunk order (the chunks of a row are consecutive
+// slots of `chunk` edges each, the last one shorter), so every chunk of the
+// row gets the same pair, then writes its alpha.
 __global__ __launch_bounds__(kItemBlock) void softmax_write(
-    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ perm,
-    const float* __restrict__ s, int H, int HP, const float* __restrict__ pm,
-    const double* __restrict__ pd, float* __restrict__ out, float* __restrict__ out_csr) {
+    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ rowptr, int chunk,
+    const int* __restrict__ perm, const float* __restrict__ s, int H, int HP,
+    const float* __restrict__ pm, const double* __restrict__ pd, float* __restrict__ out,
+    float* __restrict__ out_csr) {
   const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy) return;
   const WorkItem* itp = heavy + wid;
   const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
+  const int row = uniform(itp->row);
+  const int rb = uniform(rowptr[row]), re = uniform(rowptr[row + 1]);
+  const int s0 = pslot - (kb - rb) / chunk, nch = (re - rb + chunk - 1) / chunk;
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
   const int slot = lane / HP, hh = lane % HP;
   for (int hb = 0; hb < H; hb += HP) {
     const int h = hb + hh;
     if (h >= H) continue;
-    const float m = pm[(int64_t)pslot * H + h];
-    const double d = pd[(int64_t)pslot * H + h];
+    float m = -__builtin_huge_valf();
+    double d = 0.0;
+    for (int j = 0; j < nch; ++j)
+      stat_merge(m, d, pm[(int64_t)(s0 + j) * H + h], pd[(int64_t)(s0 + j) * H + h]);
     for (int k0 = kb + slot; k0 < ke; k0 += kSmSteps * SL) {
       int64_t e[kSmSteps];
       float v[kSmSteps];
@@ -379,12 +369,9 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
     TFG_LAUNCHED("softmax_items");
   }
   if (g.n_split > 0) {
-    const int64_t n = (int64_t)g.n_split * H;
-    softmax_merge<<<(unsigned)((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(g.split, g.n_split, H,
-                                                                          pm, pd);
     softmax_write<<<(unsigned)((g.n_heavy + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.perm, scores, H, hp, pm, pd, out, out_csr);
-    TFG_LAUNCHED("softmax_merge / softmax_write");
+        g.heavy, g.n_heavy, g.rowptr, g.chunk, g.perm, scores, H, hp, pm, pd, out, out_csr);
+    TFG_LAUNCHED("softmax_write");
   }
   return TFG_OK;
 }
