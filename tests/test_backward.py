@@ -183,6 +183,21 @@ def test_edge_reorder_bucketed(tfg, orc, idx):
     assert same_bits(host(a), host(b))
 
 
+@pytest.mark.parametrize("n,e", [
+    (1 << 16, (1 << 20) - (1 << 16)),   # E' = 2^20: the smallest bucketed scatter
+    (50_000, (1 << 21) - 50_000),       # E' = 2^21: whole tiles and buckets
+    (50_001, (1 << 21) - 50_000),       # one edge more: a one-position tile and bucket
+])
+def test_edge_reorder_bucket_boundaries(tfg, orc, n, e):
+    ei = graphgen.random_graph(n + 3, n, e)
+    g = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n, add_self_loops=True)
+    full = with_loops(ei, n)
+    v = graphgen.features(n + 3, full.shape[1], 1)[:, 0].copy()
+    p = orc.csr_by_target(full, n)[2]
+    back = tfg.tfg_edge_reorder(dev(v[p]), src=g)
+    assert same_bits(host(back), v)
+
+
 @pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
 def test_backward_transposed_order_weights(tfg, orc, reduce):
     # weights already in the transposed graph's order give the same gradients

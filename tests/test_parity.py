@@ -129,6 +129,30 @@ def test_csr_packed_and_unpacked_payloads(tfg, orc, monkeypatch, n, n_src, e, lo
         assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
 
 
+@pytest.mark.parametrize("n,n_src,e,loops,parts", [
+    (1 << 17, 1 << 17, 300_000, False, 8),            # 17-bit targets: A keeps 15 source bits
+    ((1 << 17) + 1, (1 << 17) + 1, 300_000, False, 1),  # one more node: 18-bit ids
+    (1 << 20, 1 << 22, 1 << 22, False, 1),            # source bits 10 + 12, 22-bit positions: B full
+    (70_000, 1, 500_000, False, 4),                   # a single source (0 source bits), 4 parts
+    (1 << 16, 1 << 16, (1 << 20) - (1 << 16), True, 2),  # E' = 2^20 exactly (with the loops)
+])
+def test_csr_packed_bit_boundaries(tfg, orc, n, n_src, e, loops, parts):
+    # the packed passes at the edges of their bit budget: the result is the
+    # oracle's order whatever the split of the source bits between A and B
+    ei = graphgen.random_graph(e + 7, n, e, n_src=n_src, hub=n // 5, hub_edges=e // 10)
+    g = tfg.tfg_graph_create(dev(ei.astype(np.int32)), n, N_src=n_src, add_self_loops=loops,
+                             src_parts=parts)
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    full = ei
+    if loops:
+        full = np.concatenate([ei, np.stack([np.arange(n), np.arange(n)])], axis=1)
+    ref = expected_graph(orc, full, n, parts=g.info()["src_parts"], n_src=n_src)
+    assert np.array_equal(rowptr, ref[0]) and np.array_equal(perm, ref[2])
+    assert np.array_equal(col, ref[1])
+    if g.info()["src_parts"] > 1:
+        assert np.array_equal(host(tfg.tfg_graph_segments(g)), ref[3])
+
+
 def test_auto_parts(tfg):
     # small source table: one part; large table with long rows: several
     ei = graphgen.random_graph(3, 1000, 20_000)
