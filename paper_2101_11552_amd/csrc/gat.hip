@@ -228,8 +228,8 @@ __global__ __launch_bounds__(kItemBlock) void gat_short(
 template <int V, int SLOTS, bool DOT>
 __global__ __launch_bounds__(kItemBlock) void gat_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
-    int n_long, const int* __restrict__ rowptr, const int* __restrict__ col,
-    const int* __restrict__ perm, int H, int D, int HP, Scores S, const float* __restrict__ h,
+    int n_long, const int* __restrict__ col, const int* __restrict__ perm, int H, int D, int HP,
+    Scores S, const float* __restrict__ h,
     float* __restrict__ out, float* __restrict__ alpha_out, float* __restrict__ pacc,
     float* __restrict__ pm, double* __restrict__ pd) {
   constexpr int LPS = kWave / SLOTS;
@@ -468,7 +468,7 @@ void launch_slots(int slots, dim3 grid, hipStream_t s, const GatArgs& a) {
                                                      a.alpha_out);                               \
     if (waves > 0)                                                                               \
       gat_items<V, SL, DOT><<<grid, kItemBlock, 0, s>>>(g.heavy, g.n_heavy, g.long_rows,         \
-                                                    g.n_long, g.rowptr, g.col, g.perm, a.H,      \
+                                                    g.n_long, g.col, g.perm, a.H,                \
                                                     a.D, a.HP, a.S, a.h, a.out, a.alpha_out,     \
                                                     a.pacc, a.pm, a.pd);                         \
   } while (0)

@@ -64,6 +64,7 @@ __global__ __launch_bounds__(kWave) void gather_items(const float* __restrict__ 
                                                       const int32_t* __restrict__ items,
                                                       int64_t n_items, float* __restrict__ sink) {
   const int64_t item = blockIdx.x;
+  if (item >= n_items) return;
   const int lane = threadIdx.x, slot = lane / 32, sl = lane % 32;
   const int kb = items[2 * item], ke = items[2 * item + 1];
   f4 acc[U];

@@ -210,9 +210,9 @@ __device__ __forceinline__ void load_steps(const int* __restrict__ perm,
 // long row in chunk order and writes the chunk's outputs.
 __global__ __launch_bounds__(kItemBlock) void softmax_items(
     const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ long_rows,
-    int n_long, const int* __restrict__ rowptr, const int* __restrict__ perm,
-    const float* __restrict__ s, int H, int HP, float* __restrict__ out,
-    float* __restrict__ out_csr, float* __restrict__ pm, double* __restrict__ pd) {
+    int n_long, const int* __restrict__ perm, const float* __restrict__ s, int H, int HP,
+    float* __restrict__ out, float* __restrict__ out_csr, float* __restrict__ pm,
+    double* __restrict__ pd) {
   const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
   if (wid >= n_heavy + n_long) return;
   const int lane = threadIdx.x & (kWave - 1);
@@ -364,8 +364,7 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
   const int waves = g.n_heavy + g.n_long;
   if (waves > 0) {
     softmax_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.long_rows, g.n_long, g.rowptr, g.perm, scores, H, hp, out, out_csr,
-        pm, pd);
+        g.heavy, g.n_heavy, g.long_rows, g.n_long, g.perm, scores, H, hp, out, out_csr, pm, pd);
     TFG_LAUNCHED("softmax_items");
   }
   if (g.n_split > 0) {
