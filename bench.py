@@ -453,7 +453,7 @@ def run_suite(args):
         cpu["sm"] = _oracle(lambda: oracle.segment_softmax(s_h, ei3_np[1], n3), E3, "GE/s",
                             "the whole attention graph")
     _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1),
-         kernel="softmax_short + softmax_items + softmax_write",
+         kernel="softmax_items + softmax_split",
          cpu_baseline=cpu.get("sm"))
     alpha = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3)
     dal = torch.randn_like(alpha)
