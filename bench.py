@@ -464,7 +464,7 @@ def run_suite(args):
     ms = _timed(torch, lambda: tfg.tfg_segment_softmax_backward(alpha, dal, ei3[1], n3, graph=g3),
                 reps)
     _row("segment softmax backward", wl3, ms, E3, E3 * (4 + 12 * H) + 4 * (n3 + 1),
-         kernel="softmax_grad_items + softmax_grad_write",
+         kernel="softmax_grad_items + softmax_grad_split",
          cpu_baseline=cpu.get("smb"))
     del g3, ei3, h, s, alpha, dal
     torch.cuda.empty_cache()

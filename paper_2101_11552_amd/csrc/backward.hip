@@ -16,6 +16,7 @@
 // Every result has one writer and a fixed summation order: no atomics.
 #include <cstdlib>
 
+#include "softmax_stats.h"
 #include "spmm.h"
 
 namespace tfg {
@@ -364,73 +365,267 @@ __global__ __launch_bounds__(kBlock) void to_graph_order(const int* __restrict__
   out[i] = in[(int64_t)perm[k] * H + h];
 }
 
-// Softmax gradient over the work items of the row plan; lanes are (slot,
-// head) pairs as in softmax_items. A whole row sums alpha * dalpha per head
-// (double), then writes ds; a chunk of a long row stores its sum,
-// softmax_grad_write adds the chunks of each long row in chunk order and
-// writes their ds. (A bucket of short rows, as the softmax
-// has, measured no faster here: the sweep has no exponentials.)
+// Softmax gradient ds = alpha * (dalpha - sum over the row of alpha *
+// dalpha), per head, with the products summed in double (exact products of
+// floats), in the layouts of the softmax: short rows one lane per (row,
+// head), other light rows and chunks one wavefront each with their values in
+// registers (NST slot steps, the next power of two of the item's), split rows
+// of at most kGradSplitWaves chunks one block each with the chunk sums added
+// in chunk order in LDS. Chunks of longer split rows store their sums
+// (pdot), which softmax_grad_split adds in chunk order before writing.
+constexpr int kGradCap = 8;          // slot steps held in registers
+constexpr int kGradSplitWaves = 16;  // chunks per split row done by one block
+
+__device__ __forceinline__ void grad_short_row(const WorkItem& it, const int* __restrict__ perm,
+                                               const float* __restrict__ alpha,
+                                               const float* __restrict__ da, int H, int hh,
+                                               int HP, float* __restrict__ ds) {
+  const int kb = it.kbeg, n = it.kend - it.kbeg;  // 0 <= n <= kShortRow
+  int nw = 0;  // the wavefront's longest row
+#pragma unroll
+  for (int j = 1; j <= kShortRow; ++j) nw = __any(n >= j) ? j : nw;
+  int e[kShortRow];
+#pragma unroll
+  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? perm[kb + j] : 0;
+  for (int h = hh; h < H; h += HP) {
+    float a[kShortRow], g[kShortRow];
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j) {
+      a[j] = j < n ? alpha[(int64_t)e[j] * H + h] : 0.0f;
+      g[j] = j < n ? da[(int64_t)e[j] * H + h] : 0.0f;
+    }
+    double dot = 0.0;
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j)
+      if (j < nw) dot += (double)a[j] * (double)g[j];
+#pragma unroll
+    for (int j = 0; j < kShortRow; ++j)
+      if (j < n) ds[(int64_t)e[j] * H + h] = (float)((double)a[j] * ((double)g[j] - dot));
+  }
+}
+
+// alpha and dalpha of head h for the registers' ids (0 where there is none)
+template <int NST>
+__device__ __forceinline__ void grad_load(const float* __restrict__ alpha,
+                                          const float* __restrict__ da, int H, int h, bool act,
+                                          const int (&e)[NST], float (&a)[NST],
+                                          float (&g)[NST]) {
+#pragma unroll
+  for (int u = 0; u < NST; ++u) {
+    const bool ok = act && e[u] >= 0;
+    a[u] = ok ? alpha[(int64_t)e[u] * H + h] : 0.0f;
+    g[u] = ok ? da[(int64_t)e[u] * H + h] : 0.0f;
+  }
+}
+
+template <int NST>
+__device__ __forceinline__ double grad_dot(const float (&a)[NST], const float (&g)[NST], int HP) {
+  double dot = 0.0;
+#pragma unroll
+  for (int u = 0; u < NST; ++u) dot += (double)a[u] * (double)g[u];
+  return slots_sum(dot, HP);
+}
+
+template <int NST>
+__device__ __forceinline__ void grad_write(const float (&a)[NST], const float (&g)[NST],
+                                           const int (&e)[NST], double dot, int H, int h,
+                                           bool act, float* __restrict__ ds) {
+#pragma unroll
+  for (int u = 0; u < NST; ++u)
+    if (act && e[u] >= 0) ds[(int64_t)e[u] * H + h] = (float)((double)a[u] * ((double)g[u] - dot));
+}
+
+// A whole item's sum over [kb, ke) for head h, loading the values (the items
+// longer than kGradCap slot steps), and its ds from a second sweep.
+__device__ __forceinline__ double grad_sweep_dot(const int* __restrict__ perm,
+                                                 const float* __restrict__ alpha,
+                                                 const float* __restrict__ da, int H, int h,
+                                                 bool act, int kb, int ke, int slot, int SL,
+                                                 int HP) {
+  double dot = 0.0;
+  for (int k = kb + slot; k < ke; k += SL)
+    if (act) {
+      const int64_t i = (int64_t)perm[k] * H + h;
+      dot += (double)alpha[i] * (double)da[i];
+    }
+  return slots_sum(dot, HP);
+}
+
+__device__ __forceinline__ void grad_sweep_write(const int* __restrict__ perm,
+                                                 const float* __restrict__ alpha,
+                                                 const float* __restrict__ da, int H, int h,
+                                                 bool act, int kb, int ke, int slot, int SL,
+                                                 double dot, float* __restrict__ ds) {
+  for (int k = kb + slot; k < ke; k += SL)
+    if (act) {
+      const int64_t i = (int64_t)perm[k] * H + h;
+      ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
+    }
+}
+
+template <int NST>
+__device__ __forceinline__ void grad_item_regs(const int* __restrict__ perm,
+                                               const float* __restrict__ alpha,
+                                               const float* __restrict__ da, int H, int HP,
+                                               int kb, int ke, int slot, int hh, int pslot,
+                                               float* __restrict__ ds,
+                                               double* __restrict__ pdot) {
+  const int SL = kWave / HP;
+  int e[NST];
+  load_ids<NST>(perm, kb, ke, slot, SL, e);
+  for (int hb = 0; hb < H; hb += HP) {
+    const int h = hb + hh;
+    const bool act = h < H;
+    float a[NST], g[NST];
+    grad_load<NST>(alpha, da, H, h, act, e, a, g);
+    const double dot = grad_dot<NST>(a, g, HP);
+    if (pslot >= 0) {
+      if (slot == 0 && act) pdot[(int64_t)pslot * H + h] = dot;
+      continue;
+    }
+    grad_write<NST>(a, g, e, dot, H, h, act, ds);
+  }
+}
+
+// Wavefronts [0, short_waves) take 64 / HP short rows each; the next n_long
+// one light row of more than kShortRow edges each; the rest one chunk of a
+// split row of more than kGradSplitWaves chunks (the others are left to
+// softmax_grad_split).
 __global__ __launch_bounds__(kItemBlock) void softmax_grad_items(
-    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
-    int n_light, const int* __restrict__ perm, const float* __restrict__ alpha,
-    const float* __restrict__ da, int H, int HP, float* __restrict__ ds,
-    double* __restrict__ pdot) {
-  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
-  if (wid >= n_heavy + n_light) return;
-  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
-  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
-  if (kb == ke) return;
+    const WorkItem* __restrict__ short_rows, int n_short, int short_waves,
+    const WorkItem* __restrict__ long_rows, int n_long, const WorkItem* __restrict__ heavy,
+    int n_heavy, const int* __restrict__ rowptr, int chunk, const int* __restrict__ perm,
+    const float* __restrict__ alpha, const float* __restrict__ da, int H, int HP,
+    float* __restrict__ ds, double* __restrict__ pdot) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
+  if (wid < short_waves) {
+    const int i = wid * (kWave / HP) + lane / HP;
+    if (i < n_short) grad_short_row(short_rows[i], perm, alpha, da, H, lane % HP, HP, ds);
+    return;
+  }
+  wid -= short_waves;
+  if (wid >= n_long + n_heavy) return;
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  int kb, ke, pslot = -1;
+  if (wid < n_long) {
+    kb = uniform(long_rows[wid].kbeg);
+    ke = uniform(long_rows[wid].kend);
+  } else {
+    const WorkItem* it = heavy + (wid - n_long);
+    const int row = uniform(it->row);
+    const int deg = uniform(rowptr[row + 1]) - uniform(rowptr[row]);
+    if ((deg + chunk - 1) / chunk <= kGradSplitWaves) return;
+    kb = uniform(it->kbeg);
+    ke = uniform(it->kend);
+    pslot = uniform(it->slot);
+  }
+  const int nst = (ke - kb + SL - 1) / SL;
+  if (nst <= 1) {
+    grad_item_regs<1>(perm, alpha, da, H, HP, kb, ke, slot, hh, pslot, ds, pdot);
+  } else if (nst <= 2) {
+    grad_item_regs<2>(perm, alpha, da, H, HP, kb, ke, slot, hh, pslot, ds, pdot);
+  } else if (nst <= 4) {
+    grad_item_regs<4>(perm, alpha, da, H, HP, kb, ke, slot, hh, pslot, ds, pdot);
+  } else if (nst <= kGradCap) {
+    grad_item_regs<kGradCap>(perm, alpha, da, H, HP, kb, ke, slot, hh, pslot, ds, pdot);
+  } else {
+    for (int hb = 0; hb < H; hb += HP) {
+      const int h = hb + hh;
+      const bool act = h < H;
+      const double dot = grad_sweep_dot(perm, alpha, da, H, h, act, kb, ke, slot, SL, HP);
+      if (pslot >= 0) {
+        if (slot == 0 && act) pdot[(int64_t)pslot * H + h] = dot;
+        continue;
+      }
+      grad_sweep_write(perm, alpha, da, H, h, act, kb, ke, slot, SL, dot, ds);
+    }
+  }
+}
+
+// Chunk w of a split row of at most kGradSplitWaves chunks (NST = 0: the
+// values are loaded again to write); every wavefront runs the same head
+// passes and barriers, with or without a chunk.
+template <int NST>
+__device__ __forceinline__ void grad_split_chunk(const int* __restrict__ perm,
+                                                 const float* __restrict__ alpha,
+                                                 const float* __restrict__ da, int H, int HP,
+                                                 int kb, int ke, int nch, int w, int lane,
+                                                 double (&lsum)[kGradSplitWaves][kWave],
+                                                 float* __restrict__ ds) {
+  const int SL = kWave / HP;
+  const int slot = lane / HP, hh = lane % HP;
+  const bool has = kb < ke;
+  constexpr int R = NST > 0 ? NST : 1;
+  int e[R];
+  if constexpr (NST > 0) load_ids<NST>(perm, kb, ke, slot, SL, e);
+  for (int hb = 0; hb < H; hb += HP) {
+    const int h = hb + hh;
+    const bool act = h < H;
+    float a[R], g[R];
+    double dot = 0.0;
+    if (has) {
+      if constexpr (NST > 0) {
+        grad_load<NST>(alpha, da, H, h, act, e, a, g);
+        dot = grad_dot<NST>(a, g, HP);
+      } else {
+        dot = grad_sweep_dot(perm, alpha, da, H, h, act, kb, ke, slot, SL, HP);
+      }
+    }
+    lsum[w][lane] = dot;
+    __syncthreads();
+    double tot = 0.0;
+    for (int c = 0; c < nch; ++c) tot += lsum[c][lane];
+    __syncthreads();  // the sums are read before the next head pass writes
+    if (!has) continue;
+    if constexpr (NST > 0)
+      grad_write<NST>(a, g, e, tot, H, h, act, ds);
+    else
+      grad_sweep_write(perm, alpha, da, H, h, act, kb, ke, slot, SL, tot, ds);
+  }
+}
+
+// One block per split row (kGradSplitWaves wavefronts): grad_split_chunk for
+// a row of at most kGradSplitWaves chunks; for a longer one the chunk sums
+// from softmax_grad_items, added in chunk order, and wavefront w writes
+// chunks w, w + kGradSplitWaves, ...
+__global__ __launch_bounds__(kGradSplitWaves * kWave) void softmax_grad_split(
+    const SplitRow* __restrict__ split, const int* __restrict__ rowptr, int chunk,
+    const int* __restrict__ perm, const float* __restrict__ alpha, const float* __restrict__ da,
+    int H, int HP, const double* __restrict__ pdot, float* __restrict__ ds) {
+  __shared__ double lsum[kGradSplitWaves][kWave];
+  const SplitRow* sr = split + blockIdx.x;
+  const int row = uniform(sr->row), nch = uniform(sr->nchunks), s0 = uniform(sr->slot0);
+  const int rb = uniform(rowptr[row]), re = uniform(rowptr[row + 1]);
+  const int w = uniform((int)threadIdx.x / kWave);
   const int lane = threadIdx.x & (kWave - 1);
   const int SL = kWave / HP;
+  if (nch <= kGradSplitWaves) {
+    const int kb = rb + w * chunk, ke = min(re, kb + chunk);  // kb >= ke: no chunk
+    const int cst = (chunk + SL - 1) / SL;  // slot steps of a whole chunk
+    if (cst <= 2)
+      grad_split_chunk<2>(perm, alpha, da, H, HP, kb, ke, nch, w, lane, lsum, ds);
+    else if (cst <= 4)
+      grad_split_chunk<4>(perm, alpha, da, H, HP, kb, ke, nch, w, lane, lsum, ds);
+    else if (cst <= kGradCap)
+      grad_split_chunk<kGradCap>(perm, alpha, da, H, HP, kb, ke, nch, w, lane, lsum, ds);
+    else if (cst <= 2 * kGradCap)
+      grad_split_chunk<2 * kGradCap>(perm, alpha, da, H, HP, kb, ke, nch, w, lane, lsum, ds);
+    else
+      grad_split_chunk<0>(perm, alpha, da, H, HP, kb, ke, nch, w, lane, lsum, ds);
+    return;
+  }
   const int slot = lane / HP, hh = lane % HP;
   for (int hb = 0; hb < H; hb += HP) {
     const int h = hb + hh;
     const bool act = h < H;
     double dot = 0.0;
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) {
-        const int64_t i = (int64_t)perm[k] * H + h;
-        dot += (double)alpha[i] * (double)da[i];
-      }
-    for (int off = HP; off < kWave; off <<= 1) dot += __shfl_xor(dot, off);
-    if (pslot >= 0) {
-      if (slot == 0 && act) pdot[(int64_t)pslot * H + h] = dot;
-      continue;
-    }
-    for (int k = kb + slot; k < ke; k += SL)
-      if (act) {
-        const int64_t i = (int64_t)perm[k] * H + h;
-        ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
-      }
-  }
-}
-
-// One thread per (long row, head): the chunk sums added in chunk order and
-// written back to every chunk slot of the row.
-// The chunks of long rows: each adds the sums of all chunks of its row in
-// chunk order (consecutive slots of `chunk` edges each), then writes its ds.
-__global__ __launch_bounds__(kItemBlock) void softmax_grad_write(
-    const WorkItem* __restrict__ heavy, int n_heavy, const int* __restrict__ rowptr, int chunk,
-    const int* __restrict__ perm, const float* __restrict__ alpha, const float* __restrict__ da,
-    int H, int HP, const double* __restrict__ pdot, float* __restrict__ ds) {
-  const int wid = uniform(blockIdx.x * (kItemBlock / kWave) + threadIdx.x / kWave);
-  if (wid >= n_heavy) return;
-  const WorkItem* itp = heavy + wid;
-  const int kb = uniform(itp->kbeg), ke = uniform(itp->kend), pslot = uniform(itp->slot);
-  const int row = uniform(itp->row);
-  const int rb = uniform(rowptr[row]), re = uniform(rowptr[row + 1]);
-  const int s0 = pslot - (kb - rb) / chunk, nch = (re - rb + chunk - 1) / chunk;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int SL = kWave / HP;
-  const int slot = lane / HP, hh = lane % HP;
-  for (int hb = 0; hb < H; hb += HP) {
-    const int h = hb + hh;
-    if (h >= H) continue;
-    double dot = 0.0;
-    for (int j = 0; j < nch; ++j) dot += pdot[(int64_t)(s0 + j) * H + h];
-    for (int k = kb + slot; k < ke; k += SL) {
-      const int64_t i = (int64_t)perm[k] * H + h;
-      ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
+    if (act)
+      for (int c = 0; c < nch; ++c) dot += pdot[(int64_t)(s0 + c) * H + h];
+    for (int c = w; c < nch; c += kGradSplitWaves) {
+      const int kb = rb + c * chunk, ke = min(re, kb + chunk);
+      grad_sweep_write(perm, alpha, da, H, h, act, kb, ke, slot, SL, dot, ds);
     }
   }
 }
@@ -674,16 +869,19 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
   double* pdot = reinterpret_cast<double*>(
       static_cast<char*>(ws) +
       align_up(sizeof(float) * (size_t)std::max<int64_t>((int64_t)g.n_heavy * H, 1), 256));
-  const int waves = g.n_heavy + g.n_light;
+  const int64_t short_waves = (g.n_short + kWave / hp - 1) / (kWave / hp);
+  const int64_t waves = short_waves + g.n_long + g.n_heavy;
+  if (waves > INT32_MAX) return fail(TFG_ERR_TOO_LARGE, "softmax gradient: too many work items");
   if (waves > 0) {
     softmax_grad_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.light, g.n_light, g.perm, alpha, dalpha, H, hp, ds, pdot);
+        g.short_rows, g.n_short, (int)short_waves, g.long_rows, g.n_long, g.heavy, g.n_heavy,
+        g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, ds, pdot);
     TFG_LAUNCHED("softmax_grad_items");
   }
   if (g.n_split > 0) {
-    softmax_grad_write<<<(unsigned)((g.n_heavy + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
-        g.heavy, g.n_heavy, g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, pdot, ds);
-    TFG_LAUNCHED("softmax_grad_write");
+    softmax_grad_split<<<(unsigned)g.n_split, kGradSplitWaves * kWave, 0, s>>>(
+        g.split, g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, pdot, ds);
+    TFG_LAUNCHED("softmax_grad_split");
   }
   return TFG_OK;
 }

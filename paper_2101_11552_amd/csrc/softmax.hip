@@ -194,16 +194,6 @@ __device__ __forceinline__ void softmax_short_row(const WorkItem& it,
 constexpr int kSmCap = 8;    // slot steps held in registers
 constexpr int kSmSteps = 4;  // slot steps per round of loads (the running sweep)
 
-template <int NST>
-__device__ __forceinline__ void load_ids(const int* __restrict__ perm, int kb, int ke, int slot,
-                                         int SL, int (&e)[NST]) {
-#pragma unroll
-  for (int u = 0; u < NST; ++u) {
-    const int k = kb + slot + u * SL;
-    e[u] = k < ke ? perm[k] : -1;
-  }
-}
-
 // Scores of head h for the ids (-inf where there is no edge or no head).
 template <int NST>
 __device__ __forceinline__ void load_scores(const float* __restrict__ s, int H, int h, bool act,
@@ -219,12 +209,6 @@ __device__ __forceinline__ float slots_max(float m, int HP) {
     m = o > m ? o : m;
   }
   return m;
-}
-
-// (IEEE addition commutes, so every lane of a head ends with the same sum)
-__device__ __forceinline__ double slots_sum(double d, int HP) {
-  for (int off = HP; off < kWave; off <<= 1) d += __shfl_xor(d, off);
-  return d;
 }
 
 __device__ __forceinline__ void slots_merge(float& m, double& d, int HP) {

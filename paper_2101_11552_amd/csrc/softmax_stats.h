@@ -36,4 +36,25 @@ __device__ __forceinline__ void stat_add(float& m, double& d, float v) {
   m = up ? v : m;
 }
 
+// Register sweeps of the row plan's items (softmax and its gradient): lanes
+// are (slot, head) pairs, SL = 64 / HP slots; slot step u of an item
+// starting at kb is position kb + slot + u * SL.
+// Edge ids of NST steps of [kb, ke) (-1 past ke).
+template <int NST>
+__device__ __forceinline__ void load_ids(const int* __restrict__ perm, int kb, int ke, int slot,
+                                         int SL, int (&e)[NST]) {
+#pragma unroll
+  for (int u = 0; u < NST; ++u) {
+    const int k = kb + slot + u * SL;
+    e[u] = k < ke ? perm[k] : -1;
+  }
+}
+
+// Sum over the slots of a head (lanes l, l ^ HP, l ^ 2 HP, ...). IEEE
+// addition commutes, so every lane of a head ends with the same sum.
+__device__ __forceinline__ double slots_sum(double d, int HP) {
+  for (int off = HP; off < kWave; off <<= 1) d += __shfl_xor(d, off);
+  return d;
+}
+
 }  // namespace tfg
