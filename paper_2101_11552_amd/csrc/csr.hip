@@ -44,6 +44,12 @@ __device__ __forceinline__ int tile_of(int bid, int ntiles) {
   return x * q + min(x, r) + i;
 }
 
+// Number of lanes below this one whose bit is set in mask.
+__device__ __forceinline__ int lanes_below(unsigned long long mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
+}
+
 // Edge e of the list with appended loops, as (source, sort key). Ids < E_in
 // come from edge_index (an out-of-range id is replaced by 0 and flagged), ids
 // >= E_in are the loops (i, i), i = e - E_in. key = target * P + source part.
@@ -70,38 +76,32 @@ __device__ __forceinline__ int input_edges_before(int64_t E_in, int64_t base) {
   return (int)(E_in - base);  // |E_in - base| < 2^31: both below 2^31
 }
 
-// The raw ids of N tile positions pos[i], every load issued before any is
-// used (the branches are uniform: they depend on the tile only).
+// The raw ids of the N tile positions p0 + i * step, every load issued
+// before any is used (the conditions are uniform: they depend on the tile
+// only; values of positions past the tile are never used).
 template <int N, typename IdxT>
 __device__ __forceinline__ void load_raw_all(const IdxT* __restrict__ sb,
-                                             const IdxT* __restrict__ tb, const int (&pos)[N],
-                                             int d, IdxT (&s)[N], IdxT (&t)[N]) {
-  if (d <= 0) {  // loops only
+                                             const IdxT* __restrict__ tb, int p0, int step,
+                                             int tile_n, int d, IdxT (&s)[N], IdxT (&t)[N]) {
+  // byte offsets from the tile's base addresses, 32-bit (positions < 2^13),
+  // shared by the source and target loads; positions past the input edges
+  // (loops) read the last input edge, and a tile of loops only reads nothing
+  const bool any = d > 0, has_src = sb != nullptr;
+  const int last = min(tile_n, d) - 1;
+  const char* sc = reinterpret_cast<const char*>(sb);
+  const char* tc = reinterpret_cast<const char*>(tb);
 #pragma unroll
-    for (int i = 0; i < N; ++i) s[i] = t[i] = IdxT(0);
-    return;
-  }
-  int q[N];
-#pragma unroll
-  for (int i = 0; i < N; ++i) q[i] = pos[i] < d ? pos[i] : d - 1;
-  if (sb != nullptr) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      s[i] = __builtin_nontemporal_load(sb + q[i]);
-      t[i] = __builtin_nontemporal_load(tb + q[i]);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      s[i] = IdxT(0);
-      t[i] = __builtin_nontemporal_load(tb + q[i]);
-    }
+  for (int i = 0; i < N; ++i) {
+    const unsigned q = (unsigned)min(p0 + i * step, last) * (unsigned)sizeof(IdxT);
+    s[i] = (any && has_src) ? __builtin_nontemporal_load(reinterpret_cast<const IdxT*>(sc + q))
+                            : IdxT(0);
+    t[i] = any ? __builtin_nontemporal_load(reinterpret_cast<const IdxT*>(tc + q)) : IdxT(0);
   }
 }
 
 template <typename IdxT>
-__device__ __forceinline__ void decode_edge(const KeyMap& m, int p, int d, IdxT s, IdxT t,
-                                            bool has_src, int* sv, int* key, bool* bad) {
+__device__ __forceinline__ void decode_ids(const KeyMap& m, int p, int d, IdxT s, IdxT t,
+                                           bool has_src, int* sv, int* tv, bool* bad) {
   const bool in = p < d;
   bool sbad, tbad;
   if constexpr (sizeof(IdxT) == 4) {  // counts are below 2^31: one unsigned compare
@@ -113,8 +113,15 @@ __device__ __forceinline__ void decode_edge(const KeyMap& m, int p, int d, IdxT 
   }
   const int loop = p - d;
   *sv = in ? (sbad ? 0 : (int)s) : loop;
-  const int tv = in ? (tbad ? 0 : (int)t) : loop;
+  *tv = in ? (tbad ? 0 : (int)t) : loop;
   *bad = in && (sbad || tbad);
+}
+
+template <typename IdxT>
+__device__ __forceinline__ void decode_edge(const KeyMap& m, int p, int d, IdxT s, IdxT t,
+                                            bool has_src, int* sv, int* key, bool* bad) {
+  int tv;
+  decode_ids(m, p, d, s, t, has_src, sv, &tv, bad);
   *key = m.parts == 1 ? tv : tv * m.parts + source_part(*sv, m);
 }
 
@@ -293,11 +300,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
 
   const int radix = 1 << dbits;
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = uniform((int)threadIdx.x / kWave);
   const int tile = tile_of((int)blockIdx.x, ntiles);
   const int64_t base = (int64_t)tile * kSortTile;
   const int tile_n = (int)min<int64_t>(kSortTile, E - base);
-  const unsigned long long lt = (1ull << lane) - 1ull;
 
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
   __syncthreads();
@@ -309,26 +315,23 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   const int d = input_edges_before(m.E_in, base);
   const IdxT* sb = src ? src + base : nullptr;
   const IdxT* tb = tgt + base;
-  int c[kSortItems];  // positions in the tile (clamped to its last)
-#pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int p = wave * (kWave * kSortItems) + i * kWave + lane;
-    c[i] = p < tile_n ? p : tile_n - 1;
-  }
+  const int p0 = wave * (kWave * kSortItems) + lane;  // position of item i: p0 + i * 64
   if constexpr (FIRST) {
+    // (items past the tile decode garbage that is never used)
     IdxT rs[kSortItems], rt[kSortItems];
-    load_raw_all(sb, tb, c, d, rs, rt);
+    load_raw_all(sb, tb, p0, kWave, tile_n, d, rs, rt);
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
       bool bad;
-      decode_edge(m, c[i], d, rs[i], rt[i], sb != nullptr, &ps[i], &key[i], &bad);
+      decode_edge(m, p0 + i * kWave, d, rs[i], rt[i], sb != nullptr, &ps[i], &key[i], &bad);
     }
   } else {
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
-      key[i] = kin[base + c[i]];
-      pe[i] = ein[base + c[i]];
-      ps[i] = sin[base + c[i]];
+      const int c = min(p0 + i * kWave, tile_n - 1);  // clamped to the tile's last
+      key[i] = kin[base + c];
+      pe[i] = ein[base + c];
+      ps[i] = sin[base + c];
     }
   }
 #pragma unroll
@@ -342,7 +345,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
       const unsigned long long bb = __ballot(bit);
       peers &= bit ? bb : ~bb;
     }
-    const int below = __popcll(peers & lt);
+    const int below = lanes_below(peers);
     const int run = valid ? (int)wcnt[wave][d] : 0;
     lpos[i] = run + below;  // rank within the wave for now
     if (valid && below == 0) wcnt[wave][d] = (unsigned short)(run + __popcll(peers));
@@ -471,63 +474,63 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
 
   const int radix = 1 << dbits;
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = uniform((int)threadIdx.x / kWave);
   const int tile = tile_of((int)blockIdx.x, ntiles);
   const int64_t base = (int64_t)tile * kSortTile;
   const int tile_n = (int)min<int64_t>(kSortTile, E - base);
-  const unsigned long long lt = (1ull << lane) - 1ull;
 
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
   __syncthreads();
 
+  // pk: the digit in the upper half, below it first the rank within the
+  // wave, then the position in the tile (0xFFFF: past the end of the tile)
   unsigned va[kSortItems], vb[kSortItems];
-  int dig[kSortItems], lpos[kSortItems];
+  int pk[kSortItems];
   {
     const int d = input_edges_before(m.E_in, base);
     const IdxT* sb = src ? src + base : nullptr;
     const IdxT* tb = tgt + base;
-    int c[kSortItems];  // positions in the tile (clamped to its last)
-#pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
-      const int p = wave * (kWave * kSortItems) + i * kWave + lane;
-      c[i] = p < tile_n ? p : tile_n - 1;
-    }
+    const int p0 = wave * (kWave * kSortItems) + lane;  // position of item i: p0 + i * 64
     if constexpr (MODE == 0) {
+      // (items past the tile decode garbage that is never used)
       IdxT rs[kSortItems], rt[kSortItems];
-      load_raw_all(sb, tb, c, d, rs, rt);
+      load_raw_all(sb, tb, p0, kWave, tile_n, d, rs, rt);
 #pragma unroll
       for (int i = 0; i < kSortItems; ++i) {
-        int sv, key;
+        const int p = p0 + i * kWave;
+        int sv, tv;
         bool bad;
-        decode_edge(m, c[i], d, rs[i], rt[i], sb != nullptr, &sv, &key, &bad);
-        va[i] = pack_a(key >> q.lp, sv, q);
-        vb[i] = pack_b(sv, (int)(base + c[i]), q);
-        dig[i] = key & (radix - 1);
+        decode_ids(m, p, d, rs[i], rt[i], sb != nullptr, &sv, &tv, &bad);
+        const int part = q.lp == 0 ? 0 : source_part(sv, m);  // P = 2^lp
+        va[i] = pack_a(tv, sv, q);
+        vb[i] = pack_b(sv, (int)base + p, q);
+        pk[i] = ((tv << q.lp) | part) & (radix - 1);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < kSortItems; ++i) {
-        va[i] = ain[base + c[i]];
-        vb[i] = bin[base + c[i]];
+        const int c = min(p0 + i * kWave, tile_n - 1);  // clamped to the tile's last
+        va[i] = ain[base + c];
+        vb[i] = bin[base + c];
       }
 #pragma unroll
-      for (int i = 0; i < kSortItems; ++i) dig[i] = (int)(va[i] >> shift) & (radix - 1);
+      for (int i = 0; i < kSortItems; ++i) pk[i] = (int)(va[i] >> shift) & (radix - 1);
     }
   }
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;
     const bool valid = p < tile_n;
-    const int d = dig[i];
+    const int d = pk[i];
     unsigned long long peers = __ballot(valid);
     for (int b = 0; b < dbits; ++b) {
       const int bit = (d >> b) & 1;
       const unsigned long long bb = __ballot(bit);
       peers &= bit ? bb : ~bb;
     }
-    const int below = __popcll(peers & lt);
+    const int below = lanes_below(peers);
     const int run = valid ? (int)wcnt[wave][d] : 0;
-    lpos[i] = run + below;
+    pk[i] = (d << 16) | (run + below);
     if (valid && below == 0) wcnt[wave][d] = (unsigned short)(run + __popcll(peers));
   }
   __syncthreads();
@@ -552,21 +555,26 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int p = wave * (kWave * kSortItems) + i * kWave + lane;
-    lpos[i] = p < tile_n ? lpos[i] + loff[dig[i]] + (int)wcnt[wave][dig[i]] : -1;
+    const int d = pk[i] >> 16;
+    const int pos = p < tile_n ? (pk[i] & 0xFFFF) + loff[d] + (int)wcnt[wave][d] : 0xFFFF;
+    pk[i] = (d << 16) | pos;
   }
   // The first pass's digit is not a field of A: once every position is known
   // (the barrier), the per-wave counters' LDS (exactly one byte per tile
   // position) holds the digit of every staged position instead.
   unsigned char* sdig = reinterpret_cast<unsigned char*>(&wcnt[0][0]);
   static_assert(sizeof(wcnt) >= kSortTile, "one byte per tile position");
+  static_assert(kSortTile < 0xFFFF, "tile positions fit below the 16-bit marker");
   if constexpr (MODE == 0) __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i)
-    if (lpos[i] >= 0) {
-      stage[0][lpos[i]] = va[i];
-      stage[1][lpos[i]] = vb[i];
-      if constexpr (MODE == 0) sdig[lpos[i]] = (unsigned char)dig[i];
+  for (int i = 0; i < kSortItems; ++i) {
+    const int pos = pk[i] & 0xFFFF;
+    if (pos != 0xFFFF) {
+      stage[0][pos] = va[i];
+      stage[1][pos] = vb[i];
+      if constexpr (MODE == 0) sdig[pos] = (unsigned char)(pk[i] >> 16);
     }
+  }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
