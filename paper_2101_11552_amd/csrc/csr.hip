@@ -599,34 +599,45 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
 
 // bounds[v] = first position whose sorted key is >= v (v = 0..K). Position k
 // starts the keys (key[k-1], key[k]]; k = E closes the keys after the last one.
-// Four positions per thread, read with one 16-byte load; the key before them
-// comes from the neighbouring lane.
+// Each thread takes kKbGroups groups of four positions (a group per 16-byte
+// load, consecutive threads on consecutive groups, all loads issued
+// together); the key before a group comes from the neighbouring lane.
 constexpr int kKbThreads = 256;  // threads per block of key_bounds
+constexpr int kKbGroups = 4;     // groups of four positions per thread
 __global__ __launch_bounds__(kKbThreads) void key_bounds(const int* __restrict__ keys, int64_t E,
                                                      int64_t K, int* __restrict__ bounds) {
-  const int64_t k0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  int c[4];
-  if (k0 + 4 <= E) {
-    typedef int i4 __attribute__((ext_vector_type(4)));
-    const i4 v = __builtin_nontemporal_load(reinterpret_cast<const i4*>(keys + k0));
-    c[0] = v.x;
-    c[1] = v.y;
-    c[2] = v.z;
-    c[3] = v.w;
-  } else {
+  typedef int i4 __attribute__((ext_vector_type(4)));
+  const int lane = lane_id();
+  int c[kKbGroups][4], before[kKbGroups];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c[j] = k0 + j < E ? keys[k0 + j] : (int)K;
+  for (int j = 0; j < kKbGroups; ++j) {
+    const int64_t k0 = (((int64_t)blockIdx.x * kKbGroups + j) * kKbThreads + threadIdx.x) * 4;
+    if (k0 + 4 <= E) {
+      const i4 v = __builtin_nontemporal_load(reinterpret_cast<const i4*>(keys + k0));
+      c[j][0] = v.x;
+      c[j][1] = v.y;
+      c[j][2] = v.z;
+      c[j][3] = v.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) c[j][i] = k0 + i < E ? keys[k0 + i] : (int)K;
+    }
+    before[j] = (lane == 0 && k0 > 0 && k0 <= E) ? keys[k0 - 1] : -1;
   }
-  // lane l - 1 holds keys[k0 - 1] whenever this lane has positions to close
-  int prev = __shfl_up(c[3], 1);
-  if (lane_id() == 0) prev = (k0 > 0 && k0 <= E) ? keys[k0 - 1] : -1;
-  if (k0 > E) return;
-  int64_t cur = prev;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (k0 + j > E) break;
-    for (int64_t v = cur + 1; v <= c[j]; ++v) bounds[v] = (int)(k0 + j);
-    cur = c[j];
+  for (int j = 0; j < kKbGroups; ++j) {
+    const int64_t k0 = (((int64_t)blockIdx.x * kKbGroups + j) * kKbThreads + threadIdx.x) * 4;
+    // lane l - 1 holds keys[k0 - 1] whenever this lane has positions to close
+    int prev = __shfl_up(c[j][3], 1);
+    if (lane == 0) prev = before[j];
+    if (k0 > E) continue;
+    int64_t cur = prev;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (k0 + i > E) break;
+      for (int64_t v = cur + 1; v <= c[j][i]; ++v) bounds[v] = (int)(k0 + i);
+      cur = c[j][i];
+    }
   }
 }
 
@@ -936,7 +947,8 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
   }
   // segment starts from the boundaries of the sorted keys
   const int64_t K = g.N * g.parts;
-  key_bounds<<<dim3((unsigned)((E / 4 + 1 + kKbThreads - 1) / kKbThreads)), dim3(kKbThreads), 0, s>>>(
+  const int64_t kb_per_block = (int64_t)kKbThreads * kKbGroups;  // groups of four positions
+  key_bounds<<<dim3((unsigned)((E / 4 + 1 + kb_per_block - 1) / kb_per_block)), dim3(kKbThreads), 0, s>>>(
       keys, E, K, g.segptr);
   TFG_LAUNCHED("key_bounds");
   if (g.parts > 1) {
