@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "aggregated edges/sec (GE/s) and achieved HBM GB/s for fp32 GCN sum-aggregation"
 AGG_SRC = [os.path.join(ROOT, "paper_2101_11552_amd", "csrc", f) for f in ("spmm.h", "aggregate.hip")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_rows_powerlaw.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_aggregate_powerlaw.txt")
 
 
 def algorithmic_bytes(E_total: int, N: int, F: int) -> int:
@@ -369,7 +369,7 @@ def run_suite(args):
     _row("backward dx (transposed sum aggregation)", wl, ms, Ep,
          Ep * (8 + 4 * F) + N * 4 * F + 4 * (N + 1),
          compulsory=compulsory_bytes(Ep, N, N, F, items(info_t)), gathered=Ep * 4 * F,
-         ceiling=ceiling, kernel="spmm_rows over the transposed graph",
+         ceiling=ceiling, kernel="spmm_wide over the transposed graph",
          src_parts=gt.info()["src_parts"], weights="transposed graph order",
          ms_with_edge_order_weights=round(ms_coo, 4), cpu_baseline=cpu.get("bw"))
     ms = _timed(torch, lambda: tfg.tfg_aggregate_backward(
@@ -772,12 +772,12 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
-                     "traffic_source": ("stored: profiles/traffic_spmm_rows_powerlaw.txt, rocprofv3 "
+                     "traffic_source": ("stored: profiles/traffic_aggregate_powerlaw.txt, rocprofv3 "
                                         "FETCH_SIZE + WRITE_SIZE per launch, taken on the "
                                         "current kernel source" if traffic else None),
                      "traffic_GBps": (round(traffic / (agg_ms * 1e-3) / 1e9, 1)
                                       if traffic else None),
-                     "kernel": "tfg_aggregate (spmm_rows + fixup_rows)",
+                     "kernel": "tfg_aggregate (spmm_wide + fixup_rows)",
                      "compulsory_bytes_per_launch": C,
                      "partial_row_bytes_per_launch": partial_bytes,
                      "frac_with_partials": round((C + partial_bytes) / (agg_ms * 1e-3) / 1e9

@@ -94,6 +94,170 @@ __global__ __launch_bounds__(kItemBlock) void fixup_rows(const SplitRow* __restr
   }
 }
 
+// Sum and mean with scalar edge ids: one wavefront per work item, SL edge
+// slots of 64 / SL lanes (SL = 1 or 2), lane l of a slot holding columns
+// V l .. V l + V - 1 of a 64 V / SL-column pass. The item's edge ids and
+// weights come in with one coalesced load per 64 edges and are read out edge
+// by edge into scalar registers (readlane); the scalar unit forms each row's
+// 32-bit byte offset (NARROW: the table below 4 GB; else 64-bit per lane), so
+// a lane adds its own offset and selects between the slots' values, and the
+// load takes the table's base from scalar registers. Edges go in groups of U
+// per slot, every load of a group issued before its first multiply-add; the
+// last group repeats the item's last edge in its unused places (a row already
+// loaded) and adds only the item's own edges. One accumulator chain per
+// group place, combined pairwise, then across the slots.
+template <int SL>
+__device__ __forceinline__ int pick(int a, int b, int slot) {
+  if constexpr (SL == 1) return a;
+  else return slot ? b : a;
+}
+
+template <int V, int SL, int U, bool FULL, bool NARROW>
+__device__ __forceinline__ void wide_pass(int kbeg, int kend, const int* __restrict__ col,
+                                          const int* __restrict__ perm,
+                                          const float* __restrict__ w, int w_by_perm,
+                                          const char* __restrict__ xb, int64_t row_bytes,
+                                          unsigned lane_off, int slot, bool fok,
+                                          float (&acc)[U][V]) {
+  const int lane = lane_id();
+  for (int kb = kbeg; kb < kend; kb += kWave) {
+    const int n = min(kWave, kend - kb);
+    const bool lok = lane < n;
+    const int cj = lok ? __builtin_nontemporal_load(col + kb + lane) : 0;
+    float wf = 1.0f;
+    if (w != nullptr && lok)  // weights in graph order, or in the caller's edge order
+      wf = w_by_perm ? w[__builtin_nontemporal_load(perm + kb + lane)]
+                     : __builtin_nontemporal_load(w + kb + lane);
+    const int wj = __float_as_int(wf);
+    auto group = [&](int j0, bool tail) {
+      float xv[U][V];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ja = j0 + u * SL;
+        const int ca = __builtin_amdgcn_readlane(cj, tail ? min(ja, n - 1) : ja);
+        const int cb = SL > 1 ? __builtin_amdgcn_readlane(cj, tail ? min(ja + 1, n - 1) : ja + 1) : 0;
+        if (FULL || fok) {
+          if constexpr (NARROW) {
+            const unsigned off =
+                (unsigned)pick<SL>(ca * (int)row_bytes, cb * (int)row_bytes, slot) + lane_off;
+            load_row<V>(reinterpret_cast<const float*>(xb + off), xv[u]);
+          } else {
+            const int64_t off = (int64_t)pick<SL>(ca, cb, slot) * row_bytes + lane_off;
+            load_row<V>(reinterpret_cast<const float*>(xb + off), xv[u]);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ja = j0 + u * SL;
+        if (tail && ja >= n) continue;  // uniform
+        const int wa = __builtin_amdgcn_readlane(wj, ja);
+        const int wb = SL > 1 ? __builtin_amdgcn_readlane(wj, tail ? min(ja + 1, n - 1) : ja + 1) : 0;
+        const float wt = __int_as_float(pick<SL>(wa, wb, slot));
+        if ((FULL || fok) && (!tail || ja + slot < n))
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[u][v] = __builtin_fmaf(wt, xv[u][v], acc[u][v]);
+      }
+    };
+    int j0 = 0;
+    for (; j0 + U * SL <= n; j0 += U * SL) group(j0, false);
+    if (j0 < n) group(j0, true);
+  }
+}
+
+template <int V, int SL, int U, bool NARROW>
+__global__ __launch_bounds__(kRowBlock) void spmm_wide(
+    const WorkItem* __restrict__ heavy, int n_heavy, const WorkItem* __restrict__ light,
+    int n_light, const int* __restrict__ col, const int* __restrict__ perm,
+    const float* __restrict__ w, int w_by_perm, const float* __restrict__ x, int64_t ldx, int F,
+    int mean, float* __restrict__ out, float* __restrict__ part, Epilogue ep) {
+  constexpr int LPS = kWave / SL;  // lanes per slot
+  constexpr int FC = LPS * V;      // columns per pass
+  const int wid = uniform(blockIdx.x * (kRowBlock / kWave) + threadIdx.x / kWave);
+  if (wid >= n_heavy + n_light) return;
+  const int lane = lane_id();
+  const int slot = lane / LPS, sl = lane % LPS;
+  const WorkItem* itp = wid < n_heavy ? heavy + wid : light + (wid - n_heavy);
+  const int row = uniform(itp->row), kbeg = uniform(itp->kbeg), kend = uniform(itp->kend);
+  const int pslot = uniform(itp->slot);
+  const char* xc = reinterpret_cast<const char*>(x);
+  const int64_t row_bytes = ldx * (int64_t)sizeof(float);
+  for (int f0 = 0; f0 < F; f0 += FC) {
+    const int f = f0 + sl * V;
+    const bool fok = f < F;
+    float acc[U][V];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[u][v] = 0.0f;
+    // the pass's column offset in scalar registers, the lane's in a 32-bit offset
+    const char* xb = xc + (int64_t)f0 * (int64_t)sizeof(float);
+    const unsigned lane_off = (unsigned)(sl * V) * (unsigned)sizeof(float);
+    if (f0 + FC <= F)
+      wide_pass<V, SL, U, true, NARROW>(kbeg, kend, col, perm, w, w_by_perm, xb, row_bytes,
+                                        lane_off, slot, fok, acc);
+    else
+      wide_pass<V, SL, U, false, NARROW>(kbeg, kend, col, perm, w, w_by_perm, xb, row_bytes,
+                                         lane_off, slot, fok, acc);
+#pragma unroll
+    for (int step = 1; step < U; step <<= 1)
+#pragma unroll
+      for (int u = 0; u + step < U; u += 2 * step)
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[u][v] += acc[u + step][v];
+#pragma unroll
+    for (int off = LPS; off < kWave; off <<= 1)
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[0][v] += __shfl_xor(acc[0][v], off);
+    if (slot != 0 || !fok) continue;
+    if (pslot < 0) {
+      if (mean && kend > kbeg) {
+        const float cnt = (float)(kend - kbeg);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[0][v] = acc[0][v] / cnt;
+      }
+      apply_epilogue<V>(ep, row, f, acc[0]);
+      store_row<V>(out + (int64_t)row * F + f, acc[0]);
+    } else {
+      // partial rows are read back once, by the fix-up, long after: streamed
+      // past the L2, which they would otherwise share with the gathered rows
+      store_row<V>(part + (int64_t)pslot * F + f, acc[0]);
+    }
+  }
+}
+
+// Whether the sum / mean goes through spmm_wide: rows of at least 64
+// columns (every lane busy), one weight per edge; the layout: two slots of
+// four columns per lane where 128 columns fit the alignment, else one slot of
+// two or one. TFG_WIDE_ROWS=0 keeps every aggregation on spmm_rows.
+struct WideShape {
+  int v, slots;
+};
+WideShape wide_shape(int64_t F, int vec, bool sum_like, bool heads, bool masked) {
+  if (!sum_like || heads || masked || F < kWave) return {0, 0};
+  if (const char* v = std::getenv("TFG_WIDE_ROWS"))
+    if (v[0] == '0') return {0, 0};
+  if (vec == 4 && F % 128 == 0) return {4, 2};
+  return {vec % 2 == 0 && F >= 2 * kWave ? 2 : 1, 1};
+}
+
+void launch_wide(WideShape ws, dim3 grid, hipStream_t s, const RowArgs& a, int64_t n_src) {
+  // the whole table within 32-bit byte offsets of its base
+  const bool narrow = (double)n_src * (double)a.ldx * 4.0 < 2147483648.0;
+#define TFG_WIDE(VV, SS, UU, NN)                                                       \
+  spmm_wide<VV, SS, UU, NN><<<grid, dim3(kRowBlock), 0, s>>>(                          \
+      a.heavy, a.n_heavy, a.light, a.n_light, a.col, a.perm, a.w, a.w_by_perm, a.x, a.ldx, \
+      a.F, a.mean, a.out, a.part, a.ep)
+  if (ws.slots == 2) {  // U = 4 (the power-law aggregation: 3.51 ms; U = 8: 3.69, U = 2: 3.51)
+    if (narrow) TFG_WIDE(4, 2, 4, true); else TFG_WIDE(4, 2, 4, false);
+  } else if (ws.v == 2) {
+    if (narrow) TFG_WIDE(2, 1, 8, true); else TFG_WIDE(2, 1, 8, false);
+  } else {
+    if (narrow) TFG_WIDE(1, 1, 8, true); else TFG_WIDE(1, 1, 8, false);
+  }
+#undef TFG_WIDE
+}
+
 template <bool SHORT>
 void dispatch_kind(bool mx, bool heads, int vec, int slots, dim3 grid, hipStream_t s,
                    const RowArgs& a) {
@@ -211,7 +375,10 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   const int waves = a.n_heavy + a.n_light;
   if (waves > 0) {
     dim3 grid((unsigned)((waves + kRowBlock / kWave - 1) / (kRowBlock / kWave)));
-    if (mask != nullptr)
+    const WideShape wsh = wide_shape(F, vec, !mx, heads, mask != nullptr);
+    if (wsh.v > 0)
+      launch_wide(wsh, grid, s, a, g.N_src);
+    else if (mask != nullptr)
       dispatch_masked(part_plan, heads, vec, slots, grid, s, a);
     else if (part_plan)
       dispatch_kind<true>(mx, heads, vec, slots, grid, s, a);
