@@ -388,8 +388,10 @@ int launch_aggregate(const Graph& g, const float* w, int H, int w_order, const f
   }
   if (n_rows > 0) {
     dim3 fgrid((unsigned)((n_rows + kItemBlock / kWave - 1) / (kItemBlock / kWave)));
-    // partials are dense [slot, F] rows: 16-byte accesses when F is a multiple of 4
-    const bool f4 = F % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
+    // partials are dense [slot, F] rows: 16-byte accesses when F is a multiple
+    // of 4 and the output (and the epilogue's h rows) allow them
+    const bool f4 = F % 4 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0 &&
+                    (h == nullptr || (ldh % 4 == 0 && reinterpret_cast<uintptr_t>(h) % 16 == 0));
     if (mx)
       fixup_rows<true, 1><<<fgrid, dim3(kItemBlock), 0, s>>>(rows, n_rows, a.part, a.part_arg, a.F,
                                                          a.mean, out, argmax, a.ep);
