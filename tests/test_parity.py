@@ -324,6 +324,71 @@ def test_aggregate_source_parts(tfg, orc, monkeypatch, F, H, reduce, plan):
         assert same_bits(host(res), host(coo))
 
 
+WIDE_CASES = [
+    # F, ldx: the layout the sum / mean kernel with scalar edge ids takes
+    (128, 132),  # two edge slots of 32 lanes x 4 columns
+    (256, 256),  # the same, two full passes over the columns
+    (192, 192),  # one slot of 64 lanes x 2 columns, second pass half full
+    (64, 64),    # one slot, one column per lane
+    (65, 67),    # one column per lane, a one-column second pass
+]
+
+
+@pytest.mark.parametrize("F,ldx", WIDE_CASES)
+@pytest.mark.parametrize("reduce", ["sum", "mean"])
+@pytest.mark.parametrize("plan", ["0", "1"])
+@pytest.mark.parametrize("wide", ["0", "1"])
+def test_aggregate_wide_layouts(tfg, orc, monkeypatch, F, ldx, reduce, plan, wide):
+    """Sum and mean over rows of at least 64 columns: the kernel with scalar
+    edge ids in each of its column layouts (wide=1), and the general row
+    kernel it replaces there (wide=0), on both plans, with weights in COO
+    order (gathered through the permutation), in graph order and without."""
+    monkeypatch.setenv("TFG_WIDE_ROWS", wide)
+    monkeypatch.setenv("TFG_PART_PLAN", plan)
+    n, e, parts = 1500, 50_000, 5
+    ei = graphgen.random_graph(F + ldx, n, e, hub=23, hub_edges=7000)
+    E = ei.shape[1]
+    big = graphgen.features(F + 1, n, ldx)
+    x = big[:, :F]
+    w = np.random.default_rng(F).standard_normal(E).astype(np.float32)
+    g = tfg.tfg_graph_create(dev(ei), n, src_parts=parts)
+    perm = expected_graph(orc, ei, n, parts=parts)[2]
+    xd = dev(big)[:, :F]
+    ref, S = orc.aggregate(ei, x, n, reduce, edge_weight=w)
+    coo = tfg.tfg_aggregate(dev(ei), xd, n, reduce, edge_weight=dev(w), graph=g)
+    csr = tfg.tfg_aggregate(None, xd, n, reduce, edge_weight=dev(w[perm]), weight_order="csr",
+                            graph=g)
+    what = f"{reduce} F={F} ldx={ldx} plan={plan} wide={wide}"
+    assert_scaled(host(coo), ref, S, what=what + " COO weights")
+    assert same_bits(host(coo), host(csr))
+    ref1, S1 = orc.aggregate(ei, x, n, reduce)
+    assert_scaled(host(tfg.tfg_aggregate(None, xd, n, reduce, graph=g)), ref1, S1,
+                  what=what + " unweighted")
+
+
+@pytest.mark.parametrize("plan", ["0", "1"])
+def test_aggregate_table_beyond_2gb(tfg, orc, monkeypatch, plan):
+    """A feature table whose rows span more than 2 GB (a large leading
+    dimension): row offsets no longer fit 32 bits and the gathers take
+    64-bit offsets."""
+    import torch
+    monkeypatch.setenv("TFG_PART_PLAN", plan)
+    n_src, n, e, F = 520, 700, 30_000, 128
+    ldx = (1 << 20) + 128  # 520 rows x 4 MB = 2.18 GB
+    assert n_src * ldx * 4 >= 2 ** 31
+    ei = graphgen.random_graph(77, n, e, n_src=n_src, hub=3, hub_edges=3000)
+    x = graphgen.features(78, n_src, F)
+    w = np.random.default_rng(79).standard_normal(ei.shape[1]).astype(np.float32)
+    big = torch.zeros((n_src, ldx), dtype=torch.float32, device="cuda:0")
+    big[:, :F] = dev(x)
+    g = tfg.tfg_graph_create(dev(ei), n, N_src=n_src, src_parts=4)
+    y = tfg.tfg_aggregate(dev(ei), big[:, :F], n, "sum", edge_weight=dev(w), graph=g)
+    ref, S = orc.aggregate(ei, x, n, "sum", edge_weight=w)
+    assert_scaled(host(y), ref, S, what=f"sum, ldx={ldx}, plan={plan}")
+    del big
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("reduce", ["sum", "max"])
 def test_aggregate_functional_and_csr_weights(tfg, orc, reduce):
     n, e, F = 2000, 40_000, 64
