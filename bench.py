@@ -72,7 +72,50 @@ def probe_lib():
     p, i64 = ctypes.c_void_p, ctypes.c_int64
     lib.tfg_probe_gather_window.argtypes = [p, i64, i64, i64, i64, p, p]
     lib.tfg_probe_gather_items.argtypes = [p, p, p, i64, p, p]
+    lib.tfg_probe_stream.argtypes = [p, ctypes.c_int, p, ctypes.c_int, i64, p]
     return lib
+
+
+# read / write mixes of the streaming kernels, in 4-byte words per element
+STREAM_MIXES = (("read 2", 2, 0, "first counting pass (both id rows)"),
+                ("read 1 + write 1", 1, 1, "a plain copy"),
+                ("read 2 + write 1", 2, 1, "graph-order weights (ids, key -> weight)"),
+                ("read 2 + write 2", 2, 2, "radix scatter passes over two-word payloads"),
+                ("read 2 + write 3", 2, 3, "last radix pass; COO-order weights with the edge list"),
+                ("read 8 + write 1", 8, 1, "fix-up of the partial rows (8 parts)"))
+
+
+def stream_ceiling(torch, n_edges: int, n_rows_words: int, device, reps: int = 5):
+    """Rates (GB/s of bytes read + written) of plain streams with the read /
+    write mixes of the CSR build, the normalisation and the fix-up, over as
+    many elements as those kernels move on the workload (E' per plane; the
+    fix-up mix over the output's N * F words). Best of `reps` launches."""
+    import ctypes
+    lib = probe_lib()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {}
+    for name, r, w, what in STREAM_MIXES:
+        n = n_rows_words if r == 8 else n_edges
+        n = -(-n // 4) * 4
+        src = torch.ones(r * n, dtype=torch.float32, device=device)
+        dst = torch.empty(max(w, 1) * n, dtype=torch.float32, device=device)
+        ts = []
+        for _ in range(reps + 1):
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record()
+            rc = lib.tfg_probe_stream(ctypes.c_void_p(src.data_ptr()), r,
+                                      ctypes.c_void_p(dst.data_ptr()), w, n, stream)
+            a1.record()
+            assert rc == 0, rc
+            torch.cuda.synchronize()
+            ts.append(a0.elapsed_time(a1))
+        ms = min(ts[1:])
+        out[name] = {"ms": round(ms, 4), "GBps": round((r + w) * n * 4 / (ms * 1e-3) / 1e9, 1),
+                     "words": n, "like": what}
+        del src, dst
+    torch.cuda.empty_cache()
+    return out
 
 
 def gather_ceiling(torch, x, items=None, col=None, reps: int = 5):
@@ -589,6 +632,12 @@ def run_ceiling(args):
     print(json.dumps({"row": "gather ceiling", "workload": f"power-law table [{N}, {F}] float32, "
                       f"{info['E']} gathers of 512-byte rows", "src_parts": P, "probes": res}),
           flush=True)
+    del g, items, col
+    torch.cuda.empty_cache()
+    st = stream_ceiling(torch, int(info["E"]), N * F, dev, reps=max(args.steps, 5))
+    print(json.dumps({"row": "stream ceiling", "workload": f"plain streams over E' = {info['E']} "
+                      f"elements per plane (the fix-up mix over N * F = {N * F} words)",
+                      "probes": st}), flush=True)
 
 
 def main():

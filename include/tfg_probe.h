@@ -1,12 +1,13 @@
 /*
  * Measurement probes of libtfg_probe.so: gathers with no arithmetic, used by
  * the benchmark to measure the ceiling of the row gathers that the sum
- * aggregation performs (the aggregation's roofline is the rate at which the
+ * aggregation performs, and plain streams for the ceiling of the streaming
+ * kernels (the aggregation's roofline is the rate at which the
  * CUs can pull 512-byte rows through the cache hierarchy, not HBM: the
  * gathered table of the power-law workload, 119 MB, is held by the Infinity
  * Cache). Not part of the method; the library libtfg.so does not use them.
  *
- * Both probes read rows of x ([rows, 128] float32, contiguous, 16-byte
+ * The two gather probes read rows of x ([rows, 128] float32, contiguous, 16-byte
  * aligned) with the aggregation's lane layout (two rows in flight per
  * wavefront instruction, 32 lanes x 16 bytes per row) and add the values into
  * registers; each wavefront writes one float of its sum to sink so that no
@@ -41,6 +42,19 @@ int tfg_probe_gather_window(const float *x, int64_t rows, int64_t window_rows,
  */
 int tfg_probe_gather_items(const float *x, const int32_t *col, const int32_t *items,
                            int64_t n_items, float *sink, void *stream);
+
+/*
+ * A plain stream: reads r_planes planes of n float32 words from in
+ * ([r_planes, n], contiguous) and writes w_planes planes to out
+ * ([max(w_planes, 1), n]), 16 bytes per thread and plane, each output word a
+ * sum of the input words at its index. It measures the rate of a stream with
+ * a given read / write mix (the practical ceiling of the method's streaming
+ * kernels). n: a multiple of 4; in, out: 16-byte aligned. Supported mixes
+ * (r_planes, w_planes): (2, 0), (1, 1), (2, 1), (2, 2), (2, 3), (8, 1);
+ * any other returns 1.
+ */
+int tfg_probe_stream(const float *in, int r_planes, float *out, int w_planes, int64_t n,
+                     void *stream);
 
 #ifdef __cplusplus
 }

@@ -455,6 +455,13 @@ __device__ __forceinline__ int packed_key(unsigned a, unsigned b, const KeyMap& 
   return (unpack_t(a, q) << q.lp) | source_part(unpack_s(a, b, q), m);
 }
 
+// The first pass's digit: the low bits of target << log2 P | source part.
+__device__ __forceinline__ int first_digit(unsigned a, unsigned b, const KeyMap& m,
+                                           const PackMap& q, int radix) {
+  const int part = q.lp == 0 ? 0 : source_part(unpack_s(a, b, q), m);
+  return ((unpack_t(a, q) << q.lp) | part) & (radix - 1);
+}
+
 // The scatter of one pass over packed payloads; the ranking and staging are
 // those of scatter() above. MODE 0: the first pass (reads edge_index, writes
 // A and B); 1: a middle pass (A and B to A and B); 2: the last pass (A and B
@@ -559,20 +566,13 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
     const int pos = p < tile_n ? (pk[i] & 0xFFFF) + loff[d] + (int)wcnt[wave][d] : 0xFFFF;
     pk[i] = (d << 16) | pos;
   }
-  // The first pass's digit is not a field of A: once every position is known
-  // (the barrier), the per-wave counters' LDS (exactly one byte per tile
-  // position) holds the digit of every staged position instead.
-  unsigned char* sdig = reinterpret_cast<unsigned char*>(&wcnt[0][0]);
-  static_assert(sizeof(wcnt) >= kSortTile, "one byte per tile position");
   static_assert(kSortTile < 0xFFFF, "tile positions fit below the 16-bit marker");
-  if constexpr (MODE == 0) __syncthreads();
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int pos = pk[i] & 0xFFFF;
     if (pos != 0xFFFF) {
       stage[0][pos] = va[i];
       stage[1][pos] = vb[i];
-      if constexpr (MODE == 0) sdig[pos] = (unsigned char)(pk[i] >> 16);
     }
   }
   __syncthreads();
@@ -581,7 +581,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
     const int p = i * kSortThreads + threadIdx.x;
     if (p < tile_n) {
       const unsigned a = stage[0][p], b = stage[1][p];
-      const int d = MODE == 0 ? (int)sdig[p] : (int)(a >> shift) & (radix - 1);
+      // the first pass's digit is not a field of A: it is recomputed from
+      // the unpacked ids, as the decode formed it
+      const int d = MODE == 0 ? first_digit(a, b, m, q, radix)
+                              : (int)(a >> shift) & (radix - 1);
       const int64_t gp = (int64_t)goff[d] + (p - loff[d]);
       if (gp >= 0 && gp < E) {  // always true for a consistent histogram
         if constexpr (MODE == 2) {

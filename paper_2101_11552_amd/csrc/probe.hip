@@ -94,6 +94,28 @@ __global__ __launch_bounds__(kWave) void gather_items(const float* __restrict__ 
   if (lane == 0) sink[item] = t;
 }
 
+// Streams R input planes into W output planes of n words each: every thread
+// reads one 16-byte piece of each input plane and writes the sum of the
+// pieces to each output plane (a plain stream with the read / write mix of a
+// kernel of the method, for its practical ceiling).
+template <int R, int W>
+__global__ __launch_bounds__(256) void stream_planes(const float* __restrict__ in, int64_t n,
+                                                     float* __restrict__ out) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= n) return;
+  f4 s = f4{0.f, 0.f, 0.f, 0.f};
+  f4 v[R > 0 ? R : 1];
+#pragma unroll
+  for (int r = 0; r < R; ++r) v[r] = *reinterpret_cast<const f4*>(in + (int64_t)r * n + i);
+#pragma unroll
+  for (int r = 0; r < R; ++r) s += v[r];
+#pragma unroll
+  for (int w = 0; w < W; ++w) *reinterpret_cast<f4*>(out + (int64_t)w * n + i) = s + (float)w;
+  if constexpr (W == 0) {
+    if (s.x == 1.5f && s.y == -2.5f && s.z == 3.25f && s.w == 0.125f) out[0] = s.x;  // keeps the loads
+  }
+}
+
 bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
 
 }  // namespace
@@ -122,6 +144,29 @@ int tfg_probe_gather_items(const float* x, const int32_t* col, const int32_t* it
   gather_items<4><<<(unsigned)n_items, kWave, 0, static_cast<hipStream_t>(stream)>>>(
       x, col, items, n_items, sink);
   return hipGetLastError() == hipSuccess ? 0 : 6;
+}
+
+int tfg_probe_stream(const float* in, int r_planes, float* out, int w_planes, int64_t n,
+                     void* stream) {
+  if ((r_planes > 0 && (in == nullptr || !aligned16(in))) || out == nullptr || !aligned16(out) ||
+      n < 0 || n % 4 != 0 || n / 4 / 256 >= (int64_t(1) << 31))
+    return 1;
+  if (n == 0) return 0;
+  const unsigned grid = (unsigned)((n / 4 + 255) / 256);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+#define TFG_STREAM(RR, WW)                                                 \
+  if (r_planes == RR && w_planes == WW) {                                   \
+    stream_planes<RR, WW><<<grid, 256, 0, s>>>(in, n, out);                 \
+    return hipGetLastError() == hipSuccess ? 0 : 6;                         \
+  }
+  TFG_STREAM(2, 0)
+  TFG_STREAM(1, 1)
+  TFG_STREAM(2, 1)
+  TFG_STREAM(2, 2)
+  TFG_STREAM(2, 3)
+  TFG_STREAM(8, 1)
+#undef TFG_STREAM
+  return 1;
 }
 
 }  // extern "C"
