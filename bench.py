@@ -452,6 +452,20 @@ def run_suite(args):
         return tfg.tfg_aggregate(ei3, h, n3, "sum", edge_weight=a_csr, heads=H,
                                  weight_order="csr", graph=g3)
     ms_c = _timed(torch, chain, reps)
+    # the same chain with scores, alpha and weights kept in the graph order
+    sg_out = torch.empty((E3, H), dtype=torch.float32, device=dev)
+    ag_out = torch.empty_like(sg_out)
+    sg_ws = torch.empty(max(tfg.load().tfg_gat_graph_scores_ws_bytes(g3.handle, H), 256),
+                        dtype=torch.uint8, device=dev)
+    ag_ws = torch.empty(max(tfg.load().tfg_segment_softmax_graph_ws_bytes(g3.handle, H), 256),
+                        dtype=torch.uint8, device=dev)
+
+    def chain_graph_order():
+        s = tfg.tfg_gat_graph_scores(g3, h, a_s, a_d, c["slope"], order="csr", out=sg_out, ws=sg_ws)
+        a = tfg.tfg_segment_softmax_graph(g3, s, order="csr", out=ag_out, ws=ag_ws)
+        return tfg.tfg_aggregate(None, h, n3, "sum", edge_weight=a, heads=H, weight_order="csr",
+                                 graph=g3)
+    ms_cg = _timed(torch, chain_graph_order, reps)
     ei3_np = c["edge_index"]
     if not args.no_cpu_baseline:
         cpu["gat"] = _oracle(lambda: oracle.gat_layer(ei3_np, c["h"], c["a_src"], c["a_dst"], H,
@@ -465,6 +479,7 @@ def run_suite(args):
          E3 * (4 + 4 * H + 4 * Fh) + n3 * (4 * Fh + 8 * H) + n3 * (4 * H + 4 * Fh + 4),
          kernel="node_projections_vec + gat_short + gat_items + gat_merge",
          unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
+         unfused_chain_graph_order_ms=round(ms_cg, 4),
          cpu_baseline=cpu.get("gat"), cpu_baseline_threads=cpu.get("gat_t"))
     # the Transformer-style variant: q, key, v of the same shape as h
     gen = torch.Generator(device=dev).manual_seed(3)
@@ -498,6 +513,13 @@ def run_suite(args):
     _row("segment softmax", wl3, ms, E3, E3 * (4 + 8 * H) + 4 * (n3 + 1),
          kernel="softmax_items + softmax_split",
          cpu_baseline=cpu.get("sm"))
+    # scores and alpha in the graph order: no permutation, one run per row
+    s_g = tfg.tfg_gat_graph_scores(g3, h, a_s, a_d, c["slope"], order="csr")
+    ms = _timed(torch, lambda: tfg.tfg_segment_softmax_graph(g3, s_g, order="csr", out=ag_out,
+                                                             ws=ag_ws), reps)
+    _row("segment softmax, scores and alpha in graph order", wl3, ms, E3,
+         E3 * 8 * H + 4 * (n3 + 1), kernel="softmax_items + softmax_split (no permutation)",
+         cpu_baseline=cpu.get("sm"))
     alpha = tfg.tfg_segment_softmax(s, ei3[1], n3, graph=g3)
     dal = torch.randn_like(alpha)
     if not args.no_cpu_baseline:
@@ -509,7 +531,14 @@ def run_suite(args):
     _row("segment softmax backward", wl3, ms, E3, E3 * (4 + 12 * H) + 4 * (n3 + 1),
          kernel="softmax_grad_items + softmax_grad_split",
          cpu_baseline=cpu.get("smb"))
-    del g3, ei3, h, s, alpha, dal
+    a_g = tfg.tfg_segment_softmax_graph(g3, s_g, order="csr")
+    dal_g = torch.randn_like(a_g)
+    ms = _timed(torch, lambda: tfg.tfg_segment_softmax_graph_backward(g3, a_g, dal_g, order="csr"),
+                reps)
+    _row("segment softmax backward, in graph order", wl3, ms, E3, E3 * 12 * H + 4 * (n3 + 1),
+         kernel="softmax_grad_items + softmax_grad_split (no permutation)",
+         cpu_baseline=cpu.get("smb"))
+    del g3, ei3, h, s, alpha, dal, s_g, a_g, dal_g, sg_out, ag_out
     torch.cuda.empty_cache()
 
     # --- mini-batch of small graphs: BatchGraph, 3 GCN layers, pooling

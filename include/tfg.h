@@ -373,6 +373,41 @@ int tfg_segment_softmax_backward(const float *alpha, const float *dalpha, int64_
                                  float *dscores, void *ws, size_t ws_bytes, tfg_stream_t stream);
 
 /*
+ * The same workflow over a graph handle with the per-edge arrays in `order`:
+ * TFG_COO (edge ids of g: the input edges, then the loops) or TFG_CSR (the
+ * graph order of g, position k of tfg_graph_csr, the order in which
+ * tfg_aggregate reads TFG_CSR weights). In the graph order every target's
+ * edges are one contiguous run, so the softmax reads its scores and writes
+ * its alpha without the permutation: a GAT layer can keep its scores, alpha
+ * and weights in that order from end to end (Sec. 2.1.2, Fig. 5a; the graph
+ * is the per-graph cache of Sec. 3).
+ * tfg_gat_graph_scores: the additive scores of tfg_gat_edge_scores for the
+ *   E' edges of g (sources and targets one node set of N nodes: g forward,
+ *   N_src == N); out_scores [E', H] in `order`; h [N, H*D]; a_src, a_dst
+ *   [H, D]; ws: tfg_gat_graph_scores_ws_bytes(g, H) bytes (the node
+ *   projections). Bit-identical to tfg_gat_edge_scores on the same edges.
+ * tfg_segment_softmax_graph: scores and out [E', H], both in `order`, the
+ *   segments the targets of g; bit-identical to tfg_segment_softmax with g
+ *   (TFG_CSR: to its out_csr). ws: tfg_segment_softmax_graph_ws_bytes(g, H).
+ * tfg_segment_softmax_graph_backward: its gradient as
+ *   tfg_segment_softmax_backward, alpha, dalpha and dscores [E', H] in
+ *   `order`; g forward; the same workspace size.
+ * Errors: TFG_ERR_INVALID_ARG (NULL g or pointers, bad H / D / order, a
+ * graph of the wrong kind), TFG_ERR_WORKSPACE.
+ */
+size_t tfg_gat_graph_scores_ws_bytes(const tfg_graph *g, int64_t H);
+int tfg_gat_graph_scores(const tfg_graph *g, const float *h, int64_t H, int64_t D,
+                         const float *a_src, const float *a_dst, float slope, float *out_scores,
+                         int order, void *ws, size_t ws_bytes, tfg_stream_t stream);
+size_t tfg_segment_softmax_graph_ws_bytes(const tfg_graph *g, int64_t H);
+int tfg_segment_softmax_graph(const tfg_graph *g, const float *scores, int64_t H, int order,
+                              float *out, void *ws, size_t ws_bytes, tfg_stream_t stream);
+int tfg_segment_softmax_graph_backward(const tfg_graph *g, const float *alpha,
+                                       const float *dalpha, int64_t H, int order,
+                                       float *dscores, void *ws, size_t ws_bytes,
+                                       tfg_stream_t stream);
+
+/*
  * Fused attention aggregation: the whole GAT workflow of Fig. 5(a) plus the
  * weighted message aggregation in one pass over the graph, without writing
  * the [E, H] scores or coefficients:

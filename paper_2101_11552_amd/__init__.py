@@ -26,6 +26,7 @@ __all__ = [
     "tfg_segment_pool", "tfg_segment_pool_backward",
     "tfg_batch_graphs", "tfg_batch_graphs_totals", "tfg_propagate", "tfg_gat_aggregate",
     "tfg_edge_dot_scores", "tfg_gat_dot_aggregate",
+    "tfg_gat_graph_scores", "tfg_segment_softmax_graph", "tfg_segment_softmax_graph_backward",
     "library_path", "load",
 ]
 
@@ -116,6 +117,11 @@ def load():
         "tfg_gat_dot_aggregate_ws_bytes": (sz, [p, i64, i64]),
         "tfg_gat_dot_aggregate": (ci, [p, p, p, p, i64, i64, ctypes.c_float, p, p, p, sz, p]),
         "tfg_edge_reorder": (ci, [p, p, p, i64, p, p, sz, p]),
+        "tfg_gat_graph_scores_ws_bytes": (sz, [p, i64]),
+        "tfg_gat_graph_scores": (ci, [p, p, i64, i64, p, p, ctypes.c_float, p, ci, p, sz, p]),
+        "tfg_segment_softmax_graph_ws_bytes": (sz, [p, i64]),
+        "tfg_segment_softmax_graph": (ci, [p, p, i64, ci, p, p, sz, p]),
+        "tfg_segment_softmax_graph_backward": (ci, [p, p, p, i64, ci, p, p, sz, p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -585,6 +591,72 @@ def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
         out = out.reshape(E)
         oc = oc.reshape(E) if oc is not None else None
     return (out, oc) if out_csr else out
+
+
+def tfg_gat_graph_scores(graph: Graph, h: torch.Tensor, a_src: torch.Tensor, a_dst: torch.Tensor,
+                         slope: float = 0.2, order: str = "csr", out: torch.Tensor | None = None,
+                         ws: torch.Tensor | None = None) -> torch.Tensor:
+    """The additive attention scores [E', H] of the graph's edges, in ``order``
+    ("csr": the graph order, "coo": edge ids)."""
+    lib = load()
+    dev = graph.device
+    h = _f32(h, "h", dev)
+    a_src, a_dst = _f32(a_src, "a_src", dev), _f32(a_dst, "a_dst", dev)
+    H = a_src.shape[0]
+    D = a_src.numel() // H
+    if h.dim() != 2 or h.shape != (graph.N, H * D) or a_dst.shape != a_src.shape:
+        raise ValueError("h must be [N, H*D] and a_src, a_dst [H, D]")
+    if out is None:
+        out = torch.empty((graph.E, H), dtype=torch.float32, device=dev)
+    _out(out, (graph.E, H), torch.float32, dev, "out")
+    ws = _ws(ws, lib.tfg_gat_graph_scores_ws_bytes(graph.handle, H), dev)
+    _check(lib.tfg_gat_graph_scores(graph.handle, _ptr(h), H, D, _ptr(a_src), _ptr(a_dst),
+                                    float(slope), _ptr(out), _ORDER[order], _ptr(ws), _nbytes(ws),
+                                    _stream(dev)))
+    return out
+
+
+def tfg_segment_softmax_graph(graph: Graph, scores: torch.Tensor, order: str = "csr",
+                              out: torch.Tensor | None = None,
+                              ws: torch.Tensor | None = None) -> torch.Tensor:
+    """Softmax of scores [E', H] (or [E']) over the graph's targets, scores and
+    result in ``order`` ("csr": the graph order, "coo": edge ids)."""
+    lib = load()
+    dev = graph.device
+    s = _f32(scores, "scores", dev)
+    s2 = s.reshape(s.shape[0], -1)
+    E, H = s2.shape
+    if E != graph.E:
+        raise ValueError(f"scores must hold one row per edge of the graph ({graph.E})")
+    if out is None:
+        out = torch.empty_like(s2)
+    _out(out, (E, H), torch.float32, dev, "out")
+    ws = _ws(ws, lib.tfg_segment_softmax_graph_ws_bytes(graph.handle, H), dev)
+    _check(lib.tfg_segment_softmax_graph(graph.handle, _ptr(s2), H, _ORDER[order], _ptr(out),
+                                         _ptr(ws), _nbytes(ws), _stream(dev)))
+    return out.reshape(s.shape)
+
+
+def tfg_segment_softmax_graph_backward(graph: Graph, alpha: torch.Tensor, dalpha: torch.Tensor,
+                                       order: str = "csr") -> torch.Tensor:
+    """dL/d scores from alpha and dalpha ([E', H] or [E']) in ``order``."""
+    lib = load()
+    dev = graph.device
+    a = _f32(alpha, "alpha", dev)
+    a2 = a.reshape(a.shape[0], -1)
+    da = _f32(dalpha, "dalpha", dev)
+    if da.numel() != a2.numel():
+        raise ValueError("dalpha must have the shape of alpha")
+    da = da.reshape(a2.shape)
+    E, H = a2.shape
+    if E != graph.E:
+        raise ValueError(f"alpha must hold one row per edge of the graph ({graph.E})")
+    ds = torch.empty_like(a2)
+    ws = _workspace(lib.tfg_segment_softmax_graph_ws_bytes(graph.handle, H), dev)
+    _check(lib.tfg_segment_softmax_graph_backward(graph.handle, _ptr(a2), _ptr(da), H,
+                                                  _ORDER[order], _ptr(ds), _ptr(ws), _nbytes(ws),
+                                                  _stream(dev)))
+    return ds.reshape(a.shape)
 
 
 def tfg_segment_pool(x: torch.Tensor, graph_index: torch.Tensor, G: int, reduce: str = "sum",

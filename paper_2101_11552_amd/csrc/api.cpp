@@ -876,5 +876,66 @@ int tfg_edge_dot_scores(const tfg_graph* g, const float* q, const float* key, in
                          order == TFG_COO ? 1 : 0, as_stream(stream));
 }
 
+size_t tfg_gat_graph_scores_ws_bytes(const tfg_graph* g, int64_t H) {
+  if (!g || H < 1) return 0;
+  return tfg_gat_edge_scores_ws_bytes(g->g.N, H);
+}
+
+int tfg_gat_graph_scores(const tfg_graph* g, const float* h, int64_t H, int64_t D,
+                         const float* a_src, const float* a_dst, float slope, float* out_scores,
+                         int order, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (gr.transposed || gr.N_src != gr.N)
+    return fail(TFG_ERR_INVALID_ARG,
+                "scores need a forward graph whose sources and targets are one node set");
+  if (H < 1 || D < 1 || H * D >= kMaxCount || gr.E * H >= kMaxCount)
+    return fail(TFG_ERR_INVALID_ARG, "bad H or D");
+  if (order != TFG_COO && order != TFG_CSR) return fail(TFG_ERR_INVALID_ARG, "bad order");
+  if ((gr.E > 0 && out_scores == nullptr) ||
+      (gr.N > 0 && (h == nullptr || a_src == nullptr || a_dst == nullptr)))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_gat_graph_scores_ws_bytes(g, H))) return wrc;
+  if (int e = check_device(gr)) return e;
+  return launch_gat_graph_scores(gr, h, (int)H, (int)D, a_src, a_dst, slope, out_scores,
+                                 order == TFG_COO ? 1 : 0, static_cast<float*>(ws),
+                                 as_stream(stream));
+}
+
+size_t tfg_segment_softmax_graph_ws_bytes(const tfg_graph* g, int64_t H) {
+  if (!g || H < 1) return 0;
+  return row_stats_bytes(g->g.n_heavy, H) + 256;
+}
+
+int tfg_segment_softmax_graph(const tfg_graph* g, const float* scores, int64_t H, int order,
+                              float* out, void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (H < 1 || gr.E * H >= (int64_t(1) << 62)) return fail(TFG_ERR_INVALID_ARG, "bad H");
+  if (order != TFG_COO && order != TFG_CSR) return fail(TFG_ERR_INVALID_ARG, "bad order");
+  if (gr.E > 0 && (scores == nullptr || out == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_softmax_graph_ws_bytes(g, H))) return wrc;
+  if (int e = check_device(gr)) return e;
+  return launch_segment_softmax(gr, scores, (int)H, out, nullptr, ws, as_stream(stream),
+                                order == TFG_CSR);
+}
+
+int tfg_segment_softmax_graph_backward(const tfg_graph* g, const float* alpha,
+                                       const float* dalpha, int64_t H, int order, float* dscores,
+                                       void* ws, size_t ws_bytes, tfg_stream_t stream) {
+  if (!g) return fail(TFG_ERR_INVALID_ARG, "graph is NULL");
+  const Graph& gr = g->g;
+  if (gr.transposed) return fail(TFG_ERR_INVALID_ARG, "g must be a forward graph");
+  if (H < 1 || gr.E * H >= (int64_t(1) << 62)) return fail(TFG_ERR_INVALID_ARG, "bad H");
+  if (order != TFG_COO && order != TFG_CSR) return fail(TFG_ERR_INVALID_ARG, "bad order");
+  if (gr.E > 0 && (alpha == nullptr || dalpha == nullptr || dscores == nullptr))
+    return fail(TFG_ERR_INVALID_ARG, "NULL pointer");
+  if (int wrc = check_ws(ws, ws_bytes, tfg_segment_softmax_graph_ws_bytes(g, H))) return wrc;
+  if (int e = check_device(gr)) return e;
+  return launch_segment_softmax_backward(gr, alpha, dalpha, (int)H, dscores, ws,
+                                         as_stream(stream), order == TFG_CSR);
+}
+
 }  // extern "C"
 

@@ -386,7 +386,7 @@ __device__ __forceinline__ void grad_short_row(const WorkItem& it, const int* __
   for (int j = 1; j <= kShortRow; ++j) nw = __any(n >= j) ? j : nw;
   int e[kShortRow];
 #pragma unroll
-  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? perm[kb + j] : 0;
+  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? edge_at(perm, kb + j) : 0;
   for (int h = hh; h < H; h += HP) {
     float a[kShortRow], g[kShortRow];
 #pragma unroll
@@ -445,7 +445,7 @@ __device__ __forceinline__ double grad_sweep_dot(const int* __restrict__ perm,
   double dot = 0.0;
   for (int k = kb + slot; k < ke; k += SL)
     if (act) {
-      const int64_t i = (int64_t)perm[k] * H + h;
+      const int64_t i = (int64_t)edge_at(perm, k) * H + h;
       dot += (double)alpha[i] * (double)da[i];
     }
   return slots_sum(dot, HP);
@@ -458,7 +458,7 @@ __device__ __forceinline__ void grad_sweep_write(const int* __restrict__ perm,
                                                  double dot, float* __restrict__ ds) {
   for (int k = kb + slot; k < ke; k += SL)
     if (act) {
-      const int64_t i = (int64_t)perm[k] * H + h;
+      const int64_t i = (int64_t)edge_at(perm, k) * H + h;
       ds[i] = (float)((double)alpha[i] * ((double)da[i] - dot));
     }
 }
@@ -861,8 +861,9 @@ int launch_aggregate_backward(const Graph& g, const Graph* gt, const float* w, i
 }
 
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
-                                    int H, float* ds, void* ws, hipStream_t s) {
+                                    int H, float* ds, void* ws, hipStream_t s, bool graph_order) {
   if (g.N == 0 || g.E == 0 || H == 0) return TFG_OK;
+  const int* perm = graph_order ? nullptr : g.perm;  // alpha, dalpha, ds in the graph order
   int hp = 1;
   while (hp * 2 <= std::min(H, kWave)) hp *= 2;
   // the double part of the per-chunk statistics (row_stats_bytes layout)
@@ -875,12 +876,12 @@ int launch_segment_softmax_backward(const Graph& g, const float* alpha, const fl
   if (waves > 0) {
     softmax_grad_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.short_rows, g.n_short, (int)short_waves, g.long_rows, g.n_long, g.heavy, g.n_heavy,
-        g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, ds, pdot);
+        g.rowptr, g.chunk, perm, alpha, dalpha, H, hp, ds, pdot);
     TFG_LAUNCHED("softmax_grad_items");
   }
   if (g.n_split > 0) {
     softmax_grad_split<<<(unsigned)g.n_split, kGradSplitWaves * kWave, 0, s>>>(
-        g.split, g.rowptr, g.chunk, g.perm, alpha, dalpha, H, hp, pdot, ds);
+        g.split, g.rowptr, g.chunk, perm, alpha, dalpha, H, hp, pdot, ds);
     TFG_LAUNCHED("softmax_grad_split");
   }
   return TFG_OK;

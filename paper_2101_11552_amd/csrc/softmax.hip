@@ -132,6 +132,26 @@ __global__ __launch_bounds__(kBlock) void edge_scores(const IdxT* __restrict__ s
   out[i] = z >= 0.0f ? z : slope * z;
 }
 
+// The same scores over a graph handle: one thread per (graph position, head),
+// the source from col, the target from the stored sort key (target * parts +
+// part), written at the position (graph order) or at the edge id perm[k]
+// (the caller's order). Same operands and operations as edge_scores.
+__global__ __launch_bounds__(kBlock) void edge_scores_graph(const int* __restrict__ col,
+                                                            const int* __restrict__ key,
+                                                            const int* __restrict__ perm,
+                                                            int parts, int64_t E, int H,
+                                                            const float* __restrict__ as,
+                                                            const float* __restrict__ ad,
+                                                            float slope, float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (position, head)
+  if (i >= E * H) return;
+  const int64_t k = i / H;
+  const int h = (int)(i - k * H);
+  const int64_t sv = col[k], t = key[k] / parts;
+  const float z = as[sv * H + h] + ad[t * H + h];
+  out[(int64_t)edge_at(perm, (int)k) * H + h] = z >= 0.0f ? z : slope * z;
+}
+
 // Short rows (at most kShortRow edges), 64 / HP per wavefront: lane (r, hh)
 // takes row short_rows[i] and heads hh, hh + HP, ...; the row's scores are
 // loaded at once and kept in registers: maximum, then the sum of exp(s - m)
@@ -150,7 +170,7 @@ __device__ __forceinline__ void softmax_short_row(const WorkItem& it,
   for (int j = 1; j <= kShortRow; ++j) nw = __any(n >= j) ? j : nw;
   int e[kShortRow];
 #pragma unroll
-  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? perm[kb + j] : 0;
+  for (int j = 0; j < kShortRow; ++j) e[j] = j < n ? edge_at(perm, kb + j) : 0;
   for (int h = hh; h < H; h += HP) {
     float v[kShortRow];
     float m = -__builtin_huge_valf();
@@ -267,7 +287,7 @@ __device__ __forceinline__ void load_steps(const int* __restrict__ perm,
 #pragma unroll
   for (int u = 0; u < kSmSteps; ++u) {
     const int k = k0 + u * SL;
-    e[u] = (act && k < ke) ? (int64_t)perm[k] : -1;
+    e[u] = (act && k < ke) ? (int64_t)edge_at(perm, k) : -1;
   }
 #pragma unroll
   for (int u = 0; u < kSmSteps; ++u) v[u] = e[u] >= 0 ? s[e[u] * H + h] : 0.0f;
@@ -545,14 +565,35 @@ int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const f
   return TFG_OK;
 }
 
+int launch_gat_graph_scores(const Graph& g, const float* h, int H, int D, const float* a_src,
+                            const float* a_dst, float slope, float* out, int by_perm,
+                            float* proj, hipStream_t s) {
+  float* as = proj;
+  float* ad = proj + g.N * H;
+  if (g.N * H > 0) {
+    projections(h, g.N, H, D, a_src, a_dst, as, ad, s);
+    TFG_LAUNCHED("node_projections");
+  }
+  if (g.E * H > 0) {
+    const unsigned nb = (unsigned)((g.E * H + kBlock - 1) / kBlock);
+    edge_scores_graph<<<nb, kBlock, 0, s>>>(g.col, g.key, by_perm ? g.perm : nullptr, g.parts, g.E,
+                                            H, as, ad, slope, out);
+    TFG_LAUNCHED("edge_scores_graph");
+  }
+  return TFG_OK;
+}
+
 size_t row_stats_bytes(int64_t n_chunks, int64_t H) {
   const size_t n = (size_t)std::max<int64_t>(n_chunks * H, 1);
   return align_up(sizeof(float) * n, 256) + align_up(sizeof(double) * n, 256);
 }
 
 int launch_segment_softmax(const Graph& g, const float* scores, int H, float* out, float* out_csr,
-                           void* ws, hipStream_t s) {
+                           void* ws, hipStream_t s, bool graph_order) {
   if (g.N == 0 || g.E == 0 || H == 0) return TFG_OK;
+  // scores and alpha in the graph order: position k is edge k, one output
+  const int* perm = graph_order ? nullptr : g.perm;
+  if (graph_order) out_csr = nullptr;
   int hp = 1;
   while (hp * 2 <= std::min(H, kWave)) hp *= 2;
   float* pm = static_cast<float*>(ws);
@@ -564,12 +605,12 @@ int launch_segment_softmax(const Graph& g, const float* scores, int H, float* ou
   if (waves > 0) {
     softmax_items<<<(unsigned)((waves + (kItemBlock / kWave) - 1) / (kItemBlock / kWave)), kItemBlock, 0, s>>>(
         g.short_rows, g.n_short, (int)short_waves, g.long_rows, g.n_long, g.heavy, g.n_heavy,
-        g.rowptr, g.chunk, g.perm, scores, H, hp, out, out_csr, pm, pd);
+        g.rowptr, g.chunk, perm, scores, H, hp, out, out_csr, pm, pd);
     TFG_LAUNCHED("softmax_items");
   }
   if (g.n_split > 0) {
     softmax_split<<<(unsigned)g.n_split, kSplitWaves * kWave, 0, s>>>(
-        g.split, g.rowptr, g.chunk, g.perm, scores, H, hp, pm, pd, out, out_csr);
+        g.split, g.rowptr, g.chunk, perm, scores, H, hp, pm, pd, out, out_csr);
     TFG_LAUNCHED("softmax_split");
   }
   return TFG_OK;

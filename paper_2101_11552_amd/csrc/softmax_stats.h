@@ -40,13 +40,19 @@ __device__ __forceinline__ void stat_add(float& m, double& d, float v) {
 // are (slot, head) pairs, SL = 64 / HP slots; slot step u of an item
 // starting at kb is position kb + slot + u * SL.
 // Edge ids of NST steps of [kb, ke) (-1 past ke).
+// Where the per-edge values of graph position k live: at the caller's edge id
+// perm[k], or (perm NULL: arrays kept in the graph order) at k itself.
+__device__ __forceinline__ int edge_at(const int* __restrict__ perm, int k) {
+  return perm != nullptr ? perm[k] : k;
+}
+
 template <int NST>
 __device__ __forceinline__ void load_ids(const int* __restrict__ perm, int kb, int ke, int slot,
                                          int SL, int (&e)[NST]) {
 #pragma unroll
   for (int u = 0; u < NST; ++u) {
     const int k = kb + slot + u * SL;
-    e[u] = k < ke ? perm[k] : -1;
+    e[u] = k < ke ? edge_at(perm, k) : -1;
   }
 }
 

@@ -151,8 +151,14 @@ int launch_gat_scores(const void* edge_index, int index_type, int64_t E, const f
 // Per-chunk softmax statistics of the long rows: [n_chunks, H] float maxima
 // and double sums (the workspace of the softmax launches).
 size_t row_stats_bytes(int64_t n_chunks, int64_t H);
+// graph_order: scores and out in the graph order of g (position k), out_csr unused.
 int launch_segment_softmax(const Graph& g, const float* scores, int H, float* out,
-                           float* out_csr, void* ws, hipStream_t s);
+                           float* out_csr, void* ws, hipStream_t s, bool graph_order = false);
+// The additive scores over a graph handle (projections into proj_ws, [2, N, H]),
+// written in the graph order or (by_perm) at the caller's edge ids.
+int launch_gat_graph_scores(const Graph& g, const float* h, int H, int D, const float* a_src,
+                            const float* a_dst, float slope, float* out, int by_perm,
+                            float* proj_ws, hipStream_t s);
 // pool.hip
 int launch_segment_pool(const float* x, int64_t Nb, int64_t F, int64_t ldx,
                         const void* graph_index, int index_type, int64_t G, int reduce,
@@ -184,7 +190,8 @@ size_t edge_reorder_ws_bytes(int64_t E, int H, bool from, bool to);
 int launch_edge_reorder(const int* perm_from, const int* perm_to, int64_t E, int H,
                         const float* in, float* out, void* ws, size_t ws_bytes, hipStream_t s);
 int launch_segment_softmax_backward(const Graph& g, const float* alpha, const float* dalpha,
-                                    int H, float* ds, void* ws, hipStream_t s);
+                                    int H, float* ds, void* ws, hipStream_t s,
+                                    bool graph_order = false);
 // gat.hip
 size_t gat_aggregate_ws_bytes(const Graph& g, int64_t H, int64_t D);
 // Scaled dot-product variant: D a power of two, at most 64.

@@ -490,6 +490,79 @@ def test_segment_softmax(tfg, orc, H, parts):
     assert np.all(np.abs(tot[has] - 1) <= 1e-5)
 
 
+@pytest.mark.parametrize("H,D,parts,loops", [(8, 16, 1, False), (3, 4, 1, True),
+                                             (8, 16, 4, False), (1, 5, 3, True)])
+def test_attention_in_graph_order(tfg, orc, H, D, parts, loops):
+    """Scores, softmax and its gradient over a graph handle with the per-edge
+    arrays in the graph order: the same bits as the calls in the caller's
+    order (permuted), and the oracle's values."""
+    n, e = 4000, 60_000
+    ei = graphgen.random_graph(H * D + parts, n, e, hub=3, hub_edges=5000)
+    g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=loops, src_parts=parts)
+    oei = orc.gcn_norm(ei, n)[0] if loops else ei  # the handle's edge list (loops appended)
+    E = oei.shape[1]
+    assert g.E == E
+    perm = expected_graph(orc, oei, n, parts=parts)[2]
+    h = graphgen.features(H, n, H * D)
+    r = np.random.default_rng(D)
+    a_s = r.standard_normal((H, D)).astype(np.float32)
+    a_d = r.standard_normal((H, D)).astype(np.float32)
+    s_coo = host(tfg.tfg_gat_edge_scores(dev(oei.astype(np.int32)), dev(h), dev(a_s), dev(a_d)))
+    s_csr = host(tfg.tfg_gat_graph_scores(g, dev(h), dev(a_s), dev(a_d), order="csr"))
+    assert same_bits(s_csr, s_coo[perm])
+    assert same_bits(host(tfg.tfg_gat_graph_scores(g, dev(h), dev(a_s), dev(a_d), order="coo")),
+                     s_coo)
+    # softmax: graph order == the COO call's graph-order output, bit for bit
+    a_coo, a_csr_ref = tfg.tfg_segment_softmax(dev(s_coo), dev(oei[1]), n, graph=g, out_csr=True)
+    a_csr = host(tfg.tfg_segment_softmax_graph(g, dev(s_csr), order="csr"))
+    assert same_bits(a_csr, host(a_csr_ref))
+    assert same_bits(host(tfg.tfg_segment_softmax_graph(g, dev(s_coo), order="coo")), host(a_coo))
+    ref64, a32 = orc.segment_softmax(s_coo, oei[1], n)
+    assert_rel(a_csr, ref64[perm], what="softmax in graph order")
+    # gradient in both orders
+    da = graphgen.features(H + 100, E, H)
+    ds_coo = host(tfg.tfg_segment_softmax_backward(a_coo, dev(da), dev(oei[1]), n, graph=g))
+    ds_csr = host(tfg.tfg_segment_softmax_graph_backward(g, dev(a_csr), dev(da[perm]),
+                                                         order="csr"))
+    assert same_bits(ds_csr, ds_coo[perm])
+    assert same_bits(host(tfg.tfg_segment_softmax_graph_backward(g, a_coo, dev(da), order="coo")),
+                     ds_coo)
+    a_h = host(a_coo)
+    ref = orc.segment_softmax_backward(a_h, da, oei[1], n)
+    dot = np.zeros((n, H))
+    np.add.at(dot, oei[1], a_h.astype(np.float64) * np.abs(da))
+    S = a_h * (np.abs(da) + dot[oei[1]])
+    assert_scaled(ds_csr, ref[perm], S[perm], what="dscores in graph order")
+    # a layer kept in the graph order: scores -> softmax -> aggregation, TFG_CSR weights
+    y = host(tfg.tfg_aggregate(None, dev(h), n, "sum", edge_weight=dev(a_csr), heads=H,
+                               weight_order="csr", graph=g))
+    yref, yS = orc.aggregate(oei, h, n, "sum", edge_weight=a32 if H > 1 else a32.reshape(E),
+                             heads=H)
+    assert_scaled(y, yref, yS, what="aggregation with graph-order alpha")
+
+
+def test_attention_in_graph_order_errors(tfg):
+    import torch
+    n = 50
+    ei = graphgen.random_graph(5, n, 400)
+    g = tfg.tfg_graph_create(dev(ei), n)
+    gt = tfg.tfg_graph_create_transposed(dev(ei), n)
+    h = torch.zeros((n, 8), device="cuda:0")
+    a = torch.zeros((2, 4), device="cuda:0")
+    with pytest.raises(ValueError):
+        tfg.tfg_gat_graph_scores(gt, h, a, a)  # a transposed graph
+    with pytest.raises(ValueError):
+        tfg.tfg_gat_graph_scores(g, h[:10], a, a)  # h of the wrong shape
+    s = torch.zeros((g.E, 2), device="cuda:0")
+    with pytest.raises(ValueError):
+        tfg.tfg_segment_softmax_graph(g, s[:-1])  # not one row per edge
+    with pytest.raises(ValueError):
+        tfg.tfg_segment_softmax_graph_backward(gt, s, s)  # a transposed graph
+    lib = tfg.load()
+    assert lib.tfg_segment_softmax_graph(g.handle, s.data_ptr(), 2, 7, s.data_ptr(), None, 0,
+                                         None) == 1  # bad order
+
+
 def test_segment_softmax_closed_forms(tfg):
     seg = np.array([0, 1, 1, 1, 3])
     s = np.array([5.0, 2.0, 2.0, 2.0, -7.0], np.float32)
