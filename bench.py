@@ -263,6 +263,25 @@ def cpu_baseline_threads(ei: np.ndarray, x: np.ndarray, n: int, n_edges: int):
             "cpu_model": cpu_model(), "nproc": os.cpu_count()}
 
 
+def _replayed(torch, fn, reps: int) -> float:
+    """Average ms per replay of fn() captured as one HIP graph (two warm-up
+    runs on a side stream, then the capture), replays timed back to back by
+    events on the current stream."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr):
+        fn()
+    ms = _timed(torch, gr.replay, reps)
+    del gr
+    return ms
+
+
 def _timed(torch, fn, reps: int, warm: int = 2) -> float:
     """Average ms of fn() over reps back-to-back calls, by events on the
     current stream (the stream the library launches on)."""
@@ -466,6 +485,7 @@ def run_suite(args):
         return tfg.tfg_aggregate(None, h, n3, "sum", edge_weight=a, heads=H, weight_order="csr",
                                  graph=g3)
     ms_cg = _timed(torch, chain_graph_order, reps)
+    ms_cg_replay = _replayed(torch, chain_graph_order, reps)
     ei3_np = c["edge_index"]
     if not args.no_cpu_baseline:
         cpu["gat"] = _oracle(lambda: oracle.gat_layer(ei3_np, c["h"], c["a_src"], c["a_dst"], H,
@@ -480,6 +500,7 @@ def run_suite(args):
          kernel="node_projections_vec + gat_short + gat_items + gat_merge",
          unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
          unfused_chain_graph_order_ms=round(ms_cg, 4),
+         unfused_chain_graph_order_hip_graph_ms=round(ms_cg_replay, 4),
          cpu_baseline=cpu.get("gat"), cpu_baseline_threads=cpu.get("gat_t"))
     # the Transformer-style variant: q, key, v of the same shape as h
     gen = torch.Generator(device=dev).manual_seed(3)
@@ -600,6 +621,26 @@ def run_suite(args):
     _row("mini-batch step: BatchGraph + CSR + gcn_norm + 3 GCN layers + 3 pools", wl5, ms,
          3 * (Eb + Nb), None, cpu_baseline=cpu.get("mb"), cpu_baseline_threads=cpu.get("mb_t"))
     gi = torch.from_numpy(c["graph_index"].astype(np.int32)).to(dev)
+    # the forward on a cached BatchGraph (normalisation, 3 layers, 3 pools):
+    # eager calls, then the same calls replayed as one HIP graph
+    bei_c, bgi_c, _, _ = tfg.tfg_batch_graphs(nc, ec, local, Nb, validate=False)
+    gb_c = tfg.tfg_graph_create(bei_c, Nb, add_self_loops=True)
+
+    def cached_forward():
+        nb = tfg.tfg_gcn_norm(bei_c, Nb, graph=gb_c, out_edge_index=False,
+                              out_edge_weight=False, out_deg=False)
+        hb = xb
+        for _ in range(c["layers"]):
+            hb = tfg.tfg_aggregate(None, hb, Nb, "sum", edge_weight=nb["edge_weight_csr"],
+                                   weight_order="csr", graph=gb_c)
+        return [tfg.tfg_segment_pool(hb, bgi_c, G, r, validate=False)
+                for r in ("sum", "mean", "max")]
+    ms_e = _timed(torch, cached_forward, reps)
+    ms_r = _replayed(torch, cached_forward, reps)
+    _row("mini-batch forward on a cached BatchGraph (gcn_norm + 3 GCN layers + 3 pools), "
+         "HIP graph replay", wl5, ms_r, 3 * (Eb + Nb), None, eager_ms=round(ms_e, 4),
+         speedup_vs_eager=round(ms_e / ms_r, 3))
+    del gb_c, bei_c, bgi_c
     pout = torch.empty((G, Fb), dtype=torch.float32, device=dev)
     pws = torch.empty(max(tfg.load().tfg_segment_pool_ws_bytes(Nb, G), 256), dtype=torch.uint8,
                       device=dev)
@@ -637,6 +678,20 @@ def run_suite(args):
                                   "the whole graph (normalisation on one thread)")
         _row("GCN step: CSR + gcn_norm + sum aggregation", f"uniform graph N={n}, "
              f"E'={Ec}, F={Fc}", ms, Ec, None, cpu_baseline=cb, cpu_baseline_threads=cbt)
+        # a GCN layer on the cached graph: eager, then replayed as one HIP graph
+        gcc = tfg.tfg_graph_create(eic, n, add_self_loops=True)
+
+        def gcn_layer():
+            nm = tfg.tfg_gcn_norm(eic, n, graph=gcc, out_edge_index=False, out_edge_weight=False,
+                                  out_deg=False)
+            return tfg.tfg_aggregate(None, xc, n, "sum", edge_weight=nm["edge_weight_csr"],
+                                     weight_order="csr", graph=gcc)
+        ms_e = _timed(torch, gcn_layer, reps)
+        ms_r = _replayed(torch, gcn_layer, reps)
+        _row("GCN layer on the cached graph (graph-order gcn_norm + sum aggregation), "
+             "HIP graph replay", f"uniform graph N={n}, E'={Ec}, F={Fc}", ms_r, Ec, None,
+             eager_ms=round(ms_e, 4), speedup_vs_eager=round(ms_e / ms_r, 3))
+        del gcc
 
 
 def run_ceiling(args):
