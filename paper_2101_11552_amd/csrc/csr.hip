@@ -476,7 +476,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
   __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
   __shared__ int loff[kMaxRadix];
   __shared__ int goff[kMaxRadix];
-  __shared__ unsigned stage[2][kSortTile];
+  __shared__ uint2 stage[kSortTile];  // (A, B) per staged position: one 8-byte access each
   __shared__ int tmp[kSortWaves];
 
   const int radix = 1 << dbits;
@@ -571,8 +571,7 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
   for (int i = 0; i < kSortItems; ++i) {
     const int pos = pk[i] & 0xFFFF;
     if (pos != 0xFFFF) {
-      stage[0][pos] = va[i];
-      stage[1][pos] = vb[i];
+      stage[pos] = make_uint2(va[i], vb[i]);
     }
   }
   __syncthreads();
@@ -580,7 +579,8 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
   for (int i = 0; i < kSortItems; ++i) {
     const int p = i * kSortThreads + threadIdx.x;
     if (p < tile_n) {
-      const unsigned a = stage[0][p], b = stage[1][p];
+      const uint2 ab = stage[p];
+      const unsigned a = ab.x, b = ab.y;
       // the first pass's digit is not a field of A: it is recomputed from
       // the unpacked ids, as the decode formed it
       const int d = MODE == 0 ? first_digit(a, b, m, q, radix)
