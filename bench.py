@@ -513,6 +513,13 @@ def run_suite(args):
         return tfg.tfg_aggregate(ei3, vd, n3, "sum", edge_weight=a_csr, heads=H,
                                  weight_order="csr", graph=g3)
     ms_c = _timed(torch, dot_chain, reps)
+
+    def dot_chain_graph_order():
+        s = tfg.tfg_edge_dot_scores(g3, qd, kd, H, order="csr", out=sg_out)
+        a = tfg.tfg_segment_softmax_graph(g3, s, order="csr", out=ag_out, ws=ag_ws)
+        return tfg.tfg_aggregate(None, vd, n3, "sum", edge_weight=a, heads=H, weight_order="csr",
+                                 graph=g3)
+    ms_cg = _timed(torch, dot_chain_graph_order, reps)
     if not args.no_cpu_baseline:
         qh, kh, vh = (t.cpu().numpy() for t in (qd, kd, vd))
         cpu["dot"] = _oracle(lambda: oracle.dot_layer(ei3_np, qh, kh, vh, H, 1.0 / np.sqrt(c["D"])),
@@ -522,6 +529,7 @@ def run_suite(args):
     _row("fused Transformer-style attention (scaled dot product)", wl3, ms_f, E3,
          E3 * (4 + 8 * Fh) + n3 * (8 * Fh + 4), kernel="gat_short + gat_items (dot) + gat_merge",
          unfused_chain_ms=round(ms_c, 4), speedup_vs_unfused=round(ms_c / ms_f, 3),
+         unfused_chain_graph_order_ms=round(ms_cg, 4),
          cpu_baseline=cpu.get("dot"))
     del qd, kd, vd
     s = tfg.tfg_gat_edge_scores(ei3, h, a_s, a_d, c["slope"])
