@@ -77,6 +77,17 @@ def test_gat_attention(tfg, orc):
     assert_scaled(host(y), ref, S, what="attention per-head aggregation")
     empty = np.bincount(ei[1], minlength=n) == 0
     assert empty.mean() > 0.2 and np.all(host(y)[empty] == 0)
+    # the same layer with scores and alpha kept in the graph order
+    perm = expected_graph(orc, ei, n)[2]
+    s_g = tfg.tfg_gat_graph_scores(g, dev(h), dev(c["a_src"]), dev(c["a_dst"]), c["slope"],
+                                   order="csr")
+    assert same_bits(host(s_g), s_h[perm])
+    a_g = tfg.tfg_segment_softmax_graph(g, s_g, order="csr")
+    assert same_bits(host(a_g), host(alpha_csr))
+    assert_rel(host(a_g), a64[perm], what="attention softmax in graph order")
+    y_g = tfg.tfg_aggregate(None, dev(h), n, "sum", edge_weight=a_g, heads=H, weight_order="csr",
+                            graph=g)
+    assert same_bits(host(y_g), host(y))
 
 
 def test_batched_pooling(tfg, orc):
