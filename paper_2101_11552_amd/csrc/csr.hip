@@ -276,6 +276,28 @@ __global__ __launch_bounds__(kUpThreads) void upsweep(const IdxT* __restrict__ s
   }
 }
 
+// Tables of at most this many tiles are not scanned by a launch of their own:
+// every scatter block adds up the counts it needs from the raw table.
+constexpr int kInBlockTiles = 64;
+
+// Output offset of digit d's run in this tile. scanned: hist holds the
+// exclusive scan of the digit-major table (the offset itself); otherwise the
+// raw counts, and the offset is the total of the digits below d plus the
+// counts of d in the tiles before this one. Every thread of the block calls
+// it (a block scan inside when !scanned); threads d >= radix get 0.
+__device__ __forceinline__ int tile_offset(const int* __restrict__ hist, int d, int radix,
+                                           int ntiles, int tile, int scanned, int* tmp) {
+  if (scanned) return d < radix ? hist[(int64_t)d * ntiles + tile] : 0;
+  int pre = 0, tot = 0;
+  if (d < radix)
+    for (int t = 0; t < ntiles; ++t) {
+      const int h = hist[d * ntiles + t];
+      tot += h;
+      pre += t < tile ? h : 0;
+    }
+  return block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr) + (d < radix ? pre : 0);
+}
+
 // Stable scatter of one tile by one digit. Wave w owns tile positions
 // [w*512, (w+1)*512), visited in rounds of 64 consecutive positions, so the
 // (wave, round, lane) order is the input order. Within a round, lanes with the
@@ -290,7 +312,7 @@ template <bool FIRST, typename IdxT>
 __global__ __launch_bounds__(kSortThreads, 8) void scatter(
     const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, KeyMap m,
     const int* __restrict__ kin, const int* __restrict__ ein, const int* __restrict__ sin,
-    int64_t E, int shift, int dbits, const int* __restrict__ hist, int ntiles,
+    int64_t E, int shift, int dbits, const int* __restrict__ hist, int ntiles, int scanned,
     int* __restrict__ kout, int* __restrict__ eout, int* __restrict__ sout) {
   __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
   __shared__ int loff[kMaxRadix];
@@ -366,9 +388,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
       }
     }
     const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
+    const int go = tile_offset(hist, d, radix, ntiles, tile, scanned, tmp);
     if (d < radix) {
       loff[d] = ex;
-      goff[d] = hist[(int64_t)d * ntiles + tile];
+      goff[d] = go;
     }
   }
   __syncthreads();
@@ -471,7 +494,7 @@ template <int MODE, typename IdxT>
 __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
     const IdxT* __restrict__ src, const IdxT* __restrict__ tgt, KeyMap m, PackMap q,
     const unsigned* __restrict__ ain, const unsigned* __restrict__ bin, int64_t E, int shift,
-    int dbits, const int* __restrict__ hist, int ntiles, int* __restrict__ o0,
+    int dbits, const int* __restrict__ hist, int ntiles, int scanned, int* __restrict__ o0,
     int* __restrict__ o1, int* __restrict__ o2) {
   __shared__ unsigned short wcnt[kSortWaves][kMaxRadix];
   __shared__ int loff[kMaxRadix];
@@ -553,9 +576,10 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
       }
     }
     const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
+    const int go = tile_offset(hist, d, radix, ntiles, tile, scanned, tmp);
     if (d < radix) {
       loff[d] = ex;
-      goff[d] = hist[(int64_t)d * ntiles + tile];
+      goff[d] = go;
     }
   }
   __syncthreads();
@@ -664,6 +688,17 @@ constexpr int kWlThreads = 1024;  // rows per block of the work-list kernels
 constexpr int kLists = 5;         // heavy chunks, light, split, short, long
 __constant__ const int kListCounter[kLists] = {0, 1, 2, 5, 6};  // their slots in counters
 
+// Entries of a row of `deg` edges in each list.
+__device__ __forceinline__ void row_counts(bool valid, int deg, int chunk, int (&c)[kLists]) {
+  const bool split = valid && deg > chunk;
+  const bool shrt = valid && deg <= kShortRow;
+  c[0] = split ? (deg + chunk - 1) / chunk : 0;
+  c[1] = valid && !split;
+  c[2] = split;
+  c[3] = shrt;
+  c[4] = valid && !split && !shrt;
+}
+
 __device__ __forceinline__ void row_entries(const int* __restrict__ rowptr, int64_t N, int chunk,
                                             int64_t r, int* beg, int* deg, int (&c)[kLists]) {
   *beg = 0;
@@ -672,29 +707,20 @@ __device__ __forceinline__ void row_entries(const int* __restrict__ rowptr, int6
     *beg = rowptr[r];
     *deg = rowptr[r + 1] - *beg;
   }
-  const bool valid = r < N;
-  const bool split = valid && *deg > chunk;
-  const bool shrt = valid && *deg <= kShortRow;
-  c[0] = split ? (*deg + chunk - 1) / chunk : 0;
-  c[1] = valid && !split;
-  c[2] = split;
-  c[3] = shrt;
-  c[4] = valid && !split && !shrt;
+  row_counts(r < N, *deg, chunk, c);
 }
 
 // Entries per list of each block of rows: block_sums[list * nb + block].
 __global__ __launch_bounds__(kWlThreads) void worklist_count(const int* __restrict__ rowptr,
                                                              int64_t N, int chunk,
                                                              int* __restrict__ block_sums, int nb) {
-  __shared__ int tmp[kWlThreads / kWave];
-  int beg, deg, c[kLists];
+  __shared__ int tmp[kLists * (kWlThreads / kWave)];
+  int beg, deg, c[kLists], ex[kLists], tot[kLists];
   row_entries(rowptr, N, chunk, (int64_t)blockIdx.x * kWlThreads + threadIdx.x, &beg, &deg, c);
+  block_excl_scan_lists<kWlThreads / kWave, kLists>(c, ex, tot, tmp);
+  if (threadIdx.x == 0)
 #pragma unroll
-  for (int i = 0; i < kLists; ++i) {
-    int tot;
-    block_excl_scan<kWlThreads / kWave>(c[i], tmp, &tot);
-    if (threadIdx.x == 0) block_sums[i * nb + blockIdx.x] = tot;
-  }
+    for (int i = 0; i < kLists; ++i) block_sums[i * nb + blockIdx.x] = tot[i];
 }
 
 // One block: exclusive scan of each list's block sums in place; the list
@@ -725,17 +751,29 @@ __global__ __launch_bounds__(kWlThreads) void worklist_single(
     const int* __restrict__ rowptr, int64_t N, int chunk, int* __restrict__ counters,
     WorkItem* __restrict__ heavy, WorkItem* __restrict__ light, SplitRow* __restrict__ split,
     WorkItem* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
-  __shared__ int tmp[kWlThreads / kWave];
+  __shared__ int tmp[kLists * (kWlThreads / kWave)];
   int carry[kLists] = {0, 0, 0, 0, 0};
-  for (int64_t r0 = 0; r0 < N; r0 += kWlThreads) {
-    const int64_t r = r0 + threadIdx.x;
-    int beg, deg, c[kLists], o[kLists];
-    row_entries(rowptr, N, chunk, r, &beg, &deg, c);
+  // every chunk's row pointers loaded before the first is used
+  constexpr int kChunks = kWlSingle / kWlThreads;
+  int rp[kChunks], rq[kChunks];
+#pragma unroll
+  for (int j = 0; j < kChunks; ++j) {
+    const int64_t r = (int64_t)j * kWlThreads + threadIdx.x;
+    rp[j] = r < N ? rowptr[r] : 0;
+    rq[j] = r < N ? rowptr[r + 1] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kChunks; ++j) {
+    if ((int64_t)j * kWlThreads >= N) break;  // uniform
+    const int64_t r = (int64_t)j * kWlThreads + threadIdx.x;
+    const int beg = rp[j], deg = rq[j] - rp[j];
+    int c[kLists], o[kLists], tot[kLists];
+    row_counts(r < N, deg, chunk, c);
+    block_excl_scan_lists<kWlThreads / kWave, kLists>(c, o, tot, tmp);
 #pragma unroll
     for (int i = 0; i < kLists; ++i) {
-      int tot;
-      o[i] = carry[i] + block_excl_scan<kWlThreads / kWave>(c[i], tmp, &tot);
-      carry[i] += tot;
+      o[i] += carry[i];
+      carry[i] += tot[i];
     }
     if (r < N) {
       if (c[3])
@@ -743,9 +781,9 @@ __global__ __launch_bounds__(kWlThreads) void worklist_single(
       else if (c[4])
         long_rows[o[4]] = WorkItem{(int)r, beg, beg + deg, -1};
       if (c[2]) {
-        for (int j = 0; j < c[0]; ++j) {
-          const int kb = beg + j * chunk;
-          heavy[o[0] + j] = WorkItem{(int)r, kb, min(kb + chunk, beg + deg), o[0] + j};
+        for (int q = 0; q < c[0]; ++q) {
+          const int kb = beg + q * chunk;
+          heavy[o[0] + q] = WorkItem{(int)r, kb, min(kb + chunk, beg + deg), o[0] + q};
         }
         split[o[2]] = SplitRow{(int)r, o[0], c[0], deg};
       } else {
@@ -762,13 +800,13 @@ __global__ __launch_bounds__(kWlThreads) void worklist_fill(
     const int* __restrict__ rowptr, int64_t N, int chunk, const int* __restrict__ block_sums,
     int nb, WorkItem* __restrict__ heavy, WorkItem* __restrict__ light,
     SplitRow* __restrict__ split, WorkItem* __restrict__ short_rows, WorkItem* __restrict__ long_rows) {
-  __shared__ int tmp[kWlThreads / kWave];
+  __shared__ int tmp[kLists * (kWlThreads / kWave)];
   const int64_t r = (int64_t)blockIdx.x * kWlThreads + threadIdx.x;
-  int beg, deg, c[kLists], o[kLists];
+  int beg, deg, c[kLists], o[kLists], tot[kLists];
   row_entries(rowptr, N, chunk, r, &beg, &deg, c);
+  block_excl_scan_lists<kWlThreads / kWave, kLists>(c, o, tot, tmp);
 #pragma unroll
-  for (int i = 0; i < kLists; ++i)
-    o[i] = block_sums[i * nb + blockIdx.x] + block_excl_scan<kWlThreads / kWave>(c[i], tmp, nullptr);
+  for (int i = 0; i < kLists; ++i) o[i] += block_sums[i * nb + blockIdx.x];
   if (r >= N) return;
   if (c[3])
     short_rows[o[3]] = WorkItem{(int)r, beg, beg + deg, -1};
@@ -914,9 +952,12 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
       else
         upsweep<false, IdxT><<<nt, kUpThreads, 0, s>>>(src, tgt, m, bufs[cur][0], E, dshift,
                                                          p.dbits, hist, err);
-      const int rc = exclusive_scan(hist, hist, radix * p.ntiles, sums, s);
-      if (rc) return rc;
-      TFG_LAUNCHED("radix offsets");
+      const int scanned = p.ntiles > kInBlockTiles;
+      if (scanned) {
+        const int rc = exclusive_scan(hist, hist, radix * p.ntiles, sums, s);
+        if (rc) return rc;
+        TFG_LAUNCHED("radix offsets");
+      }
       const int nxt = first ? 0 : 1 - cur;
       int* ko = last ? keys : bufs[nxt][0];
       int* eo = last ? g.perm : bufs[nxt][1];
@@ -926,23 +967,21 @@ int sort_edges(Graph& g, const IdxT* src, const IdxT* tgt, char* scratch, const 
         const unsigned* ai = reinterpret_cast<const unsigned*>(ki);
         const unsigned* bi = reinterpret_cast<const unsigned*>(ei);
         if (first)
-          scatter_packed<0, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
-                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
-                                                              so);
+          scatter_packed<0, IdxT><<<nt, kSortThreads, 0, s>>>(
+              src, tgt, m, q, ai, bi, E, dshift, p.dbits, hist, (int)p.ntiles, scanned, ko, eo, so);
         else if (last)
-          scatter_packed<2, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
-                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
-                                                              so);
+          scatter_packed<2, IdxT><<<nt, kSortThreads, 0, s>>>(
+              src, tgt, m, q, ai, bi, E, dshift, p.dbits, hist, (int)p.ntiles, scanned, ko, eo, so);
         else
-          scatter_packed<1, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, q, ai, bi, E, dshift,
-                                                              p.dbits, hist, (int)p.ntiles, ko, eo,
-                                                              so);
+          scatter_packed<1, IdxT><<<nt, kSortThreads, 0, s>>>(
+              src, tgt, m, q, ai, bi, E, dshift, p.dbits, hist, (int)p.ntiles, scanned, ko, eo, so);
       } else if (first) {
         scatter<true, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift, p.dbits,
-                                                        hist, (int)p.ntiles, ko, eo, so);
+                                                        hist, (int)p.ntiles, scanned, ko, eo, so);
       } else {
         scatter<false, IdxT><<<nt, kSortThreads, 0, s>>>(src, tgt, m, ki, ei, si, E, shift,
-                                                         p.dbits, hist, (int)p.ntiles, ko, eo, so);
+                                                         p.dbits, hist, (int)p.ntiles, scanned, ko,
+                                                         eo, so);
       }
       TFG_LAUNCHED("radix scatter");
       cur = nxt;

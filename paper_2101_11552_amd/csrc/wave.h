@@ -39,4 +39,32 @@ __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int* total) {
   return off + incl - v;
 }
 
+// K exclusive scans at once (one value per list per thread) over a block of
+// NW waves: the lists share the barriers (two in all). tmp: NW * K ints.
+template <int NW, int K>
+__device__ __forceinline__ void block_excl_scan_lists(const int (&v)[K], int (&ex)[K],
+                                                      int (&total)[K], int* tmp) {
+  const int wave = threadIdx.x / kWave;
+  int incl[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    incl[i] = wave_incl_scan(v[i]);
+    if (lane_id() == kWave - 1) tmp[i * NW + wave] = incl[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int t = tmp[i * NW + w];
+      if (w < wave) off += t;
+      tot += t;
+    }
+    ex[i] = off + incl[i] - v[i];
+    total[i] = tot;
+  }
+  __syncthreads();
+}
+
 }  // namespace tfg
