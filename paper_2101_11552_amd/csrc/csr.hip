@@ -328,6 +328,9 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
   const int tile_n = (int)min<int64_t>(kSortTile, E - base);
 
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
+  // the tile's output offset of digit threadIdx.x, first, while few registers
+  // are live (placed in LDS with the local offsets, after the ranking)
+  const int go = tile_offset(hist, (int)threadIdx.x, radix, ntiles, tile, scanned, tmp);
   __syncthreads();
 
   // Keys and payloads are loaded together up front (one round of memory
@@ -388,7 +391,6 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter(
       }
     }
     const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
-    const int go = tile_offset(hist, d, radix, ntiles, tile, scanned, tmp);
     if (d < radix) {
       loff[d] = ex;
       goff[d] = go;
@@ -510,6 +512,9 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
   const int tile_n = (int)min<int64_t>(kSortTile, E - base);
 
   for (int d = lane; d < kMaxRadix; d += kWave) wcnt[wave][d] = 0;
+  // the tile's output offset of digit threadIdx.x, first, while few registers
+  // are live (placed in LDS with the local offsets, after the ranking)
+  const int go = tile_offset(hist, (int)threadIdx.x, radix, ntiles, tile, scanned, tmp);
   __syncthreads();
 
   // pk: the digit in the upper half, below it first the rank within the
@@ -576,7 +581,6 @@ __global__ __launch_bounds__(kSortThreads, 8) void scatter_packed(
       }
     }
     const int ex = block_excl_scan<kSortWaves>(d < radix ? tot : 0, tmp, nullptr);
-    const int go = tile_offset(hist, d, radix, ntiles, tile, scanned, tmp);
     if (d < radix) {
       loff[d] = ex;
       goff[d] = go;
