@@ -86,6 +86,11 @@ int main() {
                       nullptr) == 1);
   CHECK(tfg_batch_graphs(-1, fake, fake, fake, 0, 0, 0, fake, fake, nullptr, nullptr, 1, fake,
                          1 << 20, nullptr) == 1);
+  CHECK(tfg_gat_graph_scores(nullptr, ff, 8, 16, ff, ff, 0.2f, ff, 1, fake, 1 << 20, nullptr) == 1);
+  CHECK(tfg_segment_softmax_graph(nullptr, ff, 8, 1, ff, fake, 1 << 20, nullptr) == 1);
+  CHECK(tfg_segment_softmax_graph_backward(nullptr, ff, ff, 8, 1, ff, fake, 1 << 20, nullptr) == 1);
+  CHECK(tfg_gat_graph_scores_ws_bytes(nullptr, 8) == 0);
+  CHECK(tfg_segment_softmax_graph_ws_bytes(nullptr, 8) == 0);
   int64_t nb = 0, ne = 0;
   CHECK(tfg_batch_graphs_totals(-1, fake, fake, 0, fake, 1 << 20, nullptr, &nb, &ne) == 1);
   CHECK(tfg_batch_graphs_totals(4, fake, fake, 0, fake, 1 << 20, nullptr, nullptr, &ne) == 1);

@@ -144,6 +144,14 @@ def test_host_side_argument_errors(lib):
                              None) == 1
     assert lib.tfg_batch_graphs(-1, fake, fake, fake, 0, 0, 0, fake, fake, None, None, 1, fake,
                                 1 << 20, None) == 1
+    # attention over a graph handle: no graph, and the size queries without one
+    assert lib.tfg_gat_graph_scores(None, fake, 8, 16, fake, fake, 0.2, fake, 1, fake, 1 << 20,
+                                    None) == 1
+    assert lib.tfg_segment_softmax_graph(None, fake, 8, 1, fake, fake, 1 << 20, None) == 1
+    assert lib.tfg_segment_softmax_graph_backward(None, fake, fake, 8, 1, fake, fake, 1 << 20,
+                                                  None) == 1
+    assert lib.tfg_gat_graph_scores_ws_bytes(None, 8) == 0
+    assert lib.tfg_segment_softmax_graph_ws_bytes(None, 8) == 0
 
 
 def test_python_binding_rejects_host_tensors():
