@@ -491,7 +491,8 @@ def test_segment_softmax(tfg, orc, H, parts):
 
 
 @pytest.mark.parametrize("H,D,parts,loops", [(8, 16, 1, False), (3, 4, 1, True),
-                                             (8, 16, 4, False), (1, 5, 3, True)])
+                                             (8, 16, 4, False), (1, 5, 3, True),
+                                             (80, 2, 1, False)])  # heads in two passes
 def test_attention_in_graph_order(tfg, orc, H, D, parts, loops):
     """Scores, softmax and its gradient over a graph handle with the per-edge
     arrays in the graph order: the same bits as the calls in the caller's
