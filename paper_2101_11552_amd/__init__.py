@@ -213,6 +213,11 @@ def _f32(t: torch.Tensor | None, what: str, device=None) -> torch.Tensor | None:
     return t.contiguous()
 
 
+def _per_edge(t: torch.Tensor) -> torch.Tensor:
+    """[E] or [E, H] per-edge values as [E, H] (also for E = 0)."""
+    return t.reshape(t.shape[0], t.shape[1] if t.dim() > 1 else 1)
+
+
 def _rows(x: torch.Tensor, what: str, device=None):
     """float32 2-D device tensor with unit column stride; returns (x, ldx)."""
     _dev(x, what, device)
@@ -525,7 +530,7 @@ def tfg_segment_softmax_backward(alpha: torch.Tensor, dalpha: torch.Tensor, seg:
     lib = load()
     a = _f32(alpha, "alpha")
     shape = a.shape
-    a2 = a.reshape(a.shape[0], -1)
+    a2 = _per_edge(a)
     da = _f32(dalpha, "dalpha", a.device)
     if da.numel() != a2.numel():
         raise ValueError("dalpha must have the shape of alpha")
@@ -573,7 +578,7 @@ def tfg_segment_softmax(scores: torch.Tensor, seg: torch.Tensor, N: int,
     lib = load()
     s = _f32(scores, "scores")
     squeeze = s.dim() == 1
-    s2 = s.reshape(s.shape[0], -1)
+    s2 = _per_edge(s)
     E, H = s2.shape
     seg = _dev(seg, "seg", s.device).contiguous()
     if seg.numel() != E:
@@ -624,7 +629,7 @@ def tfg_segment_softmax_graph(graph: Graph, scores: torch.Tensor, order: str = "
     lib = load()
     dev = graph.device
     s = _f32(scores, "scores", dev)
-    s2 = s.reshape(s.shape[0], -1)
+    s2 = _per_edge(s)
     E, H = s2.shape
     if E != graph.E:
         raise ValueError(f"scores must hold one row per edge of the graph ({graph.E})")
@@ -643,7 +648,7 @@ def tfg_segment_softmax_graph_backward(graph: Graph, alpha: torch.Tensor, dalpha
     lib = load()
     dev = graph.device
     a = _f32(alpha, "alpha", dev)
-    a2 = a.reshape(a.shape[0], -1)
+    a2 = _per_edge(a)
     da = _f32(dalpha, "dalpha", dev)
     if da.numel() != a2.numel():
         raise ValueError("dalpha must have the shape of alpha")

@@ -542,6 +542,34 @@ def test_attention_in_graph_order(tfg, orc, H, D, parts, loops):
     assert_scaled(y, yref, yS, what="aggregation with graph-order alpha")
 
 
+def test_attention_in_graph_order_degenerate(tfg):
+    """A graph without edges gives empty outputs; one node with only its loop
+    gives the loop's score and alpha = 1 exactly."""
+    import torch
+    empty = np.zeros((2, 0), np.int64)
+    g0 = tfg.tfg_graph_create(dev(empty), 5)
+    h = torch.ones((5, 6), device="cuda:0")
+    a = torch.ones((2, 3), device="cuda:0")
+    s0 = tfg.tfg_gat_graph_scores(g0, h, a, a)
+    assert tuple(s0.shape) == (0, 2)
+    assert tuple(tfg.tfg_segment_softmax_graph(g0, s0).shape) == (0, 2)
+    assert tuple(tfg.tfg_segment_softmax_graph_backward(g0, s0, s0).shape) == (0, 2)
+    seg0 = torch.zeros(0, dtype=torch.int64, device="cuda:0")  # the caller's-order calls too
+    assert tuple(tfg.tfg_segment_softmax(s0, seg0, 5).shape) == (0, 2)
+    assert tuple(tfg.tfg_segment_softmax_backward(s0, s0, seg0, 5).shape) == (0, 2)
+    g1 = tfg.tfg_graph_create(dev(empty), 1, add_self_loops=True)
+    h1 = torch.tensor([[1.0, -2.0, 0.5, 3.0]], device="cuda:0")
+    a_s = torch.tensor([[1.0, 1.0], [0.0, 2.0]], device="cuda:0")
+    a_d = torch.tensor([[0.5, 0.0], [1.0, 1.0]], device="cuda:0")
+    s1 = host(tfg.tfg_gat_graph_scores(g1, h1, a_s, a_d))
+    # head 0: (1 - 2) + 0.5 = -0.5 -> 0.2 * -0.5; head 1: 2 * 3 + (0.5 + 3) = 9.5
+    assert np.array_equal(s1, np.array([[np.float32(0.2) * np.float32(-0.5), 9.5]], np.float32))
+    a1 = host(tfg.tfg_segment_softmax_graph(g1, dev(s1)))
+    assert np.array_equal(a1, np.ones((1, 2), np.float32))
+    d1 = host(tfg.tfg_segment_softmax_graph_backward(g1, dev(a1), dev(np.array([[3.0, -1.0]], np.float32))))
+    assert np.array_equal(d1, np.zeros((1, 2), np.float32))
+
+
 def test_attention_in_graph_order_errors(tfg):
     import torch
     n = 50
