@@ -1102,3 +1102,53 @@ def test_random_propagation_and_batching(tfg, orc, monkeypatch, seed):
     assert np.array_equal(host(bei), ref_ei) and np.array_equal(host(bgi), ref_gi), seed
     assert np.array_equal(host(noff), orc.batch_offsets(sizes)), seed
     assert np.array_equal(host(eoff), orc.batch_offsets(counts)), seed
+
+
+def test_every_call_on_a_graph_without_edges(tfg, orc):
+    """Each entry point on a graph of 5 nodes and no edges (and, where the call
+    takes them, no loops): empty per-edge outputs, zero node outputs, no error."""
+    import torch
+    cuda = "cuda:0"
+    n, F, H, D = 5, 8, 2, 4
+    empty = dev(np.zeros((2, 0), np.int64))
+    x = dev(graphgen.features(301, n, F))
+    g = tfg.tfg_graph_create(empty, n)
+    gt = tfg.tfg_graph_create_transposed(empty, n)
+    rowptr, col, perm = (host(t) for t in tfg.tfg_graph_csr(g))
+    assert np.all(rowptr == 0) and col.size == 0 and perm.size == 0
+    tfg.tfg_check(g)
+    nz = tfg.tfg_gcn_norm(empty, n, add_self_loops=False, graph=g)
+    assert nz["edge_weight"].numel() == 0 and np.all(host(nz["deg"]) == 0)
+    nl = tfg.tfg_gcn_norm(empty, n)  # loops only: every weight 1, degree 1
+    assert np.all(host(nl["edge_weight"]) == 1) and np.all(host(nl["deg"]) == 1)
+    for red in ("sum", "mean"):
+        assert np.all(host(tfg.tfg_aggregate(None, x, n, red, graph=g)) == 0)
+        assert np.all(host(tfg.tfg_aggregate_noalloc(None, x, n, g, red)) == 0)
+    m, a = tfg.tfg_aggregate(None, x, n, "max", graph=g)
+    assert np.all(host(m) == 0) and np.all(host(a) == -1)
+    dx, dw = tfg.tfg_aggregate_backward(g, x, "sum", graph_t=gt, x=x, want_dw=True)
+    assert np.all(host(dx) == 0) and dw.numel() == 0
+    assert tfg.tfg_edge_reorder(torch.zeros(0, device=cuda), src=g).numel() == 0
+    h = dev(graphgen.features(302, n, H * D))
+    a_s = dev(graphgen.features(303, H, D))
+    assert tfg.tfg_gat_edge_scores(empty, h, a_s, a_s).shape == (0, H)
+    y = tfg.tfg_gat_aggregate(g, h, a_s, a_s)
+    assert np.all(host(y) == 0)
+    assert tfg.tfg_edge_dot_scores(g, h, h, H).shape == (0, H)
+    assert np.all(host(tfg.tfg_gat_dot_aggregate(g, h, h, h, H)) == 0)
+    # propagation: no edges leave alpha * h after each step; K = 0 copies x
+    assert np.array_equal(host(tfg.tfg_propagate(g, x, 0)), host(x))
+    assert np.all(host(tfg.tfg_propagate(g, x, 2)) == 0)
+    p = host(tfg.tfg_propagate(g, x, 2, alpha=0.5, h=x))
+    assert np.array_equal(p, (np.float32(0.5) * host(x)).astype(np.float32))
+    # pooling of no nodes into 3 graphs, and its gradient
+    gi = torch.zeros(0, dtype=torch.int64, device=cuda)
+    xp = torch.zeros((0, F), device=cuda)
+    assert np.all(host(tfg.tfg_segment_pool(xp, gi, 3, "sum")) == 0)
+    assert tfg.tfg_segment_pool_backward(torch.ones((3, F), device=cuda), gi).shape == (0, F)
+    # a batch of graphs without edges
+    nc = torch.tensor([2, 0, 3], dtype=torch.int64, device=cuda)
+    ec = torch.zeros(3, dtype=torch.int64, device=cuda)
+    bei, bgi, noff, eoff = tfg.tfg_batch_graphs(nc, ec, empty)
+    assert bei.shape == (2, 0) and np.array_equal(host(bgi), [0, 0, 2, 2, 2])
+    assert np.array_equal(host(noff), [0, 2, 2, 5]) and np.all(host(eoff) == 0)
