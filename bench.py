@@ -932,6 +932,8 @@ def main():
         "cpu_baseline": cpu,
         "cpu_baseline_threads": cpu_mt,
     }
+    if cpu_mt and cpu_mt.get("value"):  # the step's rate over the threaded oracle's
+        line["speedup_vs_cpu_baseline_threads"] = round(value / cpu_mt["value"], 1)
     print(json.dumps(line), flush=True)
 
 
