@@ -259,6 +259,34 @@ def test_gcn_norm_sliced_hub_row(tfg, orc, monkeypatch, idx):
     assert same_bits(host(r["edge_weight_csr"]), ow[perm])
 
 
+def test_row_longer_than_float32_integers(tfg, orc, monkeypatch):
+    # a target with more than 2^24 in-edges: its unit-weight degree is no
+    # longer an exact float32, so the row length is rounded once (to nearest
+    # even); weights in both orders, and the hub row of the sum and mean
+    # aggregations over the normalised weights, against the oracle
+    n, hub, F = 1000, 7, 4
+    ei = graphgen.random_graph(31, n, 20_000, hub=hub, hub_edges=2**24 + 3_000_002)
+    oei, ow, odeg = orc.gcn_norm(ei, n)
+    count = int(np.count_nonzero(oei[1] == hub))
+    assert count > 2**24 and float(np.float32(count)) != count
+    assert odeg[hub] == np.float32(count)
+    perm = orc.csr_by_target(oei, n)[2]
+    eid = dev(ei.astype(np.int32))
+    g = tfg.tfg_graph_create(eid, n, add_self_loops=True)
+    for mode in ("1", "0"):
+        monkeypatch.setenv("TFG_NORM_SLICED", mode)
+        r = tfg.tfg_gcn_norm(eid, n, graph=g)
+        assert same_bits(host(r["deg"]), odeg), mode
+        assert same_bits(host(r["edge_weight"]), ow), mode
+        assert same_bits(host(r["edge_weight_csr"]), ow[perm]), mode
+    x = graphgen.features(32, n, F)
+    for red in ("sum", "mean"):
+        y = host(tfg.tfg_aggregate(None, dev(x), n, red, edge_weight=r["edge_weight_csr"],
+                                   weight_order="csr", graph=g))
+        ref, S = orc.aggregate(oei, x, n, red, edge_weight=ow, rows=[hub])
+        assert_scaled(y[hub:hub + 1], ref, S, what=f"hub row, {red}")
+
+
 # ---------------------------------------------------------------------------
 # Aggregation
 # ---------------------------------------------------------------------------
