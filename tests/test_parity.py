@@ -518,15 +518,20 @@ def test_segment_softmax(tfg, orc, H, parts):
     assert np.all(np.abs(tot[has] - 1) <= 1e-5)
 
 
-@pytest.mark.parametrize("H,D,parts,loops", [(8, 16, 1, False), (3, 4, 1, True),
-                                             (8, 16, 4, False), (1, 5, 3, True),
-                                             (80, 2, 1, False)])  # heads in two passes
-def test_attention_in_graph_order(tfg, orc, H, D, parts, loops):
+@pytest.mark.parametrize("H,D,parts,loops,hub_edges", [
+    (8, 16, 1, False, 5000), (3, 4, 1, True, 5000), (8, 16, 4, False, 5000),
+    (1, 5, 3, True, 5000),
+    (80, 2, 1, False, 5000),  # heads in two passes
+    (8, 16, 1, True, 1500),   # a hub of 12 chunks: the split row done inside one block
+    (6, 8, 2, False, 1900)])  # the same with source parts and six heads
+def test_attention_in_graph_order(tfg, orc, H, D, parts, loops, hub_edges):
     """Scores, softmax and its gradient over a graph handle with the per-edge
     arrays in the graph order: the same bits as the calls in the caller's
-    order (permuted), and the oracle's values."""
+    order (permuted), and the oracle's values. A hub of more than 16 chunks
+    of 128 edges takes the two-launch path of the split rows, a smaller one
+    the path inside one block."""
     n, e = 4000, 60_000
-    ei = graphgen.random_graph(H * D + parts, n, e, hub=3, hub_edges=5000)
+    ei = graphgen.random_graph(H * D + parts + hub_edges, n, e, hub=3, hub_edges=hub_edges)
     g = tfg.tfg_graph_create(dev(ei), n, add_self_loops=loops, src_parts=parts)
     oei = orc.gcn_norm(ei, n)[0] if loops else ei  # the handle's edge list (loops appended)
     E = oei.shape[1]
