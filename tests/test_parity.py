@@ -1079,6 +1079,22 @@ def test_random_attention_and_pooling(tfg, orc, seed):
     alpha = tfg.tfg_segment_softmax(s, dev(ei[1]), n, graph=g)
     has = np.bincount(ei[1], minlength=n)[ei[1]] > 0
     assert_rel(host(alpha)[has], ref_alpha[has], what=what + " softmax")
+    # the same scores and softmax with the per-edge arrays in the graph order
+    perm = expected_graph(orc, ei, n, parts=g.info()["src_parts"])[2]
+    s_csr = tfg.tfg_gat_graph_scores(g, dev(h), dev(a_s), dev(a_d), 0.2, order="csr")
+    assert same_bits(host(s_csr), host(s)[perm]), what + " scores in graph order"
+    a_csr = tfg.tfg_segment_softmax_graph(g, s_csr, order="csr")
+    assert same_bits(host(a_csr), host(alpha)[perm]), what + " softmax in graph order"
+    # the softmax gradient in both orders, and against the oracle
+    da = graphgen.features(600 + seed, ei.shape[1], H)
+    ds = host(tfg.tfg_segment_softmax_backward(alpha, dev(da), dev(ei[1]), n, graph=g))
+    ds_csr = host(tfg.tfg_segment_softmax_graph_backward(g, a_csr, dev(da[perm]), order="csr"))
+    assert same_bits(ds_csr, ds[perm]), what + " softmax gradient in graph order"
+    a_h = host(alpha)
+    dref = orc.segment_softmax_backward(a_h, da, ei[1], n)
+    dot = np.zeros((n, H))
+    np.add.at(dot, ei[1], a_h.astype(np.float64) * np.abs(da))
+    assert_scaled(ds, dref, a_h * (np.abs(da) + dot[ei[1]]), what=what + " softmax gradient")
     # pooling
     G = int(r.integers(1, 800))
     sizes = r.integers(0, 30, G)
